@@ -1,0 +1,193 @@
+/*
+ * sharq.h -- C ABI of the SharQ sparse-dense FP4 linear layer for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * SharQ (arXiv 2606.26587) approximates a linear layer Y = X W^T by splitting
+ * the activation online into an N:M sparse FP4 backbone and a dense FP4
+ * residual taken against the *dequantized* backbone, then summing two FP4
+ * GEMMs that read one shared FP4 weight payload (Sec. 3.3 eqs.
+ * "sharq-sparse-backbone", "sharq-quantized-backbone", "sharq-residual",
+ * "sharq-output"; Sec. 3.4).
+ *
+ * Conventions for every entry point
+ *   - Tensor pointers are DEVICE pointers owned by the caller; the library
+ *     allocates nothing, keeps no global state and never synchronizes.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream);
+ *     all work is enqueued asynchronously on it.
+ *   - Errors are returned, never thrown.  Arguments are validated before any
+ *     launch: SHARQ_EINVAL (NULL pointer, negative size, K not a positive
+ *     multiple of 32, K % m != 0, leading dimension < K or < N),
+ *     SHARQ_EUNSUPPORTED (a format / pattern / dtype combination that is not
+ *     built), SHARQ_EALIGN (a pointer not aligned as stated below),
+ *     SHARQ_EHIP (the HIP runtime reported an error at launch).
+ *   - Inputs must be finite; NaN or Inf inputs give unspecified results.
+ *   - Row counts of 0 are valid and launch nothing.
+ *
+ * Numeric formats (App. A.1 of the paper)
+ *   E2M1 element code: bit 3 = sign, bits 0-2 index {0, .5, 1, 1.5, 2, 3, 4, 6}.
+ *   MXFP4: E2M1 + one E8M0 scale per 32 consecutive K values; E8M0 code c
+ *          means 2^(c-127).  NVFP4: E2M1 + one E4M3 scale (bias 7, max 448)
+ *          per block + one fp32 per-tensor scale.
+ *   Two 4-bit codes per byte, the element with the lower K index in the low
+ *   nibble.
+ */
+#ifndef SHARQ_H
+#define SHARQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SHARQ_OK = 0,
+  SHARQ_EINVAL = 1,
+  SHARQ_EUNSUPPORTED = 2,
+  SHARQ_EALIGN = 3,
+  SHARQ_EHIP = 4
+} sharq_status;
+
+typedef enum { SHARQ_MXFP4 = 0, SHARQ_NVFP4 = 1 } sharq_format;
+
+typedef enum { SHARQ_BF16 = 0, SHARQ_F16 = 1, SHARQ_F32 = 2 } sharq_dtype;
+
+/* N:M activation pattern: keep the n largest magnitudes of every m consecutive
+ * K positions (eq. "dynamic-mask").  Built: 2:4 and 4:8. */
+typedef struct {
+  int32_t n, m;
+} sharq_pattern;
+
+/*
+ * A prepared activation: the output of sharq_prepare, the input of
+ * sharq_linear / sharq_linear_grouped.  Row-major, one row per token.
+ *
+ *   sp_codes [rows][K*n/m/2]  backbone E2M1 codes of the kept positions only,
+ *                             in ascending K order (Sec. 3.4: "quantizes and
+ *                             compresses it"); 16-byte aligned.
+ *   sp_meta  [rows][K/8]      which positions were kept.  2:4: per group of 4
+ *                             the two kept indices i0 < i1 as i0 | i1 << 2 (a
+ *                             nibble), two groups per byte, even group low.
+ *                             4:8: per group of 8 an 8-bit keep mask (bit p =
+ *                             position p kept).  4-byte aligned.
+ *   sp_scale [rows][K/32]     backbone block scale per 32 logical K positions
+ *                             (Fig. 2 "sparse group-32 scales"): E8M0 (MXFP4)
+ *                             or E4M3 (NVFP4).
+ *   dn_codes [rows][K/2]      residual E2M1 codes, all positions; 16-byte aligned.
+ *   dn_scale [rows][K/32] (MXFP4, E8M0) | [rows][K/16] (NVFP4, E4M3).
+ *   tensor_scale              NVFP4: one fp32 per-tensor scale S (device); the
+ *                             element value is code * block_scale * S.
+ *                             MXFP4: unused (may be NULL).
+ */
+typedef struct {
+  int64_t rows, K;
+  sharq_format fmt;
+  sharq_pattern nm;
+  uint8_t *sp_codes;
+  uint8_t *sp_meta;
+  uint8_t *sp_scale;
+  uint8_t *dn_codes;
+  uint8_t *dn_scale;
+  float *tensor_scale;
+} sharq_act;
+
+/*
+ * A quantized weight: ONE shared FP4 payload for both paths with
+ * path-specific scale views (Sec. 3.4 "Shared FP4 weights with path-specific
+ * scales"; Fig. 2).  W is [N][K] (out-features x in-features), Y = X W^T.
+ * `experts` weights of identical shape may be stacked back to back (MoE);
+ * expert e starts at codes + e*N*K/2 and scale + e*N*(K/32).
+ *
+ *   codes    [experts][N][K/2]   E2M1, 16-byte aligned.
+ *   scale    [experts][N][K/32]  E8M0 (MXFP4, both paths) or E4M3 (NVFP4,
+ *                                sparse view: one scale per 32).
+ *   scale_dn [experts][N][K/16]  NVFP4 dense view: each per-32 scale repeated
+ *                                for its two 16-element halves.  MXFP4: equal
+ *                                to `scale`.
+ *   tensor_scale [experts]       NVFP4 per-tensor scale(s) S_w (device);
+ *                                MXFP4: unused.
+ */
+typedef struct {
+  int64_t N, K, experts;
+  sharq_format fmt;
+  uint8_t *codes;
+  uint8_t *scale;
+  uint8_t *scale_dn;
+  float *tensor_scale;
+} sharq_weight;
+
+/* Bytes of each buffer of a prepared activation / quantized weight (host-side
+ * sizing helpers, no device work).  Return 0 for an invalid combination. */
+size_t sharq_act_buffer_bytes(int64_t rows, int64_t K, sharq_format fmt, sharq_pattern nm,
+                              int32_t which /* 0 sp_codes, 1 sp_meta, 2 sp_scale, 3 dn_codes, 4 dn_scale */);
+size_t sharq_weight_buffer_bytes(int64_t N, int64_t K, sharq_format fmt,
+                                 int32_t which /* 0 codes, 1 scale, 2 scale_dn */);
+
+/*
+ * Quantize a weight W [N][K] (row stride ldw elements, dtype wdt = BF16 or
+ * F32) once into the shared FP4 payload and its scale views (Fig. 2 "weight
+ * preparation").  MXFP4: per row, per 32 K values, E8M0 = floor(log2 amax) - 2
+ * (OCP rule, clamped at -127), codes = E2M1(w / 2^e), ties to even, saturating.
+ * NVFP4: S_w = amax(W)/2688 computed on the device, E4M3 per 32, dense view
+ * duplicated per 16.  `out` fields N, K, fmt and the buffers must be set by
+ * the caller; experts must be 1.
+ */
+sharq_status sharq_quantize_weight(const void *W, sharq_dtype wdt, int64_t N, int64_t K, int64_t ldw,
+                                   sharq_weight *out, void *stream);
+
+/*
+ * Fused activation preparation (Sec. 3.4 "Fused sparse-residual preparation";
+ * Fig. 2): one kernel that, per row of X [M][K] (row stride ldx elements,
+ * dtype xdt = BF16):
+ *   1. if gamma != NULL (bf16 [K]): y = (x * r) * gamma with
+ *      r = 1/sqrt(mean(x^2) + eps) (sum of squares as a balanced binary tree
+ *      in fp32, r rounded from fp64); else y = x;
+ *   2. keeps the n largest |y| of every group of m (ties -> lower index);
+ *   3. quantizes the kept values per 32 logical positions (backbone);
+ *   4. forms the residual R = y - dequant(backbone) (eq. "sharq-residual");
+ *   5. quantizes R densely.
+ * NVFP4 additionally needs the per-tensor scale S: if tensor_scale_in is NULL
+ * the library computes S = amax(y)/2688 over the whole call in a pre-pass
+ * (one more read of X) and writes it to out->tensor_scale; otherwise
+ * *tensor_scale_in (device) is used and copied there.
+ * out->rows, K, fmt, nm and the buffers must match the arguments.
+ */
+sharq_status sharq_prepare(const void *X, sharq_dtype xdt, int64_t M, int64_t K, int64_t ldx,
+                           const void *gamma, float eps, sharq_pattern nm, sharq_format fmt,
+                           const float *tensor_scale_in, sharq_act *out, void *stream);
+
+/*
+ * Two-path output (eq. "sharq-output"; Sec. 3.4 "Residual path compensation
+ * by accumulation"): Y [rows][N] (row stride ldy, dtype ydt) =
+ *   dequant(backbone) * dequant_sp(W)^T + dequant(residual) * dequant_dn(W)^T,
+ * both products accumulated in one fp32 accumulator and written once.
+ * The activation and weight formats must match.
+ */
+sharq_status sharq_linear(const sharq_act *a, const sharq_weight *w, void *Y, sharq_dtype ydt,
+                          int64_t ldy, void *stream);
+
+/*
+ * Grouped form for mixture-of-experts layers: for every expert e and every
+ * i in [expert_offsets[e], expert_offsets[e+1]),
+ *   Y[i] = SharQ(A[row_index ? row_index[i] : i], W_e).
+ * expert_offsets: device int32 [w->experts + 1], non-decreasing, first 0,
+ * last == total.  row_index: device int32 [total], each in [0, a->rows), or
+ * NULL.  Y [total][N] (row stride ldy).  Offsets are read on the device; the
+ * host never waits for them.
+ */
+sharq_status sharq_linear_grouped(const sharq_act *a, const int32_t *row_index,
+                                  const int32_t *expert_offsets, int64_t total,
+                                  const sharq_weight *w, void *Y, sharq_dtype ydt, int64_t ldy,
+                                  void *stream);
+
+const char *sharq_status_str(sharq_status s);
+
+/* Library version string. */
+const char *sharq_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SHARQ_H */

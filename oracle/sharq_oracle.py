@@ -1,0 +1,545 @@
+"""SharQ CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+A plain, slow, NumPy implementation of what the SharQ sparse-dense FP4 linear
+layer computes, written from the paper's definitions (SharQ, arXiv 2606.26587):
+
+  * group-wise symmetric quantization with a codebook projection
+    (Sec. 3.1, eq. "group-quant"), instantiated as MXFP4 (E2M1 elements with an
+    E8M0 power-of-two scale per 32 values, App. A.1.1) and NVFP4 (E2M1 with an
+    E4M3 scale per 16 plus a per-tensor scale, App. A.1.2-A.1.3);
+  * the online N:M activation mask that keeps the top-N magnitudes of every
+    group of M (Sec. 3.1 eq. "dynamic-mask", Sec. 3.3 eq. "sharq-sparse-backbone");
+  * the quantized sparse backbone (Sec. 3.3 eq. "sharq-quantized-backbone") and
+    the dense residual taken against the *dequantized* backbone
+    (Sec. 3.3 eq. "sharq-residual");
+  * the two-path output, backbone GEMM plus residual GEMM over one shared
+    quantized weight (Sec. 3.3 eq. "sharq-output", Sec. 3.4);
+  * RMSNorm folded into the preparation for layers that have it (Sec. 3.4,
+    "Fused sparse-residual preparation"; Fig. 2).
+
+Only tests, the package's smoke check and the benchmark's CPU-baseline leg may
+import this module.  The product path never calls it; it shares no code with
+the HIP library (no common tables, helpers or generators).
+
+Precision.  Every step that decides an integer (a mask bit, a scale exponent,
+an FP4 code) is evaluated in IEEE fp32 with round-to-nearest-even and no fused
+multiply-add, which is the precision the kernels decide in; the paper does not
+fix one.  The RMSNorm reciprocal is evaluated in fp64 and rounded once to fp32.
+The GEMMs are evaluated in fp64 over exactly dequantized operands.
+
+Readings where the paper is silent (each also listed in the design notes):
+  R1  RMSNorm: sum of squares as a balanced binary tree over K padded with
+      zeros to a power of two, in fp32; r = fp32(1/sqrt(fp64(ss)/K + fp64(eps)));
+      y = fp32(fp32(x*r)*gamma).  Without gamma, y = x.
+  R2  The normalized row is not rounded to bf16 before masking/quantizing.
+  R3  Mask score is |y|; ties go to the lower index.
+  R4  MXFP4 scale: OCP floor rule, e = max(floor(log2 amax) - 2, -127),
+      e = -127 for an all-zero block; E2M1 saturates at 6.
+  R5  E2M1 projection ties go to the even code; the sign of zero is kept.
+  R6  Backbone scale blocks are 32 logical K positions.
+  R7  NVFP4: per-tensor scale S = amax/2688 over the whole call (S = 1 when
+      amax = 0); block scale E4M3(amax_b / (6 S)); code E2M1(y / (d_b S));
+      a zero block scale gives signed-zero codes.  Backbone blocks 32 logical
+      positions, residual blocks 16.  Weights: one E4M3 scale per 32 shared by
+      both paths, the dense view duplicating it per 16.
+"""
+
+from __future__ import annotations
+
+import itertools
+import math
+
+import numpy as np
+
+# ---------------------------------------------------------------------------
+# Element formats (App. A.1.2 "Format structure")
+# ---------------------------------------------------------------------------
+
+#: E2M1 magnitudes indexed by the three low code bits (App. A.1.2).
+E2M1_MAGNITUDES = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0], dtype=np.float64)
+E2M1_MAX = 6.0
+#: NVFP4 per-tensor target, "typically 2688 for activations" (App. A.1.3).
+PTS_TARGET = 2688.0
+E4M3_MAX = 448.0
+MX_BLOCK = 32
+NV_BLOCK = 16
+
+
+def bf16_bits_to_f32(u16: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns -> fp32 values (exact: the bf16 bits are the top half)."""
+    u16 = np.asarray(u16, dtype=np.uint16)
+    return (u16.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def e2m1_encode(v: np.ndarray) -> np.ndarray:
+    """Project fp32 values onto the E2M1 grid (eq. group-quant's projection).
+
+    Nearest representable magnitude with ties to the even code, saturating at 6;
+    bit 3 of the code is the sign bit of the input (so -0 and small negatives
+    give 0x8).  The thresholds below are the midpoints between neighbouring grid
+    magnitudes; '>' sends a tie down (to an even code), '>=' sends it up.
+    """
+    v = np.asarray(v, dtype=np.float32)
+    a = np.abs(v)
+    mag = np.zeros(a.shape, dtype=np.uint8)
+    mag += a > np.float32(0.25)   # 0 | 0.5   tie -> 0   (code 0 even)
+    mag += a >= np.float32(0.75)  # 0.5 | 1   tie -> 1   (code 2 even)
+    mag += a > np.float32(1.25)   # 1 | 1.5   tie -> 1   (code 2 even)
+    mag += a >= np.float32(1.75)  # 1.5 | 2   tie -> 2   (code 4 even)
+    mag += a > np.float32(2.5)    # 2 | 3     tie -> 2   (code 4 even)
+    mag += a >= np.float32(3.5)   # 3 | 4     tie -> 4   (code 6 even)
+    mag += a > np.float32(5.0)    # 4 | 6     tie -> 4   (code 6 even); > 6 saturates
+    sign = np.signbit(v).astype(np.uint8) << np.uint8(3)
+    return (sign | mag).astype(np.uint8)
+
+
+def e2m1_decode(codes: np.ndarray) -> np.ndarray:
+    """E2M1 code -> value in fp64: (-1)^(c>>3) * magnitude[c & 7]."""
+    c = np.asarray(codes, dtype=np.uint8)
+    mag = E2M1_MAGNITUDES[c & 7]
+    return np.where((c >> 3) & 1, -mag, mag)
+
+
+def _floor_log2_f32(a: np.ndarray) -> np.ndarray:
+    """floor(log2 a) for positive fp32 a, read exactly from the bit pattern."""
+    bits = np.asarray(a, dtype=np.float32).view(np.uint32).astype(np.int64)
+    expf = (bits >> 23) & 0xFF
+    mant = bits & 0x7FFFFF
+    # subnormal: a = mant * 2^-149, floor(log2 a) = bit_length(mant) - 1 - 149
+    # frexp(mant) = f * 2^x with f in [0.5, 1), so bit_length(mant) = x
+    sub = np.frexp(np.maximum(mant, 1).astype(np.float64))[1].astype(np.int64) - 1 - 149
+    return np.where(expf > 0, expf - 127, sub)
+
+
+def e8m0_exponent(amax: np.ndarray) -> np.ndarray:
+    """Shared MXFP4 exponent of a block with max magnitude amax (reading R4).
+
+    OCP Microscaling rule: e = floor(log2 amax) - emax(E2M1), emax = 2, clamped
+    to the E8M0 minimum -127; an all-zero block takes -127 (code 0).
+    """
+    amax = np.asarray(amax, dtype=np.float32)
+    e = np.maximum(_floor_log2_f32(np.where(amax > 0, amax, np.float32(1.0))) - 2, -127)
+    return np.where(amax > 0, e, -127).astype(np.int64)
+
+
+def pow2_f32(e: np.ndarray) -> np.ndarray:
+    """2^e as fp32 for integer e in [-149, 127] (exact, including subnormals)."""
+    e = np.asarray(e, dtype=np.int64)
+    out = np.where(e >= -126, ((np.clip(e, -126, 127) + 127) << 23), 1 << np.clip(e + 149, 0, 22))
+    return out.astype(np.uint32).view(np.float32)
+
+
+def e4m3_values() -> np.ndarray:
+    """All 126 finite non-negative E4M3 values (bias 7; exponent field 0 is subnormal).
+
+    Code (E, M): E > 0 -> 2^(E-7) (1 + M/8); E = 0 -> 2^-6 (M/8).  (E, M) = (15, 7)
+    is NaN in this variant, so the largest value is 2^8 * 1.75 = 448.
+    """
+    vals = []
+    for E in range(16):
+        for M in range(8):
+            if E == 15 and M == 7:
+                continue
+            vals.append((M / 8.0) * 2.0 ** -6 if E == 0 else (1 + M / 8.0) * 2.0 ** (E - 7))
+    return np.array(vals, dtype=np.float64)
+
+
+def e4m3_round(a: np.ndarray) -> np.ndarray:
+    """Round non-negative fp32 values to E4M3 (nearest, ties to even mantissa, saturating at 448).
+
+    Within binade 2^E (E >= -6) the E4M3 spacing is 2^(E-3); below 2^-6 the
+    subnormal spacing is 2^-9.  Returned as fp32 (every E4M3 value is exact in fp32).
+    """
+    a = np.asarray(a, dtype=np.float64)
+    E = np.frexp(np.where(a > 0, a, 1.0))[1].astype(np.float64) - 1   # floor(log2 a), exact
+    E = np.maximum(E, -6)
+    q = 2.0 ** (E - 3)
+    r = np.rint(a / q) * q          # np.rint rounds half to even; a/q is exact
+    r = np.minimum(r, E4M3_MAX)
+    r = np.where(a > 0, r, 0.0)
+    return r.astype(np.float32)
+
+
+def e4m3_encode_bits(v: np.ndarray) -> np.ndarray:
+    """E4M3 value (non-negative, exactly representable) -> its 8-bit code."""
+    v = np.asarray(v, dtype=np.float64)
+    out = np.zeros(v.shape, dtype=np.uint8)
+    nz = v > 0
+    E = np.frexp(np.where(nz, v, 1.0))[1].astype(np.int64) - 1
+    normal = nz & (E >= -6)
+    man_n = np.rint((v / 2.0 ** E - 1.0) * 8).astype(np.int64)
+    out = np.where(normal, ((E + 7) << 3) | man_n, out)
+    sub = nz & (E < -6)
+    man_s = np.rint(v / 2.0 ** -9).astype(np.int64)
+    out = np.where(sub, man_s, out)
+    return out.astype(np.uint8)
+
+
+def e4m3_decode_bits(c: np.ndarray) -> np.ndarray:
+    c = np.asarray(c, dtype=np.int64)
+    E = (c >> 3) & 15
+    M = c & 7
+    return np.where(E > 0, (1 + M / 8.0) * 2.0 ** (E - 7), (M / 8.0) * 2.0 ** -6)
+
+
+# ---------------------------------------------------------------------------
+# RMSNorm (Sec. 3.4 "Fused sparse-residual preparation", readings R1, R2)
+# ---------------------------------------------------------------------------
+
+def rms_sum_sq_tree(x: np.ndarray) -> np.ndarray:
+    """Sum of squares per row as a balanced binary tree in fp32 (reading R1).
+
+    Leaves are fl32(x_k * x_k) for k < K and zero up to the next power of two;
+    every internal node is the fp32 sum of its two children.
+    """
+    x = np.asarray(x, dtype=np.float32)
+    T, K = x.shape
+    L = 1
+    while L < K:
+        L *= 2
+    level = np.zeros((T, L), dtype=np.float32)
+    level[:, :K] = x * x
+    while level.shape[1] > 1:
+        level = level[:, 0::2] + level[:, 1::2]
+    return level[:, 0]
+
+
+def rms_reciprocal(ss: np.ndarray, K: int, eps: float) -> np.ndarray:
+    """r = fp32(1 / sqrt(fp64(ss)/K + fp64(eps))) with eps first rounded to fp32."""
+    ss64 = np.asarray(ss, dtype=np.float32).astype(np.float64)
+    eps64 = np.float64(np.float32(eps))
+    return (1.0 / np.sqrt(ss64 / np.float64(K) + eps64)).astype(np.float32)
+
+
+def rmsnorm(x: np.ndarray, gamma: np.ndarray | None, eps: float):
+    """y = (x * r) * gamma in fp32, or y = x without gamma.  Returns (y, r)."""
+    x = np.asarray(x, dtype=np.float32)
+    T, K = x.shape
+    if gamma is None:
+        return x.copy(), np.ones(T, dtype=np.float32)
+    r = rms_reciprocal(rms_sum_sq_tree(x), K, eps)
+    y = (x * r[:, None]).astype(np.float32) * np.asarray(gamma, dtype=np.float32)[None, :]
+    return y.astype(np.float32), r
+
+
+# ---------------------------------------------------------------------------
+# Online N:M mask (eq. dynamic-mask; eq. sharq-sparse-backbone; reading R3)
+# ---------------------------------------------------------------------------
+
+def nm_mask(y: np.ndarray, n: int, m: int) -> np.ndarray:
+    """Keep the n largest |y| in every group of m consecutive K positions.
+
+    rank_k = #{k' in group : |y_k'| > |y_k|, or |y_k'| == |y_k| and k' < k};
+    position k is kept iff rank_k < n, so exactly n positions survive per group.
+    """
+    y = np.asarray(y, dtype=np.float32)
+    T, K = y.shape
+    a = np.abs(y).reshape(T, K // m, m)
+    rank = np.zeros(a.shape, dtype=np.int64)
+    for k in range(m):
+        for kp in range(m):
+            if kp == k:
+                continue
+            beats = a[..., kp] > a[..., k]
+            if kp < k:
+                beats = beats | (a[..., kp] == a[..., k])
+            rank[..., k] += beats
+    return (rank < n).reshape(T, K)
+
+
+# ---------------------------------------------------------------------------
+# MXFP4 block quantization (eq. group-quant with an E8M0 block scale)
+# ---------------------------------------------------------------------------
+
+def mx_quantize(vals: np.ndarray, present: np.ndarray | None = None):
+    """Quantize rows of fp32 values to MXFP4 in blocks of 32 along K.
+
+    `present` marks the positions that belong to the tensor (the backbone's kept
+    positions); the block amax is taken over those only and the others get
+    code 0.  Returns (codes uint8 [T,K], exponent int [T,K/32], scale code
+    uint8 [T,K/32], dequantized values fp32 [T,K]).
+    """
+    v = np.asarray(vals, dtype=np.float32)
+    T, K = v.shape
+    if present is None:
+        present = np.ones(v.shape, dtype=bool)
+    mag = np.where(present, np.abs(v), np.float32(0.0)).reshape(T, K // MX_BLOCK, MX_BLOCK)
+    amax = mag.max(axis=2)
+    e = e8m0_exponent(amax)
+    e_full = np.repeat(e, MX_BLOCK, axis=1)
+    # v / 2^e: exact division by a power of two (fp32, correctly rounded);
+    # positions outside `present` may overflow here and are discarded below
+    with np.errstate(over="ignore"):
+        scaled = (v / pow2_f32(e_full)).astype(np.float32)
+    codes = np.where(present, e2m1_encode(scaled), np.uint8(0)).astype(np.uint8)
+    deq = (e2m1_decode(codes) * pow2_f32(e_full).astype(np.float64)).astype(np.float32)
+    deq = np.where(present, deq, np.float32(0.0)).astype(np.float32)
+    return codes, e, (e + 127).astype(np.uint8), deq
+
+
+# ---------------------------------------------------------------------------
+# NVFP4 block quantization (App. A.1.2-A.1.3; reading R7)
+# ---------------------------------------------------------------------------
+
+def pts_scale(amax: float) -> np.float32:
+    """Per-tensor scale S = fl32(amax / 2688), or 1 for an all-zero tensor."""
+    amax = np.float32(amax)
+    if amax == 0:
+        return np.float32(1.0)
+    return np.float32(amax / np.float32(PTS_TARGET))
+
+
+def nv_quantize(vals: np.ndarray, S: np.float32, block: int, present: np.ndarray | None = None):
+    """NVFP4 quantization of rows in blocks of `block` along K under per-tensor scale S.
+
+    d_b = E4M3(fl32(amax_b / fl32(6 S))); code = E2M1(fl32(v / fl32(d_b S)));
+    dequantized value fl32(fl32(q d_b) S).  A zero d_b gives signed-zero codes.
+    Returns (codes, scale value d_b fp32 [T,K/block], scale code uint8, deq fp32).
+    """
+    v = np.asarray(vals, dtype=np.float32)
+    T, K = v.shape
+    S = np.float32(S)
+    if present is None:
+        present = np.ones(v.shape, dtype=bool)
+    mag = np.where(present, np.abs(v), np.float32(0.0)).reshape(T, K // block, block)
+    amax = mag.max(axis=2).astype(np.float32)
+    six_s = np.float32(np.float32(E2M1_MAX) * S)
+    d = e4m3_round((amax / six_s).astype(np.float32))
+    d_full = np.repeat(d, block, axis=1)
+    step = (d_full * S).astype(np.float32)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        scaled = np.where(d_full > 0, v / np.where(step > 0, step, np.float32(1.0)), np.float32(0.0) * v)
+    scaled = scaled.astype(np.float32)
+    codes = e2m1_encode(scaled)
+    codes = np.where(d_full > 0, codes, (np.signbit(v).astype(np.uint8) << 3)).astype(np.uint8)
+    codes = np.where(present, codes, np.uint8(0)).astype(np.uint8)
+    qd = (e2m1_decode(codes) * d_full.astype(np.float64)).astype(np.float32)   # exact
+    deq = (qd * S).astype(np.float32)
+    deq = np.where(present, deq, np.float32(0.0)).astype(np.float32)
+    return codes, d, e4m3_encode_bits(d), deq
+
+
+# ---------------------------------------------------------------------------
+# Packing into the library's buffer layout
+# ---------------------------------------------------------------------------
+
+def pack_nibbles(codes: np.ndarray) -> np.ndarray:
+    """[T, 2J] 4-bit codes -> [T, J] bytes, element 2j in the low nibble."""
+    c = np.asarray(codes, dtype=np.uint8)
+    return (c[:, 0::2] & 0xF) | ((c[:, 1::2] & 0xF) << 4)
+
+
+def unpack_nibbles(b: np.ndarray) -> np.ndarray:
+    b = np.asarray(b, dtype=np.uint8)
+    out = np.empty((b.shape[0], b.shape[1] * 2), dtype=np.uint8)
+    out[:, 0::2] = b & 0xF
+    out[:, 1::2] = b >> 4
+    return out
+
+
+def pack_backbone(codes: np.ndarray, keep: np.ndarray, n: int, m: int):
+    """Compress the backbone: kept codes in ascending K, plus index metadata.
+
+    m = 4, n = 2: per group the two kept positions i0 < i1 as (i0 | i1 << 2),
+    two groups per byte (even group in the low nibble).
+    m = 8: per group an 8-bit keep mask (bit p = position p kept).
+    """
+    T, K = codes.shape
+    kept = codes[keep].reshape(T, K * n // m)
+    sp_codes = pack_nibbles(kept)
+    g = keep.reshape(T, K // m, m)
+    if m == 4 and n == 2:
+        pos = np.nonzero(g.reshape(-1, m))[1].reshape(T, K // m, 2)
+        nib = (pos[..., 0] | (pos[..., 1] << 2)).astype(np.uint8)
+        sp_meta = pack_nibbles(nib)
+    elif m == 8:
+        weights = (1 << np.arange(8)).astype(np.int64)
+        sp_meta = (g.astype(np.int64) * weights).sum(axis=2).astype(np.uint8)
+    else:
+        raise ValueError(f"no metadata layout for {n}:{m}")
+    return sp_codes, sp_meta
+
+
+def unpack_backbone(sp_codes: np.ndarray, sp_meta: np.ndarray, K: int, n: int, m: int):
+    """Inverse of pack_backbone: -> (dense codes [T,K] with 0 at pruned positions, keep)."""
+    T = sp_codes.shape[0]
+    kept = unpack_nibbles(sp_codes)
+    keep = np.zeros((T, K // m, m), dtype=bool)
+    if m == 4 and n == 2:
+        nib = unpack_nibbles(sp_meta)
+        i0 = nib & 3
+        i1 = (nib >> 2) & 3
+        t, g = np.meshgrid(np.arange(T), np.arange(K // m), indexing="ij")
+        keep[t, g, i0] = True
+        keep[t, g, i1] = True
+    elif m == 8:
+        for p in range(8):
+            keep[:, :, p] = (sp_meta >> p) & 1
+    else:
+        raise ValueError(f"no metadata layout for {n}:{m}")
+    keep = keep.reshape(T, K)
+    dense = np.zeros((T, K), dtype=np.uint8)
+    dense[keep] = kept.reshape(-1)
+    return dense, keep
+
+
+# ---------------------------------------------------------------------------
+# Preparation (Sec. 3.3 eqs. sharq-sparse-backbone / quantized-backbone / residual)
+# ---------------------------------------------------------------------------
+
+def prepare(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: int, m: int,
+            fmt: str = "mx", tensor_scale: float | None = None) -> dict:
+    """Activation preparation for one linear call.
+
+    1. y = RMSNorm(x) * gamma (or y = x);
+    2. keep = top-n of |y| per group of m;
+    3. backbone: quantize y on the kept positions (X_sp = M(X) o X, then Q_sp);
+    4. residual R = y - D_sp(Q_sp(X_sp)), taken against the dequantized backbone;
+    5. quantize R densely (Q_dn).
+    Returns the packed buffers plus debug arrays.
+    """
+    x = bf16_bits_to_f32(x_bf16)
+    T, K = x.shape
+    g = None if gamma_bf16 is None else bf16_bits_to_f32(gamma_bf16)
+    y, r = rmsnorm(x, g, eps)
+    keep = nm_mask(y, n, m) if n > 0 else np.zeros(y.shape, dtype=bool)
+    out = {"rows": T, "K": K, "n": n, "m": m, "fmt": fmt, "y": y, "r": r, "keep": keep}
+    if fmt == "mx":
+        sp_c, _, sp_s, d_sp = mx_quantize(y, keep)
+        R = (y - d_sp).astype(np.float32)
+        dn_c, _, dn_s, d_dn = mx_quantize(R)
+        out["tensor_scale"] = None
+    elif fmt == "nv":
+        if tensor_scale is None:
+            S = pts_scale(np.abs(y).max() if y.size else 0.0)
+        else:
+            S = np.float32(tensor_scale)
+        sp_c, _, sp_s, d_sp = nv_quantize(y, S, MX_BLOCK, keep)
+        R = (y - d_sp).astype(np.float32)
+        dn_c, _, dn_s, d_dn = nv_quantize(R, S, NV_BLOCK)
+        out["tensor_scale"] = np.float32(S)
+    else:
+        raise ValueError(fmt)
+    if n > 0:
+        out["sp_codes"], out["sp_meta"] = pack_backbone(sp_c, keep, n, m)
+    else:
+        out["sp_codes"] = np.zeros((T, 0), np.uint8)
+        out["sp_meta"] = np.zeros((T, 0), np.uint8)
+    out.update(sp_scale=sp_s, dn_codes=pack_nibbles(dn_c), dn_scale=dn_s,
+               d_sp=d_sp, R=R, d_dn=d_dn)
+    return out
+
+
+def quantize_weight(w_bf16: np.ndarray, fmt: str = "mx") -> dict:
+    """Quantize W [N,K] once into one shared FP4 payload (Sec. 3.4, "Shared FP4 weights").
+
+    MXFP4: E8M0 per 32 along K, used by both paths.  NVFP4: per-tensor scale
+    S_w = amax(W)/2688, E4M3 per 32 (the sparse view), and a dense view that
+    repeats every scale for its two 16-element halves.
+    """
+    w = bf16_bits_to_f32(w_bf16)
+    N, K = w.shape
+    if fmt == "mx":
+        c, _, s, deq = mx_quantize(w)
+        return {"N": N, "K": K, "fmt": "mx", "codes": pack_nibbles(c), "scale": s,
+                "scale_dn": s, "tensor_scale": None, "deq": deq}
+    S = pts_scale(np.abs(w).max() if w.size else 0.0)
+    c, _, s, deq = nv_quantize(w, S, MX_BLOCK)
+    return {"N": N, "K": K, "fmt": "nv", "codes": pack_nibbles(c), "scale": s,
+            "scale_dn": np.repeat(s, 2, axis=1), "tensor_scale": np.float32(S), "deq": deq}
+
+
+# ---------------------------------------------------------------------------
+# Dequantization from the packed buffers, and the two-path GEMM
+# ---------------------------------------------------------------------------
+
+def _block_scale_values(scale_codes: np.ndarray, fmt: str, block: int, K: int) -> np.ndarray:
+    s = np.asarray(scale_codes)
+    if fmt == "mx":
+        vals = 2.0 ** (s.astype(np.float64) - 127.0)
+    else:
+        vals = e4m3_decode_bits(s)
+    return np.repeat(vals, block, axis=1)[:, :K]
+
+
+def dequant_act(act: dict):
+    """Packed prepared activation -> (backbone fp64 [T,K], residual fp64 [T,K]).
+
+    Values are exact: E2M1 x E8M0 (or x E4M3 x S) products fit in fp64.
+    """
+    K, n, m, fmt = act["K"], act["n"], act["m"], act["fmt"]
+    T = act["dn_codes"].shape[0]
+    S = 1.0 if fmt == "mx" else float(act["tensor_scale"])
+    if n > 0:
+        dense, keep = unpack_backbone(act["sp_codes"], act["sp_meta"], K, n, m)
+        a_sp = e2m1_decode(dense) * _block_scale_values(act["sp_scale"], fmt, MX_BLOCK, K) * S
+        a_sp = np.where(keep, a_sp, 0.0)
+    else:
+        a_sp = np.zeros((T, K))
+    dn_block = MX_BLOCK if fmt == "mx" else NV_BLOCK
+    a_dn = e2m1_decode(unpack_nibbles(act["dn_codes"])) * _block_scale_values(act["dn_scale"], fmt, dn_block, K) * S
+    return a_sp, a_dn
+
+
+def dequant_weight(wq: dict, view: str = "sp") -> np.ndarray:
+    """Shared weight payload -> fp64 [N,K] through the sparse or the dense scale view."""
+    K, fmt = wq["K"], wq["fmt"]
+    S = 1.0 if fmt == "mx" else float(wq["tensor_scale"])
+    if view == "sp" or fmt == "mx":
+        sv = _block_scale_values(wq["scale"], fmt, MX_BLOCK, K)
+    else:
+        sv = _block_scale_values(wq["scale_dn"], fmt, NV_BLOCK, K)
+    return e2m1_decode(unpack_nibbles(wq["codes"])) * sv * S
+
+
+def linear(act: dict, wq: dict, rows: np.ndarray | None = None) -> np.ndarray:
+    """Two-path output (eq. sharq-output) in fp64: Y = X~_sp W_sp^T + R~ W_dn^T.
+
+    `rows` optionally restricts the computation to a subset of activation rows.
+    """
+    a_sp, a_dn = dequant_act(act)
+    if rows is not None:
+        a_sp, a_dn = a_sp[rows], a_dn[rows]
+    w_sp = dequant_weight(wq, "sp")
+    w_dn = dequant_weight(wq, "dn")
+    return a_sp @ w_sp.T + a_dn @ w_dn.T
+
+
+def linear_abs(act: dict, wq: dict, rows: np.ndarray | None = None) -> np.ndarray:
+    """sum_k |a_sp w| + |a_dn w| per output: the scale of the accumulation error."""
+    a_sp, a_dn = dequant_act(act)
+    if rows is not None:
+        a_sp, a_dn = a_sp[rows], a_dn[rows]
+    return np.abs(a_sp) @ np.abs(dequant_weight(wq, "sp")).T + np.abs(a_dn) @ np.abs(dequant_weight(wq, "dn")).T
+
+
+def linear_grouped(act: dict, row_index: np.ndarray | None, expert_offsets: np.ndarray,
+                   weights: list) -> np.ndarray:
+    """Grouped (MoE) form: Y[i] = SharQ(A[row_index[i]], W_e) for i in [off_e, off_e+1)."""
+    total = int(expert_offsets[-1])
+    N = weights[0]["N"]
+    Y = np.zeros((total, N))
+    a_sp, a_dn = dequant_act(act)
+    for e, wq in enumerate(weights):
+        lo, hi = int(expert_offsets[e]), int(expert_offsets[e + 1])
+        if hi <= lo:
+            continue
+        rows = np.arange(lo, hi) if row_index is None else np.asarray(row_index[lo:hi])
+        Y[lo:hi] = a_sp[rows] @ dequant_weight(wq, "sp").T + a_dn[rows] @ dequant_weight(wq, "dn").T
+    return Y
+
+
+def gemm_gate_error(y_hat: np.ndarray, y_ref: np.ndarray, y_abs: np.ndarray) -> float:
+    """max |Y^ - Y| / sum_k(|a_sp w| + |a_dn w|), the componentwise accumulation error."""
+    den = np.where(y_abs > 0, y_abs, 1.0)
+    err = np.abs(np.asarray(y_hat, np.float64) - y_ref) / den
+    err = np.where(y_abs > 0, err, np.abs(np.asarray(y_hat, np.float64) - y_ref))
+    return float(err.max()) if err.size else 0.0
+
+
+def subsets(m: int, n: int):
+    """All n-subsets of range(m) (helper for brute-force checks)."""
+    return itertools.combinations(range(m), n)
+
+
+__all__ = [name for name in dir() if not name.startswith("_")] + ["_floor_log2_f32"]
