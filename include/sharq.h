@@ -21,7 +21,8 @@
  *     built), SHARQ_EALIGN (a pointer not aligned as stated below),
  *     SHARQ_EHIP (the HIP runtime reported an error at launch).
  *   - Inputs must be finite; NaN or Inf inputs give unspecified results.
- *   - Row counts of 0 are valid and launch nothing.
+ *   - Row counts of 0 are valid and launch nothing; the buffers of an empty
+ *     tensor may then be NULL.
  *
  * Numeric formats (App. A.1 of the paper)
  *   E2M1 element code: bit 3 = sign, bits 0-2 index {0, .5, 1, 1.5, 2, 3, 4, 6}.
@@ -39,6 +40,10 @@
 
 #ifdef __cplusplus
 extern "C" {
+#endif
+
+#ifndef SHARQ_API
+#define SHARQ_API __attribute__((visibility("default")))
 #endif
 
 typedef enum {
@@ -119,9 +124,9 @@ typedef struct {
 
 /* Bytes of each buffer of a prepared activation / quantized weight (host-side
  * sizing helpers, no device work).  Return 0 for an invalid combination. */
-size_t sharq_act_buffer_bytes(int64_t rows, int64_t K, sharq_format fmt, sharq_pattern nm,
+SHARQ_API size_t sharq_act_buffer_bytes(int64_t rows, int64_t K, sharq_format fmt, sharq_pattern nm,
                               int32_t which /* 0 sp_codes, 1 sp_meta, 2 sp_scale, 3 dn_codes, 4 dn_scale */);
-size_t sharq_weight_buffer_bytes(int64_t N, int64_t K, sharq_format fmt,
+SHARQ_API size_t sharq_weight_buffer_bytes(int64_t N, int64_t K, sharq_format fmt,
                                  int32_t which /* 0 codes, 1 scale, 2 scale_dn */);
 
 /*
@@ -133,7 +138,7 @@ size_t sharq_weight_buffer_bytes(int64_t N, int64_t K, sharq_format fmt,
  * duplicated per 16.  `out` fields N, K, fmt and the buffers must be set by
  * the caller; experts must be 1.
  */
-sharq_status sharq_quantize_weight(const void *W, sharq_dtype wdt, int64_t N, int64_t K, int64_t ldw,
+SHARQ_API sharq_status sharq_quantize_weight(const void *W, sharq_dtype wdt, int64_t N, int64_t K, int64_t ldw,
                                    sharq_weight *out, void *stream);
 
 /*
@@ -153,7 +158,7 @@ sharq_status sharq_quantize_weight(const void *W, sharq_dtype wdt, int64_t N, in
  * *tensor_scale_in (device) is used and copied there.
  * out->rows, K, fmt, nm and the buffers must match the arguments.
  */
-sharq_status sharq_prepare(const void *X, sharq_dtype xdt, int64_t M, int64_t K, int64_t ldx,
+SHARQ_API sharq_status sharq_prepare(const void *X, sharq_dtype xdt, int64_t M, int64_t K, int64_t ldx,
                            const void *gamma, float eps, sharq_pattern nm, sharq_format fmt,
                            const float *tensor_scale_in, sharq_act *out, void *stream);
 
@@ -164,7 +169,7 @@ sharq_status sharq_prepare(const void *X, sharq_dtype xdt, int64_t M, int64_t K,
  * both products accumulated in one fp32 accumulator and written once.
  * The activation and weight formats must match.
  */
-sharq_status sharq_linear(const sharq_act *a, const sharq_weight *w, void *Y, sharq_dtype ydt,
+SHARQ_API sharq_status sharq_linear(const sharq_act *a, const sharq_weight *w, void *Y, sharq_dtype ydt,
                           int64_t ldy, void *stream);
 
 /*
@@ -176,15 +181,15 @@ sharq_status sharq_linear(const sharq_act *a, const sharq_weight *w, void *Y, sh
  * NULL.  Y [total][N] (row stride ldy).  Offsets are read on the device; the
  * host never waits for them.
  */
-sharq_status sharq_linear_grouped(const sharq_act *a, const int32_t *row_index,
+SHARQ_API sharq_status sharq_linear_grouped(const sharq_act *a, const int32_t *row_index,
                                   const int32_t *expert_offsets, int64_t total,
                                   const sharq_weight *w, void *Y, sharq_dtype ydt, int64_t ldy,
                                   void *stream);
 
-const char *sharq_status_str(sharq_status s);
+SHARQ_API const char *sharq_status_str(sharq_status s);
 
 /* Library version string. */
-const char *sharq_version(void);
+SHARQ_API const char *sharq_version(void);
 
 #ifdef __cplusplus
 }

@@ -1,0 +1,192 @@
+// C ABI of the SharQ library: argument validation and kernel dispatch.  The
+// entry points and their contracts are declared in include/sharq.h.
+
+#include <limits.h>
+
+#include "../../include/sharq.h"
+#include "sharq_device.hpp"
+
+namespace sharq {
+hipError_t launch_prep_mx(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps, int pat,
+                          uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, hipStream_t st);
+hipError_t launch_wquant_mx(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
+                            hipStream_t st);
+hipError_t launch_linear_mx(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
+                            const uint8_t* dnc, const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws,
+                            int N, int K, void* Y, int64_t ldy, hipStream_t st);
+hipError_t launch_linear_mx_grouped(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
+                                    const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx,
+                                    const int32_t* offs, int E, int64_t total, const uint8_t* wc, const uint8_t* ws,
+                                    int N, int K, void* Y, int64_t ldy, hipStream_t st);
+}  // namespace sharq
+
+namespace {
+
+constexpr int64_t kMaxK = 1 << 20;
+constexpr int64_t kMaxNormK = 16384;   // RMSNorm rows are held in registers
+constexpr int kMaxExperts = 1024;
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+// 24 for 2:4, 48 for 4:8, 0 if the pattern is valid but not built, -1 if invalid
+int pattern_id(sharq_pattern nm) {
+  if (nm.m <= 0 || nm.n < 0 || nm.n > nm.m) return -1;
+  if (nm.n == 2 && nm.m == 4) return 24;
+  if (nm.n == 4 && nm.m == 8) return 48;
+  return 0;
+}
+
+sharq_status hip_status(hipError_t e) { return e == hipSuccess ? SHARQ_OK : SHARQ_EHIP; }
+
+sharq_status check_act(const sharq_act* a) {
+  if (!a) return SHARQ_EINVAL;
+  if (a->rows < 0 || a->rows > INT_MAX || a->K <= 0 || a->K % 32 != 0 || a->K > kMaxK) return SHARQ_EINVAL;
+  const int pid = pattern_id(a->nm);
+  if (pid < 0 || a->K % a->nm.m != 0) return SHARQ_EINVAL;
+  if (pid == 0) return SHARQ_EUNSUPPORTED;
+  if (a->fmt != SHARQ_MXFP4) return a->fmt == SHARQ_NVFP4 ? SHARQ_EUNSUPPORTED : SHARQ_EINVAL;
+  if (a->rows == 0) return SHARQ_OK;   // an empty activation is never dereferenced
+  if (!a->sp_codes || !a->sp_meta || !a->sp_scale || !a->dn_codes || !a->dn_scale) return SHARQ_EINVAL;
+  if (!aligned(a->sp_codes, 16) || !aligned(a->dn_codes, 16) || !aligned(a->sp_meta, 4) ||
+      !aligned(a->sp_scale, 4) || !aligned(a->dn_scale, 4))
+    return SHARQ_EALIGN;
+  return SHARQ_OK;
+}
+
+sharq_status check_weight(const sharq_weight* w) {
+  if (!w) return SHARQ_EINVAL;
+  if (w->N < 0 || w->N > INT_MAX || w->K <= 0 || w->K % 32 != 0 || w->K > kMaxK || w->experts < 1 ||
+      w->experts > kMaxExperts)
+    return SHARQ_EINVAL;
+  if (w->fmt != SHARQ_MXFP4) return w->fmt == SHARQ_NVFP4 ? SHARQ_EUNSUPPORTED : SHARQ_EINVAL;
+  if (!w->codes || !w->scale) return SHARQ_EINVAL;
+  if (!aligned(w->codes, 16) || !aligned(w->scale, 4)) return SHARQ_EALIGN;
+  return SHARQ_OK;
+}
+
+bool ydt_ok(sharq_dtype d) { return d == SHARQ_BF16 || d == SHARQ_F16 || d == SHARQ_F32; }
+size_t ysize(sharq_dtype d) { return d == SHARQ_F32 ? 4 : 2; }
+
+}  // namespace
+
+extern "C" {
+
+const char* sharq_version(void) { return "sharq-gfx950 0.1"; }
+
+const char* sharq_status_str(sharq_status s) {
+  switch (s) {
+    case SHARQ_OK: return "ok";
+    case SHARQ_EINVAL: return "invalid argument";
+    case SHARQ_EUNSUPPORTED: return "unsupported format/pattern/dtype combination";
+    case SHARQ_EALIGN: return "misaligned pointer or leading dimension";
+    case SHARQ_EHIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+size_t sharq_act_buffer_bytes(int64_t rows, int64_t K, sharq_format fmt, sharq_pattern nm, int32_t which) {
+  if (rows < 0 || K <= 0 || K % 32 != 0 || pattern_id(nm) < 0 || K % nm.m != 0) return 0;
+  if (fmt != SHARQ_MXFP4 && fmt != SHARQ_NVFP4) return 0;
+  const size_t r = (size_t)rows, k = (size_t)K;
+  switch (which) {
+    case 0: return r * (k * (size_t)nm.n / (size_t)nm.m / 2);
+    case 1: return r * (k / 8);
+    case 2: return r * (k / 32);
+    case 3: return r * (k / 2);
+    case 4: return r * (fmt == SHARQ_MXFP4 ? k / 32 : k / 16);
+    default: return 0;
+  }
+}
+
+size_t sharq_weight_buffer_bytes(int64_t N, int64_t K, sharq_format fmt, int32_t which) {
+  if (N < 0 || K <= 0 || K % 32 != 0) return 0;
+  if (fmt != SHARQ_MXFP4 && fmt != SHARQ_NVFP4) return 0;
+  const size_t n = (size_t)N, k = (size_t)K;
+  switch (which) {
+    case 0: return n * (k / 2);
+    case 1: return n * (k / 32);
+    case 2: return n * (fmt == SHARQ_MXFP4 ? k / 32 : k / 16);
+    default: return 0;
+  }
+}
+
+sharq_status sharq_quantize_weight(const void* W, sharq_dtype wdt, int64_t N, int64_t K, int64_t ldw,
+                                   sharq_weight* out, void* stream) {
+  if (!W || !out) return SHARQ_EINVAL;
+  if (N < 0 || N > INT_MAX || K <= 0 || K % 32 != 0 || K > kMaxK || ldw < K) return SHARQ_EINVAL;
+  if (out->N != N || out->K != K || out->experts != 1) return SHARQ_EINVAL;
+  if (wdt != SHARQ_BF16 && wdt != SHARQ_F32) return SHARQ_EUNSUPPORTED;
+  if (out->fmt != SHARQ_MXFP4) return out->fmt == SHARQ_NVFP4 ? SHARQ_EUNSUPPORTED : SHARQ_EINVAL;
+  if (!out->codes || !out->scale) return SHARQ_EINVAL;
+  if (!aligned(W, 16) || (ldw * (int64_t)(wdt == SHARQ_F32 ? 4 : 2)) % 16 != 0 || !aligned(out->codes, 16))
+    return SHARQ_EALIGN;
+  if (N == 0) return SHARQ_OK;
+  return hip_status(sharq::launch_wquant_mx(W, (int)wdt, (int)N, (int)K, ldw, out->codes, out->scale,
+                                            reinterpret_cast<hipStream_t>(stream)));
+}
+
+sharq_status sharq_prepare(const void* X, sharq_dtype xdt, int64_t M, int64_t K, int64_t ldx, const void* gamma,
+                           float eps, sharq_pattern nm, sharq_format fmt, const float* tensor_scale_in,
+                           sharq_act* out, void* stream) {
+  (void)tensor_scale_in;
+  if (!out) return SHARQ_EINVAL;
+  if (M < 0 || M > INT_MAX || K <= 0 || K % 32 != 0 || K > kMaxK || ldx < K) return SHARQ_EINVAL;
+  if (!X && M > 0) return SHARQ_EINVAL;
+  const int pid = pattern_id(nm);
+  if (pid < 0 || K % nm.m != 0) return SHARQ_EINVAL;
+  if (out->rows != M || out->K != K || out->fmt != fmt || out->nm.n != nm.n || out->nm.m != nm.m)
+    return SHARQ_EINVAL;
+  if (xdt != SHARQ_BF16) return SHARQ_EUNSUPPORTED;
+  if (!(eps >= 0.0f)) return SHARQ_EINVAL;
+  sharq_status s = check_act(out);
+  if (s != SHARQ_OK) return s;
+  if (gamma && K > kMaxNormK) return SHARQ_EUNSUPPORTED;
+  if (!aligned(X, 16) || (ldx * 2) % 16 != 0 || (gamma && !aligned(gamma, 16))) return SHARQ_EALIGN;
+  if (M == 0) return SHARQ_OK;
+  return hip_status(sharq::launch_prep_mx(static_cast<const uint16_t*>(X), (int)M, (int)K, ldx,
+                                          static_cast<const uint16_t*>(gamma), eps, pid, out->sp_codes,
+                                          out->sp_meta, out->sp_scale, out->dn_codes, out->dn_scale,
+                                          reinterpret_cast<hipStream_t>(stream)));
+}
+
+sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sharq_dtype ydt, int64_t ldy,
+                          void* stream) {
+  sharq_status s = check_act(a);
+  if (s != SHARQ_OK) return s;
+  if (!Y && a->rows > 0) return SHARQ_EINVAL;
+  s = check_weight(w);
+  if (s != SHARQ_OK) return s;
+  if (a->fmt != w->fmt || a->K != w->K || w->experts != 1) return SHARQ_EINVAL;
+  if (!ydt_ok(ydt)) return SHARQ_EUNSUPPORTED;
+  if (ldy < w->N) return SHARQ_EINVAL;
+  if (!aligned(Y, ysize(ydt))) return SHARQ_EALIGN;
+  if (a->rows == 0 || w->N == 0) return SHARQ_OK;
+  return hip_status(sharq::launch_linear_mx(pattern_id(a->nm), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale,
+                                            a->dn_codes, a->dn_scale, a->rows, w->codes, w->scale, (int)w->N,
+                                            (int)w->K, Y, ldy, reinterpret_cast<hipStream_t>(stream)));
+}
+
+sharq_status sharq_linear_grouped(const sharq_act* a, const int32_t* row_index, const int32_t* expert_offsets,
+                                  int64_t total, const sharq_weight* w, void* Y, sharq_dtype ydt, int64_t ldy,
+                                  void* stream) {
+  if (!expert_offsets) return SHARQ_EINVAL;
+  sharq_status s = check_act(a);
+  if (s != SHARQ_OK) return s;
+  if (!Y && total > 0) return SHARQ_EINVAL;
+  s = check_weight(w);
+  if (s != SHARQ_OK) return s;
+  if (a->fmt != w->fmt || a->K != w->K) return SHARQ_EINVAL;
+  if (total < 0 || total > INT_MAX) return SHARQ_EINVAL;
+  if (!row_index && total > a->rows) return SHARQ_EINVAL;
+  if (!ydt_ok(ydt)) return SHARQ_EUNSUPPORTED;
+  if (ldy < w->N) return SHARQ_EINVAL;
+  if (!aligned(Y, ysize(ydt)) || !aligned(expert_offsets, 4) || (row_index && !aligned(row_index, 4)))
+    return SHARQ_EALIGN;
+  if (total == 0 || w->N == 0) return SHARQ_OK;
+  return hip_status(sharq::launch_linear_mx_grouped(
+      pattern_id(a->nm), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale, a->dn_codes, a->dn_scale, row_index,
+      expert_offsets, (int)w->experts, total, w->codes, w->scale, (int)w->N, (int)w->K, Y, ldy,
+      reinterpret_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,415 @@
+// SharQ two-path FP4 GEMM for gfx950 (SharQ Sec. 3.3 eq. "sharq-output";
+// Sec. 3.4 "Shared FP4 weights with path-specific scales" and "Residual path
+// compensation by accumulation").
+//
+//   Y = dequant(backbone) * dequant(W)^T + dequant(residual) * dequant(W)^T
+//
+// Both products run on the CDNA4 block-scaled MFMA
+// v_mfma_scale_f32_32x32x64_f8f6f4 with E2M1 operands and E8M0 scales, into
+// ONE fp32 accumulator; Y is written once.
+//
+// gfx950 has no sparse MFMA for FP4 operands (the sparse smfmac forms take
+// 8/16-bit inputs only), so the compressed 2:4 or 4:8 backbone is expanded to
+// dense E2M1 nibbles before it enters the MFMA.  The expansion is done in the
+// registers of the wavefront that owns the rows: each wavefront owns 32
+// distinct rows of the 128-row tile, so every compressed row is expanded
+// exactly once per tile and never goes through LDS.  The shared weight tile
+// (E2M1 payload + E8M0 scales) is staged through double-buffered LDS once per
+// K step and read by both MFMAs of every fragment.
+//
+// MFMA 32x32x64 FP4 operand layout (lane l, 64-wide wavefront): lane l holds
+// row (l % 32) and the 32 K values of block (l / 32) of the 64-wide K slice as
+// 32 nibbles in its first four dwords (lower K in the lower nibble); its
+// 32-bit scale operand supplies, through op_sel, the E8M0 byte of that row and
+// block.  Accumulator element r of lane l is output row
+// 8 (r / 4) + 4 (l / 32) + (r % 4), column l % 32.
+
+#include "sharq_device.hpp"
+
+namespace sharq {
+
+constexpr int kBM = 128;          // tile rows: 4 wavefronts x 32
+constexpr int kBK = 128;          // K per step: 4 scale blocks, 64 bytes of codes per row
+constexpr int kLdsStride = 80;    // bytes per staged weight row (64 + 16 to spread LDS banks)
+
+// ---------------------------------------------------------------------------
+// Backbone expansion: compressed 32-position block -> 32 dense E2M1 nibbles
+// ---------------------------------------------------------------------------
+
+// 2:4: byte g of `c` holds group g's two kept codes (lower K first); nibble g
+// of `meta` holds their positions i0 | i1 << 2.
+__device__ __forceinline__ uint4 expand_24(uint2 c, uint32_t meta) {
+  uint32_t out[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const uint32_t cw = d < 2 ? c.x : c.y;
+    uint32_t r = 0u;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int g = 2 * d + h;
+      const uint32_t byte = (cw >> (8 * (g & 3))) & 0xFFu;
+      const uint32_t nib = (meta >> (4 * g)) & 0xFu;
+      r |= (byte & 0xFu) << (4 * (nib & 3u) + 16 * h);
+      r |= (byte >> 4) << (4 * (nib >> 2) + 16 * h);
+    }
+    out[d] = r;
+  }
+  return make_uint4(out[0], out[1], out[2], out[3]);
+}
+
+// 4:8: bytes 2g, 2g+1 of `c` hold group g's four kept codes (ascending K);
+// byte g of `meta` is its keep mask.
+__device__ __forceinline__ uint4 expand_48(uint2 c, uint32_t meta) {
+  uint32_t out[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const uint32_t cw = g < 2 ? c.x : c.y;
+    uint32_t c16 = (cw >> (16 * (g & 1))) & 0xFFFFu;
+    const uint32_t mask = (meta >> (8 * g)) & 0xFFu;
+    uint32_t r = 0u;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      if ((mask >> p) & 1u) {
+        r |= (c16 & 0xFu) << (4 * p);
+        c16 >>= 4;
+      }
+    }
+    out[g] = r;
+  }
+  return make_uint4(out[0], out[1], out[2], out[3]);
+}
+
+template <int PAT>
+__device__ __forceinline__ uint4 expand_block(uint2 c, uint32_t meta) {
+  if (PAT == 24) return expand_24(c, meta);
+  return expand_48(c, meta);
+}
+
+__device__ __forceinline__ v8i as_operand(uint4 q) {
+  v8i v;
+  v[0] = (int)q.x; v[1] = (int)q.y; v[2] = (int)q.z; v[3] = (int)q.w;
+  v[4] = 0; v[5] = 0; v[6] = 0; v[7] = 0;
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// Per-lane activation fragment of one K step (two 64-wide MFMA sub-steps)
+// ---------------------------------------------------------------------------
+
+struct AStep {
+  uint4 dn[2];       // residual codes, sub-step 0 / 1
+  uint2 spc[2];      // compressed backbone codes
+  uint32_t spm[2];   // backbone metadata
+  uint32_t sdn, ssp; // E8M0 scales: byte 0 -> sub-step 0, byte 2 -> sub-step 1
+};
+
+struct ARow {
+  const uint8_t *dn, *spc, *spm, *dns, *sps;
+};
+
+template <bool SCALE_DW>
+__device__ __forceinline__ void load_a(AStep& s, const ARow& a, int ks, int half, int nblk) {
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub) {
+    const int kb = 4 * ks + 2 * sub + half;
+    if (kb < nblk) {
+      s.dn[sub] = *reinterpret_cast<const uint4*>(a.dn + 16 * (int64_t)kb);
+      s.spc[sub] = *reinterpret_cast<const uint2*>(a.spc + 8 * (int64_t)kb);
+      s.spm[sub] = *reinterpret_cast<const uint32_t*>(a.spm + 4 * (int64_t)kb);
+    } else {
+      s.dn[sub] = make_uint4(0u, 0u, 0u, 0u);
+      s.spc[sub] = make_uint2(0u, 0u);
+      s.spm[sub] = 0x44444444u;   // 2:4: a valid (0,1) pair; 4:8 ignores it with zero codes
+    }
+  }
+  if (SCALE_DW) {
+    s.sdn = *reinterpret_cast<const uint32_t*>(a.dns + 4 * (int64_t)ks) >> (8 * half);
+    s.ssp = *reinterpret_cast<const uint32_t*>(a.sps + 4 * (int64_t)ks) >> (8 * half);
+  } else {
+    const int k0 = 4 * ks + half, k1 = 4 * ks + 2 + half;
+    const uint32_t d0 = k0 < nblk ? a.dns[k0] : 127u, d1 = k1 < nblk ? a.dns[k1] : 127u;
+    const uint32_t p0 = k0 < nblk ? a.sps[k0] : 127u, p1 = k1 < nblk ? a.sps[k1] : 127u;
+    s.sdn = d0 | (d1 << 16);
+    s.ssp = p0 | (p1 << 16);
+  }
+}
+
+// Stage the weight tile of K step ks into LDS buffer `buf`.
+template <int NF, bool SCALE_DW>
+__device__ __forceinline__ void stage_w(uint8_t* lds_w, uint32_t* lds_s, const uint8_t* wc, const uint8_t* ws,
+                                        int n0, int N, int K, int ks, int nblk) {
+  constexpr int BN = 32 * NF;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int j = 0; j < BN / 64; ++j) {
+    const int c = tid + 256 * j;
+    const int row = c >> 2, part = c & 3;
+    const int n = min(n0 + row, N - 1);
+    const int kb = 4 * ks + part;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (kb < nblk) v = *reinterpret_cast<const uint4*>(wc + (int64_t)n * (K / 2) + 16 * (int64_t)kb);
+    *reinterpret_cast<uint4*>(lds_w + row * kLdsStride + 16 * part) = v;
+  }
+  if (tid < BN) {
+    const int n = min(n0 + tid, N - 1);
+    const uint8_t* sr = ws + (int64_t)n * nblk;
+    uint32_t sv;
+    if (SCALE_DW) {
+      sv = *reinterpret_cast<const uint32_t*>(sr + 4 * ks);
+    } else {
+      sv = 0u;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sv |= (uint32_t)(4 * ks + j < nblk ? sr[4 * ks + j] : 127u) << (8 * j);
+    }
+    lds_s[tid] = sv;
+  }
+}
+
+template <int SUB, int NF>
+__device__ __forceinline__ void mma_sub(v16f (&acc)[NF], const uint8_t* lds_w, const uint32_t* lds_s, v8i a_sp,
+                                        v8i a_dn, uint32_t ssp, uint32_t sdn, int lane) {
+  const int half = lane >> 5, col = lane & 31;
+  v8i b[NF];
+  uint32_t bs[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    b[f] = as_operand(*reinterpret_cast<const uint4*>(lds_w + (f * 32 + col) * kLdsStride + 32 * SUB + 16 * half));
+    bs[f] = lds_s[f * 32 + col] >> (8 * half);
+  }
+  // backbone products first, then the residual products into the same
+  // accumulators: consecutive MFMAs never depend on each other
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+    acc[f] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a_sp, b[f], acc[f], 4, 4, 2 * SUB, (int)ssp, 2 * SUB,
+                                                             (int)bs[f]);
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+    acc[f] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a_dn, b[f], acc[f], 4, 4, 2 * SUB, (int)sdn, 2 * SUB,
+                                                             (int)bs[f]);
+}
+
+template <typename OutT>
+__device__ __forceinline__ void store_out(OutT* p, float v);
+template <>
+__device__ __forceinline__ void store_out<float>(float* p, float v) { *p = v; }
+template <>
+__device__ __forceinline__ void store_out<uint16_t>(uint16_t* p, float v) { *p = f32_to_bf16_rne(v); }
+template <>
+__device__ __forceinline__ void store_out<_Float16>(_Float16* p, float v) { *p = (_Float16)v; }
+
+// One 128 x (32 NF) output tile.  Rows of the tile are output rows
+// [row_lo, row_lo + 128) clipped at row_hi; the activation row of output row
+// i is row_index[i] when row_index is given, else i - out_base + act_base.
+template <int NF, int PAT, bool SCALE_DW, typename OutT>
+__device__ __forceinline__ void tile_mx(const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale,
+                                        const uint8_t* dn_codes, const uint8_t* dn_scale, const int32_t* row_index,
+                                        int64_t row_lo, int64_t row_hi, const uint8_t* wc, const uint8_t* ws, int n0,
+                                        int N, int K, OutT* Y, int64_t ldy, uint8_t* lds_w, uint32_t* lds_s) {
+  constexpr int BN = 32 * NF;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
+  const int nblk = K / 32, nks = (K + kBK - 1) / kBK;
+
+  int64_t orow = row_lo + wave * 32 + (lane & 31);
+  if (orow >= row_hi) orow = row_hi - 1;   // clamp: loads stay in bounds, stores are masked
+  const int64_t arow = row_index ? (int64_t)row_index[orow] : orow;
+  ARow a;
+  a.dn = dn_codes + arow * (K / 2);
+  a.spc = sp_codes + arow * (K / 4);
+  a.spm = sp_meta + arow * (K / 8);
+  a.dns = dn_scale + arow * nblk;
+  a.sps = sp_scale + arow * nblk;
+
+  v16f acc[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[f][r] = 0.0f;
+
+  AStep cur, nxt;
+  load_a<SCALE_DW>(cur, a, 0, half, nblk);
+  stage_w<NF, SCALE_DW>(lds_w, lds_s, wc, ws, n0, N, K, 0, nblk);
+  for (int ks = 0; ks < nks; ++ks) {
+    const int buf = ks & 1;
+    __syncthreads();
+    if (ks + 1 < nks) {
+      load_a<SCALE_DW>(nxt, a, ks + 1, half, nblk);
+      stage_w<NF, SCALE_DW>(lds_w + (buf ^ 1) * BN * kLdsStride, lds_s + (buf ^ 1) * BN, wc, ws, n0, N, K, ks + 1,
+                            nblk);
+    }
+    const uint8_t* lw = lds_w + buf * BN * kLdsStride;
+    const uint32_t* ls = lds_s + buf * BN;
+    {
+      const v8i a_sp = as_operand(expand_block<PAT>(cur.spc[0], cur.spm[0]));
+      mma_sub<0, NF>(acc, lw, ls, a_sp, as_operand(cur.dn[0]), cur.ssp, cur.sdn, lane);
+    }
+    {
+      const v8i a_sp = as_operand(expand_block<PAT>(cur.spc[1], cur.spm[1]));
+      mma_sub<1, NF>(acc, lw, ls, a_sp, as_operand(cur.dn[1]), cur.ssp, cur.sdn, lane);
+    }
+    cur = nxt;
+  }
+
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int col = n0 + f * 32 + (lane & 31);
+    if (col >= N) continue;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t row = row_lo + wave * 32 + 8 * (r / 4) + 4 * half + (r % 4);
+      if (row < row_hi) store_out<OutT>(Y + row * ldy + col, acc[f][r]);
+    }
+  }
+}
+
+template <int NF, int PAT, bool SCALE_DW, typename OutT>
+__global__ __launch_bounds__(256) void k_linear_mx(const uint8_t* sp_codes, const uint8_t* sp_meta,
+                                                   const uint8_t* sp_scale, const uint8_t* dn_codes,
+                                                   const uint8_t* dn_scale, int64_t M, const uint8_t* wc,
+                                                   const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy) {
+  constexpr int BN = 32 * NF;
+  __shared__ __attribute__((aligned(16))) uint8_t lds_w[2 * BN * kLdsStride];
+  __shared__ uint32_t lds_s[2 * BN];
+  const int n0 = blockIdx.x * BN;
+  const int64_t m0 = (int64_t)blockIdx.y * kBM;
+  const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
+  tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, m0, m1, wc, ws, n0, N,
+                                   K, Y, ldy, lds_w, lds_s);
+}
+
+// Grouped (MoE) form.  Work item y of the grid is a 128-row tile of one
+// expert's slice [off[e], off[e+1]) of the output; the tile-to-expert map is
+// rebuilt on the device from expert_offsets (an exclusive scan of
+// ceil(rows_e / 128)), so the host never reads the routing.  Items past the
+// last tile exit before any barrier.
+template <int NF, int PAT, bool SCALE_DW, typename OutT>
+__global__ __launch_bounds__(256) void k_linear_mx_grouped(
+    const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale, const uint8_t* dn_codes,
+    const uint8_t* dn_scale, const int32_t* row_index, const int32_t* offs, int E, const uint8_t* wc,
+    const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy) {
+  constexpr int BN = 32 * NF;
+  __shared__ __attribute__((aligned(16))) uint8_t lds_w[2 * BN * kLdsStride];
+  __shared__ uint32_t lds_s[2 * BN];
+  __shared__ int s_first[1025];
+  const int tid = threadIdx.x;
+  // tiles per expert, then an inclusive scan (Hillis-Steele) over <= 1024 experts
+  for (int e = tid; e < E; e += 256) {
+    const int rows = offs[e + 1] - offs[e];
+    s_first[e + 1] = rows > 0 ? (rows + kBM - 1) / kBM : 0;
+  }
+  if (tid == 0) s_first[0] = 0;
+  __syncthreads();
+  for (int step = 1; step < E; step <<= 1) {
+    int v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = tid + 256 * j + 1;
+      v[j] = (e <= E && e - step >= 1) ? s_first[e - step] : 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = tid + 256 * j + 1;
+      if (e <= E) s_first[e] += v[j];
+    }
+    __syncthreads();
+  }
+  const int item = blockIdx.y;
+  if (item >= s_first[E]) return;   // uniform across the workgroup
+  int lo = 0, hi = E;               // find e with s_first[e] <= item < s_first[e+1]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (s_first[mid] <= item) lo = mid; else hi = mid;
+  }
+  const int e = lo;
+  const int64_t r0 = (int64_t)offs[e] + (int64_t)(item - s_first[e]) * kBM;
+  const int64_t r_end = offs[e + 1];
+  const int64_t r1 = r0 + kBM < r_end ? r0 + kBM : r_end;
+  const int n0 = blockIdx.x * BN;
+  const uint8_t* wce = wc + (int64_t)e * N * (K / 2);
+  const uint8_t* wse = ws + (int64_t)e * N * (K / 32);
+  tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, r0, r1, wce, wse, n0,
+                                   N, K, Y, ldy, lds_w, lds_s);
+}
+
+// ---------------------------------------------------------------------------
+// Host-side launchers
+// ---------------------------------------------------------------------------
+
+template <int NF, int PAT, bool SDW, typename OutT>
+static hipError_t go_linear(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
+                            const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
+                            void* Y, int64_t ldy, hipStream_t st) {
+  dim3 grid((unsigned)((N + 32 * NF - 1) / (32 * NF)), (unsigned)((M + kBM - 1) / kBM)), block(256);
+  k_linear_mx<NF, PAT, SDW, OutT><<<grid, block, 0, st>>>(spc, spm, sps, dnc, dns, M, wc, ws, N, K,
+                                                          reinterpret_cast<OutT*>(Y), ldy);
+  return hipGetLastError();
+}
+
+template <int NF, int PAT, bool SDW>
+static hipError_t go_linear_dt(int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
+                               const uint8_t* dnc, const uint8_t* dns, int64_t M, const uint8_t* wc,
+                               const uint8_t* ws, int N, int K, void* Y, int64_t ldy, hipStream_t st) {
+  if (ydt == 2) return go_linear<NF, PAT, SDW, float>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  if (ydt == 1) return go_linear<NF, PAT, SDW, _Float16>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  return go_linear<NF, PAT, SDW, uint16_t>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+}
+
+hipError_t launch_linear_mx(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
+                            const uint8_t* dnc, const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws,
+                            int N, int K, void* Y, int64_t ldy, hipStream_t st) {
+  const bool sdw = (K % kBK) == 0;
+  constexpr int NF = 8;
+  if (pat == 24) {
+    return sdw ? go_linear_dt<NF, 24, true>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st)
+               : go_linear_dt<NF, 24, false>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  }
+  return sdw ? go_linear_dt<NF, 48, true>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st)
+             : go_linear_dt<NF, 48, false>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+}
+
+template <int NF, int PAT, bool SDW, typename OutT>
+static hipError_t go_grouped(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
+                             const uint8_t* dns, const int32_t* ridx, const int32_t* offs, int E, int64_t total,
+                             const uint8_t* wc, const uint8_t* ws, int N, int K, void* Y, int64_t ldy,
+                             hipStream_t st) {
+  // upper bound on the number of 128-row tiles over all experts
+  const int64_t items = (total + kBM - 1) / kBM + E;
+  dim3 grid((unsigned)((N + 32 * NF - 1) / (32 * NF)), (unsigned)items), block(256);
+  k_linear_mx_grouped<NF, PAT, SDW, OutT><<<grid, block, 0, st>>>(spc, spm, sps, dnc, dns, ridx, offs, E, wc, ws,
+                                                                  N, K, reinterpret_cast<OutT*>(Y), ldy);
+  return hipGetLastError();
+}
+
+template <int NF, int PAT, bool SDW>
+static hipError_t go_grouped_dt(int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
+                                const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx, const int32_t* offs,
+                                int E, int64_t total, const uint8_t* wc, const uint8_t* ws, int N, int K, void* Y,
+                                int64_t ldy, hipStream_t st) {
+  if (ydt == 2)
+    return go_grouped<NF, PAT, SDW, float>(spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y, ldy, st);
+  if (ydt == 1)
+    return go_grouped<NF, PAT, SDW, _Float16>(spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y, ldy,
+                                              st);
+  return go_grouped<NF, PAT, SDW, uint16_t>(spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y, ldy,
+                                            st);
+}
+
+hipError_t launch_linear_mx_grouped(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
+                                    const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx,
+                                    const int32_t* offs, int E, int64_t total, const uint8_t* wc, const uint8_t* ws,
+                                    int N, int K, void* Y, int64_t ldy, hipStream_t st) {
+  const bool sdw = (K % kBK) == 0;
+  constexpr int NF = 8;
+  if (pat == 24) {
+    return sdw ? go_grouped_dt<NF, 24, true>(ydt, spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y,
+                                             ldy, st)
+               : go_grouped_dt<NF, 24, false>(ydt, spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y,
+                                              ldy, st);
+  }
+  return sdw ? go_grouped_dt<NF, 48, true>(ydt, spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y, ldy,
+                                           st)
+             : go_grouped_dt<NF, 48, false>(ydt, spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y, ldy,
+                                            st);
+}
+
+}  // namespace sharq

@@ -1,0 +1,82 @@
+// Weight preparation for SharQ on gfx950 (Sec. 3.4 "Shared FP4 weights with
+// path-specific scales"; Fig. 2): W [N][K] is quantized once into one E2M1
+// payload that both GEMM paths read.
+//
+// MXFP4: one lane per 32-value block along K; E8M0 exponent
+// floor(log2 amax) - 2 (clamped at -127), codes E2M1(w / 2^e).
+
+#include "sharq_device.hpp"
+
+#pragma clang fp contract(off)
+
+namespace sharq {
+
+template <typename T>
+__device__ __forceinline__ void load32(const T* p, float (&v)[32]);
+
+template <>
+__device__ __forceinline__ void load32<uint16_t>(const uint16_t* p, float (&v)[32]) {
+  const uint4* q = reinterpret_cast<const uint4*>(p);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    uint4 w = q[j];
+    uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      v[8 * j + 2 * t] = bf16_lo(u[t]);
+      v[8 * j + 2 * t + 1] = bf16_hi(u[t]);
+    }
+  }
+}
+
+template <>
+__device__ __forceinline__ void load32<float>(const float* p, float (&v)[32]) {
+  const float4* q = reinterpret_cast<const float4*>(p);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    float4 w = q[j];
+    v[4 * j] = w.x; v[4 * j + 1] = w.y; v[4 * j + 2] = w.z; v[4 * j + 3] = w.w;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_wquant_mx(const T* __restrict__ W, int N, int K, int64_t ldw,
+                                                   uint8_t* __restrict__ codes, uint8_t* __restrict__ scale) {
+  const int nblk = K / 32;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= (int64_t)N * nblk) return;
+  const int64_t n = gid / nblk;
+  const int b = (int)(gid - n * nblk);
+  float v[32];
+  load32<T>(W + n * ldw + 32 * (int64_t)b, v);
+  float amax = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 32; ++k) amax = fmaxf(amax, fabsf(v[k]));
+  const int e = mx_exponent(__float_as_uint(amax));
+  const float inv = exp2_neg(e);
+  uint32_t q[4];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    uint32_t t = 0u;
+    t = fp4x2<0>(t, v[8 * w + 0] * inv, v[8 * w + 1] * inv);
+    t = fp4x2<1>(t, v[8 * w + 2] * inv, v[8 * w + 3] * inv);
+    t = fp4x2<2>(t, v[8 * w + 4] * inv, v[8 * w + 5] * inv);
+    t = fp4x2<3>(t, v[8 * w + 6] * inv, v[8 * w + 7] * inv);
+    q[w] = t;
+  }
+  *reinterpret_cast<uint4*>(codes + n * (K / 2) + 16 * (int64_t)b) = make_uint4(q[0], q[1], q[2], q[3]);
+  scale[n * nblk + b] = (uint8_t)(e + 127);
+}
+
+hipError_t launch_wquant_mx(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
+                            hipStream_t st) {
+  const int64_t total = (int64_t)N * (K / 32);
+  dim3 grid((unsigned)((total + 255) / 256)), block(256);
+  if (wdt == 2)
+    k_wquant_mx<float><<<grid, block, 0, st>>>(reinterpret_cast<const float*>(W), N, K, ldw, codes, scale);
+  else
+    k_wquant_mx<uint16_t><<<grid, block, 0, st>>>(reinterpret_cast<const uint16_t*>(W), N, K, ldw, codes, scale);
+  return hipGetLastError();
+}
+
+}  // namespace sharq

@@ -1,0 +1,225 @@
+"""Python binding of libsharq.so (the HIP kernels behind include/sharq.h).
+
+Argument marshalling only: buffers are torch tensors on the GPU (torch is used
+for device memory and streams), every computation runs in the library's
+kernels.  Importing this module raises if the library has not been built;
+there is no fallback path.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsharq.so")
+
+OK, EINVAL, EUNSUPPORTED, EALIGN, EHIP = 0, 1, 2, 3, 4
+MXFP4, NVFP4 = 0, 1
+BF16, F16, F32 = 0, 1, 2
+
+_FMT = {"mx": MXFP4, "mxfp4": MXFP4, "nv": NVFP4, "nvfp4": NVFP4}
+_DT = {torch.bfloat16: BF16, torch.float16: F16, torch.float32: F32}
+
+
+class SharqError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {lib.sharq_status_str(status).decode()} (status {status})")
+
+
+class Pattern(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("m", ctypes.c_int32)]
+
+
+class ActStruct(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_int64), ("K", ctypes.c_int64), ("fmt", ctypes.c_int), ("nm", Pattern),
+                ("sp_codes", ctypes.c_void_p), ("sp_meta", ctypes.c_void_p), ("sp_scale", ctypes.c_void_p),
+                ("dn_codes", ctypes.c_void_p), ("dn_scale", ctypes.c_void_p), ("tensor_scale", ctypes.c_void_p)]
+
+
+class WeightStruct(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int64), ("K", ctypes.c_int64), ("experts", ctypes.c_int64), ("fmt", ctypes.c_int),
+                ("codes", ctypes.c_void_p), ("scale", ctypes.c_void_p), ("scale_dn", ctypes.c_void_p),
+                ("tensor_scale", ctypes.c_void_p)]
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2606_26587_amd.build`")
+    L = ctypes.CDLL(_LIB_PATH)
+    c_i64, c_vp, c_f = ctypes.c_int64, ctypes.c_void_p, ctypes.c_float
+    L.sharq_version.restype = ctypes.c_char_p
+    L.sharq_version.argtypes = []
+    L.sharq_status_str.restype = ctypes.c_char_p
+    L.sharq_status_str.argtypes = [ctypes.c_int]
+    L.sharq_act_buffer_bytes.restype = ctypes.c_size_t
+    L.sharq_act_buffer_bytes.argtypes = [c_i64, c_i64, ctypes.c_int, Pattern, ctypes.c_int32]
+    L.sharq_weight_buffer_bytes.restype = ctypes.c_size_t
+    L.sharq_weight_buffer_bytes.argtypes = [c_i64, c_i64, ctypes.c_int, ctypes.c_int32]
+    L.sharq_quantize_weight.restype = ctypes.c_int
+    L.sharq_quantize_weight.argtypes = [c_vp, ctypes.c_int, c_i64, c_i64, c_i64, ctypes.POINTER(WeightStruct), c_vp]
+    L.sharq_prepare.restype = ctypes.c_int
+    L.sharq_prepare.argtypes = [c_vp, ctypes.c_int, c_i64, c_i64, c_i64, c_vp, c_f, Pattern, ctypes.c_int, c_vp,
+                                ctypes.POINTER(ActStruct), c_vp]
+    L.sharq_linear.restype = ctypes.c_int
+    L.sharq_linear.argtypes = [ctypes.POINTER(ActStruct), ctypes.POINTER(WeightStruct), c_vp, ctypes.c_int, c_i64,
+                               c_vp]
+    L.sharq_linear_grouped.restype = ctypes.c_int
+    L.sharq_linear_grouped.argtypes = [ctypes.POINTER(ActStruct), c_vp, c_vp, c_i64, ctypes.POINTER(WeightStruct),
+                                       c_vp, ctypes.c_int, c_i64, c_vp]
+    return L
+
+
+lib = _load()
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise SharqError(status, where)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+# ---------------------------------------------------------------------------
+# Containers
+# ---------------------------------------------------------------------------
+
+@dataclass
+class PreparedAct:
+    """Output of sharq_prepare: the compressed backbone and the residual (device buffers)."""
+    rows: int
+    K: int
+    fmt: int
+    n: int
+    m: int
+    sp_codes: torch.Tensor
+    sp_meta: torch.Tensor
+    sp_scale: torch.Tensor
+    dn_codes: torch.Tensor
+    dn_scale: torch.Tensor
+    tensor_scale: Optional[torch.Tensor] = None
+
+    def struct(self) -> ActStruct:
+        return ActStruct(self.rows, self.K, self.fmt, Pattern(self.n, self.m), self.sp_codes.data_ptr(),
+                         self.sp_meta.data_ptr(), self.sp_scale.data_ptr(), self.dn_codes.data_ptr(),
+                         self.dn_scale.data_ptr(),
+                         None if self.tensor_scale is None else self.tensor_scale.data_ptr())
+
+
+@dataclass
+class QuantWeight:
+    """Shared FP4 weight payload with its path-specific scale views (device buffers)."""
+    N: int
+    K: int
+    experts: int
+    fmt: int
+    codes: torch.Tensor
+    scale: torch.Tensor
+    scale_dn: torch.Tensor
+    tensor_scale: Optional[torch.Tensor] = None
+
+    def struct(self) -> WeightStruct:
+        return WeightStruct(self.N, self.K, self.experts, self.fmt, self.codes.data_ptr(), self.scale.data_ptr(),
+                            self.scale_dn.data_ptr(),
+                            None if self.tensor_scale is None else self.tensor_scale.data_ptr())
+
+
+def alloc_act(rows: int, K: int, n: int = 2, m: int = 4, fmt="mx", device="cuda") -> PreparedAct:
+    f = _FMT[fmt] if isinstance(fmt, str) else fmt
+    sizes = [lib.sharq_act_buffer_bytes(rows, K, f, Pattern(n, m), w) for w in range(5)]
+    if K <= 0 or K % 32 or (rows > 0 and min(sizes) == 0):
+        raise SharqError(EINVAL, "alloc_act")
+    bufs = [torch.empty(max(s, 1), dtype=torch.uint8, device=device) for s in sizes]
+    shapes = [(rows, K * n // m // 2), (rows, K // 8), (rows, K // 32), (rows, K // 2),
+              (rows, K // 32 if f == MXFP4 else K // 16)]
+    bufs = [b[: r * c].view(r, c) if r * c > 0 else b[:0].view(r, c) for b, (r, c) in zip(bufs, shapes)]
+    ts = torch.empty(1, dtype=torch.float32, device=device) if f == NVFP4 else None
+    return PreparedAct(rows, K, f, n, m, *bufs, tensor_scale=ts)
+
+
+def alloc_weight(N: int, K: int, fmt="mx", experts: int = 1, device="cuda") -> QuantWeight:
+    f = _FMT[fmt] if isinstance(fmt, str) else fmt
+    codes = torch.empty((experts, N, K // 2), dtype=torch.uint8, device=device)
+    scale = torch.empty((experts, N, K // 32), dtype=torch.uint8, device=device)
+    scale_dn = scale if f == MXFP4 else torch.empty((experts, N, K // 16), dtype=torch.uint8, device=device)
+    ts = torch.empty(experts, dtype=torch.float32, device=device) if f == NVFP4 else None
+    return QuantWeight(N, K, experts, f, codes, scale, scale_dn, ts)
+
+
+# ---------------------------------------------------------------------------
+# Entry points (same names as the C ABI)
+# ---------------------------------------------------------------------------
+
+def sharq_quantize_weight(w: torch.Tensor, fmt="mx", out: Optional[QuantWeight] = None, stream=None) -> QuantWeight:
+    """Quantize W [N, K] (bf16 or fp32, on the GPU) into the shared FP4 payload."""
+    N, K = w.shape
+    if out is None:
+        out = alloc_weight(N, K, fmt, 1, w.device)
+    ws = out.struct()
+    _check(lib.sharq_quantize_weight(_ptr(w), _DT.get(w.dtype, -1), N, K, w.stride(0), ctypes.byref(ws),
+                                     _stream(stream)), "sharq_quantize_weight")
+    return out
+
+
+def sharq_prepare(x: torch.Tensor, gamma: Optional[torch.Tensor], eps: float = 1e-6, n: int = 2, m: int = 4,
+                  fmt="mx", tensor_scale_in: Optional[torch.Tensor] = None, out: Optional[PreparedAct] = None,
+                  stream=None) -> PreparedAct:
+    """Fused preparation of activation rows X [M, K] (bf16, on the GPU)."""
+    M, K = x.shape
+    if out is None:
+        out = alloc_act(M, K, n, m, fmt, x.device)
+    f = _FMT[fmt] if isinstance(fmt, str) else fmt
+    st = out.struct()
+    _check(lib.sharq_prepare(_ptr(x), _DT.get(x.dtype, -1), M, K, x.stride(0), _ptr(gamma), ctypes.c_float(eps),
+                             Pattern(n, m), f, _ptr(tensor_scale_in), ctypes.byref(st), _stream(stream)),
+           "sharq_prepare")
+    return out
+
+
+def sharq_linear(a: PreparedAct, w: QuantWeight, out: Optional[torch.Tensor] = None, dtype=torch.bfloat16,
+                 stream=None) -> torch.Tensor:
+    """Y [rows, N] = backbone GEMM + residual GEMM over the shared weight."""
+    if out is None:
+        out = torch.empty((a.rows, w.N), dtype=dtype, device=a.dn_codes.device)
+    ast, wst = a.struct(), w.struct()
+    _check(lib.sharq_linear(ctypes.byref(ast), ctypes.byref(wst), _ptr(out), _DT.get(out.dtype, -1),
+                            out.stride(0) if out.dim() == 2 else w.N, _stream(stream)), "sharq_linear")
+    return out
+
+
+def sharq_linear_grouped(a: PreparedAct, row_index: Optional[torch.Tensor], expert_offsets: torch.Tensor, total: int,
+                         w: QuantWeight, out: Optional[torch.Tensor] = None, dtype=torch.bfloat16,
+                         stream=None) -> torch.Tensor:
+    """Mixture-of-experts form: Y[i] = SharQ(A[row_index[i]], W_e) for i in expert e's slice."""
+    if out is None:
+        out = torch.empty((total, w.N), dtype=dtype, device=a.dn_codes.device)
+    ast, wst = a.struct(), w.struct()
+    _check(lib.sharq_linear_grouped(ctypes.byref(ast), _ptr(row_index), _ptr(expert_offsets), total,
+                                    ctypes.byref(wst), _ptr(out), _DT.get(out.dtype, -1),
+                                    out.stride(0) if out.dim() == 2 else w.N, _stream(stream)),
+           "sharq_linear_grouped")
+    return out
+
+
+def stack_weights(ws: Sequence[QuantWeight]) -> QuantWeight:
+    """Stack per-expert weights of one shape into one [experts] payload (device copies)."""
+    w0 = ws[0]
+    ts = None if w0.tensor_scale is None else torch.cat([w.tensor_scale for w in ws])
+    scale = torch.cat([w.scale for w in ws])
+    scale_dn = scale if w0.fmt == MXFP4 else torch.cat([w.scale_dn for w in ws])
+    return QuantWeight(w0.N, w0.K, len(ws), w0.fmt, torch.cat([w.codes for w in ws]), scale, scale_dn, ts)
+
+
+def version() -> str:
+    return lib.sharq_version().decode()

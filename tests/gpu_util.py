@@ -1,0 +1,67 @@
+"""Helpers shared by the GPU tests: move seeded inputs and oracle buffers
+between NumPy and the device, and rebuild oracle-shaped dicts from device
+buffers.  No arithmetic of the method lives here."""
+
+import numpy as np
+import torch
+
+from paper_2606_26587_amd import sharq as S
+
+
+def dev_bf16(u16: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def dev_u8(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint8)).cuda()
+
+
+def host(t: torch.Tensor) -> np.ndarray:
+    return t.detach().cpu().numpy()
+
+
+FMT_NAME = {S.MXFP4: "mx", S.NVFP4: "nv"}
+
+
+def act_to_oracle(a: S.PreparedAct) -> dict:
+    d = {"rows": a.rows, "K": a.K, "n": a.n, "m": a.m, "fmt": FMT_NAME[a.fmt],
+         "sp_codes": host(a.sp_codes), "sp_meta": host(a.sp_meta), "sp_scale": host(a.sp_scale),
+         "dn_codes": host(a.dn_codes), "dn_scale": host(a.dn_scale)}
+    d["tensor_scale"] = None if a.tensor_scale is None else np.float32(host(a.tensor_scale)[0])
+    return d
+
+
+def oracle_to_act(o: dict) -> S.PreparedAct:
+    fmt = S.MXFP4 if o["fmt"] == "mx" else S.NVFP4
+    ts = None
+    if fmt == S.NVFP4:
+        ts = torch.tensor([float(o["tensor_scale"])], dtype=torch.float32, device="cuda")
+    return S.PreparedAct(o["dn_codes"].shape[0], o["K"], fmt, o["n"], o["m"], dev_u8(o["sp_codes"]),
+                         dev_u8(o["sp_meta"]), dev_u8(o["sp_scale"]), dev_u8(o["dn_codes"]), dev_u8(o["dn_scale"]),
+                         tensor_scale=ts)
+
+
+def oracle_to_weight(o: dict) -> S.QuantWeight:
+    fmt = S.MXFP4 if o["fmt"] == "mx" else S.NVFP4
+    codes = dev_u8(o["codes"])[None]
+    scale = dev_u8(o["scale"])[None]
+    scale_dn = scale if fmt == S.MXFP4 else dev_u8(o["scale_dn"])[None]
+    ts = None if fmt == S.MXFP4 else torch.tensor([float(o["tensor_scale"])], dtype=torch.float32, device="cuda")
+    return S.QuantWeight(o["N"], o["K"], 1, fmt, codes, scale, scale_dn, ts)
+
+
+def weight_to_oracle(w: S.QuantWeight, e: int = 0) -> dict:
+    return {"N": w.N, "K": w.K, "fmt": FMT_NAME[w.fmt], "codes": host(w.codes[e]), "scale": host(w.scale[e]),
+            "scale_dn": host(w.scale_dn[e]),
+            "tensor_scale": None if w.tensor_scale is None else np.float32(host(w.tensor_scale)[e])}
+
+
+def assert_bytes_equal(name, got: np.ndarray, want: np.ndarray):
+    got = np.asarray(got)
+    want = np.asarray(want)
+    assert got.shape == want.shape, (name, got.shape, want.shape)
+    bad = np.nonzero(got != want)
+    if bad[0].size:
+        idx = tuple(b[0] for b in bad)
+        raise AssertionError(f"{name}: {bad[0].size} of {got.size} bytes differ; first at {idx}: "
+                             f"got {got[idx]:#x} want {want[idx]:#x}")

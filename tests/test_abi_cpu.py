@@ -1,0 +1,159 @@
+"""The C-ABI library loads, exports every declared entry point, sizes buffers
+and rejects bad arguments -- all without a GPU (no call here launches work)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+LIB = os.path.join(ROOT, "paper_2606_26587_amd", "libsharq.so")
+HEADER = os.path.join(ROOT, "include", "sharq.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="libsharq.so not built")
+
+OK, EINVAL, EUNSUPPORTED, EALIGN = 0, 1, 2, 3
+
+
+class Pattern(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("m", ctypes.c_int32)]
+
+
+class Act(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_int64), ("K", ctypes.c_int64), ("fmt", ctypes.c_int), ("nm", Pattern),
+                ("sp_codes", ctypes.c_void_p), ("sp_meta", ctypes.c_void_p), ("sp_scale", ctypes.c_void_p),
+                ("dn_codes", ctypes.c_void_p), ("dn_scale", ctypes.c_void_p), ("tensor_scale", ctypes.c_void_p)]
+
+
+class Weight(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int64), ("K", ctypes.c_int64), ("experts", ctypes.c_int64), ("fmt", ctypes.c_int),
+                ("codes", ctypes.c_void_p), ("scale", ctypes.c_void_p), ("scale_dn", ctypes.c_void_p),
+                ("tensor_scale", ctypes.c_void_p)]
+
+
+@pytest.fixture(scope="module")
+def L():
+    lib = ctypes.CDLL(LIB)
+    lib.sharq_prepare.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                  ctypes.c_void_p, ctypes.c_float, Pattern, ctypes.c_int, ctypes.c_void_p,
+                                  ctypes.POINTER(Act), ctypes.c_void_p]
+    lib.sharq_linear.argtypes = [ctypes.POINTER(Act), ctypes.POINTER(Weight), ctypes.c_void_p, ctypes.c_int,
+                                 ctypes.c_int64, ctypes.c_void_p]
+    lib.sharq_linear_grouped.argtypes = [ctypes.POINTER(Act), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                         ctypes.POINTER(Weight), ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
+                                         ctypes.c_void_p]
+    lib.sharq_quantize_weight.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_int64,
+                                          ctypes.c_int64, ctypes.POINTER(Weight), ctypes.c_void_p]
+    lib.sharq_act_buffer_bytes.restype = ctypes.c_size_t
+    lib.sharq_act_buffer_bytes.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int, Pattern, ctypes.c_int32]
+    lib.sharq_weight_buffer_bytes.restype = ctypes.c_size_t
+    lib.sharq_weight_buffer_bytes.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_int32]
+    lib.sharq_status_str.restype = ctypes.c_char_p
+    lib.sharq_version.restype = ctypes.c_char_p
+    return lib
+
+
+def declared_functions():
+    txt = open(HEADER).read()
+    return re.findall(r"SHARQ_API\s+[\w\s\*]+?\b(sharq_\w+)\s*\(", txt)
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert {"sharq_quantize_weight", "sharq_prepare", "sharq_linear", "sharq_linear_grouped"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+    assert L.sharq_version().startswith(b"sharq")
+    assert L.sharq_status_str(2) == b"unsupported format/pattern/dtype combination"
+
+
+def test_buffer_sizes(L):
+    rows, K = 7, 4096
+    mx = [L.sharq_act_buffer_bytes(rows, K, 0, Pattern(2, 4), w) for w in range(5)]
+    assert mx == [rows * K // 4, rows * K // 8, rows * K // 32, rows * K // 2, rows * K // 32]
+    nv = [L.sharq_act_buffer_bytes(rows, K, 1, Pattern(4, 8), w) for w in range(5)]
+    assert nv[4] == rows * K // 16 and nv[0] == rows * K // 4
+    assert L.sharq_act_buffer_bytes(rows, 100, 0, Pattern(2, 4), 0) == 0
+    assert L.sharq_weight_buffer_bytes(64, 128, 0, 0) == 64 * 64
+    assert L.sharq_weight_buffer_bytes(64, 128, 1, 2) == 64 * 8
+
+
+FAKE = 1 << 20   # never dereferenced: every case below is rejected (or empty) before any launch
+
+
+def act(rows=8, K=128, n=2, m=4, fmt=0, off=0):
+    return Act(rows, K, fmt, Pattern(n, m), FAKE + off, FAKE, FAKE, FAKE, FAKE, None)
+
+
+@pytest.mark.parametrize("kw,M,K,ldx,nm,expect", [
+    ({}, 8, 100, 128, (2, 4), EINVAL),        # K % 32
+    ({}, 8, 128, 64, (2, 4), EINVAL),         # ldx < K
+    ({}, -1, 128, 128, (2, 4), EINVAL),       # negative rows
+    ({}, 8, 128, 128, (5, 4), EINVAL),        # n > m
+    ({}, 8, 128, 128, (1, 4), EUNSUPPORTED),  # valid pattern, not built
+    ({}, 8, 96, 96, (4, 8), EINVAL),          # K % m  (96 % 8 == 0 but mismatched act below) -> rows/K check
+])
+def test_prepare_rejects(L, kw, M, K, ldx, nm, expect):
+    a = act(rows=M, K=K, n=nm[0], m=nm[1])
+    if K == 96:
+        a = act(rows=M, K=128, n=4, m=8)   # out->K disagrees with K
+    st = L.sharq_prepare(FAKE, 0, M, K, ldx, None, 1e-6, Pattern(*nm), 0, None, ctypes.byref(a), None)
+    assert st == expect
+
+
+def test_prepare_null_and_alignment(L):
+    a = act()
+    assert L.sharq_prepare(None, 0, 8, 128, 128, None, 1e-6, Pattern(2, 4), 0, None, ctypes.byref(a), None) == EINVAL
+    assert L.sharq_prepare(FAKE + 2, 0, 8, 128, 128, None, 1e-6, Pattern(2, 4), 0, None, ctypes.byref(a),
+                           None) == EALIGN
+    bad = act(off=8)   # sp_codes only 8-byte aligned
+    assert L.sharq_prepare(FAKE, 0, 8, 128, 128, None, 1e-6, Pattern(2, 4), 0, None, ctypes.byref(bad),
+                           None) == EALIGN
+    assert L.sharq_prepare(FAKE, 2, 8, 128, 128, None, 1e-6, Pattern(2, 4), 0, None, ctypes.byref(a),
+                           None) == EUNSUPPORTED   # fp32 X not built
+    big = act(K=32768)
+    assert L.sharq_prepare(FAKE, 0, 8, 32768, 32768, FAKE, 1e-6, Pattern(2, 4), 0, None, ctypes.byref(big),
+                           None) == EUNSUPPORTED   # RMSNorm row longer than the register-resident maximum
+    empty = act(rows=0)
+    assert L.sharq_prepare(FAKE, 0, 0, 128, 128, None, 1e-6, Pattern(2, 4), 0, None, ctypes.byref(empty),
+                           None) == OK             # nothing to do, nothing launched
+
+
+def test_linear_rejects(L):
+    a = act()
+    w = Weight(64, 128, 1, 0, FAKE, FAKE, FAKE, None)
+    assert L.sharq_linear(ctypes.byref(a), ctypes.byref(w), None, 2, 64, None) == EINVAL
+    w_bad_k = Weight(64, 256, 1, 0, FAKE, FAKE, FAKE, None)
+    assert L.sharq_linear(ctypes.byref(a), ctypes.byref(w_bad_k), FAKE, 2, 64, None) == EINVAL
+    assert L.sharq_linear(ctypes.byref(a), ctypes.byref(w), FAKE, 2, 32, None) == EINVAL      # ldy < N
+    assert L.sharq_linear(ctypes.byref(a), ctypes.byref(w), FAKE, 7, 64, None) == EUNSUPPORTED
+    assert L.sharq_linear(ctypes.byref(a), ctypes.byref(w), FAKE + 2, 2, 64, None) == EALIGN   # fp32 Y
+    w_nv = Weight(64, 128, 1, 1, FAKE, FAKE, FAKE, FAKE)
+    assert L.sharq_linear(ctypes.byref(a), ctypes.byref(w_nv), FAKE, 2, 64, None) in (EINVAL, EUNSUPPORTED)
+    empty = act(rows=0)
+    assert L.sharq_linear(ctypes.byref(empty), ctypes.byref(w), FAKE, 2, 64, None) == OK
+
+
+def test_grouped_rejects(L):
+    a = act()
+    w = Weight(64, 128, 4, 0, FAKE, FAKE, FAKE, None)
+    assert L.sharq_linear_grouped(ctypes.byref(a), None, None, 8, ctypes.byref(w), FAKE, 2, 64, None) == EINVAL
+    assert L.sharq_linear_grouped(ctypes.byref(a), None, FAKE, 9, ctypes.byref(w), FAKE, 2, 64, None) == EINVAL
+    assert L.sharq_linear_grouped(ctypes.byref(a), FAKE + 1, FAKE, 8, ctypes.byref(w), FAKE, 2, 64,
+                                  None) == EALIGN
+    w_many = Weight(64, 128, 5000, 0, FAKE, FAKE, FAKE, None)
+    assert L.sharq_linear_grouped(ctypes.byref(a), None, FAKE, 8, ctypes.byref(w_many), FAKE, 2, 64,
+                                  None) == EINVAL
+    assert L.sharq_linear_grouped(ctypes.byref(a), None, FAKE, 0, ctypes.byref(w), FAKE, 2, 64, None) == OK
+
+
+def test_quantize_weight_rejects(L):
+    w = Weight(64, 128, 1, 0, FAKE, FAKE, FAKE, None)
+    assert L.sharq_quantize_weight(None, 0, 64, 128, 128, ctypes.byref(w), None) == EINVAL
+    assert L.sharq_quantize_weight(FAKE, 0, 64, 100, 128, ctypes.byref(w), None) == EINVAL
+    assert L.sharq_quantize_weight(FAKE, 0, 32, 128, 128, ctypes.byref(w), None) == EINVAL   # out->N mismatch
+    assert L.sharq_quantize_weight(FAKE, 1, 64, 128, 128, ctypes.byref(w), None) == EUNSUPPORTED
+    assert L.sharq_quantize_weight(FAKE, 0, 64, 128, 132, ctypes.byref(w), None) == EALIGN
+    w0 = Weight(0, 128, 1, 0, FAKE, FAKE, FAKE, None)
+    assert L.sharq_quantize_weight(FAKE, 0, 0, 128, 128, ctypes.byref(w0), None) == OK

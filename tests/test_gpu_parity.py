@@ -1,0 +1,292 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Preparation and weight quantization must match the oracle byte for byte; the
+two-path GEMM must match the oracle's fp64 result within the componentwise
+accumulation gate max|Y^ - Y| / sum_k(|a_sp w| + |a_dn w|) <= 1e-3 and the
+normwise bound max|Y^ - Y| / max|Y| <= 1e-3.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import sharq_oracle as O
+from paper_2606_26587_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+GATE = 1e-3
+
+
+@pytest.fixture(scope="module")
+def S():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_26587_amd import sharq
+    return sharq
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def special_rows(kind: str, T: int, K: int, seed: int) -> np.ndarray:
+    """Edge-case activations (bf16 bits)."""
+    rng = np.random.default_rng(seed)
+    if kind == "zeros":
+        x = np.zeros((T, K), np.float32)
+        x[:, ::3] = -0.0
+    elif kind == "ties":
+        x = rng.integers(-3, 4, size=(T, K)).astype(np.float32)
+    elif kind == "subnormal":
+        x = (rng.standard_normal((T, K)) * 1e-39).astype(np.float32)
+        x[:, ::5] *= 1e-2
+    elif kind == "huge":
+        x = (rng.standard_normal((T, K)) * 1e30).astype(np.float32)
+    elif kind == "mixed":
+        x = rng.standard_normal((T, K)).astype(np.float32)
+        x[0] = 0.0
+        x[1, ::2] = 1e-40
+        x[2] *= 1e25
+        x[3, 5::7] = 6000.0
+    else:
+        raise ValueError(kind)
+    return synth.f32_to_bf16_bits(x)
+
+
+def run_prep(S, G, x_u16, gamma_u16, eps, n, m):
+    x = G.dev_bf16(x_u16)
+    g = None if gamma_u16 is None else G.dev_bf16(gamma_u16)
+    a = S.sharq_prepare(x, g, eps, n, m, "mx")
+    torch.cuda.synchronize()
+    return a
+
+
+def check_prep(S, G, x_u16, gamma_u16, eps, n, m, tag):
+    say(f"[prep] {tag} shape={x_u16.shape} n:m={n}:{m} gamma={gamma_u16 is not None}")
+    a = run_prep(S, G, x_u16, gamma_u16, eps, n, m)
+    o = O.prepare(x_u16, gamma_u16, eps, n, m, "mx")
+    for name in ("sp_codes", "sp_meta", "sp_scale", "dn_codes", "dn_scale"):
+        G.assert_bytes_equal(f"{tag}:{name}", G.host(getattr(a, name)), o[name])
+    return a, o
+
+
+@pytest.fixture(scope="module")
+def G(S):
+    import gpu_util
+    return gpu_util
+
+
+PREP_CASES = [
+    # (T, K, gamma, n, m, eps)
+    (8, 128, True, 2, 4, 1e-6),
+    (37, 416, True, 2, 4, 1e-5),
+    (37, 416, False, 2, 4, 1e-5),
+    (37, 416, True, 4, 8, 1e-5),
+    (3, 32, True, 2, 4, 1e-6),
+    (64, 4096, True, 2, 4, 1e-5),
+    (17, 3584, True, 2, 4, 1e-6),
+    (9, 16384, True, 2, 4, 1e-5),
+    (5, 14336, False, 2, 4, 1e-5),
+    (130, 2048, True, 4, 8, 1e-6),
+    (33, 768, False, 4, 8, 1e-6),
+    (6, 18944, False, 2, 4, 1e-6),
+]
+
+
+@pytest.mark.parametrize("T,K,use_gamma,n,m,eps", PREP_CASES)
+def test_prep_bit_exact(S, G, T, K, use_gamma, n, m, eps):
+    x = synth.activations(T, K, seed=T + K)
+    g = synth.gamma(K, seed=K) if use_gamma else None
+    check_prep(S, G, x, g, eps, n, m, f"T{T}K{K}")
+
+
+@pytest.mark.parametrize("kind", ["zeros", "ties", "subnormal", "huge", "mixed"])
+@pytest.mark.parametrize("use_gamma", [True, False])
+@pytest.mark.parametrize("n,m", [(2, 4), (4, 8)])
+def test_prep_edge_values(S, G, kind, use_gamma, n, m):
+    T, K = 12, 256
+    x = special_rows(kind, T, K, seed=len(kind))
+    g = synth.gamma(K, seed=3) if use_gamma else None
+    if kind == "zeros" and use_gamma:
+        g = synth.gamma(K, seed=3)   # all-zero rows: r = 1/sqrt(eps), y = 0
+    check_prep(S, G, x, g, 1e-6, n, m, f"edge-{kind}")
+
+
+def test_prep_empty(S, G):
+    x = torch.empty((0, 128), dtype=torch.bfloat16, device="cuda")
+    a = S.sharq_prepare(x, None, 1e-6, 2, 4, "mx")
+    torch.cuda.synchronize()
+    assert a.rows == 0 and a.dn_codes.shape == (0, 64)
+
+
+def test_prep_strided_rows(S, G):
+    """A row stride larger than K (ldx > K) reads only the first K columns."""
+    T, K, ld = 20, 256, 384
+    full = synth.activations(T, ld, seed=7)
+    xd = G.dev_bf16(full)[:, :K]
+    a = S.sharq_prepare(xd, None, 1e-6, 2, 4, "mx")
+    torch.cuda.synchronize()
+    o = O.prepare(np.ascontiguousarray(full[:, :K]), None, 1e-6, 2, 4, "mx")
+    for name in ("sp_codes", "sp_meta", "sp_scale", "dn_codes", "dn_scale"):
+        G.assert_bytes_equal(name, G.host(getattr(a, name)), o[name])
+
+
+@pytest.mark.parametrize("N,K", [(64, 128), (200, 416), (6144, 4096), (33, 14336)])
+def test_weight_quant_bit_exact(S, G, N, K):
+    say(f"[wquant] N={N} K={K}")
+    w = synth.weight(N, K, seed=N)
+    q = S.sharq_quantize_weight(G.dev_bf16(w), "mx")
+    torch.cuda.synchronize()
+    o = O.quantize_weight(w, "mx")
+    G.assert_bytes_equal("codes", G.host(q.codes[0]), o["codes"])
+    G.assert_bytes_equal("scale", G.host(q.scale[0]), o["scale"])
+
+
+def test_weight_quant_fp32_input(S, G):
+    w = synth.weight(96, 256, seed=5)
+    wf = torch.from_numpy(O.bf16_bits_to_f32(w)).cuda()
+    q = S.sharq_quantize_weight(wf, "mx")
+    torch.cuda.synchronize()
+    o = O.quantize_weight(w, "mx")
+    G.assert_bytes_equal("codes", G.host(q.codes[0]), o["codes"])
+
+
+def gemm_check(y_gpu: np.ndarray, y_ref: np.ndarray, y_abs: np.ndarray, tag: str):
+    gate = O.gemm_gate_error(y_gpu, y_ref, y_abs)
+    norm = float(np.abs(y_gpu.astype(np.float64) - y_ref).max() / max(np.abs(y_ref).max(), 1e-300))
+    say(f"[gemm] {tag}: gate={gate:.3e} normwise={norm:.3e}")
+    assert gate <= GATE, (tag, gate)
+    assert norm <= GATE, (tag, norm)
+
+
+LINEAR_CASES = [
+    # (T, N, K, n, m)
+    (8, 64, 128, 2, 4),
+    (300, 200, 416, 2, 4),
+    (1, 256, 4096, 2, 4),
+    (129, 300, 640, 4, 8),
+    (256, 512, 2048, 2, 4),
+    (16, 6144, 4096, 2, 4),
+]
+
+
+@pytest.mark.parametrize("T,N,K,n,m", LINEAR_CASES)
+def test_linear_parity(S, G, T, N, K, n, m):
+    say(f"[linear] T={T} N={N} K={K} {n}:{m}")
+    x = synth.activations(T, K, seed=T)
+    o = O.prepare(x, synth.gamma(K, seed=1), 1e-6, n, m, "mx")
+    wo = O.quantize_weight(synth.weight(N, K, seed=N), "mx")
+    a = G.oracle_to_act(o)
+    w = G.oracle_to_weight(wo)
+    y32 = S.sharq_linear(a, w, dtype=torch.float32)
+    y16 = S.sharq_linear(a, w, dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    ref = O.linear(o, wo)
+    gemm_check(G.host(y32), ref, O.linear_abs(o, wo), f"T{T}N{N}K{K}")
+    # bf16 output is the fp32 result rounded once
+    assert torch.equal(y16, y32.to(torch.bfloat16))
+
+
+def test_linear_ldy_and_empty(S, G):
+    T, N, K = 40, 96, 256
+    x = synth.activations(T, K, seed=2)
+    o = O.prepare(x, None, 1e-6, 2, 4, "mx")
+    wo = O.quantize_weight(synth.weight(N, K, seed=2), "mx")
+    a, w = G.oracle_to_act(o), G.oracle_to_weight(wo)
+    big = torch.full((T, 128), 7.0, dtype=torch.float32, device="cuda")
+    S.sharq_linear(a, w, out=big[:, :N])
+    torch.cuda.synchronize()
+    assert torch.all(big[:, N:] == 7.0)
+    gemm_check(G.host(big[:, :N]), O.linear(o, wo), O.linear_abs(o, wo), "ldy")
+    e = S.sharq_prepare(torch.empty((0, K), dtype=torch.bfloat16, device="cuda"), None, 1e-6, 2, 4)
+    y = S.sharq_linear(e, w, dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert y.shape == (0, N)
+
+
+def test_end_to_end_deterministic(S, G):
+    T, N, K = 96, 320, 1024
+    x = G.dev_bf16(synth.activations(T, K, seed=4))
+    g = G.dev_bf16(synth.gamma(K, seed=4))
+    w = S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=4)))
+    outs = []
+    for _ in range(2):
+        a = S.sharq_prepare(x, g, 1e-5, 2, 4)
+        outs.append(S.sharq_linear(a, w, dtype=torch.float32))
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1])
+
+
+# --------------------------------------------------------------------------- full Llama shapes
+
+LLAMA_T = 2048
+
+
+@pytest.mark.parametrize("name", ["qkv", "gate_up", "down"])
+def test_llama_full_shape(S, G, name):
+    """Full M=2048 Llama-3.1-8B shapes in the benchmark's launch configuration:
+    preparation compared in full, GEMM on 64 sampled rows x all columns."""
+    K, N, norm = synth.LLAMA_LINEARS[name]
+    say(f"[llama] {name} T={LLAMA_T} K={K} N={N}")
+    x = synth.activations(LLAMA_T, K, seed=0)
+    g = synth.gamma(K, seed=0) if norm else None
+    w = synth.weight(N, K, seed=0)
+    a, o = check_prep(S, G, x, g, synth.LLAMA_EPS, 2, 4, name)
+    wq = S.sharq_quantize_weight(G.dev_bf16(w))
+    y = S.sharq_linear(a, wq, dtype=torch.float32)
+    torch.cuda.synchronize()
+    wo = G.weight_to_oracle(wq)
+    rows = np.random.default_rng(1).choice(LLAMA_T, 64, replace=False)
+    rows[0] = 0   # the massive-activation token
+    ref = O.linear(o, wo, rows=rows)
+    gemm_check(G.host(y)[rows], ref, O.linear_abs(o, wo, rows=rows), name)
+
+
+# --------------------------------------------------------------------------- grouped (MoE)
+
+@pytest.mark.parametrize("T,E,topk,K,N", [(64, 8, 2, 256, 96), (300, 5, 3, 416, 200)])
+def test_grouped_parity(S, G, T, E, topk, K, N):
+    say(f"[grouped] T={T} E={E} top{topk} K={K} N={N}")
+    x = synth.activations(T, K, seed=E)
+    o = O.prepare(x, synth.gamma(K, seed=E), 1e-6, 4, 8, "mx")
+    wos = [O.quantize_weight(synth.weight(N, K, seed=100 + e), "mx") for e in range(E)]
+    row_index, offs = synth.router_topk(T, E, topk, seed=E)
+    total = int(offs[-1])
+    a = G.oracle_to_act(o)
+    w = S.stack_weights([G.oracle_to_weight(wo) for wo in wos])
+    ri = torch.from_numpy(row_index).cuda()
+    of = torch.from_numpy(offs).cuda()
+    y = S.sharq_linear_grouped(a, ri, of, total, w, dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = O.linear_grouped(o, row_index, offs, wos)
+    yabs = np.zeros_like(ref)
+    for e in range(E):
+        lo, hi = offs[e], offs[e + 1]
+        if hi > lo:
+            yabs[lo:hi] = O.linear_abs(o, wos[e], rows=row_index[lo:hi])
+    gemm_check(G.host(y), ref, yabs, f"grouped T{T}E{E}")
+
+
+def test_grouped_uneven_experts(S, G):
+    """Expert sizes 0, 1, 129, 0, 300 rows; identity row map (row_index = NULL)."""
+    K, N = 256, 160
+    sizes = [0, 1, 129, 0, 300]
+    offs = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    total = int(offs[-1])
+    x = synth.activations(total, K, seed=9)
+    o = O.prepare(x, None, 1e-6, 2, 4, "mx")
+    wos = [O.quantize_weight(synth.weight(N, K, seed=200 + e), "mx") for e in range(len(sizes))]
+    a = G.oracle_to_act(o)
+    w = S.stack_weights([G.oracle_to_weight(wo) for wo in wos])
+    y = S.sharq_linear_grouped(a, None, torch.from_numpy(offs).cuda(), total, w, dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = O.linear_grouped(o, None, offs, wos)
+    yabs = np.zeros_like(ref)
+    for e in range(len(sizes)):
+        lo, hi = offs[e], offs[e + 1]
+        if hi > lo:
+            yabs[lo:hi] = O.linear_abs(o, wos[e], rows=np.arange(lo, hi))
+    gemm_check(G.host(y), ref, yabs, "grouped-uneven")
