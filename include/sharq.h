@@ -31,7 +31,19 @@
  *          per block + one fp32 per-tensor scale.
  *   Two 4-bit codes per byte, the element with the lower K index in the low
  *   nibble.
+ *
+ * Buffer layout: PANEL-MAJOR.  Every buffer below holds a fixed number of
+ * bytes per 32 consecutive K positions of a row (its "row bytes").  K is cut
+ * into panels of SHARQ_PANEL_K = 128 positions (the last panel is narrower
+ * when K % 128 != 0); panel p stores the row bytes of ALL rows of the tensor
+ * for K range [128 p, 128 p + width_p), row after row, and panels follow each
+ * other.  Byte offset of (panel p, row r) in a buffer with b bytes per 32 K
+ * positions and R rows: p * R * 4 b + r * (width_p / 32) * b.  A tile of
+ * consecutive rows is thus one contiguous run per panel, which is how the
+ * GEMM streams it; a single row is still addressable (row gathers).  The
+ * total size equals the row-major size R * (K / 32) * b.
  */
+#define SHARQ_PANEL_K 128
 #ifndef SHARQ_H
 #define SHARQ_H
 
@@ -66,7 +78,8 @@ typedef struct {
 
 /*
  * A prepared activation: the output of sharq_prepare, the input of
- * sharq_linear / sharq_linear_grouped.  Row-major, one row per token.
+ * sharq_linear / sharq_linear_grouped.  One row per token; panel-major (see
+ * above).  Row bytes per row are listed as [rows][...].
  *
  *   sp_codes [rows][K*n/m/2]  backbone E2M1 codes of the kept positions only,
  *                             in ascending K order (Sec. 3.4: "quantizes and
@@ -100,7 +113,8 @@ typedef struct {
 /*
  * A quantized weight: ONE shared FP4 payload for both paths with
  * path-specific scale views (Sec. 3.4 "Shared FP4 weights with path-specific
- * scales"; Fig. 2).  W is [N][K] (out-features x in-features), Y = X W^T.
+ * scales"; Fig. 2).  W is [N][K] (out-features x in-features), Y = X W^T;
+ * each expert's buffers are panel-major over its N rows.
  * `experts` weights of identical shape may be stacked back to back (MoE);
  * expert e starts at codes + e*N*K/2 and scale + e*N*(K/32).
  *

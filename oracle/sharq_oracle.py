@@ -384,6 +384,76 @@ def unpack_backbone(sp_codes: np.ndarray, sp_meta: np.ndarray, K: int, n: int, m
 
 
 # ---------------------------------------------------------------------------
+# Panel-major buffer layout of the library (data movement only)
+# ---------------------------------------------------------------------------
+
+PANEL_K = 128
+
+
+def to_panels(rowmajor: np.ndarray, K: int) -> np.ndarray:
+    """Row-major [R, bytes(K)] -> flat panel-major bytes.
+
+    Every buffer holds a fixed number of bytes per 32 K positions, so K splits
+    into panels of 128 positions (the last one may be narrower); panel p stores
+    the bytes of all R rows for its K range, row after row, and panels follow
+    each other.
+    """
+    a = np.asarray(rowmajor, dtype=np.uint8)
+    R, B = a.shape
+    per32 = B // (K // 32)
+    parts = []
+    for lo in range(0, K, PANEL_K):
+        hi = min(lo + PANEL_K, K)
+        parts.append(a[:, lo // 32 * per32: hi // 32 * per32].reshape(-1))
+    return np.concatenate(parts) if parts else np.zeros(0, np.uint8)
+
+
+def from_panels(flat: np.ndarray, R: int, K: int, bytes_per_row: int) -> np.ndarray:
+    """Inverse of to_panels: flat panel-major bytes -> row-major [R, bytes_per_row]."""
+    flat = np.asarray(flat, dtype=np.uint8).reshape(-1)
+    per32 = bytes_per_row // (K // 32)
+    out = np.zeros((R, bytes_per_row), dtype=np.uint8)
+    off = 0
+    for lo in range(0, K, PANEL_K):
+        hi = min(lo + PANEL_K, K)
+        w = (hi - lo) // 32 * per32
+        out[:, lo // 32 * per32: hi // 32 * per32] = flat[off: off + R * w].reshape(R, w)
+        off += R * w
+    return out
+
+
+ACT_BUFFERS = ("sp_codes", "sp_meta", "sp_scale", "dn_codes", "dn_scale")
+WEIGHT_BUFFERS = ("codes", "scale", "scale_dn")
+
+
+def act_to_device_layout(act: dict) -> dict:
+    """The prepared-activation buffers in the library's panel-major layout."""
+    return {k: to_panels(act[k], act["K"]) for k in ACT_BUFFERS}
+
+
+def act_from_device_layout(bufs: dict, rows: int, K: int, n: int, m: int, fmt: str, tensor_scale=None) -> dict:
+    """Panel-major device buffers -> the row-major dict the oracle's GEMM reads."""
+    widths = {"sp_codes": K * n // m // 2, "sp_meta": K // 8, "sp_scale": K // 32, "dn_codes": K // 2,
+              "dn_scale": K // 32 if fmt == "mx" else K // 16}
+    d = {"rows": rows, "K": K, "n": n, "m": m, "fmt": fmt, "tensor_scale": tensor_scale}
+    for k in ACT_BUFFERS:
+        d[k] = from_panels(bufs[k], rows, K, widths[k])
+    return d
+
+
+def weight_to_device_layout(wq: dict) -> dict:
+    return {k: to_panels(wq[k], wq["K"]) for k in WEIGHT_BUFFERS}
+
+
+def weight_from_device_layout(bufs: dict, N: int, K: int, fmt: str, tensor_scale=None) -> dict:
+    widths = {"codes": K // 2, "scale": K // 32, "scale_dn": K // 32 if fmt == "mx" else K // 16}
+    d = {"N": N, "K": K, "fmt": fmt, "tensor_scale": tensor_scale}
+    for k in WEIGHT_BUFFERS:
+        d[k] = from_panels(bufs[k], N, K, widths[k])
+    return d
+
+
+# ---------------------------------------------------------------------------
 # Preparation (Sec. 3.3 eqs. sharq-sparse-backbone / quantized-backbone / residual)
 # ---------------------------------------------------------------------------
 

@@ -100,92 +100,178 @@ struct AStep {
   uint4 dn[2];       // residual codes, sub-step 0 / 1
   uint2 spc[2];      // compressed backbone codes
   uint32_t spm[2];   // backbone metadata
-  uint32_t sdn, ssp; // E8M0 scales: byte 0 -> sub-step 0, byte 2 -> sub-step 1
+  uint32_t sdn, ssp; // E8M0 scales of the step's 4 blocks (byte j = block 4 ks + j)
 };
 
+// Activation rows live in panel-major buffers: K is cut into panels of 128
+// positions (one K step; the last panel may be narrower) and panel p stores
+// all R rows' bytes for its K range back to back, so the 32 rows of a
+// wavefront are 2 KB (codes), 1 KB (backbone), 512 B (metadata) and 128 B
+// (scales) of contiguous memory per step.
 struct ARow {
-  const uint8_t *dn, *spc, *spm, *dns, *sps;
+  const uint8_t *dn, *spc, *spm, *dns, *sps;   // buffer bases
+  int64_t r, R;                                // this lane's activation row, rows in the buffers
 };
 
 template <bool SCALE_DW>
-__device__ __forceinline__ void load_a(AStep& s, const ARow& a, int ks, int half, int nblk) {
+__device__ __forceinline__ void load_a(AStep& s, const ARow& a, int ks, int half, int nblk, int K) {
+  // SCALE_DW: K is a multiple of 128, every panel is full and every block exists
+  const int wp = SCALE_DW ? 128 : min(128, K - 128 * ks);
+  const int64_t pr = (int64_t)ks * a.R;
+  const uint8_t* dn = a.dn + pr * 64 + a.r * (wp / 2);
+  const uint8_t* spc = a.spc + pr * 32 + a.r * (wp / 4);
+  const uint8_t* spm = a.spm + pr * 16 + a.r * (wp / 8);
 #pragma unroll
   for (int sub = 0; sub < 2; ++sub) {
-    const int kb = 4 * ks + 2 * sub + half;
-    if (kb < nblk) {
-      s.dn[sub] = *reinterpret_cast<const uint4*>(a.dn + 16 * (int64_t)kb);
-      s.spc[sub] = *reinterpret_cast<const uint2*>(a.spc + 8 * (int64_t)kb);
-      s.spm[sub] = *reinterpret_cast<const uint32_t*>(a.spm + 4 * (int64_t)kb);
+    const int j = 2 * sub + half;   // block within the panel
+    if (SCALE_DW || 4 * ks + j < nblk) {
+      s.dn[sub] = *reinterpret_cast<const uint4*>(dn + 16 * j);
+      s.spc[sub] = *reinterpret_cast<const uint2*>(spc + 8 * j);
+      s.spm[sub] = *reinterpret_cast<const uint32_t*>(spm + 4 * j);
     } else {
       s.dn[sub] = make_uint4(0u, 0u, 0u, 0u);
       s.spc[sub] = make_uint2(0u, 0u);
       s.spm[sub] = 0x44444444u;   // 2:4: a valid (0,1) pair; 4:8 ignores it with zero codes
     }
   }
+  const uint8_t* dns = a.dns + pr * 4 + a.r * (wp / 32);
+  const uint8_t* sps = a.sps + pr * 4 + a.r * (wp / 32);
   if (SCALE_DW) {
-    s.sdn = *reinterpret_cast<const uint32_t*>(a.dns + 4 * (int64_t)ks) >> (8 * half);
-    s.ssp = *reinterpret_cast<const uint32_t*>(a.sps + 4 * (int64_t)ks) >> (8 * half);
+    // raw dwords: the per-lane byte shift is applied at the point of use so
+    // that no instruction waits on these loads before the MFMAs need them
+    s.sdn = *reinterpret_cast<const uint32_t*>(dns);
+    s.ssp = *reinterpret_cast<const uint32_t*>(sps);
   } else {
-    const int k0 = 4 * ks + half, k1 = 4 * ks + 2 + half;
-    const uint32_t d0 = k0 < nblk ? a.dns[k0] : 127u, d1 = k1 < nblk ? a.dns[k1] : 127u;
-    const uint32_t p0 = k0 < nblk ? a.sps[k0] : 127u, p1 = k1 < nblk ? a.sps[k1] : 127u;
-    s.sdn = d0 | (d1 << 16);
-    s.ssp = p0 | (p1 << 16);
+    // same byte order as the dword form: byte j = block 4 ks + j (127 past K)
+    s.sdn = 0u;
+    s.ssp = 0u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool ok = 4 * ks + j < nblk;
+      s.sdn |= (uint32_t)(ok ? dns[j] : 127u) << (8 * j);
+      s.ssp |= (uint32_t)(ok ? sps[j] : 127u) << (8 * j);
+    }
   }
 }
 
-// Stage the weight tile of K step ks into LDS buffer `buf`.
+// The weight tile of one K step held in registers between its global load and
+// its LDS store: BN rows x 64 bytes of codes (16 bytes per thread and chunk)
+// plus one dword of four E8M0 scales per row.
+template <int NF>
+struct WStep {
+  uint4 q[NF / 2];
+  uint32_t s;
+};
+
 template <int NF, bool SCALE_DW>
-__device__ __forceinline__ void stage_w(uint8_t* lds_w, uint32_t* lds_s, const uint8_t* wc, const uint8_t* ws,
-                                        int n0, int N, int K, int ks, int nblk) {
+__device__ __forceinline__ void load_w(WStep<NF>& w, const uint8_t* wc, const uint8_t* ws, int n0, int N, int K,
+                                       int ks, int nblk) {
+  // panel-major weight: panel ks holds all N rows' 64 bytes (or fewer for a
+  // narrow last panel), so a full tile of BN rows is one contiguous run
+  constexpr int BN = 32 * NF;
+  const int tid = threadIdx.x;
+  const int wp = SCALE_DW ? 128 : min(128, K - 128 * ks);
+  const int64_t pn = (int64_t)ks * N;
+#pragma unroll
+  for (int j = 0; j < BN / 64; ++j) {
+    const int c = tid + 256 * j;
+    const int row = c >> 2, part = c & 3;
+    const int n = min(n0 + row, N - 1);
+    w.q[j] = (SCALE_DW || 4 * ks + part < nblk)
+                 ? *reinterpret_cast<const uint4*>(wc + pn * 64 + (int64_t)n * (wp / 2) + 16 * part)
+                 : make_uint4(0u, 0u, 0u, 0u);
+  }
+  w.s = 0u;
+  if (BN >= 256 || tid < BN) {
+    const int n = min(n0 + tid, N - 1);
+    const uint8_t* sr = ws + pn * 4 + (int64_t)n * (wp / 32);
+    if (SCALE_DW) {
+      w.s = *reinterpret_cast<const uint32_t*>(sr);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w.s |= (uint32_t)(4 * ks + j < nblk ? sr[j] : 127u) << (8 * j);
+    }
+  }
+}
+
+// Weight scales in LDS are laid out per (column, lane half): lane (col, h)
+// finds, at byte 2f + sub of its 2 NF-byte record, the E8M0 scale of weight row
+// f*32 + col for block 4 ks + 2 sub + h -- exactly the byte its MFMA for
+// fragment f, sub-step sub needs -- so one LDS read fetches all of them and
+// op_sel selects the byte.
+template <int NF>
+__device__ __forceinline__ void store_w(const WStep<NF>& w, uint8_t* lds_w, uint8_t* lds_s) {
   constexpr int BN = 32 * NF;
   const int tid = threadIdx.x;
 #pragma unroll
   for (int j = 0; j < BN / 64; ++j) {
     const int c = tid + 256 * j;
     const int row = c >> 2, part = c & 3;
-    const int n = min(n0 + row, N - 1);
-    const int kb = 4 * ks + part;
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (kb < nblk) v = *reinterpret_cast<const uint4*>(wc + (int64_t)n * (K / 2) + 16 * (int64_t)kb);
-    *reinterpret_cast<uint4*>(lds_w + row * kLdsStride + 16 * part) = v;
+    *reinterpret_cast<uint4*>(lds_w + row * kLdsStride + 16 * part) = w.q[j];
   }
-  if (tid < BN) {
-    const int n = min(n0 + tid, N - 1);
-    const uint8_t* sr = ws + (int64_t)n * nblk;
-    uint32_t sv;
-    if (SCALE_DW) {
-      sv = *reinterpret_cast<const uint32_t*>(sr + 4 * ks);
-    } else {
-      sv = 0u;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) sv |= (uint32_t)(4 * ks + j < nblk ? sr[4 * ks + j] : 127u) << (8 * j);
-    }
-    lds_s[tid] = sv;
+  if (BN >= 256 || tid < BN) {
+    const int f = tid >> 5, col = tid & 31;
+    // blocks 0 and 2 of the step go to half 0, blocks 1 and 3 to half 1
+    const uint32_t h0 = __builtin_amdgcn_perm(0u, w.s, 0x0c0c0200u);   // b0 | b2 << 8
+    const uint32_t h1 = __builtin_amdgcn_perm(0u, w.s, 0x0c0c0301u);   // b1 | b3 << 8
+    *reinterpret_cast<uint16_t*>(lds_s + (2 * col + 0) * (2 * NF) + 2 * f) = (uint16_t)h0;
+    *reinterpret_cast<uint16_t*>(lds_s + (2 * col + 1) * (2 * NF) + 2 * f) = (uint16_t)h1;
   }
 }
 
+template <int SA, int SB>
+__device__ __forceinline__ v16f mfma_fp4(v8i a, v8i b, v16f c, uint32_t sa, uint32_t sb) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 4, 4, SA, (int)sa, SB, (int)sb);
+}
+
 template <int SUB, int NF>
-__device__ __forceinline__ void mma_sub(v16f (&acc)[NF], const uint8_t* lds_w, const uint32_t* lds_s, v8i a_sp,
-                                        v8i a_dn, uint32_t ssp, uint32_t sdn, int lane) {
+__device__ __forceinline__ void mma_sub(v16f (&acc)[NF], const uint8_t* lds_w, const uint32_t (&bw)[NF / 2],
+                                        v8i a_sp, v8i a_dn, uint32_t ssp, uint32_t sdn, int lane) {
   const int half = lane >> 5, col = lane & 31;
   v8i b[NF];
-  uint32_t bs[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+    b[f] = as_operand(*reinterpret_cast<const uint4*>(lds_w + (f * 32 + col) * kLdsStride + 32 * SUB + 16 * half));
+  // backbone products first, then the residual products into the same
+  // accumulators: consecutive MFMAs never depend on each other.  The weight
+  // scale of fragment f is byte 2 (f & 1) + SUB of word f / 2.
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
-    b[f] = as_operand(*reinterpret_cast<const uint4*>(lds_w + (f * 32 + col) * kLdsStride + 32 * SUB + 16 * half));
-    bs[f] = lds_s[f * 32 + col] >> (8 * half);
+    if (f & 1) acc[f] = mfma_fp4<2 * SUB, 2 + SUB>(a_sp, b[f], acc[f], ssp, bw[f >> 1]);
+    else       acc[f] = mfma_fp4<2 * SUB, SUB>(a_sp, b[f], acc[f], ssp, bw[f >> 1]);
   }
-  // backbone products first, then the residual products into the same
-  // accumulators: consecutive MFMAs never depend on each other
 #pragma unroll
-  for (int f = 0; f < NF; ++f)
-    acc[f] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a_sp, b[f], acc[f], 4, 4, 2 * SUB, (int)ssp, 2 * SUB,
-                                                             (int)bs[f]);
-#pragma unroll
-  for (int f = 0; f < NF; ++f)
-    acc[f] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a_dn, b[f], acc[f], 4, 4, 2 * SUB, (int)sdn, 2 * SUB,
-                                                             (int)bs[f]);
+  for (int f = 0; f < NF; ++f) {
+    if (f & 1) acc[f] = mfma_fp4<2 * SUB, 2 + SUB>(a_dn, b[f], acc[f], sdn, bw[f >> 1]);
+    else       acc[f] = mfma_fp4<2 * SUB, SUB>(a_dn, b[f], acc[f], sdn, bw[f >> 1]);
+  }
+}
+
+// One K step: expand the backbone of both sub-steps, then 2 x NF backbone and
+// 2 x NF residual MFMAs against the staged weight tile.
+template <int NF, int PAT>
+__device__ __forceinline__ void step_mx(v16f (&acc)[NF], const AStep& cur, const uint8_t* lw, const uint8_t* ls,
+                                        int lane) {
+  static_assert(NF == 8 || NF == 4, "scale record is read as 16 or 8 bytes");
+  const int half = lane >> 5, col = lane & 31;
+  uint32_t bw[NF / 2];
+  if (NF == 8) {
+    const uint4 q = *reinterpret_cast<const uint4*>(ls + (2 * col + half) * (2 * NF));
+    bw[0] = q.x; bw[1] = q.y; bw[NF / 2 > 2 ? 2 : 0] = q.z; bw[NF / 2 > 3 ? 3 : 0] = q.w;
+  } else {
+    const uint2 q = *reinterpret_cast<const uint2*>(ls + (2 * col + half) * (2 * NF));
+    bw[0] = q.x; bw[NF / 2 > 1 ? 1 : 0] = q.y;
+  }
+  // op_sel 0 / 2 then picks block 4 ks + half (sub-step 0) / 4 ks + 2 + half (sub-step 1)
+  const uint32_t ssp = cur.ssp >> (8 * half), sdn = cur.sdn >> (8 * half);
+  {
+    const v8i a_sp = as_operand(expand_block<PAT>(cur.spc[0], cur.spm[0]));
+    mma_sub<0, NF>(acc, lw, bw, a_sp, as_operand(cur.dn[0]), ssp, sdn, lane);
+  }
+  {
+    const v8i a_sp = as_operand(expand_block<PAT>(cur.spc[1], cur.spm[1]));
+    mma_sub<1, NF>(acc, lw, bw, a_sp, as_operand(cur.dn[1]), ssp, sdn, lane);
+  }
 }
 
 template <typename OutT>
@@ -203,21 +289,23 @@ __device__ __forceinline__ void store_out<_Float16>(_Float16* p, float v) { *p =
 template <int NF, int PAT, bool SCALE_DW, typename OutT>
 __device__ __forceinline__ void tile_mx(const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale,
                                         const uint8_t* dn_codes, const uint8_t* dn_scale, const int32_t* row_index,
-                                        int64_t row_lo, int64_t row_hi, const uint8_t* wc, const uint8_t* ws, int n0,
-                                        int N, int K, OutT* Y, int64_t ldy, uint8_t* lds_w, uint32_t* lds_s) {
+                                        int64_t act_rows, int64_t row_lo, int64_t row_hi, const uint8_t* wc,
+                                        const uint8_t* ws, int n0,
+                                        int N, int K, OutT* Y, int64_t ldy, uint8_t* lds_w, uint8_t* lds_s) {
   constexpr int BN = 32 * NF;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
   const int nblk = K / 32, nks = (K + kBK - 1) / kBK;
 
   int64_t orow = row_lo + wave * 32 + (lane & 31);
   if (orow >= row_hi) orow = row_hi - 1;   // clamp: loads stay in bounds, stores are masked
-  const int64_t arow = row_index ? (int64_t)row_index[orow] : orow;
   ARow a;
-  a.dn = dn_codes + arow * (K / 2);
-  a.spc = sp_codes + arow * (K / 4);
-  a.spm = sp_meta + arow * (K / 8);
-  a.dns = dn_scale + arow * nblk;
-  a.sps = sp_scale + arow * nblk;
+  a.r = row_index ? (int64_t)row_index[orow] : orow;
+  a.R = act_rows;
+  a.dn = dn_codes;
+  a.spc = sp_codes;
+  a.spm = sp_meta;
+  a.dns = dn_scale;
+  a.sps = sp_scale;
 
   v16f acc[NF];
 #pragma unroll
@@ -225,28 +313,47 @@ __device__ __forceinline__ void tile_mx(const uint8_t* sp_codes, const uint8_t* 
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[f][r] = 0.0f;
 
-  AStep cur, nxt;
-  load_a<SCALE_DW>(cur, a, 0, half, nblk);
-  stage_w<NF, SCALE_DW>(lds_w, lds_s, wc, ws, n0, N, K, 0, nblk);
-  for (int ks = 0; ks < nks; ++ks) {
-    const int buf = ks & 1;
+  // Software pipeline over K steps, unrolled by two so that the two
+  // activation register sets alternate by position instead of being copied.
+  // Step ks computes from LDS buffer ks & 1 and register set ks & 1; after
+  // its MFMAs the weight tile of step ks+1 (loaded one step earlier) goes to
+  // the other LDS buffer and the loads of step ks+2 are issued, so every
+  // global load has one full step of MFMA work to arrive.  Loads past the
+  // last step re-read the last step (clamped) and are never used.
+  AStep a0, a1;
+  WStep<NF> wn;
+  const int last = nks - 1;
+  load_w<NF, SCALE_DW>(wn, wc, ws, n0, N, K, 0, nblk);
+  load_a<SCALE_DW>(a0, a, 0, half, nblk, K);
+  store_w<NF>(wn, lds_w, lds_s);
+  load_w<NF, SCALE_DW>(wn, wc, ws, n0, N, K, min(1, last), nblk);
+  load_a<SCALE_DW>(a1, a, min(1, last), half, nblk, K);
+  // The scheduling fences keep each phase in place: without them the
+  // compiler hoists ALU work on freshly issued loads into the preceding MFMA
+  // phase, which then has to wait for those loads.
+  constexpr int SREC = 64 * 2 * NF;   // bytes of one buffer's scale records
+  int ks = 0;
+  for (; ks + 1 < nks; ks += 2) {   // one exit: the accumulators stay in place
     __syncthreads();
-    if (ks + 1 < nks) {
-      load_a<SCALE_DW>(nxt, a, ks + 1, half, nblk);
-      stage_w<NF, SCALE_DW>(lds_w + (buf ^ 1) * BN * kLdsStride, lds_s + (buf ^ 1) * BN, wc, ws, n0, N, K, ks + 1,
-                            nblk);
-    }
-    const uint8_t* lw = lds_w + buf * BN * kLdsStride;
-    const uint32_t* ls = lds_s + buf * BN;
-    {
-      const v8i a_sp = as_operand(expand_block<PAT>(cur.spc[0], cur.spm[0]));
-      mma_sub<0, NF>(acc, lw, ls, a_sp, as_operand(cur.dn[0]), cur.ssp, cur.sdn, lane);
-    }
-    {
-      const v8i a_sp = as_operand(expand_block<PAT>(cur.spc[1], cur.spm[1]));
-      mma_sub<1, NF>(acc, lw, ls, a_sp, as_operand(cur.dn[1]), cur.ssp, cur.sdn, lane);
-    }
-    cur = nxt;
+    __builtin_amdgcn_sched_barrier(0);
+    step_mx<NF, PAT>(acc, a0, lds_w, lds_s, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    store_w<NF>(wn, lds_w + BN * kLdsStride, lds_s + SREC);
+    load_w<NF, SCALE_DW>(wn, wc, ws, n0, N, K, min(ks + 2, last), nblk);
+    load_a<SCALE_DW>(a0, a, min(ks + 2, last), half, nblk, K);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+    step_mx<NF, PAT>(acc, a1, lds_w + BN * kLdsStride, lds_s + SREC, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    store_w<NF>(wn, lds_w, lds_s);
+    load_w<NF, SCALE_DW>(wn, wc, ws, n0, N, K, min(ks + 3, last), nblk);
+    load_a<SCALE_DW>(a1, a, min(ks + 3, last), half, nblk, K);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if (ks < nks) {   // odd number of steps: the last one is in buffer 0 / set 0
+    __syncthreads();
+    step_mx<NF, PAT>(acc, a0, lds_w, lds_s, lane);
   }
 
 #pragma unroll
@@ -268,12 +375,12 @@ __global__ __launch_bounds__(256) void k_linear_mx(const uint8_t* sp_codes, cons
                                                    const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy) {
   constexpr int BN = 32 * NF;
   __shared__ __attribute__((aligned(16))) uint8_t lds_w[2 * BN * kLdsStride];
-  __shared__ uint32_t lds_s[2 * BN];
+  __shared__ __attribute__((aligned(16))) uint8_t lds_s[2 * 64 * 2 * NF];
   const int n0 = blockIdx.x * BN;
   const int64_t m0 = (int64_t)blockIdx.y * kBM;
   const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
-  tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, m0, m1, wc, ws, n0, N,
-                                   K, Y, ldy, lds_w, lds_s);
+  tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws, n0,
+                                   N, K, Y, ldy, lds_w, lds_s);
 }
 
 // Grouped (MoE) form.  Work item y of the grid is a 128-row tile of one
@@ -284,11 +391,11 @@ __global__ __launch_bounds__(256) void k_linear_mx(const uint8_t* sp_codes, cons
 template <int NF, int PAT, bool SCALE_DW, typename OutT>
 __global__ __launch_bounds__(256) void k_linear_mx_grouped(
     const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale, const uint8_t* dn_codes,
-    const uint8_t* dn_scale, const int32_t* row_index, const int32_t* offs, int E, const uint8_t* wc,
-    const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy) {
+    const uint8_t* dn_scale, const int32_t* row_index, int64_t act_rows, const int32_t* offs, int E,
+    const uint8_t* wc, const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy) {
   constexpr int BN = 32 * NF;
   __shared__ __attribute__((aligned(16))) uint8_t lds_w[2 * BN * kLdsStride];
-  __shared__ uint32_t lds_s[2 * BN];
+  __shared__ __attribute__((aligned(16))) uint8_t lds_s[2 * 64 * 2 * NF];
   __shared__ int s_first[1025];
   const int tid = threadIdx.x;
   // tiles per expert, then an inclusive scan (Hillis-Steele) over <= 1024 experts
@@ -327,8 +434,8 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
   const int n0 = blockIdx.x * BN;
   const uint8_t* wce = wc + (int64_t)e * N * (K / 2);
   const uint8_t* wse = ws + (int64_t)e * N * (K / 32);
-  tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, r0, r1, wce, wse, n0,
-                                   N, K, Y, ldy, lds_w, lds_s);
+  tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, act_rows, r0, r1,
+                                   wce, wse, n0, N, K, Y, ldy, lds_w, lds_s);
 }
 
 // ---------------------------------------------------------------------------
@@ -369,46 +476,46 @@ hipError_t launch_linear_mx(int pat, int ydt, const uint8_t* spc, const uint8_t*
 
 template <int NF, int PAT, bool SDW, typename OutT>
 static hipError_t go_grouped(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
-                             const uint8_t* dns, const int32_t* ridx, const int32_t* offs, int E, int64_t total,
-                             const uint8_t* wc, const uint8_t* ws, int N, int K, void* Y, int64_t ldy,
+                             const uint8_t* dns, const int32_t* ridx, int64_t act_rows, const int32_t* offs, int E,
+                             int64_t total, const uint8_t* wc, const uint8_t* ws, int N, int K, void* Y, int64_t ldy,
                              hipStream_t st) {
   // upper bound on the number of 128-row tiles over all experts
   const int64_t items = (total + kBM - 1) / kBM + E;
   dim3 grid((unsigned)((N + 32 * NF - 1) / (32 * NF)), (unsigned)items), block(256);
-  k_linear_mx_grouped<NF, PAT, SDW, OutT><<<grid, block, 0, st>>>(spc, spm, sps, dnc, dns, ridx, offs, E, wc, ws,
-                                                                  N, K, reinterpret_cast<OutT*>(Y), ldy);
+  k_linear_mx_grouped<NF, PAT, SDW, OutT><<<grid, block, 0, st>>>(spc, spm, sps, dnc, dns, ridx, act_rows, offs, E,
+                                                                  wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy);
   return hipGetLastError();
 }
 
 template <int NF, int PAT, bool SDW>
 static hipError_t go_grouped_dt(int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
-                                const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx, const int32_t* offs,
-                                int E, int64_t total, const uint8_t* wc, const uint8_t* ws, int N, int K, void* Y,
-                                int64_t ldy, hipStream_t st) {
+                                const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx, int64_t act_rows,
+                                const int32_t* offs, int E, int64_t total, const uint8_t* wc, const uint8_t* ws, int N,
+                                int K, void* Y, int64_t ldy, hipStream_t st) {
   if (ydt == 2)
-    return go_grouped<NF, PAT, SDW, float>(spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y, ldy, st);
+    return go_grouped<NF, PAT, SDW, float>(spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, total, wc, ws, N, K, Y, ldy, st);
   if (ydt == 1)
-    return go_grouped<NF, PAT, SDW, _Float16>(spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y, ldy,
+    return go_grouped<NF, PAT, SDW, _Float16>(spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, total, wc, ws, N, K, Y, ldy,
                                               st);
-  return go_grouped<NF, PAT, SDW, uint16_t>(spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y, ldy,
+  return go_grouped<NF, PAT, SDW, uint16_t>(spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, total, wc, ws, N, K, Y, ldy,
                                             st);
 }
 
 hipError_t launch_linear_mx_grouped(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
-                                    const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx,
+                                    const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx, int64_t act_rows,
                                     const int32_t* offs, int E, int64_t total, const uint8_t* wc, const uint8_t* ws,
                                     int N, int K, void* Y, int64_t ldy, hipStream_t st) {
   const bool sdw = (K % kBK) == 0;
   constexpr int NF = 8;
   if (pat == 24) {
-    return sdw ? go_grouped_dt<NF, 24, true>(ydt, spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y,
+    return sdw ? go_grouped_dt<NF, 24, true>(ydt, spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, total, wc, ws, N, K, Y,
                                              ldy, st)
-               : go_grouped_dt<NF, 24, false>(ydt, spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y,
+               : go_grouped_dt<NF, 24, false>(ydt, spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, total, wc, ws, N, K, Y,
                                               ldy, st);
   }
-  return sdw ? go_grouped_dt<NF, 48, true>(ydt, spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y, ldy,
+  return sdw ? go_grouped_dt<NF, 48, true>(ydt, spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, total, wc, ws, N, K, Y, ldy,
                                            st)
-             : go_grouped_dt<NF, 48, false>(ydt, spc, spm, sps, dnc, dns, ridx, offs, E, total, wc, ws, N, K, Y, ldy,
+             : go_grouped_dt<NF, 48, false>(ydt, spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, total, wc, ws, N, K, Y, ldy,
                                             st);
 }
 

@@ -219,20 +219,31 @@ __device__ __forceinline__ float wave_tree_sum(float v) {
   return v;
 }
 
-// Row pointers of the five output buffers for block b of a row.
-struct ActRow {
+// Output addressing.  Every buffer is panel-major: K is cut into panels of
+// 128 positions (4 scale blocks; the last panel may be narrower) and panel p
+// stores the bytes of all M rows for its K range, row after row.  Block b of
+// a row is block j = b % 4 of panel p = b / 4.
+struct ActOut {
+  uint8_t *spc, *spm, *sps, *dnc, *dns;
+  int64_t M;
+  int K;
+};
+
+struct BlockOut {
   uint8_t *spc, *spm, *sps, *dnc, *dns;
 };
 
-__device__ __forceinline__ ActRow act_row(uint8_t* sp_codes, uint8_t* sp_meta, uint8_t* sp_scale, uint8_t* dn_codes,
-                                          uint8_t* dn_scale, int64_t row, int K) {
-  ActRow a;
-  a.spc = sp_codes + row * (int64_t)(K / 4);
-  a.spm = sp_meta + row * (int64_t)(K / 8);
-  a.sps = sp_scale + row * (int64_t)(K / 32);
-  a.dnc = dn_codes + row * (int64_t)(K / 2);
-  a.dns = dn_scale + row * (int64_t)(K / 32);
-  return a;
+__device__ __forceinline__ BlockOut block_out(const ActOut& o, int64_t row, int b) {
+  const int p = b >> 2, j = b & 3;
+  const int wp = min(128, o.K - 128 * p);   // panel width in K positions
+  const int64_t pm = (int64_t)p * o.M;
+  BlockOut r;
+  r.dnc = o.dnc + pm * 64 + row * (wp / 2) + 16 * j;
+  r.spc = o.spc + pm * 32 + row * (wp / 4) + 8 * j;
+  r.spm = o.spm + pm * 16 + row * (wp / 8) + 4 * j;
+  r.sps = o.sps + pm * 4 + row * (wp / 32) + j;
+  r.dns = o.dns + pm * 4 + row * (wp / 32) + j;
+  return r;
 }
 
 // RMSNorm variant: the row's blocks stay in registers between the sum of
@@ -272,7 +283,7 @@ __global__ __launch_bounds__(256) void k_prep_mx_norm(const uint16_t* __restrict
     for (int k = 0; k < w; ++k) chunk[k] = chunk[2 * k] + chunk[2 * k + 1];
   const float r = (float)(1.0 / __builtin_sqrt((double)chunk[0] / (double)K + (double)eps));
 
-  ActRow o = act_row(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row, K);
+  const ActOut o{sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, (int64_t)M, K};
   const uint4* gr = reinterpret_cast<const uint4*>(gamma);
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
@@ -289,7 +300,8 @@ __global__ __launch_bounds__(256) void k_prep_mx_norm(const uint16_t* __restrict
       float t = x[k] * r;
       y[k] = t * g[k];
     }
-    block_mx<PAT>(y, o.spc + 8 * b, o.spm + 4 * b, o.sps + b, o.dnc + 16 * b, o.dns + b);
+    const BlockOut d = block_out(o, row, b);
+    block_mx<PAT>(y, d.spc, d.spm, d.sps, d.dnc, d.dns);
   }
 }
 
@@ -303,14 +315,15 @@ __global__ __launch_bounds__(256) void k_prep_mx_plain(const uint16_t* __restric
   if (row >= M) return;
   const int nblk = K / 32;
   const uint4* xr = reinterpret_cast<const uint4*>(X + row * ldx);
-  ActRow o = act_row(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row, K);
+  const ActOut o{sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, (int64_t)M, K};
   for (int b = lane; b < nblk; b += 64) {
     uint4 q[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) q[j] = xr[4 * b + j];
     float y[32];
     unpack_bf16x32(q, y);
-    block_mx<PAT>(y, o.spc + 8 * b, o.spm + 4 * b, o.sps + b, o.dnc + 16 * b, o.dns + b);
+    const BlockOut d = block_out(o, row, b);
+    block_mx<PAT>(y, d.spc, d.spm, d.sps, d.dnc, d.dns);
   }
 }
 

@@ -3,7 +3,9 @@
 // payload that both GEMM paths read.
 //
 // MXFP4: one lane per 32-value block along K; E8M0 exponent
-// floor(log2 amax) - 2 (clamped at -127), codes E2M1(w / 2^e).
+// floor(log2 amax) - 2 (clamped at -127), codes E2M1(w / 2^e).  The payload
+// and its scales are written panel-major (panels of 128 K positions, all N
+// rows of a panel back to back), the layout the GEMM streams.
 
 #include "sharq_device.hpp"
 
@@ -64,8 +66,11 @@ __global__ __launch_bounds__(256) void k_wquant_mx(const T* __restrict__ W, int 
     t = fp4x2<3>(t, v[8 * w + 6] * inv, v[8 * w + 7] * inv);
     q[w] = t;
   }
-  *reinterpret_cast<uint4*>(codes + n * (K / 2) + 16 * (int64_t)b) = make_uint4(q[0], q[1], q[2], q[3]);
-  scale[n * nblk + b] = (uint8_t)(e + 127);
+  // panel-major: panel p = b / 4 holds 128 K positions of all N rows
+  const int p = b >> 2, j = b & 3, wp = min(128, K - 128 * p);
+  const int64_t pn = (int64_t)p * N;
+  *reinterpret_cast<uint4*>(codes + pn * 64 + n * (wp / 2) + 16 * j) = make_uint4(q[0], q[1], q[2], q[3]);
+  scale[pn * 4 + n * (wp / 32) + j] = (uint8_t)(e + 127);
 }
 
 hipError_t launch_wquant_mx(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,

@@ -136,23 +136,22 @@ class QuantWeight:
 
 
 def alloc_act(rows: int, K: int, n: int = 2, m: int = 4, fmt="mx", device="cuda") -> PreparedAct:
+    """Device buffers of a prepared activation (flat, panel-major; see include/sharq.h)."""
     f = _FMT[fmt] if isinstance(fmt, str) else fmt
     sizes = [lib.sharq_act_buffer_bytes(rows, K, f, Pattern(n, m), w) for w in range(5)]
     if K <= 0 or K % 32 or (rows > 0 and min(sizes) == 0):
         raise SharqError(EINVAL, "alloc_act")
-    bufs = [torch.empty(max(s, 1), dtype=torch.uint8, device=device) for s in sizes]
-    shapes = [(rows, K * n // m // 2), (rows, K // 8), (rows, K // 32), (rows, K // 2),
-              (rows, K // 32 if f == MXFP4 else K // 16)]
-    bufs = [b[: r * c].view(r, c) if r * c > 0 else b[:0].view(r, c) for b, (r, c) in zip(bufs, shapes)]
+    bufs = [torch.empty(sz, dtype=torch.uint8, device=device) for sz in sizes]
     ts = torch.empty(1, dtype=torch.float32, device=device) if f == NVFP4 else None
     return PreparedAct(rows, K, f, n, m, *bufs, tensor_scale=ts)
 
 
 def alloc_weight(N: int, K: int, fmt="mx", experts: int = 1, device="cuda") -> QuantWeight:
+    """Device buffers of a quantized weight, one flat panel-major row per expert."""
     f = _FMT[fmt] if isinstance(fmt, str) else fmt
-    codes = torch.empty((experts, N, K // 2), dtype=torch.uint8, device=device)
-    scale = torch.empty((experts, N, K // 32), dtype=torch.uint8, device=device)
-    scale_dn = scale if f == MXFP4 else torch.empty((experts, N, K // 16), dtype=torch.uint8, device=device)
+    codes = torch.empty((experts, N * K // 2), dtype=torch.uint8, device=device)
+    scale = torch.empty((experts, N * K // 32), dtype=torch.uint8, device=device)
+    scale_dn = scale if f == MXFP4 else torch.empty((experts, N * K // 16), dtype=torch.uint8, device=device)
     ts = torch.empty(experts, dtype=torch.float32, device=device) if f == NVFP4 else None
     return QuantWeight(N, K, experts, f, codes, scale, scale_dn, ts)
 

@@ -5,6 +5,7 @@ buffers.  No arithmetic of the method lives here."""
 import numpy as np
 import torch
 
+from oracle import sharq_oracle as O
 from paper_2606_26587_amd import sharq as S
 
 
@@ -24,36 +25,38 @@ FMT_NAME = {S.MXFP4: "mx", S.NVFP4: "nv"}
 
 
 def act_to_oracle(a: S.PreparedAct) -> dict:
-    d = {"rows": a.rows, "K": a.K, "n": a.n, "m": a.m, "fmt": FMT_NAME[a.fmt],
-         "sp_codes": host(a.sp_codes), "sp_meta": host(a.sp_meta), "sp_scale": host(a.sp_scale),
-         "dn_codes": host(a.dn_codes), "dn_scale": host(a.dn_scale)}
-    d["tensor_scale"] = None if a.tensor_scale is None else np.float32(host(a.tensor_scale)[0])
-    return d
+    """Device prepared activation -> the oracle's row-major dict."""
+    bufs = {k: host(getattr(a, k)) for k in O.ACT_BUFFERS}
+    ts = None if a.tensor_scale is None else np.float32(host(a.tensor_scale)[0])
+    return O.act_from_device_layout(bufs, a.rows, a.K, a.n, a.m, FMT_NAME[a.fmt], ts)
 
 
 def oracle_to_act(o: dict) -> S.PreparedAct:
+    """Oracle prepared activation -> device buffers in the library's layout."""
     fmt = S.MXFP4 if o["fmt"] == "mx" else S.NVFP4
+    dev = O.act_to_device_layout(o)
     ts = None
     if fmt == S.NVFP4:
         ts = torch.tensor([float(o["tensor_scale"])], dtype=torch.float32, device="cuda")
-    return S.PreparedAct(o["dn_codes"].shape[0], o["K"], fmt, o["n"], o["m"], dev_u8(o["sp_codes"]),
-                         dev_u8(o["sp_meta"]), dev_u8(o["sp_scale"]), dev_u8(o["dn_codes"]), dev_u8(o["dn_scale"]),
-                         tensor_scale=ts)
+    return S.PreparedAct(o["dn_codes"].shape[0], o["K"], fmt, o["n"], o["m"], dev_u8(dev["sp_codes"]),
+                         dev_u8(dev["sp_meta"]), dev_u8(dev["sp_scale"]), dev_u8(dev["dn_codes"]),
+                         dev_u8(dev["dn_scale"]), tensor_scale=ts)
 
 
 def oracle_to_weight(o: dict) -> S.QuantWeight:
     fmt = S.MXFP4 if o["fmt"] == "mx" else S.NVFP4
-    codes = dev_u8(o["codes"])[None]
-    scale = dev_u8(o["scale"])[None]
-    scale_dn = scale if fmt == S.MXFP4 else dev_u8(o["scale_dn"])[None]
+    dev = O.weight_to_device_layout(o)
+    codes = dev_u8(dev["codes"])[None]
+    scale = dev_u8(dev["scale"])[None]
+    scale_dn = scale if fmt == S.MXFP4 else dev_u8(dev["scale_dn"])[None]
     ts = None if fmt == S.MXFP4 else torch.tensor([float(o["tensor_scale"])], dtype=torch.float32, device="cuda")
     return S.QuantWeight(o["N"], o["K"], 1, fmt, codes, scale, scale_dn, ts)
 
 
 def weight_to_oracle(w: S.QuantWeight, e: int = 0) -> dict:
-    return {"N": w.N, "K": w.K, "fmt": FMT_NAME[w.fmt], "codes": host(w.codes[e]), "scale": host(w.scale[e]),
-            "scale_dn": host(w.scale_dn[e]),
-            "tensor_scale": None if w.tensor_scale is None else np.float32(host(w.tensor_scale)[e])}
+    bufs = {"codes": host(w.codes[e]), "scale": host(w.scale[e]), "scale_dn": host(w.scale_dn[e])}
+    ts = None if w.tensor_scale is None else np.float32(host(w.tensor_scale)[e])
+    return O.weight_from_device_layout(bufs, w.N, w.K, FMT_NAME[w.fmt], ts)
 
 
 def assert_bytes_equal(name, got: np.ndarray, want: np.ndarray):

@@ -68,8 +68,9 @@ def check_prep(S, G, x_u16, gamma_u16, eps, n, m, tag):
     say(f"[prep] {tag} shape={x_u16.shape} n:m={n}:{m} gamma={gamma_u16 is not None}")
     a = run_prep(S, G, x_u16, gamma_u16, eps, n, m)
     o = O.prepare(x_u16, gamma_u16, eps, n, m, "mx")
-    for name in ("sp_codes", "sp_meta", "sp_scale", "dn_codes", "dn_scale"):
-        G.assert_bytes_equal(f"{tag}:{name}", G.host(getattr(a, name)), o[name])
+    dev = O.act_to_device_layout(o)
+    for name in O.ACT_BUFFERS:
+        G.assert_bytes_equal(f"{tag}:{name}", G.host(getattr(a, name)), dev[name])
     return a, o
 
 
@@ -119,7 +120,7 @@ def test_prep_empty(S, G):
     x = torch.empty((0, 128), dtype=torch.bfloat16, device="cuda")
     a = S.sharq_prepare(x, None, 1e-6, 2, 4, "mx")
     torch.cuda.synchronize()
-    assert a.rows == 0 and a.dn_codes.shape == (0, 64)
+    assert a.rows == 0 and a.dn_codes.numel() == 0
 
 
 def test_prep_strided_rows(S, G):
@@ -130,8 +131,9 @@ def test_prep_strided_rows(S, G):
     a = S.sharq_prepare(xd, None, 1e-6, 2, 4, "mx")
     torch.cuda.synchronize()
     o = O.prepare(np.ascontiguousarray(full[:, :K]), None, 1e-6, 2, 4, "mx")
-    for name in ("sp_codes", "sp_meta", "sp_scale", "dn_codes", "dn_scale"):
-        G.assert_bytes_equal(name, G.host(getattr(a, name)), o[name])
+    dev = O.act_to_device_layout(o)
+    for name in O.ACT_BUFFERS:
+        G.assert_bytes_equal(name, G.host(getattr(a, name)), dev[name])
 
 
 @pytest.mark.parametrize("N,K", [(64, 128), (200, 416), (6144, 4096), (33, 14336)])
@@ -140,7 +142,7 @@ def test_weight_quant_bit_exact(S, G, N, K):
     w = synth.weight(N, K, seed=N)
     q = S.sharq_quantize_weight(G.dev_bf16(w), "mx")
     torch.cuda.synchronize()
-    o = O.quantize_weight(w, "mx")
+    o = O.weight_to_device_layout(O.quantize_weight(w, "mx"))
     G.assert_bytes_equal("codes", G.host(q.codes[0]), o["codes"])
     G.assert_bytes_equal("scale", G.host(q.scale[0]), o["scale"])
 
@@ -150,7 +152,7 @@ def test_weight_quant_fp32_input(S, G):
     wf = torch.from_numpy(O.bf16_bits_to_f32(w)).cuda()
     q = S.sharq_quantize_weight(wf, "mx")
     torch.cuda.synchronize()
-    o = O.quantize_weight(w, "mx")
+    o = O.weight_to_device_layout(O.quantize_weight(w, "mx"))
     G.assert_bytes_equal("codes", G.host(q.codes[0]), o["codes"])
 
 

@@ -388,3 +388,21 @@ def test_nv_weight_views_share_payload():
     wq = O.quantize_weight(w, "nv")
     assert np.array_equal(O.dequant_weight(wq, "sp"), O.dequant_weight(wq, "dn"))
     assert wq["scale_dn"].shape[1] == 2 * wq["scale"].shape[1]
+
+
+# ----------------------------------------------------------------------------- panel layout
+
+@pytest.mark.parametrize("K", [32, 128, 416, 4096])
+def test_panel_layout_roundtrip_and_order(K):
+    rng = np.random.default_rng(K)
+    R = 7
+    a = rng.integers(0, 256, size=(R, K // 2), dtype=np.uint8)
+    flat = O.to_panels(a, K)
+    assert flat.size == a.size
+    assert np.array_equal(O.from_panels(flat, R, K, K // 2), a)
+    # panel 0 holds row 0's first 64 bytes, then row 1's first 64 bytes, ...
+    w0 = min(128, K) // 2
+    assert np.array_equal(flat[:w0], a[0, :w0]) and np.array_equal(flat[w0:2 * w0], a[1, :w0])
+    if K > 128:
+        assert np.array_equal(flat[R * 64: R * 64 + 64 if K - 128 >= 128 else R * 64 + (K - 128) // 2],
+                              a[0, 64: 128 if K - 128 >= 128 else 64 + (K - 128) // 2])
