@@ -368,16 +368,39 @@ __device__ __forceinline__ void tile_mx(const uint8_t* sp_codes, const uint8_t* 
   }
 }
 
+// Tile order.  Workgroups are dispatched round-robin over the 8 XCDs
+// (workgroup id mod 8), each with its own L2.  The ids are renumbered so that
+// each XCD walks a contiguous range of tiles, ordered in blocks of 4 M-tiles
+// x 8 N-tiles: the 32 workgroups an XCD runs at once then share 4 activation
+// tiles and 8 weight tiles in its L2.  Other grid shapes keep row-major order.
+__device__ __forceinline__ void tile_of(int id, int gx, int gy, int& mt, int& nt) {
+  const int total = gx * gy;
+  if ((gx & 7) == 0 && (gy & 3) == 0) {
+    const int per = total >> 3;
+    const int idp = (id & 7) * per + (id >> 3);
+    const int blk = idp >> 5, in = idp & 31;
+    const int bx = gx >> 3;
+    mt = (blk / bx) * 4 + (in & 3);
+    nt = (blk % bx) * 8 + (in >> 2);
+  } else {
+    mt = id / gx;
+    nt = id - mt * gx;
+  }
+}
+
 template <int NF, int PAT, bool SCALE_DW, typename OutT>
 __global__ __launch_bounds__(256) void k_linear_mx(const uint8_t* sp_codes, const uint8_t* sp_meta,
                                                    const uint8_t* sp_scale, const uint8_t* dn_codes,
                                                    const uint8_t* dn_scale, int64_t M, const uint8_t* wc,
-                                                   const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy) {
+                                                   const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy, int gx,
+                                                   int gy) {
   constexpr int BN = 32 * NF;
   __shared__ __attribute__((aligned(16))) uint8_t lds_w[2 * BN * kLdsStride];
   __shared__ __attribute__((aligned(16))) uint8_t lds_s[2 * 64 * 2 * NF];
-  const int n0 = blockIdx.x * BN;
-  const int64_t m0 = (int64_t)blockIdx.y * kBM;
+  int mt, nt;
+  tile_of(blockIdx.x, gx, gy, mt, nt);
+  const int n0 = nt * BN;
+  const int64_t m0 = (int64_t)mt * kBM;
   const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
   tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws, n0,
                                    N, K, Y, ldy, lds_w, lds_s);
@@ -446,9 +469,9 @@ template <int NF, int PAT, bool SDW, typename OutT>
 static hipError_t go_linear(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
                             const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
                             void* Y, int64_t ldy, hipStream_t st) {
-  dim3 grid((unsigned)((N + 32 * NF - 1) / (32 * NF)), (unsigned)((M + kBM - 1) / kBM)), block(256);
-  k_linear_mx<NF, PAT, SDW, OutT><<<grid, block, 0, st>>>(spc, spm, sps, dnc, dns, M, wc, ws, N, K,
-                                                          reinterpret_cast<OutT*>(Y), ldy);
+  const int gx = (N + 32 * NF - 1) / (32 * NF), gy = (int)((M + kBM - 1) / kBM);
+  k_linear_mx<NF, PAT, SDW, OutT><<<dim3((unsigned)(gx * gy)), dim3(256), 0, st>>>(
+      spc, spm, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
   return hipGetLastError();
 }
 
