@@ -43,9 +43,10 @@
  * GEMM streams it; a single row is still addressable (row gathers).  The
  * total size equals the row-major size R * (K / 32) * b.
  */
-#define SHARQ_PANEL_K 128
 #ifndef SHARQ_H
 #define SHARQ_H
+
+#define SHARQ_PANEL_K 128
 
 #include <stddef.h>
 #include <stdint.h>
@@ -181,7 +182,11 @@ SHARQ_API sharq_status sharq_prepare(const void *X, sharq_dtype xdt, int64_t M, 
  * by accumulation"): Y [rows][N] (row stride ldy, dtype ydt) =
  *   dequant(backbone) * dequant_sp(W)^T + dequant(residual) * dequant_dn(W)^T,
  * both products accumulated in one fp32 accumulator and written once.
- * The activation and weight formats must match.
+ * The activation and weight formats must match.  MXFP4 runs on the
+ * block-scaled FP4 matrix cores; NVFP4 (whose E4M3 block scales those cannot
+ * apply) multiplies the exactly dequantized bf16 values q * d and applies
+ * S_x * S_w once to the fp32 sums.  NVFP4 needs a->tensor_scale and
+ * w->tensor_scale.
  */
 SHARQ_API sharq_status sharq_linear(const sharq_act *a, const sharq_weight *w, void *Y, sharq_dtype ydt,
                           int64_t ldy, void *stream);
@@ -193,7 +198,8 @@ SHARQ_API sharq_status sharq_linear(const sharq_act *a, const sharq_weight *w, v
  * expert_offsets: device int32 [w->experts + 1], non-decreasing, first 0,
  * last == total.  row_index: device int32 [total], each in [0, a->rows), or
  * NULL.  Y [total][N] (row stride ldy).  Offsets are read on the device; the
- * host never waits for them.
+ * host never waits for them.  Built for MXFP4; NVFP4 returns
+ * SHARQ_EUNSUPPORTED.
  */
 SHARQ_API sharq_status sharq_linear_grouped(const sharq_act *a, const int32_t *row_index,
                                   const int32_t *expert_offsets, int64_t total,

@@ -7,9 +7,16 @@
 #include "sharq_device.hpp"
 
 namespace sharq {
-hipError_t launch_prep_mx(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps, int pat,
-                          uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, hipStream_t st);
+hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps, int pat,
+                       bool nv, const float* ts_in, float* ts_out, uint8_t* spc, uint8_t* spm, uint8_t* sps,
+                       uint8_t* dnc, uint8_t* dns, hipStream_t st);
 hipError_t launch_wquant_mx(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
+                            hipStream_t st);
+hipError_t launch_wquant_nv(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
+                            uint8_t* scale_dn, float* ts, hipStream_t st);
+hipError_t launch_linear_nv(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
+                            const uint8_t* dnc, const uint8_t* dns, const float* tsx, int64_t M, const uint8_t* wc,
+                            const uint8_t* ws, const float* tsw, int N, int K, void* Y, int64_t ldy,
                             hipStream_t st);
 hipError_t launch_linear_mx(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                             const uint8_t* dnc, const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws,
@@ -44,11 +51,12 @@ sharq_status check_act(const sharq_act* a) {
   const int pid = pattern_id(a->nm);
   if (pid < 0 || a->K % a->nm.m != 0) return SHARQ_EINVAL;
   if (pid == 0) return SHARQ_EUNSUPPORTED;
-  if (a->fmt != SHARQ_MXFP4) return a->fmt == SHARQ_NVFP4 ? SHARQ_EUNSUPPORTED : SHARQ_EINVAL;
+  if (a->fmt != SHARQ_MXFP4 && a->fmt != SHARQ_NVFP4) return SHARQ_EINVAL;
   if (a->rows == 0) return SHARQ_OK;   // an empty activation is never dereferenced
   if (!a->sp_codes || !a->sp_meta || !a->sp_scale || !a->dn_codes || !a->dn_scale) return SHARQ_EINVAL;
+  if (a->fmt == SHARQ_NVFP4 && !a->tensor_scale) return SHARQ_EINVAL;
   if (!aligned(a->sp_codes, 16) || !aligned(a->dn_codes, 16) || !aligned(a->sp_meta, 4) ||
-      !aligned(a->sp_scale, 4) || !aligned(a->dn_scale, 4))
+      !aligned(a->sp_scale, 4) || !aligned(a->dn_scale, 4) || !aligned(a->tensor_scale, 4))
     return SHARQ_EALIGN;
   return SHARQ_OK;
 }
@@ -58,9 +66,10 @@ sharq_status check_weight(const sharq_weight* w) {
   if (w->N < 0 || w->N > INT_MAX || w->K <= 0 || w->K % 32 != 0 || w->K > kMaxK || w->experts < 1 ||
       w->experts > kMaxExperts)
     return SHARQ_EINVAL;
-  if (w->fmt != SHARQ_MXFP4) return w->fmt == SHARQ_NVFP4 ? SHARQ_EUNSUPPORTED : SHARQ_EINVAL;
+  if (w->fmt != SHARQ_MXFP4 && w->fmt != SHARQ_NVFP4) return SHARQ_EINVAL;
   if (!w->codes || !w->scale) return SHARQ_EINVAL;
-  if (!aligned(w->codes, 16) || !aligned(w->scale, 4)) return SHARQ_EALIGN;
+  if (w->fmt == SHARQ_NVFP4 && (!w->scale_dn || !w->tensor_scale)) return SHARQ_EINVAL;
+  if (!aligned(w->codes, 16) || !aligned(w->scale, 4) || !aligned(w->tensor_scale, 4)) return SHARQ_EALIGN;
   return SHARQ_OK;
 }
 
@@ -116,19 +125,24 @@ sharq_status sharq_quantize_weight(const void* W, sharq_dtype wdt, int64_t N, in
   if (N < 0 || N > INT_MAX || K <= 0 || K % 32 != 0 || K > kMaxK || ldw < K) return SHARQ_EINVAL;
   if (out->N != N || out->K != K || out->experts != 1) return SHARQ_EINVAL;
   if (wdt != SHARQ_BF16 && wdt != SHARQ_F32) return SHARQ_EUNSUPPORTED;
-  if (out->fmt != SHARQ_MXFP4) return out->fmt == SHARQ_NVFP4 ? SHARQ_EUNSUPPORTED : SHARQ_EINVAL;
+  if (out->fmt != SHARQ_MXFP4 && out->fmt != SHARQ_NVFP4) return SHARQ_EINVAL;
+  const bool nv = out->fmt == SHARQ_NVFP4;
   if (!out->codes || !out->scale) return SHARQ_EINVAL;
-  if (!aligned(W, 16) || (ldw * (int64_t)(wdt == SHARQ_F32 ? 4 : 2)) % 16 != 0 || !aligned(out->codes, 16))
+  if (nv && (!out->scale_dn || !out->tensor_scale)) return SHARQ_EINVAL;
+  if (!aligned(W, 16) || (ldw * (int64_t)(wdt == SHARQ_F32 ? 4 : 2)) % 16 != 0 || !aligned(out->codes, 16) ||
+      !aligned(out->tensor_scale, 4))
     return SHARQ_EALIGN;
   if (N == 0) return SHARQ_OK;
-  return hip_status(sharq::launch_wquant_mx(W, (int)wdt, (int)N, (int)K, ldw, out->codes, out->scale,
-                                            reinterpret_cast<hipStream_t>(stream)));
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (nv)
+    return hip_status(sharq::launch_wquant_nv(W, (int)wdt, (int)N, (int)K, ldw, out->codes, out->scale,
+                                              out->scale_dn, out->tensor_scale, st));
+  return hip_status(sharq::launch_wquant_mx(W, (int)wdt, (int)N, (int)K, ldw, out->codes, out->scale, st));
 }
 
 sharq_status sharq_prepare(const void* X, sharq_dtype xdt, int64_t M, int64_t K, int64_t ldx, const void* gamma,
                            float eps, sharq_pattern nm, sharq_format fmt, const float* tensor_scale_in,
                            sharq_act* out, void* stream) {
-  (void)tensor_scale_in;
   if (!out) return SHARQ_EINVAL;
   if (M < 0 || M > INT_MAX || K <= 0 || K % 32 != 0 || K > kMaxK || ldx < K) return SHARQ_EINVAL;
   if (!X && M > 0) return SHARQ_EINVAL;
@@ -141,12 +155,15 @@ sharq_status sharq_prepare(const void* X, sharq_dtype xdt, int64_t M, int64_t K,
   sharq_status s = check_act(out);
   if (s != SHARQ_OK) return s;
   if (gamma && K > kMaxNormK) return SHARQ_EUNSUPPORTED;
-  if (!aligned(X, 16) || (ldx * 2) % 16 != 0 || (gamma && !aligned(gamma, 16))) return SHARQ_EALIGN;
+  const bool nv = fmt == SHARQ_NVFP4;
+  if (nv && M > 0 && !out->tensor_scale) return SHARQ_EINVAL;
+  if (!aligned(X, 16) || (ldx * 2) % 16 != 0 || (gamma && !aligned(gamma, 16)) || !aligned(tensor_scale_in, 4))
+    return SHARQ_EALIGN;
   if (M == 0) return SHARQ_OK;
-  return hip_status(sharq::launch_prep_mx(static_cast<const uint16_t*>(X), (int)M, (int)K, ldx,
-                                          static_cast<const uint16_t*>(gamma), eps, pid, out->sp_codes,
-                                          out->sp_meta, out->sp_scale, out->dn_codes, out->dn_scale,
-                                          reinterpret_cast<hipStream_t>(stream)));
+  return hip_status(sharq::launch_prep(static_cast<const uint16_t*>(X), (int)M, (int)K, ldx,
+                                       static_cast<const uint16_t*>(gamma), eps, pid, nv, nv ? tensor_scale_in : nullptr,
+                                       nv ? out->tensor_scale : nullptr, out->sp_codes, out->sp_meta, out->sp_scale,
+                                       out->dn_codes, out->dn_scale, reinterpret_cast<hipStream_t>(stream)));
 }
 
 sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sharq_dtype ydt, int64_t ldy,
@@ -161,9 +178,14 @@ sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sh
   if (ldy < w->N) return SHARQ_EINVAL;
   if (!aligned(Y, ysize(ydt))) return SHARQ_EALIGN;
   if (a->rows == 0 || w->N == 0) return SHARQ_OK;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (a->fmt == SHARQ_NVFP4)
+    return hip_status(sharq::launch_linear_nv(pattern_id(a->nm), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale,
+                                              a->dn_codes, a->dn_scale, a->tensor_scale, a->rows, w->codes,
+                                              w->scale, w->tensor_scale, (int)w->N, (int)w->K, Y, ldy, st));
   return hip_status(sharq::launch_linear_mx(pattern_id(a->nm), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale,
                                             a->dn_codes, a->dn_scale, a->rows, w->codes, w->scale, (int)w->N,
-                                            (int)w->K, Y, ldy, reinterpret_cast<hipStream_t>(stream)));
+                                            (int)w->K, Y, ldy, st));
 }
 
 sharq_status sharq_linear_grouped(const sharq_act* a, const int32_t* row_index, const int32_t* expert_offsets,
@@ -176,6 +198,7 @@ sharq_status sharq_linear_grouped(const sharq_act* a, const int32_t* row_index, 
   s = check_weight(w);
   if (s != SHARQ_OK) return s;
   if (a->fmt != w->fmt || a->K != w->K) return SHARQ_EINVAL;
+  if (a->fmt == SHARQ_NVFP4) return SHARQ_EUNSUPPORTED;
   if (total < 0 || total > INT_MAX) return SHARQ_EINVAL;
   if (!row_index && total > a->rows) return SHARQ_EINVAL;
   if (!ydt_ok(ydt)) return SHARQ_EUNSUPPORTED;

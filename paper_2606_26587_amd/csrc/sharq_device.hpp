@@ -97,4 +97,43 @@ __device__ __forceinline__ float e4m3_value(uint32_t c) {
   return E ? exp2_int((int)E - 7) * (1.0f + (float)M * 0.125f) : (float)M * 0.001953125f;
 }
 
+// Block quantizer policies.  enc(v) is the value handed to the E2M1
+// converter (whose scale operand stays 1.0: the hardware uses only the
+// exponent of that operand), dec(q) the dequantized value of a decoded code q.
+//   MXFP4: power-of-two scale 2^e, both directions exact.
+//   NVFP4: E4M3 block scale d under per-tensor scale S: enc = fl(v / fl(d S)),
+//          dec = fl(fl(q d) S); a zero block scale gives signed-zero codes.
+struct MxQ {
+  float inv, sc;
+  __device__ __forceinline__ float enc(float v) const { return v * inv; }
+  __device__ __forceinline__ float dec(float q) const { return q * sc; }
+};
+
+struct NvQ {
+  float d, step, S;
+  __device__ __forceinline__ float enc(float v) const {
+    if (!(d > 0.0f)) return v * 0.0f;   // keeps the sign of v
+    return step > 0.0f ? v / step : v;
+  }
+  __device__ __forceinline__ float dec(float q) const { return (q * d) * S; }
+  __device__ static NvQ make(float amax, float six_s, float S) {
+    NvQ q;
+    q.d = e4m3_round(amax / six_s);
+    q.step = q.d * S;
+    q.S = S;
+    return q;
+  }
+};
+
+// Eight consecutive values -> one dword of E2M1 codes under quantizer qz.
+template <class Q>
+__device__ __forceinline__ uint32_t enc8(const float* v, const Q& qz) {
+  uint32_t t = 0u;
+  t = fp4x2<0>(t, qz.enc(v[0]), qz.enc(v[1]));
+  t = fp4x2<1>(t, qz.enc(v[2]), qz.enc(v[3]));
+  t = fp4x2<2>(t, qz.enc(v[4]), qz.enc(v[5]));
+  t = fp4x2<3>(t, qz.enc(v[6]), qz.enc(v[7]));
+  return t;
+}
+
 }  // namespace sharq

@@ -462,6 +462,224 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
 }
 
 // ---------------------------------------------------------------------------
+// NVFP4 two-path GEMM
+// ---------------------------------------------------------------------------
+//
+// NVFP4 block scales are E4M3 (not powers of two), which the block-scaled FP4
+// MFMA cannot apply, and the products q * d of an E2M1 code and an E4M3 scale
+// carry up to 6 significant bits -- exact in bf16 but not in FP8.  So both
+// operands are dequantized to bf16 (q * d, exact) and multiplied on
+// v_mfma_f32_32x32x16_bf16; the per-tensor scales S_x * S_w are applied once
+// in the epilogue.  One K step is one 32-position block.  Activation
+// fragments are dequantized in the registers of the wavefront that owns the
+// rows; the weight tile is dequantized once per workgroup into LDS (bf16,
+// 64 bytes per row, parts XOR-swizzled like the MXFP4 path).
+//
+// bf16 32x32x16 operand layout: lane l holds row l % 32 and K values
+// 8 (l / 32) + 0..7; the accumulator layout is that of the FP4 MFMA.
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ int swz_nv(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
+
+// Eight E2M1 codes (one dword, lower K in the lower nibble) times scale d ->
+// eight exact bf16 values (4 dwords).  The fp32 products have at most 6
+// significant bits, so dropping the low 16 bits is exact.
+__device__ __forceinline__ uint4 dequant8_bf16(uint32_t codes, float d) {
+  uint32_t o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v2f v;
+    switch (i) {
+      case 0: v = fp4x2_decode<0>(codes); break;
+      case 1: v = fp4x2_decode<1>(codes); break;
+      case 2: v = fp4x2_decode<2>(codes); break;
+      default: v = fp4x2_decode<3>(codes); break;
+    }
+    const float a = v.x * d, b = v.y * d;
+    o[i] = __builtin_amdgcn_perm(__float_as_uint(b), __float_as_uint(a), 0x07060302u);
+  }
+  return make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 q) {
+  bf16x8 v;
+  __builtin_memcpy(&v, &q, 16);
+  return v;
+}
+
+struct NvA {         // one lane's activation data for one 32-position block
+  uint4 dn;          // residual codes
+  uint2 spc;         // compressed backbone codes
+  uint32_t spm;      // backbone metadata
+  uint32_t ssc;      // backbone E4M3 scale (byte 0)
+  uint32_t dsc;      // residual E4M3 scales of the two 16-halves (bytes 0, 1)
+};
+
+struct NvW {         // one thread's weight row for one block
+  uint4 codes;
+  uint32_t sc;
+};
+
+__device__ __forceinline__ void load_nv_a(NvA& s, const ARow& a, int ks, int K) {
+  const int p = ks >> 2, j = ks & 3, wp = min(128, K - 128 * p);
+  const int64_t pr = (int64_t)p * a.R;
+  s.dn = *reinterpret_cast<const uint4*>(a.dn + pr * 64 + a.r * (wp / 2) + 16 * j);
+  s.spc = *reinterpret_cast<const uint2*>(a.spc + pr * 32 + a.r * (wp / 4) + 8 * j);
+  s.spm = *reinterpret_cast<const uint32_t*>(a.spm + pr * 16 + a.r * (wp / 8) + 4 * j);
+  s.ssc = a.sps[pr * 4 + a.r * (wp / 32) + j];
+  s.dsc = *reinterpret_cast<const uint16_t*>(a.dns + pr * 8 + a.r * (wp / 16) + 2 * j);
+}
+
+template <int NF>
+__device__ __forceinline__ void load_nv_w(NvW& w, const uint8_t* wc, const uint8_t* ws, int n0, int N, int K,
+                                          int ks) {
+  static_assert(NF == 8, "one weight row per thread");
+  const int p = ks >> 2, j = ks & 3, wp = min(128, K - 128 * p);
+  const int64_t pn = (int64_t)p * N;
+  const int n = min(n0 + (int)threadIdx.x, N - 1);
+  w.codes = *reinterpret_cast<const uint4*>(wc + pn * 64 + (int64_t)n * (wp / 2) + 16 * j);
+  w.sc = ws[pn * 4 + (int64_t)n * (wp / 32) + j];
+}
+
+// Dequantize this thread's weight row (32 values) into the LDS tile as bf16.
+__device__ __forceinline__ void store_nv_w(const NvW& w, uint8_t* lds) {
+  const int row = threadIdx.x;
+  const float d = e4m3_value(w.sc);
+  const uint32_t c[4] = {w.codes.x, w.codes.y, w.codes.z, w.codes.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    *reinterpret_cast<uint4*>(lds + row * 64 + 16 * (q ^ swz_nv(row))) = dequant8_bf16(c[q], d);
+}
+
+template <int PAT, int NF>
+__device__ __forceinline__ void step_nv(v16f (&acc)[NF], const NvA& a, const uint8_t* lw, int lane) {
+  const int half = lane >> 5, col = lane & 31;
+  const uint4 sp = expand_block<PAT>(a.spc, a.spm);
+  const float dsp = e4m3_value(a.ssc & 0xFFu);
+  const float d0 = e4m3_value(a.dsc & 0xFFu), d1 = e4m3_value((a.dsc >> 8) & 0xFFu);
+  const uint32_t spw[4] = {sp.x, sp.y, sp.z, sp.w};
+  const uint32_t dnw[4] = {a.dn.x, a.dn.y, a.dn.z, a.dn.w};
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    // K values 8 half + 16 t + 0..7: dword (half + 2 t) of the block; the
+    // residual's 16-half is t
+    const bf16x8 asp = as_bf16x8(dequant8_bf16(spw[half + 2 * t], dsp));
+    const bf16x8 adn = as_bf16x8(dequant8_bf16(dnw[half + 2 * t], t ? d1 : d0));
+    bf16x8 b[NF];
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      const int row = f * 32 + col;
+      b[f] = as_bf16x8(*reinterpret_cast<const uint4*>(lw + row * 64 + 16 * ((half + 2 * t) ^ swz_nv(row))));
+    }
+#pragma unroll
+    for (int f = 0; f < NF; ++f) acc[f] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(asp, b[f], acc[f], 0, 0, 0);
+#pragma unroll
+    for (int f = 0; f < NF; ++f) acc[f] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(adn, b[f], acc[f], 0, 0, 0);
+  }
+}
+
+template <int NF, int PAT, typename OutT>
+__global__ __launch_bounds__(256) void k_linear_nv(const uint8_t* sp_codes, const uint8_t* sp_meta,
+                                                   const uint8_t* sp_scale, const uint8_t* dn_codes,
+                                                   const uint8_t* dn_scale, const float* ts_x, int64_t M,
+                                                   const uint8_t* wc, const uint8_t* ws, const float* ts_w, int N,
+                                                   int K, OutT* Y, int64_t ldy, int gx, int gy) {
+  constexpr int BN = 32 * NF;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * BN * 64];
+  int mt, nt;
+  tile_of(blockIdx.x, gx, gy, mt, nt);
+  const int n0 = nt * BN;
+  const int64_t row_lo = (int64_t)mt * kBM;
+  const int64_t row_hi = row_lo + kBM < M ? row_lo + kBM : M;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
+  const int nks = K / 32;
+
+  int64_t orow = row_lo + wave * 32 + (lane & 31);
+  if (orow >= row_hi) orow = row_hi - 1;
+  ARow a;
+  a.r = orow;
+  a.R = M;
+  a.dn = dn_codes;
+  a.spc = sp_codes;
+  a.spm = sp_meta;
+  a.dns = dn_scale;
+  a.sps = sp_scale;
+
+  v16f acc[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[f][r] = 0.0f;
+
+  NvA a0, a1;
+  NvW wn;
+  const int last = nks - 1;
+  load_nv_w<NF>(wn, wc, ws, n0, N, K, 0);
+  load_nv_a(a0, a, 0, K);
+  store_nv_w(wn, lds);
+  load_nv_w<NF>(wn, wc, ws, n0, N, K, min(1, last));
+  load_nv_a(a1, a, min(1, last), K);
+  int ks = 0;
+  for (; ks + 1 < nks; ks += 2) {
+    __syncthreads();
+    step_nv<PAT, NF>(acc, a0, lds, lane);
+    store_nv_w(wn, lds + BN * 64);
+    load_nv_w<NF>(wn, wc, ws, n0, N, K, min(ks + 2, last));
+    load_nv_a(a0, a, min(ks + 2, last), K);
+    __syncthreads();
+    step_nv<PAT, NF>(acc, a1, lds + BN * 64, lane);
+    store_nv_w(wn, lds);
+    load_nv_w<NF>(wn, wc, ws, n0, N, K, min(ks + 3, last));
+    load_nv_a(a1, a, min(ks + 3, last), K);
+  }
+  if (ks < nks) {
+    __syncthreads();
+    step_nv<PAT, NF>(acc, a0, lds, lane);
+  }
+
+  const float scale = *ts_x * *ts_w;
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int col = n0 + f * 32 + (lane & 31);
+    if (col >= N) continue;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t row = row_lo + wave * 32 + 8 * (r / 4) + 4 * half + (r % 4);
+      if (row < row_hi) store_out<OutT>(Y + row * ldy + col, acc[f][r] * scale);
+    }
+  }
+}
+
+template <int PAT, typename OutT>
+static hipError_t go_nv(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
+                        const uint8_t* dns, const float* tsx, int64_t M, const uint8_t* wc, const uint8_t* ws,
+                        const float* tsw, int N, int K, void* Y, int64_t ldy, hipStream_t st) {
+  constexpr int NF = 8;
+  const int gx = (N + 32 * NF - 1) / (32 * NF), gy = (int)((M + kBM - 1) / kBM);
+  k_linear_nv<NF, PAT, OutT><<<dim3((unsigned)(gx * gy)), dim3(256), 0, st>>>(
+      spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
+  return hipGetLastError();
+}
+
+template <int PAT>
+static hipError_t go_nv_dt(int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
+                           const uint8_t* dns, const float* tsx, int64_t M, const uint8_t* wc, const uint8_t* ws,
+                           const float* tsw, int N, int K, void* Y, int64_t ldy, hipStream_t st) {
+  if (ydt == 2) return go_nv<PAT, float>(spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
+  if (ydt == 1) return go_nv<PAT, _Float16>(spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
+  return go_nv<PAT, uint16_t>(spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
+}
+
+hipError_t launch_linear_nv(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
+                            const uint8_t* dnc, const uint8_t* dns, const float* tsx, int64_t M, const uint8_t* wc,
+                            const uint8_t* ws, const float* tsw, int N, int K, void* Y, int64_t ldy,
+                            hipStream_t st) {
+  return pat == 24 ? go_nv_dt<24>(ydt, spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, Y, ldy, st)
+                   : go_nv_dt<48>(ydt, spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
+}
+
+// ---------------------------------------------------------------------------
 // Host-side launchers
 // ---------------------------------------------------------------------------
 

@@ -71,8 +71,9 @@ __device__ __forceinline__ v2f get_pair_dyn(uint32_t word, int sel) {
 }
 
 // Backbone of one block for the 2:4 pattern.  Returns the residual in R.
-__device__ __forceinline__ void backbone_24(const float (&y)[32], float inv, float sc, uint32_t (&codes)[2],
-                                            uint32_t& meta, float (&R)[32]) {
+template <class Q>
+__device__ __forceinline__ void backbone_24(const float (&y)[32], const Q& qz, uint32_t (&codes)[2], uint32_t& meta,
+                                            float (&R)[32]) {
   codes[0] = codes[1] = 0u;
   meta = 0u;
 #pragma unroll
@@ -85,9 +86,9 @@ __device__ __forceinline__ void backbone_24(const float (&y)[32], float inv, flo
     uint32_t i0 = k0 ? 0u : (k1 ? 1u : 2u);
     uint32_t i1 = k3 ? 3u : (k2 ? 2u : 1u);
     meta |= (i0 | (i1 << 2)) << (4 * g);
-    put_pair_dyn(codes[g >> 2], g, v0 * inv, v1 * inv);
+    put_pair_dyn(codes[g >> 2], g, qz.enc(v0), qz.enc(v1));
     v2f d = get_pair_dyn(codes[g >> 2], g);
-    float d0 = d.x * sc, d1 = d.y * sc;            // exact: power-of-two scale
+    float d0 = qz.dec(d.x), d1 = qz.dec(d.y);
     R[4 * g + 0] = y0 - (k0 ? d0 : 0.0f);
     R[4 * g + 1] = y1 - (k1 ? (k0 ? d1 : d0) : 0.0f);
     R[4 * g + 2] = y2 - (k2 ? (k3 ? d0 : d1) : 0.0f);
@@ -96,8 +97,9 @@ __device__ __forceinline__ void backbone_24(const float (&y)[32], float inv, flo
 }
 
 // Backbone of one block for the 4:8 pattern (keep mask metadata).
-__device__ __forceinline__ void backbone_48(const float (&y)[32], float inv, float sc, uint32_t (&codes)[2],
-                                            uint32_t& meta, float (&R)[32]) {
+template <class Q>
+__device__ __forceinline__ void backbone_48(const float (&y)[32], const Q& qz, uint32_t (&codes)[2], uint32_t& meta,
+                                            float (&R)[32]) {
   codes[0] = codes[1] = 0u;
   meta = 0u;
 #pragma unroll
@@ -132,11 +134,11 @@ __device__ __forceinline__ void backbone_48(const float (&y)[32], float inv, flo
     }
     meta |= mask << (8 * g);
     int byte0 = 2 * g;   // group g's four codes occupy bytes 2g, 2g+1 of the 8
-    put_pair_dyn(codes[byte0 >> 2], byte0, v[0] * inv, v[1] * inv);
-    put_pair_dyn(codes[(byte0 + 1) >> 2], byte0 + 1, v[2] * inv, v[3] * inv);
+    put_pair_dyn(codes[byte0 >> 2], byte0, qz.enc(v[0]), qz.enc(v[1]));
+    put_pair_dyn(codes[(byte0 + 1) >> 2], byte0 + 1, qz.enc(v[2]), qz.enc(v[3]));
     v2f d01 = get_pair_dyn(codes[byte0 >> 2], byte0);
     v2f d23 = get_pair_dyn(codes[(byte0 + 1) >> 2], byte0 + 1);
-    float d[4] = {d01.x * sc, d01.y * sc, d23.x * sc, d23.y * sc};
+    float d[4] = {qz.dec(d01.x), qz.dec(d01.y), qz.dec(d23.x), qz.dec(d23.y)};
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
       float dp = 0.0f;
@@ -148,45 +150,68 @@ __device__ __forceinline__ void backbone_48(const float (&y)[32], float inv, flo
   }
 }
 
-// Quantize and store one block: backbone + residual.
+__device__ __forceinline__ float absmax32(const float* v) {
+  float m = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 32; ++k) m = fmaxf(m, fabsf(v[k]));
+  return m;
+}
+
+__device__ __forceinline__ float absmax16(const float* v) {
+  float m = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) m = fmaxf(m, fabsf(v[k]));
+  return m;
+}
+
+// Quantize and store one MXFP4 block: backbone + residual.  The group maximum
+// is always kept, so the backbone block max equals the block max of y.
 template <int PAT>
 __device__ __forceinline__ void block_mx(const float (&y)[32], uint8_t* __restrict__ spc, uint8_t* __restrict__ spm,
                                          uint8_t* __restrict__ sps, uint8_t* __restrict__ dnc,
                                          uint8_t* __restrict__ dns) {
-  // The group maximum is always kept, so the backbone block max equals the
-  // block max of y.
-  float amax = 0.0f;
-#pragma unroll
-  for (int k = 0; k < 32; ++k) amax = fmaxf(amax, fabsf(y[k]));
-  int e = mx_exponent(__float_as_uint(amax));
-  float inv = exp2_neg(e), sc = exp2_int(e);
+  const int e = mx_exponent(__float_as_uint(absmax32(y)));
+  const MxQ qb{exp2_neg(e), exp2_int(e)};
   uint32_t codes[2], meta;
   float R[32];
   if (PAT == 24)
-    backbone_24(y, inv, sc, codes, meta, R);
+    backbone_24(y, qb, codes, meta, R);
   else
-    backbone_48(y, inv, sc, codes, meta, R);
-
-  float ramax = 0.0f;
-#pragma unroll
-  for (int k = 0; k < 32; ++k) ramax = fmaxf(ramax, fabsf(R[k]));
-  int er = mx_exponent(__float_as_uint(ramax));
-  float rinv = exp2_neg(er);
+    backbone_48(y, qb, codes, meta, R);
+  const int er = mx_exponent(__float_as_uint(absmax32(R)));
+  const MxQ qr{exp2_neg(er), exp2_int(er)};
   uint32_t dn[4];
 #pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    uint32_t t = 0u;
-    t = fp4x2<0>(t, R[8 * w + 0] * rinv, R[8 * w + 1] * rinv);
-    t = fp4x2<1>(t, R[8 * w + 2] * rinv, R[8 * w + 3] * rinv);
-    t = fp4x2<2>(t, R[8 * w + 4] * rinv, R[8 * w + 5] * rinv);
-    t = fp4x2<3>(t, R[8 * w + 6] * rinv, R[8 * w + 7] * rinv);
-    dn[w] = t;
-  }
+  for (int w = 0; w < 4; ++w) dn[w] = enc8(R + 8 * w, qr);
   *reinterpret_cast<uint2*>(spc) = make_uint2(codes[0], codes[1]);
   *reinterpret_cast<uint32_t*>(spm) = meta;
   *sps = (uint8_t)(e + 127);
   *reinterpret_cast<uint4*>(dnc) = make_uint4(dn[0], dn[1], dn[2], dn[3]);
   *dns = (uint8_t)(er + 127);
+}
+
+// Quantize and store one NVFP4 block: E4M3 backbone scale per 32 positions,
+// E4M3 residual scales per 16 positions (two bytes), per-tensor scale S.
+template <int PAT>
+__device__ __forceinline__ void block_nv(const float (&y)[32], float S, float six_s, uint8_t* __restrict__ spc,
+                                         uint8_t* __restrict__ spm, uint8_t* __restrict__ sps,
+                                         uint8_t* __restrict__ dnc, uint8_t* __restrict__ dns) {
+  const NvQ qb = NvQ::make(absmax32(y), six_s, S);
+  uint32_t codes[2], meta;
+  float R[32];
+  if (PAT == 24)
+    backbone_24(y, qb, codes, meta, R);
+  else
+    backbone_48(y, qb, codes, meta, R);
+  const NvQ q0 = NvQ::make(absmax16(R), six_s, S);
+  const NvQ q1 = NvQ::make(absmax16(R + 16), six_s, S);
+  const uint32_t dn0 = enc8(R, q0), dn1 = enc8(R + 8, q0), dn2 = enc8(R + 16, q1), dn3 = enc8(R + 24, q1);
+  *reinterpret_cast<uint2*>(spc) = make_uint2(codes[0], codes[1]);
+  *reinterpret_cast<uint32_t*>(spm) = meta;
+  *sps = (uint8_t)e4m3_bits(qb.d);
+  *reinterpret_cast<uint4*>(dnc) = make_uint4(dn0, dn1, dn2, dn3);
+  dns[0] = (uint8_t)e4m3_bits(q0.d);
+  dns[1] = (uint8_t)e4m3_bits(q1.d);
 }
 
 __device__ __forceinline__ void unpack_bf16x32(const uint4 (&q)[4], float (&x)[32]) {
@@ -222,7 +247,8 @@ __device__ __forceinline__ float wave_tree_sum(float v) {
 // Output addressing.  Every buffer is panel-major: K is cut into panels of
 // 128 positions (4 scale blocks; the last panel may be narrower) and panel p
 // stores the bytes of all M rows for its K range, row after row.  Block b of
-// a row is block j = b % 4 of panel p = b / 4.
+// a row is block j = b % 4 of panel p = b / 4.  The NVFP4 residual keeps two
+// scale bytes per block (blocks of 16).
 struct ActOut {
   uint8_t *spc, *spm, *sps, *dnc, *dns;
   int64_t M;
@@ -233,6 +259,7 @@ struct BlockOut {
   uint8_t *spc, *spm, *sps, *dnc, *dns;
 };
 
+template <bool NV>
 __device__ __forceinline__ BlockOut block_out(const ActOut& o, int64_t row, int b) {
   const int p = b >> 2, j = b & 3;
   const int wp = min(128, o.K - 128 * p);   // panel width in K positions
@@ -242,23 +269,30 @@ __device__ __forceinline__ BlockOut block_out(const ActOut& o, int64_t row, int 
   r.spc = o.spc + pm * 32 + row * (wp / 4) + 8 * j;
   r.spm = o.spm + pm * 16 + row * (wp / 8) + 4 * j;
   r.sps = o.sps + pm * 4 + row * (wp / 32) + j;
-  r.dns = o.dns + pm * 4 + row * (wp / 32) + j;
+  r.dns = NV ? o.dns + pm * 8 + row * (wp / 16) + 2 * j : o.dns + pm * 4 + row * (wp / 32) + j;
   return r;
 }
 
-// RMSNorm variant: the row's blocks stay in registers between the sum of
-// squares and the quantization.  NB = blocks per lane, a power of two.
-template <int NB, int PAT>
-__global__ __launch_bounds__(256) void k_prep_mx_norm(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
-                                                      const uint16_t* __restrict__ gamma, float eps,
-                                                      uint8_t* sp_codes, uint8_t* sp_meta, uint8_t* sp_scale,
-                                                      uint8_t* dn_codes, uint8_t* dn_scale) {
-  const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= M) return;   // whole wavefront; the kernel has no block barrier
-  const int nblk = K / 32;
-  const uint4* xr = reinterpret_cast<const uint4*>(X + row * ldx);
-  uint4 xs[NB][4];
+template <int PAT, bool NV>
+__device__ __forceinline__ void block_out_write(const float (&y)[32], const ActOut& o, int64_t row, int b, float S,
+                                                float six_s) {
+  const BlockOut d = block_out<NV>(o, row, b);
+  if (NV)
+    block_nv<PAT>(y, S, six_s, d.spc, d.spm, d.sps, d.dnc, d.dns);
+  else
+    block_mx<PAT>(y, d.spc, d.spm, d.sps, d.dnc, d.dns);
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
+  return v;
+}
+
+// Load a row's blocks (NB per lane) and return its RMSNorm reciprocal r.
+template <int NB>
+__device__ __forceinline__ float load_row_rms(const uint4* xr, int lane, int nblk, int K, float eps,
+                                              uint4 (&xs)[NB][4]) {
   float chunk[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
@@ -281,81 +315,182 @@ __global__ __launch_bounds__(256) void k_prep_mx_norm(const uint16_t* __restrict
   for (int w = NB / 2; w >= 1; w >>= 1)
 #pragma unroll
     for (int k = 0; k < w; ++k) chunk[k] = chunk[2 * k] + chunk[2 * k + 1];
-  const float r = (float)(1.0 / __builtin_sqrt((double)chunk[0] / (double)K + (double)eps));
+  return (float)(1.0 / __builtin_sqrt((double)chunk[0] / (double)K + (double)eps));
+}
 
-  const ActOut o{sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, (int64_t)M, K};
+// y = (x * r) * gamma for one block.
+__device__ __forceinline__ void norm_block(const uint4 (&xq)[4], const uint4* gr, int b, float r, float (&y)[32]) {
+  uint4 gq[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) gq[j] = gr[4 * b + j];
+  float x[32], g[32];
+  unpack_bf16x32(xq, x);
+  unpack_bf16x32(gq, g);
+#pragma unroll
+  for (int k = 0; k < 32; ++k) {
+    const float t = x[k] * r;
+    y[k] = t * g[k];
+  }
+}
+
+// RMSNorm variant: the row's blocks stay in registers between the sum of
+// squares and the quantization.  NB = blocks per lane, a power of two.
+// NVFP4 reads the per-tensor scale S from S_ptr.
+template <int NB, int PAT, bool NV>
+__global__ __launch_bounds__(256) void k_prep_norm(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
+                                                   const uint16_t* __restrict__ gamma, float eps, ActOut o,
+                                                   const float* S_ptr) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;   // whole wavefront; the kernel has no block barrier
+  const int nblk = K / 32;
+  const float S = NV ? *S_ptr : 1.0f, six_s = 6.0f * S;
+  uint4 xs[NB][4];
+  const float r = load_row_rms<NB>(reinterpret_cast<const uint4*>(X + row * ldx), lane, nblk, K, eps, xs);
   const uint4* gr = reinterpret_cast<const uint4*>(gamma);
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
     const int b = lane + 64 * i;
     if (b >= nblk) break;
-    uint4 gq[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) gq[j] = gr[4 * b + j];
-    float x[32], g[32], y[32];
-    unpack_bf16x32(xs[i], x);
-    unpack_bf16x32(gq, g);
-#pragma unroll
-    for (int k = 0; k < 32; ++k) {
-      float t = x[k] * r;
-      y[k] = t * g[k];
-    }
-    const BlockOut d = block_out(o, row, b);
-    block_mx<PAT>(y, d.spc, d.spm, d.sps, d.dnc, d.dns);
+    float y[32];
+    norm_block(xs[i], gr, b, r, y);
+    block_out_write<PAT, NV>(y, o, row, b, S, six_s);
   }
 }
 
 // Variant without RMSNorm: a plain stream over the row's blocks.
-template <int PAT>
-__global__ __launch_bounds__(256) void k_prep_mx_plain(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
-                                                       uint8_t* sp_codes, uint8_t* sp_meta, uint8_t* sp_scale,
-                                                       uint8_t* dn_codes, uint8_t* dn_scale) {
+template <int PAT, bool NV>
+__global__ __launch_bounds__(256) void k_prep_plain(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
+                                                    ActOut o, const float* S_ptr) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
   const int nblk = K / 32;
+  const float S = NV ? *S_ptr : 1.0f, six_s = 6.0f * S;
   const uint4* xr = reinterpret_cast<const uint4*>(X + row * ldx);
-  const ActOut o{sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, (int64_t)M, K};
   for (int b = lane; b < nblk; b += 64) {
     uint4 q[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) q[j] = xr[4 * b + j];
     float y[32];
     unpack_bf16x32(q, y);
-    const BlockOut d = block_out(o, row, b);
-    block_mx<PAT>(y, d.spc, d.spm, d.sps, d.dnc, d.dns);
+    block_out_write<PAT, NV>(y, o, row, b, S, six_s);
   }
+}
+
+// ---------------------------------------------------------------------------
+// NVFP4 per-tensor scale (App. A.1.3): S = amax(y) / 2688 over the whole call,
+// 1 for an all-zero tensor.  The running maximum is kept as the bit pattern
+// of a non-negative float in the output's tensor_scale slot (bit patterns of
+// non-negative floats order like the floats), then replaced by S.
+// ---------------------------------------------------------------------------
+
+__global__ void k_store_u32(uint32_t* p, uint32_t v) { *p = v; }
+
+__global__ void k_copy_f32(const float* src, float* dst) { *dst = *src; }
+
+__global__ void k_pts_finalize(uint32_t* slot) {
+  const float amax = __uint_as_float(*slot);
+  const float S = amax > 0.0f ? amax / 2688.0f : 1.0f;
+  *reinterpret_cast<float*>(slot) = S;
+}
+
+template <int NB>
+__global__ __launch_bounds__(256) void k_amax_norm(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
+                                                   const uint16_t* __restrict__ gamma, float eps, uint32_t* slot) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const int nblk = K / 32;
+  uint4 xs[NB][4];
+  const float r = load_row_rms<NB>(reinterpret_cast<const uint4*>(X + row * ldx), lane, nblk, K, eps, xs);
+  const uint4* gr = reinterpret_cast<const uint4*>(gamma);
+  float m = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const int b = lane + 64 * i;
+    if (b >= nblk) break;
+    float y[32];
+    norm_block(xs[i], gr, b, r, y);
+    m = fmaxf(m, absmax32(y));
+  }
+  m = wave_max(m);
+  if (lane == 0) atomicMax(slot, __float_as_uint(m));
+}
+
+__global__ __launch_bounds__(256) void k_amax_plain(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
+                                                    uint32_t* slot) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const uint4* xr = reinterpret_cast<const uint4*>(X + row * ldx);
+  float m = 0.0f;
+  for (int b = lane; b < K / 32; b += 64) {
+    uint4 q[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) q[j] = xr[4 * b + j];
+    float y[32];
+    unpack_bf16x32(q, y);
+    m = fmaxf(m, absmax32(y));
+  }
+  m = wave_max(m);
+  if (lane == 0) atomicMax(slot, __float_as_uint(m));
 }
 
 // ---------------------------------------------------------------------------
 // Host-side launchers (called from the C ABI after validation)
 // ---------------------------------------------------------------------------
 
-template <int PAT>
-static hipError_t launch_prep_mx_pat(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps,
-                                     uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns,
-                                     hipStream_t st) {
-  dim3 grid((unsigned)((M + 3) / 4)), block(256);
+template <int PAT, bool NV>
+static void go_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps, const ActOut& o,
+                    const float* S_ptr, dim3 grid, hipStream_t st) {
+  dim3 block(256);
   if (gamma == nullptr) {
-    k_prep_mx_plain<PAT><<<grid, block, 0, st>>>(X, M, K, ldx, spc, spm, sps, dnc, dns);
-  } else {
-    const int chunks = (K / 32 + 63) / 64;
-    if (chunks <= 1)
-      k_prep_mx_norm<1, PAT><<<grid, block, 0, st>>>(X, M, K, ldx, gamma, eps, spc, spm, sps, dnc, dns);
-    else if (chunks <= 2)
-      k_prep_mx_norm<2, PAT><<<grid, block, 0, st>>>(X, M, K, ldx, gamma, eps, spc, spm, sps, dnc, dns);
-    else if (chunks <= 4)
-      k_prep_mx_norm<4, PAT><<<grid, block, 0, st>>>(X, M, K, ldx, gamma, eps, spc, spm, sps, dnc, dns);
-    else
-      k_prep_mx_norm<8, PAT><<<grid, block, 0, st>>>(X, M, K, ldx, gamma, eps, spc, spm, sps, dnc, dns);
+    k_prep_plain<PAT, NV><<<grid, block, 0, st>>>(X, M, K, ldx, o, S_ptr);
+    return;
   }
-  return hipGetLastError();
+  const int chunks = (K / 32 + 63) / 64;
+  if (chunks <= 1)
+    k_prep_norm<1, PAT, NV><<<grid, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
+  else if (chunks <= 2)
+    k_prep_norm<2, PAT, NV><<<grid, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
+  else if (chunks <= 4)
+    k_prep_norm<4, PAT, NV><<<grid, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
+  else
+    k_prep_norm<8, PAT, NV><<<grid, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
 }
 
-hipError_t launch_prep_mx(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps, int pat,
-                          uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, hipStream_t st) {
-  if (pat == 24) return launch_prep_mx_pat<24>(X, M, K, ldx, gamma, eps, spc, spm, sps, dnc, dns, st);
-  return launch_prep_mx_pat<48>(X, M, K, ldx, gamma, eps, spc, spm, sps, dnc, dns, st);
+// nv: NVFP4 with the per-tensor scale written to ts_out (from ts_in when
+// given, else computed from the data).
+hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps, int pat,
+                       bool nv, const float* ts_in, float* ts_out, uint8_t* spc, uint8_t* spm, uint8_t* sps,
+                       uint8_t* dnc, uint8_t* dns, hipStream_t st) {
+  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K};
+  const dim3 grid((unsigned)((M + 3) / 4));
+  if (nv) {
+    if (ts_in) {
+      k_copy_f32<<<1, 1, 0, st>>>(ts_in, ts_out);
+    } else {
+      uint32_t* slot = reinterpret_cast<uint32_t*>(ts_out);
+      k_store_u32<<<1, 1, 0, st>>>(slot, 0u);
+      if (gamma == nullptr) {
+        k_amax_plain<<<grid, 256, 0, st>>>(X, M, K, ldx, slot);
+      } else {
+        const int chunks = (K / 32 + 63) / 64;
+        if (chunks <= 1) k_amax_norm<1><<<grid, 256, 0, st>>>(X, M, K, ldx, gamma, eps, slot);
+        else if (chunks <= 2) k_amax_norm<2><<<grid, 256, 0, st>>>(X, M, K, ldx, gamma, eps, slot);
+        else if (chunks <= 4) k_amax_norm<4><<<grid, 256, 0, st>>>(X, M, K, ldx, gamma, eps, slot);
+        else k_amax_norm<8><<<grid, 256, 0, st>>>(X, M, K, ldx, gamma, eps, slot);
+      }
+      k_pts_finalize<<<1, 1, 0, st>>>(slot);
+    }
+    if (pat == 24) go_prep<24, true>(X, M, K, ldx, gamma, eps, o, ts_out, grid, st);
+    else go_prep<48, true>(X, M, K, ldx, gamma, eps, o, ts_out, grid, st);
+  } else {
+    if (pat == 24) go_prep<24, false>(X, M, K, ldx, gamma, eps, o, nullptr, grid, st);
+    else go_prep<48, false>(X, M, K, ldx, gamma, eps, o, nullptr, grid, st);
+  }
+  return hipGetLastError();
 }
 
 }  // namespace sharq

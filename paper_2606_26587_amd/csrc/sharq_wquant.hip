@@ -56,21 +56,74 @@ __global__ __launch_bounds__(256) void k_wquant_mx(const T* __restrict__ W, int 
   for (int k = 0; k < 32; ++k) amax = fmaxf(amax, fabsf(v[k]));
   const int e = mx_exponent(__float_as_uint(amax));
   const float inv = exp2_neg(e);
+  const MxQ qz{inv, 1.0f};
   uint32_t q[4];
 #pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    uint32_t t = 0u;
-    t = fp4x2<0>(t, v[8 * w + 0] * inv, v[8 * w + 1] * inv);
-    t = fp4x2<1>(t, v[8 * w + 2] * inv, v[8 * w + 3] * inv);
-    t = fp4x2<2>(t, v[8 * w + 4] * inv, v[8 * w + 5] * inv);
-    t = fp4x2<3>(t, v[8 * w + 6] * inv, v[8 * w + 7] * inv);
-    q[w] = t;
-  }
+  for (int w = 0; w < 4; ++w) q[w] = enc8(v + 8 * w, qz);
   // panel-major: panel p = b / 4 holds 128 K positions of all N rows
   const int p = b >> 2, j = b & 3, wp = min(128, K - 128 * p);
   const int64_t pn = (int64_t)p * N;
   *reinterpret_cast<uint4*>(codes + pn * 64 + n * (wp / 2) + 16 * j) = make_uint4(q[0], q[1], q[2], q[3]);
   scale[pn * 4 + n * (wp / 32) + j] = (uint8_t)(e + 127);
+}
+
+__device__ __forceinline__ float absmax32w(const float* v) {
+  float m = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 32; ++k) m = fmaxf(m, fabsf(v[k]));
+  return m;
+}
+
+// NVFP4 weight (App. A.1.2-A.1.3; Fig. 2): per-tensor S_w = amax(W) / 2688,
+// one E4M3 scale per 32 values (the sparse view), the dense view repeating it
+// for both 16-value halves.  The running maximum is the bit pattern of a
+// non-negative float in the tensor_scale slot, replaced by S_w afterwards.
+template <typename T>
+__global__ __launch_bounds__(256) void k_w_amax(const T* __restrict__ W, int N, int K, int64_t ldw, uint32_t* slot) {
+  const int nblk = K / 32;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  float m = 0.0f;
+  if (gid < (int64_t)N * nblk) {
+    const int64_t n = gid / nblk;
+    const int b = (int)(gid - n * nblk);
+    float v[32];
+    load32<T>(W + n * ldw + 32 * (int64_t)b, v);
+    m = absmax32w(v);
+  }
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1) m = fmaxf(m, __shfl_xor(m, s, 64));
+  if ((threadIdx.x & 63) == 0) atomicMax(slot, __float_as_uint(m));
+}
+
+__global__ void k_w_store_u32(uint32_t* p, uint32_t v) { *p = v; }
+
+__global__ void k_w_pts_finalize(uint32_t* slot) {
+  const float amax = __uint_as_float(*slot);
+  *reinterpret_cast<float*>(slot) = amax > 0.0f ? amax / 2688.0f : 1.0f;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_wquant_nv(const T* __restrict__ W, int N, int K, int64_t ldw,
+                                                   const float* S_ptr, uint8_t* __restrict__ codes,
+                                                   uint8_t* __restrict__ scale, uint8_t* __restrict__ scale_dn) {
+  const int nblk = K / 32;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= (int64_t)N * nblk) return;
+  const int64_t n = gid / nblk;
+  const int b = (int)(gid - n * nblk);
+  float v[32];
+  load32<T>(W + n * ldw + 32 * (int64_t)b, v);
+  const float S = *S_ptr;
+  const NvQ q = NvQ::make(absmax32w(v), 6.0f * S, S);
+  const int p = b >> 2, j = b & 3, wp = min(128, K - 128 * p);
+  const int64_t pn = (int64_t)p * N;
+  *reinterpret_cast<uint4*>(codes + pn * 64 + n * (wp / 2) + 16 * j) =
+      make_uint4(enc8(v, q), enc8(v + 8, q), enc8(v + 16, q), enc8(v + 24, q));
+  const uint8_t sb = (uint8_t)e4m3_bits(q.d);
+  scale[pn * 4 + n * (wp / 32) + j] = sb;
+  uint8_t* sd = scale_dn + pn * 8 + n * (wp / 16) + 2 * j;
+  sd[0] = sb;
+  sd[1] = sb;
 }
 
 hipError_t launch_wquant_mx(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
@@ -81,6 +134,26 @@ hipError_t launch_wquant_mx(const void* W, int wdt, int N, int K, int64_t ldw, u
     k_wquant_mx<float><<<grid, block, 0, st>>>(reinterpret_cast<const float*>(W), N, K, ldw, codes, scale);
   else
     k_wquant_mx<uint16_t><<<grid, block, 0, st>>>(reinterpret_cast<const uint16_t*>(W), N, K, ldw, codes, scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_wquant_nv(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
+                            uint8_t* scale_dn, float* ts, hipStream_t st) {
+  const int64_t total = (int64_t)N * (K / 32);
+  dim3 grid((unsigned)((total + 255) / 256)), block(256);
+  uint32_t* slot = reinterpret_cast<uint32_t*>(ts);
+  k_w_store_u32<<<1, 1, 0, st>>>(slot, 0u);
+  if (wdt == 2) {
+    k_w_amax<float><<<grid, block, 0, st>>>(reinterpret_cast<const float*>(W), N, K, ldw, slot);
+    k_w_pts_finalize<<<1, 1, 0, st>>>(slot);
+    k_wquant_nv<float><<<grid, block, 0, st>>>(reinterpret_cast<const float*>(W), N, K, ldw, ts, codes, scale,
+                                               scale_dn);
+  } else {
+    k_w_amax<uint16_t><<<grid, block, 0, st>>>(reinterpret_cast<const uint16_t*>(W), N, K, ldw, slot);
+    k_w_pts_finalize<<<1, 1, 0, st>>>(slot);
+    k_wquant_nv<uint16_t><<<grid, block, 0, st>>>(reinterpret_cast<const uint16_t*>(W), N, K, ldw, ts, codes,
+                                                  scale, scale_dn);
+  }
   return hipGetLastError();
 }
 

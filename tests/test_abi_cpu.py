@@ -130,7 +130,7 @@ def test_linear_rejects(L):
     assert L.sharq_linear(ctypes.byref(a), ctypes.byref(w), FAKE, 7, 64, None) == EUNSUPPORTED
     assert L.sharq_linear(ctypes.byref(a), ctypes.byref(w), FAKE + 2, 2, 64, None) == EALIGN   # fp32 Y
     w_nv = Weight(64, 128, 1, 1, FAKE, FAKE, FAKE, FAKE)
-    assert L.sharq_linear(ctypes.byref(a), ctypes.byref(w_nv), FAKE, 2, 64, None) in (EINVAL, EUNSUPPORTED)
+    assert L.sharq_linear(ctypes.byref(a), ctypes.byref(w_nv), FAKE, 2, 64, None) == EINVAL   # format mismatch
     empty = act(rows=0)
     assert L.sharq_linear(ctypes.byref(empty), ctypes.byref(w), FAKE, 2, 64, None) == OK
 
@@ -157,3 +157,32 @@ def test_quantize_weight_rejects(L):
     assert L.sharq_quantize_weight(FAKE, 0, 64, 128, 132, ctypes.byref(w), None) == EALIGN
     w0 = Weight(0, 128, 1, 0, FAKE, FAKE, FAKE, None)
     assert L.sharq_quantize_weight(FAKE, 0, 0, 128, 128, ctypes.byref(w0), None) == OK
+
+
+def nv_act(rows=8, K=128, ts=FAKE):
+    return Act(rows, K, 1, Pattern(2, 4), FAKE, FAKE, FAKE, FAKE, FAKE, ts)
+
+
+def test_nvfp4_needs_tensor_scales(L):
+    w = Weight(64, 128, 1, 1, FAKE, FAKE, FAKE, FAKE)
+    no_ts = nv_act(ts=None)
+    assert L.sharq_linear(ctypes.byref(no_ts), ctypes.byref(w), FAKE, 2, 64, None) == EINVAL
+    w_no_ts = Weight(64, 128, 1, 1, FAKE, FAKE, FAKE, None)
+    assert L.sharq_linear(ctypes.byref(nv_act()), ctypes.byref(w_no_ts), FAKE, 2, 64, None) == EINVAL
+    w_no_dn = Weight(64, 128, 1, 1, FAKE, FAKE, None, FAKE)
+    assert L.sharq_linear(ctypes.byref(nv_act()), ctypes.byref(w_no_dn), FAKE, 2, 64, None) == EINVAL
+    assert L.sharq_linear(ctypes.byref(nv_act(ts=FAKE + 2)), ctypes.byref(w), FAKE, 2, 64, None) == EALIGN
+    assert L.sharq_quantize_weight(FAKE, 0, 64, 128, 128, ctypes.byref(w_no_ts), None) == EINVAL
+    assert L.sharq_prepare(FAKE, 0, 8, 128, 128, None, 1e-6, Pattern(2, 4), 1, None, ctypes.byref(no_ts),
+                           None) == EINVAL
+    assert L.sharq_prepare(FAKE, 0, 8, 128, 128, None, 1e-6, Pattern(2, 4), 1, FAKE + 1, ctypes.byref(nv_act()),
+                           None) == EALIGN
+    # the activation's format must be the one asked for
+    assert L.sharq_prepare(FAKE, 0, 8, 128, 128, None, 1e-6, Pattern(2, 4), 0, None, ctypes.byref(nv_act()),
+                           None) == EINVAL
+
+
+def test_nvfp4_grouped_not_built(L):
+    w = Weight(64, 128, 4, 1, FAKE, FAKE, FAKE, FAKE)
+    assert L.sharq_linear_grouped(ctypes.byref(nv_act()), None, FAKE, 8, ctypes.byref(w), FAKE, 2, 64,
+                                  None) == EUNSUPPORTED

@@ -1,0 +1,200 @@
+"""NVFP4 variant of the HIP path (through the C ABI) against the CPU oracle.
+
+Preparation, the per-tensor scales and weight quantization must match the
+oracle byte for byte (the per-tensor scale as fp32 bits); the two-path GEMM
+must meet the same 1e-3 accumulation gate as the MXFP4 path.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import sharq_oracle as O
+from paper_2606_26587_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+GATE = 1e-3
+
+
+@pytest.fixture(scope="module")
+def S():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_26587_amd import sharq
+    return sharq
+
+
+@pytest.fixture(scope="module")
+def G(S):
+    import gpu_util
+    return gpu_util
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def f32_bits(v) -> int:
+    return int(np.asarray(v, dtype=np.float32).view(np.uint32))
+
+
+def check_prep_nv(S, G, x, g, eps, n, m, tag, ts_in=None):
+    say(f"[nv-prep] {tag} shape={x.shape} n:m={n}:{m} gamma={g is not None} ts_in={ts_in}")
+    xd = G.dev_bf16(x)
+    gd = None if g is None else G.dev_bf16(g)
+    tsd = None if ts_in is None else torch.tensor([ts_in], dtype=torch.float32, device="cuda")
+    a = S.sharq_prepare(xd, gd, eps, n, m, "nv", tensor_scale_in=tsd)
+    torch.cuda.synchronize()
+    o = O.prepare(x, g, eps, n, m, "nv", tensor_scale=ts_in)
+    assert f32_bits(G.host(a.tensor_scale)[0]) == f32_bits(o["tensor_scale"]), \
+        (tag, float(G.host(a.tensor_scale)[0]), float(o["tensor_scale"]))
+    dev = O.act_to_device_layout(o)
+    for name in O.ACT_BUFFERS:
+        G.assert_bytes_equal(f"{tag}:{name}", G.host(getattr(a, name)), dev[name])
+    return a, o
+
+
+NV_PREP_CASES = [
+    # (T, K, gamma, n, m, eps)
+    (8, 128, True, 2, 4, 1e-6),
+    (37, 416, True, 2, 4, 1e-5),
+    (37, 416, False, 2, 4, 1e-5),
+    (37, 416, True, 4, 8, 1e-5),
+    (3, 32, False, 2, 4, 1e-6),
+    (64, 3584, True, 2, 4, 1e-6),
+    (9, 18944, False, 2, 4, 1e-6),
+    (130, 2048, True, 4, 8, 1e-6),
+    (5, 16384, True, 2, 4, 1e-5),
+]
+
+
+@pytest.mark.parametrize("T,K,use_gamma,n,m,eps", NV_PREP_CASES)
+def test_nv_prep_bit_exact(S, G, T, K, use_gamma, n, m, eps):
+    x = synth.activations(T, K, seed=T + 3 * K)
+    g = synth.gamma(K, seed=K + 1) if use_gamma else None
+    check_prep_nv(S, G, x, g, eps, n, m, f"T{T}K{K}")
+
+
+@pytest.mark.parametrize("ts", [0.02, 1.0, 3.0e-4])
+def test_nv_prep_given_tensor_scale(S, G, ts):
+    """A caller-supplied S (e.g. calibrated offline) is used as is and copied out."""
+    x = synth.activations(20, 512, seed=11)
+    check_prep_nv(S, G, x, synth.gamma(512, seed=2), 1e-6, 2, 4, f"ts{ts}", ts_in=ts)
+
+
+@pytest.mark.parametrize("kind", ["zeros", "ties", "huge", "mixed", "onehot"])
+@pytest.mark.parametrize("n,m", [(2, 4), (4, 8)])
+def test_nv_prep_edge_values(S, G, kind, n, m):
+    T, K = 12, 256
+    rng = np.random.default_rng(len(kind))
+    if kind == "zeros":          # all-zero tensor: S = 1, every block scale 0
+        x = np.zeros((T, K), np.float32)
+        x[:, ::3] = -0.0
+    elif kind == "ties":
+        x = rng.integers(-3, 4, size=(T, K)).astype(np.float32)
+    elif kind == "huge":
+        x = (rng.standard_normal((T, K)) * 1e30).astype(np.float32)
+    elif kind == "mixed":        # blocks whose E4M3 scale underflows to 0 next to large ones
+        x = rng.standard_normal((T, K)).astype(np.float32)
+        x[0] = 0.0
+        x[1, ::2] = 1e-30
+        x[2] *= 1e6
+        x[3, 5::7] = 6000.0
+    else:                        # one large value per row: its block saturates, others are tiny
+        x = (rng.standard_normal((T, K)) * 1e-3).astype(np.float32)
+        x[np.arange(T), rng.integers(0, K, T)] = 5000.0
+    check_prep_nv(S, G, synth.f32_to_bf16_bits(x), None, 1e-6, n, m, f"nv-edge-{kind}")
+
+
+def test_nv_prep_empty(S, G):
+    x = torch.empty((0, 256), dtype=torch.bfloat16, device="cuda")
+    a = S.sharq_prepare(x, None, 1e-6, 2, 4, "nv")
+    torch.cuda.synchronize()
+    assert a.rows == 0
+
+
+@pytest.mark.parametrize("N,K,dt", [(64, 128, "bf16"), (200, 416, "bf16"), (3584, 3584, "bf16"),
+                                    (33, 18944, "bf16"), (96, 256, "f32")])
+def test_nv_weight_quant_bit_exact(S, G, N, K, dt):
+    say(f"[nv-wquant] N={N} K={K} {dt}")
+    w = synth.weight(N, K, seed=N + 1)
+    wd = G.dev_bf16(w) if dt == "bf16" else torch.from_numpy(O.bf16_bits_to_f32(w)).cuda()
+    q = S.sharq_quantize_weight(wd, "nv")
+    torch.cuda.synchronize()
+    wo = O.quantize_weight(w, "nv")
+    o = O.weight_to_device_layout(wo)
+    assert f32_bits(G.host(q.tensor_scale)[0]) == f32_bits(wo["tensor_scale"])
+    for name in O.WEIGHT_BUFFERS:
+        G.assert_bytes_equal(name, G.host(getattr(q, name)[0]), o[name])
+
+
+def gemm_check(y_gpu, y_ref, y_abs, tag):
+    gate = O.gemm_gate_error(y_gpu, y_ref, y_abs)
+    norm = float(np.abs(y_gpu.astype(np.float64) - y_ref).max() / max(np.abs(y_ref).max(), 1e-300))
+    say(f"[nv-gemm] {tag}: gate={gate:.3e} normwise={norm:.3e}")
+    assert gate <= GATE, (tag, gate)
+    assert norm <= GATE, (tag, norm)
+
+
+NV_LINEAR_CASES = [
+    # (T, N, K, n, m)
+    (8, 64, 128, 2, 4),
+    (300, 200, 416, 2, 4),
+    (1, 256, 3584, 2, 4),
+    (129, 300, 640, 4, 8),
+    (256, 512, 2048, 2, 4),
+    (16, 3584, 18944, 2, 4),
+]
+
+
+@pytest.mark.parametrize("T,N,K,n,m", NV_LINEAR_CASES)
+def test_nv_linear_parity(S, G, T, N, K, n, m):
+    say(f"[nv-linear] T={T} N={N} K={K} {n}:{m}")
+    x = synth.activations(T, K, seed=T + 5)
+    o = O.prepare(x, synth.gamma(K, seed=3), 1e-6, n, m, "nv")
+    wo = O.quantize_weight(synth.weight(N, K, seed=N + 7), "nv")
+    a, w = G.oracle_to_act(o), G.oracle_to_weight(wo)
+    y32 = S.sharq_linear(a, w, dtype=torch.float32)
+    y16 = S.sharq_linear(a, w, dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    gemm_check(G.host(y32), O.linear(o, wo), O.linear_abs(o, wo), f"T{T}N{N}K{K}")
+    assert torch.equal(y16, y32.to(torch.bfloat16))
+
+
+def test_nv_end_to_end_on_device(S, G):
+    """Prep + quantize + GEMM all on the device, checked against the oracle run on the same inputs."""
+    T, N, K = 96, 320, 1024
+    x = synth.activations(T, K, seed=21)
+    g = synth.gamma(K, seed=21)
+    w = synth.weight(N, K, seed=21)
+    a = S.sharq_prepare(G.dev_bf16(x), G.dev_bf16(g), 1e-6, 4, 8, "nv")
+    wq = S.sharq_quantize_weight(G.dev_bf16(w), "nv")
+    y = S.sharq_linear(a, wq, dtype=torch.float32)
+    torch.cuda.synchronize()
+    o = O.prepare(x, g, 1e-6, 4, 8, "nv")
+    wo = O.quantize_weight(w, "nv")
+    gemm_check(G.host(y), O.linear(o, wo), O.linear_abs(o, wo), "e2e")
+
+
+QWEN_T = 4096
+
+
+@pytest.mark.parametrize("name", ["gate_up", "down"])
+def test_qwen_full_shape_nv(S, G, name):
+    """Full M=4096 Qwen2.5-7B shapes: preparation compared in full, the GEMM on
+    64 sampled rows x all columns."""
+    K, N, norm = synth.QWEN_LINEARS[name]
+    say(f"[qwen-nv] {name} T={QWEN_T} K={K} N={N}")
+    x = synth.activations(QWEN_T, K, seed=1)
+    g = synth.gamma(K, seed=1) if norm else None
+    a, o = check_prep_nv(S, G, x, g, 1e-6, 2, 4, name)
+    wq = S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=1)), "nv")
+    y = S.sharq_linear(a, wq, dtype=torch.float32)
+    torch.cuda.synchronize()
+    wo = G.weight_to_oracle(wq)
+    rows = np.random.default_rng(2).choice(QWEN_T, 64, replace=False)
+    rows[0] = 0
+    gemm_check(G.host(y)[rows], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), name)
