@@ -1,22 +1,33 @@
 """Benchmark of the SharQ sparse-dense FP4 linear layer on one MI355X.
 
-One step = the whole hot path over one batch of synthetic input: for each of
-the three Llama-3.1-8B linear shapes at M = 2048 tokens (QKV and gate/up with
-the fused RMSNorm, down without), the fused preparation kernel followed by the
-two-path FP4 GEMM (2:4 backbone + dense residual, MXFP4, bf16 output).  Weights
-are quantized once before timing, as in inference.
+Default workload (the headline): one step = the whole hot path over one batch
+of synthetic input -- for each of the three Llama-3.1-8B linear shapes at
+M = 2048 tokens (QKV and gate/up with the fused RMSNorm, down without), the
+fused preparation kernel followed by the two-path FP4 GEMM (2:4 backbone +
+dense residual, MXFP4, bf16 output).  Weights are quantized once before
+timing, as in inference.
 
 Printed: one JSON line with the step throughput (TFLOP/s over the two FP4
 GEMMs' executed work, prep time included), the roofline of the dominant kernel
 (the two-path GEMM, against the dense MXFP4 MFMA peak), the preparation
 kernel's HBM rate, and the CPU oracle timed on a bounded sample.
 
-    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+Other workloads (--workload), one JSON line each:
+  llama-decode  the same three linears at M = 1, 16, 64, 256 (weight-stream bound)
+  qwen-nvfp4    Qwen2.5-7B gate/up and down at M = 4096, NVFP4 with the dynamic
+                per-tensor scale pre-pass
+  moe           Qwen3-30B-A3B expert layers, 4096 tokens, top-8 of 128 experts,
+                4:8 backbone, grouped GEMMs
+--calibrate-copy MiB runs a plain device copy of that size (the reference
+kernel for scaling the profiler's HBM byte counters) and nothing else.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--workload NAME] [--no-cpu-baseline]
 """
 
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import platform
@@ -25,11 +36,21 @@ import time
 
 import numpy as np
 
+ROOT = os.path.dirname(os.path.abspath(__file__))
+
 METRIC = "SharQ linear TFLOPS (prep+2 FP4 GEMMs) & prep HBM GB/s, Llama-8B M=2048"
 PEAK_FP4_TFLOPS = 10100.0     # MI355X dense MXFP4 MFMA
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
 T_TOKENS = 2048
 N_INPUT_SETS = 2              # activations rotate between steps (defeats the 256 MB last-level cache)
+
+# HBM traffic of the dominant kernel (k_linear_mx at the default workload,
+# mean over its three launch shapes), from two rocprofv3 --pmc runs
+# (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors a plain 1 GiB device copy
+# gives).  Valid only for the GEMM source it was measured on (sha256 prefix);
+# reported as null once that source has changed.
+TRAFFIC = {"gemm_source": "557b648b570b5fb0", "bytes_per_launch": 261.59e6}
 
 
 def log(*a):
@@ -41,22 +62,37 @@ def gemm_flops(T, N, K):
     return 4.0 * T * N * K
 
 
-def prep_bytes(T, K, norm):
-    """Algorithmic HBM bytes of one preparation call (MXFP4, 2:4): bf16 X and gamma in;
-    backbone codes K/4, metadata K/8, two scale rows K/32 each, residual codes K/2 out."""
-    return 2.0 * T * K + (2.0 * K if norm else 0.0) + T * (K / 4 + K / 8 + K / 32 + K / 2 + K / 32)
+def prep_bytes(T, K, norm, n=2, m=4, fmt="mx"):
+    """Algorithmic HBM bytes of one preparation call: bf16 X (and gamma) in;
+    backbone codes K n/m/2, metadata K/8, backbone scales K/32, residual codes
+    K/2 and residual scales K/32 (MXFP4) or K/16 (NVFP4) out."""
+    out = K * n / m / 2 + K / 8 + K / 32 + K / 2 + (K / 32 if fmt == "mx" else K / 16)
+    return 2.0 * T * K + (2.0 * K if norm else 0.0) + T * out
 
 
-def cpu_baseline(rows=128):
+def weight_bytes(N, K, fmt="mx"):
+    """Bytes of the shared FP4 weight payload and the scales one GEMM reads."""
+    return N * K / 2 + N * K / 32
+
+
+def gemm_source_digest():
+    with open(os.path.join(ROOT, "paper_2606_26587_amd", "csrc", "sharq_gemm.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def cpu_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return int(max([p.get("num_threads", 1) for p in threadpool_info()] or [1]))
+    except Exception:
+        return 1
+
+
+def cpu_baseline(rows=T_TOKENS):
     """The CPU oracle on a bounded sample of the same step: `rows` of the 2048
     token rows of each linear (preparation + two-path fp64 GEMM)."""
     from oracle import sharq_oracle as O
     from paper_2606_26587_amd import synth
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
     flops = 0.0
     elapsed = 0.0
     for name, (K, N, norm) in synth.LLAMA_LINEARS.items():
@@ -68,10 +104,247 @@ def cpu_baseline(rows=128):
         O.linear(a, wq)
         elapsed += time.perf_counter() - t0
         flops += gemm_flops(rows, N, K)
-    return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{rows} of {T_TOKENS} token rows of each Llama linear (qkv, gate_up, down): "
+    return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": cpu_threads(), "kind": "oracle",
+            "sample": f"{rows} of the {T_TOKENS} token rows of each Llama linear (qkv, gate_up, down): "
                       f"NumPy preparation + fp64 two-path GEMM; weight quantization untimed",
             "seconds": elapsed, "host_cpus": len(os.sched_getaffinity(0)), "cpu": platform.processor() or None}
+
+
+class Timer:
+    """Brackets every op of a step with HIP events on the launch stream."""
+
+    def __init__(self, torch, stream, n_ops, steps):
+        self.stream = stream
+        self.ev = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ops + 1)] for _ in range(steps)]
+
+    def mark(self, step, i):
+        self.ev[step][i].record(self.stream)
+
+    def op_ms(self, i):
+        return float(np.mean([e[i].elapsed_time(e[i + 1]) for e in self.ev]))
+
+
+def run_steps(torch, stream, step, n_ops, steps, warmup):
+    """Warm up, then time exactly `steps` steps synchronized on both sides."""
+    for i in range(warmup):
+        step(i, None)
+    torch.cuda.synchronize()
+    tm = Timer(torch, stream, n_ops, steps)
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record(stream)
+    for i in range(steps):
+        step(i, lambda k, i=i: tm.mark(i, k))
+    t1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    return t0.elapsed_time(t1) / steps, wall * 1e3 / steps, tm
+
+
+def base_record(args, metric, value, unit, ms_step, dtype, config):
+    return {"metric": metric, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": dtype, "data": "synthetic", "config": config}
+
+
+# ---------------------------------------------------------------------------
+# workloads
+# ---------------------------------------------------------------------------
+
+def dense_layers(torch, S, synth, dev, shapes, T, fmt, n, m, n_sets):
+    def to_dev(u16):
+        return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).to(dev)
+    layers = []
+    for name, (K, N, norm) in shapes.items():
+        xs = [to_dev(synth.activations(T, K, seed=s)) for s in range(n_sets)]
+        g = to_dev(synth.gamma(K, seed=0)) if norm else None
+        w = S.sharq_quantize_weight(to_dev(synth.weight(N, K, seed=0)), fmt)
+        acts = [S.alloc_act(T, K, n, m, fmt, dev) for _ in range(n_sets)]
+        ys = [torch.empty((T, N), dtype=torch.bfloat16, device=dev) for _ in range(n_sets)]
+        layers.append(dict(name=name, K=K, N=N, norm=norm, xs=xs, g=g, w=w, acts=acts, ys=ys))
+    torch.cuda.synchronize()
+    return layers
+
+
+def dense_step(S, layers, stream, eps, n, m, fmt, n_sets):
+    def step(i, mark):
+        j = i % n_sets
+        for li, L in enumerate(layers):
+            if mark:
+                mark(2 * li)
+            S.sharq_prepare(L["xs"][j], L["g"], eps, n, m, fmt, out=L["acts"][j], stream=stream)
+            if mark:
+                mark(2 * li + 1)
+            S.sharq_linear(L["acts"][j], L["w"], out=L["ys"][j], stream=stream)
+        if mark:
+            mark(2 * len(layers))
+    return step
+
+
+def per_linear(layers, tm, T, fmt, n, m):
+    per = []
+    for li, L in enumerate(layers):
+        prep_ms, gemm_ms = tm.op_ms(2 * li), tm.op_ms(2 * li + 1)
+        f = gemm_flops(T, L["N"], L["K"])
+        b = prep_bytes(T, L["K"], L["norm"], n, m, fmt)
+        wb = weight_bytes(L["N"], L["K"], fmt)
+        per.append({"linear": L["name"], "K": L["K"], "N": L["N"], "rmsnorm": L["norm"],
+                    "prep_us": prep_ms * 1e3, "prep_bytes": b, "prep_GBps": b / (prep_ms * 1e-3) / 1e9,
+                    "gemm_us": gemm_ms * 1e3, "gemm_flops": f, "gemm_TFLOPs": f / (gemm_ms * 1e-3) / 1e12,
+                    "weight_bytes": wb, "weight_GBps": wb / (gemm_ms * 1e-3) / 1e9})
+        log(f"[bench] {L['name']:8s} T={T:5d} prep {prep_ms * 1e3:8.2f} us {per[-1]['prep_GBps']:8.1f} GB/s | "
+            f"gemm {gemm_ms * 1e3:8.2f} us {per[-1]['gemm_TFLOPs']:8.1f} TFLOP/s "
+            f"{per[-1]['weight_GBps']:8.1f} GB/s of weight")
+    return per
+
+
+def llama_prefill(args, torch, S, synth, dev, stream):
+    layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T_TOKENS, "mx", 2, 4, N_INPUT_SETS)
+    log(f"[bench] set up {len(layers)} linears, M={T_TOKENS}")
+    step = dense_step(S, layers, stream, synth.LLAMA_EPS, 2, 4, "mx", N_INPUT_SETS)
+    ms_step, wall_ms, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
+    log(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step (wall {wall_ms:.4f} ms/step)")
+    per = per_linear(layers, tm, T_TOKENS, "mx", 2, 4)
+    flops_step = sum(p["gemm_flops"] for p in per)
+    t_gemm = sum(p["gemm_us"] for p in per) * 1e-6
+    t_prep = sum(p["prep_us"] for p in per) * 1e-6
+    bytes_prep = sum(p["prep_bytes"] for p in per)
+    gemm_tf = flops_step / t_gemm / 1e12
+    prep_gbps = bytes_prep / t_prep / 1e9
+    traffic = None
+    if TRAFFIC is not None and TRAFFIC["gemm_source"] == gemm_source_digest():
+        traffic = TRAFFIC["bytes_per_launch"]
+    out = base_record(
+        args, METRIC, flops_step / (ms_step * 1e-3) / 1e12, "TFLOP/s", ms_step, "mxfp4",
+        {"workload": "Llama-3.1-8B prefill linears qkv (K4096,N6144,RMSNorm), gate_up (K4096,N28672,"
+                     "RMSNorm), down (K14336,N4096); M=2048 tokens; 2:4 backbone; MXFP4; bf16 out",
+         "tokens": T_TOKENS, "pattern": "2:4", "format": "MXFP4", "flops_per_step": flops_step,
+         "flops_counting": "4*M*N*K per linear (two dense-executed FP4 GEMMs)"})
+    out["roofline"] = {"bound": "mfma", "kernel": "k_linear_mx (two-path FP4 GEMM)", "achieved": gemm_tf,
+                       "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s", "frac": gemm_tf / PEAK_FP4_TFLOPS,
+                       "traffic": traffic, "flops_per_launch": flops_step / len(per),
+                       "us_per_launch": t_gemm * 1e6 / len(per)}
+    out["prep"] = {"bound": "hbm", "kernel": "k_prep_norm / k_prep_plain (fused preparation)",
+                   "achieved": prep_gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": prep_gbps / PEAK_HBM_GBPS}
+    out["per_linear"] = per
+    out["wall_ms_per_step"] = wall_ms
+    return out
+
+
+def llama_decode(args, torch, S, synth, dev, stream):
+    outs = []
+    for T in (1, 16, 64, 256):
+        layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T, "mx", 2, 4, 1)
+        step = dense_step(S, layers, stream, synth.LLAMA_EPS, 2, 4, "mx", 1)
+        ms_step, wall_ms, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
+        per = per_linear(layers, tm, T, "mx", 2, 4)
+        wb = sum(p["weight_bytes"] for p in per)
+        t_gemm = sum(p["gemm_us"] for p in per) * 1e-6
+        out = base_record(args, "SharQ decode linears weight-stream GB/s (prep+GEMM), Llama-8B",
+                          wb / (ms_step * 1e-3) / 1e9, "GB/s", ms_step, "mxfp4",
+                          {"workload": f"Llama-3.1-8B decode linears qkv, gate_up, down; M={T}; 2:4; MXFP4",
+                           "tokens": T})
+        out["roofline"] = {"bound": "hbm", "kernel": "k_linear_mx", "achieved": wb / t_gemm / 1e9,
+                           "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": wb / t_gemm / 1e9 / PEAK_HBM_GBPS,
+                           "traffic": None}
+        out["per_linear"] = per
+        outs.append(out)
+        del layers
+        torch.cuda.empty_cache()
+    return outs
+
+
+def qwen_nvfp4(args, torch, S, synth, dev, stream):
+    T = 4096
+    layers = dense_layers(torch, S, synth, dev, synth.QWEN_LINEARS, T, "nv", 2, 4, N_INPUT_SETS)
+    step = dense_step(S, layers, stream, 1e-6, 2, 4, "nv", N_INPUT_SETS)
+    ms_step, wall_ms, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
+    per = per_linear(layers, tm, T, "nv", 2, 4)
+    flops = sum(p["gemm_flops"] for p in per)
+    t_gemm = sum(p["gemm_us"] for p in per) * 1e-6
+    t_prep = sum(p["prep_us"] for p in per) * 1e-6
+    pb = sum(p["prep_bytes"] for p in per)
+    out = base_record(args, "SharQ linear TFLOPS (prep+2 FP4 GEMMs), Qwen2.5-7B M=4096 NVFP4",
+                      flops / (ms_step * 1e-3) / 1e12, "TFLOP/s", ms_step, "nvfp4",
+                      {"workload": "Qwen2.5-7B prefill linears gate_up (K3584,N37888,RMSNorm), down (K18944,N3584); "
+                                   "M=4096; 2:4; NVFP4 with dynamic per-tensor scale", "tokens": T})
+    out["roofline"] = {"bound": "mfma", "kernel": "k_linear_nv (bf16 MFMA over dequantized FP4)",
+                       "achieved": flops / t_gemm / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                       "frac": flops / t_gemm / 1e12 / PEAK_BF16_TFLOPS, "traffic": None}
+    out["prep"] = {"bound": "hbm", "achieved": pb / t_prep / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                   "frac": pb / t_prep / 1e9 / PEAK_HBM_GBPS,
+                   "note": "time includes the per-tensor amax pre-pass (a second read of X)"}
+    out["per_linear"] = per
+    return out
+
+
+def moe(args, torch, S, synth, dev, stream):
+    cfg = synth.MOE
+    T, H, E, I, k = cfg["tokens"], cfg["hidden"], cfg["experts"], cfg["inter"], cfg["topk"]
+
+    def to_dev(u16):
+        return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    x = to_dev(synth.activations(T, H, seed=0))
+    g = to_dev(synth.gamma(H, seed=0))
+    ridx, offs = synth.router_topk(T, E, k, seed=0)
+    total = int(offs[-1])
+    h = to_dev(synth.activations(total, I, seed=1))   # stands in for SiLU(gate) * up, expert-sorted
+    log(f"[bench] moe: quantizing {E} experts x (gate_up {2 * I}x{H}, down {H}x{I})")
+    w_gu = S.stack_weights([S.sharq_quantize_weight(to_dev(synth.weight(2 * I, H, seed=100 + e)), "mx")
+                            for e in range(E)])
+    w_dn = S.stack_weights([S.sharq_quantize_weight(to_dev(synth.weight(H, I, seed=1000 + e)), "mx")
+                            for e in range(E)])
+    ri = torch.from_numpy(ridx).to(dev)
+    of = torch.from_numpy(offs).to(dev)
+    a1 = S.alloc_act(T, H, 4, 8, "mx", dev)
+    a2 = S.alloc_act(total, I, 4, 8, "mx", dev)
+    y1 = torch.empty((total, 2 * I), dtype=torch.bfloat16, device=dev)
+    y2 = torch.empty((total, H), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+
+    def step(i, mark):
+        if mark:
+            mark(0)
+        S.sharq_prepare(x, g, 1e-6, 4, 8, "mx", out=a1, stream=stream)
+        if mark:
+            mark(1)
+        S.sharq_linear_grouped(a1, ri, of, total, w_gu, out=y1, stream=stream)
+        if mark:
+            mark(2)
+        S.sharq_prepare(h, None, 1e-6, 4, 8, "mx", out=a2, stream=stream)
+        if mark:
+            mark(3)
+        S.sharq_linear_grouped(a2, None, of, total, w_dn, out=y2, stream=stream)
+        if mark:
+            mark(4)
+
+    ms_step, wall_ms, tm = run_steps(torch, stream, step, 4, args.steps, args.warmup)
+    f1, f2 = gemm_flops(total, 2 * I, H), gemm_flops(total, H, I)
+    ops = {"prep_gate_up_us": tm.op_ms(0) * 1e3, "grouped_gate_up_us": tm.op_ms(1) * 1e3,
+           "prep_down_us": tm.op_ms(2) * 1e3, "grouped_down_us": tm.op_ms(3) * 1e3}
+    t_g = (tm.op_ms(1) + tm.op_ms(3)) * 1e-3
+    log(f"[bench] moe {ops}")
+    out = base_record(args, "SharQ MoE expert layers TFLOPS (prep+grouped FP4 GEMMs), Qwen3-30B-A3B 4096 tokens",
+                      (f1 + f2) / (ms_step * 1e-3) / 1e12, "TFLOP/s", ms_step, "mxfp4",
+                      {"workload": f"Qwen3-30B-A3B experts: {T} tokens, top-{k} of {E}, gate_up {2 * I}x{H} "
+                                   f"(RMSNorm), down {H}x{I}; 4:8; MXFP4", "tokens": T, "routed_rows": total})
+    out["roofline"] = {"bound": "mfma", "kernel": "k_linear_mx_grouped", "achieved": (f1 + f2) / t_g / 1e12,
+                       "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s", "frac": (f1 + f2) / t_g / 1e12 / PEAK_FP4_TFLOPS,
+                       "traffic": None}
+    out["ops"] = ops
+    return out
+
+
+def calibrate_copy(torch, dev, mib):
+    n = mib * (1 << 20)
+    src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes": n, "launches": 5}), flush=True)
 
 
 def main():
@@ -79,13 +352,15 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama-prefill",
+                    choices=["llama-prefill", "llama-decode", "qwen-nvfp4", "moe"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=128)
+    ap.add_argument("--cpu-rows", type=int, default=T_TOKENS)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              f"(the layer shards by rows or columns without kernel changes; see the design notes)",
-              file=sys.stderr)
+              f"(the layer shards by token rows or weight columns without kernel changes)", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -95,97 +370,25 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
+    if args.calibrate_copy:
+        calibrate_copy(torch, dev, args.calibrate_copy)
+        return
 
-    def to_dev(u16):
-        return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).to(dev)
-
-    layers = []
-    for name, (K, N, norm) in synth.LLAMA_LINEARS.items():
-        xs = [to_dev(synth.activations(T_TOKENS, K, seed=s)) for s in range(N_INPUT_SETS)]
-        g = to_dev(synth.gamma(K, seed=0)) if norm else None
-        w = S.sharq_quantize_weight(to_dev(synth.weight(N, K, seed=0)))
-        acts = [S.alloc_act(T_TOKENS, K, 2, 4, "mx", dev) for _ in range(N_INPUT_SETS)]
-        ys = [torch.empty((T_TOKENS, N), dtype=torch.bfloat16, device=dev) for _ in range(N_INPUT_SETS)]
-        layers.append(dict(name=name, K=K, N=N, norm=norm, xs=xs, g=g, w=w, acts=acts, ys=ys))
-    torch.cuda.synchronize()
-    log(f"[bench] set up {len(layers)} linears, M={T_TOKENS}")
-
-    def step(i, ev=None):
-        j = i % N_INPUT_SETS
-        for li, L in enumerate(layers):
-            if ev is not None:
-                ev[li][0].record(stream)
-            S.sharq_prepare(L["xs"][j], L["g"], synth.LLAMA_EPS, 2, 4, "mx", out=L["acts"][j], stream=stream)
-            if ev is not None:
-                ev[li][1].record(stream)
-            S.sharq_linear(L["acts"][j], L["w"], out=L["ys"][j], stream=stream)
-            if ev is not None:
-                ev[li][2].record(stream)
-
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    log(f"[bench] warmup {args.warmup} done")
-
-    # timed region: exactly K steps, synchronized on both sides; per-kernel
-    # HIP events are recorded on the launch stream inside the same region
-    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in layers] for _ in range(args.steps)]
-    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    t_start.record(stream)
-    for i in range(args.steps):
-        step(i, evs[i])
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ms_total = t_start.elapsed_time(t_end)
-    ms_step = ms_total / args.steps
-    log(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step (wall {wall * 1e3 / args.steps:.4f} ms/step)")
-
-    per = []
-    flops_step = 0.0
-    t_gemm = t_prep = 0.0
-    bytes_prep = 0.0
-    for li, L in enumerate(layers):
-        prep_ms = float(np.mean([evs[i][li][0].elapsed_time(evs[i][li][1]) for i in range(args.steps)]))
-        gemm_ms = float(np.mean([evs[i][li][1].elapsed_time(evs[i][li][2]) for i in range(args.steps)]))
-        f = gemm_flops(T_TOKENS, L["N"], L["K"])
-        b = prep_bytes(T_TOKENS, L["K"], L["norm"])
-        flops_step += f
-        t_gemm += gemm_ms
-        t_prep += prep_ms
-        bytes_prep += b
-        per.append({"linear": L["name"], "K": L["K"], "N": L["N"], "rmsnorm": L["norm"],
-                    "prep_us": prep_ms * 1e3, "prep_GBps": b / (prep_ms * 1e-3) / 1e9,
-                    "gemm_us": gemm_ms * 1e3, "gemm_TFLOPs": f / (gemm_ms * 1e-3) / 1e12})
-    value = flops_step / (ms_step * 1e-3) / 1e12
-    gemm_tf = flops_step / (t_gemm * 1e-3) / 1e12
-    prep_gbps = bytes_prep / (t_prep * 1e-3) / 1e9
-    for p in per:
-        log(f"[bench] {p['linear']:8s} prep {p['prep_us']:8.2f} us {p['prep_GBps']:8.1f} GB/s | "
-            f"gemm {p['gemm_us']:8.2f} us {p['gemm_TFLOPs']:8.1f} TFLOP/s")
-
-    out = {
-        "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "mxfp4", "data": "synthetic",
-        "config": {"workload": "Llama-3.1-8B prefill linears qkv (K4096,N6144,RMSNorm), gate_up (K4096,N28672,"
-                               "RMSNorm), down (K14336,N4096); M=2048 tokens; 2:4 backbone; MXFP4; bf16 out",
-                   "tokens": T_TOKENS, "pattern": "2:4", "format": "MXFP4",
-                   "flops_per_step": flops_step, "flops_counting": "4*M*N*K per linear (two dense-executed FP4 GEMMs)"},
-        "roofline": {"bound": "mfma", "kernel": "k_linear_mx (two-path FP4 GEMM)", "achieved": gemm_tf,
-                     "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s", "frac": gemm_tf / PEAK_FP4_TFLOPS, "traffic": None},
-        "prep": {"bound": "hbm", "kernel": "k_prep_mx_* (fused preparation)", "achieved": prep_gbps,
-                 "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": prep_gbps / PEAK_HBM_GBPS},
-        "per_linear": per,
-        "wall_ms_per_step": wall * 1e3 / args.steps,
-    }
-    if not args.no_cpu_baseline:
-        log("[bench] timing the CPU oracle on a bounded sample ...")
-        out["cpu_baseline"] = cpu_baseline(args.cpu_rows)
-        log(f"[bench] cpu oracle: {out['cpu_baseline']['value']:.4f} TFLOP/s in {out['cpu_baseline']['seconds']:.1f} s")
-    print(json.dumps(out), flush=True)
+    if args.workload == "llama-prefill":
+        out = llama_prefill(args, torch, S, synth, dev, stream)
+        if not args.no_cpu_baseline:
+            log("[bench] timing the CPU oracle on a bounded sample ...")
+            out["cpu_baseline"] = cpu_baseline(args.cpu_rows)
+            log(f"[bench] cpu oracle: {out['cpu_baseline']['value']:.4f} TFLOP/s "
+                f"in {out['cpu_baseline']['seconds']:.1f} s")
+        print(json.dumps(out), flush=True)
+    elif args.workload == "llama-decode":
+        for o in llama_decode(args, torch, S, synth, dev, stream):
+            print(json.dumps(o), flush=True)
+    elif args.workload == "qwen-nvfp4":
+        print(json.dumps(qwen_nvfp4(args, torch, S, synth, dev, stream)), flush=True)
+    else:
+        print(json.dumps(moe(args, torch, S, synth, dev, stream)), flush=True)
 
 
 if __name__ == "__main__":
