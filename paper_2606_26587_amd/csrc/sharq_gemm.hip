@@ -36,37 +36,27 @@ constexpr int kLdsStride = 80;    // bytes per staged weight row (64 + 16 to spr
 // Backbone expansion: compressed 32-position block -> 32 dense E2M1 nibbles
 // ---------------------------------------------------------------------------
 
+// One output dword (8 K positions) of an expanded block.
 // 2:4: byte g of `c` holds group g's two kept codes (lower K first); nibble g
-// of `meta` holds their positions i0 | i1 << 2.
-__device__ __forceinline__ uint4 expand_24(uint2 c, uint32_t meta) {
-  uint32_t out[4];
-#pragma unroll
-  for (int d = 0; d < 4; ++d) {
-    const uint32_t cw = d < 2 ? c.x : c.y;
-    uint32_t r = 0u;
+// of `meta` holds their positions i0 | i1 << 2.  Dword D covers groups 2D, 2D+1.
+// 4:8: bytes 2g, 2g+1 of `c` hold group g's four kept codes (ascending K);
+// byte g of `meta` is its keep mask.  Dword D is group D.
+template <int PAT, int D>
+__device__ __forceinline__ uint32_t expand_dw(uint2 c, uint32_t meta) {
+  const uint32_t cw = D < 2 ? c.x : c.y;
+  uint32_t r = 0u;
+  if (PAT == 24) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int g = 2 * d + h;
+      const int g = 2 * D + h;
       const uint32_t byte = (cw >> (8 * (g & 3))) & 0xFFu;
       const uint32_t nib = (meta >> (4 * g)) & 0xFu;
       r |= (byte & 0xFu) << (4 * (nib & 3u) + 16 * h);
       r |= (byte >> 4) << (4 * (nib >> 2) + 16 * h);
     }
-    out[d] = r;
-  }
-  return make_uint4(out[0], out[1], out[2], out[3]);
-}
-
-// 4:8: bytes 2g, 2g+1 of `c` hold group g's four kept codes (ascending K);
-// byte g of `meta` is its keep mask.
-__device__ __forceinline__ uint4 expand_48(uint2 c, uint32_t meta) {
-  uint32_t out[4];
-#pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    const uint32_t cw = g < 2 ? c.x : c.y;
-    uint32_t c16 = (cw >> (16 * (g & 1))) & 0xFFFFu;
-    const uint32_t mask = (meta >> (8 * g)) & 0xFFu;
-    uint32_t r = 0u;
+  } else {
+    uint32_t c16 = (cw >> (16 * (D & 1))) & 0xFFFFu;
+    const uint32_t mask = (meta >> (8 * D)) & 0xFFu;
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
       if ((mask >> p) & 1u) {
@@ -74,15 +64,15 @@ __device__ __forceinline__ uint4 expand_48(uint2 c, uint32_t meta) {
         c16 >>= 4;
       }
     }
-    out[g] = r;
   }
-  return make_uint4(out[0], out[1], out[2], out[3]);
+  return r;
 }
 
+// A compressed 32-position block -> 32 dense E2M1 nibbles.
 template <int PAT>
 __device__ __forceinline__ uint4 expand_block(uint2 c, uint32_t meta) {
-  if (PAT == 24) return expand_24(c, meta);
-  return expand_48(c, meta);
+  return make_uint4(expand_dw<PAT, 0>(c, meta), expand_dw<PAT, 1>(c, meta), expand_dw<PAT, 2>(c, meta),
+                    expand_dw<PAT, 3>(c, meta));
 }
 
 __device__ __forceinline__ v8i as_operand(uint4 q) {
@@ -368,6 +358,302 @@ __device__ __forceinline__ void tile_mx(const uint8_t* sp_codes, const uint8_t* 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Interleaved main loop (K a multiple of 128, 256 output columns)
+// ---------------------------------------------------------------------------
+//
+// With one wavefront per SIMD the matrix core idles whenever the wavefront
+// issues anything but MFMAs, unless that work sits between MFMAs it does not
+// feed and is short enough (a wave64 VALU instruction takes 4 cycles, one
+// FP4 32x32x64 MFMA 32) to finish before the next MFMA may issue.  Each K step
+// therefore runs its 32 MFMAs as fixed slots and spreads the preparation of
+// later steps thinly between them: the weight reads of its second sub-step,
+// the expansion of the next step's backbone (one 16-bit piece, ~8 VALU, per
+// slot), the copy of its residual operand, the LDS store of the weight tile
+// two steps ahead and the reads of the next step's first weight operands.
+// The weight tile goes through three LDS stages, so the tile of step k+1 is
+// published one barrier before step k ends and its first operands are already
+// in registers when step k+1 begins.  Global loads are issued before the
+// first slot: the weights three steps ahead, the activations two steps ahead.
+// Scheduling fences keep every slot in place.
+
+struct AOps {        // MFMA-ready activation operands of one K step
+  uint4 sp[2], dn[2];
+  uint32_t ssp, sdn; // E8M0 scale dwords shifted to this lane's half
+};
+
+#define SHARQ_FENCE() __builtin_amdgcn_sched_barrier(0)
+
+constexpr int kStageW = 256 * kLdsStride;        // weight codes of one stage
+constexpr int kStageBytes = kStageW + 64 * 16;   // + the 64 scale records
+
+// Piece Q (0..15) of the next step's expanded backbone: block Q / 8, output
+// dword (Q % 8) / 2, 16-bit half Q % 2 (returned in place within the dword).
+template <int PAT, int Q>
+__device__ __forceinline__ uint32_t exp_piece(const AStep& r) {
+  constexpr int B = Q / 8, D = (Q % 8) / 2, H = Q % 2;
+  const uint2 c = r.spc[B];
+  const uint32_t meta = r.spm[B];
+  if (PAT == 24) {
+    constexpr int G = 2 * D + H;   // group of 4 positions
+    const uint32_t cw = G < 4 ? c.x : c.y;
+    const uint32_t byte = (cw >> (8 * (G & 3))) & 0xFFu;
+    const uint32_t nib = (meta >> (4 * G)) & 0xFu;
+    return ((byte & 0xFu) << (4 * (nib & 3u) + 16 * H)) | ((byte >> 4) << (4 * (nib >> 2) + 16 * H));
+  } else {
+    constexpr int G = D;           // group of 8 positions, half H of it
+    const uint32_t cw = G < 2 ? c.x : c.y;
+    uint32_t c16 = (cw >> (16 * (G & 1))) & 0xFFFFu;
+    const uint32_t mask = (meta >> (8 * G)) & 0xFFu;
+    if (H == 1) c16 >>= 4 * __builtin_popcount(mask & 0xFu);
+    uint32_t out = 0u;
+#pragma unroll
+    for (int p = 4 * H; p < 4 * H + 4; ++p) {
+      if ((mask >> p) & 1u) {
+        out |= (c16 & 0xFu) << (4 * p);
+        c16 >>= 4;
+      }
+    }
+    return out;
+  }
+}
+
+template <int PAT, int Q>
+__device__ __forceinline__ void put_piece(AOps& o, const AStep& r) {
+  constexpr int B = Q / 8, D = (Q % 8) / 2, H = Q % 2;
+  const uint32_t v = exp_piece<PAT, Q>(r);
+  uint32_t& d = D == 0 ? o.sp[B].x : D == 1 ? o.sp[B].y : D == 2 ? o.sp[B].z : o.sp[B].w;
+  d = H == 0 ? v : (d | v);
+}
+
+template <int SUB, int F>
+__device__ __forceinline__ void mma_sp(v16f (&acc)[8], const AOps& a, const uint4 (&b)[8], const uint32_t (&bw)[4]) {
+  acc[F] = mfma_fp4<SUB, (F & 1) ? 2 + SUB : SUB>(as_operand(a.sp[SUB]), as_operand(b[F]), acc[F], a.ssp,
+                                                 bw[F >> 1]);
+}
+
+template <int SUB, int F>
+__device__ __forceinline__ void mma_dn(v16f (&acc)[8], const AOps& a, const uint4 (&b)[8], const uint32_t (&bw)[4]) {
+  acc[F] = mfma_fp4<SUB, (F & 1) ? 2 + SUB : SUB>(as_operand(a.dn[SUB]), as_operand(b[F]), acc[F], a.sdn,
+                                                 bw[F >> 1]);
+}
+
+template <int SUB, int F0, int F1>
+__device__ __forceinline__ void read_b(uint4 (&b)[8], const uint8_t* lw, int lane) {
+  const int half = lane >> 5, col = lane & 31;
+#pragma unroll
+  for (int f = F0; f < F1; ++f)
+    b[f] = *reinterpret_cast<const uint4*>(lw + (f * 32 + col) * kLdsStride + 32 * half + 16 * SUB);
+}
+
+__device__ __forceinline__ void read_bw(uint32_t (&bw)[4], const uint8_t* stage, int lane) {
+  const int half = lane >> 5, col = lane & 31;
+  const uint4 q = *reinterpret_cast<const uint4*>(stage + kStageW + (2 * col + half) * 16);
+  bw[0] = q.x; bw[1] = q.y; bw[2] = q.z; bw[3] = q.w;
+}
+
+// One K step k.  In: b0 / bw = sub-step 0 weight operands and scale records
+// of step k (read from stage `cur`); ops = expanded activations of step k.
+// Out: b0 / bwn = those of step k+1 (from stage `nxt`); opsn.sp and scales =
+// expansion of raw (step k+1; its residual codes are loaded into opsn.dn by
+// `issue`); wst (step k+2) stored to stage `wr`.
+template <int PAT, class Issue>
+__device__ __forceinline__ void step5(v16f (&acc)[8], const AOps& ops, uint4 (&b0)[8], const uint32_t (&bw)[4],
+                                      uint32_t (&bwn)[4], const uint8_t* cur, const uint8_t* nxt, uint8_t* wr,
+                                      AOps& opsn, const AStep& raw, const WStep<8>& wst, int lane, Issue issue) {
+  const int half = lane >> 5, tid = threadIdx.x;
+  uint4 b1[8];
+  // LDS traffic is spread at about one instruction per slot (a 1 KB
+  // wavefront access keeps the LDS busy for several MFMA-lengths when four
+  // wavefronts burst together); VALU work stays under ~8 instructions per slot.
+  issue();
+  SHARQ_FENCE();
+  // ---- sub-step 0, backbone: second sub-step's weight operands
+  mma_sp<0, 0>(acc, ops, b0, bw); read_b<1, 0, 1>(b1, cur, lane); put_piece<PAT, 0>(opsn, raw); SHARQ_FENCE();
+  mma_sp<0, 1>(acc, ops, b0, bw); read_b<1, 1, 2>(b1, cur, lane); SHARQ_FENCE();
+  mma_sp<0, 2>(acc, ops, b0, bw); read_b<1, 2, 3>(b1, cur, lane); put_piece<PAT, 1>(opsn, raw); SHARQ_FENCE();
+  mma_sp<0, 3>(acc, ops, b0, bw); read_b<1, 3, 4>(b1, cur, lane); SHARQ_FENCE();
+  mma_sp<0, 4>(acc, ops, b0, bw); read_b<1, 4, 5>(b1, cur, lane); put_piece<PAT, 2>(opsn, raw); SHARQ_FENCE();
+  mma_sp<0, 5>(acc, ops, b0, bw); read_b<1, 5, 6>(b1, cur, lane); SHARQ_FENCE();
+  mma_sp<0, 6>(acc, ops, b0, bw); read_b<1, 6, 7>(b1, cur, lane); put_piece<PAT, 3>(opsn, raw); SHARQ_FENCE();
+  mma_sp<0, 7>(acc, ops, b0, bw); read_b<1, 7, 8>(b1, cur, lane); SHARQ_FENCE();
+  // ---- sub-step 0, residual: the weight tile two steps ahead to LDS
+  mma_dn<0, 0>(acc, ops, b0, bw); put_piece<PAT, 4>(opsn, raw); SHARQ_FENCE();
+  mma_dn<0, 1>(acc, ops, b0, bw);
+  *reinterpret_cast<uint4*>(wr + (tid >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[0];
+  SHARQ_FENCE();
+  mma_dn<0, 2>(acc, ops, b0, bw); put_piece<PAT, 5>(opsn, raw); SHARQ_FENCE();
+  mma_dn<0, 3>(acc, ops, b0, bw);
+  *reinterpret_cast<uint4*>(wr + ((tid + 256) >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[1];
+  SHARQ_FENCE();
+  mma_dn<0, 4>(acc, ops, b0, bw); put_piece<PAT, 6>(opsn, raw); SHARQ_FENCE();
+  mma_dn<0, 5>(acc, ops, b0, bw);
+  *reinterpret_cast<uint4*>(wr + ((tid + 512) >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[2];
+  SHARQ_FENCE();
+  mma_dn<0, 6>(acc, ops, b0, bw); put_piece<PAT, 7>(opsn, raw); SHARQ_FENCE();
+  mma_dn<0, 7>(acc, ops, b0, bw);
+  *reinterpret_cast<uint4*>(wr + ((tid + 768) >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[3];
+  SHARQ_FENCE();
+  // ---- sub-step 1, backbone: weight scales, then the next step's operands
+  mma_sp<1, 0>(acc, ops, b1, bw); put_piece<PAT, 8>(opsn, raw); SHARQ_FENCE();
+  mma_sp<1, 1>(acc, ops, b1, bw);
+  {
+    const int f = tid >> 5, c = tid & 31;
+    // record (c, h) byte 2 (f & 1) + sub <- block 2 h + sub of weight row 32 f + c
+    *reinterpret_cast<uint16_t*>(wr + kStageW + (2 * c + 0) * 16 + 2 * f) = (uint16_t)wst.s;
+    *reinterpret_cast<uint16_t*>(wr + kStageW + (2 * c + 1) * 16 + 2 * f) = (uint16_t)(wst.s >> 16);
+  }
+  SHARQ_FENCE();
+  mma_sp<1, 2>(acc, ops, b1, bw); put_piece<PAT, 9>(opsn, raw); SHARQ_FENCE();
+  mma_sp<1, 3>(acc, ops, b1, bw); read_b<0, 0, 1>(b0, nxt, lane); SHARQ_FENCE();
+  mma_sp<1, 4>(acc, ops, b1, bw); put_piece<PAT, 10>(opsn, raw); SHARQ_FENCE();
+  mma_sp<1, 5>(acc, ops, b1, bw); read_b<0, 1, 2>(b0, nxt, lane); SHARQ_FENCE();
+  mma_sp<1, 6>(acc, ops, b1, bw); put_piece<PAT, 11>(opsn, raw); SHARQ_FENCE();
+  mma_sp<1, 7>(acc, ops, b1, bw); read_b<0, 2, 3>(b0, nxt, lane); SHARQ_FENCE();
+  // ---- sub-step 1, residual
+  mma_dn<1, 0>(acc, ops, b1, bw); put_piece<PAT, 12>(opsn, raw); read_b<0, 3, 4>(b0, nxt, lane); SHARQ_FENCE();
+  mma_dn<1, 1>(acc, ops, b1, bw); read_b<0, 4, 5>(b0, nxt, lane); SHARQ_FENCE();
+  mma_dn<1, 2>(acc, ops, b1, bw); put_piece<PAT, 13>(opsn, raw); read_b<0, 5, 6>(b0, nxt, lane); SHARQ_FENCE();
+  mma_dn<1, 3>(acc, ops, b1, bw); read_b<0, 6, 7>(b0, nxt, lane); SHARQ_FENCE();
+  mma_dn<1, 4>(acc, ops, b1, bw); put_piece<PAT, 14>(opsn, raw); read_b<0, 7, 8>(b0, nxt, lane); SHARQ_FENCE();
+  mma_dn<1, 5>(acc, ops, b1, bw); read_bw(bwn, nxt, lane); SHARQ_FENCE();
+  mma_dn<1, 6>(acc, ops, b1, bw); put_piece<PAT, 15>(opsn, raw); SHARQ_FENCE();
+  mma_dn<1, 7>(acc, ops, b1, bw);
+  opsn.ssp = raw.ssp >> (16 * half);
+  opsn.sdn = raw.sdn >> (16 * half);
+  SHARQ_FENCE();
+}
+
+// Residual codes of step ks straight into the operand registers, and the
+// backbone codes / metadata / scales of step ks into a raw set (panel-major,
+// K a multiple of 128).
+// In this loop lane half h takes blocks 2h and 2h+1 of each 128-position
+// step (sub-step s uses block 2h + s), so a lane's bytes of every buffer are
+// contiguous: 32 bytes of residual codes, 16 of backbone codes, 8 of metadata.
+__device__ __forceinline__ void load_a_dn(AOps& o, const ARow& a, int ks, int half) {
+  const uint8_t* dn = a.dn + (int64_t)ks * a.R * 64 + a.r * 64 + 32 * half;
+  o.dn[0] = *reinterpret_cast<const uint4*>(dn);
+  o.dn[1] = *reinterpret_cast<const uint4*>(dn + 16);
+}
+
+__device__ __forceinline__ void load_a_meta(AStep& s, const ARow& a, int ks, int half) {
+  const int64_t pr = (int64_t)ks * a.R;
+  const uint4 c = *reinterpret_cast<const uint4*>(a.spc + pr * 32 + a.r * 32 + 16 * half);
+  const uint2 m = *reinterpret_cast<const uint2*>(a.spm + pr * 16 + a.r * 16 + 8 * half);
+  s.spc[0] = make_uint2(c.x, c.y);
+  s.spc[1] = make_uint2(c.z, c.w);
+  s.spm[0] = m.x;
+  s.spm[1] = m.y;
+  s.sdn = *reinterpret_cast<const uint32_t*>(a.dns + pr * 4 + a.r * 4);
+  s.ssp = *reinterpret_cast<const uint32_t*>(a.sps + pr * 4 + a.r * 4);
+}
+
+
+__device__ __forceinline__ void store_w_stage(const WStep<8>& w, uint8_t* stage) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c = tid + 256 * j;
+    *reinterpret_cast<uint4*>(stage + (c >> 2) * kLdsStride + 16 * (c & 3)) = w.q[j];
+  }
+  const int f = tid >> 5, c = tid & 31;
+  *reinterpret_cast<uint16_t*>(stage + kStageW + (2 * c + 0) * 16 + 2 * f) = (uint16_t)w.s;
+  *reinterpret_cast<uint16_t*>(stage + kStageW + (2 * c + 1) * 16 + 2 * f) = (uint16_t)(w.s >> 16);
+}
+
+template <int PAT, typename OutT>
+__device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale,
+                                           const uint8_t* dn_codes, const uint8_t* dn_scale, const int32_t* row_index,
+                                           int64_t act_rows, int64_t row_lo, int64_t row_hi, const uint8_t* wc,
+                                           const uint8_t* ws, int n0, int N, int K, OutT* Y, int64_t ldy,
+                                           uint8_t* lds) {
+  constexpr int NF = 8;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
+  const int nblk = K / 32, nks = K / kBK;
+
+  int64_t orow = row_lo + wave * 32 + (lane & 31);
+  if (orow >= row_hi) orow = row_hi - 1;   // clamp: loads stay in bounds, stores are masked
+  ARow a;
+  a.r = row_index ? (int64_t)row_index[orow] : orow;
+  a.R = act_rows;
+  a.dn = dn_codes;
+  a.spc = sp_codes;
+  a.spm = sp_meta;
+  a.dns = dn_scale;
+  a.sps = sp_scale;
+
+  v16f acc[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[f][r] = 0.0f;
+
+  // Register sets alternate with the parity of the step (the loop is
+  // unrolled by two); LDS stages rotate through three buffers.  Loads past
+  // the last step re-read it (clamped) and their results are never used.
+  const int last = nks - 1;
+  AStep r0, r1;
+  WStep<NF> w0, w1;
+  AOps o0, o1;
+  uint4 b0[8];
+  uint32_t bwa[4], bwb[4];
+  uint8_t* st0 = lds;
+  uint8_t* st1 = lds + kStageBytes;
+  uint8_t* st2 = lds + 2 * kStageBytes;
+  load_w<NF, true>(w0, wc, ws, n0, N, K, 0, nblk);
+  load_a_meta(r0, a, 0, half);
+  load_a_dn(o0, a, 0, half);
+  load_w<NF, true>(w1, wc, ws, n0, N, K, min(1, last), nblk);
+  load_a_meta(r1, a, min(1, last), half);
+  store_w_stage(w0, st0);
+  store_w_stage(w1, st1);
+  o0.sp[0] = expand_block<PAT>(r0.spc[0], r0.spm[0]);
+  o0.sp[1] = expand_block<PAT>(r0.spc[1], r0.spm[1]);
+  o0.ssp = r0.ssp >> (16 * half);
+  o0.sdn = r0.sdn >> (16 * half);
+  load_w<NF, true>(w0, wc, ws, n0, N, K, min(2, last), nblk);
+  __syncthreads();
+  read_bw(bwa, st0, lane);
+  read_b<0, 0, 8>(b0, st0, lane);
+
+  // invariant at step k: stages (k, k+1) hold W(k), W(k+1); b0 / bw hold
+  // step k's first operands; o[k%2] = A(k); r[(k+1)%2] = raw A(k+1);
+  // w[k%2] = raw W(k+2)
+  int ks = 0;
+  for (; ks + 1 < nks; ks += 2) {
+    step5<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w0, lane, [&] {
+      load_w<NF, true>(w1, wc, ws, n0, N, K, min(ks + 3, last), nblk);
+      load_a_meta(r0, a, min(ks + 2, last), half);
+      load_a_dn(o1, a, ks + 1, half);
+    });
+    __syncthreads();
+    step5<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o0, r0, w1, lane, [&] {
+      load_w<NF, true>(w0, wc, ws, n0, N, K, min(ks + 4, last), nblk);
+      load_a_meta(r1, a, min(ks + 3, last), half);
+      load_a_dn(o0, a, min(ks + 2, last), half);
+    });
+    __syncthreads();
+    uint8_t* t = st0;   // rotate the stages by two
+    st0 = st2;
+    st2 = st1;
+    st1 = t;
+  }
+  if (ks < nks) {   // odd number of steps: the last one uses set 0
+    step5<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w0, lane, [] {});
+  }
+
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int col = n0 + f * 32 + (lane & 31);
+    if (col >= N) continue;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t row = row_lo + wave * 32 + 8 * (r / 4) + 4 * half + (r % 4);
+      if (row < row_hi) store_out<OutT>(Y + row * ldy + col, acc[f][r]);
+    }
+  }
+}
+
 // Tile order.  Workgroups are dispatched round-robin over the 8 XCDs
 // (workgroup id mod 8), each with its own L2.  The ids are renumbered so that
 // each XCD walks a contiguous range of tiles, ordered in blocks of 4 M-tiles
@@ -395,15 +681,21 @@ __global__ __launch_bounds__(256) void k_linear_mx(const uint8_t* sp_codes, cons
                                                    const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy, int gx,
                                                    int gy) {
   constexpr int BN = 32 * NF;
-  __shared__ __attribute__((aligned(16))) uint8_t lds_w[2 * BN * kLdsStride];
-  __shared__ __attribute__((aligned(16))) uint8_t lds_s[2 * 64 * 2 * NF];
+  constexpr int kOld = 2 * BN * kLdsStride + 2 * 64 * 2 * NF;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kOld > 3 * kStageBytes ? kOld : 3 * kStageBytes];
+  uint8_t* lds_w = lds;
+  uint8_t* lds_s = lds + 2 * BN * kLdsStride;
   int mt, nt;
   tile_of(blockIdx.x, gx, gy, mt, nt);
   const int n0 = nt * BN;
   const int64_t m0 = (int64_t)mt * kBM;
   const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
-  tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws, n0,
-                                   N, K, Y, ldy, lds_w, lds_s);
+  if constexpr (SCALE_DW && NF == 8)
+    tile_mx_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws, n0, N, K, Y,
+                          ldy, lds);
+  else
+    tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws, n0,
+                                     N, K, Y, ldy, lds_w, lds_s);
 }
 
 // Grouped (MoE) form.  Work item y of the grid is a 128-row tile of one
@@ -417,8 +709,10 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
     const uint8_t* dn_scale, const int32_t* row_index, int64_t act_rows, const int32_t* offs, int E,
     const uint8_t* wc, const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy) {
   constexpr int BN = 32 * NF;
-  __shared__ __attribute__((aligned(16))) uint8_t lds_w[2 * BN * kLdsStride];
-  __shared__ __attribute__((aligned(16))) uint8_t lds_s[2 * 64 * 2 * NF];
+  constexpr int kOld = 2 * BN * kLdsStride + 2 * 64 * 2 * NF;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kOld > 3 * kStageBytes ? kOld : 3 * kStageBytes];
+  uint8_t* lds_w = lds;
+  uint8_t* lds_s = lds + 2 * BN * kLdsStride;
   __shared__ int s_first[1025];
   const int tid = threadIdx.x;
   // tiles per expert, then an inclusive scan (Hillis-Steele) over <= 1024 experts
@@ -457,8 +751,12 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
   const int n0 = blockIdx.x * BN;
   const uint8_t* wce = wc + (int64_t)e * N * (K / 2);
   const uint8_t* wse = ws + (int64_t)e * N * (K / 32);
-  tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, act_rows, r0, r1,
-                                   wce, wse, n0, N, K, Y, ldy, lds_w, lds_s);
+  if constexpr (SCALE_DW && NF == 8)
+    tile_mx_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, act_rows, r0, r1, wce, wse, n0,
+                          N, K, Y, ldy, lds);
+  else
+    tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, act_rows, r0, r1,
+                                     wce, wse, n0, N, K, Y, ldy, lds_w, lds_s);
 }
 
 // ---------------------------------------------------------------------------
