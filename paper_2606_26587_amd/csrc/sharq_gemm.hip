@@ -426,17 +426,50 @@ __device__ __forceinline__ void put_piece(AOps& o, const AStep& r) {
   d = H == 0 ? v : (d | v);
 }
 
+// The weight is the MFMA's first operand and the activation its second, so
+// the accumulator is the transposed tile: lane l holds activation row
+// l % 32 and, in element r, output column 8 (r / 4) + 4 (l / 32) + r % 4 of
+// the fragment -- four consecutive columns per group of four elements.
 template <int SUB, int F>
 __device__ __forceinline__ void mma_sp(v16f (&acc)[8], const AOps& a, const uint4 (&b)[8], const uint32_t (&bw)[4]) {
-  acc[F] = mfma_fp4<SUB, (F & 1) ? 2 + SUB : SUB>(as_operand(a.sp[SUB]), as_operand(b[F]), acc[F], a.ssp,
-                                                 bw[F >> 1]);
+  acc[F] = mfma_fp4<(F & 1) ? 2 + SUB : SUB, SUB>(as_operand(b[F]), as_operand(a.sp[SUB]), acc[F], bw[F >> 1],
+                                                 a.ssp);
 }
 
 template <int SUB, int F>
 __device__ __forceinline__ void mma_dn(v16f (&acc)[8], const AOps& a, const uint4 (&b)[8], const uint32_t (&bw)[4]) {
-  acc[F] = mfma_fp4<SUB, (F & 1) ? 2 + SUB : SUB>(as_operand(a.dn[SUB]), as_operand(b[F]), acc[F], a.sdn,
-                                                 bw[F >> 1]);
+  acc[F] = mfma_fp4<(F & 1) ? 2 + SUB : SUB, SUB>(as_operand(b[F]), as_operand(a.dn[SUB]), acc[F], bw[F >> 1],
+                                                 a.sdn);
 }
+
+template <typename OutT>
+struct Vec4Out;
+template <>
+struct Vec4Out<float> {
+  static __device__ __forceinline__ void put(float* p, float a, float b, float c, float d) {
+    *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+  }
+  static constexpr int kAlign = 16;
+};
+template <>
+struct Vec4Out<uint16_t> {
+  static __device__ __forceinline__ void put(uint16_t* p, float a, float b, float c, float d) {
+    const uint32_t lo = (uint32_t)f32_to_bf16_rne(a) | ((uint32_t)f32_to_bf16_rne(b) << 16);
+    const uint32_t hi = (uint32_t)f32_to_bf16_rne(c) | ((uint32_t)f32_to_bf16_rne(d) << 16);
+    *reinterpret_cast<uint2*>(p) = make_uint2(lo, hi);
+  }
+  static constexpr int kAlign = 8;
+};
+template <>
+struct Vec4Out<_Float16> {
+  static __device__ __forceinline__ void put(_Float16* p, float a, float b, float c, float d) {
+    typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+    h4 v;
+    v[0] = (_Float16)a; v[1] = (_Float16)b; v[2] = (_Float16)c; v[3] = (_Float16)d;
+    *reinterpret_cast<h4*>(p) = v;
+  }
+  static constexpr int kAlign = 8;
+};
 
 template <int SUB, int F0, int F1>
 __device__ __forceinline__ void read_b(uint4 (&b)[8], const uint8_t* lw, int lane) {
@@ -588,68 +621,95 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[f][r] = 0.0f;
 
-  // Register sets alternate with the parity of the step (the loop is
-  // unrolled by two); LDS stages rotate through three buffers.  Loads past
-  // the last step re-read it (clamped) and their results are never used.
+  // Register sets rotate with period three, so the loop is unrolled by
+  // three and the LDS stages are fixed per unrolled step.  Invariant at the
+  // start of step k (sets indexed by k mod 3): stages k, k+1 hold W(k),
+  // W(k+1); b0 / bw hold step k's first weight operands; o[k] is complete;
+  // o[k+1].dn = residual codes of step k+1 (in flight); r[k+1], r[k+2] = raw
+  // backbone data of steps k+1, k+2; w[k+2], w[k] = raw W(k+2), W(k+3).
+  // Step k loads the residual codes of step k+2, the raw backbone of step k+3
+  // and W(k+4): every load has two full steps to arrive.  Loads past the last
+  // step re-read it (clamped) and their results are never used.
   const int last = nks - 1;
-  AStep r0, r1;
-  WStep<NF> w0, w1;
-  AOps o0, o1;
+  AStep r0, r1, r2;
+  WStep<NF> w0, w1, w2;
+  AOps o0, o1, o2;
   uint4 b0[8];
   uint32_t bwa[4], bwb[4];
-  uint8_t* st0 = lds;
-  uint8_t* st1 = lds + kStageBytes;
-  uint8_t* st2 = lds + 2 * kStageBytes;
+  uint8_t* const st0 = lds;
+  uint8_t* const st1 = lds + kStageBytes;
+  uint8_t* const st2 = lds + 2 * kStageBytes;
+  const auto cl = [&](int k) { return k < last ? k : last; };
   load_w<NF, true>(w0, wc, ws, n0, N, K, 0, nblk);
   load_a_meta(r0, a, 0, half);
   load_a_dn(o0, a, 0, half);
-  load_w<NF, true>(w1, wc, ws, n0, N, K, min(1, last), nblk);
-  load_a_meta(r1, a, min(1, last), half);
+  load_w<NF, true>(w1, wc, ws, n0, N, K, cl(1), nblk);
   store_w_stage(w0, st0);
   store_w_stage(w1, st1);
   o0.sp[0] = expand_block<PAT>(r0.spc[0], r0.spm[0]);
   o0.sp[1] = expand_block<PAT>(r0.spc[1], r0.spm[1]);
   o0.ssp = r0.ssp >> (16 * half);
   o0.sdn = r0.sdn >> (16 * half);
-  load_w<NF, true>(w0, wc, ws, n0, N, K, min(2, last), nblk);
+  load_a_dn(o1, a, cl(1), half);
+  load_a_meta(r1, a, cl(1), half);
+  load_a_meta(r2, a, cl(2), half);
+  load_w<NF, true>(w2, wc, ws, n0, N, K, cl(2), nblk);
+  load_w<NF, true>(w0, wc, ws, n0, N, K, cl(3), nblk);
   __syncthreads();
   read_bw(bwa, st0, lane);
   read_b<0, 0, 8>(b0, st0, lane);
 
-  // invariant at step k: stages (k, k+1) hold W(k), W(k+1); b0 / bw hold
-  // step k's first operands; o[k%2] = A(k); r[(k+1)%2] = raw A(k+1);
-  // w[k%2] = raw W(k+2)
   int ks = 0;
-  for (; ks + 1 < nks; ks += 2) {
-    step5<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w0, lane, [&] {
-      load_w<NF, true>(w1, wc, ws, n0, N, K, min(ks + 3, last), nblk);
-      load_a_meta(r0, a, min(ks + 2, last), half);
-      load_a_dn(o1, a, ks + 1, half);
+  for (; ks + 2 < nks; ks += 3) {
+    step5<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [&] {
+      load_a_dn(o2, a, cl(ks + 2), half);
+      load_a_meta(r0, a, cl(ks + 3), half);
+      load_w<NF, true>(w1, wc, ws, n0, N, K, cl(ks + 4), nblk);
     });
     __syncthreads();
-    step5<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o0, r0, w1, lane, [&] {
-      load_w<NF, true>(w0, wc, ws, n0, N, K, min(ks + 4, last), nblk);
-      load_a_meta(r1, a, min(ks + 3, last), half);
-      load_a_dn(o0, a, min(ks + 2, last), half);
+    step5<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [&] {
+      load_a_dn(o0, a, cl(ks + 3), half);
+      load_a_meta(r1, a, cl(ks + 4), half);
+      load_w<NF, true>(w2, wc, ws, n0, N, K, cl(ks + 5), nblk);
     });
     __syncthreads();
-    uint8_t* t = st0;   // rotate the stages by two
-    st0 = st2;
-    st2 = st1;
-    st1 = t;
+    step5<PAT>(acc, o2, b0, bwa, bwb, st2, st0, st1, o0, r0, w1, lane, [&] {
+      load_a_dn(o1, a, cl(ks + 4), half);
+      load_a_meta(r2, a, cl(ks + 5), half);
+      load_w<NF, true>(w0, wc, ws, n0, N, K, cl(ks + 6), nblk);
+    });
+    __syncthreads();
+    // bw alternates with period two: after three steps the roles swap
+    uint32_t t[4] = {bwa[0], bwa[1], bwa[2], bwa[3]};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { bwa[i] = bwb[i]; bwb[i] = t[i]; }
   }
-  if (ks < nks) {   // odd number of steps: the last one uses set 0
-    step5<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w0, lane, [] {});
+  if (ks < nks) {   // one or two steps left, in sets 0 and 1
+    step5<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [] {});
+    if (ks + 1 < nks) {
+      __syncthreads();
+      step5<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [] {});
+    }
   }
 
+  // Epilogue: this lane's output row, four consecutive columns per store.
+  const int64_t row = row_lo + wave * 32 + (lane & 31);
+  if (row >= row_hi) return;
+  OutT* yr = Y + row * ldy;
+  const bool vec = ((reinterpret_cast<uintptr_t>(Y) | (uintptr_t)(ldy * (int64_t)sizeof(OutT))) &
+                    (uintptr_t)(Vec4Out<OutT>::kAlign - 1)) == 0;
 #pragma unroll
   for (int f = 0; f < NF; ++f) {
-    const int col = n0 + f * 32 + (lane & 31);
-    if (col >= N) continue;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int64_t row = row_lo + wave * 32 + 8 * (r / 4) + 4 * half + (r % 4);
-      if (row < row_hi) store_out<OutT>(Y + row * ldy + col, acc[f][r]);
+    for (int g = 0; g < 4; ++g) {
+      const int col = n0 + f * 32 + 8 * g + 4 * half;
+      if (vec && col + 3 < N) {
+        Vec4Out<OutT>::put(yr + col, acc[f][4 * g], acc[f][4 * g + 1], acc[f][4 * g + 2], acc[f][4 * g + 3]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (col + e < N) store_out<OutT>(yr + col + e, acc[f][4 * g + e]);
+      }
     }
   }
 }
