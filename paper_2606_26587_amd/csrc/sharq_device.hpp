@@ -128,8 +128,11 @@ struct NvQ {
 // Eight consecutive values -> one dword of E2M1 codes under quantizer qz.
 template <class Q>
 __device__ __forceinline__ uint32_t enc8(const float* v, const Q& qz) {
-  uint32_t t = 0u;
-  t = fp4x2<0>(t, qz.enc(v[0]), qz.enc(v[1]));
+  const float e0 = qz.enc(v[0]);
+  // bytes 1-3 are written below, so the first conversion may start from any
+  // register (e0's, which is dead after it)
+  uint32_t t = __float_as_uint(e0);
+  t = fp4x2<0>(t, e0, qz.enc(v[1]));
   t = fp4x2<1>(t, qz.enc(v[2]), qz.enc(v[3]));
   t = fp4x2<2>(t, qz.enc(v[4]), qz.enc(v[5]));
   t = fp4x2<3>(t, qz.enc(v[6]), qz.enc(v[7]));

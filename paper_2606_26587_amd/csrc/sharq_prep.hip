@@ -33,18 +33,22 @@ namespace sharq {
 // N:M selection inside one block
 // ---------------------------------------------------------------------------
 
-// 2:4 on one group: keep bits of positions 0..3 (exactly two set).
-__device__ __forceinline__ void top2of4(float y0, float y1, float y2, float y3, bool& k0, bool& k1,
-                                        bool& k2, bool& k3) {
-  float a0 = fabsf(y0), a1 = fabsf(y1), a2 = fabsf(y2), a3 = fabsf(y3);
-  // cij: position i wins against position j (i < j; a tie goes to i)
-  int c01 = a0 >= a1, c02 = a0 >= a2, c03 = a0 >= a3;
-  int c12 = a1 >= a2, c13 = a1 >= a3, c23 = a2 >= a3;
-  // position p is kept iff it wins at least 2 of its 3 comparisons
-  k0 = (c01 + c02 + c03) >= 2;
-  k1 = ((1 - c01) + c12 + c13) >= 2;
-  k2 = ((1 - c02) + (1 - c12) + c23) >= 2;
-  k3 = ((1 - c03) + (1 - c13) + (1 - c23)) >= 2;
+// Smallest float above a non-negative finite a (FLT_MAX -> +inf).
+__device__ __forceinline__ float next_up(float a) { return __uint_as_float(__float_as_uint(a) + 1u); }
+
+// 2:4 on one group: keep bits of positions 0..3 (exactly two set).  Position
+// p is kept iff it beats at least two of the other three, a tie going to the
+// lower index -- i.e. iff |y_p| is at least the median of the other three
+// magnitudes, where a lower-index rival q (which wins ties) enters as the
+// next float above |y_q|.  One med3 and one compare per position.
+__device__ __forceinline__ void top2of4(float y0, float y1, float y2, float y3, bool& k0, bool& k1, bool& k2,
+                                        bool& k3) {
+  const float a0 = fabsf(y0), a1 = fabsf(y1), a2 = fabsf(y2), a3 = fabsf(y3);
+  const float u0 = next_up(a0), u1 = next_up(a1), u2 = next_up(a2);
+  k0 = a0 >= __builtin_amdgcn_fmed3f(a1, a2, a3);
+  k1 = a1 >= __builtin_amdgcn_fmed3f(u0, a2, a3);
+  k2 = a2 >= __builtin_amdgcn_fmed3f(u0, u1, a3);
+  k3 = a3 >= __builtin_amdgcn_fmed3f(u0, u1, u2);
 }
 
 template <int SEL>
@@ -70,29 +74,37 @@ __device__ __forceinline__ v2f get_pair_dyn(uint32_t word, int sel) {
   }
 }
 
-// Backbone of one block for the 2:4 pattern.  Returns the residual in R.
+// Backbone of one block for the 2:4 pattern.  Returns the residual in R:
+// y minus the dequantized code at kept positions, y elsewhere.
 template <class Q>
 __device__ __forceinline__ void backbone_24(const float (&y)[32], const Q& qz, uint32_t (&codes)[2], uint32_t& meta,
                                             float (&R)[32]) {
   codes[0] = codes[1] = 0u;
   meta = 0u;
+  // groups from the last to the first so the metadata is shifted in four
+  // bits at a time (small select constants stay inline)
 #pragma unroll
-  for (int g = 0; g < 8; ++g) {
-    float y0 = y[4 * g], y1 = y[4 * g + 1], y2 = y[4 * g + 2], y3 = y[4 * g + 3];
+  for (int g = 7; g >= 0; --g) {
+    const float y0 = y[4 * g], y1 = y[4 * g + 1], y2 = y[4 * g + 2], y3 = y[4 * g + 3];
     bool k0, k1, k2, k3;
     top2of4(y0, y1, y2, y3, k0, k1, k2, k3);
-    float v0 = k0 ? y0 : (k1 ? y1 : y2);            // first kept (ascending K)
-    float v1 = k3 ? y3 : (k2 ? y2 : y1);            // second kept
-    uint32_t i0 = k0 ? 0u : (k1 ? 1u : 2u);
-    uint32_t i1 = k3 ? 3u : (k2 ? 2u : 1u);
-    meta |= (i0 | (i1 << 2)) << (4 * g);
-    put_pair_dyn(codes[g >> 2], g, qz.enc(v0), qz.enc(v1));
-    v2f d = get_pair_dyn(codes[g >> 2], g);
-    float d0 = qz.dec(d.x), d1 = qz.dec(d.y);
-    R[4 * g + 0] = y0 - (k0 ? d0 : 0.0f);
-    R[4 * g + 1] = y1 - (k1 ? (k0 ? d1 : d0) : 0.0f);
-    R[4 * g + 2] = y2 - (k2 ? (k3 ? d0 : d1) : 0.0f);
-    R[4 * g + 3] = y3 - (k3 ? d1 : 0.0f);
+    const float v0 = k0 ? y0 : (k1 ? y1 : y2);            // first kept (ascending K)
+    const float v1 = k3 ? y3 : (k2 ? y2 : y1);            // second kept
+    uint32_t nib = (k0 ? 0u : (k1 ? 1u : 2u)) | (k3 ? 12u : (k2 ? 8u : 4u));
+    asm("" : "+v"(nib));   // keep the nibble a register value: folding the
+                           // shift into the select constants costs moves
+    meta = (meta << 4) | nib;
+    const float e0 = qz.enc(v0), e1 = qz.enc(v1);
+    // the other bytes of a codes dword are written by the groups that follow
+    // in this loop, so the dword's first group may start from any register
+    if ((g & 3) == 3) codes[g >> 2] = __float_as_uint(e0);
+    put_pair_dyn(codes[g >> 2], g, e0, e1);
+    const v2f d = get_pair_dyn(codes[g >> 2], g);
+    const float r0 = v0 - qz.dec(d.x), r1 = v1 - qz.dec(d.y);
+    R[4 * g + 0] = k0 ? r0 : y0;
+    R[4 * g + 1] = k1 ? (k0 ? r1 : r0) : y1;
+    R[4 * g + 2] = k2 ? (k3 ? r0 : r1) : y2;
+    R[4 * g + 3] = k3 ? r1 : y3;
   }
 }
 
@@ -259,18 +271,29 @@ struct BlockOut {
   uint8_t *spc, *spm, *sps, *dnc, *dns;
 };
 
+// Panel-major order is block-major order: block b of a row is block number
+// V = 4 M p + row (wp / 32) + j (p = b / 4, j = b % 4, wp = panel width), and
+// every buffer holds its bytes for block V at V times its bytes per block.
+__device__ __forceinline__ int64_t block_index(int64_t M, int K, int64_t row, int b) {
+  const int p = b >> 2, j = b & 3;
+  const int wp = min(128, K - 128 * p);
+  return (int64_t)p * M * 4 + row * (wp / 32) + j;
+}
+
+template <bool NV>
+__device__ __forceinline__ BlockOut block_at(const ActOut& o, int64_t V) {
+  BlockOut r;
+  r.dnc = o.dnc + V * 16;
+  r.spc = o.spc + V * 8;
+  r.spm = o.spm + V * 4;
+  r.sps = o.sps + V;
+  r.dns = o.dns + (NV ? V * 2 : V);
+  return r;
+}
+
 template <bool NV>
 __device__ __forceinline__ BlockOut block_out(const ActOut& o, int64_t row, int b) {
-  const int p = b >> 2, j = b & 3;
-  const int wp = min(128, o.K - 128 * p);   // panel width in K positions
-  const int64_t pm = (int64_t)p * o.M;
-  BlockOut r;
-  r.dnc = o.dnc + pm * 64 + row * (wp / 2) + 16 * j;
-  r.spc = o.spc + pm * 32 + row * (wp / 4) + 8 * j;
-  r.spm = o.spm + pm * 16 + row * (wp / 8) + 4 * j;
-  r.sps = o.sps + pm * 4 + row * (wp / 32) + j;
-  r.dns = NV ? o.dns + pm * 8 + row * (wp / 16) + 2 * j : o.dns + pm * 4 + row * (wp / 32) + j;
-  return r;
+  return block_at<NV>(o, block_index(o.M, o.K, row, b));
 }
 
 template <int PAT, bool NV>
@@ -378,6 +401,106 @@ __global__ __launch_bounds__(256) void k_prep_plain(const uint16_t* __restrict__
   }
 }
 
+// RMSNorm variant with C wavefronts per row (C = 1, 2, 4; K <= 64 C blocks):
+// wavefront c owns blocks 64 c + lane, so each lane holds one block.  Each
+// wavefront reduces its 2048-position chunk with the in-lane tree and the
+// lane butterfly; the C chunk sums meet in LDS and are added pairwise -- the
+// same balanced tree as the one-wavefront-per-row kernel.  Workgroup w
+// handles row groups w, w + G, ... (G = grid size), loading the next group's
+// rows before quantizing the current one.
+template <int C, int PAT, bool NV>
+__global__ __launch_bounds__(256) void k_prep_norm_split(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
+                                                         const uint16_t* __restrict__ gamma, float eps, ActOut o,
+                                                         const float* S_ptr) {
+  __shared__ float part[2][4];
+  constexpr int RPG = 4 / C;   // rows per group (one group per workgroup pass)
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nblk = K / 32, b = (wave % C) * 64 + lane;
+  const int groups = (M + RPG - 1) / RPG;
+  const float S = NV ? *S_ptr : 1.0f, six_s = 6.0f * S;
+  const uint4* gr = reinterpret_cast<const uint4*>(gamma);
+
+  auto load = [&](int grp, uint4 (&q)[4]) {
+    int64_t row = (int64_t)grp * RPG + wave / C;
+    if (row >= M) row = M - 1;   // loads stay in bounds
+    const uint4* xr = reinterpret_cast<const uint4*>(X + row * ldx);
+    if (b < nblk) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) q[j] = xr[4 * b + j];
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) q[j] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+
+  uint4 xq[4], xn[4];
+  int grp = blockIdx.x;
+  if (grp < groups) load(grp, xq);
+  for (int it = 0; grp < groups; grp += gridDim.x, ++it) {
+    const int nxt = grp + gridDim.x;
+    if (nxt < groups) load(nxt, xn);
+    float x[32];
+    unpack_bf16x32(xq, x);
+    const float cs = wave_tree_sum(block_sum_sq(x));
+    float total = cs;
+    if (C > 1) {
+      // two alternating slots: a wavefront may write the next pass's sums
+      // while a slower one still reads this pass's
+      if (lane == 0) part[it & 1][wave] = cs;
+      __syncthreads();
+      const int base = (wave / C) * C;
+      const float* pp = part[it & 1];
+      if (C == 2) total = pp[base] + pp[base + 1];
+      else total = (pp[base] + pp[base + 1]) + (pp[base + 2] + pp[base + 3]);
+    }
+    const float r = (float)(1.0 / __builtin_sqrt((double)total / (double)K + (double)eps));
+    const int64_t row = (int64_t)grp * RPG + wave / C;
+    if (row < M && b < nblk) {
+      float y[32];
+      norm_block(xq, gr, b, r, y);
+      block_out_write<PAT, NV>(y, o, row, b, S, six_s);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) xq[j] = xn[j];
+  }
+}
+
+// Variant without RMSNorm: every block is independent, one thread per block.
+// Grid (x, y) = (threads over one panel's blocks, panel): thread t of panel
+// p takes block number V = 4 M p + t of the panel-major order, so
+// consecutive threads write consecutive bytes of every output buffer (and
+// read 256-byte row pieces of X).  The last panel may hold q < 4 blocks per
+// row.
+template <int PAT, bool NV>
+__global__ __launch_bounds__(256) void k_prep_blocks(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
+                                                     ActOut o, const float* S_ptr) {
+  const int nblk = K / 32, p = blockIdx.y;
+  const int q = min(4, nblk - 4 * p);      // blocks per row in this panel
+  const uint32_t t = blockIdx.x * 256u + threadIdx.x;
+  if (t >= (uint32_t)q * (uint32_t)M) return;
+  uint32_t row, j;
+  if (q == 4) {
+    row = t >> 2;
+    j = t & 3u;
+  } else {
+    row = t / (uint32_t)q;
+    j = t - row * (uint32_t)q;
+  }
+  const int b = 4 * p + (int)j;
+  const float S = NV ? *S_ptr : 1.0f, six_s = 6.0f * S;
+  const uint4* xr = reinterpret_cast<const uint4*>(X + (int64_t)row * ldx);
+  uint4 xq[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) xq[i] = xr[4 * b + i];
+  float y[32];
+  unpack_bf16x32(xq, y);
+  const BlockOut d = block_at<NV>(o, (int64_t)p * M * 4 + t);
+  if (NV)
+    block_nv<PAT>(y, S, six_s, d.spc, d.spm, d.sps, d.dnc, d.dns);
+  else
+    block_mx<PAT>(y, d.spc, d.spm, d.sps, d.dnc, d.dns);
+}
+
 // ---------------------------------------------------------------------------
 // NVFP4 per-tensor scale (App. A.1.3): S = amax(y) / 2688 over the whole call,
 // 1 for an all-zero tensor.  The running maximum is kept as the bit pattern
@@ -441,12 +564,29 @@ __global__ __launch_bounds__(256) void k_amax_plain(const uint16_t* __restrict__
 // Host-side launchers (called from the C ABI after validation)
 // ---------------------------------------------------------------------------
 
+// Workgroups of the RMSNorm kernel.  Measured at M = 2048: one row group per
+// workgroup is fastest (walking 2 or 4 groups per workgroup with a prefetch
+// was slower), so workgroups only iterate beyond 16 per CU.
+constexpr int kPersistWG = 4096;
+
 template <int PAT, bool NV>
 static void go_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps, const ActOut& o,
                     const float* S_ptr, dim3 grid, hipStream_t st) {
   dim3 block(256);
+  const int nblk = K / 32;
   if (gamma == nullptr) {
-    k_prep_plain<PAT, NV><<<grid, block, 0, st>>>(X, M, K, ldx, o, S_ptr);
+    const dim3 g2((unsigned)((4 * (int64_t)M + 255) / 256), (unsigned)((nblk + 3) / 4));
+    k_prep_blocks<PAT, NV><<<g2, block, 0, st>>>(X, M, K, ldx, o, S_ptr);
+    return;
+  }
+  if (nblk <= 256) {
+    // persistent: at most kPersistWG workgroups, each walking row groups
+    const int C = nblk <= 64 ? 1 : (nblk <= 128 ? 2 : 4);
+    const int groups = (M + 4 / C - 1) / (4 / C);
+    const dim3 g1((unsigned)(groups < kPersistWG ? groups : kPersistWG));
+    if (C == 1) k_prep_norm_split<1, PAT, NV><<<g1, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
+    else if (C == 2) k_prep_norm_split<2, PAT, NV><<<g1, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
+    else k_prep_norm_split<4, PAT, NV><<<g1, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
     return;
   }
   const int chunks = (K / 32 + 63) / 64;
