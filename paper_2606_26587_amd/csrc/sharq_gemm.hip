@@ -31,6 +31,7 @@ namespace sharq {
 constexpr int kBM = 128;          // tile rows: 4 wavefronts x 32
 constexpr int kBK = 128;          // K per step: 4 scale blocks, 64 bytes of codes per row
 constexpr int kLdsStride = 80;    // bytes per staged weight row (64 + 16 to spread LDS banks)
+constexpr int kSkinnyMaxM = 64;   // activation rows up to which the small-M kernel runs
 
 // ---------------------------------------------------------------------------
 // Backbone expansion: compressed 32-position block -> 32 dense E2M1 nibbles
@@ -820,6 +821,193 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
 }
 
 // ---------------------------------------------------------------------------
+// Small-M (decode) MXFP4 GEMM
+// ---------------------------------------------------------------------------
+//
+// With few activation rows the layer streams its weight from HBM and the
+// prefill tile (128 x 256 outputs) leaves most CUs idle.  Here a workgroup
+// owns 16 NB output columns and all M <= 16 MF rows, on the FP4 MFMA
+// v_mfma_scale_f32_16x16x128_f8f6f4 (lane l holds row / column l % 16 and
+// the 32 K values of block l / 16 of a 128-position panel; accumulator
+// element r of lane l is row 4 (l / 16) + r, column l % 16).  Its KS
+// wavefronts split K into KS ranges; each streams its weight slice straight
+// from HBM into MFMA operands (1 KB loads per panel, coalesced by the
+// panel-major layout) with a two-deep register prefetch, expands each
+// activation block once for all NB column fragments, and the KS partial
+// tiles are added in LDS in a fixed order.
+
+typedef float v4f_t __attribute__((ext_vector_type(4)));
+
+template <int MF, int NB>
+struct SkinnyStage {
+  uint4 w[NB];             // weight codes: column 16 n + l % 16, block l / 16
+  uint32_t ws[NB];         // their E8M0 scales (bytes)
+  uint4 dn[MF];            // residual codes of row 16 m + l % 16, block l / 16
+  uint2 spc[MF];           // backbone codes and metadata of the same block
+  uint32_t spm[MF];
+  uint32_t sdn[MF], ssp[MF];
+};
+
+template <int MF, int NB>
+__device__ __forceinline__ void skinny_load(SkinnyStage<MF, NB>& st, const uint8_t* spc, const uint8_t* spm,
+                                            const uint8_t* sps, const uint8_t* dnc, const uint8_t* dns, int64_t M,
+                                            const uint8_t* wc, const uint8_t* ws, int N, int n0, int ks, int lane) {
+  const int j = lane >> 4;   // block within the panel
+  const int64_t pn = (int64_t)ks * N, pm = (int64_t)ks * M;
+#pragma unroll
+  for (int n = 0; n < NB; ++n) {
+    const int col = min(n0 + 16 * n + (lane & 15), N - 1);
+    st.w[n] = *reinterpret_cast<const uint4*>(wc + (pn + col) * 64 + 16 * j);
+    st.ws[n] = ws[(pn + col) * 4 + j];
+  }
+#pragma unroll
+  for (int m = 0; m < MF; ++m) {
+    int64_t row = 16 * m + (lane & 15);
+    if (row >= M) row = M - 1;
+    const int64_t V = (pm + row) * 4 + j;   // block-major index of (row, block)
+    st.dn[m] = *reinterpret_cast<const uint4*>(dnc + V * 16);
+    st.spc[m] = *reinterpret_cast<const uint2*>(spc + V * 8);
+    st.spm[m] = *reinterpret_cast<const uint32_t*>(spm + V * 4);
+    st.sdn[m] = dns[V];
+    st.ssp[m] = sps[V];
+  }
+}
+
+// The weight is the MFMA's first operand: accumulator element r of lane l is
+// then output column 4 (l / 16) + r of the fragment and activation row l % 16.
+template <int MF, int NB, int PAT>
+__device__ __forceinline__ void skinny_step(v4f_t (&acc)[MF][NB], const SkinnyStage<MF, NB>& st) {
+#pragma unroll
+  for (int m = 0; m < MF; ++m) {
+    const v8i asp = as_operand(expand_block<PAT>(st.spc[m], st.spm[m]));
+    const v8i adn = as_operand(st.dn[m]);
+#pragma unroll
+    for (int n = 0; n < NB; ++n) {
+      const v8i b = as_operand(st.w[n]);
+      acc[m][n] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(b, asp, acc[m][n], 4, 4, 0, (int)st.ws[n], 0,
+                                                                  (int)st.ssp[m]);
+      acc[m][n] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(b, adn, acc[m][n], 4, 4, 0, (int)st.ws[n], 0,
+                                                                  (int)st.sdn[m]);
+    }
+  }
+}
+
+template <int MF, int NB, int KS, int PAT, typename OutT>
+__global__ __launch_bounds__(64 * KS) void k_linear_mx_skinny(const uint8_t* sp_codes, const uint8_t* sp_meta,
+                                                              const uint8_t* sp_scale, const uint8_t* dn_codes,
+                                                              const uint8_t* dn_scale, int64_t M, const uint8_t* wc,
+                                                              const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy) {
+  __shared__ float part[KS - 1][MF * NB][64][4];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int n0 = blockIdx.x * 16 * NB;
+  const int nks = K / kBK;
+  const int per = (nks + KS - 1) / KS;
+  const int k0 = wave * per, k1 = min(nks, k0 + per);
+
+  v4f_t acc[MF][NB];
+#pragma unroll
+  for (int m = 0; m < MF; ++m)
+#pragma unroll
+    for (int n = 0; n < NB; ++n) acc[m][n] = v4f_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+  SkinnyStage<MF, NB> s0, s1;
+  if (k0 < k1)
+    skinny_load<MF, NB>(s0, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, wc, ws, N, n0, k0, lane);
+  if (k0 + 1 < k1)
+    skinny_load<MF, NB>(s1, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, wc, ws, N, n0, k0 + 1, lane);
+  int ks = k0;
+  for (; ks + 1 < k1; ks += 2) {
+    skinny_step<MF, NB, PAT>(acc, s0);
+    if (ks + 2 < k1)
+      skinny_load<MF, NB>(s0, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, wc, ws, N, n0, ks + 2, lane);
+    skinny_step<MF, NB, PAT>(acc, s1);
+    if (ks + 3 < k1)
+      skinny_load<MF, NB>(s1, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, wc, ws, N, n0, ks + 3, lane);
+  }
+  if (ks < k1) skinny_step<MF, NB, PAT>(acc, s0);
+
+  // partial tiles of wavefronts 1..KS-1 to LDS; wavefront 0 adds them in order
+  if (wave > 0) {
+#pragma unroll
+    for (int m = 0; m < MF; ++m)
+#pragma unroll
+      for (int n = 0; n < NB; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) part[wave - 1][m * NB + n][lane][r] = acc[m][n][r];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  for (int w = 0; w < KS - 1; ++w)
+#pragma unroll
+    for (int m = 0; m < MF; ++m)
+#pragma unroll
+      for (int n = 0; n < NB; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[m][n][r] += part[w][m * NB + n][lane][r];
+#pragma unroll
+  for (int m = 0; m < MF; ++m) {
+    const int64_t row = 16 * m + (lane & 15);
+    if (row >= M) continue;
+#pragma unroll
+    for (int n = 0; n < NB; ++n)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int c = n0 + 16 * n + 4 * (lane >> 4) + r;
+        if (c < N) store_out<OutT>(Y + row * ldy + c, acc[m][n][r]);
+      }
+  }
+}
+
+template <int MF, int NB, int KS, int PAT, typename OutT>
+static hipError_t go_skinny(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
+                            const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
+                            void* Y, int64_t ldy, hipStream_t st) {
+  k_linear_mx_skinny<MF, NB, KS, PAT, OutT><<<dim3((unsigned)((N + 16 * NB - 1) / (16 * NB))), dim3(64 * KS), 0, st>>>(
+      spc, spm, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy);
+  return hipGetLastError();
+}
+
+// K split for the small-M kernel: about 8192 wavefronts in flight (8 per
+// SIMD) to keep the weight stream busy, at least 4 panels per wavefront, at
+// most `cap` wavefronts per workgroup.
+static int skinny_split(int N, int K, int NB, int cap) {
+  const int wgs = (N + 16 * NB - 1) / (16 * NB), nks = K / kBK;
+  int ks = 4;
+  while (ks < cap && wgs * ks * 2 <= 8192 && nks >= 4 * ks * 2) ks *= 2;
+  return ks;
+}
+
+// (row fragments, column fragments, K splits) by M: every activation block
+// expansion feeds NB column fragments; the K split keeps enough wavefronts
+// streaming the weight.
+template <int PAT, typename OutT>
+static hipError_t go_skinny_m(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
+                              const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
+                              void* Y, int64_t ldy, hipStream_t st) {
+  if (M <= 16) {
+    const int ks = skinny_split(N, K, 1, 16);
+    if (ks == 16) return go_skinny<1, 1, 16, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+    if (ks == 8) return go_skinny<1, 1, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+    return go_skinny<1, 1, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  }
+  if (M <= 32) {
+    if (skinny_split(N, K, 2, 8) == 8)
+      return go_skinny<2, 2, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+    return go_skinny<2, 2, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  }
+  return go_skinny<4, 4, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+}
+
+template <int PAT>
+static hipError_t go_skinny_dt(int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
+                               const uint8_t* dnc, const uint8_t* dns, int64_t M, const uint8_t* wc,
+                               const uint8_t* ws, int N, int K, void* Y, int64_t ldy, hipStream_t st) {
+  if (ydt == 2) return go_skinny_m<PAT, float>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  if (ydt == 1) return go_skinny_m<PAT, _Float16>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  return go_skinny_m<PAT, uint16_t>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+}
+
+// ---------------------------------------------------------------------------
 // NVFP4 two-path GEMM
 // ---------------------------------------------------------------------------
 //
@@ -1065,6 +1253,10 @@ hipError_t launch_linear_mx(int pat, int ydt, const uint8_t* spc, const uint8_t*
                             int N, int K, void* Y, int64_t ldy, hipStream_t st) {
   const bool sdw = (K % kBK) == 0;
   constexpr int NF = 8;
+  if (sdw && M <= kSkinnyMaxM) {
+    return pat == 24 ? go_skinny_dt<24>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st)
+                     : go_skinny_dt<48>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  }
   if (pat == 24) {
     return sdw ? go_linear_dt<NF, 24, true>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st)
                : go_linear_dt<NF, 24, false>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);

@@ -247,6 +247,38 @@ def test_llama_full_shape(S, G, name):
     gemm_check(G.host(y)[rows], ref, O.linear_abs(o, wo, rows=rows), name)
 
 
+# --------------------------------------------------------------------------- decode shapes
+
+@pytest.mark.parametrize("name,T", [("qkv", 1), ("qkv", 16), ("down", 64), ("gate_up", 33), ("down", 5)])
+def test_llama_decode_shape(S, G, name, T):
+    """Small-M (decode) Llama-3.1-8B shapes, as the decode benchmark runs them:
+    preparation in full, GEMM on every row."""
+    K, N, norm = synth.LLAMA_LINEARS[name]
+    say(f"[decode] {name} T={T} K={K} N={N}")
+    x = synth.activations(T, K, seed=T)
+    g = synth.gamma(K, seed=0) if norm else None
+    a, o = check_prep(S, G, x, g, synth.LLAMA_EPS, 2, 4, f"{name}-T{T}")
+    wq = S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=0)))
+    y = S.sharq_linear(a, wq, dtype=torch.float32)
+    y16 = S.sharq_linear(a, wq, dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    wo = G.weight_to_oracle(wq)
+    gemm_check(G.host(y), O.linear(o, wo), O.linear_abs(o, wo), f"decode {name} T{T}")
+    assert torch.equal(y16, y.to(torch.bfloat16))
+
+
+@pytest.mark.parametrize("T,N,K,n,m", [(7, 40, 256, 4, 8), (64, 96, 1280, 2, 4), (17, 16, 128, 2, 4)])
+def test_small_m_ragged(S, G, T, N, K, n, m):
+    """Small-M kernel: column tails (N % 16), K ranges shorter than four panels, 4:8."""
+    x = synth.activations(T, K, seed=K)
+    o = O.prepare(x, synth.gamma(K, seed=2), 1e-6, n, m, "mx")
+    wo = O.quantize_weight(synth.weight(N, K, seed=N), "mx")
+    a, w = G.oracle_to_act(o), G.oracle_to_weight(wo)
+    y = S.sharq_linear(a, w, dtype=torch.float32)
+    torch.cuda.synchronize()
+    gemm_check(G.host(y), O.linear(o, wo), O.linear_abs(o, wo), f"small-M T{T}N{N}K{K}")
+
+
 # --------------------------------------------------------------------------- grouped (MoE)
 
 @pytest.mark.parametrize("T,E,topk,K,N", [(64, 8, 2, 256, 96), (300, 5, 3, 416, 200)])
