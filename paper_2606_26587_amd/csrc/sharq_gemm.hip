@@ -1197,12 +1197,288 @@ __global__ __launch_bounds__(256) void k_linear_nv(const uint8_t* sp_codes, cons
   }
 }
 
+// ---------------------------------------------------------------------------
+// Interleaved NVFP4 main loop (K a multiple of 128)
+// ---------------------------------------------------------------------------
+//
+// The same slot schedule as the MXFP4 loop, on v_mfma_f32_32x32x16_bf16 with
+// the weight as first operand (each lane then owns an output row).  One K
+// step is one 32-position block: two 16-position MFMA sub-steps t, where lane
+// half h supplies positions 16 h + 8 t + 0..7 -- so a lane needs only its
+// half of each block (one residual scale, 8 bytes of residual codes, half the
+// backbone).  Between the step's 32 MFMAs run the weight reads of sub-step 1,
+// the bf16 dequantization of the next step's activations, the dequantization
+// and LDS store of the weight two steps ahead (three LDS stages) and the
+// reads of the next step's first weight operands.
+
+struct NvRaw {          // this lane's raw activation data of one step
+  uint2 dn;             // residual codes of positions 16 h + 0..15
+  uint32_t spc;         // compressed backbone codes of the same 16 positions
+  uint32_t spm;         // their metadata (low 16 bits)
+  uint32_t ssc, dsc;    // backbone and residual E4M3 scales (bytes)
+};
+
+struct NvOps {          // MFMA-ready bf16 operands of one step
+  uint4 sp[2], dn[2];
+};
+
+struct NvWRaw {         // one weight row of one step
+  uint4 codes;
+  uint32_t sc;
+};
+
+constexpr int kNvStage = 256 * 64;   // bf16 weight tile of one step: 256 rows x 32 positions
+
+// Pieces of the exact bf16 dequantization q * d: codes byte SEL (two E2M1
+// values, lower position in the low nibble) -> one packed bf16 pair.
+template <int SEL>
+__device__ __forceinline__ uint32_t bf16_pair(uint32_t codes, float d) {
+  const v2f v = fp4x2_decode<SEL>(codes);
+  return __builtin_amdgcn_perm(__float_as_uint(v.y * d), __float_as_uint(v.x * d), 0x07060302u);
+}
+
+__device__ __forceinline__ void nv_load_a(NvRaw& s, const ARow& a, int ks, int half) {
+  const int64_t V = ((int64_t)(ks >> 2) * a.R + a.r) * 4 + (ks & 3);   // block-major index
+  s.dn = *reinterpret_cast<const uint2*>(a.dn + V * 16 + 8 * half);
+  s.spc = *reinterpret_cast<const uint32_t*>(a.spc + V * 8 + 4 * half);
+  s.spm = (uint32_t)*reinterpret_cast<const uint16_t*>(a.spm + V * 4 + 2 * half);
+  s.ssc = a.sps[V];
+  s.dsc = a.dns[V * 2 + half];
+}
+
+__device__ __forceinline__ void nv_load_w(NvWRaw& w, const uint8_t* wc, const uint8_t* ws, int n0, int N, int ks) {
+  const int n = min(n0 + (int)threadIdx.x, N - 1);
+  const int64_t V = ((int64_t)(ks >> 2) * N + n) * 4 + (ks & 3);
+  w.codes = *reinterpret_cast<const uint4*>(wc + V * 16);
+  w.sc = ws[V];
+}
+
+template <int SUB, int F0, int F1>
+__device__ __forceinline__ void nv_read_b(uint4 (&b)[8], const uint8_t* lw, int lane) {
+  const int half = lane >> 5, col = lane & 31;
+#pragma unroll
+  for (int f = F0; f < F1; ++f) {
+    const int row = f * 32 + col;
+    b[f] = *reinterpret_cast<const uint4*>(lw + row * 64 + 16 * ((2 * half + SUB) ^ swz_nv(row)));
+  }
+}
+
+template <int SUB, int F>
+__device__ __forceinline__ void nv_mma(v16f (&acc)[8], const uint4& a, const uint4 (&b)[8]) {
+  acc[F] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(b[F]), as_bf16x8(a), acc[F], 0, 0, 0);
+}
+
+template <int PAT, class Issue>
+__device__ __forceinline__ void nv_step(v16f (&acc)[8], const NvOps& ops, uint4 (&b0)[8], const uint8_t* cur,
+                                        const uint8_t* nxt, uint8_t* wr, NvOps& opsn, const NvRaw& raw,
+                                        const NvWRaw& wst, int lane, Issue issue) {
+  const int tid = threadIdx.x;
+  uint4 b1[8];
+  issue();
+  SHARQ_FENCE();
+  // next step's activations: backbone expanded to 16 codes, then dequantized
+  const float dsp = e4m3_value(raw.ssc), ddn = e4m3_value(raw.dsc);
+  uint32_t e0 = 0u, e1 = 0u;
+  const uint2 cw = make_uint2(raw.spc, 0u);
+  // ---- sub-step 0, backbone
+  nv_mma<0, 0>(acc, ops.sp[0], b0); nv_read_b<1, 0, 1>(b1, cur, lane); SHARQ_FENCE();
+  nv_mma<0, 1>(acc, ops.sp[0], b0); nv_read_b<1, 1, 2>(b1, cur, lane); e0 = expand_dw<PAT, 0>(cw, raw.spm); SHARQ_FENCE();
+  nv_mma<0, 2>(acc, ops.sp[0], b0); nv_read_b<1, 2, 3>(b1, cur, lane); SHARQ_FENCE();
+  nv_mma<0, 3>(acc, ops.sp[0], b0); nv_read_b<1, 3, 4>(b1, cur, lane); e1 = expand_dw<PAT, 1>(cw, raw.spm); SHARQ_FENCE();
+  nv_mma<0, 4>(acc, ops.sp[0], b0); nv_read_b<1, 4, 5>(b1, cur, lane);
+  opsn.sp[0].x = bf16_pair<0>(e0, dsp); opsn.sp[0].y = bf16_pair<1>(e0, dsp); SHARQ_FENCE();
+  nv_mma<0, 5>(acc, ops.sp[0], b0); nv_read_b<1, 5, 6>(b1, cur, lane);
+  opsn.sp[0].z = bf16_pair<2>(e0, dsp); opsn.sp[0].w = bf16_pair<3>(e0, dsp); SHARQ_FENCE();
+  nv_mma<0, 6>(acc, ops.sp[0], b0); nv_read_b<1, 6, 7>(b1, cur, lane);
+  opsn.sp[1].x = bf16_pair<0>(e1, dsp); opsn.sp[1].y = bf16_pair<1>(e1, dsp); SHARQ_FENCE();
+  nv_mma<0, 7>(acc, ops.sp[0], b0); nv_read_b<1, 7, 8>(b1, cur, lane);
+  opsn.sp[1].z = bf16_pair<2>(e1, dsp); opsn.sp[1].w = bf16_pair<3>(e1, dsp); SHARQ_FENCE();
+  // ---- sub-step 0, residual
+  nv_mma<0, 0>(acc, ops.dn[0], b0);
+  opsn.dn[0].x = bf16_pair<0>(raw.dn.x, ddn); opsn.dn[0].y = bf16_pair<1>(raw.dn.x, ddn); SHARQ_FENCE();
+  nv_mma<0, 1>(acc, ops.dn[0], b0);
+  opsn.dn[0].z = bf16_pair<2>(raw.dn.x, ddn); opsn.dn[0].w = bf16_pair<3>(raw.dn.x, ddn); SHARQ_FENCE();
+  nv_mma<0, 2>(acc, ops.dn[0], b0);
+  opsn.dn[1].x = bf16_pair<0>(raw.dn.y, ddn); opsn.dn[1].y = bf16_pair<1>(raw.dn.y, ddn); SHARQ_FENCE();
+  nv_mma<0, 3>(acc, ops.dn[0], b0);
+  opsn.dn[1].z = bf16_pair<2>(raw.dn.y, ddn); opsn.dn[1].w = bf16_pair<3>(raw.dn.y, ddn); SHARQ_FENCE();
+  // the weight row two steps ahead: dequantized into the other stage
+  const float dw = e4m3_value(wst.sc);
+  const int wrow = tid;
+  nv_mma<0, 4>(acc, ops.dn[0], b0);
+  *reinterpret_cast<uint4*>(wr + wrow * 64 + 16 * (0 ^ swz_nv(wrow))) =
+      make_uint4(bf16_pair<0>(wst.codes.x, dw), bf16_pair<1>(wst.codes.x, dw), bf16_pair<2>(wst.codes.x, dw),
+                 bf16_pair<3>(wst.codes.x, dw));
+  SHARQ_FENCE();
+  nv_mma<0, 5>(acc, ops.dn[0], b0); SHARQ_FENCE();
+  nv_mma<0, 6>(acc, ops.dn[0], b0);
+  *reinterpret_cast<uint4*>(wr + wrow * 64 + 16 * (1 ^ swz_nv(wrow))) =
+      make_uint4(bf16_pair<0>(wst.codes.y, dw), bf16_pair<1>(wst.codes.y, dw), bf16_pair<2>(wst.codes.y, dw),
+                 bf16_pair<3>(wst.codes.y, dw));
+  SHARQ_FENCE();
+  nv_mma<0, 7>(acc, ops.dn[0], b0); SHARQ_FENCE();
+  // ---- sub-step 1, backbone
+  nv_mma<1, 0>(acc, ops.sp[1], b1);
+  *reinterpret_cast<uint4*>(wr + wrow * 64 + 16 * (2 ^ swz_nv(wrow))) =
+      make_uint4(bf16_pair<0>(wst.codes.z, dw), bf16_pair<1>(wst.codes.z, dw), bf16_pair<2>(wst.codes.z, dw),
+                 bf16_pair<3>(wst.codes.z, dw));
+  SHARQ_FENCE();
+  nv_mma<1, 1>(acc, ops.sp[1], b1); SHARQ_FENCE();
+  nv_mma<1, 2>(acc, ops.sp[1], b1);
+  *reinterpret_cast<uint4*>(wr + wrow * 64 + 16 * (3 ^ swz_nv(wrow))) =
+      make_uint4(bf16_pair<0>(wst.codes.w, dw), bf16_pair<1>(wst.codes.w, dw), bf16_pair<2>(wst.codes.w, dw),
+                 bf16_pair<3>(wst.codes.w, dw));
+  SHARQ_FENCE();
+  nv_mma<1, 3>(acc, ops.sp[1], b1); SHARQ_FENCE();
+  nv_mma<1, 4>(acc, ops.sp[1], b1); SHARQ_FENCE();
+  nv_mma<1, 5>(acc, ops.sp[1], b1); SHARQ_FENCE();
+  nv_mma<1, 6>(acc, ops.sp[1], b1); SHARQ_FENCE();
+  nv_mma<1, 7>(acc, ops.sp[1], b1); SHARQ_FENCE();
+  // ---- sub-step 1, residual; the next step's first weight operands
+  nv_mma<1, 0>(acc, ops.dn[1], b1); nv_read_b<0, 0, 1>(b0, nxt, lane); SHARQ_FENCE();
+  nv_mma<1, 1>(acc, ops.dn[1], b1); nv_read_b<0, 1, 2>(b0, nxt, lane); SHARQ_FENCE();
+  nv_mma<1, 2>(acc, ops.dn[1], b1); nv_read_b<0, 2, 3>(b0, nxt, lane); SHARQ_FENCE();
+  nv_mma<1, 3>(acc, ops.dn[1], b1); nv_read_b<0, 3, 4>(b0, nxt, lane); SHARQ_FENCE();
+  nv_mma<1, 4>(acc, ops.dn[1], b1); nv_read_b<0, 4, 5>(b0, nxt, lane); SHARQ_FENCE();
+  nv_mma<1, 5>(acc, ops.dn[1], b1); nv_read_b<0, 5, 6>(b0, nxt, lane); SHARQ_FENCE();
+  nv_mma<1, 6>(acc, ops.dn[1], b1); nv_read_b<0, 6, 7>(b0, nxt, lane); SHARQ_FENCE();
+  nv_mma<1, 7>(acc, ops.dn[1], b1); nv_read_b<0, 7, 8>(b0, nxt, lane); SHARQ_FENCE();
+}
+
+template <int PAT>
+__device__ __forceinline__ void nv_ops_from_raw(NvOps& o, const NvRaw& r) {
+  const float dsp = e4m3_value(r.ssc), ddn = e4m3_value(r.dsc);
+  const uint2 cw = make_uint2(r.spc, 0u);
+  const uint32_t e0 = expand_dw<PAT, 0>(cw, r.spm), e1 = expand_dw<PAT, 1>(cw, r.spm);
+  o.sp[0] = make_uint4(bf16_pair<0>(e0, dsp), bf16_pair<1>(e0, dsp), bf16_pair<2>(e0, dsp), bf16_pair<3>(e0, dsp));
+  o.sp[1] = make_uint4(bf16_pair<0>(e1, dsp), bf16_pair<1>(e1, dsp), bf16_pair<2>(e1, dsp), bf16_pair<3>(e1, dsp));
+  o.dn[0] = make_uint4(bf16_pair<0>(r.dn.x, ddn), bf16_pair<1>(r.dn.x, ddn), bf16_pair<2>(r.dn.x, ddn),
+                       bf16_pair<3>(r.dn.x, ddn));
+  o.dn[1] = make_uint4(bf16_pair<0>(r.dn.y, ddn), bf16_pair<1>(r.dn.y, ddn), bf16_pair<2>(r.dn.y, ddn),
+                       bf16_pair<3>(r.dn.y, ddn));
+}
+
+__device__ __forceinline__ void nv_store_w(const NvWRaw& w, uint8_t* stage) {
+  const int row = threadIdx.x;
+  const float d = e4m3_value(w.sc);
+  const uint32_t c[4] = {w.codes.x, w.codes.y, w.codes.z, w.codes.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    *reinterpret_cast<uint4*>(stage + row * 64 + 16 * (q ^ swz_nv(row))) =
+        make_uint4(bf16_pair<0>(c[q], d), bf16_pair<1>(c[q], d), bf16_pair<2>(c[q], d), bf16_pair<3>(c[q], d));
+}
+
+template <int PAT, typename OutT>
+__global__ __launch_bounds__(256) void k_linear_nv_il(const uint8_t* sp_codes, const uint8_t* sp_meta,
+                                                      const uint8_t* sp_scale, const uint8_t* dn_codes,
+                                                      const uint8_t* dn_scale, const float* ts_x, int64_t M,
+                                                      const uint8_t* wc, const uint8_t* ws, const float* ts_w, int N,
+                                                      int K, OutT* Y, int64_t ldy, int gx, int gy) {
+  constexpr int NF = 8;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[3 * kNvStage];
+  int mt, nt;
+  tile_of(blockIdx.x, gx, gy, mt, nt);
+  const int n0 = nt * 256;
+  const int64_t row_lo = (int64_t)mt * kBM;
+  const int64_t row_hi = row_lo + kBM < M ? row_lo + kBM : M;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
+  const int nks = K / 32;   // one step per 32-position block
+
+  int64_t orow = row_lo + wave * 32 + (lane & 31);
+  if (orow >= row_hi) orow = row_hi - 1;   // clamp: loads stay in bounds, stores are masked
+  ARow a;
+  a.r = orow;
+  a.R = M;
+  a.dn = dn_codes;
+  a.spc = sp_codes;
+  a.spm = sp_meta;
+  a.dns = dn_scale;
+  a.sps = sp_scale;
+
+  v16f acc[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[f][r] = 0.0f;
+
+  // invariant at step k (sets by k mod 2, stages by k mod 3): stages k, k+1
+  // hold W(k), W(k+1); b0 = step k's first operands; o[k] ready;
+  // r[k+1] = raw A(k+1); w[k] = raw W(k+2)
+  const int last = nks - 1;
+  const auto cl = [&](int k) { return k < last ? k : last; };
+  NvRaw r0, r1;
+  NvWRaw w0, w1;
+  NvOps o0, o1;
+  uint4 b0[8];
+  uint8_t* st0 = lds;
+  uint8_t* st1 = lds + kNvStage;
+  uint8_t* st2 = lds + 2 * kNvStage;
+  nv_load_w(w0, wc, ws, n0, N, 0);
+  nv_load_w(w1, wc, ws, n0, N, cl(1));
+  nv_load_a(r0, a, 0, half);
+  nv_load_a(r1, a, cl(1), half);
+  nv_store_w(w0, st0);
+  nv_store_w(w1, st1);
+  nv_ops_from_raw<PAT>(o0, r0);
+  nv_load_w(w0, wc, ws, n0, N, cl(2));
+  __syncthreads();
+  nv_read_b<0, 0, 8>(b0, st0, lane);
+
+  int ks = 0;
+  for (; ks + 1 < nks; ks += 2) {
+    nv_step<PAT>(acc, o0, b0, st0, st1, st2, o1, r1, w0, lane, [&] {
+      nv_load_w(w1, wc, ws, n0, N, cl(ks + 3));
+      nv_load_a(r0, a, cl(ks + 2), half);
+    });
+    __syncthreads();
+    nv_step<PAT>(acc, o1, b0, st1, st2, st0, o0, r0, w1, lane, [&] {
+      nv_load_w(w0, wc, ws, n0, N, cl(ks + 4));
+      nv_load_a(r1, a, cl(ks + 3), half);
+    });
+    __syncthreads();
+    uint8_t* t = st0;   // rotate the stages by two
+    st0 = st2;
+    st2 = st1;
+    st1 = t;
+  }
+  if (ks < nks) nv_step<PAT>(acc, o0, b0, st0, st1, st2, o1, r1, w0, lane, [] {});
+
+  const float scale = *ts_x * *ts_w;
+  const int64_t row = row_lo + wave * 32 + (lane & 31);
+  if (row >= row_hi) return;
+  OutT* yr = Y + row * ldy;
+  const bool vec = ((reinterpret_cast<uintptr_t>(Y) | (uintptr_t)(ldy * (int64_t)sizeof(OutT))) &
+                    (uintptr_t)(Vec4Out<OutT>::kAlign - 1)) == 0;
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int col = n0 + f * 32 + 8 * g + 4 * half;
+      const float v0 = acc[f][4 * g] * scale, v1 = acc[f][4 * g + 1] * scale;
+      const float v2 = acc[f][4 * g + 2] * scale, v3 = acc[f][4 * g + 3] * scale;
+      if (vec && col + 3 < N) {
+        Vec4Out<OutT>::put(yr + col, v0, v1, v2, v3);
+      } else {
+        if (col < N) store_out<OutT>(yr + col, v0);
+        if (col + 1 < N) store_out<OutT>(yr + col + 1, v1);
+        if (col + 2 < N) store_out<OutT>(yr + col + 2, v2);
+        if (col + 3 < N) store_out<OutT>(yr + col + 3, v3);
+      }
+    }
+  }
+}
+
 template <int PAT, typename OutT>
 static hipError_t go_nv(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
                         const uint8_t* dns, const float* tsx, int64_t M, const uint8_t* wc, const uint8_t* ws,
                         const float* tsw, int N, int K, void* Y, int64_t ldy, hipStream_t st) {
   constexpr int NF = 8;
   const int gx = (N + 32 * NF - 1) / (32 * NF), gy = (int)((M + kBM - 1) / kBM);
+  if (K % kBK == 0) {
+    k_linear_nv_il<PAT, OutT><<<dim3((unsigned)(gx * gy)), dim3(256), 0, st>>>(
+        spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
+    return hipGetLastError();
+  }
   k_linear_nv<NF, PAT, OutT><<<dim3((unsigned)(gx * gy)), dim3(256), 0, st>>>(
       spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
   return hipGetLastError();
