@@ -388,6 +388,35 @@ struct AOps {        // MFMA-ready activation operands of one K step
 constexpr int kStageW = 256 * kLdsStride;        // weight codes of one stage
 constexpr int kStageBytes = kStageW + 64 * 16;   // + the 64 scale records
 
+// 4:8 expansion through a table.  For a keep mask m, entry m holds two
+// v_perm selectors: byte i of the first picks the code for position 2 i (its
+// index among the kept codes, or 0x0C = zero if position 2 i is dropped), the
+// second the code for position 2 i + 1.  The group's four codes are spread to
+// bytes, permuted twice (once shifted into the high nibbles) and OR-ed.
+__device__ __forceinline__ uint2 lut48_entry(uint32_t m) {
+  uint32_t se = 0u, so = 0u, idx = 0u;
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    uint32_t sel = 0x0Cu;
+    if ((m >> p) & 1u) sel = idx++;
+    if (p & 1) so |= sel << (8 * (p >> 1));
+    else se |= sel << (8 * (p >> 1));
+  }
+  return make_uint2(se, so);
+}
+
+__device__ __forceinline__ uint32_t expand48_lut(uint32_t c16, uint2 sel) {
+  uint32_t x = (c16 | (c16 << 8)) & 0x00FF00FFu;   // bytes 0, 2: code pairs (0, 1), (2, 3)
+  x = (x | (x << 4)) & 0x0F0F0F0Fu;                 // byte i: code i
+  return __builtin_amdgcn_perm(0u, x, sel.x) | __builtin_amdgcn_perm(0u, x << 4, sel.y);
+}
+
+// Fill a workgroup's 256-entry table (one entry per thread); the caller
+// synchronizes before the first use.
+__device__ __forceinline__ void lut48_fill(uint2* lut) {
+  if (threadIdx.x < 256) lut[threadIdx.x] = lut48_entry(threadIdx.x);
+}
+
 // Piece Q (0..15) of the next step's expanded backbone: block Q / 8, output
 // dword (Q % 8) / 2, 16-bit half Q % 2 (returned in place within the dword).
 template <int PAT, int Q>
@@ -420,11 +449,19 @@ __device__ __forceinline__ uint32_t exp_piece(const AStep& r) {
 }
 
 template <int PAT, int Q>
-__device__ __forceinline__ void put_piece(AOps& o, const AStep& r) {
+__device__ __forceinline__ void put_piece(AOps& o, const AStep& r, const uint2 (&sel)[8]) {
   constexpr int B = Q / 8, D = (Q % 8) / 2, H = Q % 2;
-  const uint32_t v = exp_piece<PAT, Q>(r);
   uint32_t& d = D == 0 ? o.sp[B].x : D == 1 ? o.sp[B].y : D == 2 ? o.sp[B].z : o.sp[B].w;
-  d = H == 0 ? v : (d | v);
+  if (PAT == 48) {
+    // a whole group (output dword) per even piece, from its table entry
+    if (H == 0) {
+      const uint32_t cw = D < 2 ? r.spc[B].x : r.spc[B].y;
+      d = expand48_lut((cw >> (16 * (D & 1))) & 0xFFFFu, sel[4 * B + D]);
+    }
+  } else {
+    const uint32_t v = exp_piece<PAT, Q>(r);
+    d = H == 0 ? v : (d | v);
+  }
 }
 
 // The weight is the MFMA's first operand and the activation its second, so
@@ -494,42 +531,48 @@ __device__ __forceinline__ void read_bw(uint32_t (&bw)[4], const uint8_t* stage,
 template <int PAT, class Issue>
 __device__ __forceinline__ void step5(v16f (&acc)[8], const AOps& ops, uint4 (&b0)[8], const uint32_t (&bw)[4],
                                       uint32_t (&bwn)[4], const uint8_t* cur, const uint8_t* nxt, uint8_t* wr,
-                                      AOps& opsn, const AStep& raw, const WStep<8>& wst, int lane, Issue issue) {
+                                      AOps& opsn, const AStep& raw, const WStep<8>& wst, int lane, Issue issue,
+                                      const uint2* lut) {
   const int half = lane >> 5, tid = threadIdx.x;
   uint4 b1[8];
+  uint2 sel[8];
+  if (PAT == 48) {   // table entries of the next step's eight 4:8 groups
+#pragma unroll
+    for (int i = 0; i < 8; ++i) sel[i] = lut[(raw.spm[i >> 2] >> (8 * (i & 3))) & 0xFFu];
+  }
   // LDS traffic is spread at about one instruction per slot (a 1 KB
   // wavefront access keeps the LDS busy for several MFMA-lengths when four
   // wavefronts burst together); VALU work stays under ~8 instructions per slot.
   issue();
   SHARQ_FENCE();
   // ---- sub-step 0, backbone: second sub-step's weight operands
-  mma_sp<0, 0>(acc, ops, b0, bw); read_b<1, 0, 1>(b1, cur, lane); put_piece<PAT, 0>(opsn, raw); SHARQ_FENCE();
+  mma_sp<0, 0>(acc, ops, b0, bw); read_b<1, 0, 1>(b1, cur, lane); put_piece<PAT, 0>(opsn, raw, sel); SHARQ_FENCE();
   mma_sp<0, 1>(acc, ops, b0, bw); read_b<1, 1, 2>(b1, cur, lane); SHARQ_FENCE();
-  mma_sp<0, 2>(acc, ops, b0, bw); read_b<1, 2, 3>(b1, cur, lane); put_piece<PAT, 1>(opsn, raw); SHARQ_FENCE();
+  mma_sp<0, 2>(acc, ops, b0, bw); read_b<1, 2, 3>(b1, cur, lane); put_piece<PAT, 1>(opsn, raw, sel); SHARQ_FENCE();
   mma_sp<0, 3>(acc, ops, b0, bw); read_b<1, 3, 4>(b1, cur, lane); SHARQ_FENCE();
-  mma_sp<0, 4>(acc, ops, b0, bw); read_b<1, 4, 5>(b1, cur, lane); put_piece<PAT, 2>(opsn, raw); SHARQ_FENCE();
+  mma_sp<0, 4>(acc, ops, b0, bw); read_b<1, 4, 5>(b1, cur, lane); put_piece<PAT, 2>(opsn, raw, sel); SHARQ_FENCE();
   mma_sp<0, 5>(acc, ops, b0, bw); read_b<1, 5, 6>(b1, cur, lane); SHARQ_FENCE();
-  mma_sp<0, 6>(acc, ops, b0, bw); read_b<1, 6, 7>(b1, cur, lane); put_piece<PAT, 3>(opsn, raw); SHARQ_FENCE();
+  mma_sp<0, 6>(acc, ops, b0, bw); read_b<1, 6, 7>(b1, cur, lane); put_piece<PAT, 3>(opsn, raw, sel); SHARQ_FENCE();
   mma_sp<0, 7>(acc, ops, b0, bw); read_b<1, 7, 8>(b1, cur, lane); SHARQ_FENCE();
   // ---- sub-step 0, residual: the weight tile two steps ahead to LDS
-  mma_dn<0, 0>(acc, ops, b0, bw); put_piece<PAT, 4>(opsn, raw); SHARQ_FENCE();
+  mma_dn<0, 0>(acc, ops, b0, bw); put_piece<PAT, 4>(opsn, raw, sel); SHARQ_FENCE();
   mma_dn<0, 1>(acc, ops, b0, bw);
   *reinterpret_cast<uint4*>(wr + (tid >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[0];
   SHARQ_FENCE();
-  mma_dn<0, 2>(acc, ops, b0, bw); put_piece<PAT, 5>(opsn, raw); SHARQ_FENCE();
+  mma_dn<0, 2>(acc, ops, b0, bw); put_piece<PAT, 5>(opsn, raw, sel); SHARQ_FENCE();
   mma_dn<0, 3>(acc, ops, b0, bw);
   *reinterpret_cast<uint4*>(wr + ((tid + 256) >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[1];
   SHARQ_FENCE();
-  mma_dn<0, 4>(acc, ops, b0, bw); put_piece<PAT, 6>(opsn, raw); SHARQ_FENCE();
+  mma_dn<0, 4>(acc, ops, b0, bw); put_piece<PAT, 6>(opsn, raw, sel); SHARQ_FENCE();
   mma_dn<0, 5>(acc, ops, b0, bw);
   *reinterpret_cast<uint4*>(wr + ((tid + 512) >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[2];
   SHARQ_FENCE();
-  mma_dn<0, 6>(acc, ops, b0, bw); put_piece<PAT, 7>(opsn, raw); SHARQ_FENCE();
+  mma_dn<0, 6>(acc, ops, b0, bw); put_piece<PAT, 7>(opsn, raw, sel); SHARQ_FENCE();
   mma_dn<0, 7>(acc, ops, b0, bw);
   *reinterpret_cast<uint4*>(wr + ((tid + 768) >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[3];
   SHARQ_FENCE();
   // ---- sub-step 1, backbone: weight scales, then the next step's operands
-  mma_sp<1, 0>(acc, ops, b1, bw); put_piece<PAT, 8>(opsn, raw); SHARQ_FENCE();
+  mma_sp<1, 0>(acc, ops, b1, bw); put_piece<PAT, 8>(opsn, raw, sel); SHARQ_FENCE();
   mma_sp<1, 1>(acc, ops, b1, bw);
   {
     const int f = tid >> 5, c = tid & 31;
@@ -538,20 +581,20 @@ __device__ __forceinline__ void step5(v16f (&acc)[8], const AOps& ops, uint4 (&b
     *reinterpret_cast<uint16_t*>(wr + kStageW + (2 * c + 1) * 16 + 2 * f) = (uint16_t)(wst.s >> 16);
   }
   SHARQ_FENCE();
-  mma_sp<1, 2>(acc, ops, b1, bw); put_piece<PAT, 9>(opsn, raw); SHARQ_FENCE();
+  mma_sp<1, 2>(acc, ops, b1, bw); put_piece<PAT, 9>(opsn, raw, sel); SHARQ_FENCE();
   mma_sp<1, 3>(acc, ops, b1, bw); read_b<0, 0, 1>(b0, nxt, lane); SHARQ_FENCE();
-  mma_sp<1, 4>(acc, ops, b1, bw); put_piece<PAT, 10>(opsn, raw); SHARQ_FENCE();
+  mma_sp<1, 4>(acc, ops, b1, bw); put_piece<PAT, 10>(opsn, raw, sel); SHARQ_FENCE();
   mma_sp<1, 5>(acc, ops, b1, bw); read_b<0, 1, 2>(b0, nxt, lane); SHARQ_FENCE();
-  mma_sp<1, 6>(acc, ops, b1, bw); put_piece<PAT, 11>(opsn, raw); SHARQ_FENCE();
+  mma_sp<1, 6>(acc, ops, b1, bw); put_piece<PAT, 11>(opsn, raw, sel); SHARQ_FENCE();
   mma_sp<1, 7>(acc, ops, b1, bw); read_b<0, 2, 3>(b0, nxt, lane); SHARQ_FENCE();
   // ---- sub-step 1, residual
-  mma_dn<1, 0>(acc, ops, b1, bw); put_piece<PAT, 12>(opsn, raw); read_b<0, 3, 4>(b0, nxt, lane); SHARQ_FENCE();
+  mma_dn<1, 0>(acc, ops, b1, bw); put_piece<PAT, 12>(opsn, raw, sel); read_b<0, 3, 4>(b0, nxt, lane); SHARQ_FENCE();
   mma_dn<1, 1>(acc, ops, b1, bw); read_b<0, 4, 5>(b0, nxt, lane); SHARQ_FENCE();
-  mma_dn<1, 2>(acc, ops, b1, bw); put_piece<PAT, 13>(opsn, raw); read_b<0, 5, 6>(b0, nxt, lane); SHARQ_FENCE();
+  mma_dn<1, 2>(acc, ops, b1, bw); put_piece<PAT, 13>(opsn, raw, sel); read_b<0, 5, 6>(b0, nxt, lane); SHARQ_FENCE();
   mma_dn<1, 3>(acc, ops, b1, bw); read_b<0, 6, 7>(b0, nxt, lane); SHARQ_FENCE();
-  mma_dn<1, 4>(acc, ops, b1, bw); put_piece<PAT, 14>(opsn, raw); read_b<0, 7, 8>(b0, nxt, lane); SHARQ_FENCE();
+  mma_dn<1, 4>(acc, ops, b1, bw); put_piece<PAT, 14>(opsn, raw, sel); read_b<0, 7, 8>(b0, nxt, lane); SHARQ_FENCE();
   mma_dn<1, 5>(acc, ops, b1, bw); read_bw(bwn, nxt, lane); SHARQ_FENCE();
-  mma_dn<1, 6>(acc, ops, b1, bw); put_piece<PAT, 15>(opsn, raw); SHARQ_FENCE();
+  mma_dn<1, 6>(acc, ops, b1, bw); put_piece<PAT, 15>(opsn, raw, sel); SHARQ_FENCE();
   mma_dn<1, 7>(acc, ops, b1, bw);
   opsn.ssp = raw.ssp >> (16 * half);
   opsn.sdn = raw.sdn >> (16 * half);
@@ -600,7 +643,7 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
                                            const uint8_t* dn_codes, const uint8_t* dn_scale, const int32_t* row_index,
                                            int64_t act_rows, int64_t row_lo, int64_t row_hi, const uint8_t* wc,
                                            const uint8_t* ws, int n0, int N, int K, OutT* Y, int64_t ldy,
-                                           uint8_t* lds) {
+                                           uint8_t* lds, const uint2* lut) {
   constexpr int NF = 8;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
   const int nblk = K / 32, nks = K / kBK;
@@ -666,19 +709,19 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
       load_a_dn(o2, a, cl(ks + 2), half);
       load_a_meta(r0, a, cl(ks + 3), half);
       load_w<NF, true>(w1, wc, ws, n0, N, K, cl(ks + 4), nblk);
-    });
+    }, lut);
     __syncthreads();
     step5<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [&] {
       load_a_dn(o0, a, cl(ks + 3), half);
       load_a_meta(r1, a, cl(ks + 4), half);
       load_w<NF, true>(w2, wc, ws, n0, N, K, cl(ks + 5), nblk);
-    });
+    }, lut);
     __syncthreads();
     step5<PAT>(acc, o2, b0, bwa, bwb, st2, st0, st1, o0, r0, w1, lane, [&] {
       load_a_dn(o1, a, cl(ks + 4), half);
       load_a_meta(r2, a, cl(ks + 5), half);
       load_w<NF, true>(w0, wc, ws, n0, N, K, cl(ks + 6), nblk);
-    });
+    }, lut);
     __syncthreads();
     // bw alternates with period two: after three steps the roles swap
     uint32_t t[4] = {bwa[0], bwa[1], bwa[2], bwa[3]};
@@ -686,10 +729,10 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
     for (int i = 0; i < 4; ++i) { bwa[i] = bwb[i]; bwb[i] = t[i]; }
   }
   if (ks < nks) {   // one or two steps left, in sets 0 and 1
-    step5<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [] {});
+    step5<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [] {}, lut);
     if (ks + 1 < nks) {
       __syncthreads();
-      step5<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [] {});
+      step5<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [] {}, lut);
     }
   }
 
@@ -752,8 +795,15 @@ __global__ __launch_bounds__(256) void k_linear_mx(const uint8_t* sp_codes, cons
   const int64_t m0 = (int64_t)mt * kBM;
   const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
   if constexpr (SCALE_DW && NF == 8)
+  {
+    __shared__ uint2 lut48[256];
+    if (PAT == 48) {
+      lut48_fill(lut48);
+      __syncthreads();
+    }
     tile_mx_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws, n0, N, K, Y,
-                          ldy, lds);
+                          ldy, lds, lut48);
+  }
   else
     tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws, n0,
                                      N, K, Y, ldy, lds_w, lds_s);
@@ -813,8 +863,15 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
   const uint8_t* wce = wc + (int64_t)e * N * (K / 2);
   const uint8_t* wse = ws + (int64_t)e * N * (K / 32);
   if constexpr (SCALE_DW && NF == 8)
+  {
+    __shared__ uint2 lut48[256];
+    if (PAT == 48) {
+      lut48_fill(lut48);
+      __syncthreads();
+    }
     tile_mx_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, act_rows, r0, r1, wce, wse, n0,
-                          N, K, Y, ldy, lds);
+                          N, K, Y, ldy, lds, lut48);
+  }
   else
     tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, act_rows, r0, r1,
                                      wce, wse, n0, N, K, Y, ldy, lds_w, lds_s);
