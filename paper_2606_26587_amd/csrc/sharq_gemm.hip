@@ -809,16 +809,16 @@ __global__ __launch_bounds__(256) void k_linear_mx(const uint8_t* sp_codes, cons
                                      N, K, Y, ldy, lds_w, lds_s);
 }
 
-// Grouped (MoE) form.  Work item y of the grid is a 128-row tile of one
-// expert's slice [off[e], off[e+1]) of the output; the tile-to-expert map is
-// rebuilt on the device from expert_offsets (an exclusive scan of
-// ceil(rows_e / 128)), so the host never reads the routing.  Items past the
-// last tile exit before any barrier.
+// Grouped (MoE) form.  The grid is (column tiles) x (items); an item is a
+// 128-row tile of one expert's slice [off[e], off[e+1]) of the output.  The
+// tile-to-expert map is rebuilt on the device from expert_offsets (an
+// exclusive scan of ceil(rows_e / 128)), so the host never reads the
+// routing.  Items past the last tile exit before any barrier.
 template <int NF, int PAT, bool SCALE_DW, typename OutT>
 __global__ __launch_bounds__(256) void k_linear_mx_grouped(
     const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale, const uint8_t* dn_codes,
     const uint8_t* dn_scale, const int32_t* row_index, int64_t act_rows, const int32_t* offs, int E,
-    const uint8_t* wc, const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy) {
+    const uint8_t* wc, const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy, int gx) {
   constexpr int BN = 32 * NF;
   constexpr int kOld = 2 * BN * kLdsStride + 2 * 64 * 2 * NF;
   __shared__ __attribute__((aligned(16))) uint8_t lds[kOld > 3 * kStageBytes ? kOld : 3 * kStageBytes];
@@ -848,7 +848,15 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
     }
     __syncthreads();
   }
-  const int item = blockIdx.y;
+  // Workgroups go round-robin over the 8 XCDs; renumber so that each XCD
+  // walks a contiguous range of (column tile, item) pairs in column-major
+  // order: the few row tiles of one expert that share a weight tile then run
+  // back to back on one XCD and reuse it from that XCD's L2.
+  const int items = (int)gridDim.x / gx;
+  const int total_wg = (int)gridDim.x;
+  int idp = blockIdx.x;
+  if ((total_wg & 7) == 0) idp = (blockIdx.x & 7) * (total_wg >> 3) + (blockIdx.x >> 3);
+  const int xt = idp / items, item = idp - xt * items;
   if (item >= s_first[E]) return;   // uniform across the workgroup
   int lo = 0, hi = E;               // find e with s_first[e] <= item < s_first[e+1]
   while (hi - lo > 1) {
@@ -859,7 +867,7 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
   const int64_t r0 = (int64_t)offs[e] + (int64_t)(item - s_first[e]) * kBM;
   const int64_t r_end = offs[e + 1];
   const int64_t r1 = r0 + kBM < r_end ? r0 + kBM : r_end;
-  const int n0 = blockIdx.x * BN;
+  const int n0 = xt * BN;
   const uint8_t* wce = wc + (int64_t)e * N * (K / 2);
   const uint8_t* wse = ws + (int64_t)e * N * (K / 32);
   if constexpr (SCALE_DW && NF == 8)
@@ -1605,9 +1613,11 @@ static hipError_t go_grouped(const uint8_t* spc, const uint8_t* spm, const uint8
                              hipStream_t st) {
   // upper bound on the number of 128-row tiles over all experts
   const int64_t items = (total + kBM - 1) / kBM + E;
-  dim3 grid((unsigned)((N + 32 * NF - 1) / (32 * NF)), (unsigned)items), block(256);
+  const int gx = (N + 32 * NF - 1) / (32 * NF);
+  if ((int64_t)gx * items > (int64_t)INT32_MAX) return hipErrorInvalidValue;
+  dim3 grid((unsigned)(gx * items)), block(256);
   k_linear_mx_grouped<NF, PAT, SDW, OutT><<<grid, block, 0, st>>>(spc, spm, sps, dnc, dns, ridx, act_rows, offs, E,
-                                                                  wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy);
+                                                                  wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx);
   return hipGetLastError();
 }
 
