@@ -324,3 +324,30 @@ def test_grouped_uneven_experts(S, G):
         if hi > lo:
             yabs[lo:hi] = O.linear_abs(o, wos[e], rows=np.arange(lo, hi))
     gemm_check(G.host(y), ref, yabs, "grouped-uneven")
+
+
+def test_moe_full_config(S, G):
+    """Qwen3-30B-A3B expert layers at full size, in the benchmark's launch
+    configuration: 4096 tokens, top-8 of 128 experts, gate/up 1536 x 2048 with
+    RMSNorm, 4:8.  Preparation compared in full; the grouped GEMM on the
+    slices of four experts (all their rows, all columns)."""
+    cfg = synth.MOE
+    T, H, E, I, k = cfg["tokens"], cfg["hidden"], cfg["experts"], cfg["inter"], cfg["topk"]
+    say(f"[moe] T={T} H={H} E={E} I={I} top{k}")
+    x = synth.activations(T, H, seed=0)
+    g = synth.gamma(H, seed=0)
+    a, o = check_prep(S, G, x, g, 1e-6, 4, 8, "moe-gate_up-input")
+    ridx, offs = synth.router_topk(T, E, k, seed=0)
+    total = int(offs[-1])
+    ws = [synth.weight(2 * I, H, seed=100 + e) for e in range(E)]
+    w = S.stack_weights([S.sharq_quantize_weight(G.dev_bf16(we)) for we in ws])
+    y = S.sharq_linear_grouped(a, torch.from_numpy(ridx).cuda(), torch.from_numpy(offs).cuda(), total, w,
+                               dtype=torch.float32)
+    torch.cuda.synchronize()
+    yh = G.host(y)
+    for e in (0, 1, 63, 127):
+        lo, hi = int(offs[e]), int(offs[e + 1])
+        wo = O.quantize_weight(ws[e], "mx")
+        rows = ridx[lo:hi]
+        assert hi - lo > 0 and np.abs(yh[lo:hi]).max() > 0, (e, lo, hi)
+        gemm_check(yh[lo:hi], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), f"moe expert {e}")
