@@ -492,9 +492,11 @@ struct Vec4Out<float> {
 template <>
 struct Vec4Out<uint16_t> {
   static __device__ __forceinline__ void put(uint16_t* p, float a, float b, float c, float d) {
-    const uint32_t lo = (uint32_t)f32_to_bf16_rne(a) | ((uint32_t)f32_to_bf16_rne(b) << 16);
-    const uint32_t hi = (uint32_t)f32_to_bf16_rne(c) | ((uint32_t)f32_to_bf16_rne(d) << 16);
-    *reinterpret_cast<uint2*>(p) = make_uint2(lo, hi);
+    // v_cvt_pk_bf16_f32: two round-to-nearest-even conversions per instruction
+    typedef __bf16 bf4 __attribute__((ext_vector_type(4)));
+    bf4 v;
+    v[0] = (__bf16)a; v[1] = (__bf16)b; v[2] = (__bf16)c; v[3] = (__bf16)d;
+    *reinterpret_cast<bf4*>(p) = v;
   }
   static constexpr int kAlign = 8;
 };
@@ -638,6 +640,40 @@ __device__ __forceinline__ void store_w_stage(const WStep<8>& w, uint8_t* stage)
   *reinterpret_cast<uint16_t*>(stage + kStageW + (2 * c + 1) * 16 + 2 * f) = (uint16_t)(w.s >> 16);
 }
 
+// Epilogue of a wavefront's 32 x 256 block of 2-byte outputs through LDS.
+// In the accumulator layout a lane holds 8-byte pieces of one output row, so
+// direct stores put 32 scattered 16-byte pieces in every instruction (rows
+// are N outputs apart); measured on the Llama prefill shapes this cost about
+// 5 us per round of tiles.  Here the block is staged in LDS and read back
+// along rows: each store instruction then writes two whole 512-byte row
+// segments.  The wavefront owns its LDS region, and its LDS accesses execute
+// in order, so no barrier is needed inside.
+constexpr int kEpiStride = 528;            // bytes per staged row: 512 + 16 (spreads rows over banks)
+constexpr int kEpiWave = 32 * kEpiStride;  // one wavefront's region
+constexpr int kTileLds = 4 * kEpiWave > 3 * kStageBytes ? 4 * kEpiWave : 3 * kStageBytes;
+
+template <typename OutT>
+__device__ __forceinline__ void store_tile_lds(const v16f (&acc)[8], OutT* Y, int64_t ldy, int64_t row0,
+                                               int64_t row_hi, int n0, int N, uint8_t* buf, int lane) {
+  const int r = lane & 31, half = lane >> 5;
+#pragma unroll
+  for (int f = 0; f < 8; ++f) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      Vec4Out<OutT>::put(reinterpret_cast<OutT*>(buf + r * kEpiStride + (32 * f + 8 * g + 4 * half) * 2),
+                         acc[f][4 * g], acc[f][4 * g + 1], acc[f][4 * g + 2], acc[f][4 * g + 3]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int rr = 2 * i + (lane >> 5), ch = lane & 31;
+    const uint4 v = *reinterpret_cast<const uint4*>(buf + rr * kEpiStride + ch * 16);
+    const int64_t row = row0 + rr;
+    const int col = n0 + 8 * ch;
+    if (row < row_hi && col < N) *reinterpret_cast<uint4*>(Y + row * ldy + col) = v;
+  }
+}
+
 template <int PAT, typename OutT>
 __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale,
                                            const uint8_t* dn_codes, const uint8_t* dn_scale, const int32_t* row_index,
@@ -736,7 +772,16 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
     }
   }
 
-  // Epilogue: this lane's output row, four consecutive columns per store.
+  // Epilogue.  2-byte outputs go through LDS as whole row segments when the
+  // output allows 16-byte stores (every workgroup-uniform condition).
+  if constexpr (sizeof(OutT) == 2) {
+    if (((reinterpret_cast<uintptr_t>(Y) | (uintptr_t)(ldy * 2)) & 15u) == 0 && N % 8 == 0) {
+      __syncthreads();   // every wavefront is done with the weight stages
+      store_tile_lds<OutT>(acc, Y, ldy, row_lo + wave * 32, row_hi, n0, N, lds + wave * kEpiWave, lane);
+      return;
+    }
+  }
+  // Otherwise this lane's output row, four consecutive columns per store.
   const int64_t row = row_lo + wave * 32 + (lane & 31);
   if (row >= row_hi) return;
   OutT* yr = Y + row * ldy;
@@ -786,7 +831,7 @@ __global__ __launch_bounds__(256) void k_linear_mx(const uint8_t* sp_codes, cons
                                                    int gy) {
   constexpr int BN = 32 * NF;
   constexpr int kOld = 2 * BN * kLdsStride + 2 * 64 * 2 * NF;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kOld > 3 * kStageBytes ? kOld : 3 * kStageBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kOld > kTileLds ? kOld : kTileLds];
   uint8_t* lds_w = lds;
   uint8_t* lds_s = lds + 2 * BN * kLdsStride;
   int mt, nt;
@@ -821,7 +866,7 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
     const uint8_t* wc, const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy, int gx) {
   constexpr int BN = 32 * NF;
   constexpr int kOld = 2 * BN * kLdsStride + 2 * 64 * 2 * NF;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kOld > 3 * kStageBytes ? kOld : 3 * kStageBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kOld > kTileLds ? kOld : kTileLds];
   uint8_t* lds_w = lds;
   uint8_t* lds_s = lds + 2 * BN * kLdsStride;
   __shared__ int s_first[1025];
