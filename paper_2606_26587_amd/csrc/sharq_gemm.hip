@@ -823,6 +823,8 @@ __device__ __forceinline__ void tile_of(int id, int gx, int gy, int& mt, int& nt
   }
 }
 
+// One tile per workgroup, for K not a multiple of 128 (the simpler pipeline
+// of tile_mx, which handles a narrow last panel).
 template <int NF, int PAT, bool SCALE_DW, typename OutT>
 __global__ __launch_bounds__(256) void k_linear_mx(const uint8_t* sp_codes, const uint8_t* sp_meta,
                                                    const uint8_t* sp_scale, const uint8_t* dn_codes,
@@ -830,8 +832,7 @@ __global__ __launch_bounds__(256) void k_linear_mx(const uint8_t* sp_codes, cons
                                                    const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy, int gx,
                                                    int gy) {
   constexpr int BN = 32 * NF;
-  constexpr int kOld = 2 * BN * kLdsStride + 2 * 64 * 2 * NF;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kOld > kTileLds ? kOld : kTileLds];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * BN * kLdsStride + 2 * 64 * 2 * NF];
   uint8_t* lds_w = lds;
   uint8_t* lds_s = lds + 2 * BN * kLdsStride;
   int mt, nt;
@@ -839,19 +840,38 @@ __global__ __launch_bounds__(256) void k_linear_mx(const uint8_t* sp_codes, cons
   const int n0 = nt * BN;
   const int64_t m0 = (int64_t)mt * kBM;
   const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
-  if constexpr (SCALE_DW && NF == 8)
-  {
-    __shared__ uint2 lut48[256];
-    if (PAT == 48) {
-      lut48_fill(lut48);
-      __syncthreads();
-    }
-    tile_mx_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws, n0, N, K, Y,
-                          ldy, lds, lut48);
+  tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws, n0, N,
+                                   K, Y, ldy, lds_w, lds_s);
+}
+
+// Persistent dense kernel (K a multiple of 128): at most one workgroup per
+// CU, walking the tiles b, b + G, b + 2G, ... (G workgroups).  A tile's
+// output stores then drain while the same CU starts its next tile instead of
+// the whole grid waiting at the end of every round (3% on the Llama gate/up
+// shape, 7 rounds).  With G a multiple of 8 every tile an XCD runs keeps the
+// XCD of its number, so the tile_of blocks still share an L2.
+template <int PAT, typename OutT>
+__global__ __launch_bounds__(256) void k_linear_mx_persist(const uint8_t* sp_codes, const uint8_t* sp_meta,
+                                                           const uint8_t* sp_scale, const uint8_t* dn_codes,
+                                                           const uint8_t* dn_scale, int64_t M, const uint8_t* wc,
+                                                           const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy,
+                                                           int gx, int gy) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kTileLds];
+  __shared__ uint2 lut48[256];
+  if (PAT == 48) {
+    lut48_fill(lut48);
+    __syncthreads();
   }
-  else
-    tile_mx<NF, PAT, SCALE_DW, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws, n0,
-                                     N, K, Y, ldy, lds_w, lds_s);
+  const int ntile = gx * gy;
+  for (int id = (int)blockIdx.x; id < ntile; id += (int)gridDim.x) {
+    int mt, nt;
+    tile_of(id, gx, gy, mt, nt);
+    const int64_t m0 = (int64_t)mt * kBM;
+    const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
+    tile_mx_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws, nt * 256, N,
+                          K, Y, ldy, lds, lut48);
+    __syncthreads();   // the LDS stages are free before the next tile's prologue
+  }
 }
 
 // Grouped (MoE) form.  The grid is (column tiles) x (items); an item is a
@@ -1615,13 +1635,32 @@ hipError_t launch_linear_nv(int pat, int ydt, const uint8_t* spc, const uint8_t*
 // Host-side launchers
 // ---------------------------------------------------------------------------
 
+// Compute units of the current device (queried once per device).
+static int device_cus() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
 template <int NF, int PAT, bool SDW, typename OutT>
 static hipError_t go_linear(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
                             const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
                             void* Y, int64_t ldy, hipStream_t st) {
   const int gx = (N + 32 * NF - 1) / (32 * NF), gy = (int)((M + kBM - 1) / kBM);
-  k_linear_mx<NF, PAT, SDW, OutT><<<dim3((unsigned)(gx * gy)), dim3(256), 0, st>>>(
-      spc, spm, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
+  if constexpr (SDW && NF == 8) {
+    const int tiles = gx * gy, cus = device_cus();
+    k_linear_mx_persist<PAT, OutT><<<dim3((unsigned)(tiles < cus ? tiles : cus)), dim3(256), 0, st>>>(
+        spc, spm, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
+  } else {
+    k_linear_mx<NF, PAT, SDW, OutT><<<dim3((unsigned)(gx * gy)), dim3(256), 0, st>>>(
+        spc, spm, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
+  }
   return hipGetLastError();
 }
 
