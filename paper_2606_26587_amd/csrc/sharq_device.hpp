@@ -5,9 +5,10 @@
 // uses an E4M3 block scale plus a per-tensor fp32 scale (App. A.1.1-A.1.3).
 //
 // The hardware converter v_cvt_scalef32_pk_fp4_f32 rounds to the nearest E2M1
-// value with ties to the even code, saturates at 6 and keeps the sign of zero;
-// the kernels always hand it values already divided by the block scale and a
-// unit scale operand, so the scale operand never has to represent 2^-127.
+// value with ties to the even code, saturates at 6 and keeps the sign of zero.
+// MXFP4 blocks hand it their power-of-two scale through its scale operand;
+// NVFP4 blocks hand it values already divided by their scale, with a unit
+// scale operand.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -36,9 +37,6 @@ __device__ __forceinline__ int mx_exponent(uint32_t amax_bits) {
   int e = floor_log2_abs_bits(amax_bits) - 2;
   return e < -127 ? -127 : e;
 }
-
-// 2^-e as fp32 for e in [-127, 125]: always a normal number.
-__device__ __forceinline__ float exp2_neg(int e) { return __uint_as_float((uint32_t)(127 - e) << 23); }
 
 // 2^e as fp32 for e in [-149, 127] (2^-127 is subnormal).
 __device__ __forceinline__ float exp2_int(int e) {
@@ -97,16 +95,34 @@ __device__ __forceinline__ float e4m3_value(uint32_t c) {
   return E ? exp2_int((int)E - 7) * (1.0f + (float)M * 0.125f) : (float)M * 0.001953125f;
 }
 
-// Block quantizer policies.  enc(v) is the value handed to the E2M1
-// converter (whose scale operand stays 1.0: the hardware uses only the
-// exponent of that operand), dec(q) the dequantized value of a decoded code q.
-//   MXFP4: power-of-two scale 2^e, both directions exact.
-//   NVFP4: E4M3 block scale d under per-tensor scale S: enc = fl(v / fl(d S)),
-//          dec = fl(fl(q d) S); a zero block scale gives signed-zero codes.
+// Block quantizer policies.  enc2<SEL>(old, a, b) writes the E2M1 codes of
+// two values into byte SEL of `old` (first value in the low nibble);
+// dec2<SEL>(packed) returns the dequantized values of the two codes in byte
+// SEL.
+//   MXFP4: power-of-two block scale 2^e.  The converters divide (encode) or
+//          multiply (decode) by 2^k, k the exponent field of their scale
+//          operand minus 127 (checked on gfx950 for every k in [-127, 127],
+//          subnormal values included), so the block exponent goes straight
+//          into that operand: a float with exponent field e + 127, which is
+//          the bit pattern of 0.0f for e = -127.  Both directions are exact.
+//   NVFP4: E4M3 block scale d under per-tensor scale S: the converter gets
+//          fl(v / fl(d S)) with a unit scale, dec = fl(fl(q d) S); a zero
+//          block scale gives signed-zero codes.
 struct MxQ {
-  float inv, sc;
-  __device__ __forceinline__ float enc(float v) const { return v * inv; }
-  __device__ __forceinline__ float dec(float q) const { return q * sc; }
+  float sc;
+  __device__ static MxQ make(int e) {
+    MxQ q;
+    q.sc = __uint_as_float((uint32_t)(e + 127) << 23);
+    return q;
+  }
+  template <int SEL>
+  __device__ __forceinline__ uint32_t enc2(uint32_t old, float a, float b) const {
+    return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, a, b, sc, SEL);
+  }
+  template <int SEL>
+  __device__ __forceinline__ v2f dec2(uint32_t packed) const {
+    return __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(packed, sc, SEL);
+  }
 };
 
 struct NvQ {
@@ -116,6 +132,18 @@ struct NvQ {
     return step > 0.0f ? v / step : v;
   }
   __device__ __forceinline__ float dec(float q) const { return (q * d) * S; }
+  template <int SEL>
+  __device__ __forceinline__ uint32_t enc2(uint32_t old, float a, float b) const {
+    return fp4x2<SEL>(old, enc(a), enc(b));
+  }
+  template <int SEL>
+  __device__ __forceinline__ v2f dec2(uint32_t packed) const {
+    const v2f q = fp4x2_decode<SEL>(packed);
+    v2f r;
+    r.x = dec(q.x);
+    r.y = dec(q.y);
+    return r;
+  }
   __device__ static NvQ make(float amax, float six_s, float S) {
     NvQ q;
     q.d = e4m3_round(amax / six_s);
@@ -128,14 +156,13 @@ struct NvQ {
 // Eight consecutive values -> one dword of E2M1 codes under quantizer qz.
 template <class Q>
 __device__ __forceinline__ uint32_t enc8(const float* v, const Q& qz) {
-  const float e0 = qz.enc(v[0]);
   // bytes 1-3 are written below, so the first conversion may start from any
-  // register (e0's, which is dead after it)
-  uint32_t t = __float_as_uint(e0);
-  t = fp4x2<0>(t, e0, qz.enc(v[1]));
-  t = fp4x2<1>(t, qz.enc(v[2]), qz.enc(v[3]));
-  t = fp4x2<2>(t, qz.enc(v[4]), qz.enc(v[5]));
-  t = fp4x2<3>(t, qz.enc(v[6]), qz.enc(v[7]));
+  // register (v[0]'s)
+  uint32_t t = __float_as_uint(v[0]);
+  t = qz.template enc2<0>(t, v[0], v[1]);
+  t = qz.template enc2<1>(t, v[2], v[3]);
+  t = qz.template enc2<2>(t, v[4], v[5]);
+  t = qz.template enc2<3>(t, v[6], v[7]);
   return t;
 }
 

@@ -36,41 +36,69 @@ namespace sharq {
 // Smallest float above a non-negative finite a (FLT_MAX -> +inf).
 __device__ __forceinline__ float next_up(float a) { return __uint_as_float(__float_as_uint(a) + 1u); }
 
-// 2:4 on one group: keep bits of positions 0..3 (exactly two set).  Position
-// p is kept iff it beats at least two of the other three, a tie going to the
-// lower index -- i.e. iff |y_p| is at least the median of the other three
-// magnitudes, where a lower-index rival q (which wins ties) enters as the
-// next float above |y_q|.  One med3 and one compare per position.
-__device__ __forceinline__ void top2of4(float y0, float y1, float y2, float y3, bool& k0, bool& k1, bool& k2,
-                                        bool& k3) {
+// Lane masks.  A comparison over the wavefront is one vector instruction that
+// leaves a 64-bit mask in scalar registers; logic on masks runs on the
+// scalar unit, beside the vector work of the other wavefronts, and the masks
+// drive per-lane selects directly.
+typedef uint64_t lmask;
+
+__device__ __forceinline__ lmask ge_mask(float a, float b) { return __builtin_amdgcn_ballot_w64(a >= b); }
+
+// this lane's bit of m ? t : f
+__device__ __forceinline__ float lsel(lmask m, float t, float f) {
+  float r;
+  asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(f), "v"(t), "s"(m));
+  return r;
+}
+
+// 2 v + this lane's bit of m (the metadata is shifted in one bit at a time)
+__device__ __forceinline__ uint32_t push_bit(uint32_t v, lmask m) {
+  uint32_t r;
+  lmask carry;
+  asm("v_addc_co_u32_e64 %0, %1, %2, %2, %3" : "=v"(r), "=s"(carry) : "v"(v), "s"(m));
+  return r;
+}
+
+__device__ __forceinline__ lmask maj3(lmask a, lmask b, lmask c) { return (a & b) | (c & (a | b)); }
+
+// 2:4 on one group: keep masks of positions 0..3 (exactly two set per lane).
+// Position p survives iff it beats at least two of the other three, where of
+// p < q, p beats q iff |y_p| >= |y_q| (a tie goes to the lower index): six
+// comparisons, then four majority votes on the scalar unit.
+__device__ __forceinline__ void top2of4(float y0, float y1, float y2, float y3, lmask& k0, lmask& k1, lmask& k2,
+                                        lmask& k3) {
   const float a0 = fabsf(y0), a1 = fabsf(y1), a2 = fabsf(y2), a3 = fabsf(y3);
-  const float u0 = next_up(a0), u1 = next_up(a1), u2 = next_up(a2);
-  k0 = a0 >= __builtin_amdgcn_fmed3f(a1, a2, a3);
-  k1 = a1 >= __builtin_amdgcn_fmed3f(u0, a2, a3);
-  k2 = a2 >= __builtin_amdgcn_fmed3f(u0, u1, a3);
-  k3 = a3 >= __builtin_amdgcn_fmed3f(u0, u1, u2);
+  const lmask c01 = ge_mask(a0, a1), c02 = ge_mask(a0, a2), c03 = ge_mask(a0, a3);
+  const lmask c12 = ge_mask(a1, a2), c13 = ge_mask(a1, a3), c23 = ge_mask(a2, a3);
+  k0 = maj3(c01, c02, c03);
+  k1 = maj3(~c01, c12, c13);
+  k2 = maj3(~c02, ~c12, c23);
+  k3 = maj3(~c03, ~c13, ~c23);
 }
 
-template <int SEL>
-__device__ __forceinline__ void put_pair(uint32_t& word, float a, float b) {
-  word = fp4x2<SEL>(word, a, b);
+template <int SEL, class Q>
+__device__ __forceinline__ void put_pair(const Q& qz, uint32_t& word, float a, float b) {
+  word = qz.template enc2<SEL>(word, a, b);
 }
 
-__device__ __forceinline__ void put_pair_dyn(uint32_t& word, int sel, float a, float b) {
+template <class Q>
+__device__ __forceinline__ void put_pair_dyn(const Q& qz, uint32_t& word, int sel, float a, float b) {
   switch (sel & 3) {
-    case 0: put_pair<0>(word, a, b); break;
-    case 1: put_pair<1>(word, a, b); break;
-    case 2: put_pair<2>(word, a, b); break;
-    default: put_pair<3>(word, a, b); break;
+    case 0: put_pair<0>(qz, word, a, b); break;
+    case 1: put_pair<1>(qz, word, a, b); break;
+    case 2: put_pair<2>(qz, word, a, b); break;
+    default: put_pair<3>(qz, word, a, b); break;
   }
 }
 
-__device__ __forceinline__ v2f get_pair_dyn(uint32_t word, int sel) {
+// dequantized values of the two codes in byte `sel` of `word`
+template <class Q>
+__device__ __forceinline__ v2f get_pair_dyn(const Q& qz, uint32_t word, int sel) {
   switch (sel & 3) {
-    case 0: return fp4x2_decode<0>(word);
-    case 1: return fp4x2_decode<1>(word);
-    case 2: return fp4x2_decode<2>(word);
-    default: return fp4x2_decode<3>(word);
+    case 0: return qz.template dec2<0>(word);
+    case 1: return qz.template dec2<1>(word);
+    case 2: return qz.template dec2<2>(word);
+    default: return qz.template dec2<3>(word);
   }
 }
 
@@ -81,30 +109,30 @@ __device__ __forceinline__ void backbone_24(const float (&y)[32], const Q& qz, u
                                             float (&R)[32]) {
   codes[0] = codes[1] = 0u;
   meta = 0u;
-  // groups from the last to the first so the metadata is shifted in four
-  // bits at a time (small select constants stay inline)
+  // groups from the last to the first: the metadata is shifted in from its
+  // top bit down
 #pragma unroll
   for (int g = 7; g >= 0; --g) {
     const float y0 = y[4 * g], y1 = y[4 * g + 1], y2 = y[4 * g + 2], y3 = y[4 * g + 3];
-    bool k0, k1, k2, k3;
+    lmask k0, k1, k2, k3;
     top2of4(y0, y1, y2, y3, k0, k1, k2, k3);
-    const float v0 = k0 ? y0 : (k1 ? y1 : y2);            // first kept (ascending K)
-    const float v1 = k3 ? y3 : (k2 ? y2 : y1);            // second kept
-    uint32_t nib = (k0 ? 0u : (k1 ? 1u : 2u)) | (k3 ? 12u : (k2 ? 8u : 4u));
-    asm("" : "+v"(nib));   // keep the nibble a register value: folding the
-                           // shift into the select constants costs moves
-    meta = (meta << 4) | nib;
-    const float e0 = qz.enc(v0), e1 = qz.enc(v1);
+    const float v0 = lsel(k0, y0, lsel(k1, y1, y2));   // first kept (ascending K)
+    const float v1 = lsel(k3, y3, lsel(k2, y2, y1));   // second kept
+    // nibble i0 | i1 << 2: i0 = 0, 1, 2 and i1 = 3, 2, 1 as above
+    meta = push_bit(meta, k3 | k2);                    // bit 3: i1 >= 2
+    meta = push_bit(meta, k3 | ~k2);                   // bit 2: i1 odd
+    meta = push_bit(meta, ~(k0 | k1));                 // bit 1: i0 == 2
+    meta = push_bit(meta, k1 & ~k0);                   // bit 0: i0 == 1
     // the other bytes of a codes dword are written by the groups that follow
     // in this loop, so the dword's first group may start from any register
-    if ((g & 3) == 3) codes[g >> 2] = __float_as_uint(e0);
-    put_pair_dyn(codes[g >> 2], g, e0, e1);
-    const v2f d = get_pair_dyn(codes[g >> 2], g);
-    const float r0 = v0 - qz.dec(d.x), r1 = v1 - qz.dec(d.y);
-    R[4 * g + 0] = k0 ? r0 : y0;
-    R[4 * g + 1] = k1 ? (k0 ? r1 : r0) : y1;
-    R[4 * g + 2] = k2 ? (k3 ? r0 : r1) : y2;
-    R[4 * g + 3] = k3 ? r1 : y3;
+    if ((g & 3) == 3) codes[g >> 2] = __float_as_uint(v0);
+    put_pair_dyn(qz, codes[g >> 2], g, v0, v1);
+    const v2f d = get_pair_dyn(qz, codes[g >> 2], g);
+    const float r0 = v0 - d.x, r1 = v1 - d.y;
+    R[4 * g + 0] = lsel(k0, r0, y0);
+    R[4 * g + 1] = lsel(k1, lsel(k0, r1, r0), y1);
+    R[4 * g + 2] = lsel(k2, lsel(k3, r0, r1), y2);
+    R[4 * g + 3] = lsel(k3, r1, y3);
   }
 }
 
@@ -146,11 +174,11 @@ __device__ __forceinline__ void backbone_48(const float (&y)[32], const Q& qz, u
     }
     meta |= mask << (8 * g);
     int byte0 = 2 * g;   // group g's four codes occupy bytes 2g, 2g+1 of the 8
-    put_pair_dyn(codes[byte0 >> 2], byte0, qz.enc(v[0]), qz.enc(v[1]));
-    put_pair_dyn(codes[(byte0 + 1) >> 2], byte0 + 1, qz.enc(v[2]), qz.enc(v[3]));
-    v2f d01 = get_pair_dyn(codes[byte0 >> 2], byte0);
-    v2f d23 = get_pair_dyn(codes[(byte0 + 1) >> 2], byte0 + 1);
-    float d[4] = {qz.dec(d01.x), qz.dec(d01.y), qz.dec(d23.x), qz.dec(d23.y)};
+    put_pair_dyn(qz, codes[byte0 >> 2], byte0, v[0], v[1]);
+    put_pair_dyn(qz, codes[(byte0 + 1) >> 2], byte0 + 1, v[2], v[3]);
+    const v2f d01 = get_pair_dyn(qz, codes[byte0 >> 2], byte0);
+    const v2f d23 = get_pair_dyn(qz, codes[(byte0 + 1) >> 2], byte0 + 1);
+    float d[4] = {d01.x, d01.y, d23.x, d23.y};
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
       float dp = 0.0f;
@@ -183,7 +211,7 @@ __device__ __forceinline__ void block_mx(const float (&y)[32], uint8_t* __restri
                                          uint8_t* __restrict__ sps, uint8_t* __restrict__ dnc,
                                          uint8_t* __restrict__ dns) {
   const int e = mx_exponent(__float_as_uint(absmax32(y)));
-  const MxQ qb{exp2_neg(e), exp2_int(e)};
+  const MxQ qb = MxQ::make(e);
   uint32_t codes[2], meta;
   float R[32];
   if (PAT == 24)
@@ -191,7 +219,7 @@ __device__ __forceinline__ void block_mx(const float (&y)[32], uint8_t* __restri
   else
     backbone_48(y, qb, codes, meta, R);
   const int er = mx_exponent(__float_as_uint(absmax32(R)));
-  const MxQ qr{exp2_neg(er), exp2_int(er)};
+  const MxQ qr = MxQ::make(er);
   uint32_t dn[4];
 #pragma unroll
   for (int w = 0; w < 4; ++w) dn[w] = enc8(R + 8 * w, qr);
@@ -341,11 +369,8 @@ __device__ __forceinline__ float load_row_rms(const uint4* xr, int lane, int nbl
   return (float)(1.0 / __builtin_sqrt((double)chunk[0] / (double)K + (double)eps));
 }
 
-// y = (x * r) * gamma for one block.
-__device__ __forceinline__ void norm_block(const uint4 (&xq)[4], const uint4* gr, int b, float r, float (&y)[32]) {
-  uint4 gq[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) gq[j] = gr[4 * b + j];
+// y = (x * r) * gamma for one block (gq: the block's 32 bf16 gamma values).
+__device__ __forceinline__ void norm_block(const uint4 (&xq)[4], const uint4 (&gq)[4], float r, float (&y)[32]) {
   float x[32], g[32];
   unpack_bf16x32(xq, x);
   unpack_bf16x32(gq, g);
@@ -375,8 +400,11 @@ __global__ __launch_bounds__(256) void k_prep_norm(const uint16_t* __restrict__ 
   for (int i = 0; i < NB; ++i) {
     const int b = lane + 64 * i;
     if (b >= nblk) break;
+    uint4 gq[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) gq[j] = gr[4 * b + j];
     float y[32];
-    norm_block(xs[i], gr, b, r, y);
+    norm_block(xs[i], gq, r, y);
     block_out_write<PAT, NV>(y, o, row, b, S, six_s);
   }
 }
@@ -433,6 +461,11 @@ __global__ __launch_bounds__(256) void k_prep_norm_split(const uint16_t* __restr
     }
   };
 
+  // this lane's gamma block, loaded once with the first rows so that its
+  // latency is not on the path after the reduction
+  uint4 gq[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) gq[j] = b < nblk ? gr[4 * b + j] : make_uint4(0u, 0u, 0u, 0u);
   uint4 xq[4], xn[4];
   int grp = blockIdx.x;
   if (grp < groups) load(grp, xq);
@@ -457,7 +490,7 @@ __global__ __launch_bounds__(256) void k_prep_norm_split(const uint16_t* __restr
     const int64_t row = (int64_t)grp * RPG + wave / C;
     if (row < M && b < nblk) {
       float y[32];
-      norm_block(xq, gr, b, r, y);
+      norm_block(xq, gq, r, y);
       block_out_write<PAT, NV>(y, o, row, b, S, six_s);
     }
 #pragma unroll
@@ -533,8 +566,11 @@ __global__ __launch_bounds__(256) void k_amax_norm(const uint16_t* __restrict__ 
   for (int i = 0; i < NB; ++i) {
     const int b = lane + 64 * i;
     if (b >= nblk) break;
+    uint4 gq[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) gq[j] = gr[4 * b + j];
     float y[32];
-    norm_block(xs[i], gr, b, r, y);
+    norm_block(xs[i], gq, r, y);
     m = fmaxf(m, absmax32(y));
   }
   m = wave_max(m);

@@ -55,8 +55,7 @@ __global__ __launch_bounds__(256) void k_wquant_mx(const T* __restrict__ W, int 
 #pragma unroll
   for (int k = 0; k < 32; ++k) amax = fmaxf(amax, fabsf(v[k]));
   const int e = mx_exponent(__float_as_uint(amax));
-  const float inv = exp2_neg(e);
-  const MxQ qz{inv, 1.0f};
+  const MxQ qz = MxQ::make(e);
   uint32_t q[4];
 #pragma unroll
   for (int w = 0; w < 4; ++w) q[w] = enc8(v + 8 * w, qz);
