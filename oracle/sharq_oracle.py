@@ -42,6 +42,11 @@ Readings where the paper is silent (each also listed in the design notes):
       a zero block scale gives signed-zero codes.  Backbone blocks 32 logical
       positions, residual blocks 16.  Weights: one E4M3 scale per 32 shared by
       both paths, the dense view duplicating it per 16.
+  R8  NVFP4's 4:8 in pairs (App. A.1.4 "Sparsity support"; Fig. 2 "pair-topk"):
+      the 8 positions of a group form 4 pairs (2i, 2i+1) and 2 whole pairs
+      survive.  A pair's score is the larger magnitude of its two elements,
+      so the group maximum is always kept; of equal scores the lower pair
+      wins.  Metadata: the same 8-bit keep mask per group as plain 4:8.
 """
 
 from __future__ import annotations
@@ -245,6 +250,32 @@ def nm_mask(y: np.ndarray, n: int, m: int) -> np.ndarray:
                 beats = beats | (a[..., kp] == a[..., k])
             rank[..., k] += beats
     return (rank < n).reshape(T, K)
+
+
+def nm_pair_mask(y: np.ndarray, n: int, m: int) -> np.ndarray:
+    """n:m selection in pairs (reading R8): the m positions of a group are m/2
+    adjacent pairs, and the n/2 pairs with the largest pair scores survive.
+
+    score_i = max(|y_2i|, |y_2i+1|); pair i is kept iff
+    #{j : score_j > score_i, or score_j == score_i and j < i} < n/2,
+    and a kept pair keeps both of its positions.
+    """
+    y = np.asarray(y, dtype=np.float32)
+    T, K = y.shape
+    a = np.abs(y).reshape(T, K // m, m // 2, 2)
+    score = a.max(axis=3)
+    P = m // 2
+    rank = np.zeros(score.shape, dtype=np.int64)
+    for i in range(P):
+        for j in range(P):
+            if j == i:
+                continue
+            beats = score[..., j] > score[..., i]
+            if j < i:
+                beats = beats | (score[..., j] == score[..., i])
+            rank[..., i] += beats
+    keep_pair = rank < n // 2
+    return np.repeat(keep_pair, 2, axis=2).reshape(T, K)
 
 
 # ---------------------------------------------------------------------------
@@ -458,11 +489,11 @@ def weight_from_device_layout(bufs: dict, N: int, K: int, fmt: str, tensor_scale
 # ---------------------------------------------------------------------------
 
 def prepare(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: int, m: int,
-            fmt: str = "mx", tensor_scale: float | None = None) -> dict:
+            fmt: str = "mx", tensor_scale: float | None = None, pairs: bool = False) -> dict:
     """Activation preparation for one linear call.
 
     1. y = RMSNorm(x) * gamma (or y = x);
-    2. keep = top-n of |y| per group of m;
+    2. keep = top-n of |y| per group of m (pairs: the top n/2 pairs, R8);
     3. backbone: quantize y on the kept positions (X_sp = M(X) o X, then Q_sp);
     4. residual R = y - D_sp(Q_sp(X_sp)), taken against the dequantized backbone;
     5. quantize R densely (Q_dn).
@@ -472,8 +503,13 @@ def prepare(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: in
     T, K = x.shape
     g = None if gamma_bf16 is None else bf16_bits_to_f32(gamma_bf16)
     y, r = rmsnorm(x, g, eps)
-    keep = nm_mask(y, n, m) if n > 0 else np.zeros(y.shape, dtype=bool)
-    out = {"rows": T, "K": K, "n": n, "m": m, "fmt": fmt, "y": y, "r": r, "keep": keep}
+    if n == 0:
+        keep = np.zeros(y.shape, dtype=bool)
+    elif pairs:
+        keep = nm_pair_mask(y, n, m)
+    else:
+        keep = nm_mask(y, n, m)
+    out = {"rows": T, "K": K, "n": n, "m": m, "pairs": pairs, "fmt": fmt, "y": y, "r": r, "keep": keep}
     if fmt == "mx":
         sp_c, _, sp_s, d_sp = mx_quantize(y, keep)
         R = (y - d_sp).astype(np.float32)

@@ -132,6 +132,68 @@ def test_mask_exactly_n_and_keeps_group_max():
         assert np.all(np.take_along_axis(g, first_max[..., None], axis=2))
 
 
+def test_pair_mask_is_brute_force_dominant_pair_set():
+    """4:8 in pairs (App. A.1.4): of the 6 ways to keep 2 of the 4 pairs, the
+    kept one is the only set whose every pair outranks every dropped pair
+    (larger score max(|y_2i|, |y_2i+1|), or equal score and lower pair)."""
+    rng = np.random.default_rng(11)
+    y = np.concatenate([rng.integers(-3, 4, size=(300, 8)).astype(np.float32),
+                        rng.standard_normal((300, 8)).astype(np.float32)], axis=0)
+    keep = O.nm_pair_mask(y, 4, 8)
+    for row, k in zip(y, keep):
+        score = [max(abs(float(row[2 * i])), abs(float(row[2 * i + 1]))) for i in range(4)]
+        outranks = lambda i, j: score[i] > score[j] or (score[i] == score[j] and i < j)
+        dominant = [S for S in itertools.combinations(range(4), 2)
+                    if all(outranks(i, j) for i in S for j in range(4) if j not in S)]
+        assert len(dominant) == 1
+        want = np.zeros(8, dtype=bool)
+        for i in dominant[0]:
+            want[2 * i] = want[2 * i + 1] = True
+        assert np.array_equal(k, want)
+
+
+def test_pair_mask_whole_pairs_and_group_max():
+    x = synth.activations(16, 256, seed=6)
+    y = O.bf16_bits_to_f32(x)
+    keep = O.nm_pair_mask(y, 4, 8)
+    g = keep.reshape(16, -1, 8)
+    assert np.all(g.sum(axis=2) == 4)
+    assert np.array_equal(g[..., 0::2], g[..., 1::2])          # whole pairs
+    a = np.abs(y).reshape(16, -1, 8)
+    first_max = np.argmax(a, axis=2)
+    assert np.all(np.take_along_axis(g, first_max[..., None], axis=2))
+
+
+def test_pair_mask_reduces_to_plain_4of8_on_equal_pairs():
+    """When both elements of every pair have the same magnitude and the pair
+    magnitudes are distinct, the top 2 pairs are exactly the top 4 elements."""
+    rng = np.random.default_rng(12)
+    mags = np.stack([rng.permutation(4) + 1.0 for _ in range(500)]).astype(np.float32)   # distinct per group
+    y = np.repeat(mags, 2, axis=1) * rng.choice([-1.0, 1.0], size=(500, 8)).astype(np.float32)
+    assert np.array_equal(O.nm_pair_mask(y, 4, 8), O.nm_mask(y, 4, 8))
+
+
+def test_prepare_in_pairs_backbone_and_residual():
+    """NVFP4 with 4:8 in pairs (the paper's primary instantiation): the packed
+    backbone round-trips to whole pairs, the backbone scale equals the dense
+    block scale (the group maximum is kept), and y = d_sp + R exactly where R
+    is the residual before its own quantization."""
+    x = synth.activations(12, 256, seed=7)
+    g = synth.gamma(256, seed=7)
+    for fmt in ("nv", "mx"):
+        o = O.prepare(x, g, 1e-6, 4, 8, fmt, pairs=True)
+        dense, keep = O.unpack_backbone(o["sp_codes"], o["sp_meta"], 256, 4, 8)
+        assert np.array_equal(keep, o["keep"])
+        kk = keep.reshape(12, -1, 8)
+        assert np.array_equal(kk[..., 0::2], kk[..., 1::2])
+        assert np.array_equal(o["R"][~keep], o["y"][~keep])
+        if fmt == "mx":   # exact residual and the dense block scale (Sterbenz, group max kept)
+            y = o["y"].astype(np.float64)
+            assert np.array_equal(y, o["d_sp"].astype(np.float64) + o["R"].astype(np.float64))
+            dense_e = O.e8m0_exponent(np.abs(o["y"]).reshape(12, -1, 32).max(axis=2))
+            assert np.array_equal(o["sp_scale"].astype(np.int64) - 127, dense_e)
+
+
 # ----------------------------------------------------------------------------- RMSNorm
 
 def test_rms_tree_equals_recursive_traversal():
