@@ -72,9 +72,14 @@ typedef enum { SHARQ_MXFP4 = 0, SHARQ_NVFP4 = 1 } sharq_format;
 typedef enum { SHARQ_BF16 = 0, SHARQ_F16 = 1, SHARQ_F32 = 2 } sharq_dtype;
 
 /* N:M activation pattern: keep the n largest magnitudes of every m consecutive
- * K positions (eq. "dynamic-mask").  Built: 2:4 and 4:8. */
+ * K positions (eq. "dynamic-mask").  pairs = 1 selects in pairs, NVFP4's
+ * "4:8 in pairs" (App. A.1.4; Fig. 2 "pair-topk"): the m positions of a group
+ * are m/2 adjacent pairs (2i, 2i+1), and the n/2 pairs with the largest score
+ * max(|y_2i|, |y_2i+1|) survive whole (ties -> lower pair).  Built: 2:4, 4:8
+ * and 4:8 in pairs (with either format). */
 typedef struct {
   int32_t n, m;
+  int32_t pairs;   /* 0: element-wise top-n, 1: in pairs */
 } sharq_pattern;
 
 /*
@@ -88,8 +93,9 @@ typedef struct {
  *   sp_meta  [rows][K/8]      which positions were kept.  2:4: per group of 4
  *                             the two kept indices i0 < i1 as i0 | i1 << 2 (a
  *                             nibble), two groups per byte, even group low.
- *                             4:8: per group of 8 an 8-bit keep mask (bit p =
- *                             position p kept).  4-byte aligned.
+ *                             4:8 (also in pairs): per group of 8 an 8-bit
+ *                             keep mask (bit p = position p kept).  4-byte
+ *                             aligned.
  *   sp_scale [rows][K/32]     backbone block scale per 32 logical K positions
  *                             (Fig. 2 "sparse group-32 scales"): E8M0 (MXFP4)
  *                             or E4M3 (NVFP4).
@@ -163,7 +169,8 @@ SHARQ_API sharq_status sharq_quantize_weight(const void *W, sharq_dtype wdt, int
  *   1. if gamma != NULL (bf16 [K]): y = (x * r) * gamma with
  *      r = 1/sqrt(mean(x^2) + eps) (sum of squares as a balanced binary tree
  *      in fp32, r rounded from fp64); else y = x;
- *   2. keeps the n largest |y| of every group of m (ties -> lower index);
+ *   2. keeps the n largest |y| of every group of m (ties -> lower index),
+ *      or the n/2 best pairs when nm.pairs = 1;
  *   3. quantizes the kept values per 32 logical positions (backbone);
  *   4. forms the residual R = y - dequant(backbone) (eq. "sharq-residual");
  *   5. quantizes R densely.

@@ -35,13 +35,18 @@ constexpr int kMaxExperts = 1024;
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-// 24 for 2:4, 48 for 4:8, 0 if the pattern is valid but not built, -1 if invalid
+// 24 for 2:4, 48 for 4:8, 49 for 4:8 in pairs, 0 if the pattern is valid but
+// not built, -1 if invalid
 int pattern_id(sharq_pattern nm) {
-  if (nm.m <= 0 || nm.n < 0 || nm.n > nm.m) return -1;
-  if (nm.n == 2 && nm.m == 4) return 24;
-  if (nm.n == 4 && nm.m == 8) return 48;
+  if (nm.m <= 0 || nm.n < 0 || nm.n > nm.m || (nm.pairs != 0 && nm.pairs != 1)) return -1;
+  if (nm.pairs && (nm.m % 2 != 0 || nm.n % 2 != 0)) return -1;
+  if (!nm.pairs && nm.n == 2 && nm.m == 4) return 24;
+  if (nm.n == 4 && nm.m == 8) return nm.pairs ? 49 : 48;
   return 0;
 }
+
+// The GEMMs read the metadata only: 4:8 in pairs has the 4:8 keep-mask layout.
+int gemm_pattern(int pid) { return pid == 49 ? 48 : pid; }
 
 sharq_status hip_status(hipError_t e) { return e == hipSuccess ? SHARQ_OK : SHARQ_EHIP; }
 
@@ -148,7 +153,8 @@ sharq_status sharq_prepare(const void* X, sharq_dtype xdt, int64_t M, int64_t K,
   if (!X && M > 0) return SHARQ_EINVAL;
   const int pid = pattern_id(nm);
   if (pid < 0 || K % nm.m != 0) return SHARQ_EINVAL;
-  if (out->rows != M || out->K != K || out->fmt != fmt || out->nm.n != nm.n || out->nm.m != nm.m)
+  if (out->rows != M || out->K != K || out->fmt != fmt || out->nm.n != nm.n || out->nm.m != nm.m ||
+      out->nm.pairs != nm.pairs)
     return SHARQ_EINVAL;
   if (xdt != SHARQ_BF16) return SHARQ_EUNSUPPORTED;
   if (!(eps >= 0.0f)) return SHARQ_EINVAL;
@@ -180,10 +186,10 @@ sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sh
   if (a->rows == 0 || w->N == 0) return SHARQ_OK;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   if (a->fmt == SHARQ_NVFP4)
-    return hip_status(sharq::launch_linear_nv(pattern_id(a->nm), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale,
+    return hip_status(sharq::launch_linear_nv(gemm_pattern(pattern_id(a->nm)), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale,
                                               a->dn_codes, a->dn_scale, a->tensor_scale, a->rows, w->codes,
                                               w->scale, w->tensor_scale, (int)w->N, (int)w->K, Y, ldy, st));
-  return hip_status(sharq::launch_linear_mx(pattern_id(a->nm), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale,
+  return hip_status(sharq::launch_linear_mx(gemm_pattern(pattern_id(a->nm)), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale,
                                             a->dn_codes, a->dn_scale, a->rows, w->codes, w->scale, (int)w->N,
                                             (int)w->K, Y, ldy, st));
 }
@@ -207,7 +213,7 @@ sharq_status sharq_linear_grouped(const sharq_act* a, const int32_t* row_index, 
     return SHARQ_EALIGN;
   if (total == 0 || w->N == 0) return SHARQ_OK;
   return hip_status(sharq::launch_linear_mx_grouped(
-      pattern_id(a->nm), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale, a->dn_codes, a->dn_scale, row_index,
+      gemm_pattern(pattern_id(a->nm)), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale, a->dn_codes, a->dn_scale, row_index,
       a->rows, expert_offsets, (int)w->experts, total, w->codes, w->scale, (int)w->N, (int)w->K, Y, ldy,
       reinterpret_cast<hipStream_t>(stream)));
 }

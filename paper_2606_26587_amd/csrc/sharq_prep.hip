@@ -190,6 +190,54 @@ __device__ __forceinline__ void backbone_48(const float (&y)[32], const Q& qz, u
   }
 }
 
+// Backbone of one block for NVFP4's 4:8 in pairs (App. A.1.4): the 8
+// positions of a group are 4 adjacent pairs and the 2 pairs with the largest
+// scores max(|y_2i|, |y_2i+1|) survive, a tie going to the lower pair -- the
+// 2:4 selection applied to the pair scores.  The group maximum lies in a kept
+// pair, so the block maximum of the backbone is that of y.  Metadata: the 8-bit
+// keep mask of plain 4:8 (whole pairs set).
+template <class Q>
+__device__ __forceinline__ void backbone_48p(const float (&y)[32], const Q& qz, uint32_t (&codes)[2],
+                                             uint32_t& meta, float (&R)[32]) {
+  codes[0] = codes[1] = 0u;
+  meta = 0u;
+  // groups from the last to the first: the metadata is shifted in from its
+  // top bit down
+#pragma unroll
+  for (int g = 3; g >= 0; --g) {
+    const float* e = y + 8 * g;
+    const float s0 = fmaxf(fabsf(e[0]), fabsf(e[1])), s1 = fmaxf(fabsf(e[2]), fabsf(e[3]));
+    const float s2 = fmaxf(fabsf(e[4]), fabsf(e[5])), s3 = fmaxf(fabsf(e[6]), fabsf(e[7]));
+    lmask p0, p1, p2, p3;
+    top2of4(s0, s1, s2, s3, p0, p1, p2, p3);
+    // first kept pair (a) and second (b), ascending K
+    const float a0 = lsel(p0, e[0], lsel(p1, e[2], e[4])), a1 = lsel(p0, e[1], lsel(p1, e[3], e[5]));
+    const float b0 = lsel(p3, e[6], lsel(p2, e[4], e[2])), b1 = lsel(p3, e[7], lsel(p2, e[5], e[3]));
+    meta = push_bit(meta, p3);
+    meta = push_bit(meta, p3);
+    meta = push_bit(meta, p2);
+    meta = push_bit(meta, p2);
+    meta = push_bit(meta, p1);
+    meta = push_bit(meta, p1);
+    meta = push_bit(meta, p0);
+    meta = push_bit(meta, p0);
+    // the group's four codes go to bytes 2 g (pair a) and 2 g + 1 (pair b)
+    put_pair_dyn(qz, codes[g >> 1], 2 * g, a0, a1);
+    put_pair_dyn(qz, codes[g >> 1], 2 * g + 1, b0, b1);
+    const v2f da = get_pair_dyn(qz, codes[g >> 1], 2 * g);
+    const v2f db = get_pair_dyn(qz, codes[g >> 1], 2 * g + 1);
+    const float ra0 = a0 - da.x, ra1 = a1 - da.y, rb0 = b0 - db.x, rb1 = b1 - db.y;
+    R[8 * g + 0] = lsel(p0, ra0, e[0]);
+    R[8 * g + 1] = lsel(p0, ra1, e[1]);
+    R[8 * g + 2] = lsel(p1, lsel(p0, rb0, ra0), e[2]);
+    R[8 * g + 3] = lsel(p1, lsel(p0, rb1, ra1), e[3]);
+    R[8 * g + 4] = lsel(p2, lsel(p3, ra0, rb0), e[4]);
+    R[8 * g + 5] = lsel(p2, lsel(p3, ra1, rb1), e[5]);
+    R[8 * g + 6] = lsel(p3, rb0, e[6]);
+    R[8 * g + 7] = lsel(p3, rb1, e[7]);
+  }
+}
+
 __device__ __forceinline__ float absmax32(const float* v) {
   float m = 0.0f;
 #pragma unroll
@@ -216,6 +264,8 @@ __device__ __forceinline__ void block_mx(const float (&y)[32], uint8_t* __restri
   float R[32];
   if (PAT == 24)
     backbone_24(y, qb, codes, meta, R);
+  else if (PAT == 49)
+    backbone_48p(y, qb, codes, meta, R);
   else
     backbone_48(y, qb, codes, meta, R);
   const int er = mx_exponent(__float_as_uint(absmax32(R)));
@@ -241,6 +291,8 @@ __device__ __forceinline__ void block_nv(const float (&y)[32], float S, float si
   float R[32];
   if (PAT == 24)
     backbone_24(y, qb, codes, meta, R);
+  else if (PAT == 49)
+    backbone_48p(y, qb, codes, meta, R);
   else
     backbone_48(y, qb, codes, meta, R);
   const NvQ q0 = NvQ::make(absmax16(R), six_s, S);
@@ -661,9 +713,11 @@ hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint1
       k_pts_finalize<<<1, 1, 0, st>>>(slot);
     }
     if (pat == 24) go_prep<24, true>(X, M, K, ldx, gamma, eps, o, ts_out, grid, st);
+    else if (pat == 49) go_prep<49, true>(X, M, K, ldx, gamma, eps, o, ts_out, grid, st);
     else go_prep<48, true>(X, M, K, ldx, gamma, eps, o, ts_out, grid, st);
   } else {
     if (pat == 24) go_prep<24, false>(X, M, K, ldx, gamma, eps, o, nullptr, grid, st);
+    else if (pat == 49) go_prep<49, false>(X, M, K, ldx, gamma, eps, o, nullptr, grid, st);
     else go_prep<48, false>(X, M, K, ldx, gamma, eps, o, nullptr, grid, st);
   }
   return hipGetLastError();

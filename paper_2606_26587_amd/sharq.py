@@ -32,7 +32,7 @@ class SharqError(RuntimeError):
 
 
 class Pattern(ctypes.Structure):
-    _fields_ = [("n", ctypes.c_int32), ("m", ctypes.c_int32)]
+    _fields_ = [("n", ctypes.c_int32), ("m", ctypes.c_int32), ("pairs", ctypes.c_int32)]
 
 
 class ActStruct(ctypes.Structure):
@@ -109,9 +109,10 @@ class PreparedAct:
     dn_codes: torch.Tensor
     dn_scale: torch.Tensor
     tensor_scale: Optional[torch.Tensor] = None
+    pairs: bool = False
 
     def struct(self) -> ActStruct:
-        return ActStruct(self.rows, self.K, self.fmt, Pattern(self.n, self.m), self.sp_codes.data_ptr(),
+        return ActStruct(self.rows, self.K, self.fmt, Pattern(self.n, self.m, int(self.pairs)), self.sp_codes.data_ptr(),
                          self.sp_meta.data_ptr(), self.sp_scale.data_ptr(), self.dn_codes.data_ptr(),
                          self.dn_scale.data_ptr(),
                          None if self.tensor_scale is None else self.tensor_scale.data_ptr())
@@ -135,15 +136,16 @@ class QuantWeight:
                             None if self.tensor_scale is None else self.tensor_scale.data_ptr())
 
 
-def alloc_act(rows: int, K: int, n: int = 2, m: int = 4, fmt="mx", device="cuda") -> PreparedAct:
-    """Device buffers of a prepared activation (flat, panel-major; see include/sharq.h)."""
+def alloc_act(rows: int, K: int, n: int = 2, m: int = 4, fmt="mx", device="cuda", pairs: bool = False) -> PreparedAct:
+    """Device buffers of a prepared activation (flat, panel-major; see include/sharq.h).
+    pairs=True: n:m selection in pairs (4:8 in pairs)."""
     f = _FMT[fmt] if isinstance(fmt, str) else fmt
-    sizes = [lib.sharq_act_buffer_bytes(rows, K, f, Pattern(n, m), w) for w in range(5)]
+    sizes = [lib.sharq_act_buffer_bytes(rows, K, f, Pattern(n, m, int(pairs)), w) for w in range(5)]
     if K <= 0 or K % 32 or (rows > 0 and min(sizes) == 0):
         raise SharqError(EINVAL, "alloc_act")
     bufs = [torch.empty(sz, dtype=torch.uint8, device=device) for sz in sizes]
     ts = torch.empty(1, dtype=torch.float32, device=device) if f == NVFP4 else None
-    return PreparedAct(rows, K, f, n, m, *bufs, tensor_scale=ts)
+    return PreparedAct(rows, K, f, n, m, *bufs, tensor_scale=ts, pairs=pairs)
 
 
 def alloc_weight(N: int, K: int, fmt="mx", experts: int = 1, device="cuda") -> QuantWeight:
@@ -173,15 +175,16 @@ def sharq_quantize_weight(w: torch.Tensor, fmt="mx", out: Optional[QuantWeight] 
 
 def sharq_prepare(x: torch.Tensor, gamma: Optional[torch.Tensor], eps: float = 1e-6, n: int = 2, m: int = 4,
                   fmt="mx", tensor_scale_in: Optional[torch.Tensor] = None, out: Optional[PreparedAct] = None,
-                  stream=None) -> PreparedAct:
-    """Fused preparation of activation rows X [M, K] (bf16, on the GPU)."""
+                  stream=None, pairs: bool = False) -> PreparedAct:
+    """Fused preparation of activation rows X [M, K] (bf16, on the GPU).
+    pairs=True: n:m selection in pairs (NVFP4's 4:8 in pairs)."""
     M, K = x.shape
     if out is None:
-        out = alloc_act(M, K, n, m, fmt, x.device)
+        out = alloc_act(M, K, n, m, fmt, x.device, pairs)
     f = _FMT[fmt] if isinstance(fmt, str) else fmt
     st = out.struct()
     _check(lib.sharq_prepare(_ptr(x), _DT.get(x.dtype, -1), M, K, x.stride(0), _ptr(gamma), ctypes.c_float(eps),
-                             Pattern(n, m), f, _ptr(tensor_scale_in), ctypes.byref(st), _stream(stream)),
+                             Pattern(n, m, int(pairs)), f, _ptr(tensor_scale_in), ctypes.byref(st), _stream(stream)),
            "sharq_prepare")
     return out
 

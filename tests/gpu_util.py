@@ -40,7 +40,7 @@ def oracle_to_act(o: dict) -> S.PreparedAct:
         ts = torch.tensor([float(o["tensor_scale"])], dtype=torch.float32, device="cuda")
     return S.PreparedAct(o["dn_codes"].shape[0], o["K"], fmt, o["n"], o["m"], dev_u8(dev["sp_codes"]),
                          dev_u8(dev["sp_meta"]), dev_u8(dev["sp_scale"]), dev_u8(dev["dn_codes"]),
-                         dev_u8(dev["dn_scale"]), tensor_scale=ts)
+                         dev_u8(dev["dn_scale"]), tensor_scale=ts, pairs=bool(o.get("pairs", False)))
 
 
 def oracle_to_weight(o: dict) -> S.QuantWeight:

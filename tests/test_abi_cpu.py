@@ -17,7 +17,7 @@ OK, EINVAL, EUNSUPPORTED, EALIGN = 0, 1, 2, 3
 
 
 class Pattern(ctypes.Structure):
-    _fields_ = [("n", ctypes.c_int32), ("m", ctypes.c_int32)]
+    _fields_ = [("n", ctypes.c_int32), ("m", ctypes.c_int32), ("pairs", ctypes.c_int32)]
 
 
 class Act(ctypes.Structure):
@@ -75,6 +75,9 @@ def test_buffer_sizes(L):
     nv = [L.sharq_act_buffer_bytes(rows, K, 1, Pattern(4, 8), w) for w in range(5)]
     assert nv[4] == rows * K // 16 and nv[0] == rows * K // 4
     assert L.sharq_act_buffer_bytes(rows, 100, 0, Pattern(2, 4), 0) == 0
+    # 4:8 in pairs has the 4:8 layout
+    assert [L.sharq_act_buffer_bytes(rows, K, 1, Pattern(4, 8, 1), w) for w in range(5)] == nv
+    assert L.sharq_act_buffer_bytes(rows, K, 1, Pattern(3, 8, 1), 0) == 0   # odd n cannot be whole pairs
     assert L.sharq_weight_buffer_bytes(64, 128, 0, 0) == 64 * 64
     assert L.sharq_weight_buffer_bytes(64, 128, 1, 2) == 64 * 8
 
@@ -82,8 +85,8 @@ def test_buffer_sizes(L):
 FAKE = 1 << 20   # never dereferenced: every case below is rejected (or empty) before any launch
 
 
-def act(rows=8, K=128, n=2, m=4, fmt=0, off=0):
-    return Act(rows, K, fmt, Pattern(n, m), FAKE + off, FAKE, FAKE, FAKE, FAKE, None)
+def act(rows=8, K=128, n=2, m=4, fmt=0, off=0, pairs=0):
+    return Act(rows, K, fmt, Pattern(n, m, pairs), FAKE + off, FAKE, FAKE, FAKE, FAKE, None)
 
 
 @pytest.mark.parametrize("kw,M,K,ldx,nm,expect", [
@@ -100,6 +103,26 @@ def test_prepare_rejects(L, kw, M, K, ldx, nm, expect):
         a = act(rows=M, K=128, n=4, m=8)   # out->K disagrees with K
     st = L.sharq_prepare(FAKE, 0, M, K, ldx, None, 1e-6, Pattern(*nm), 0, None, ctypes.byref(a), None)
     assert st == expect
+
+
+@pytest.mark.parametrize("nm,expect", [
+    ((4, 8, 2), EINVAL),         # pairs must be 0 or 1
+    ((3, 8, 1), EINVAL),         # odd n: not whole pairs
+    ((2, 4, 1), EUNSUPPORTED),   # 2:4 in pairs (one pair of two) is valid but not built
+    ((2, 8, 1), EUNSUPPORTED),
+])
+def test_prepare_pair_patterns(L, nm, expect):
+    a = act(rows=8, K=128, n=nm[0], m=nm[1], pairs=nm[2])
+    assert L.sharq_prepare(FAKE, 0, 8, 128, 128, None, 1e-6, Pattern(*nm), 0, None, ctypes.byref(a), None) == expect
+
+
+def test_prepare_pairs_must_match_out(L):
+    a = act(rows=8, K=128, n=4, m=8, pairs=0)
+    assert L.sharq_prepare(FAKE, 0, 8, 128, 128, None, 1e-6, Pattern(4, 8, 1), 0, None, ctypes.byref(a),
+                           None) == EINVAL
+    empty = act(rows=0, K=128, n=4, m=8, pairs=1)
+    assert L.sharq_prepare(FAKE, 0, 0, 128, 128, None, 1e-6, Pattern(4, 8, 1), 0, None, ctypes.byref(empty),
+                           None) == OK
 
 
 def test_prepare_null_and_alignment(L):
