@@ -16,6 +16,8 @@ Other workloads (--workload), one JSON line each:
   llama-decode  the same three linears at M = 1, 16, 64, 256 (weight-stream bound)
   qwen-nvfp4    Qwen2.5-7B gate/up and down at M = 4096, NVFP4 with the dynamic
                 per-tensor scale pre-pass
+  llama-nvfp4-pairs  the Llama prefill linears in the paper's own setting:
+                NVFP4 with the 4:8 in-pairs backbone
   moe           Qwen3-30B-A3B expert layers, 4096 tokens, top-8 of 128 experts,
                 4:8 backbone, grouped GEMMs
 --calibrate-copy MiB runs a plain device copy of that size (the reference
@@ -164,7 +166,7 @@ def base_record(args, metric, value, unit, ms_step, dtype, config):
 # workloads
 # ---------------------------------------------------------------------------
 
-def dense_layers(torch, S, synth, dev, shapes, T, fmt, n, m, n_sets):
+def dense_layers(torch, S, synth, dev, shapes, T, fmt, n, m, n_sets, pairs=False):
     def to_dev(u16):
         return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).to(dev)
     layers = []
@@ -172,20 +174,20 @@ def dense_layers(torch, S, synth, dev, shapes, T, fmt, n, m, n_sets):
         xs = [to_dev(synth.activations(T, K, seed=s)) for s in range(n_sets)]
         g = to_dev(synth.gamma(K, seed=0)) if norm else None
         w = S.sharq_quantize_weight(to_dev(synth.weight(N, K, seed=0)), fmt)
-        acts = [S.alloc_act(T, K, n, m, fmt, dev) for _ in range(n_sets)]
+        acts = [S.alloc_act(T, K, n, m, fmt, dev, pairs) for _ in range(n_sets)]
         ys = [torch.empty((T, N), dtype=torch.bfloat16, device=dev) for _ in range(n_sets)]
         layers.append(dict(name=name, K=K, N=N, norm=norm, xs=xs, g=g, w=w, acts=acts, ys=ys))
     torch.cuda.synchronize()
     return layers
 
 
-def dense_step(S, layers, stream, eps, n, m, fmt, n_sets):
+def dense_step(S, layers, stream, eps, n, m, fmt, n_sets, pairs=False):
     def step(i, mark):
         j = i % n_sets
         for li, L in enumerate(layers):
             if mark:
                 mark(2 * li)
-            S.sharq_prepare(L["xs"][j], L["g"], eps, n, m, fmt, out=L["acts"][j], stream=stream)
+            S.sharq_prepare(L["xs"][j], L["g"], eps, n, m, fmt, out=L["acts"][j], stream=stream, pairs=pairs)
             if mark:
                 mark(2 * li + 1)
             S.sharq_linear(L["acts"][j], L["w"], out=L["ys"][j], stream=stream)
@@ -291,6 +293,31 @@ def qwen_nvfp4(args, torch, S, synth, dev, stream):
     return out
 
 
+def llama_nvfp4_pairs(args, torch, S, synth, dev, stream):
+    """The paper's own instantiation on the headline shapes: NVFP4 with the
+    4:8 in-pairs backbone, Llama-3.1-8B prefill linears at M = 2048."""
+    layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T_TOKENS, "nv", 4, 8, N_INPUT_SETS, True)
+    step = dense_step(S, layers, stream, synth.LLAMA_EPS, 4, 8, "nv", N_INPUT_SETS, True)
+    ms_step, wall_ms, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
+    per = per_linear(layers, tm, T_TOKENS, "nv", 4, 8)
+    flops = sum(p["gemm_flops"] for p in per)
+    t_gemm = sum(p["gemm_us"] for p in per) * 1e-6
+    t_prep = sum(p["prep_us"] for p in per) * 1e-6
+    pb = sum(p["prep_bytes"] for p in per)
+    out = base_record(args, "SharQ linear TFLOPS (prep+2 FP4 GEMMs), Llama-8B M=2048, NVFP4 4:8 in pairs",
+                      flops / (ms_step * 1e-3) / 1e12, "TFLOP/s", ms_step, "nvfp4",
+                      {"workload": "Llama-3.1-8B prefill linears qkv, gate_up (RMSNorm), down; M=2048; "
+                                   "4:8 in pairs; NVFP4 with dynamic per-tensor scale", "tokens": T_TOKENS})
+    out["roofline"] = {"bound": "mfma", "kernel": "k_linear_nv (bf16 MFMA over dequantized FP4)",
+                       "achieved": flops / t_gemm / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                       "frac": flops / t_gemm / 1e12 / PEAK_BF16_TFLOPS, "traffic": None}
+    out["prep"] = {"bound": "hbm", "achieved": pb / t_prep / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                   "frac": pb / t_prep / 1e9 / PEAK_HBM_GBPS,
+                   "note": "time includes the per-tensor amax pre-pass (a second read of X)"}
+    out["per_linear"] = per
+    return out
+
+
 def moe(args, torch, S, synth, dev, stream):
     cfg = synth.MOE
     T, H, E, I, k = cfg["tokens"], cfg["hidden"], cfg["experts"], cfg["inter"], cfg["topk"]
@@ -365,7 +392,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama-prefill",
-                    choices=["llama-prefill", "llama-decode", "qwen-nvfp4", "moe"])
+                    choices=["llama-prefill", "llama-decode", "qwen-nvfp4", "llama-nvfp4-pairs", "moe"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=T_TOKENS)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
@@ -399,6 +426,8 @@ def main():
             print(json.dumps(o), flush=True)
     elif args.workload == "qwen-nvfp4":
         print(json.dumps(qwen_nvfp4(args, torch, S, synth, dev, stream)), flush=True)
+    elif args.workload == "llama-nvfp4-pairs":
+        print(json.dumps(llama_nvfp4_pairs(args, torch, S, synth, dev, stream)), flush=True)
     else:
         print(json.dumps(moe(args, torch, S, synth, dev, stream)), flush=True)
 
