@@ -185,6 +185,23 @@ SHARQ_API sharq_status sharq_prepare(const void *X, sharq_dtype xdt, int64_t M, 
                            const float *tensor_scale_in, sharq_act *out, void *stream);
 
 /*
+ * Preparation with the residual add that precedes a transformer block's
+ * RMSNorm fused in on the producer side (Sec. 4.3: the preparation absorbs
+ * the preprocessing steps of the data flow instead of running them as
+ * separate operators).  Per element, h = bf16(x + residual): the two bf16
+ * values added in fp32 and rounded to nearest even once.  h is written to
+ * h_out (bf16 [M][K], row stride ldh; it may be `residual` itself, updated in
+ * place, when ldh == ldr) and then prepared exactly as sharq_prepare prepares
+ * X.  residual: bf16 [M][K], row stride ldr.  Both 16-byte aligned with
+ * 16-byte row strides.  With NVFP4 and no tensor_scale_in the amax pre-pass
+ * forms h as well.  Other arguments, errors and outputs as for sharq_prepare.
+ */
+SHARQ_API sharq_status sharq_prepare_residual(const void *X, const void *residual, void *h_out, sharq_dtype xdt,
+                                    int64_t M, int64_t K, int64_t ldx, int64_t ldr, int64_t ldh,
+                                    const void *gamma, float eps, sharq_pattern nm, sharq_format fmt,
+                                    const float *tensor_scale_in, sharq_act *out, void *stream);
+
+/*
  * Two-path output (eq. "sharq-output"; Sec. 3.4 "Residual path compensation
  * by accumulation"): Y [rows][N] (row stride ldy, dtype ydt) =
  *   dequant(backbone) * dequant_sp(W)^T + dequant(residual) * dequant_dn(W)^T,

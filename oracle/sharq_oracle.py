@@ -47,6 +47,8 @@ Readings where the paper is silent (each also listed in the design notes):
       survive.  A pair's score is the larger magnitude of its two elements,
       so the group maximum is always kept; of equal scores the lower pair
       wins.  Metadata: the same 8-bit keep mask per group as plain 4:8.
+  R9  Residual add fused into the preparation: h = bf16(fp32(x) + fp32(res)),
+      each rounding to nearest even; the preparation then works on h.
 """
 
 from __future__ import annotations
@@ -533,6 +535,26 @@ def prepare(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: in
         out["sp_meta"] = np.zeros((T, 0), np.uint8)
     out.update(sp_scale=sp_s, dn_codes=pack_nibbles(dn_c), dn_scale=dn_s,
                d_sp=d_sp, R=R, d_dn=d_dn)
+    return out
+
+
+def residual_add_bf16(x_bf16: np.ndarray, res_bf16: np.ndarray) -> np.ndarray:
+    """h = bf16(x + res) (reading R9): the two bf16 values added in fp32 (IEEE,
+    nearest even) and the fp32 sum rounded to bf16, nearest even.  Returns
+    bf16 bit patterns."""
+    s = (bf16_bits_to_f32(x_bf16) + bf16_bits_to_f32(res_bf16)).astype(np.float32)
+    u = s.view(np.uint32).astype(np.uint64)
+    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return rounded.astype(np.uint16)
+
+
+def prepare_residual(x_bf16: np.ndarray, res_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: int,
+                     m: int, fmt: str = "mx", tensor_scale: float | None = None, pairs: bool = False) -> dict:
+    """Preparation with the residual add in front of the RMSNorm: h = bf16(x + res)
+    (R9), then prepare(h).  The dict also carries h (bf16 bits)."""
+    h = residual_add_bf16(x_bf16, res_bf16)
+    out = prepare(h, gamma_bf16, eps, n, m, fmt, tensor_scale, pairs)
+    out["h"] = h
     return out
 
 

@@ -7,9 +7,10 @@
 #include "sharq_device.hpp"
 
 namespace sharq {
-hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps, int pat,
-                       bool nv, const float* ts_in, float* ts_out, uint8_t* spc, uint8_t* spm, uint8_t* sps,
-                       uint8_t* dnc, uint8_t* dns, hipStream_t st);
+hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* res, int64_t ldr, uint16_t* h,
+                       int64_t ldh, const uint16_t* gamma, float eps, int pat, bool nv, const float* ts_in,
+                       float* ts_out, uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns,
+                       hipStream_t st);
 hipError_t launch_wquant_mx(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
                             hipStream_t st);
 hipError_t launch_wquant_nv(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
@@ -145,12 +146,19 @@ sharq_status sharq_quantize_weight(const void* W, sharq_dtype wdt, int64_t N, in
   return hip_status(sharq::launch_wquant_mx(W, (int)wdt, (int)N, (int)K, ldw, out->codes, out->scale, st));
 }
 
-sharq_status sharq_prepare(const void* X, sharq_dtype xdt, int64_t M, int64_t K, int64_t ldx, const void* gamma,
-                           float eps, sharq_pattern nm, sharq_format fmt, const float* tensor_scale_in,
-                           sharq_act* out, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared by sharq_prepare and sharq_prepare_residual (res == NULL: no
+// residual input).
+sharq_status prepare_impl(const void* X, const void* res, void* h_out, sharq_dtype xdt, int64_t M, int64_t K,
+                          int64_t ldx, int64_t ldr, int64_t ldh, const void* gamma, float eps, sharq_pattern nm,
+                          sharq_format fmt, const float* tensor_scale_in, sharq_act* out, void* stream) {
   if (!out) return SHARQ_EINVAL;
   if (M < 0 || M > INT_MAX || K <= 0 || K % 32 != 0 || K > kMaxK || ldx < K) return SHARQ_EINVAL;
   if (!X && M > 0) return SHARQ_EINVAL;
+  if (res && (ldr < K || ldh < K || (!h_out && M > 0))) return SHARQ_EINVAL;
   const int pid = pattern_id(nm);
   if (pid < 0 || K % nm.m != 0) return SHARQ_EINVAL;
   if (out->rows != M || out->K != K || out->fmt != fmt || out->nm.n != nm.n || out->nm.m != nm.m ||
@@ -165,11 +173,34 @@ sharq_status sharq_prepare(const void* X, sharq_dtype xdt, int64_t M, int64_t K,
   if (nv && M > 0 && !out->tensor_scale) return SHARQ_EINVAL;
   if (!aligned(X, 16) || (ldx * 2) % 16 != 0 || (gamma && !aligned(gamma, 16)) || !aligned(tensor_scale_in, 4))
     return SHARQ_EALIGN;
+  if (res && (!aligned(res, 16) || !aligned(h_out, 16) || (ldr * 2) % 16 != 0 || (ldh * 2) % 16 != 0))
+    return SHARQ_EALIGN;
   if (M == 0) return SHARQ_OK;
   return hip_status(sharq::launch_prep(static_cast<const uint16_t*>(X), (int)M, (int)K, ldx,
+                                       static_cast<const uint16_t*>(res), ldr, static_cast<uint16_t*>(h_out), ldh,
                                        static_cast<const uint16_t*>(gamma), eps, pid, nv, nv ? tensor_scale_in : nullptr,
                                        nv ? out->tensor_scale : nullptr, out->sp_codes, out->sp_meta, out->sp_scale,
                                        out->dn_codes, out->dn_scale, reinterpret_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+sharq_status sharq_prepare(const void* X, sharq_dtype xdt, int64_t M, int64_t K, int64_t ldx, const void* gamma,
+                           float eps, sharq_pattern nm, sharq_format fmt, const float* tensor_scale_in,
+                           sharq_act* out, void* stream) {
+  return prepare_impl(X, nullptr, nullptr, xdt, M, K, ldx, K, K, gamma, eps, nm, fmt, tensor_scale_in, out, stream);
+}
+
+sharq_status sharq_prepare_residual(const void* X, const void* residual, void* h_out, sharq_dtype xdt, int64_t M,
+                                    int64_t K, int64_t ldx, int64_t ldr, int64_t ldh, const void* gamma, float eps,
+                                    sharq_pattern nm, sharq_format fmt, const float* tensor_scale_in,
+                                    sharq_act* out, void* stream) {
+  if (!residual && M > 0) return SHARQ_EINVAL;
+  if (M == 0) residual = nullptr;
+  return prepare_impl(X, residual, h_out, xdt, M, K, ldx, ldr, ldh, gamma, eps, nm, fmt, tensor_scale_in, out,
+                      stream);
 }
 
 sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sharq_dtype ydt, int64_t ldy,

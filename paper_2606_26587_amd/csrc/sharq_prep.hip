@@ -392,17 +392,65 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// The activation rows a preparation reads.  Without a residual input they
+// are X itself.  With one -- the residual add that precedes a transformer
+// block's RMSNorm, fused into the preparation on the producer side -- a row
+// is h = bf16(x + res): the two bf16 values added in fp32 and rounded to
+// nearest even once.  The preparation kernels also write h to H (the updated
+// residual stream, which may be the residual input itself) and then work on
+// h; the NVFP4 amax pre-pass recomputes h without writing it.
+struct XSrc {
+  const uint16_t* X;
+  int64_t ldx;
+  const uint16_t* Rs;
+  int64_t ldr;
+  uint16_t* H;
+  int64_t ldh;
+};
+
+__device__ __forceinline__ uint32_t add_bf16x2(uint32_t a, uint32_t b) {
+  typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+  bf2 v;
+  v[0] = (__bf16)(bf16_lo(a) + bf16_lo(b));   // v_cvt_pk_bf16_f32: nearest even
+  v[1] = (__bf16)(bf16_hi(a) + bf16_hi(b));
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// Block b (32 values, four 16-byte pieces) of `row`; with a residual input,
+// h is formed and, when write_h, stored.  Every (row, block) is stored by
+// exactly one lane, which read its residual before: in place is safe.
+template <bool RES>
+__device__ __forceinline__ void load_block(const XSrc& s, int64_t row, int b, uint4 (&q)[4], bool write_h) {
+  const uint4* xr = reinterpret_cast<const uint4*>(s.X + row * s.ldx);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) q[j] = xr[4 * b + j];
+  if (RES) {
+    const uint4* rr = reinterpret_cast<const uint4*>(s.Rs + row * s.ldr);
+    uint4 rq[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) rq[j] = rr[4 * b + j];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      q[j] = make_uint4(add_bf16x2(q[j].x, rq[j].x), add_bf16x2(q[j].y, rq[j].y), add_bf16x2(q[j].z, rq[j].z),
+                        add_bf16x2(q[j].w, rq[j].w));
+    if (write_h) {
+      uint4* hr = reinterpret_cast<uint4*>(s.H + row * s.ldh);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) hr[4 * b + j] = q[j];
+    }
+  }
+}
+
 // Load a row's blocks (NB per lane) and return its RMSNorm reciprocal r.
-template <int NB>
-__device__ __forceinline__ float load_row_rms(const uint4* xr, int lane, int nblk, int K, float eps,
-                                              uint4 (&xs)[NB][4]) {
+template <int NB, bool RES>
+__device__ __forceinline__ float load_row_rms(const XSrc& src, int64_t row, bool write_h, int lane, int nblk, int K,
+                                              float eps, uint4 (&xs)[NB][4]) {
   float chunk[NB];
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
     const int b = lane + 64 * i;
     if (b < nblk) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) xs[i][j] = xr[4 * b + j];
+      load_block<RES>(src, row, b, xs[i], write_h);
     } else {
 #pragma unroll
       for (int j = 0; j < 4; ++j) xs[i][j] = make_uint4(0u, 0u, 0u, 0u);
@@ -436,17 +484,16 @@ __device__ __forceinline__ void norm_block(const uint4 (&xq)[4], const uint4 (&g
 // RMSNorm variant: the row's blocks stay in registers between the sum of
 // squares and the quantization.  NB = blocks per lane, a power of two.
 // NVFP4 reads the per-tensor scale S from S_ptr.
-template <int NB, int PAT, bool NV>
-__global__ __launch_bounds__(256) void k_prep_norm(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
-                                                   const uint16_t* __restrict__ gamma, float eps, ActOut o,
-                                                   const float* S_ptr) {
+template <int NB, int PAT, bool NV, bool RES>
+__global__ __launch_bounds__(256) void k_prep_norm(XSrc src, int M, int K, const uint16_t* __restrict__ gamma,
+                                                   float eps, ActOut o, const float* S_ptr) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;   // whole wavefront; the kernel has no block barrier
   const int nblk = K / 32;
   const float S = NV ? *S_ptr : 1.0f, six_s = 6.0f * S;
   uint4 xs[NB][4];
-  const float r = load_row_rms<NB>(reinterpret_cast<const uint4*>(X + row * ldx), lane, nblk, K, eps, xs);
+  const float r = load_row_rms<NB, RES>(src, row, true, lane, nblk, K, eps, xs);
   const uint4* gr = reinterpret_cast<const uint4*>(gamma);
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
@@ -461,26 +508,6 @@ __global__ __launch_bounds__(256) void k_prep_norm(const uint16_t* __restrict__ 
   }
 }
 
-// Variant without RMSNorm: a plain stream over the row's blocks.
-template <int PAT, bool NV>
-__global__ __launch_bounds__(256) void k_prep_plain(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
-                                                    ActOut o, const float* S_ptr) {
-  const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= M) return;
-  const int nblk = K / 32;
-  const float S = NV ? *S_ptr : 1.0f, six_s = 6.0f * S;
-  const uint4* xr = reinterpret_cast<const uint4*>(X + row * ldx);
-  for (int b = lane; b < nblk; b += 64) {
-    uint4 q[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) q[j] = xr[4 * b + j];
-    float y[32];
-    unpack_bf16x32(q, y);
-    block_out_write<PAT, NV>(y, o, row, b, S, six_s);
-  }
-}
-
 // RMSNorm variant with C wavefronts per row (C = 1, 2, 4; K <= 64 C blocks):
 // wavefront c owns blocks 64 c + lane, so each lane holds one block.  Each
 // wavefront reduces its 2048-position chunk with the in-lane tree and the
@@ -488,10 +515,9 @@ __global__ __launch_bounds__(256) void k_prep_plain(const uint16_t* __restrict__
 // same balanced tree as the one-wavefront-per-row kernel.  Workgroup w
 // handles row groups w, w + G, ... (G = grid size), loading the next group's
 // rows before quantizing the current one.
-template <int C, int PAT, bool NV>
-__global__ __launch_bounds__(256) void k_prep_norm_split(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
-                                                         const uint16_t* __restrict__ gamma, float eps, ActOut o,
-                                                         const float* S_ptr) {
+template <int C, int PAT, bool NV, bool RES>
+__global__ __launch_bounds__(256) void k_prep_norm_split(XSrc src, int M, int K, const uint16_t* __restrict__ gamma,
+                                                         float eps, ActOut o, const float* S_ptr) {
   __shared__ float part[2][4];
   constexpr int RPG = 4 / C;   // rows per group (one group per workgroup pass)
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -502,11 +528,10 @@ __global__ __launch_bounds__(256) void k_prep_norm_split(const uint16_t* __restr
 
   auto load = [&](int grp, uint4 (&q)[4]) {
     int64_t row = (int64_t)grp * RPG + wave / C;
-    if (row >= M) row = M - 1;   // loads stay in bounds
-    const uint4* xr = reinterpret_cast<const uint4*>(X + row * ldx);
+    const bool real = row < M;
+    if (!real) row = M - 1;   // loads stay in bounds; only real rows store h
     if (b < nblk) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) q[j] = xr[4 * b + j];
+      load_block<RES>(src, row, b, q, real);
     } else {
 #pragma unroll
       for (int j = 0; j < 4; ++j) q[j] = make_uint4(0u, 0u, 0u, 0u);
@@ -556,9 +581,8 @@ __global__ __launch_bounds__(256) void k_prep_norm_split(const uint16_t* __restr
 // consecutive threads write consecutive bytes of every output buffer (and
 // read 256-byte row pieces of X).  The last panel may hold q < 4 blocks per
 // row.
-template <int PAT, bool NV>
-__global__ __launch_bounds__(256) void k_prep_blocks(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
-                                                     ActOut o, const float* S_ptr) {
+template <int PAT, bool NV, bool RES>
+__global__ __launch_bounds__(256) void k_prep_blocks(XSrc src, int M, int K, ActOut o, const float* S_ptr) {
   const int nblk = K / 32, p = blockIdx.y;
   const int q = min(4, nblk - 4 * p);      // blocks per row in this panel
   const uint32_t t = blockIdx.x * 256u + threadIdx.x;
@@ -573,10 +597,8 @@ __global__ __launch_bounds__(256) void k_prep_blocks(const uint16_t* __restrict_
   }
   const int b = 4 * p + (int)j;
   const float S = NV ? *S_ptr : 1.0f, six_s = 6.0f * S;
-  const uint4* xr = reinterpret_cast<const uint4*>(X + (int64_t)row * ldx);
   uint4 xq[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) xq[i] = xr[4 * b + i];
+  load_block<RES>(src, (int64_t)row, b, xq, true);
   float y[32];
   unpack_bf16x32(xq, y);
   const BlockOut d = block_at<NV>(o, (int64_t)p * M * 4 + t);
@@ -603,15 +625,15 @@ __global__ void k_pts_finalize(uint32_t* slot) {
   *reinterpret_cast<float*>(slot) = S;
 }
 
-template <int NB>
-__global__ __launch_bounds__(256) void k_amax_norm(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
-                                                   const uint16_t* __restrict__ gamma, float eps, uint32_t* slot) {
+template <int NB, bool RES>
+__global__ __launch_bounds__(256) void k_amax_norm(XSrc src, int M, int K, const uint16_t* __restrict__ gamma,
+                                                   float eps, uint32_t* slot) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
   const int nblk = K / 32;
   uint4 xs[NB][4];
-  const float r = load_row_rms<NB>(reinterpret_cast<const uint4*>(X + row * ldx), lane, nblk, K, eps, xs);
+  const float r = load_row_rms<NB, RES>(src, row, false, lane, nblk, K, eps, xs);
   const uint4* gr = reinterpret_cast<const uint4*>(gamma);
   float m = 0.0f;
 #pragma unroll
@@ -629,17 +651,15 @@ __global__ __launch_bounds__(256) void k_amax_norm(const uint16_t* __restrict__ 
   if (lane == 0) atomicMax(slot, __float_as_uint(m));
 }
 
-__global__ __launch_bounds__(256) void k_amax_plain(const uint16_t* __restrict__ X, int M, int K, int64_t ldx,
-                                                    uint32_t* slot) {
+template <bool RES>
+__global__ __launch_bounds__(256) void k_amax_plain(XSrc src, int M, int K, uint32_t* slot) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
-  const uint4* xr = reinterpret_cast<const uint4*>(X + row * ldx);
   float m = 0.0f;
   for (int b = lane; b < K / 32; b += 64) {
     uint4 q[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) q[j] = xr[4 * b + j];
+    load_block<RES>(src, row, b, q, false);
     float y[32];
     unpack_bf16x32(q, y);
     m = fmaxf(m, absmax32(y));
@@ -657,14 +677,14 @@ __global__ __launch_bounds__(256) void k_amax_plain(const uint16_t* __restrict__
 // was slower), so workgroups only iterate beyond 16 per CU.
 constexpr int kPersistWG = 4096;
 
-template <int PAT, bool NV>
-static void go_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps, const ActOut& o,
+template <int PAT, bool NV, bool RES>
+static void go_prep(const XSrc& src, int M, int K, const uint16_t* gamma, float eps, const ActOut& o,
                     const float* S_ptr, dim3 grid, hipStream_t st) {
   dim3 block(256);
   const int nblk = K / 32;
   if (gamma == nullptr) {
     const dim3 g2((unsigned)((4 * (int64_t)M + 255) / 256), (unsigned)((nblk + 3) / 4));
-    k_prep_blocks<PAT, NV><<<g2, block, 0, st>>>(X, M, K, ldx, o, S_ptr);
+    k_prep_blocks<PAT, NV, RES><<<g2, block, 0, st>>>(src, M, K, o, S_ptr);
     return;
   }
   if (nblk <= 256) {
@@ -672,28 +692,59 @@ static void go_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t
     const int C = nblk <= 64 ? 1 : (nblk <= 128 ? 2 : 4);
     const int groups = (M + 4 / C - 1) / (4 / C);
     const dim3 g1((unsigned)(groups < kPersistWG ? groups : kPersistWG));
-    if (C == 1) k_prep_norm_split<1, PAT, NV><<<g1, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
-    else if (C == 2) k_prep_norm_split<2, PAT, NV><<<g1, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
-    else k_prep_norm_split<4, PAT, NV><<<g1, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
+    if (C == 1) k_prep_norm_split<1, PAT, NV, RES><<<g1, block, 0, st>>>(src, M, K, gamma, eps, o, S_ptr);
+    else if (C == 2) k_prep_norm_split<2, PAT, NV, RES><<<g1, block, 0, st>>>(src, M, K, gamma, eps, o, S_ptr);
+    else k_prep_norm_split<4, PAT, NV, RES><<<g1, block, 0, st>>>(src, M, K, gamma, eps, o, S_ptr);
     return;
   }
   const int chunks = (K / 32 + 63) / 64;
   if (chunks <= 1)
-    k_prep_norm<1, PAT, NV><<<grid, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
+    k_prep_norm<1, PAT, NV, RES><<<grid, block, 0, st>>>(src, M, K, gamma, eps, o, S_ptr);
   else if (chunks <= 2)
-    k_prep_norm<2, PAT, NV><<<grid, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
+    k_prep_norm<2, PAT, NV, RES><<<grid, block, 0, st>>>(src, M, K, gamma, eps, o, S_ptr);
   else if (chunks <= 4)
-    k_prep_norm<4, PAT, NV><<<grid, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
+    k_prep_norm<4, PAT, NV, RES><<<grid, block, 0, st>>>(src, M, K, gamma, eps, o, S_ptr);
   else
-    k_prep_norm<8, PAT, NV><<<grid, block, 0, st>>>(X, M, K, ldx, gamma, eps, o, S_ptr);
+    k_prep_norm<8, PAT, NV, RES><<<grid, block, 0, st>>>(src, M, K, gamma, eps, o, S_ptr);
+}
+
+template <bool RES>
+static void go_amax(const XSrc& src, int M, int K, const uint16_t* gamma, float eps, uint32_t* slot, dim3 grid,
+                    hipStream_t st) {
+  if (gamma == nullptr) {
+    k_amax_plain<RES><<<grid, 256, 0, st>>>(src, M, K, slot);
+    return;
+  }
+  const int chunks = (K / 32 + 63) / 64;
+  if (chunks <= 1) k_amax_norm<1, RES><<<grid, 256, 0, st>>>(src, M, K, gamma, eps, slot);
+  else if (chunks <= 2) k_amax_norm<2, RES><<<grid, 256, 0, st>>>(src, M, K, gamma, eps, slot);
+  else if (chunks <= 4) k_amax_norm<4, RES><<<grid, 256, 0, st>>>(src, M, K, gamma, eps, slot);
+  else k_amax_norm<8, RES><<<grid, 256, 0, st>>>(src, M, K, gamma, eps, slot);
+}
+
+template <bool RES>
+static void go_prep_pat(int pat, bool nv, const XSrc& src, int M, int K, const uint16_t* gamma, float eps,
+                        const ActOut& o, const float* S_ptr, dim3 grid, hipStream_t st) {
+  if (nv) {
+    if (pat == 24) go_prep<24, true, RES>(src, M, K, gamma, eps, o, S_ptr, grid, st);
+    else if (pat == 49) go_prep<49, true, RES>(src, M, K, gamma, eps, o, S_ptr, grid, st);
+    else go_prep<48, true, RES>(src, M, K, gamma, eps, o, S_ptr, grid, st);
+  } else {
+    if (pat == 24) go_prep<24, false, RES>(src, M, K, gamma, eps, o, nullptr, grid, st);
+    else if (pat == 49) go_prep<49, false, RES>(src, M, K, gamma, eps, o, nullptr, grid, st);
+    else go_prep<48, false, RES>(src, M, K, gamma, eps, o, nullptr, grid, st);
+  }
 }
 
 // nv: NVFP4 with the per-tensor scale written to ts_out (from ts_in when
-// given, else computed from the data).
-hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps, int pat,
-                       bool nv, const float* ts_in, float* ts_out, uint8_t* spc, uint8_t* spm, uint8_t* sps,
-                       uint8_t* dnc, uint8_t* dns, hipStream_t st) {
+// given, else computed from the data).  res / h: the residual input and the
+// h output of the fused residual add (both NULL without it).
+hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* res, int64_t ldr, uint16_t* h,
+                       int64_t ldh, const uint16_t* gamma, float eps, int pat, bool nv, const float* ts_in,
+                       float* ts_out, uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns,
+                       hipStream_t st) {
   const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K};
+  const XSrc src{X, ldx, res, ldr, h, ldh};
   const dim3 grid((unsigned)((M + 3) / 4));
   if (nv) {
     if (ts_in) {
@@ -701,25 +752,13 @@ hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint1
     } else {
       uint32_t* slot = reinterpret_cast<uint32_t*>(ts_out);
       k_store_u32<<<1, 1, 0, st>>>(slot, 0u);
-      if (gamma == nullptr) {
-        k_amax_plain<<<grid, 256, 0, st>>>(X, M, K, ldx, slot);
-      } else {
-        const int chunks = (K / 32 + 63) / 64;
-        if (chunks <= 1) k_amax_norm<1><<<grid, 256, 0, st>>>(X, M, K, ldx, gamma, eps, slot);
-        else if (chunks <= 2) k_amax_norm<2><<<grid, 256, 0, st>>>(X, M, K, ldx, gamma, eps, slot);
-        else if (chunks <= 4) k_amax_norm<4><<<grid, 256, 0, st>>>(X, M, K, ldx, gamma, eps, slot);
-        else k_amax_norm<8><<<grid, 256, 0, st>>>(X, M, K, ldx, gamma, eps, slot);
-      }
+      if (res) go_amax<true>(src, M, K, gamma, eps, slot, grid, st);
+      else go_amax<false>(src, M, K, gamma, eps, slot, grid, st);
       k_pts_finalize<<<1, 1, 0, st>>>(slot);
     }
-    if (pat == 24) go_prep<24, true>(X, M, K, ldx, gamma, eps, o, ts_out, grid, st);
-    else if (pat == 49) go_prep<49, true>(X, M, K, ldx, gamma, eps, o, ts_out, grid, st);
-    else go_prep<48, true>(X, M, K, ldx, gamma, eps, o, ts_out, grid, st);
-  } else {
-    if (pat == 24) go_prep<24, false>(X, M, K, ldx, gamma, eps, o, nullptr, grid, st);
-    else if (pat == 49) go_prep<49, false>(X, M, K, ldx, gamma, eps, o, nullptr, grid, st);
-    else go_prep<48, false>(X, M, K, ldx, gamma, eps, o, nullptr, grid, st);
   }
+  if (res) go_prep_pat<true>(pat, nv, src, M, K, gamma, eps, o, ts_out, grid, st);
+  else go_prep_pat<false>(pat, nv, src, M, K, gamma, eps, o, ts_out, grid, st);
   return hipGetLastError();
 }
 

@@ -65,6 +65,9 @@ def _load():
     L.sharq_prepare.restype = ctypes.c_int
     L.sharq_prepare.argtypes = [c_vp, ctypes.c_int, c_i64, c_i64, c_i64, c_vp, c_f, Pattern, ctypes.c_int, c_vp,
                                 ctypes.POINTER(ActStruct), c_vp]
+    L.sharq_prepare_residual.restype = ctypes.c_int
+    L.sharq_prepare_residual.argtypes = [c_vp, c_vp, c_vp, ctypes.c_int, c_i64, c_i64, c_i64, c_i64, c_i64, c_vp, c_f,
+                                         Pattern, ctypes.c_int, c_vp, ctypes.POINTER(ActStruct), c_vp]
     L.sharq_linear.restype = ctypes.c_int
     L.sharq_linear.argtypes = [ctypes.POINTER(ActStruct), ctypes.POINTER(WeightStruct), c_vp, ctypes.c_int, c_i64,
                                c_vp]
@@ -187,6 +190,27 @@ def sharq_prepare(x: torch.Tensor, gamma: Optional[torch.Tensor], eps: float = 1
                              Pattern(n, m, int(pairs)), f, _ptr(tensor_scale_in), ctypes.byref(st), _stream(stream)),
            "sharq_prepare")
     return out
+
+
+def sharq_prepare_residual(x: torch.Tensor, residual: torch.Tensor, gamma: Optional[torch.Tensor], eps: float = 1e-6,
+                           n: int = 2, m: int = 4, fmt="mx", h_out: Optional[torch.Tensor] = None,
+                           tensor_scale_in: Optional[torch.Tensor] = None, out: Optional[PreparedAct] = None,
+                           stream=None, pairs: bool = False):
+    """Residual add fused into the preparation: h = bf16(x + residual) is
+    written to h_out (a new tensor, or e.g. `residual` itself for an in-place
+    update) and prepared.  Returns (prepared activation, h)."""
+    M, K = x.shape
+    if out is None:
+        out = alloc_act(M, K, n, m, fmt, x.device, pairs)
+    if h_out is None:
+        h_out = torch.empty_like(x)
+    f = _FMT[fmt] if isinstance(fmt, str) else fmt
+    st = out.struct()
+    _check(lib.sharq_prepare_residual(_ptr(x), _ptr(residual), _ptr(h_out), _DT.get(x.dtype, -1), M, K, x.stride(0),
+                                      residual.stride(0), h_out.stride(0), _ptr(gamma), ctypes.c_float(eps),
+                                      Pattern(n, m, int(pairs)), f, _ptr(tensor_scale_in), ctypes.byref(st),
+                                      _stream(stream)), "sharq_prepare_residual")
+    return out, h_out
 
 
 def sharq_linear(a: PreparedAct, w: QuantWeight, out: Optional[torch.Tensor] = None, dtype=torch.bfloat16,

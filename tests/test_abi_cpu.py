@@ -38,6 +38,10 @@ def L():
     lib.sharq_prepare.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                                   ctypes.c_void_p, ctypes.c_float, Pattern, ctypes.c_int, ctypes.c_void_p,
                                   ctypes.POINTER(Act), ctypes.c_void_p]
+    lib.sharq_prepare_residual.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                           ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                           ctypes.c_int64, ctypes.c_void_p, ctypes.c_float, Pattern, ctypes.c_int,
+                                           ctypes.c_void_p, ctypes.POINTER(Act), ctypes.c_void_p]
     lib.sharq_linear.argtypes = [ctypes.POINTER(Act), ctypes.POINTER(Weight), ctypes.c_void_p, ctypes.c_int,
                                  ctypes.c_int64, ctypes.c_void_p]
     lib.sharq_linear_grouped.argtypes = [ctypes.POINTER(Act), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
@@ -123,6 +127,23 @@ def test_prepare_pairs_must_match_out(L):
     empty = act(rows=0, K=128, n=4, m=8, pairs=1)
     assert L.sharq_prepare(FAKE, 0, 0, 128, 128, None, 1e-6, Pattern(4, 8, 1), 0, None, ctypes.byref(empty),
                            None) == OK
+
+
+def test_prepare_residual_rejects(L):
+    a = act()
+    P = Pattern(2, 4, 0)
+    call = lambda res, h, ldr, ldh, X=FAKE: L.sharq_prepare_residual(X, res, h, 0, 8, 128, 128, ldr, ldh, None, 1e-6,
+                                                                     P, 0, None, ctypes.byref(a), None)
+    assert call(None, FAKE, 128, 128) == EINVAL          # no residual
+    assert call(FAKE, None, 128, 128) == EINVAL          # no h output
+    assert call(FAKE, FAKE, 64, 128) == EINVAL           # ldr < K
+    assert call(FAKE, FAKE, 128, 100) == EINVAL          # ldh < K
+    assert call(FAKE + 2, FAKE, 128, 128) == EALIGN      # residual not 16-byte aligned
+    assert call(FAKE, FAKE, 132, 128) == EALIGN          # residual row stride not 16 bytes
+    assert call(FAKE, FAKE + 8, 128, 128) == EALIGN      # h not 16-byte aligned
+    empty = act(rows=0)
+    assert L.sharq_prepare_residual(FAKE, None, None, 0, 0, 128, 128, 128, 128, None, 1e-6, P, 0, None,
+                                    ctypes.byref(empty), None) == OK
 
 
 def test_prepare_null_and_alignment(L):

@@ -194,6 +194,55 @@ def test_prepare_in_pairs_backbone_and_residual():
             assert np.array_equal(o["sp_scale"].astype(np.int64) - 127, dense_e)
 
 
+# ----------------------------------------------------------------------------- fused residual add
+
+def _bf16_value(u):
+    return Fraction(float(np.array([int(u) << 16], dtype=np.uint32).view(np.float32)[0]))
+
+
+def _bf16_round_exact(v: Fraction) -> int:
+    """Nearest bf16 to an exact rational (ties to the even pattern), by search
+    over the finite bf16 values around it."""
+    f = float(v)
+    u = int(np.array([f], dtype=np.float32).view(np.uint32)[0]) >> 16
+    cands = {c & 0xFFFF for c in (u - 1, u, u + 1, u + 2)}
+    cands = [c for c in cands if (c & 0x7F80) != 0x7F80]
+    best = min(cands, key=lambda c: (abs(_bf16_value(c) - v), c & 1))
+    return best
+
+
+def test_residual_add_is_the_correctly_rounded_bf16_sum():
+    """h = bf16(fp32(x) + fp32(res)) equals the bf16 value nearest to the exact
+    sum (ties to even): the fp32 intermediate never double-rounds for two
+    bf16 operands."""
+    rng = np.random.default_rng(31)
+    n = 4000
+    e1 = rng.integers(-20, 20, n)
+    e2 = e1 + rng.integers(-30, 30, n)
+    m1, m2 = rng.integers(128, 256, n), rng.integers(128, 256, n)
+    x = (np.sign(rng.standard_normal(n)) * m1 * np.exp2(e1 - 7.0)).astype(np.float32)
+    r = (np.sign(rng.standard_normal(n)) * m2 * np.exp2(e2 - 7.0)).astype(np.float32)
+    xb = (x.view(np.uint32) >> 16).astype(np.uint16)
+    rb = (r.view(np.uint32) >> 16).astype(np.uint16)
+    # exact ties and cancellations: 1 + 2^-8, subnormals, opposite signs
+    xb = np.concatenate([xb, np.array([0x3F80, 0x3F81, 0x0001, 0x4000, 0x8000], np.uint16)])
+    rb = np.concatenate([rb, np.array([0x3B80, 0x3B80, 0x0001, 0xC000, 0x0000], np.uint16)])
+    h = O.residual_add_bf16(xb, rb)
+    for a, b, got in zip(xb, rb, h):
+        want = _bf16_round_exact(_bf16_value(a) + _bf16_value(b))
+        assert int(got) == want or (_bf16_value(got) == 0 and _bf16_value(want) == 0), (hex(a), hex(b), hex(got), hex(want))
+
+
+def test_prepare_residual_is_prepare_of_the_sum():
+    x = synth.activations(8, 256, seed=8)
+    res = synth.activations(8, 256, seed=9)
+    g = synth.gamma(256, seed=8)
+    o = O.prepare_residual(x, res, g, 1e-6, 2, 4, "mx")
+    p = O.prepare(O.residual_add_bf16(x, res), g, 1e-6, 2, 4, "mx")
+    for k in O.ACT_BUFFERS:
+        assert np.array_equal(o[k], p[k])
+
+
 # ----------------------------------------------------------------------------- RMSNorm
 
 def test_rms_tree_equals_recursive_traversal():
