@@ -49,6 +49,16 @@ Readings where the paper is silent (each also listed in the design notes):
       wins.  Metadata: the same 8-bit keep mask per group as plain 4:8.
   R9  Residual add fused into the preparation: h = bf16(fp32(x) + fp32(res)),
       each rounding to nearest even; the preparation then works on h.
+  R10 Path combinations (Sec. 4.4, table "ablation-combination"; Sec. 3.1 eq.
+      "direct-sparse-quant"; the RTN rows of table "ablation-format").  Every
+      mode has two path slots: path 1 quantizes y, path 2 quantizes the
+      residual of y against path 1's dequantized values.  A sparse path is
+      the backbone quantizer (N:M mask of its own input, blocks of 32 logical
+      positions); a dense path is the format's plain quantizer (MXFP4 blocks
+      of 32, NVFP4 blocks of 16).  Sparse = (sparse, none); plain FP4 RTN =
+      (none, dense); Dense+Dense = (dense, dense); Sparse+Sparse = (sparse,
+      sparse), whose second mask is chosen on |R|; SharQ = (sparse, dense).
+      NVFP4 uses one per-tensor scale S = amax(y)/2688 for both paths.
 """
 
 from __future__ import annotations
@@ -456,21 +466,44 @@ def from_panels(flat: np.ndarray, R: int, K: int, bytes_per_row: int) -> np.ndar
 
 
 ACT_BUFFERS = ("sp_codes", "sp_meta", "sp_scale", "dn_codes", "dn_scale")
+#: every buffer a prepared activation may use (dn_meta: a sparse second path)
+ACT_BUFFERS_ALL = ACT_BUFFERS + ("dn_meta",)
 WEIGHT_BUFFERS = ("codes", "scale", "scale_dn")
+
+
+def path_widths(kind, K: int, n: int, m: int, fmt: str):
+    """Row bytes (codes, meta, scale) of one path slot of kind 'sparse', 'dense' or None."""
+    if kind is None:
+        return 0, 0, 0
+    if kind == "sparse":
+        return K * n // m // 2, K // 8, K // 32
+    return K // 2, 0, K // 32 if fmt == "mx" else K // 16
+
+
+def act_widths(K: int, n: int, m: int, fmt: str, mode: str = "sharq") -> dict:
+    """Row bytes of every buffer of a prepared activation in `mode` (0 = unused)."""
+    k1, k2 = MODE_PATHS[mode]
+    c1, m1, s1 = path_widths(k1, K, n, m, fmt)
+    c2, m2, s2 = path_widths(k2, K, n, m, fmt)
+    return {"sp_codes": c1, "sp_meta": m1, "sp_scale": s1, "dn_codes": c2, "dn_meta": m2, "dn_scale": s2}
 
 
 def act_to_device_layout(act: dict) -> dict:
     """The prepared-activation buffers in the library's panel-major layout."""
-    return {k: to_panels(act[k], act["K"]) for k in ACT_BUFFERS}
+    return {k: to_panels(act[k], act["K"]) for k in ACT_BUFFERS_ALL if k in act}
 
 
-def act_from_device_layout(bufs: dict, rows: int, K: int, n: int, m: int, fmt: str, tensor_scale=None) -> dict:
+def act_from_device_layout(bufs: dict, rows: int, K: int, n: int, m: int, fmt: str, tensor_scale=None,
+                           mode: str = "sharq", pairs: bool = False) -> dict:
     """Panel-major device buffers -> the row-major dict the oracle's GEMM reads."""
-    widths = {"sp_codes": K * n // m // 2, "sp_meta": K // 8, "sp_scale": K // 32, "dn_codes": K // 2,
-              "dn_scale": K // 32 if fmt == "mx" else K // 16}
-    d = {"rows": rows, "K": K, "n": n, "m": m, "fmt": fmt, "tensor_scale": tensor_scale}
-    for k in ACT_BUFFERS:
-        d[k] = from_panels(bufs[k], rows, K, widths[k])
+    widths = act_widths(K, n, m, fmt, mode)
+    d = {"rows": rows, "K": K, "n": n, "m": m, "fmt": fmt, "tensor_scale": tensor_scale, "mode": mode,
+         "pairs": pairs}
+    for k in ACT_BUFFERS_ALL:
+        if widths[k] == 0:
+            d[k] = np.zeros((rows, 0), np.uint8)
+        else:
+            d[k] = from_panels(bufs[k], rows, K, widths[k])
     return d
 
 
@@ -538,6 +571,89 @@ def prepare(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: in
     return out
 
 
+# ---------------------------------------------------------------------------
+# Path combinations (Sec. 4.4 table "ablation-combination"; reading R10)
+# ---------------------------------------------------------------------------
+
+#: The kinds of the two path slots of every mode.  Path 1 quantizes y; path 2
+#: quantizes the residual of y against path 1's dequantized values.
+MODE_PATHS = {
+    "sharq": ("sparse", "dense"),
+    "sparse": ("sparse", None),
+    "dense": (None, "dense"),
+    "dense_dense": ("dense", "dense"),
+    "sparse_sparse": ("sparse", "sparse"),
+}
+#: the numbering of the modes at the library's C interface
+MODE_IDS = {"sharq": 0, "sparse": 1, "dense": 2, "dense_dense": 3, "sparse_sparse": 4}
+
+
+def quantize_path(v: np.ndarray, kind: str, n: int, m: int, fmt: str, S, pairs: bool = False) -> dict:
+    """One path applied to rows v: a sparse path keeps the top n of every m
+    (of |v|, or in pairs) and quantizes the kept values in blocks of 32
+    logical positions (eq. sharq-quantized-backbone); a dense path is the
+    format's plain quantizer (MXFP4 blocks of 32, NVFP4 blocks of 16)."""
+    T, K = v.shape
+    if kind == "sparse":
+        if n == 0:
+            keep = np.zeros(v.shape, dtype=bool)
+        else:
+            keep = nm_pair_mask(v, n, m) if pairs else nm_mask(v, n, m)
+        if fmt == "mx":
+            c, _, sc, deq = mx_quantize(v, keep)
+        else:
+            c, _, sc, deq = nv_quantize(v, S, MX_BLOCK, keep)
+        if n > 0:
+            codes, meta = pack_backbone(c, keep, n, m)
+        else:
+            codes, meta = np.zeros((T, 0), np.uint8), np.zeros((T, 0), np.uint8)
+        return {"codes": codes, "meta": meta, "scale": sc, "deq": deq, "keep": keep}
+    if fmt == "mx":
+        c, _, sc, deq = mx_quantize(v)
+    else:
+        c, _, sc, deq = nv_quantize(v, S, NV_BLOCK)
+    return {"codes": pack_nibbles(c), "meta": np.zeros((T, 0), np.uint8), "scale": sc, "deq": deq,
+            "keep": np.ones(v.shape, dtype=bool)}
+
+
+def prepare_mode(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: int, m: int, fmt: str = "mx",
+                 mode: str = "sharq", tensor_scale: float | None = None, pairs: bool = False) -> dict:
+    """Preparation for one path combination (reading R10).
+
+    1. y = RMSNorm(x) * gamma (or y = x); for NVFP4 one S = amax(y)/2688;
+    2. path 1 quantizes y (nothing when absent);
+    3. R = y - D(path 1), in fp32;
+    4. path 2 quantizes R (nothing when absent).
+    Path 1's buffers are sp_codes / sp_meta / sp_scale, path 2's dn_codes /
+    dn_meta / dn_scale; an absent path or a dense path's metadata has width 0.
+    Mode "sharq" gives the buffers of prepare().
+    """
+    k1, k2 = MODE_PATHS[mode]
+    x = bf16_bits_to_f32(x_bf16)
+    T, K = x.shape
+    g = None if gamma_bf16 is None else bf16_bits_to_f32(gamma_bf16)
+    y, r = rmsnorm(x, g, eps)
+    S = None
+    if fmt == "nv":
+        S = pts_scale(np.abs(y).max() if y.size else 0.0) if tensor_scale is None else np.float32(tensor_scale)
+    elif fmt != "mx":
+        raise ValueError(fmt)
+    empty = np.zeros((T, 0), np.uint8)
+    out = {"rows": T, "K": K, "n": n, "m": m, "pairs": pairs, "fmt": fmt, "mode": mode, "y": y, "r": r,
+           "tensor_scale": None if S is None else np.float32(S)}
+    p1 = quantize_path(y, k1, n, m, fmt, S, pairs) if k1 else None
+    d1 = p1["deq"] if p1 else np.zeros(y.shape, np.float32)
+    R = (y - d1).astype(np.float32)
+    p2 = quantize_path(R, k2, n, m, fmt, S, pairs) if k2 else None
+    d2 = p2["deq"] if p2 else np.zeros(y.shape, np.float32)
+    out.update(sp_codes=p1["codes"] if p1 else empty, sp_meta=p1["meta"] if p1 else empty,
+               sp_scale=p1["scale"] if p1 else empty, dn_codes=p2["codes"] if p2 else empty,
+               dn_meta=p2["meta"] if p2 else empty, dn_scale=p2["scale"] if p2 else empty,
+               keep=p1["keep"] if p1 else np.zeros(y.shape, bool),
+               keep2=p2["keep"] if p2 else np.zeros(y.shape, bool), d_sp=d1, R=R, d_dn=d2)
+    return out
+
+
 def residual_add_bf16(x_bf16: np.ndarray, res_bf16: np.ndarray) -> np.ndarray:
     """h = bf16(x + res) (reading R9): the two bf16 values added in fp32 (IEEE,
     nearest even) and the fp32 sum rounded to bf16, nearest even.  Returns
@@ -590,23 +706,36 @@ def _block_scale_values(scale_codes: np.ndarray, fmt: str, block: int, K: int) -
     return np.repeat(vals, block, axis=1)[:, :K]
 
 
+def _dequant_path(kind, codes, meta, scale, T: int, K: int, n: int, m: int, fmt: str, S: float) -> np.ndarray:
+    if kind is None or (kind == "sparse" and n == 0):
+        return np.zeros((T, K))
+    if kind == "sparse":
+        dense, keep = unpack_backbone(codes, meta, K, n, m)
+        vals = e2m1_decode(dense) * _block_scale_values(scale, fmt, MX_BLOCK, K) * S
+        return np.where(keep, vals, 0.0)
+    block = MX_BLOCK if fmt == "mx" else NV_BLOCK
+    return e2m1_decode(unpack_nibbles(codes)) * _block_scale_values(scale, fmt, block, K) * S
+
+
 def dequant_act(act: dict):
-    """Packed prepared activation -> (backbone fp64 [T,K], residual fp64 [T,K]).
+    """Packed prepared activation -> (path 1 fp64 [T,K], path 2 fp64 [T,K]);
+    for SharQ the backbone and the residual.  An absent path is zero.
 
     Values are exact: E2M1 x E8M0 (or x E4M3 x S) products fit in fp64.
     """
     K, n, m, fmt = act["K"], act["n"], act["m"], act["fmt"]
-    T = act["dn_codes"].shape[0]
+    T = act["rows"]
+    k1, k2 = MODE_PATHS[act.get("mode", "sharq")]
     S = 1.0 if fmt == "mx" else float(act["tensor_scale"])
-    if n > 0:
-        dense, keep = unpack_backbone(act["sp_codes"], act["sp_meta"], K, n, m)
-        a_sp = e2m1_decode(dense) * _block_scale_values(act["sp_scale"], fmt, MX_BLOCK, K) * S
-        a_sp = np.where(keep, a_sp, 0.0)
-    else:
-        a_sp = np.zeros((T, K))
-    dn_block = MX_BLOCK if fmt == "mx" else NV_BLOCK
-    a_dn = e2m1_decode(unpack_nibbles(act["dn_codes"])) * _block_scale_values(act["dn_scale"], fmt, dn_block, K) * S
-    return a_sp, a_dn
+    a1 = _dequant_path(k1, act["sp_codes"], act["sp_meta"], act["sp_scale"], T, K, n, m, fmt, S)
+    a2 = _dequant_path(k2, act["dn_codes"], act.get("dn_meta"), act["dn_scale"], T, K, n, m, fmt, S)
+    return a1, a2
+
+
+def _views(act: dict):
+    """Weight scale view each path reads: the sparse view for a sparse path,
+    the dense view for a dense one (Sec. 3.4)."""
+    return tuple("sp" if k == "sparse" else "dn" for k in MODE_PATHS[act.get("mode", "sharq")])
 
 
 def dequant_weight(wq: dict, view: str = "sp") -> np.ndarray:
@@ -621,24 +750,25 @@ def dequant_weight(wq: dict, view: str = "sp") -> np.ndarray:
 
 
 def linear(act: dict, wq: dict, rows: np.ndarray | None = None) -> np.ndarray:
-    """Two-path output (eq. sharq-output) in fp64: Y = X~_sp W_sp^T + R~ W_dn^T.
+    """Two-path output (eq. sharq-output) in fp64: Y = X~_sp W_sp^T + R~ W_dn^T;
+    for the other modes the sum over their paths, each through its view.
 
     `rows` optionally restricts the computation to a subset of activation rows.
     """
-    a_sp, a_dn = dequant_act(act)
+    a1, a2 = dequant_act(act)
     if rows is not None:
-        a_sp, a_dn = a_sp[rows], a_dn[rows]
-    w_sp = dequant_weight(wq, "sp")
-    w_dn = dequant_weight(wq, "dn")
-    return a_sp @ w_sp.T + a_dn @ w_dn.T
+        a1, a2 = a1[rows], a2[rows]
+    v1, v2 = _views(act)
+    return a1 @ dequant_weight(wq, v1).T + a2 @ dequant_weight(wq, v2).T
 
 
 def linear_abs(act: dict, wq: dict, rows: np.ndarray | None = None) -> np.ndarray:
-    """sum_k |a_sp w| + |a_dn w| per output: the scale of the accumulation error."""
-    a_sp, a_dn = dequant_act(act)
+    """sum_k |a_1 w| + |a_2 w| per output: the scale of the accumulation error."""
+    a1, a2 = dequant_act(act)
     if rows is not None:
-        a_sp, a_dn = a_sp[rows], a_dn[rows]
-    return np.abs(a_sp) @ np.abs(dequant_weight(wq, "sp")).T + np.abs(a_dn) @ np.abs(dequant_weight(wq, "dn")).T
+        a1, a2 = a1[rows], a2[rows]
+    v1, v2 = _views(act)
+    return np.abs(a1) @ np.abs(dequant_weight(wq, v1)).T + np.abs(a2) @ np.abs(dequant_weight(wq, v2)).T
 
 
 def linear_grouped(act: dict, row_index: np.ndarray | None, expert_offsets: np.ndarray,
