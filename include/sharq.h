@@ -83,9 +83,39 @@ typedef struct {
 } sharq_pattern;
 
 /*
+ * Path combination of a prepared activation (Sec. 4.4, table
+ * "ablation-combination"; Sec. 3.1 eq. "direct-sparse-quant"; the
+ * round-to-nearest FP4 rows of table "ablation-format").  Every mode has two
+ * path slots: path 1 quantizes y, path 2 quantizes the residual of y against
+ * path 1's dequantized values; the GEMM sums the paths' products into one
+ * accumulator.  A sparse path keeps the top n of every m of ITS OWN input and
+ * quantizes the kept values in blocks of 32 logical positions (the backbone
+ * quantizer); a dense path is the format's plain quantizer (MXFP4 per 32,
+ * NVFP4 per 16).  NVFP4 uses one per-tensor scale for both paths.
+ *
+ *   mode                       path 1   path 2
+ *   SHARQ_MODE_SHARQ           sparse   dense     the method (default, 0)
+ *   SHARQ_MODE_SPARSE          sparse   -         no residual compensation
+ *   SHARQ_MODE_DENSE           -        dense     plain FP4 (RTN), i.e. n = 0
+ *   SHARQ_MODE_DENSE_DENSE     dense    dense     two dense paths
+ *   SHARQ_MODE_SPARSE_SPARSE   sparse   sparse    second mask chosen on |R|
+ *
+ * Only SHARQ_MODE_SHARQ is the method; the others exist for ablation.  They
+ * run on generic (non-interleaved) GEMM kernels and are not built for the
+ * grouped form or with the fused residual add.
+ */
+typedef enum {
+  SHARQ_MODE_SHARQ = 0,
+  SHARQ_MODE_SPARSE = 1,
+  SHARQ_MODE_DENSE = 2,
+  SHARQ_MODE_DENSE_DENSE = 3,
+  SHARQ_MODE_SPARSE_SPARSE = 4
+} sharq_mode;
+
+/*
  * A prepared activation: the output of sharq_prepare, the input of
  * sharq_linear / sharq_linear_grouped.  One row per token; panel-major (see
- * above).  Row bytes per row are listed as [rows][...].
+ * above).  Row bytes per row are listed as [rows][...].  In SHARQ_MODE_SHARQ:
  *
  *   sp_codes [rows][K*n/m/2]  backbone E2M1 codes of the kept positions only,
  *                             in ascending K order (Sec. 3.4: "quantizes and
@@ -104,6 +134,16 @@ typedef struct {
  *   tensor_scale              NVFP4: one fp32 per-tensor scale S (device); the
  *                             element value is code * block_scale * S.
  *                             MXFP4: unused (may be NULL).
+ *   mode                      SHARQ_MODE_SHARQ (0).
+ *   dn_meta                   unused (may be NULL).
+ *
+ * Other modes: path 1 lives in sp_codes / sp_meta / sp_scale and path 2 in
+ * dn_codes / dn_meta / dn_scale.  A sparse path has the backbone layout above
+ * (codes [rows][K*n/m/2], meta [rows][K/8], scale [rows][K/32]); a dense path
+ * the residual layout (codes [rows][K/2], no meta, scale [rows][K/32] MXFP4 or
+ * [rows][K/16] NVFP4); an absent path's buffers are unused and may be NULL.
+ * sharq_act_buffer_bytes_mode gives every size (0 = unused).  Alignment as
+ * above (dn_meta 4-byte aligned).
  */
 typedef struct {
   int64_t rows, K;
@@ -115,6 +155,8 @@ typedef struct {
   uint8_t *dn_codes;
   uint8_t *dn_scale;
   float *tensor_scale;
+  sharq_mode mode;
+  uint8_t *dn_meta;
 } sharq_act;
 
 /*
@@ -149,6 +191,10 @@ SHARQ_API size_t sharq_act_buffer_bytes(int64_t rows, int64_t K, sharq_format fm
                               int32_t which /* 0 sp_codes, 1 sp_meta, 2 sp_scale, 3 dn_codes, 4 dn_scale */);
 SHARQ_API size_t sharq_weight_buffer_bytes(int64_t N, int64_t K, sharq_format fmt,
                                  int32_t which /* 0 codes, 1 scale, 2 scale_dn */);
+/* Buffer sizes of a prepared activation in a given mode; which 5 = dn_meta.
+ * 0 for a buffer the mode does not use, or for an invalid combination. */
+SHARQ_API size_t sharq_act_buffer_bytes_mode(int64_t rows, int64_t K, sharq_format fmt, sharq_pattern nm,
+                                   sharq_mode mode, int32_t which);
 
 /*
  * Quantize a weight W [N][K] (row stride ldw elements, dtype wdt = BF16 or
@@ -179,6 +225,10 @@ SHARQ_API sharq_status sharq_quantize_weight(const void *W, sharq_dtype wdt, int
  * (one more read of X) and writes it to out->tensor_scale; otherwise
  * *tensor_scale_in (device) is used and copied there.
  * out->rows, K, fmt, nm and the buffers must match the arguments.
+ * out->mode selects the path combination (see sharq_mode): steps 2-5 then
+ * become path 1 on y, the residual R = y - dequant(path 1), and path 2 on R.
+ * A mode with a sparse path needs a built pattern; SHARQ_MODE_DENSE and
+ * SHARQ_MODE_DENSE_DENSE ignore nm (it must still be valid).
  */
 SHARQ_API sharq_status sharq_prepare(const void *X, sharq_dtype xdt, int64_t M, int64_t K, int64_t ldx,
                            const void *gamma, float eps, sharq_pattern nm, sharq_format fmt,
@@ -194,7 +244,8 @@ SHARQ_API sharq_status sharq_prepare(const void *X, sharq_dtype xdt, int64_t M, 
  * place, when ldh == ldr) and then prepared exactly as sharq_prepare prepares
  * X.  residual: bf16 [M][K], row stride ldr.  Both 16-byte aligned with
  * 16-byte row strides.  With NVFP4 and no tensor_scale_in the amax pre-pass
- * forms h as well.  Other arguments, errors and outputs as for sharq_prepare.
+ * forms h as well.  Other arguments, errors and outputs as for sharq_prepare;
+ * out->mode must be SHARQ_MODE_SHARQ (others: SHARQ_EUNSUPPORTED).
  */
 SHARQ_API sharq_status sharq_prepare_residual(const void *X, const void *residual, void *h_out, sharq_dtype xdt,
                                     int64_t M, int64_t K, int64_t ldx, int64_t ldr, int64_t ldh,
@@ -210,7 +261,9 @@ SHARQ_API sharq_status sharq_prepare_residual(const void *X, const void *residua
  * block-scaled FP4 matrix cores; NVFP4 (whose E4M3 block scales those cannot
  * apply) multiplies the exactly dequantized bf16 values q * d and applies
  * S_x * S_w once to the fp32 sums.  NVFP4 needs a->tensor_scale and
- * w->tensor_scale.
+ * w->tensor_scale.  For the other modes of a->mode, Y is the sum over the
+ * mode's paths, each against the weight's view of its kind (sparse view for a
+ * sparse path, dense view for a dense one).
  */
 SHARQ_API sharq_status sharq_linear(const sharq_act *a, const sharq_weight *w, void *Y, sharq_dtype ydt,
                           int64_t ldy, void *stream);
@@ -222,8 +275,8 @@ SHARQ_API sharq_status sharq_linear(const sharq_act *a, const sharq_weight *w, v
  * expert_offsets: device int32 [w->experts + 1], non-decreasing, first 0,
  * last == total.  row_index: device int32 [total], each in [0, a->rows), or
  * NULL.  Y [total][N] (row stride ldy).  Offsets are read on the device; the
- * host never waits for them.  Built for MXFP4; NVFP4 returns
- * SHARQ_EUNSUPPORTED.
+ * host never waits for them.  Built for MXFP4 in SHARQ_MODE_SHARQ; NVFP4 or
+ * another mode returns SHARQ_EUNSUPPORTED.
  */
 SHARQ_API sharq_status sharq_linear_grouped(const sharq_act *a, const int32_t *row_index,
                                   const int32_t *expert_offsets, int64_t total,

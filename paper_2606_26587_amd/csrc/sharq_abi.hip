@@ -22,6 +22,13 @@ hipError_t launch_linear_nv(int pat, int ydt, const uint8_t* spc, const uint8_t*
 hipError_t launch_linear_mx(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                             const uint8_t* dnc, const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws,
                             int N, int K, void* Y, int64_t ldy, hipStream_t st);
+hipError_t launch_prep_mode(int mode, const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps,
+                            int pat, bool nv, const float* ts_in, float* ts_out, uint8_t* c1, uint8_t* m1,
+                            uint8_t* s1, uint8_t* c2, uint8_t* m2, uint8_t* s2, hipStream_t st);
+hipError_t launch_linear_slots(int mode, int pat, int ydt, bool nv, const uint8_t* c1, const uint8_t* m1,
+                               const uint8_t* s1, const uint8_t* c2, const uint8_t* m2, const uint8_t* s2,
+                               const float* tsx, int64_t M, const uint8_t* wc, const uint8_t* ws, const float* tsw,
+                               int N, int K, void* Y, int64_t ldy, hipStream_t st);
 hipError_t launch_linear_mx_grouped(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                                     const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx, int64_t act_rows,
                                     const int32_t* offs, int E, int64_t total, const uint8_t* wc, const uint8_t* ws,
@@ -51,18 +58,40 @@ int gemm_pattern(int pid) { return pid == 49 ? 48 : pid; }
 
 sharq_status hip_status(hipError_t e) { return e == hipSuccess ? SHARQ_OK : SHARQ_EHIP; }
 
+// Path kinds of the two slots of a mode: 0 absent, 1 sparse, 2 dense.
+constexpr int kNone = 0, kSparse = 1, kDense = 2;
+bool mode_ok(int mode) { return mode >= SHARQ_MODE_SHARQ && mode <= SHARQ_MODE_SPARSE_SPARSE; }
+int kind1(int mode) { return mode == SHARQ_MODE_DENSE ? kNone : (mode == SHARQ_MODE_DENSE_DENSE ? kDense : kSparse); }
+int kind2(int mode) {
+  return mode == SHARQ_MODE_SPARSE ? kNone : (mode == SHARQ_MODE_SPARSE_SPARSE ? kSparse : kDense);
+}
+bool has_sparse(int mode) { return kind1(mode) == kSparse || kind2(mode) == kSparse; }
+
+// Row bytes per 32 K positions of a slot's codes / metadata / scales.
+size_t slot_bytes(int kind, sharq_pattern nm, sharq_format fmt, int what, size_t k) {
+  if (kind == kNone) return 0;
+  if (kind == kSparse) return what == 0 ? k * (size_t)nm.n / (size_t)nm.m / 2 : what == 1 ? k / 8 : k / 32;
+  return what == 0 ? k / 2 : what == 1 ? 0 : (fmt == SHARQ_MXFP4 ? k / 32 : k / 16);
+}
+
 sharq_status check_act(const sharq_act* a) {
   if (!a) return SHARQ_EINVAL;
   if (a->rows < 0 || a->rows > INT_MAX || a->K <= 0 || a->K % 32 != 0 || a->K > kMaxK) return SHARQ_EINVAL;
-  const int pid = pattern_id(a->nm);
+  if (!mode_ok((int)a->mode)) return SHARQ_EINVAL;
+  const int mode = (int)a->mode;
+  const int pid = pattern_id(a->nm);   // 0: valid, not built
   if (pid < 0 || a->K % a->nm.m != 0) return SHARQ_EINVAL;
-  if (pid == 0) return SHARQ_EUNSUPPORTED;
+  if (pid == 0 && has_sparse(mode)) return SHARQ_EUNSUPPORTED;
   if (a->fmt != SHARQ_MXFP4 && a->fmt != SHARQ_NVFP4) return SHARQ_EINVAL;
   if (a->rows == 0) return SHARQ_OK;   // an empty activation is never dereferenced
-  if (!a->sp_codes || !a->sp_meta || !a->sp_scale || !a->dn_codes || !a->dn_scale) return SHARQ_EINVAL;
+  const int k1 = kind1(mode), k2 = kind2(mode);
+  if (k1 != kNone && (!a->sp_codes || !a->sp_scale || (k1 == kSparse && !a->sp_meta))) return SHARQ_EINVAL;
+  if (k2 != kNone && (!a->dn_codes || !a->dn_scale)) return SHARQ_EINVAL;
+  if (k2 == kSparse && !a->dn_meta) return SHARQ_EINVAL;
   if (a->fmt == SHARQ_NVFP4 && !a->tensor_scale) return SHARQ_EINVAL;
   if (!aligned(a->sp_codes, 16) || !aligned(a->dn_codes, 16) || !aligned(a->sp_meta, 4) ||
-      !aligned(a->sp_scale, 4) || !aligned(a->dn_scale, 4) || !aligned(a->tensor_scale, 4))
+      !aligned(a->sp_scale, 4) || !aligned(a->dn_scale, 4) || !aligned(a->tensor_scale, 4) ||
+      !aligned(a->dn_meta, 4))
     return SHARQ_EALIGN;
   return SHARQ_OK;
 }
@@ -109,6 +138,25 @@ size_t sharq_act_buffer_bytes(int64_t rows, int64_t K, sharq_format fmt, sharq_p
     case 2: return r * (k / 32);
     case 3: return r * (k / 2);
     case 4: return r * (fmt == SHARQ_MXFP4 ? k / 32 : k / 16);
+    default: return 0;
+  }
+}
+
+size_t sharq_act_buffer_bytes_mode(int64_t rows, int64_t K, sharq_format fmt, sharq_pattern nm, sharq_mode mode,
+                                   int32_t which) {
+  if (rows < 0 || K <= 0 || K % 32 != 0 || !mode_ok((int)mode)) return 0;
+  const int pid = pattern_id(nm);
+  if (pid < 0 || K % nm.m != 0 || (pid == 0 && has_sparse((int)mode))) return 0;
+  if (fmt != SHARQ_MXFP4 && fmt != SHARQ_NVFP4) return 0;
+  const size_t r = (size_t)rows, k = (size_t)K;
+  const int k1 = kind1((int)mode), k2 = kind2((int)mode);
+  switch (which) {
+    case 0: return r * slot_bytes(k1, nm, fmt, 0, k);
+    case 1: return r * slot_bytes(k1, nm, fmt, 1, k);
+    case 2: return r * slot_bytes(k1, nm, fmt, 2, k);
+    case 3: return r * slot_bytes(k2, nm, fmt, 0, k);
+    case 4: return r * slot_bytes(k2, nm, fmt, 2, k);
+    case 5: return r * slot_bytes(k2, nm, fmt, 1, k);
     default: return 0;
   }
 }
@@ -175,7 +223,17 @@ sharq_status prepare_impl(const void* X, const void* res, void* h_out, sharq_dty
     return SHARQ_EALIGN;
   if (res && (!aligned(res, 16) || !aligned(h_out, 16) || (ldr * 2) % 16 != 0 || (ldh * 2) % 16 != 0))
     return SHARQ_EALIGN;
+  if (res && out->mode != SHARQ_MODE_SHARQ) return SHARQ_EUNSUPPORTED;
   if (M == 0) return SHARQ_OK;
+  const int mode = (int)out->mode;
+  if (mode != SHARQ_MODE_SHARQ) {
+    if (res) return SHARQ_EUNSUPPORTED;
+    return hip_status(sharq::launch_prep_mode(mode, static_cast<const uint16_t*>(X), (int)M, (int)K, ldx,
+                                              static_cast<const uint16_t*>(gamma), eps, pid, nv,
+                                              nv ? tensor_scale_in : nullptr, nv ? out->tensor_scale : nullptr,
+                                              out->sp_codes, out->sp_meta, out->sp_scale, out->dn_codes,
+                                              out->dn_meta, out->dn_scale, reinterpret_cast<hipStream_t>(stream)));
+  }
   return hip_status(sharq::launch_prep(static_cast<const uint16_t*>(X), (int)M, (int)K, ldx,
                                        static_cast<const uint16_t*>(res), ldr, static_cast<uint16_t*>(h_out), ldh,
                                        static_cast<const uint16_t*>(gamma), eps, pid, nv, nv ? tensor_scale_in : nullptr,
@@ -216,6 +274,14 @@ sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sh
   if (!aligned(Y, ysize(ydt))) return SHARQ_EALIGN;
   if (a->rows == 0 || w->N == 0) return SHARQ_OK;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (a->mode != SHARQ_MODE_SHARQ) {
+    const int pid = pattern_id(a->nm);
+    return hip_status(sharq::launch_linear_slots((int)a->mode, pid > 0 ? gemm_pattern(pid) : 24, (int)ydt,
+                                                 a->fmt == SHARQ_NVFP4, a->sp_codes, a->sp_meta, a->sp_scale,
+                                                 a->dn_codes, a->dn_meta, a->dn_scale, a->tensor_scale, a->rows,
+                                                 w->codes, w->scale, w->tensor_scale, (int)w->N, (int)w->K, Y, ldy,
+                                                 st));
+  }
   if (a->fmt == SHARQ_NVFP4)
     return hip_status(sharq::launch_linear_nv(gemm_pattern(pattern_id(a->nm)), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale,
                                               a->dn_codes, a->dn_scale, a->tensor_scale, a->rows, w->codes,
@@ -235,7 +301,7 @@ sharq_status sharq_linear_grouped(const sharq_act* a, const int32_t* row_index, 
   s = check_weight(w);
   if (s != SHARQ_OK) return s;
   if (a->fmt != w->fmt || a->K != w->K) return SHARQ_EINVAL;
-  if (a->fmt == SHARQ_NVFP4) return SHARQ_EUNSUPPORTED;
+  if (a->fmt == SHARQ_NVFP4 || a->mode != SHARQ_MODE_SHARQ) return SHARQ_EUNSUPPORTED;
   if (total < 0 || total > INT_MAX) return SHARQ_EINVAL;
   if (!row_index && total > a->rows) return SHARQ_EINVAL;
   if (!ydt_ok(ydt)) return SHARQ_EUNSUPPORTED;

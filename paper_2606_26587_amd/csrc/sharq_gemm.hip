@@ -1632,6 +1632,291 @@ hipError_t launch_linear_nv(int pat, int ydt, const uint8_t* spc, const uint8_t*
 }
 
 // ---------------------------------------------------------------------------
+// Path combinations (Sec. 4.4, table "ablation-combination"): the sum of up
+// to two paths, each sparse (compressed codes + metadata, expanded in
+// registers; scale per 32 logical positions) or dense (plain codes), into one
+// accumulator.  Path 1 reads the sp_* buffers, path 2 the dn_* buffers.  A
+// slot kind is 0 (absent), kSlotDense, or the sparse metadata layout (24 for
+// 2:4, 48 for 4:8).  Generic kernels -- one tile per workgroup, double-
+// buffered weight stages, any K a multiple of 32 -- since the combinations
+// other than SharQ's exist for ablation.
+// ---------------------------------------------------------------------------
+
+constexpr int kSlotDense = 1;
+
+struct SlotBuf {
+  const uint8_t *c, *m, *s;   // codes, metadata (sparse only), scales
+};
+
+// One slot's data of one MXFP4 K step for this lane: per sub-step the codes
+// (dense: 16 bytes; sparse: 8 bytes in .x/.y and the metadata dword in .z)
+// and the four E8M0 scales of the step's blocks (byte j = block 4 ks + j).
+struct SlotStep {
+  uint4 c[2];
+  uint32_t s;
+};
+
+template <int KIND>
+__device__ __forceinline__ void load_slot_mx(SlotStep& d, const SlotBuf& b, int64_t r, int64_t R, int ks, int half,
+                                             int nblk, int K) {
+  if (KIND == 0) return;
+  const int wp = min(128, K - 128 * ks);
+  const int64_t pr = (int64_t)ks * R;
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub) {
+    const int j = 2 * sub + half;
+    const bool ok = 4 * ks + j < nblk;
+    if (KIND == kSlotDense) {
+      d.c[sub] = ok ? *reinterpret_cast<const uint4*>(b.c + pr * 64 + r * (wp / 2) + 16 * j) : make_uint4(0u, 0u, 0u, 0u);
+    } else {
+      const uint2 c = ok ? *reinterpret_cast<const uint2*>(b.c + pr * 32 + r * (wp / 4) + 8 * j) : make_uint2(0u, 0u);
+      const uint32_t m = ok ? *reinterpret_cast<const uint32_t*>(b.m + pr * 16 + r * (wp / 8) + 4 * j) : 0x44444444u;
+      d.c[sub] = make_uint4(c.x, c.y, m, 0u);
+    }
+  }
+  const uint8_t* sr = b.s + pr * 4 + r * (wp / 32);
+  d.s = 0u;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) d.s |= (uint32_t)(4 * ks + j < nblk ? sr[j] : 127u) << (8 * j);
+}
+
+template <int KIND>
+__device__ __forceinline__ v8i slot_operand(const uint4& c) {
+  if (KIND == kSlotDense) return as_operand(c);
+  return as_operand(expand_block<KIND>(make_uint2(c.x, c.y), c.z));
+}
+
+template <int SUB, int KIND>
+__device__ __forceinline__ void mma_slot(v16f (&acc)[8], const v8i (&b)[8], const SlotStep& a, const uint32_t (&bw)[4],
+                                         int half) {
+  if (KIND == 0) return;
+  const v8i op = slot_operand<KIND>(a.c[SUB]);
+  const uint32_t sa = a.s >> (8 * half);
+#pragma unroll
+  for (int f = 0; f < 8; ++f) {
+    if (f & 1) acc[f] = mfma_fp4<2 * SUB, 2 + SUB>(op, b[f], acc[f], sa, bw[f >> 1]);
+    else       acc[f] = mfma_fp4<2 * SUB, SUB>(op, b[f], acc[f], sa, bw[f >> 1]);
+  }
+}
+
+template <int K1, int K2>
+__device__ __forceinline__ void step_slots(v16f (&acc)[8], const SlotStep& a1, const SlotStep& a2, const uint8_t* lw,
+                                           const uint8_t* ls, int lane) {
+  const int half = lane >> 5, col = lane & 31;
+  uint32_t bw[4];
+  const uint4 q = *reinterpret_cast<const uint4*>(ls + (2 * col + half) * 16);
+  bw[0] = q.x; bw[1] = q.y; bw[2] = q.z; bw[3] = q.w;
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub) {
+    v8i b[8];
+#pragma unroll
+    for (int f = 0; f < 8; ++f)
+      b[f] = as_operand(*reinterpret_cast<const uint4*>(lw + (f * 32 + col) * kLdsStride + 32 * sub + 16 * half));
+    if (sub == 0) {
+      mma_slot<0, K1>(acc, b, a1, bw, half);
+      mma_slot<0, K2>(acc, b, a2, bw, half);
+    } else {
+      mma_slot<1, K1>(acc, b, a1, bw, half);
+      mma_slot<1, K2>(acc, b, a2, bw, half);
+    }
+  }
+}
+
+template <int K1, int K2, typename OutT>
+__global__ __launch_bounds__(256) void k_linear_slots_mx(SlotBuf p1, SlotBuf p2, int64_t M, const uint8_t* wc,
+                                                         const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy,
+                                                         int gx, int gy) {
+  constexpr int NF = 8, BN = 256;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * BN * kLdsStride + 2 * 64 * 16];
+  uint8_t* const lds_w = lds;
+  uint8_t* const lds_s = lds + 2 * BN * kLdsStride;
+  constexpr int SREC = 64 * 16;
+  int mt, nt;
+  tile_of(blockIdx.x, gx, gy, mt, nt);
+  const int n0 = nt * BN;
+  const int64_t row_lo = (int64_t)mt * kBM;
+  const int64_t row_hi = row_lo + kBM < M ? row_lo + kBM : M;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
+  const int nblk = K / 32, nks = (K + kBK - 1) / kBK;
+  int64_t r = row_lo + wave * 32 + (lane & 31);
+  if (r >= row_hi) r = row_hi - 1;   // clamp: loads stay in bounds, stores are masked
+
+  v16f acc[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[f][e] = 0.0f;
+
+  // the double-buffered pipeline of tile_mx: step ks computes from buffer
+  // ks & 1 while the weight tile of ks + 1 goes to the other buffer and the
+  // loads of ks + 2 are issued
+  SlotStep a0[2], a1[2];
+  WStep<NF> wn;
+  const int last = nks - 1;
+  load_w<NF, false>(wn, wc, ws, n0, N, K, 0, nblk);
+  load_slot_mx<K1>(a0[0], p1, r, M, 0, half, nblk, K);
+  load_slot_mx<K2>(a0[1], p2, r, M, 0, half, nblk, K);
+  store_w<NF>(wn, lds_w, lds_s);
+  load_w<NF, false>(wn, wc, ws, n0, N, K, min(1, last), nblk);
+  load_slot_mx<K1>(a1[0], p1, r, M, min(1, last), half, nblk, K);
+  load_slot_mx<K2>(a1[1], p2, r, M, min(1, last), half, nblk, K);
+  int ks = 0;
+  for (; ks + 1 < nks; ks += 2) {
+    __syncthreads();
+    step_slots<K1, K2>(acc, a0[0], a0[1], lds_w, lds_s, lane);
+    store_w<NF>(wn, lds_w + BN * kLdsStride, lds_s + SREC);
+    load_w<NF, false>(wn, wc, ws, n0, N, K, min(ks + 2, last), nblk);
+    load_slot_mx<K1>(a0[0], p1, r, M, min(ks + 2, last), half, nblk, K);
+    load_slot_mx<K2>(a0[1], p2, r, M, min(ks + 2, last), half, nblk, K);
+    __syncthreads();
+    step_slots<K1, K2>(acc, a1[0], a1[1], lds_w + BN * kLdsStride, lds_s + SREC, lane);
+    store_w<NF>(wn, lds_w, lds_s);
+    load_w<NF, false>(wn, wc, ws, n0, N, K, min(ks + 3, last), nblk);
+    load_slot_mx<K1>(a1[0], p1, r, M, min(ks + 3, last), half, nblk, K);
+    load_slot_mx<K2>(a1[1], p2, r, M, min(ks + 3, last), half, nblk, K);
+  }
+  if (ks < nks) {
+    __syncthreads();
+    step_slots<K1, K2>(acc, a0[0], a0[1], lds_w, lds_s, lane);
+  }
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int col = n0 + f * 32 + (lane & 31);
+    if (col >= N) continue;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int64_t row = row_lo + wave * 32 + 8 * (e / 4) + 4 * half + (e % 4);
+      if (row < row_hi) store_out<OutT>(Y + row * ldy + col, acc[f][e]);
+    }
+  }
+}
+
+// NVFP4: one K step is one 32-position block; both operands are exactly
+// dequantized to bf16 (see k_linear_nv).  A dense slot has two E4M3 scales
+// per block (halves of 16), a sparse slot one.
+struct SlotNv {
+  uint4 c;      // dense: codes; sparse: codes in .x/.y, metadata in .z
+  uint32_t s;   // scale byte(s)
+};
+
+template <int KIND>
+__device__ __forceinline__ void load_slot_nv(SlotNv& d, const SlotBuf& b, int64_t r, int64_t R, int ks, int K) {
+  if (KIND == 0) return;
+  const int p = ks >> 2, j = ks & 3, wp = min(128, K - 128 * p);
+  const int64_t pr = (int64_t)p * R;
+  if (KIND == kSlotDense) {
+    d.c = *reinterpret_cast<const uint4*>(b.c + pr * 64 + r * (wp / 2) + 16 * j);
+    d.s = *reinterpret_cast<const uint16_t*>(b.s + pr * 8 + r * (wp / 16) + 2 * j);
+  } else {
+    const uint2 c = *reinterpret_cast<const uint2*>(b.c + pr * 32 + r * (wp / 4) + 8 * j);
+    d.c = make_uint4(c.x, c.y, *reinterpret_cast<const uint32_t*>(b.m + pr * 16 + r * (wp / 8) + 4 * j), 0u);
+    d.s = b.s[pr * 4 + r * (wp / 32) + j];
+  }
+}
+
+// this lane's bf16 operand of sub-step t: K values 8 half + 16 t + 0..7
+template <int KIND>
+__device__ __forceinline__ bf16x8 slot_nv_operand(const SlotNv& a, int t, int half) {
+  if (KIND == kSlotDense) {
+    const uint32_t w[4] = {a.c.x, a.c.y, a.c.z, a.c.w};
+    const float d = e4m3_value(t ? (a.s >> 8) & 0xFFu : a.s & 0xFFu);
+    return as_bf16x8(dequant8_bf16(w[half + 2 * t], d));
+  }
+  const uint4 e = expand_block<KIND>(make_uint2(a.c.x, a.c.y), a.c.z);
+  const uint32_t w[4] = {e.x, e.y, e.z, e.w};
+  return as_bf16x8(dequant8_bf16(w[half + 2 * t], e4m3_value(a.s & 0xFFu)));
+}
+
+template <int K1, int K2>
+__device__ __forceinline__ void step_slots_nv(v16f (&acc)[8], const SlotNv& a1, const SlotNv& a2, const uint8_t* lw,
+                                              int lane) {
+  const int half = lane >> 5, col = lane & 31;
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    bf16x8 b[8];
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      const int row = f * 32 + col;
+      b[f] = as_bf16x8(*reinterpret_cast<const uint4*>(lw + row * 64 + 16 * ((half + 2 * t) ^ swz_nv(row))));
+    }
+    if (K1 != 0) {
+      const bf16x8 a = slot_nv_operand<K1>(a1, t, half);
+#pragma unroll
+      for (int f = 0; f < 8; ++f) acc[f] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[f], acc[f], 0, 0, 0);
+    }
+    if (K2 != 0) {
+      const bf16x8 a = slot_nv_operand<K2>(a2, t, half);
+#pragma unroll
+      for (int f = 0; f < 8; ++f) acc[f] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[f], acc[f], 0, 0, 0);
+    }
+  }
+}
+
+template <int K1, int K2, typename OutT>
+__global__ __launch_bounds__(256) void k_linear_slots_nv(SlotBuf p1, SlotBuf p2, const float* ts_x, int64_t M,
+                                                         const uint8_t* wc, const uint8_t* ws, const float* ts_w,
+                                                         int N, int K, OutT* Y, int64_t ldy, int gx, int gy) {
+  constexpr int NF = 8, BN = 256;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * BN * 64];
+  int mt, nt;
+  tile_of(blockIdx.x, gx, gy, mt, nt);
+  const int n0 = nt * BN;
+  const int64_t row_lo = (int64_t)mt * kBM;
+  const int64_t row_hi = row_lo + kBM < M ? row_lo + kBM : M;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
+  const int nks = K / 32;
+  int64_t r = row_lo + wave * 32 + (lane & 31);
+  if (r >= row_hi) r = row_hi - 1;
+
+  v16f acc[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[f][e] = 0.0f;
+
+  SlotNv a0[2], a1[2];
+  NvW wn;
+  const int last = nks - 1;
+  load_nv_w<NF>(wn, wc, ws, n0, N, K, 0);
+  load_slot_nv<K1>(a0[0], p1, r, M, 0, K);
+  load_slot_nv<K2>(a0[1], p2, r, M, 0, K);
+  store_nv_w(wn, lds);
+  load_nv_w<NF>(wn, wc, ws, n0, N, K, min(1, last));
+  load_slot_nv<K1>(a1[0], p1, r, M, min(1, last), K);
+  load_slot_nv<K2>(a1[1], p2, r, M, min(1, last), K);
+  int ks = 0;
+  for (; ks + 1 < nks; ks += 2) {
+    __syncthreads();
+    step_slots_nv<K1, K2>(acc, a0[0], a0[1], lds, lane);
+    store_nv_w(wn, lds + BN * 64);
+    load_nv_w<NF>(wn, wc, ws, n0, N, K, min(ks + 2, last));
+    load_slot_nv<K1>(a0[0], p1, r, M, min(ks + 2, last), K);
+    load_slot_nv<K2>(a0[1], p2, r, M, min(ks + 2, last), K);
+    __syncthreads();
+    step_slots_nv<K1, K2>(acc, a1[0], a1[1], lds + BN * 64, lane);
+    store_nv_w(wn, lds);
+    load_nv_w<NF>(wn, wc, ws, n0, N, K, min(ks + 3, last));
+    load_slot_nv<K1>(a1[0], p1, r, M, min(ks + 3, last), K);
+    load_slot_nv<K2>(a1[1], p2, r, M, min(ks + 3, last), K);
+  }
+  if (ks < nks) {
+    __syncthreads();
+    step_slots_nv<K1, K2>(acc, a0[0], a0[1], lds, lane);
+  }
+  const float scale = *ts_x * *ts_w;
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int col = n0 + f * 32 + (lane & 31);
+    if (col >= N) continue;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int64_t row = row_lo + wave * 32 + 8 * (e / 4) + 4 * half + (e % 4);
+      if (row < row_hi) store_out<OutT>(Y + row * ldy + col, acc[f][e] * scale);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Host-side launchers
 // ---------------------------------------------------------------------------
 
@@ -1735,6 +2020,52 @@ hipError_t launch_linear_mx_grouped(int pat, int ydt, const uint8_t* spc, const 
                                            st)
              : go_grouped_dt<NF, 48, false>(ydt, spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, total, wc, ws, N, K, Y, ldy,
                                             st);
+}
+
+
+template <int K1, int K2, typename OutT>
+static hipError_t go_slots(bool nv, const SlotBuf& p1, const SlotBuf& p2, const float* tsx, int64_t M,
+                           const uint8_t* wc, const uint8_t* ws, const float* tsw, int N, int K, void* Y, int64_t ldy,
+                           hipStream_t st) {
+  const int gx = (N + 255) / 256, gy = (int)((M + kBM - 1) / kBM);
+  const dim3 grid((unsigned)(gx * gy)), block(256);
+  if (nv)
+    k_linear_slots_nv<K1, K2, OutT><<<grid, block, 0, st>>>(p1, p2, tsx, M, wc, ws, tsw, N, K,
+                                                            reinterpret_cast<OutT*>(Y), ldy, gx, gy);
+  else
+    k_linear_slots_mx<K1, K2, OutT><<<grid, block, 0, st>>>(p1, p2, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy,
+                                                            gx, gy);
+  return hipGetLastError();
+}
+
+template <int K1, int K2>
+static hipError_t go_slots_dt(int ydt, bool nv, const SlotBuf& p1, const SlotBuf& p2, const float* tsx, int64_t M,
+                              const uint8_t* wc, const uint8_t* ws, const float* tsw, int N, int K, void* Y,
+                              int64_t ldy, hipStream_t st) {
+  if (ydt == 2) return go_slots<K1, K2, float>(nv, p1, p2, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
+  if (ydt == 1) return go_slots<K1, K2, _Float16>(nv, p1, p2, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
+  return go_slots<K1, K2, uint16_t>(nv, p1, p2, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
+}
+
+// Path combinations (modes 1-4 of the C interface): 1 sparse, 2 dense (RTN),
+// 3 dense + dense, 4 sparse + sparse.  pat: 24 or 48 (the sparse metadata
+// layout).  nv: NVFP4 (the weight's sparse view `ws` serves every path: its
+// per-16 dense view holds the same values).
+hipError_t launch_linear_slots(int mode, int pat, int ydt, bool nv, const uint8_t* c1, const uint8_t* m1,
+                               const uint8_t* s1, const uint8_t* c2, const uint8_t* m2, const uint8_t* s2,
+                               const float* tsx, int64_t M, const uint8_t* wc, const uint8_t* ws, const float* tsw,
+                               int N, int K, void* Y, int64_t ldy, hipStream_t st) {
+  const SlotBuf p1{c1, m1, s1}, p2{c2, m2, s2};
+  const bool p24 = pat == 24;
+  switch (mode) {
+    case 1: return p24 ? go_slots_dt<24, 0>(ydt, nv, p1, p2, tsx, M, wc, ws, tsw, N, K, Y, ldy, st)
+                       : go_slots_dt<48, 0>(ydt, nv, p1, p2, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
+    case 2: return go_slots_dt<0, kSlotDense>(ydt, nv, p1, p2, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
+    case 3: return go_slots_dt<kSlotDense, kSlotDense>(ydt, nv, p1, p2, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
+    case 4: return p24 ? go_slots_dt<24, 24>(ydt, nv, p1, p2, tsx, M, wc, ws, tsw, N, K, Y, ldy, st)
+                       : go_slots_dt<48, 48>(ydt, nv, p1, p2, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace sharq

@@ -669,6 +669,172 @@ __global__ __launch_bounds__(256) void k_amax_plain(XSrc src, int M, int K, uint
 }
 
 // ---------------------------------------------------------------------------
+// Path combinations (Sec. 4.4, table "ablation-combination"; Sec. 3.1 eq.
+// "direct-sparse-quant").  Path 1 quantizes y, path 2 the residual of y
+// against path 1's dequantized values.  A sparse path keeps the top n of every
+// m of its own input and quantizes the kept values per 32 logical positions
+// (the backbone quantizer above); a dense path is the format's plain
+// quantizer (MXFP4 per 32, NVFP4 per 16).  Path 1 is stored in the sp_*
+// buffers and path 2 in the dn_* buffers (plus dn_meta for a sparse path 2),
+// each with the block layout of its kind.
+// ---------------------------------------------------------------------------
+
+enum PathKind { kPathNone = 0, kPathSparse = 1, kPathDense = 2 };
+
+// mode ids of the C interface: 1 sparse, 2 dense (RTN), 3 dense+dense,
+// 4 sparse+sparse (0, the method itself, runs the kernels above)
+__host__ __device__ constexpr int path1_kind(int mode) {
+  return mode == 2 ? kPathNone : (mode == 3 ? kPathDense : kPathSparse);
+}
+__host__ __device__ constexpr int path2_kind(int mode) {
+  return mode == 1 ? kPathNone : (mode == 4 ? kPathSparse : kPathDense);
+}
+
+struct PathBufs {
+  uint8_t *c1, *m1, *s1, *c2, *m2, *s2;
+  int64_t M;
+  int K;
+};
+
+template <int PAT, class Q>
+__device__ __forceinline__ void backbone_of(const float (&v)[32], const Q& qz, uint32_t (&codes)[2], uint32_t& meta,
+                                            float (&R)[32]) {
+  if (PAT == 24)
+    backbone_24(v, qz, codes, meta, R);
+  else if (PAT == 49)
+    backbone_48p(v, qz, codes, meta, R);
+  else
+    backbone_48(v, qz, codes, meta, R);
+}
+
+// One path of kind KIND applied to the 32 values v of block number V (the
+// panel-major block order of block_index): its codes / metadata / scales are
+// stored, and R receives v minus the path's dequantized values.
+template <int KIND, int PAT, bool NV>
+__device__ __forceinline__ void path_block(const float (&v)[32], float S, float six_s, uint8_t* __restrict__ c,
+                                           uint8_t* __restrict__ mt, uint8_t* __restrict__ sc, int64_t V,
+                                           float (&R)[32]) {
+  if (KIND == kPathSparse) {
+    // the group maximum is always kept, so the kept values' block max is v's
+    uint32_t codes[2], meta;
+    if (NV) {
+      const NvQ q = NvQ::make(absmax32(v), six_s, S);
+      backbone_of<PAT>(v, q, codes, meta, R);
+      sc[V] = (uint8_t)e4m3_bits(q.d);
+    } else {
+      const int e = mx_exponent(__float_as_uint(absmax32(v)));
+      backbone_of<PAT>(v, MxQ::make(e), codes, meta, R);
+      sc[V] = (uint8_t)(e + 127);
+    }
+    *reinterpret_cast<uint2*>(c + V * 8) = make_uint2(codes[0], codes[1]);
+    *reinterpret_cast<uint32_t*>(mt + V * 4) = meta;
+  } else {
+    uint32_t w[4];
+    if (NV) {
+      const NvQ q0 = NvQ::make(absmax16(v), six_s, S), q1 = NvQ::make(absmax16(v + 16), six_s, S);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const NvQ& q = i < 2 ? q0 : q1;
+        w[i] = enc8(v + 8 * i, q);
+        const v2f d0 = q.template dec2<0>(w[i]), d1 = q.template dec2<1>(w[i]);
+        const v2f d2 = q.template dec2<2>(w[i]), d3 = q.template dec2<3>(w[i]);
+        R[8 * i + 0] = v[8 * i + 0] - d0.x; R[8 * i + 1] = v[8 * i + 1] - d0.y;
+        R[8 * i + 2] = v[8 * i + 2] - d1.x; R[8 * i + 3] = v[8 * i + 3] - d1.y;
+        R[8 * i + 4] = v[8 * i + 4] - d2.x; R[8 * i + 5] = v[8 * i + 5] - d2.y;
+        R[8 * i + 6] = v[8 * i + 6] - d3.x; R[8 * i + 7] = v[8 * i + 7] - d3.y;
+      }
+      sc[V * 2] = (uint8_t)e4m3_bits(q0.d);
+      sc[V * 2 + 1] = (uint8_t)e4m3_bits(q1.d);
+    } else {
+      const int e = mx_exponent(__float_as_uint(absmax32(v)));
+      const MxQ q = MxQ::make(e);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        w[i] = enc8(v + 8 * i, q);
+        const v2f d0 = q.template dec2<0>(w[i]), d1 = q.template dec2<1>(w[i]);
+        const v2f d2 = q.template dec2<2>(w[i]), d3 = q.template dec2<3>(w[i]);
+        R[8 * i + 0] = v[8 * i + 0] - d0.x; R[8 * i + 1] = v[8 * i + 1] - d0.y;
+        R[8 * i + 2] = v[8 * i + 2] - d1.x; R[8 * i + 3] = v[8 * i + 3] - d1.y;
+        R[8 * i + 4] = v[8 * i + 4] - d2.x; R[8 * i + 5] = v[8 * i + 5] - d2.y;
+        R[8 * i + 6] = v[8 * i + 6] - d3.x; R[8 * i + 7] = v[8 * i + 7] - d3.y;
+      }
+      sc[V] = (uint8_t)(e + 127);
+    }
+    *reinterpret_cast<uint4*>(c + V * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+template <int MODE, int PAT, bool NV>
+__device__ __forceinline__ void mode_block(const float (&y)[32], const PathBufs& o, int64_t V, float S, float six_s) {
+  constexpr int K1 = path1_kind(MODE), K2 = path2_kind(MODE);
+  float R[32];
+  if (K1 != kPathNone) {
+    path_block<K1, PAT, NV>(y, S, six_s, o.c1, o.m1, o.s1, V, R);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 32; ++k) R[k] = y[k];
+  }
+  if (K2 != kPathNone) {
+    float R2[32];   // the second path's own residual is not used
+    path_block<K2, PAT, NV>(R, S, six_s, o.c2, o.m2, o.s2, V, R2);
+  }
+}
+
+// One wavefront per row (4 rows per workgroup), lane l owning blocks
+// l, l + 64, ...  With RMSNorm (NORM) the row is read twice: a first pass
+// forms the same balanced tree as the other kernels (in-lane block sums, the
+// lane butterfly per 2048-position chunk, the chunks pairwise; chunks past the
+// row add exact zeros), a second pass quantizes.  Not a tuned kernel: the path
+// combinations exist for ablation, not for the method's hot path.
+template <int MODE, int PAT, bool NV, bool NORM>
+__global__ __launch_bounds__(256) void k_prep_mode(XSrc src, int M, int K, const uint16_t* __restrict__ gamma,
+                                                   float eps, PathBufs o, const float* S_ptr) {
+  constexpr int NB = 8;   // chunks of 2048 positions (K <= 16384 with RMSNorm)
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;   // whole wavefront; the kernel has no block barrier
+  const int nblk = K / 32;
+  const float S = NV ? *S_ptr : 1.0f, six_s = 6.0f * S;
+  float r = 1.0f;
+  if (NORM) {
+    float chunk[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int b = lane + 64 * i;
+      float ss = 0.0f;
+      if (b < nblk) {
+        uint4 q[4];
+        load_block<false>(src, row, b, q, false);
+        float x[32];
+        unpack_bf16x32(q, x);
+        ss = block_sum_sq(x);
+      }
+      chunk[i] = wave_tree_sum(ss);
+    }
+#pragma unroll
+    for (int w = NB / 2; w >= 1; w >>= 1)
+#pragma unroll
+      for (int k = 0; k < w; ++k) chunk[k] = chunk[2 * k] + chunk[2 * k + 1];
+    r = (float)(1.0 / __builtin_sqrt((double)chunk[0] / (double)K + (double)eps));
+  }
+  const uint4* gr = reinterpret_cast<const uint4*>(gamma);
+  for (int b = lane; b < nblk; b += 64) {
+    uint4 q[4];
+    load_block<false>(src, row, b, q, false);
+    float y[32];
+    if (NORM) {
+      uint4 gq[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) gq[j] = gr[4 * b + j];
+      norm_block(q, gq, r, y);
+    } else {
+      unpack_bf16x32(q, y);
+    }
+    mode_block<MODE, PAT, NV>(y, o, block_index(o.M, o.K, row, b), S, six_s);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Host-side launchers (called from the C ABI after validation)
 // ---------------------------------------------------------------------------
 
@@ -759,6 +925,61 @@ hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint1
   }
   if (res) go_prep_pat<true>(pat, nv, src, M, K, gamma, eps, o, ts_out, grid, st);
   else go_prep_pat<false>(pat, nv, src, M, K, gamma, eps, o, ts_out, grid, st);
+  return hipGetLastError();
+}
+
+template <int MODE, int PAT, bool NV>
+static void go_prep_mode(const XSrc& src, int M, int K, const uint16_t* gamma, float eps, const PathBufs& o,
+                         const float* S_ptr, dim3 grid, hipStream_t st) {
+  if (gamma)
+    k_prep_mode<MODE, PAT, NV, true><<<grid, 256, 0, st>>>(src, M, K, gamma, eps, o, S_ptr);
+  else
+    k_prep_mode<MODE, PAT, NV, false><<<grid, 256, 0, st>>>(src, M, K, gamma, eps, o, S_ptr);
+}
+
+template <int MODE, bool NV>
+static void go_prep_mode_pat(int pat, const XSrc& src, int M, int K, const uint16_t* gamma, float eps,
+                             const PathBufs& o, const float* S_ptr, dim3 grid, hipStream_t st) {
+  if (path1_kind(MODE) != kPathSparse && path2_kind(MODE) != kPathSparse)
+    go_prep_mode<MODE, 24, NV>(src, M, K, gamma, eps, o, S_ptr, grid, st);   // the pattern is not used
+  else if (pat == 24)
+    go_prep_mode<MODE, 24, NV>(src, M, K, gamma, eps, o, S_ptr, grid, st);
+  else if (pat == 49)
+    go_prep_mode<MODE, 49, NV>(src, M, K, gamma, eps, o, S_ptr, grid, st);
+  else
+    go_prep_mode<MODE, 48, NV>(src, M, K, gamma, eps, o, S_ptr, grid, st);
+}
+
+// Preparation of a path combination (mode 1-4; see PathKind).  Buffers c1,
+// m1, s1 receive path 1 and c2, m2, s2 path 2, in the layout of their kinds.
+hipError_t launch_prep_mode(int mode, const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps,
+                            int pat, bool nv, const float* ts_in, float* ts_out, uint8_t* c1, uint8_t* m1,
+                            uint8_t* s1, uint8_t* c2, uint8_t* m2, uint8_t* s2, hipStream_t st) {
+  const PathBufs o{c1, m1, s1, c2, m2, s2, (int64_t)M, K};
+  const XSrc src{X, ldx, nullptr, 0, nullptr, 0};
+  const dim3 grid((unsigned)((M + 3) / 4));
+  if (nv) {
+    if (ts_in) {
+      k_copy_f32<<<1, 1, 0, st>>>(ts_in, ts_out);
+    } else {
+      uint32_t* slot = reinterpret_cast<uint32_t*>(ts_out);
+      k_store_u32<<<1, 1, 0, st>>>(slot, 0u);
+      go_amax<false>(src, M, K, gamma, eps, slot, grid, st);
+      k_pts_finalize<<<1, 1, 0, st>>>(slot);
+    }
+  }
+  const float* S = nv ? ts_out : nullptr;
+  switch (mode) {
+    case 1: nv ? go_prep_mode_pat<1, true>(pat, src, M, K, gamma, eps, o, S, grid, st)
+               : go_prep_mode_pat<1, false>(pat, src, M, K, gamma, eps, o, S, grid, st); break;
+    case 2: nv ? go_prep_mode_pat<2, true>(pat, src, M, K, gamma, eps, o, S, grid, st)
+               : go_prep_mode_pat<2, false>(pat, src, M, K, gamma, eps, o, S, grid, st); break;
+    case 3: nv ? go_prep_mode_pat<3, true>(pat, src, M, K, gamma, eps, o, S, grid, st)
+               : go_prep_mode_pat<3, false>(pat, src, M, K, gamma, eps, o, S, grid, st); break;
+    case 4: nv ? go_prep_mode_pat<4, true>(pat, src, M, K, gamma, eps, o, S, grid, st)
+               : go_prep_mode_pat<4, false>(pat, src, M, K, gamma, eps, o, S, grid, st); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

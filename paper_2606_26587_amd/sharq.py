@@ -22,6 +22,8 @@ MXFP4, NVFP4 = 0, 1
 BF16, F16, F32 = 0, 1, 2
 
 _FMT = {"mx": MXFP4, "mxfp4": MXFP4, "nv": NVFP4, "nvfp4": NVFP4}
+#: path combinations (sharq_mode): the method, and the ablation modes
+MODES = {"sharq": 0, "sparse": 1, "dense": 2, "dense_dense": 3, "sparse_sparse": 4}
 _DT = {torch.bfloat16: BF16, torch.float16: F16, torch.float32: F32}
 
 
@@ -38,7 +40,8 @@ class Pattern(ctypes.Structure):
 class ActStruct(ctypes.Structure):
     _fields_ = [("rows", ctypes.c_int64), ("K", ctypes.c_int64), ("fmt", ctypes.c_int), ("nm", Pattern),
                 ("sp_codes", ctypes.c_void_p), ("sp_meta", ctypes.c_void_p), ("sp_scale", ctypes.c_void_p),
-                ("dn_codes", ctypes.c_void_p), ("dn_scale", ctypes.c_void_p), ("tensor_scale", ctypes.c_void_p)]
+                ("dn_codes", ctypes.c_void_p), ("dn_scale", ctypes.c_void_p), ("tensor_scale", ctypes.c_void_p),
+                ("mode", ctypes.c_int), ("dn_meta", ctypes.c_void_p)]
 
 
 class WeightStruct(ctypes.Structure):
@@ -58,6 +61,8 @@ def _load():
     L.sharq_status_str.argtypes = [ctypes.c_int]
     L.sharq_act_buffer_bytes.restype = ctypes.c_size_t
     L.sharq_act_buffer_bytes.argtypes = [c_i64, c_i64, ctypes.c_int, Pattern, ctypes.c_int32]
+    L.sharq_act_buffer_bytes_mode.restype = ctypes.c_size_t
+    L.sharq_act_buffer_bytes_mode.argtypes = [c_i64, c_i64, ctypes.c_int, Pattern, ctypes.c_int, ctypes.c_int32]
     L.sharq_weight_buffer_bytes.restype = ctypes.c_size_t
     L.sharq_weight_buffer_bytes.argtypes = [c_i64, c_i64, ctypes.c_int, ctypes.c_int32]
     L.sharq_quantize_weight.restype = ctypes.c_int
@@ -100,7 +105,9 @@ def _stream(stream) -> ctypes.c_void_p:
 
 @dataclass
 class PreparedAct:
-    """Output of sharq_prepare: the compressed backbone and the residual (device buffers)."""
+    """Output of sharq_prepare: the compressed backbone and the residual (device
+    buffers).  In the ablation modes path 1 lives in the sp_* buffers and path 2
+    in the dn_* buffers (dn_meta: a sparse path 2)."""
     rows: int
     K: int
     fmt: int
@@ -113,12 +120,15 @@ class PreparedAct:
     dn_scale: torch.Tensor
     tensor_scale: Optional[torch.Tensor] = None
     pairs: bool = False
+    mode: int = 0
+    dn_meta: Optional[torch.Tensor] = None
 
     def struct(self) -> ActStruct:
         return ActStruct(self.rows, self.K, self.fmt, Pattern(self.n, self.m, int(self.pairs)), self.sp_codes.data_ptr(),
                          self.sp_meta.data_ptr(), self.sp_scale.data_ptr(), self.dn_codes.data_ptr(),
                          self.dn_scale.data_ptr(),
-                         None if self.tensor_scale is None else self.tensor_scale.data_ptr())
+                         None if self.tensor_scale is None else self.tensor_scale.data_ptr(), self.mode,
+                         None if self.dn_meta is None else self.dn_meta.data_ptr())
 
 
 @dataclass
@@ -139,16 +149,20 @@ class QuantWeight:
                             None if self.tensor_scale is None else self.tensor_scale.data_ptr())
 
 
-def alloc_act(rows: int, K: int, n: int = 2, m: int = 4, fmt="mx", device="cuda", pairs: bool = False) -> PreparedAct:
+def alloc_act(rows: int, K: int, n: int = 2, m: int = 4, fmt="mx", device="cuda", pairs: bool = False,
+              mode="sharq") -> PreparedAct:
     """Device buffers of a prepared activation (flat, panel-major; see include/sharq.h).
-    pairs=True: n:m selection in pairs (4:8 in pairs)."""
+    pairs=True: n:m selection in pairs (4:8 in pairs).  mode: a key of MODES
+    (or its id); buffers a mode does not use are empty."""
     f = _FMT[fmt] if isinstance(fmt, str) else fmt
-    sizes = [lib.sharq_act_buffer_bytes(rows, K, f, Pattern(n, m, int(pairs)), w) for w in range(5)]
-    if K <= 0 or K % 32 or (rows > 0 and min(sizes) == 0):
+    md = MODES[mode] if isinstance(mode, str) else int(mode)
+    sizes = [lib.sharq_act_buffer_bytes_mode(rows, K, f, Pattern(n, m, int(pairs)), md, w) for w in range(6)]
+    used = sizes[:5] if md == 0 else [z for z in sizes if z]
+    if K <= 0 or K % 32 or (rows > 0 and (not used or min(used) == 0)):
         raise SharqError(EINVAL, "alloc_act")
     bufs = [torch.empty(sz, dtype=torch.uint8, device=device) for sz in sizes]
     ts = torch.empty(1, dtype=torch.float32, device=device) if f == NVFP4 else None
-    return PreparedAct(rows, K, f, n, m, *bufs, tensor_scale=ts, pairs=pairs)
+    return PreparedAct(rows, K, f, n, m, *bufs[:5], tensor_scale=ts, pairs=pairs, mode=md, dn_meta=bufs[5])
 
 
 def alloc_weight(N: int, K: int, fmt="mx", experts: int = 1, device="cuda") -> QuantWeight:
@@ -178,12 +192,13 @@ def sharq_quantize_weight(w: torch.Tensor, fmt="mx", out: Optional[QuantWeight] 
 
 def sharq_prepare(x: torch.Tensor, gamma: Optional[torch.Tensor], eps: float = 1e-6, n: int = 2, m: int = 4,
                   fmt="mx", tensor_scale_in: Optional[torch.Tensor] = None, out: Optional[PreparedAct] = None,
-                  stream=None, pairs: bool = False) -> PreparedAct:
+                  stream=None, pairs: bool = False, mode="sharq") -> PreparedAct:
     """Fused preparation of activation rows X [M, K] (bf16, on the GPU).
-    pairs=True: n:m selection in pairs (NVFP4's 4:8 in pairs)."""
+    pairs=True: n:m selection in pairs (NVFP4's 4:8 in pairs).  mode: the
+    path combination (MODES; ignored when `out` is given, which carries it)."""
     M, K = x.shape
     if out is None:
-        out = alloc_act(M, K, n, m, fmt, x.device, pairs)
+        out = alloc_act(M, K, n, m, fmt, x.device, pairs, mode)
     f = _FMT[fmt] if isinstance(fmt, str) else fmt
     st = out.struct()
     _check(lib.sharq_prepare(_ptr(x), _DT.get(x.dtype, -1), M, K, x.stride(0), _ptr(gamma), ctypes.c_float(eps),

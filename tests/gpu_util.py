@@ -22,13 +22,17 @@ def host(t: torch.Tensor) -> np.ndarray:
 
 
 FMT_NAME = {S.MXFP4: "mx", S.NVFP4: "nv"}
+MODE_NAME = {v: k for k, v in S.MODES.items()}
 
 
 def act_to_oracle(a: S.PreparedAct) -> dict:
     """Device prepared activation -> the oracle's row-major dict."""
     bufs = {k: host(getattr(a, k)) for k in O.ACT_BUFFERS}
+    if a.dn_meta is not None:
+        bufs["dn_meta"] = host(a.dn_meta)
     ts = None if a.tensor_scale is None else np.float32(host(a.tensor_scale)[0])
-    return O.act_from_device_layout(bufs, a.rows, a.K, a.n, a.m, FMT_NAME[a.fmt], ts)
+    return O.act_from_device_layout(bufs, a.rows, a.K, a.n, a.m, FMT_NAME[a.fmt], ts, mode=MODE_NAME[a.mode],
+                                    pairs=a.pairs)
 
 
 def oracle_to_act(o: dict) -> S.PreparedAct:
@@ -38,9 +42,12 @@ def oracle_to_act(o: dict) -> S.PreparedAct:
     ts = None
     if fmt == S.NVFP4:
         ts = torch.tensor([float(o["tensor_scale"])], dtype=torch.float32, device="cuda")
-    return S.PreparedAct(o["dn_codes"].shape[0], o["K"], fmt, o["n"], o["m"], dev_u8(dev["sp_codes"]),
+    mode = S.MODES[o.get("mode", "sharq")]
+    dn_meta = dev_u8(dev["dn_meta"]) if "dn_meta" in dev else None
+    return S.PreparedAct(o["rows"], o["K"], fmt, o["n"], o["m"], dev_u8(dev["sp_codes"]),
                          dev_u8(dev["sp_meta"]), dev_u8(dev["sp_scale"]), dev_u8(dev["dn_codes"]),
-                         dev_u8(dev["dn_scale"]), tensor_scale=ts, pairs=bool(o.get("pairs", False)))
+                         dev_u8(dev["dn_scale"]), tensor_scale=ts, pairs=bool(o.get("pairs", False)), mode=mode,
+                         dn_meta=dn_meta)
 
 
 def oracle_to_weight(o: dict) -> S.QuantWeight:

@@ -23,7 +23,8 @@ class Pattern(ctypes.Structure):
 class Act(ctypes.Structure):
     _fields_ = [("rows", ctypes.c_int64), ("K", ctypes.c_int64), ("fmt", ctypes.c_int), ("nm", Pattern),
                 ("sp_codes", ctypes.c_void_p), ("sp_meta", ctypes.c_void_p), ("sp_scale", ctypes.c_void_p),
-                ("dn_codes", ctypes.c_void_p), ("dn_scale", ctypes.c_void_p), ("tensor_scale", ctypes.c_void_p)]
+                ("dn_codes", ctypes.c_void_p), ("dn_scale", ctypes.c_void_p), ("tensor_scale", ctypes.c_void_p),
+                ("mode", ctypes.c_int), ("dn_meta", ctypes.c_void_p)]
 
 
 class Weight(ctypes.Structure):
@@ -51,6 +52,9 @@ def L():
                                           ctypes.c_int64, ctypes.POINTER(Weight), ctypes.c_void_p]
     lib.sharq_act_buffer_bytes.restype = ctypes.c_size_t
     lib.sharq_act_buffer_bytes.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int, Pattern, ctypes.c_int32]
+    lib.sharq_act_buffer_bytes_mode.restype = ctypes.c_size_t
+    lib.sharq_act_buffer_bytes_mode.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int, Pattern, ctypes.c_int,
+                                                ctypes.c_int32]
     lib.sharq_weight_buffer_bytes.restype = ctypes.c_size_t
     lib.sharq_weight_buffer_bytes.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_int32]
     lib.sharq_status_str.restype = ctypes.c_char_p
@@ -89,8 +93,8 @@ def test_buffer_sizes(L):
 FAKE = 1 << 20   # never dereferenced: every case below is rejected (or empty) before any launch
 
 
-def act(rows=8, K=128, n=2, m=4, fmt=0, off=0, pairs=0):
-    return Act(rows, K, fmt, Pattern(n, m, pairs), FAKE + off, FAKE, FAKE, FAKE, FAKE, None)
+def act(rows=8, K=128, n=2, m=4, fmt=0, off=0, pairs=0, mode=0, dn_meta=None):
+    return Act(rows, K, fmt, Pattern(n, m, pairs), FAKE + off, FAKE, FAKE, FAKE, FAKE, None, mode, dn_meta)
 
 
 @pytest.mark.parametrize("kw,M,K,ldx,nm,expect", [
@@ -230,3 +234,54 @@ def test_nvfp4_grouped_not_built(L):
     w = Weight(64, 128, 4, 1, FAKE, FAKE, FAKE, FAKE)
     assert L.sharq_linear_grouped(ctypes.byref(nv_act()), None, FAKE, 8, ctypes.byref(w), FAKE, 2, 64,
                                   None) == EUNSUPPORTED
+
+
+# ----------------------------------------------------------------------------- path combinations
+
+SHARQ, SPARSE, DENSE, DENSE_DENSE, SPARSE_SPARSE = range(5)
+
+
+def test_buffer_sizes_per_mode(L):
+    rows, K = 5, 256
+    f = lambda fmt, nm, mode: [L.sharq_act_buffer_bytes_mode(rows, K, fmt, nm, mode, w) for w in range(6)]
+    p24 = Pattern(2, 4)
+    # which: 0 sp_codes, 1 sp_meta, 2 sp_scale, 3 dn_codes, 4 dn_scale, 5 dn_meta
+    assert f(0, p24, SHARQ) == [rows * K // 4, rows * K // 8, rows * K // 32, rows * K // 2, rows * K // 32, 0]
+    assert f(0, p24, SHARQ)[:5] == [L.sharq_act_buffer_bytes(rows, K, 0, p24, w) for w in range(5)]
+    assert f(0, p24, SPARSE) == [rows * K // 4, rows * K // 8, rows * K // 32, 0, 0, 0]
+    assert f(1, p24, DENSE) == [0, 0, 0, rows * K // 2, rows * K // 16, 0]
+    assert f(1, p24, DENSE_DENSE) == [rows * K // 2, 0, rows * K // 16, rows * K // 2, rows * K // 16, 0]
+    assert f(1, Pattern(4, 8, 1), SPARSE_SPARSE) == [rows * K // 4, rows * K // 8, rows * K // 32,
+                                                     rows * K // 4, rows * K // 32, rows * K // 8]
+    # a dense-only mode accepts a valid pattern that no sparse path is built for
+    assert f(0, Pattern(1, 4), DENSE)[3] == rows * K // 2
+    assert f(0, Pattern(1, 4), SPARSE) == [0] * 6
+    assert f(0, p24, 5) == [0] * 6 and f(0, p24, -1) == [0] * 6
+
+
+def test_mode_rejections(L):
+    def prep(a, nm=(2, 4)):
+        return L.sharq_prepare(FAKE, 0, a.rows, a.K, a.K, None, 1e-6, Pattern(*nm), a.fmt, None, ctypes.byref(a),
+                               None)
+    assert prep(act(mode=5)) == EINVAL
+    assert prep(act(mode=-1)) == EINVAL
+    assert prep(act(n=1, m=4, mode=SPARSE), (1, 4)) == EUNSUPPORTED
+    assert prep(act(n=1, m=4, mode=SPARSE_SPARSE), (1, 4)) == EUNSUPPORTED
+    assert prep(act(mode=SPARSE_SPARSE, dn_meta=None)) == EINVAL        # a sparse path 2 needs its metadata
+    assert prep(act(mode=SPARSE_SPARSE, dn_meta=FAKE + 2)) == EALIGN
+    # the fused residual add and the grouped GEMM are built for the method only
+    a = act(mode=DENSE_DENSE)
+    st = L.sharq_prepare_residual(FAKE, FAKE, FAKE, 0, 8, 128, 128, 128, 128, None, 1e-6, Pattern(2, 4), 0, None,
+                                  ctypes.byref(a), None)
+    assert st == EUNSUPPORTED
+    w = Weight(64, 128, 1, 0, FAKE, FAKE, FAKE, None)
+    st = L.sharq_linear_grouped(ctypes.byref(act(mode=SPARSE)), None, FAKE, 8, ctypes.byref(w), FAKE, 0, 64, None)
+    assert st == EUNSUPPORTED
+
+
+def test_mode_empty_calls_launch_nothing(L):
+    for mode in range(5):
+        a = act(rows=0, mode=mode)
+        assert L.sharq_prepare(None, 0, 0, 128, 128, None, 1e-6, Pattern(2, 4), 0, None, ctypes.byref(a), None) == OK
+        w = Weight(64, 128, 1, 0, FAKE, FAKE, FAKE, None)
+        assert L.sharq_linear(ctypes.byref(a), ctypes.byref(w), None, 0, 64, None) == OK
