@@ -20,6 +20,10 @@ Other workloads (--workload), one JSON line each:
                 NVFP4 with the 4:8 in-pairs backbone
   moe           Qwen3-30B-A3B expert layers, 4096 tokens, top-8 of 128 experts,
                 4:8 backbone, grouped GEMMs
+  ablation      the path combinations (Sparse, plain FP4 RTN, Dense+Dense,
+                Sparse+Sparse, SharQ) on the Llama prefill linears, MXFP4 2:4
+                and NVFP4 4:8 in pairs: time per step and the output error
+                against the unquantized product, per mode
 --calibrate-copy MiB runs a plain device copy of that size (the reference
 kernel for scaling the profiler's HBM byte counters) and nothing else.
 
@@ -376,6 +380,84 @@ def moe(args, torch, S, synth, dev, stream):
     return out
 
 
+ABLATION_MODES = ["sharq", "sparse", "dense", "dense_dense", "sparse_sparse"]
+MODE_PATHS = {"sharq": 2, "sparse": 1, "dense": 1, "dense_dense": 2, "sparse_sparse": 2}
+
+
+def ablation(args, torch, S, synth, dev, stream):
+    """Path combinations (the paper's ablation over sparse / dense paths) on
+    the Llama-3.1-8B prefill linears at M = 2048, in MXFP4 2:4 and in the
+    paper's NVFP4 4:8-in-pairs setting.  Per mode: the step time (prep + GEMM
+    of the three linears) and, as an accuracy proxy that needs no dataset, the
+    mean per-row relative error of Y against the unquantized product y W^T
+    (fp32; weight quantization included, the same for every mode)."""
+    def to_dev(u16):
+        return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    T = T_TOKENS
+    eps = synth.LLAMA_EPS
+    outs = []
+    for fmt, n, m, pairs in (("mx", 2, 4, False), ("nv", 4, 8, True)):
+        layers = []
+        for name, (K, N, norm) in synth.LLAMA_LINEARS.items():
+            x = to_dev(synth.activations(T, K, seed=0))
+            g = to_dev(synth.gamma(K, seed=0)) if norm else None
+            w_bf = to_dev(synth.weight(N, K, seed=0))
+            # the unquantized product, in fp32: y = RMSNorm(x) * gamma (or x), Y = y W^T
+            xf = x.float()
+            if norm:
+                r = torch.rsqrt(xf.pow(2).mean(dim=1, keepdim=True) + eps)
+                yf = (xf * r) * g.float()[None, :]
+            else:
+                yf = xf
+            yref = yf @ w_bf.float().t().contiguous()
+            layers.append(dict(name=name, K=K, N=N, norm=norm, x=x, g=g, w=S.sharq_quantize_weight(w_bf, fmt),
+                               yref=yref, y=torch.empty((T, N), dtype=torch.float32, device=dev)))
+            del xf, yf
+        torch.cuda.synchronize()
+        res = {}
+        for mode in ABLATION_MODES:
+            acts = [S.alloc_act(T, L["K"], n, m, fmt, dev, pairs, mode) for L in layers]
+
+            def step(i, mark, acts=acts):
+                for li, L in enumerate(layers):
+                    if mark:
+                        mark(2 * li)
+                    S.sharq_prepare(L["x"], L["g"], eps, n, m, fmt, out=acts[li], stream=stream, pairs=pairs)
+                    if mark:
+                        mark(2 * li + 1)
+                    S.sharq_linear(acts[li], L["w"], out=L["y"], stream=stream)
+                if mark:
+                    mark(2 * len(layers))
+
+            ms_step, _, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
+            errs = {}
+            for L in layers:
+                d = (L["y"] - L["yref"]).norm(dim=1) / L["yref"].norm(dim=1).clamp_min(1e-30)
+                errs[L["name"]] = float(d.mean())
+            flops = sum(2.0 * MODE_PATHS[mode] * T * L["N"] * L["K"] for L in layers)
+            res[mode] = {"ms_per_step": ms_step, "executed_TFLOPs": flops / (ms_step * 1e-3) / 1e12,
+                         "prep_us": [tm.op_ms(2 * li) * 1e3 for li in range(len(layers))],
+                         "gemm_us": [tm.op_ms(2 * li + 1) * 1e3 for li in range(len(layers))],
+                         "rel_err": errs, "rel_err_mean": float(np.mean(list(errs.values())))}
+            log(f"[bench] ablation {fmt} {mode:14s} {ms_step:7.4f} ms/step  rel err "
+                + "  ".join(f"{k} {v:.4f}" for k, v in errs.items()))
+            del acts
+        setting = "MXFP4 2:4" if fmt == "mx" else "NVFP4 4:8 in pairs"
+        out = base_record(args, "SharQ path-combination ablation: time per step and output error, Llama-8B M=2048",
+                          res["sharq"]["executed_TFLOPs"], "TFLOP/s", res["sharq"]["ms_per_step"],
+                          "mxfp4" if fmt == "mx" else "nvfp4",
+                          {"workload": f"Llama-3.1-8B prefill linears qkv, gate_up (RMSNorm), down; M=2048; "
+                                       f"{setting}; fp32 out; modes " + ", ".join(ABLATION_MODES), "tokens": T})
+        out["modes"] = res
+        out["error_definition"] = ("mean over token rows of |Y_t - y_t W^T| / |y_t W^T| (fp32 reference with the "
+                                   "unquantized weight), per linear")
+        outs.append(out)
+        del layers
+        torch.cuda.empty_cache()
+    return outs
+
+
 def calibrate_copy(torch, dev, mib):
     n = mib * (1 << 20)
     src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
@@ -392,7 +474,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama-prefill",
-                    choices=["llama-prefill", "llama-decode", "qwen-nvfp4", "llama-nvfp4-pairs", "moe"])
+                    choices=["llama-prefill", "llama-decode", "qwen-nvfp4", "llama-nvfp4-pairs", "moe",
+                             "ablation"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=T_TOKENS)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
@@ -428,6 +511,9 @@ def main():
         print(json.dumps(qwen_nvfp4(args, torch, S, synth, dev, stream)), flush=True)
     elif args.workload == "llama-nvfp4-pairs":
         print(json.dumps(llama_nvfp4_pairs(args, torch, S, synth, dev, stream)), flush=True)
+    elif args.workload == "ablation":
+        for o in ablation(args, torch, S, synth, dev, stream):
+            print(json.dumps(o), flush=True)
     else:
         print(json.dumps(moe(args, torch, S, synth, dev, stream)), flush=True)
 
