@@ -32,6 +32,7 @@ constexpr int kBM = 128;          // tile rows: 4 wavefronts x 32
 constexpr int kBK = 128;          // K per step: 4 scale blocks, 64 bytes of codes per row
 constexpr int kLdsStride = 80;    // bytes per staged weight row (64 + 16 to spread LDS banks)
 constexpr int kSkinnyMaxM = 64;   // activation rows up to which the small-M kernel runs
+constexpr int kSkinnyMaxRowTiled = 256;   // ... and, when the main kernel has few tiles, up to this many
 
 // ---------------------------------------------------------------------------
 // Backbone expansion: compressed 32-position block -> 32 dense E2M1 nibbles
@@ -416,6 +417,7 @@ __device__ __forceinline__ uint32_t expand48_lut(uint32_t c16, uint2 sel) {
 __device__ __forceinline__ void lut48_fill(uint2* lut) {
   if (threadIdx.x < 256) lut[threadIdx.x] = lut48_entry(threadIdx.x);
 }
+
 
 // Piece Q (0..15) of the next step's expanded backbone: block Q / 8, output
 // dword (Q % 8) / 2, 16-bit half Q % 2 (returned in place within the dword).
@@ -981,7 +983,8 @@ struct SkinnyStage {
 template <int MF, int NB>
 __device__ __forceinline__ void skinny_load(SkinnyStage<MF, NB>& st, const uint8_t* spc, const uint8_t* spm,
                                             const uint8_t* sps, const uint8_t* dnc, const uint8_t* dns, int64_t M,
-                                            const uint8_t* wc, const uint8_t* ws, int N, int n0, int ks, int lane) {
+                                            int64_t r0, const uint8_t* wc, const uint8_t* ws, int N, int n0, int ks,
+                                            int lane) {
   const int j = lane >> 4;   // block within the panel
   const int64_t pn = (int64_t)ks * N, pm = (int64_t)ks * M;
 #pragma unroll
@@ -992,7 +995,7 @@ __device__ __forceinline__ void skinny_load(SkinnyStage<MF, NB>& st, const uint8
   }
 #pragma unroll
   for (int m = 0; m < MF; ++m) {
-    int64_t row = 16 * m + (lane & 15);
+    int64_t row = r0 + 16 * m + (lane & 15);
     if (row >= M) row = M - 1;
     const int64_t V = (pm + row) * 4 + j;   // block-major index of (row, block)
     st.dn[m] = *reinterpret_cast<const uint4*>(dnc + V * 16);
@@ -1022,14 +1025,35 @@ __device__ __forceinline__ void skinny_step(v4f_t (&acc)[MF][NB], const SkinnySt
   }
 }
 
+// Workgroup id -> (column group, row tile).  Workgroups are dispatched
+// round-robin over the 8 XCDs; with several row tiles the ids are renumbered
+// to give each XCD a contiguous range in which the row tiles of one column
+// group follow each other, so the workgroups that read the same weight
+// columns share an L2.
+__device__ __forceinline__ void skinny_tile(int id, int ncg, int nrt, int& cg, int& rt) {
+  if (nrt == 1) {
+    cg = id;
+    rt = 0;
+    return;
+  }
+  const int total = ncg * nrt;
+  const int idp = (total & 7) == 0 ? (id & 7) * (total >> 3) + (id >> 3) : id;
+  cg = idp / nrt;
+  rt = idp - cg * nrt;
+}
+
 template <int MF, int NB, int KS, int PAT, typename OutT>
 __global__ __launch_bounds__(64 * KS) void k_linear_mx_skinny(const uint8_t* sp_codes, const uint8_t* sp_meta,
                                                               const uint8_t* sp_scale, const uint8_t* dn_codes,
                                                               const uint8_t* dn_scale, int64_t M, const uint8_t* wc,
-                                                              const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy) {
+                                                              const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy,
+                                                              int ncg, int nrt) {
   __shared__ float part[KS - 1][MF * NB][64][4];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int n0 = blockIdx.x * 16 * NB;
+  int cg, rt;
+  skinny_tile(blockIdx.x, ncg, nrt, cg, rt);
+  const int n0 = cg * 16 * NB;
+  const int64_t r0 = (int64_t)rt * 16 * MF;
   const int nks = K / kBK;
   const int per = (nks + KS - 1) / KS;
   const int k0 = wave * per, k1 = min(nks, k0 + per);
@@ -1042,17 +1066,17 @@ __global__ __launch_bounds__(64 * KS) void k_linear_mx_skinny(const uint8_t* sp_
 
   SkinnyStage<MF, NB> s0, s1;
   if (k0 < k1)
-    skinny_load<MF, NB>(s0, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, wc, ws, N, n0, k0, lane);
+    skinny_load<MF, NB>(s0, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, r0, wc, ws, N, n0, k0, lane);
   if (k0 + 1 < k1)
-    skinny_load<MF, NB>(s1, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, wc, ws, N, n0, k0 + 1, lane);
+    skinny_load<MF, NB>(s1, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, r0, wc, ws, N, n0, k0 + 1, lane);
   int ks = k0;
   for (; ks + 1 < k1; ks += 2) {
     skinny_step<MF, NB, PAT>(acc, s0);
     if (ks + 2 < k1)
-      skinny_load<MF, NB>(s0, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, wc, ws, N, n0, ks + 2, lane);
+      skinny_load<MF, NB>(s0, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, r0, wc, ws, N, n0, ks + 2, lane);
     skinny_step<MF, NB, PAT>(acc, s1);
     if (ks + 3 < k1)
-      skinny_load<MF, NB>(s1, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, wc, ws, N, n0, ks + 3, lane);
+      skinny_load<MF, NB>(s1, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, r0, wc, ws, N, n0, ks + 3, lane);
   }
   if (ks < k1) skinny_step<MF, NB, PAT>(acc, s0);
 
@@ -1076,7 +1100,7 @@ __global__ __launch_bounds__(64 * KS) void k_linear_mx_skinny(const uint8_t* sp_
         for (int r = 0; r < 4; ++r) acc[m][n][r] += part[w][m * NB + n][lane][r];
 #pragma unroll
   for (int m = 0; m < MF; ++m) {
-    const int64_t row = 16 * m + (lane & 15);
+    const int64_t row = r0 + 16 * m + (lane & 15);
     if (row >= M) continue;
 #pragma unroll
     for (int n = 0; n < NB; ++n)
@@ -1092,16 +1116,18 @@ template <int MF, int NB, int KS, int PAT, typename OutT>
 static hipError_t go_skinny(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
                             const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
                             void* Y, int64_t ldy, hipStream_t st) {
-  k_linear_mx_skinny<MF, NB, KS, PAT, OutT><<<dim3((unsigned)((N + 16 * NB - 1) / (16 * NB))), dim3(64 * KS), 0, st>>>(
-      spc, spm, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy);
+  const int ncg = (N + 16 * NB - 1) / (16 * NB);
+  const int nrt = (int)((M + 16 * MF - 1) / (16 * MF));
+  k_linear_mx_skinny<MF, NB, KS, PAT, OutT><<<dim3((unsigned)(ncg * nrt)), dim3(64 * KS), 0, st>>>(
+      spc, spm, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, ncg, nrt);
   return hipGetLastError();
 }
 
 // K split for the small-M kernel: about 8192 wavefronts in flight (8 per
 // SIMD) to keep the weight stream busy, at least 4 panels per wavefront, at
 // most `cap` wavefronts per workgroup.
-static int skinny_split(int N, int K, int NB, int cap) {
-  const int wgs = (N + 16 * NB - 1) / (16 * NB), nks = K / kBK;
+static int skinny_split(int wgs, int K, int cap) {
+  const int nks = K / kBK;
   int ks = 4;
   while (ks < cap && wgs * ks * 2 <= 8192 && nks >= 4 * ks * 2) ks *= 2;
   return ks;
@@ -1109,23 +1135,47 @@ static int skinny_split(int N, int K, int NB, int cap) {
 
 // (row fragments, column fragments, K splits) by M: every activation block
 // expansion feeds NB column fragments; the K split keeps enough wavefronts
-// streaming the weight.
+// streaming the weight.  Above 32 rows the workgroups tile M by 64.
 template <int PAT, typename OutT>
 static hipError_t go_skinny_m(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
                               const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
                               void* Y, int64_t ldy, hipStream_t st) {
   if (M <= 16) {
-    const int ks = skinny_split(N, K, 1, 16);
+    const int ks = skinny_split((N + 15) / 16, K, 16);
     if (ks == 16) return go_skinny<1, 1, 16, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
     if (ks == 8) return go_skinny<1, 1, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
     return go_skinny<1, 1, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
   }
   if (M <= 32) {
-    if (skinny_split(N, K, 2, 8) == 8)
+    if (skinny_split((N + 31) / 32, K, 8) == 8)
       return go_skinny<2, 2, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
     return go_skinny<2, 2, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
   }
-  return go_skinny<4, 4, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  // Of (row fragments, column fragments, K splits) = (4, 4, 4), (2, 4, 8)
+  // and (2, 2, 8), the one whose wavefront count is nearest to 2048 (in
+  // ratio; ties to the first): measured on the Llama decode shapes at
+  // M = 64-256, fewer wavefronts leave the weight stream short of loads in
+  // flight and more re-read the weight for too many row tiles.
+  const int64_t rt64 = (M + 63) / 64, rt32 = (M + 31) / 32;
+  const int64_t w444 = ((N + 63) / 64) * rt64 * 4, w248 = ((N + 63) / 64) * rt32 * 8,
+                w228 = ((N + 31) / 32) * rt32 * 8;
+  const auto dist = [](int64_t w) { return w >= 2048 ? (double)w / 2048.0 : 2048.0 / (double)w; };
+  if (dist(w444) <= dist(w248) && dist(w444) <= dist(w228))
+    return go_skinny<4, 4, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  if (dist(w248) <= dist(w228))
+    return go_skinny<2, 4, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  return go_skinny<2, 2, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+}
+
+// The small-M kernel serves M <= 64, and M <= 256 while the main kernel
+// would have fewer than 48 tiles of 128 x 256 (measured on the Llama decode
+// shapes: at 48 tiles the two are even, at 112 the main kernel is twice as
+// fast).
+static bool use_skinny(int64_t M, int N, int K) {
+  if (K % kBK != 0) return false;
+  if (M <= kSkinnyMaxM) return true;
+  const int64_t tiles = ((M + kBM - 1) / kBM) * (int64_t)((N + 255) / 256);
+  return M <= kSkinnyMaxRowTiled && tiles < 48;
 }
 
 template <int PAT>
@@ -1963,7 +2013,7 @@ hipError_t launch_linear_mx(int pat, int ydt, const uint8_t* spc, const uint8_t*
                             int N, int K, void* Y, int64_t ldy, hipStream_t st) {
   const bool sdw = (K % kBK) == 0;
   constexpr int NF = 8;
-  if (sdw && M <= kSkinnyMaxM) {
+  if (use_skinny(M, N, K)) {
     return pat == 24 ? go_skinny_dt<24>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st)
                      : go_skinny_dt<48>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
   }

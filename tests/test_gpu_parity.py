@@ -249,7 +249,8 @@ def test_llama_full_shape(S, G, name):
 
 # --------------------------------------------------------------------------- decode shapes
 
-@pytest.mark.parametrize("name,T", [("qkv", 1), ("qkv", 16), ("down", 64), ("gate_up", 33), ("down", 5)])
+@pytest.mark.parametrize("name,T", [("qkv", 1), ("qkv", 16), ("down", 64), ("gate_up", 33), ("down", 5), ("qkv", 48),
+                                    ("down", 100), ("qkv", 128), ("down", 256)])
 def test_llama_decode_shape(S, G, name, T):
     """Small-M (decode) Llama-3.1-8B shapes, as the decode benchmark runs them:
     preparation in full, GEMM on every row."""
@@ -267,9 +268,11 @@ def test_llama_decode_shape(S, G, name, T):
     assert torch.equal(y16, y.to(torch.bfloat16))
 
 
-@pytest.mark.parametrize("T,N,K,n,m", [(7, 40, 256, 4, 8), (64, 96, 1280, 2, 4), (17, 16, 128, 2, 4)])
+@pytest.mark.parametrize("T,N,K,n,m", [(7, 40, 256, 4, 8), (64, 96, 1280, 2, 4), (17, 16, 128, 2, 4),
+                                       (70, 40, 256, 2, 4), (200, 96, 1280, 4, 8), (129, 4104, 512, 2, 4)])
 def test_small_m_ragged(S, G, T, N, K, n, m):
-    """Small-M kernel: column tails (N % 16), K ranges shorter than four panels, 4:8."""
+    """Small-M kernel: column tails (N % 16), K ranges shorter than four panels,
+    4:8, and row tiles with a ragged last tile (M > 64 with few main-kernel tiles)."""
     x = synth.activations(T, K, seed=K)
     o = O.prepare(x, synth.gamma(K, seed=2), 1e-6, n, m, "mx")
     wo = O.quantize_weight(synth.weight(N, K, seed=N), "mx")
