@@ -59,6 +59,20 @@ Readings where the paper is silent (each also listed in the design notes):
       (none, dense); Dense+Dense = (dense, dense); Sparse+Sparse = (sparse,
       sparse), whose second mask is chosen on |R|; SharQ = (sparse, dense).
       NVFP4 uses one per-tensor scale S = amax(y)/2688 for both paths.
+  R11 HiF4 (App. "HiFloat4 (HiF4) Data Format", Algorithm "bf16-to-hif4",
+      eq. "hif4-value"): units of 64 positions along K; the algorithm runs
+      on the fp32 values it is given (y, R or W) with fp32 arithmetic:
+      SF = fl32(Vmax * bf16(1/7)); E6M2 = SF rounded to 2 mantissa bits
+      (nearest, ties to even), clamped to [2^-48, 1.5 * 2^15] (no zero;
+      the all-ones code is NaN); REC = bf16(1/1.M) * 2^-E (the 4-entry
+      reciprocal table); E1_8[j] = (V8[j] * REC >= 4); E1_16[k] =
+      (V16[k] * REC * 2^-E1_8[k/2] >= 2); scaled = fl32(v * REC) *
+      2^-(E1_8 + E1_16); S1P2 code = nearest multiple of 1/4 (ties to even),
+      saturating at 1.75, sign kept.  Element k (0-based) uses E1_8[k/8] and
+      E1_16[k/4].  Value = E6M2 * 2^(E1_8 + E1_16) * S1P2.  A backbone unit
+      spans 64 logical positions (dropped positions are zero).  No per-tensor
+      scale.  Metadata bytes per unit: E6M2 code, E1_8 bits, E1_16 bits
+      (low byte, high byte), bit j = group j.
 """
 
 from __future__ import annotations
@@ -363,6 +377,124 @@ def nv_quantize(vals: np.ndarray, S: np.float32, block: int, present: np.ndarray
 
 
 # ---------------------------------------------------------------------------
+# HiF4 (App. "HiFloat4 (HiF4) Data Format"; reading R11)
+# ---------------------------------------------------------------------------
+
+HIF4_UNIT = 64
+E6M2_BIAS = 48
+E6M2_NAN = 0xFF
+S1P2_MAX = 1.75
+
+
+def bf16_round_f32(v) -> np.ndarray:
+    """fp32 -> nearest bf16 value (ties to even), returned as fp32."""
+    u = np.asarray(v, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    return r.astype(np.uint32).view(np.float32)
+
+
+def e6m2_decode(code) -> np.ndarray:
+    """E6M2 code -> value 2^(E-48) * (1 + M/4) in fp64 (eq. "e6m2"); NaN for 0xFF."""
+    c = np.asarray(code, dtype=np.int64)
+    v = np.ldexp(1.0 + (c & 3) / 4.0, (c >> 2) - E6M2_BIAS)
+    return np.where(c == E6M2_NAN, np.nan, v)
+
+
+def e6m2_round(a) -> np.ndarray:
+    """Non-negative fp32 -> E6M2 code: 2 mantissa bits, nearest with ties to
+    even, clamped to the normal range [2^-48, 1.5 * 2^15] (R11)."""
+    a = np.asarray(a, dtype=np.float64)
+    E = np.frexp(np.where(a > 0, a, 1.0))[1].astype(np.int64) - 1          # floor(log2 a)
+    q = np.rint(np.ldexp(a, -E) * 4.0)                                     # 4 * mantissa in [4, 8]
+    E = np.where(q == 8, E + 1, E)
+    q = np.where(q == 8, 4, q).astype(np.int64)
+    code = ((E + E6M2_BIAS) << 2) | (q - 4)
+    code = np.where(E > 15, (63 << 2) | 2, code)
+    code = np.where((E == 15) & (q - 4 == 3), (63 << 2) | 2, code)        # 1.75 * 2^15 is the NaN code
+    code = np.where((E < -E6M2_BIAS) | (a <= 0), 0, code)
+    return code.astype(np.uint8)
+
+
+#: bf16(1/1.M) for M = 0..3, the reciprocal table of Algorithm "bf16-to-hif4"
+E6M2_REC_TABLE = bf16_round_f32(np.array([1.0, 1 / 1.25, 1 / 1.5, 1 / 1.75], dtype=np.float64).astype(np.float32))
+#: bf16(1/7), the constant of the level-1 scale
+ONE_SEVENTH_BF16 = bf16_round_f32(np.float32(1.0 / 7.0))
+
+
+def e6m2_reciprocal(code) -> np.ndarray:
+    """REC = table[M] * 2^-E in fp32 (exact scaling of the table entry)."""
+    c = np.asarray(code, dtype=np.int64)
+    return np.ldexp(E6M2_REC_TABLE[c & 3].astype(np.float64), -((c >> 2) - E6M2_BIAS)).astype(np.float32)
+
+
+def s1p2_encode(v) -> np.ndarray:
+    """Scaled fp32 -> S1P2 code: sign bit 3, magnitude m in bits 0-2 (value m/4);
+    nearest multiple of 1/4 with ties to even m, saturating at 1.75."""
+    v = np.asarray(v, dtype=np.float32)
+    m = np.minimum(np.rint(np.abs(v).astype(np.float64) * 4.0), 7).astype(np.uint8)
+    return ((np.signbit(v).astype(np.uint8) << 3) | m).astype(np.uint8)
+
+
+def s1p2_decode(codes) -> np.ndarray:
+    c = np.asarray(codes, dtype=np.uint8)
+    mag = (c & 7).astype(np.float64) / 4.0
+    return np.where((c >> 3) & 1, -mag, mag)
+
+
+def hif4_quantize(vals: np.ndarray, present: np.ndarray | None = None):
+    """HiF4 quantization of rows in units of 64 along K (Algorithm
+    "bf16-to-hif4", reading R11).  `present` marks the positions of the tensor
+    (the backbone's kept ones); the others count as zero and get code 0.
+    Returns (codes uint8 [T,K], meta uint8 [T,K/64*4], deq fp32 [T,K])."""
+    v = np.asarray(vals, dtype=np.float32)
+    T, K = v.shape
+    if present is None:
+        present = np.ones(v.shape, dtype=bool)
+    v = np.where(present, v, np.float32(0.0)).astype(np.float32)
+    U = K // HIF4_UNIT
+    a = np.abs(v).reshape(T, U, HIF4_UNIT)
+    v16 = a.reshape(T, U, 16, 4).max(axis=3)                 # stage 1: three-level tree of maxima
+    v8 = v16.reshape(T, U, 8, 2).max(axis=3)
+    vmax = v8.max(axis=2)
+    sf = (vmax * ONE_SEVENTH_BF16).astype(np.float32)          # stage 2: scaling metadata
+    e6 = e6m2_round(sf)
+    rec = e6m2_reciprocal(e6)
+    e1_8 = ((v8 * rec[..., None]).astype(np.float32) >= np.float32(4.0)).astype(np.int64)
+    e8_of16 = np.repeat(e1_8, 2, axis=2)
+    t16 = np.ldexp((v16 * rec[..., None]).astype(np.float32).astype(np.float64), -e8_of16)
+    e1_16 = (t16 >= 2.0).astype(np.int64)
+    # stage 3: scale and quantize every element
+    shift = np.repeat(e1_8, 8, axis=2) + np.repeat(e1_16, 4, axis=2)
+    scaled = (v.reshape(T, U, HIF4_UNIT) * rec[..., None]).astype(np.float32)
+    scaled = np.ldexp(scaled.astype(np.float64), -shift).astype(np.float32)
+    codes = s1p2_encode(scaled).reshape(T, K)
+    codes = np.where(present, codes, np.uint8(0)).astype(np.uint8)
+    meta = np.zeros((T, U, 4), dtype=np.uint8)
+    meta[..., 0] = e6
+    meta[..., 1] = (e1_8 << np.arange(8)).sum(axis=2).astype(np.uint8)
+    b16 = (e1_16 << np.arange(16)).sum(axis=2)
+    meta[..., 2] = (b16 & 0xFF).astype(np.uint8)
+    meta[..., 3] = (b16 >> 8).astype(np.uint8)
+    meta = meta.reshape(T, U * 4)
+    return codes, meta, hif4_decode(codes, meta).astype(np.float32)
+
+
+def hif4_decode(codes: np.ndarray, meta: np.ndarray) -> np.ndarray:
+    """eq. "hif4-value": V_k = E6M2 * 2^(E1_8[k/8] + E1_16[k/4]) * S1P2_k (fp64, exact)."""
+    c = np.asarray(codes, dtype=np.uint8)
+    T, K = c.shape
+    U = K // HIF4_UNIT
+    m = np.asarray(meta, dtype=np.uint8).reshape(T, U, 4).astype(np.int64)
+    base = e6m2_decode(m[..., 0])
+    e8 = (m[..., 1:2] >> np.arange(8)) & 1
+    b16 = m[..., 2] | (m[..., 3] << 8)
+    e16 = (b16[..., None] >> np.arange(16)) & 1
+    shift = np.repeat(e8, 8, axis=2) + np.repeat(e16, 4, axis=2)
+    return (np.repeat(base, HIF4_UNIT, axis=1).reshape(T, U, HIF4_UNIT) * np.ldexp(1.0, shift)
+            * s1p2_decode(c).reshape(T, U, HIF4_UNIT)).reshape(T, K)
+
+
+# ---------------------------------------------------------------------------
 # Packing into the library's buffer layout
 # ---------------------------------------------------------------------------
 
@@ -475,8 +607,9 @@ def path_widths(kind, K: int, n: int, m: int, fmt: str):
     """Row bytes (codes, meta, scale) of one path slot of kind 'sparse', 'dense' or None."""
     if kind is None:
         return 0, 0, 0
+    scale_sparse = K // 16 if fmt == "hif4" else K // 32
     if kind == "sparse":
-        return K * n // m // 2, K // 8, K // 32
+        return K * n // m // 2, K // 8, scale_sparse
     return K // 2, 0, K // 32 if fmt == "mx" else K // 16
 
 
@@ -512,7 +645,8 @@ def weight_to_device_layout(wq: dict) -> dict:
 
 
 def weight_from_device_layout(bufs: dict, N: int, K: int, fmt: str, tensor_scale=None) -> dict:
-    widths = {"codes": K // 2, "scale": K // 32, "scale_dn": K // 32 if fmt == "mx" else K // 16}
+    widths = {"codes": K // 2, "scale": K // 16 if fmt == "hif4" else K // 32,
+              "scale_dn": K // 32 if fmt == "mx" else K // 16}
     d = {"N": N, "K": K, "fmt": fmt, "tensor_scale": tensor_scale}
     for k in WEIGHT_BUFFERS:
         d[k] = from_panels(bufs[k], N, K, widths[k])
@@ -559,6 +693,11 @@ def prepare(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: in
         R = (y - d_sp).astype(np.float32)
         dn_c, _, dn_s, d_dn = nv_quantize(R, S, NV_BLOCK)
         out["tensor_scale"] = np.float32(S)
+    elif fmt == "hif4":
+        sp_c, sp_s, d_sp = hif4_quantize(y, keep)
+        R = (y - d_sp).astype(np.float32)
+        dn_c, dn_s, d_dn = hif4_quantize(R)
+        out["tensor_scale"] = None
     else:
         raise ValueError(fmt)
     if n > 0:
@@ -601,6 +740,8 @@ def quantize_path(v: np.ndarray, kind: str, n: int, m: int, fmt: str, S, pairs: 
             keep = nm_pair_mask(v, n, m) if pairs else nm_mask(v, n, m)
         if fmt == "mx":
             c, _, sc, deq = mx_quantize(v, keep)
+        elif fmt == "hif4":
+            c, sc, deq = hif4_quantize(v, keep)
         else:
             c, _, sc, deq = nv_quantize(v, S, MX_BLOCK, keep)
         if n > 0:
@@ -610,6 +751,8 @@ def quantize_path(v: np.ndarray, kind: str, n: int, m: int, fmt: str, S, pairs: 
         return {"codes": codes, "meta": meta, "scale": sc, "deq": deq, "keep": keep}
     if fmt == "mx":
         c, _, sc, deq = mx_quantize(v)
+    elif fmt == "hif4":
+        c, sc, deq = hif4_quantize(v)
     else:
         c, _, sc, deq = nv_quantize(v, S, NV_BLOCK)
     return {"codes": pack_nibbles(c), "meta": np.zeros((T, 0), np.uint8), "scale": sc, "deq": deq,
@@ -636,7 +779,7 @@ def prepare_mode(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, 
     S = None
     if fmt == "nv":
         S = pts_scale(np.abs(y).max() if y.size else 0.0) if tensor_scale is None else np.float32(tensor_scale)
-    elif fmt != "mx":
+    elif fmt not in ("mx", "hif4"):
         raise ValueError(fmt)
     empty = np.zeros((T, 0), np.uint8)
     out = {"rows": T, "K": K, "n": n, "m": m, "pairs": pairs, "fmt": fmt, "mode": mode, "y": y, "r": r,
@@ -679,7 +822,8 @@ def quantize_weight(w_bf16: np.ndarray, fmt: str = "mx") -> dict:
 
     MXFP4: E8M0 per 32 along K, used by both paths.  NVFP4: per-tensor scale
     S_w = amax(W)/2688, E4M3 per 32 (the sparse view), and a dense view that
-    repeats every scale for its two 16-element halves.
+    repeats every scale for its two 16-element halves.  HiF4: units of 64
+    along K with their three-level metadata, one view for both paths.
     """
     w = bf16_bits_to_f32(w_bf16)
     N, K = w.shape
@@ -687,6 +831,10 @@ def quantize_weight(w_bf16: np.ndarray, fmt: str = "mx") -> dict:
         c, _, s, deq = mx_quantize(w)
         return {"N": N, "K": K, "fmt": "mx", "codes": pack_nibbles(c), "scale": s,
                 "scale_dn": s, "tensor_scale": None, "deq": deq}
+    if fmt == "hif4":
+        c, meta, deq = hif4_quantize(w)
+        return {"N": N, "K": K, "fmt": "hif4", "codes": pack_nibbles(c), "scale": meta, "scale_dn": meta,
+                "tensor_scale": None, "deq": deq}
     S = pts_scale(np.abs(w).max() if w.size else 0.0)
     c, _, s, deq = nv_quantize(w, S, MX_BLOCK)
     return {"N": N, "K": K, "fmt": "nv", "codes": pack_nibbles(c), "scale": s,
@@ -709,6 +857,9 @@ def _block_scale_values(scale_codes: np.ndarray, fmt: str, block: int, K: int) -
 def _dequant_path(kind, codes, meta, scale, T: int, K: int, n: int, m: int, fmt: str, S: float) -> np.ndarray:
     if kind is None or (kind == "sparse" and n == 0):
         return np.zeros((T, K))
+    if fmt == "hif4":
+        dense = unpack_backbone(codes, meta, K, n, m)[0] if kind == "sparse" else unpack_nibbles(codes)
+        return hif4_decode(dense, scale)
     if kind == "sparse":
         dense, keep = unpack_backbone(codes, meta, K, n, m)
         vals = e2m1_decode(dense) * _block_scale_values(scale, fmt, MX_BLOCK, K) * S
@@ -726,7 +877,7 @@ def dequant_act(act: dict):
     K, n, m, fmt = act["K"], act["n"], act["m"], act["fmt"]
     T = act["rows"]
     k1, k2 = MODE_PATHS[act.get("mode", "sharq")]
-    S = 1.0 if fmt == "mx" else float(act["tensor_scale"])
+    S = 1.0 if fmt != "nv" else float(act["tensor_scale"])
     a1 = _dequant_path(k1, act["sp_codes"], act["sp_meta"], act["sp_scale"], T, K, n, m, fmt, S)
     a2 = _dequant_path(k2, act["dn_codes"], act.get("dn_meta"), act["dn_scale"], T, K, n, m, fmt, S)
     return a1, a2
@@ -741,6 +892,8 @@ def _views(act: dict):
 def dequant_weight(wq: dict, view: str = "sp") -> np.ndarray:
     """Shared weight payload -> fp64 [N,K] through the sparse or the dense scale view."""
     K, fmt = wq["K"], wq["fmt"]
+    if fmt == "hif4":
+        return hif4_decode(unpack_nibbles(wq["codes"]), wq["scale"])
     S = 1.0 if fmt == "mx" else float(wq["tensor_scale"])
     if view == "sp" or fmt == "mx":
         sv = _block_scale_values(wq["scale"], fmt, MX_BLOCK, K)

@@ -1,0 +1,233 @@
+"""Pins of the oracle's HiF4 codec (App. "HiFloat4 (HiF4) Data Format",
+Algorithm "bf16-to-hif4", eq. "hif4-value") against the values the paper
+prints, exhaustive searches, a scalar step-by-step rebuild of the algorithm
+with exact rational arithmetic, and invariants.  None of these needs a GPU."""
+
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import sharq_oracle as O
+from paper_2606_26587_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def facts():
+    with open(os.path.join(GOLDEN, "paper_format_facts.json")) as f:
+        return {k: v["value"] for k, v in json.load(f).items() if not k.startswith("_")}
+
+
+def f32(x) -> float:
+    """Round a rational (or float) to the nearest fp32 value, ties to even."""
+    return float(np.float32(float(Fraction(x)))) if not isinstance(x, Fraction) else _f32_frac(x)
+
+
+def _f32_frac(q: Fraction) -> float:
+    # nearest fp32 to an exact rational by checking the two fp32 neighbours of its double rounding
+    d = float(q)
+    c = np.float32(d)
+    best = None
+    for cand in (np.nextafter(c, np.float32(-np.inf)), c, np.nextafter(c, np.float32(np.inf))):
+        err = abs(Fraction(float(cand)) - q)
+        key = (err, int(np.array(cand, np.float32).view(np.uint32)) & 1)
+        if best is None or key < best[0]:
+            best = (key, float(cand))
+    return best[1]
+
+
+def bf16_of(q: Fraction) -> Fraction:
+    """Nearest bf16 value to an exact rational (ties to even), by search over 8-bit significands."""
+    if q == 0:
+        return Fraction(0)
+    e = math.floor(math.log2(q))
+    cands = [Fraction(m, 128) * Fraction(2) ** e for m in range(128, 257)]
+    return min(cands, key=lambda c: (abs(c - q), (c / Fraction(2) ** e * 128) % 2))
+
+
+# ----------------------------------------------------------------------------- formats
+
+def test_format_facts_are_the_papers():
+    F = facts()
+    vals = O.e6m2_decode(np.arange(255))
+    assert np.isnan(O.e6m2_decode(np.array([F["e6m2_nan_code"]])))[0]
+    assert vals.max() == 2.0 ** F["e6m2_max"][0] * F["e6m2_max"][1]
+    assert vals.min() == 2.0 ** F["e6m2_min"][0] * F["e6m2_min"][1]
+    assert [int(np.log2(vals.min())), int(np.floor(np.log2(vals.max())))] == F["e6m2_unbiased_exponent_range"]
+    s = O.s1p2_decode(np.arange(8, dtype=np.uint8))
+    assert s.max() == F["s1p2_max"] and s[s > 0].min() == F["s1p2_min_positive"]
+    peak = 2.0 ** 2 * F["s1p2_max"]
+    assert peak == F["hif4_group_peak"]
+    top = vals.max() * peak
+    assert top == 2.0 ** F["hif4_max_positive"][0] * F["hif4_max_positive"][1]
+    bottom = vals.min() * F["s1p2_min_positive"]
+    assert math.log2(bottom) == F["hif4_min_positive_log2"]
+    assert math.floor(math.log2(top)) - math.log2(bottom) + 1 == F["hif4_global_binades"]
+    assert round(math.log2(peak / F["s1p2_min_positive"]), 2) == F["hif4_local_binades"]
+    G = F["hif4_group"]
+    assert (G * 4 + 8 + 8 + 16) / G == F["hif4_bits_per_value"]
+    assert O.E6M2_BIAS == F["e6m2_bias"]
+
+
+def test_e6m2_round_is_exhaustive_nearest_even():
+    vals = O.e6m2_decode(np.arange(255)).astype(np.float64)   # every finite code, ascending
+    mids = (vals[1:] + vals[:-1]) / 2
+    rng = np.random.default_rng(3)
+    a = np.concatenate([vals, mids, vals * (1 + 2.0 ** -20), mids * (1 - 2.0 ** -20),
+                        2.0 ** rng.uniform(-47, 15.5, 3000)]).astype(np.float32)
+    got = O.e6m2_round(a)
+    for x, c in zip(a.astype(np.float64).tolist(), got.tolist()):
+        if x < vals[0]:
+            assert c == 0   # below the smallest normal: clamped (no zero, no subnormals)
+            continue
+        d = np.abs(vals - x)
+        ties = np.flatnonzero(d == d.min())
+        want = ties[0] if len(ties) == 1 else [t for t in ties if t % 2 == 0][0]
+        assert c == want, (x, c, want)
+    assert O.e6m2_round(np.float32(1e30)) == 254 and O.e6m2_round(np.float32(0.0)) == 0
+
+
+def test_reciprocal_table_and_one_seventh_are_bf16_roundings():
+    for M in range(4):
+        assert Fraction(float(O.E6M2_REC_TABLE[M])) == bf16_of(1 / (1 + Fraction(M, 4)))
+    assert Fraction(float(O.ONE_SEVENTH_BF16)) == bf16_of(Fraction(1, 7))
+    codes = np.arange(255)
+    prod = O.e6m2_reciprocal(codes).astype(np.float64) * O.e6m2_decode(codes)
+    assert np.all(np.abs(prod - 1.0) <= 2.0 ** -8)
+
+
+def test_s1p2_encode_is_exhaustive_nearest_even():
+    grid = [Fraction(m, 4) for m in range(8)]
+    xs = [Fraction(k, 64) for k in range(0, 140)] + [Fraction(3), Fraction(100)]
+    for x in xs:
+        for sign in (1, -1):
+            v = np.float32(sign * float(x))
+            c = int(O.s1p2_encode(v))
+            best = min(range(8), key=lambda m: (abs(grid[m] - x), m % 2))
+            assert c & 7 == best and (c >> 3) == (sign < 0), (x, sign, c)
+
+
+# ----------------------------------------------------------------------------- the algorithm
+
+def scalar_unit(v):
+    """Algorithm 'bf16-to-hif4' on one unit of 64 fp32 values, one element at a
+    time with exact rationals and explicit fp32 rounding (reading R11)."""
+    V = [Fraction(float(x)) for x in v]
+    V16 = [max(abs(V[4 * i + j]) for j in range(4)) for i in range(16)]
+    V8 = [max(V16[2 * i], V16[2 * i + 1]) for i in range(8)]
+    vmax = max(V8)
+    sf = _f32_frac(vmax * bf16_of(Fraction(1, 7)))
+    # E6M2 by search over all finite codes (nearest, ties to the even code, clamped)
+    vals = [Fraction(float(O.e6m2_decode(np.array([c]))[0])) for c in range(255)]
+    if sf <= vals[0]:
+        e6 = 0
+    else:
+        e6 = min(range(255), key=lambda c: (abs(vals[c] - Fraction(sf)), c % 2))
+    E, M = (e6 >> 2) - 48, e6 & 3
+    rec = bf16_of(1 / (1 + Fraction(M, 4))) * Fraction(2) ** (-E)
+    e8 = [1 if Fraction(_f32_frac(V8[i] * rec)) >= 4 else 0 for i in range(8)]
+    e16 = [1 if Fraction(_f32_frac(V16[k] * rec)) / 2 ** e8[k // 2] >= 2 else 0 for k in range(16)]
+    codes, out = [], []
+    for k in range(64):
+        sc = Fraction(_f32_frac(V[k] * rec)) / 2 ** (e8[k // 8] + e16[k // 4])
+        mag = min(range(8), key=lambda m: (abs(Fraction(m, 4) - abs(sc)), m % 2))
+        neg = V[k] < 0 or (V[k] == 0 and math.copysign(1.0, float(v[k])) < 0)
+        codes.append((8 if neg else 0) | mag)
+        out.append(float(vals[e6] * 2 ** (e8[k // 8] + e16[k // 4]) * Fraction(mag, 4) * (-1 if neg else 1)))
+    meta = [e6, sum(b << i for i, b in enumerate(e8)), sum(b << i for i, b in enumerate(e16[:8])),
+            sum(b << i for i, b in enumerate(e16[8:]))]
+    return codes, meta, out
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_quantizer_matches_scalar_rebuild(seed):
+    rng = np.random.default_rng(seed)
+    v = (rng.standard_normal((3, 128)) * np.exp(rng.uniform(-3, 3, (3, 128)))).astype(np.float32)
+    v[0, 5] = 40.0           # an outlier: level-2 and level-3 bits separate the groups
+    v[1, :64] *= 1e-12       # tiny unit
+    v[2, 64:] = 0.0          # all-zero unit
+    v[2, 3] = -0.0
+    codes, meta, deq = O.hif4_quantize(v)
+    for t in range(3):
+        for u in range(2):
+            c, m, d = scalar_unit(v[t, 64 * u: 64 * u + 64])
+            assert codes[t, 64 * u: 64 * u + 64].tolist() == c, (t, u)
+            assert meta[t, 4 * u: 4 * u + 4].tolist() == m, (t, u)
+            assert deq[t, 64 * u: 64 * u + 64].astype(np.float64).tolist() == d
+
+
+def test_constant_unit_closed_form():
+    """Equal magnitudes c: E6M2 = e6m2(c * bf16(1/7)), every micro-exponent
+    bit set, magnitude code m = min(7, rint(fl32(c * REC))) and value E6M2 * m."""
+    for c in (1.0, 3.0, 1e-5, 123.0, 7.0):
+        v = np.full((1, 64), c, np.float32)
+        v[0, ::3] *= -1
+        codes, meta, deq = O.hif4_quantize(v)
+        e6 = int(O.e6m2_round(np.float32(np.float32(c) * O.ONE_SEVENTH_BF16)))
+        assert meta[0].tolist() == [e6, 255, 255, 255]
+        E, M = (e6 >> 2) - 48, e6 & 3
+        rec = bf16_of(1 / (1 + Fraction(M, 4))) * Fraction(2) ** (-E)
+        m = min(7, round(Fraction(_f32_frac(Fraction(c) * rec))))
+        assert np.all(codes & 7 == m)
+        assert np.all(np.signbit(deq[0, ::3]))
+        want = float(Fraction(float(O.e6m2_decode(np.array([e6]))[0])) * m)
+        assert np.array_equal(np.abs(deq[0]).astype(np.float64), np.full(64, want))
+
+
+def test_error_bound_and_peak_normalization():
+    x = synth.activations(16, 512, seed=5)
+    v = O.bf16_bits_to_f32(x)
+    codes, meta, deq = O.hif4_quantize(v)
+    m = meta.reshape(16, 8, 4).astype(np.int64)
+    base = np.repeat(O.e6m2_decode(m[..., 0]), 64, axis=1)
+    e8 = np.repeat((m[..., 1:2] >> np.arange(8)) & 1, 8, axis=2).reshape(16, 512)
+    b16 = (m[..., 2] | (m[..., 3] << 8))[..., None]
+    e16 = np.repeat((b16 >> np.arange(16)) & 1, 4, axis=2).reshape(16, 512)
+    step = base * np.ldexp(0.25, e8 + e16)
+    err = np.abs(v.astype(np.float64) - deq)
+    unsat = (codes & 7) < 7
+    # one fp32 rounding of v * REC can move a tie: allow a hair above half a step
+    assert np.all(err[unsat] <= step[unsat] * (0.5 + 2.0 ** -20))
+    # the peak of every unit lies in the top level-2 and level-3 groups' range
+    peak = np.abs(v).reshape(16, 8, 64).argmax(axis=2)
+    for t in range(16):
+        for u in range(8):
+            k = 64 * u + peak[t, u]
+            assert e8[t, k] == 1 and e16[t, k] == 1
+
+
+def test_hif4_backbone_residual_and_gemm():
+    c = synth.tiny_case()
+    a = O.prepare(c["x"], c["gamma"], c["eps"], 2, 4, "hif4")
+    assert a["sp_scale"].shape == (8, 128 // 16) and a["dn_scale"].shape == (8, 128 // 16)
+    assert np.all(a["d_sp"][~a["keep"]] == 0)
+    y = a["y"].astype(np.float64)
+    assert np.array_equal(y - (a["d_sp"].astype(np.float64) + a["d_dn"]), a["R"].astype(np.float64) - a["d_dn"])
+    # the backbone unit is 64 logical positions; quantizing the masked row gives the same values
+    _, _, direct = O.hif4_quantize(np.where(a["keep"], a["y"], np.float32(0)))
+    assert np.array_equal(direct, a["d_sp"])
+    wq = O.quantize_weight(c["w"], "hif4")
+    Y = O.linear(a, wq)
+    a1, a2 = O.dequant_act(a)
+    W = O.dequant_weight(wq)
+    for t in range(0, 8, 3):
+        for nn in range(0, 64, 11):
+            exact = sum((Fraction(float(a1[t, k])) + Fraction(float(a2[t, k]))) * Fraction(float(W[nn, k]))
+                        for k in range(128))
+            assert abs(float(exact) - Y[t, nn]) <= 1e-12 * max(1.0, abs(float(exact)))
+
+
+def test_hif4_device_layout_roundtrip():
+    x = synth.activations(9, 384, seed=2)
+    o = O.prepare(x, None, 1e-6, 2, 4, "hif4")
+    back = O.act_from_device_layout(O.act_to_device_layout(o), 9, 384, 2, 4, "hif4")
+    for k in O.ACT_BUFFERS:
+        assert np.array_equal(back[k], o[k]), k
+    wq = O.quantize_weight(synth.weight(40, 384, seed=2), "hif4")
+    wb = O.weight_from_device_layout(O.weight_to_device_layout(wq), 40, 384, "hif4")
+    for k in O.WEIGHT_BUFFERS:
+        assert np.array_equal(wb[k], wq[k]), k
