@@ -29,6 +29,15 @@
  *   MXFP4: E2M1 + one E8M0 scale per 32 consecutive K values; E8M0 code c
  *          means 2^(c-127).  NVFP4: E2M1 + one E4M3 scale (bias 7, max 448)
  *          per block + one fp32 per-tensor scale.
+ *   HiF4 (App. "HiFloat4 (HiF4) Data Format"): units of 64 K positions; each
+ *          element an S1P2 code (bit 3 sign, bits 0-2 magnitude m, value
+ *          m/4); per unit 4 metadata bytes [E6M2, E1_8, E1_16 low, E1_16
+ *          high]: an E6M2 scale (6 exponent bits, bias 48, 2 mantissa bits,
+ *          normal values only) and one-bit micro-exponents per 8 and per 4
+ *          elements (bit j = group j); value = E6M2 * 2^(E1_8 + E1_16) *
+ *          S1P2 (eq. "hif4-value").  The 4 bytes of a unit occupy the 2-byte
+ *          scale slots of its two 32-position blocks.  K must be a multiple of
+ *          64; built with the 2:4 pattern, SHARQ_MODE_SHARQ, no grouped form.
  *   Two 4-bit codes per byte, the element with the lower K index in the low
  *   nibble.
  *
@@ -67,7 +76,7 @@ typedef enum {
   SHARQ_EHIP = 4
 } sharq_status;
 
-typedef enum { SHARQ_MXFP4 = 0, SHARQ_NVFP4 = 1 } sharq_format;
+typedef enum { SHARQ_MXFP4 = 0, SHARQ_NVFP4 = 1, SHARQ_HIF4 = 2 } sharq_format;
 
 typedef enum { SHARQ_BF16 = 0, SHARQ_F16 = 1, SHARQ_F32 = 2 } sharq_dtype;
 
@@ -128,9 +137,11 @@ typedef enum {
  *                             aligned.
  *   sp_scale [rows][K/32]     backbone block scale per 32 logical K positions
  *                             (Fig. 2 "sparse group-32 scales"): E8M0 (MXFP4)
- *                             or E4M3 (NVFP4).
+ *                             or E4M3 (NVFP4); HiF4: [rows][K/16], the unit
+ *                             metadata of each 64 logical positions.
  *   dn_codes [rows][K/2]      residual E2M1 codes, all positions; 16-byte aligned.
- *   dn_scale [rows][K/32] (MXFP4, E8M0) | [rows][K/16] (NVFP4, E4M3).
+ *   dn_scale [rows][K/32] (MXFP4, E8M0) | [rows][K/16] (NVFP4, E4M3; HiF4,
+ *                             unit metadata).
  *   tensor_scale              NVFP4: one fp32 per-tensor scale S (device); the
  *                             element value is code * block_scale * S.
  *                             MXFP4: unused (may be NULL).
@@ -173,6 +184,8 @@ typedef struct {
  *   scale_dn [experts][N][K/16]  NVFP4 dense view: each per-32 scale repeated
  *                                for its two 16-element halves.  MXFP4: equal
  *                                to `scale`.
+ *   HiF4: scale [experts][N][K/16] holds the unit metadata, one view for
+ *   both paths (scale_dn unused, may equal `scale`).
  *   tensor_scale [experts]       NVFP4 per-tensor scale(s) S_w (device);
  *                                MXFP4: unused.
  */
@@ -202,8 +215,9 @@ SHARQ_API size_t sharq_act_buffer_bytes_mode(int64_t rows, int64_t K, sharq_form
  * preparation").  MXFP4: per row, per 32 K values, E8M0 = floor(log2 amax) - 2
  * (OCP rule, clamped at -127), codes = E2M1(w / 2^e), ties to even, saturating.
  * NVFP4: S_w = amax(W)/2688 computed on the device, E4M3 per 32, dense view
- * duplicated per 16.  `out` fields N, K, fmt and the buffers must be set by
- * the caller; experts must be 1.
+ * duplicated per 16.  HiF4: units of 64 along K, the conversion of the HiF4
+ * appendix (its algorithm "bf16-to-hif4") on the fp32 values.  `out` fields
+ * N, K, fmt and the buffers must be set by the caller; experts must be 1.
  */
 SHARQ_API sharq_status sharq_quantize_weight(const void *W, sharq_dtype wdt, int64_t N, int64_t K, int64_t ldw,
                                    sharq_weight *out, void *stream);

@@ -29,6 +29,13 @@ hipError_t launch_linear_slots(int mode, int pat, int ydt, bool nv, const uint8_
                                const uint8_t* s1, const uint8_t* c2, const uint8_t* m2, const uint8_t* s2,
                                const float* tsx, int64_t M, const uint8_t* wc, const uint8_t* ws, const float* tsw,
                                int N, int K, void* Y, int64_t ldy, hipStream_t st);
+hipError_t launch_prep_hif4(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps,
+                            uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, hipStream_t st);
+hipError_t launch_wquant_hif4(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
+                              hipStream_t st);
+hipError_t launch_linear_hif4(int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
+                              const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
+                              void* Y, int64_t ldy, hipStream_t st);
 hipError_t launch_linear_mx_grouped(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                                     const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx, int64_t act_rows,
                                     const int32_t* offs, int E, int64_t total, const uint8_t* wc, const uint8_t* ws,
@@ -58,6 +65,8 @@ int gemm_pattern(int pid) { return pid == 49 ? 48 : pid; }
 
 sharq_status hip_status(hipError_t e) { return e == hipSuccess ? SHARQ_OK : SHARQ_EHIP; }
 
+bool fmt_ok(int f) { return f == SHARQ_MXFP4 || f == SHARQ_NVFP4 || f == SHARQ_HIF4; }
+
 // Path kinds of the two slots of a mode: 0 absent, 1 sparse, 2 dense.
 constexpr int kNone = 0, kSparse = 1, kDense = 2;
 bool mode_ok(int mode) { return mode >= SHARQ_MODE_SHARQ && mode <= SHARQ_MODE_SPARSE_SPARSE; }
@@ -70,7 +79,8 @@ bool has_sparse(int mode) { return kind1(mode) == kSparse || kind2(mode) == kSpa
 // Row bytes per 32 K positions of a slot's codes / metadata / scales.
 size_t slot_bytes(int kind, sharq_pattern nm, sharq_format fmt, int what, size_t k) {
   if (kind == kNone) return 0;
-  if (kind == kSparse) return what == 0 ? k * (size_t)nm.n / (size_t)nm.m / 2 : what == 1 ? k / 8 : k / 32;
+  if (kind == kSparse)
+    return what == 0 ? k * (size_t)nm.n / (size_t)nm.m / 2 : what == 1 ? k / 8 : (fmt == SHARQ_HIF4 ? k / 16 : k / 32);
   return what == 0 ? k / 2 : what == 1 ? 0 : (fmt == SHARQ_MXFP4 ? k / 32 : k / 16);
 }
 
@@ -82,7 +92,11 @@ sharq_status check_act(const sharq_act* a) {
   const int pid = pattern_id(a->nm);   // 0: valid, not built
   if (pid < 0 || a->K % a->nm.m != 0) return SHARQ_EINVAL;
   if (pid == 0 && has_sparse(mode)) return SHARQ_EUNSUPPORTED;
-  if (a->fmt != SHARQ_MXFP4 && a->fmt != SHARQ_NVFP4) return SHARQ_EINVAL;
+  if (!fmt_ok(a->fmt)) return SHARQ_EINVAL;
+  if (a->fmt == SHARQ_HIF4) {   // built: 2:4 backbone, the method's path combination
+    if (a->K % 64 != 0) return SHARQ_EINVAL;
+    if (pid != 24 || mode != SHARQ_MODE_SHARQ) return SHARQ_EUNSUPPORTED;
+  }
   if (a->rows == 0) return SHARQ_OK;   // an empty activation is never dereferenced
   const int k1 = kind1(mode), k2 = kind2(mode);
   if (k1 != kNone && (!a->sp_codes || !a->sp_scale || (k1 == kSparse && !a->sp_meta))) return SHARQ_EINVAL;
@@ -101,7 +115,8 @@ sharq_status check_weight(const sharq_weight* w) {
   if (w->N < 0 || w->N > INT_MAX || w->K <= 0 || w->K % 32 != 0 || w->K > kMaxK || w->experts < 1 ||
       w->experts > kMaxExperts)
     return SHARQ_EINVAL;
-  if (w->fmt != SHARQ_MXFP4 && w->fmt != SHARQ_NVFP4) return SHARQ_EINVAL;
+  if (!fmt_ok(w->fmt)) return SHARQ_EINVAL;
+  if (w->fmt == SHARQ_HIF4 && w->K % 64 != 0) return SHARQ_EINVAL;
   if (!w->codes || !w->scale) return SHARQ_EINVAL;
   if (w->fmt == SHARQ_NVFP4 && (!w->scale_dn || !w->tensor_scale)) return SHARQ_EINVAL;
   if (!aligned(w->codes, 16) || !aligned(w->scale, 4) || !aligned(w->tensor_scale, 4)) return SHARQ_EALIGN;
@@ -129,17 +144,8 @@ const char* sharq_status_str(sharq_status s) {
 }
 
 size_t sharq_act_buffer_bytes(int64_t rows, int64_t K, sharq_format fmt, sharq_pattern nm, int32_t which) {
-  if (rows < 0 || K <= 0 || K % 32 != 0 || pattern_id(nm) < 0 || K % nm.m != 0) return 0;
-  if (fmt != SHARQ_MXFP4 && fmt != SHARQ_NVFP4) return 0;
-  const size_t r = (size_t)rows, k = (size_t)K;
-  switch (which) {
-    case 0: return r * (k * (size_t)nm.n / (size_t)nm.m / 2);
-    case 1: return r * (k / 8);
-    case 2: return r * (k / 32);
-    case 3: return r * (k / 2);
-    case 4: return r * (fmt == SHARQ_MXFP4 ? k / 32 : k / 16);
-    default: return 0;
-  }
+  if (which < 0 || which > 4) return 0;
+  return sharq_act_buffer_bytes_mode(rows, K, fmt, nm, SHARQ_MODE_SHARQ, which);
 }
 
 size_t sharq_act_buffer_bytes_mode(int64_t rows, int64_t K, sharq_format fmt, sharq_pattern nm, sharq_mode mode,
@@ -147,7 +153,7 @@ size_t sharq_act_buffer_bytes_mode(int64_t rows, int64_t K, sharq_format fmt, sh
   if (rows < 0 || K <= 0 || K % 32 != 0 || !mode_ok((int)mode)) return 0;
   const int pid = pattern_id(nm);
   if (pid < 0 || K % nm.m != 0 || (pid == 0 && has_sparse((int)mode))) return 0;
-  if (fmt != SHARQ_MXFP4 && fmt != SHARQ_NVFP4) return 0;
+  if (!fmt_ok(fmt) || (fmt == SHARQ_HIF4 && K % 64 != 0)) return 0;
   const size_t r = (size_t)rows, k = (size_t)K;
   const int k1 = kind1((int)mode), k2 = kind2((int)mode);
   switch (which) {
@@ -163,11 +169,11 @@ size_t sharq_act_buffer_bytes_mode(int64_t rows, int64_t K, sharq_format fmt, sh
 
 size_t sharq_weight_buffer_bytes(int64_t N, int64_t K, sharq_format fmt, int32_t which) {
   if (N < 0 || K <= 0 || K % 32 != 0) return 0;
-  if (fmt != SHARQ_MXFP4 && fmt != SHARQ_NVFP4) return 0;
+  if (!fmt_ok(fmt) || (fmt == SHARQ_HIF4 && K % 64 != 0)) return 0;
   const size_t n = (size_t)N, k = (size_t)K;
   switch (which) {
     case 0: return n * (k / 2);
-    case 1: return n * (k / 32);
+    case 1: return n * (fmt == SHARQ_HIF4 ? k / 16 : k / 32);
     case 2: return n * (fmt == SHARQ_MXFP4 ? k / 32 : k / 16);
     default: return 0;
   }
@@ -179,7 +185,8 @@ sharq_status sharq_quantize_weight(const void* W, sharq_dtype wdt, int64_t N, in
   if (N < 0 || N > INT_MAX || K <= 0 || K % 32 != 0 || K > kMaxK || ldw < K) return SHARQ_EINVAL;
   if (out->N != N || out->K != K || out->experts != 1) return SHARQ_EINVAL;
   if (wdt != SHARQ_BF16 && wdt != SHARQ_F32) return SHARQ_EUNSUPPORTED;
-  if (out->fmt != SHARQ_MXFP4 && out->fmt != SHARQ_NVFP4) return SHARQ_EINVAL;
+  if (!fmt_ok(out->fmt)) return SHARQ_EINVAL;
+  if (out->fmt == SHARQ_HIF4 && K % 64 != 0) return SHARQ_EINVAL;
   const bool nv = out->fmt == SHARQ_NVFP4;
   if (!out->codes || !out->scale) return SHARQ_EINVAL;
   if (nv && (!out->scale_dn || !out->tensor_scale)) return SHARQ_EINVAL;
@@ -188,6 +195,8 @@ sharq_status sharq_quantize_weight(const void* W, sharq_dtype wdt, int64_t N, in
     return SHARQ_EALIGN;
   if (N == 0) return SHARQ_OK;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (out->fmt == SHARQ_HIF4)
+    return hip_status(sharq::launch_wquant_hif4(W, (int)wdt, (int)N, (int)K, ldw, out->codes, out->scale, st));
   if (nv)
     return hip_status(sharq::launch_wquant_nv(W, (int)wdt, (int)N, (int)K, ldw, out->codes, out->scale,
                                               out->scale_dn, out->tensor_scale, st));
@@ -224,7 +233,13 @@ sharq_status prepare_impl(const void* X, const void* res, void* h_out, sharq_dty
   if (res && (!aligned(res, 16) || !aligned(h_out, 16) || (ldr * 2) % 16 != 0 || (ldh * 2) % 16 != 0))
     return SHARQ_EALIGN;
   if (res && out->mode != SHARQ_MODE_SHARQ) return SHARQ_EUNSUPPORTED;
+  if (res && fmt == SHARQ_HIF4) return SHARQ_EUNSUPPORTED;
   if (M == 0) return SHARQ_OK;
+  if (fmt == SHARQ_HIF4)
+    return hip_status(sharq::launch_prep_hif4(static_cast<const uint16_t*>(X), (int)M, (int)K, ldx,
+                                              static_cast<const uint16_t*>(gamma), eps, out->sp_codes, out->sp_meta,
+                                              out->sp_scale, out->dn_codes, out->dn_scale,
+                                              reinterpret_cast<hipStream_t>(stream)));
   const int mode = (int)out->mode;
   if (mode != SHARQ_MODE_SHARQ) {
     if (res) return SHARQ_EUNSUPPORTED;
@@ -274,6 +289,10 @@ sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sh
   if (!aligned(Y, ysize(ydt))) return SHARQ_EALIGN;
   if (a->rows == 0 || w->N == 0) return SHARQ_OK;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (a->fmt == SHARQ_HIF4)
+    return hip_status(sharq::launch_linear_hif4((int)ydt, a->sp_codes, a->sp_meta, a->sp_scale, a->dn_codes,
+                                                a->dn_scale, a->rows, w->codes, w->scale, (int)w->N, (int)w->K, Y,
+                                                ldy, st));
   if (a->mode != SHARQ_MODE_SHARQ) {
     const int pid = pattern_id(a->nm);
     return hip_status(sharq::launch_linear_slots((int)a->mode, pid > 0 ? gemm_pattern(pid) : 24, (int)ydt,
@@ -301,7 +320,7 @@ sharq_status sharq_linear_grouped(const sharq_act* a, const int32_t* row_index, 
   s = check_weight(w);
   if (s != SHARQ_OK) return s;
   if (a->fmt != w->fmt || a->K != w->K) return SHARQ_EINVAL;
-  if (a->fmt == SHARQ_NVFP4 || a->mode != SHARQ_MODE_SHARQ) return SHARQ_EUNSUPPORTED;
+  if (a->fmt != SHARQ_MXFP4 || a->mode != SHARQ_MODE_SHARQ) return SHARQ_EUNSUPPORTED;
   if (total < 0 || total > INT_MAX) return SHARQ_EINVAL;
   if (!row_index && total > a->rows) return SHARQ_EINVAL;
   if (!ydt_ok(ydt)) return SHARQ_EUNSUPPORTED;

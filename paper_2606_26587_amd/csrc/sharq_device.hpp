@@ -166,4 +166,59 @@ __device__ __forceinline__ uint32_t enc8(const float* v, const Q& qz) {
   return t;
 }
 
+// ---------------------------------------------------------------------------
+// HiF4 (a three-level scaled 4-bit format; App. "HiFloat4 (HiF4) Data
+// Format"): units of 64 values along K; an E6M2 level-1 scale (6 exponent
+// bits, bias 48, 2 mantissa bits, normal values only, all-ones = NaN), one
+// micro-exponent bit per 8 values (E1_8) and per 4 values (E1_16), S1P2
+// elements (sign, magnitude m in {0..7}, value m/4).  V = E6M2 *
+// 2^(E1_8 + E1_16) * S1P2 (eq. "hif4-value").  The conversion follows the
+// paper's algorithm on fp32 inputs: SF = fl(Vmax * bf16(1/7)), E6M2 = SF to
+// 2 mantissa bits (nearest even, clamped to [2^-48, 1.5 * 2^15]),
+// REC = bf16(1/1.M) * 2^-E, E1_8 = (V8 * REC >= 4), E1_16 = (V16 * REC >=
+// 2^(1 + E1_8)), scaled = fl(v * REC) * 2^-(E1_8 + E1_16), S1P2 = nearest
+// quarter, ties to even, saturating at 1.75.
+// ---------------------------------------------------------------------------
+
+constexpr float kOneSeventhBf16 = 0.142578125f;   // bf16(1/7)
+
+__device__ __forceinline__ uint32_t e6m2_code(float sf) {
+  if (!(sf >= 0x1p-48f)) return 0u;   // below the smallest normal (zero included)
+  const uint32_t b = __float_as_uint(sf);
+  int E = (int)(b >> 23) - 127;
+  const uint32_t mant = b & 0x7FFFFFu;
+  uint32_t q = mant >> 21;
+  const uint32_t rest = mant & 0x1FFFFFu;
+  if (rest > 0x100000u || (rest == 0x100000u && (q & 1u))) ++q;
+  if (q == 4u) {
+    q = 0u;
+    ++E;
+  }
+  if (E > 15 || (E == 15 && q == 3u)) return 0xFEu;   // largest finite: 1.5 * 2^15
+  return ((uint32_t)(E + 48) << 2) | q;
+}
+
+__device__ __forceinline__ float e6m2_value(uint32_t code) {
+  return exp2_int((int)(code >> 2) - 48) * (1.0f + 0.25f * (float)(code & 3u));
+}
+
+// bf16(1/1.M) * 2^-E: the reciprocal table of the conversion algorithm
+__device__ __forceinline__ float e6m2_rec(uint32_t code) {
+  const uint32_t M = code & 3u;
+  const float t = M == 0 ? 1.0f : M == 1 ? 0.80078125f : M == 2 ? 0.66796875f : 0.5703125f;
+  return t * exp2_int(48 - (int)(code >> 2));
+}
+
+// scaled fp32 value -> S1P2 code (bit 3 sign, bits 0-2 magnitude)
+__device__ __forceinline__ uint32_t s1p2_code(float s) {
+  const float m = fminf(__builtin_rintf(fabsf(s) * 4.0f), 7.0f);
+  return ((__float_as_uint(s) >> 28) & 8u) | (uint32_t)m;
+}
+
+// S1P2 code times a (power-of-two multiple of the) level-1 scale
+__device__ __forceinline__ float s1p2_value(uint32_t c, float scale) {
+  const float v = (float)(c & 7u) * 0.25f * scale;
+  return (c & 8u) ? -v : v;
+}
+
 }  // namespace sharq

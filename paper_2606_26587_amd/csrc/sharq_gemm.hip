@@ -1967,6 +1967,165 @@ __global__ __launch_bounds__(256) void k_linear_slots_nv(SlotBuf p1, SlotBuf p2,
 }
 
 // ---------------------------------------------------------------------------
+// HiF4 two-path GEMM (2:4 backbone + dense residual).  No matrix instruction
+// takes HiF4, but every HiF4 value E6M2 * 2^(E1_8 + E1_16) * S1P2 has at most
+// 6 significant bits and an exponent in [-50, 17], so both operands are
+// dequantized exactly to bf16 and multiplied on v_mfma_f32_32x32x16_bf16, as
+// in the NVFP4 kernel (one K step = one 32-position block, the weight tile
+// dequantized once per workgroup into LDS).  A unit's 4 metadata bytes
+// [E6M2, E1_8, E1_16 low, E1_16 high] sit at its even block's 2-byte slots.
+// ---------------------------------------------------------------------------
+
+// The unit metadata word of block j of panel row (pr, r).
+__device__ __forceinline__ uint32_t hif4_word_at(const uint8_t* sc, int64_t pr, int64_t r, int wp, int j) {
+  return *reinterpret_cast<const uint32_t*>(sc + (pr * 4 + r * (wp / 32) + (j & ~1)) * 2);
+}
+
+// Eight codes (dword q of block half hb of a unit) -> eight exact bf16 values.
+__device__ __forceinline__ uint4 hif4_dequant8_bf16(uint32_t codes, uint32_t word, int hb, int q) {
+  const float base = e6m2_value(word & 0xFFu);
+  const int l2 = 4 * hb + q, l3 = 8 * hb + 2 * q;
+  const int e8 = (int)((word >> (8 + l2)) & 1u);
+  const float sc0 = base * exp2_int(e8 + (int)((word >> (16 + l3)) & 1u));
+  const float sc1 = base * exp2_int(e8 + (int)((word >> (17 + l3)) & 1u));
+  uint32_t o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float sc = i < 2 ? sc0 : sc1;
+    const float a = s1p2_value((codes >> (8 * i)) & 0xFu, sc), b = s1p2_value((codes >> (8 * i + 4)) & 0xFu, sc);
+    o[i] = __builtin_amdgcn_perm(__float_as_uint(b), __float_as_uint(a), 0x07060302u);
+  }
+  return make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+struct HfA {           // one lane's activation data for one block
+  uint4 dn;            // residual codes
+  uint2 spc;           // compressed backbone codes
+  uint32_t spm;        // backbone metadata (2:4)
+  uint32_t sw, dw;     // backbone and residual unit words
+};
+
+struct HfW {           // one thread's weight row for one block
+  uint4 codes;
+  uint32_t word;
+};
+
+__device__ __forceinline__ void load_hf_a(HfA& s, const ARow& a, int ks, int K) {
+  const int p = ks >> 2, j = ks & 3, wp = min(128, K - 128 * p);
+  const int64_t pr = (int64_t)p * a.R;
+  s.dn = *reinterpret_cast<const uint4*>(a.dn + pr * 64 + a.r * (wp / 2) + 16 * j);
+  s.spc = *reinterpret_cast<const uint2*>(a.spc + pr * 32 + a.r * (wp / 4) + 8 * j);
+  s.spm = *reinterpret_cast<const uint32_t*>(a.spm + pr * 16 + a.r * (wp / 8) + 4 * j);
+  s.sw = hif4_word_at(a.sps, pr, a.r, wp, j);
+  s.dw = hif4_word_at(a.dns, pr, a.r, wp, j);
+}
+
+__device__ __forceinline__ void load_hf_w(HfW& w, const uint8_t* wc, const uint8_t* ws, int n0, int N, int K, int ks) {
+  const int p = ks >> 2, j = ks & 3, wp = min(128, K - 128 * p);
+  const int64_t pn = (int64_t)p * N;
+  const int n = min(n0 + (int)threadIdx.x, N - 1);
+  w.codes = *reinterpret_cast<const uint4*>(wc + pn * 64 + (int64_t)n * (wp / 2) + 16 * j);
+  w.word = hif4_word_at(ws, pn, n, wp, j);
+}
+
+__device__ __forceinline__ void store_hf_w(const HfW& w, uint8_t* lds, int hb) {
+  const int row = threadIdx.x;
+  const uint32_t c[4] = {w.codes.x, w.codes.y, w.codes.z, w.codes.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    *reinterpret_cast<uint4*>(lds + row * 64 + 16 * (q ^ swz_nv(row))) = hif4_dequant8_bf16(c[q], w.word, hb, q);
+}
+
+__device__ __forceinline__ void step_hf(v16f (&acc)[8], const HfA& a, int hb, const uint8_t* lw, int lane) {
+  const int half = lane >> 5, col = lane & 31;
+  const uint4 sp = expand_block<24>(a.spc, a.spm);
+  const uint32_t spw[4] = {sp.x, sp.y, sp.z, sp.w};
+  const uint32_t dnw[4] = {a.dn.x, a.dn.y, a.dn.z, a.dn.w};
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int q = half + 2 * t;   // K values 8 q .. 8 q + 7 of the block
+    const bf16x8 asp = as_bf16x8(hif4_dequant8_bf16(spw[q], a.sw, hb, q));
+    const bf16x8 adn = as_bf16x8(hif4_dequant8_bf16(dnw[q], a.dw, hb, q));
+    bf16x8 b[8];
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      const int row = f * 32 + col;
+      b[f] = as_bf16x8(*reinterpret_cast<const uint4*>(lw + row * 64 + 16 * (q ^ swz_nv(row))));
+    }
+#pragma unroll
+    for (int f = 0; f < 8; ++f) acc[f] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(asp, b[f], acc[f], 0, 0, 0);
+#pragma unroll
+    for (int f = 0; f < 8; ++f) acc[f] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(adn, b[f], acc[f], 0, 0, 0);
+  }
+}
+
+template <typename OutT>
+__global__ __launch_bounds__(256) void k_linear_hif4(const uint8_t* sp_codes, const uint8_t* sp_meta,
+                                                     const uint8_t* sp_scale, const uint8_t* dn_codes,
+                                                     const uint8_t* dn_scale, int64_t M, const uint8_t* wc,
+                                                     const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy, int gx,
+                                                     int gy) {
+  constexpr int NF = 8, BN = 256;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * BN * 64];
+  int mt, nt;
+  tile_of(blockIdx.x, gx, gy, mt, nt);
+  const int n0 = nt * BN;
+  const int64_t row_lo = (int64_t)mt * kBM;
+  const int64_t row_hi = row_lo + kBM < M ? row_lo + kBM : M;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
+  const int nks = K / 32;
+  int64_t orow = row_lo + wave * 32 + (lane & 31);
+  if (orow >= row_hi) orow = row_hi - 1;
+  ARow a;
+  a.r = orow;
+  a.R = M;
+  a.dn = dn_codes;
+  a.spc = sp_codes;
+  a.spm = sp_meta;
+  a.dns = dn_scale;
+  a.sps = sp_scale;
+
+  v16f acc[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[f][e] = 0.0f;
+
+  // the double-buffered pipeline of k_linear_nv; block ks is half ks & 1 of its unit
+  HfA a0, a1;
+  HfW wn;
+  const int last = nks - 1;
+  load_hf_w(wn, wc, ws, n0, N, K, 0);
+  load_hf_a(a0, a, 0, K);
+  store_hf_w(wn, lds, 0);
+  load_hf_w(wn, wc, ws, n0, N, K, min(1, last));
+  load_hf_a(a1, a, min(1, last), K);
+  int ks = 0;
+  for (; ks + 1 < nks; ks += 2) {   // nks is even: blocks ks, ks + 1 are the halves of one unit
+    __syncthreads();
+    step_hf(acc, a0, 0, lds, lane);
+    store_hf_w(wn, lds + BN * 64, 1);
+    load_hf_w(wn, wc, ws, n0, N, K, min(ks + 2, last));
+    load_hf_a(a0, a, min(ks + 2, last), K);
+    __syncthreads();
+    step_hf(acc, a1, 1, lds + BN * 64, lane);
+    store_hf_w(wn, lds, 0);
+    load_hf_w(wn, wc, ws, n0, N, K, min(ks + 3, last));
+    load_hf_a(a1, a, min(ks + 3, last), K);
+  }
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int col = n0 + f * 32 + (lane & 31);
+    if (col >= N) continue;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int64_t row = row_lo + wave * 32 + 8 * (e / 4) + 4 * half + (e % 4);
+      if (row < row_hi) store_out<OutT>(Y + row * ldy + col, acc[f][e]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Host-side launchers
 // ---------------------------------------------------------------------------
 
@@ -2116,6 +2275,25 @@ hipError_t launch_linear_slots(int mode, int pat, int ydt, bool nv, const uint8_
                        : go_slots_dt<48, 48>(ydt, nv, p1, p2, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
     default: return hipErrorInvalidValue;
   }
+}
+
+
+// HiF4 (2:4 backbone, K a multiple of 64).
+hipError_t launch_linear_hif4(int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
+                              const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
+                              void* Y, int64_t ldy, hipStream_t st) {
+  const int gx = (N + 255) / 256, gy = (int)((M + kBM - 1) / kBM);
+  const dim3 grid((unsigned)(gx * gy)), block(256);
+  if (ydt == 2)
+    k_linear_hif4<float><<<grid, block, 0, st>>>(spc, spm, sps, dnc, dns, M, wc, ws, N, K,
+                                                 reinterpret_cast<float*>(Y), ldy, gx, gy);
+  else if (ydt == 1)
+    k_linear_hif4<_Float16><<<grid, block, 0, st>>>(spc, spm, sps, dnc, dns, M, wc, ws, N, K,
+                                                    reinterpret_cast<_Float16*>(Y), ldy, gx, gy);
+  else
+    k_linear_hif4<uint16_t><<<grid, block, 0, st>>>(spc, spm, sps, dnc, dns, M, wc, ws, N, K,
+                                                    reinterpret_cast<uint16_t*>(Y), ldy, gx, gy);
+  return hipGetLastError();
 }
 
 }  // namespace sharq

@@ -780,6 +780,32 @@ __device__ __forceinline__ void mode_block(const float (&y)[32], const PathBufs&
   }
 }
 
+// RMSNorm reciprocal of one row from a first pass over it (NB chunks of 2048
+// positions, K <= 2048 NB): the balanced tree of the other kernels, with the
+// chunks past the row adding exact zeros.
+template <int NB>
+__device__ __forceinline__ float row_rms_2pass(const XSrc& src, int64_t row, int lane, int nblk, int K, float eps) {
+  float chunk[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const int b = lane + 64 * i;
+    float ss = 0.0f;
+    if (b < nblk) {
+      uint4 q[4];
+      load_block<false>(src, row, b, q, false);
+      float x[32];
+      unpack_bf16x32(q, x);
+      ss = block_sum_sq(x);
+    }
+    chunk[i] = wave_tree_sum(ss);
+  }
+#pragma unroll
+  for (int w = NB / 2; w >= 1; w >>= 1)
+#pragma unroll
+    for (int k = 0; k < w; ++k) chunk[k] = chunk[2 * k] + chunk[2 * k + 1];
+  return (float)(1.0 / __builtin_sqrt((double)chunk[0] / (double)K + (double)eps));
+}
+
 // One wavefront per row (4 rows per workgroup), lane l owning blocks
 // l, l + 64, ...  With RMSNorm (NORM) the row is read twice: a first pass
 // forms the same balanced tree as the other kernels (in-lane block sums, the
@@ -795,28 +821,7 @@ __global__ __launch_bounds__(256) void k_prep_mode(XSrc src, int M, int K, const
   if (row >= M) return;   // whole wavefront; the kernel has no block barrier
   const int nblk = K / 32;
   const float S = NV ? *S_ptr : 1.0f, six_s = 6.0f * S;
-  float r = 1.0f;
-  if (NORM) {
-    float chunk[NB];
-#pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const int b = lane + 64 * i;
-      float ss = 0.0f;
-      if (b < nblk) {
-        uint4 q[4];
-        load_block<false>(src, row, b, q, false);
-        float x[32];
-        unpack_bf16x32(q, x);
-        ss = block_sum_sq(x);
-      }
-      chunk[i] = wave_tree_sum(ss);
-    }
-#pragma unroll
-    for (int w = NB / 2; w >= 1; w >>= 1)
-#pragma unroll
-      for (int k = 0; k < w; ++k) chunk[k] = chunk[2 * k] + chunk[2 * k + 1];
-    r = (float)(1.0 / __builtin_sqrt((double)chunk[0] / (double)K + (double)eps));
-  }
+  const float r = NORM ? row_rms_2pass<NB>(src, row, lane, nblk, K, eps) : 1.0f;
   const uint4* gr = reinterpret_cast<const uint4*>(gamma);
   for (int b = lane; b < nblk; b += 64) {
     uint4 q[4];
@@ -831,6 +836,138 @@ __global__ __launch_bounds__(256) void k_prep_mode(XSrc src, int M, int K, const
       unpack_bf16x32(q, y);
     }
     mode_block<MODE, PAT, NV>(y, o, block_index(o.M, o.K, row, b), S, six_s);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// HiF4 preparation (2:4 backbone + dense residual).  A HiF4 unit of 64
+// positions is the block pair (2u, 2u + 1), held by the lanes (2j, 2j + 1) of
+// the row loop below; the unit maximum crosses the pair with one lane swap,
+// everything else stays in the lane.  The backbone unit spans 64 logical
+// positions: every group of 4 keeps its maximum, so its scales are those of
+// the dense row.
+// ---------------------------------------------------------------------------
+
+struct HfScale {
+  uint32_t code;   // E6M2
+  float base, rec;
+  uint32_t e8;     // this lane's 4 level-2 bits (bit i: values 8 i .. 8 i + 7 of its block)
+  uint32_t e16;    // this lane's 8 level-3 bits (bit g: values 4 g .. 4 g + 3)
+};
+
+__device__ __forceinline__ HfScale hif4_scale(const float (&v)[32]) {
+  float v16[8], v8[4];
+#pragma unroll
+  for (int g = 0; g < 8; ++g)
+    v16[g] = fmaxf(fmaxf(fabsf(v[4 * g]), fabsf(v[4 * g + 1])), fmaxf(fabsf(v[4 * g + 2]), fabsf(v[4 * g + 3])));
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v8[i] = fmaxf(v16[2 * i], v16[2 * i + 1]);
+  const float bm = fmaxf(fmaxf(v8[0], v8[1]), fmaxf(v8[2], v8[3]));
+  const float um = fmaxf(bm, __shfl_xor(bm, 1, 64));
+  HfScale h;
+  h.code = e6m2_code(um * kOneSeventhBf16);
+  h.base = e6m2_value(h.code);
+  h.rec = e6m2_rec(h.code);
+  h.e8 = 0u;
+  h.e16 = 0u;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) h.e8 |= (uint32_t)(v8[i] * h.rec >= 4.0f) << i;
+#pragma unroll
+  for (int g = 0; g < 8; ++g) h.e16 |= (uint32_t)(v16[g] * h.rec >= (((h.e8 >> (g >> 1)) & 1u) ? 4.0f : 2.0f)) << g;
+  return h;
+}
+
+// micro-exponent of level-3 group g (0..7) of the lane's block
+__device__ __forceinline__ int hif4_shift(const HfScale& h, int g) {
+  return (int)(((h.e8 >> (g >> 1)) & 1u) + ((h.e16 >> g) & 1u));
+}
+
+// The unit's 4 metadata bytes [E6M2, E1_8, E1_16 low, E1_16 high] (valid in
+// the even lane of the pair).
+__device__ __forceinline__ uint32_t hif4_word(const HfScale& h) {
+  const uint32_t mine = h.e8 | (h.e16 << 4);
+  const uint32_t other = (uint32_t)__shfl_xor((int)mine, 1, 64);
+  return h.code | (((mine & 0xFu) | ((other & 0xFu) << 4)) << 8) | (((mine >> 4) & 0xFFu) << 16) |
+         (((other >> 4) & 0xFFu) << 24);
+}
+
+__device__ __forceinline__ uint32_t hif4_enc(float v, const HfScale& h, int sh) {
+  return s1p2_code((v * h.rec) * exp2_int(-sh));
+}
+
+// 2:4 backbone of one block under HiF4: the selection and metadata of
+// backbone_24, each kept value quantized with its level-3 group's scale.
+__device__ __forceinline__ void backbone_24_hif4(const float (&y)[32], const HfScale& h, uint32_t (&codes)[2],
+                                                 uint32_t& meta, float (&R)[32]) {
+  codes[0] = codes[1] = 0u;
+  meta = 0u;
+#pragma unroll
+  for (int g = 7; g >= 0; --g) {
+    const float y0 = y[4 * g], y1 = y[4 * g + 1], y2 = y[4 * g + 2], y3 = y[4 * g + 3];
+    lmask k0, k1, k2, k3;
+    top2of4(y0, y1, y2, y3, k0, k1, k2, k3);
+    const float v0 = lsel(k0, y0, lsel(k1, y1, y2));
+    const float v1 = lsel(k3, y3, lsel(k2, y2, y1));
+    meta = push_bit(meta, k3 | k2);
+    meta = push_bit(meta, k3 | ~k2);
+    meta = push_bit(meta, ~(k0 | k1));
+    meta = push_bit(meta, k1 & ~k0);
+    const int sh = hif4_shift(h, g);
+    const uint32_t c0 = hif4_enc(v0, h, sh), c1 = hif4_enc(v1, h, sh);
+    codes[g >> 2] |= (c0 | (c1 << 4)) << (8 * (g & 3));
+    const float sc = h.base * exp2_int(sh);
+    const float r0 = v0 - s1p2_value(c0, sc), r1 = v1 - s1p2_value(c1, sc);
+    R[4 * g + 0] = lsel(k0, r0, y0);
+    R[4 * g + 1] = lsel(k1, lsel(k0, r1, r0), y1);
+    R[4 * g + 2] = lsel(k2, lsel(k3, r0, r1), y2);
+    R[4 * g + 3] = lsel(k3, r1, y3);
+  }
+}
+
+template <bool NORM>
+__global__ __launch_bounds__(256) void k_prep_hif4(XSrc src, int M, int K, const uint16_t* __restrict__ gamma,
+                                                   float eps, ActOut o) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;   // whole wavefront; the kernel has no block barrier
+  const int nblk = K / 32;
+  const float r = NORM ? row_rms_2pass<8>(src, row, lane, nblk, K, eps) : 1.0f;
+  const uint4* gr = reinterpret_cast<const uint4*>(gamma);
+  // nblk is even, so both lanes of a pair take the same iterations
+  for (int b = lane; b < nblk; b += 64) {
+    uint4 q[4];
+    load_block<false>(src, row, b, q, false);
+    float y[32];
+    if (NORM) {
+      uint4 gq[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) gq[j] = gr[4 * b + j];
+      norm_block(q, gq, r, y);
+    } else {
+      unpack_bf16x32(q, y);
+    }
+    const HfScale hb = hif4_scale(y);
+    uint32_t codes[2], meta;
+    float R[32];
+    backbone_24_hif4(y, hb, codes, meta, R);
+    const HfScale hr = hif4_scale(R);
+    uint32_t dn[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      uint32_t d = 0u;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) d |= hif4_enc(R[8 * w + i], hr, hif4_shift(hr, 2 * w + (i >> 2))) << (4 * i);
+      dn[w] = d;
+    }
+    const uint32_t wb = hif4_word(hb), wr = hif4_word(hr);
+    const int64_t V = block_index(o.M, o.K, row, b);
+    *reinterpret_cast<uint2*>(o.spc + V * 8) = make_uint2(codes[0], codes[1]);
+    *reinterpret_cast<uint32_t*>(o.spm + V * 4) = meta;
+    *reinterpret_cast<uint4*>(o.dnc + V * 16) = make_uint4(dn[0], dn[1], dn[2], dn[3]);
+    if ((lane & 1) == 0) {   // the unit's metadata at the even block's 2-byte slots
+      *reinterpret_cast<uint32_t*>(o.sps + V * 2) = wb;
+      *reinterpret_cast<uint32_t*>(o.dns + V * 2) = wr;
+    }
   }
 }
 
@@ -980,6 +1117,20 @@ hipError_t launch_prep_mode(int mode, const uint16_t* X, int M, int K, int64_t l
                : go_prep_mode_pat<4, false>(pat, src, M, K, gamma, eps, o, S, grid, st); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+// HiF4 preparation (2:4 backbone, SharQ mode; K a multiple of 64, K <= 16384
+// with RMSNorm).
+hipError_t launch_prep_hif4(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps,
+                            uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, hipStream_t st) {
+  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K};
+  const XSrc src{X, ldx, nullptr, 0, nullptr, 0};
+  const dim3 grid((unsigned)((M + 3) / 4));
+  if (gamma)
+    k_prep_hif4<true><<<grid, 256, 0, st>>>(src, M, K, gamma, eps, o);
+  else
+    k_prep_hif4<false><<<grid, 256, 0, st>>>(src, M, K, gamma, eps, o);
   return hipGetLastError();
 }
 

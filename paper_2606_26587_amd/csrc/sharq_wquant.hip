@@ -5,7 +5,8 @@
 // MXFP4: one lane per 32-value block along K; E8M0 exponent
 // floor(log2 amax) - 2 (clamped at -127), codes E2M1(w / 2^e).  The payload
 // and its scales are written panel-major (panels of 128 K positions, all N
-// rows of a panel back to back), the layout the GEMM streams.
+// rows of a panel back to back), the layout the GEMM streams.  NVFP4 and
+// HiF4 follow below.
 
 #include "sharq_device.hpp"
 
@@ -123,6 +124,70 @@ __global__ __launch_bounds__(256) void k_wquant_nv(const T* __restrict__ W, int 
   uint8_t* sd = scale_dn + pn * 8 + n * (wp / 16) + 2 * j;
   sd[0] = sb;
   sd[1] = sb;
+}
+
+// HiF4 weight: one thread per unit of 64 values along K (the conversion of
+// the HiF4 appendix; see sharq_device.hpp).  Codes go to the unit's two
+// 16-byte block slots, its 4 metadata bytes [E6M2, E1_8, E1_16 low, E1_16
+// high] to the even block's 2-byte scale slots (one view for both paths).
+template <typename T>
+__global__ __launch_bounds__(256) void k_wquant_hif4(const T* __restrict__ W, int N, int K, int64_t ldw,
+                                                     uint8_t* __restrict__ codes, uint8_t* __restrict__ scale) {
+  const int nu = K / 64;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= (int64_t)N * nu) return;
+  const int64_t n = gid / nu;
+  const int u = (int)(gid - n * nu);
+  float v[64];
+  load32<T>(W + n * ldw + 64 * (int64_t)u, *reinterpret_cast<float(*)[32]>(v));
+  load32<T>(W + n * ldw + 64 * (int64_t)u + 32, *reinterpret_cast<float(*)[32]>(v + 32));
+  float v16[16], v8[8];
+#pragma unroll
+  for (int g = 0; g < 16; ++g)
+    v16[g] = fmaxf(fmaxf(fabsf(v[4 * g]), fabsf(v[4 * g + 1])), fmaxf(fabsf(v[4 * g + 2]), fabsf(v[4 * g + 3])));
+  float vmax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    v8[i] = fmaxf(v16[2 * i], v16[2 * i + 1]);
+    vmax = fmaxf(vmax, v8[i]);
+  }
+  const uint32_t code = e6m2_code(vmax * kOneSeventhBf16);
+  const float rec = e6m2_rec(code);
+  uint32_t e8 = 0u, e16 = 0u;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) e8 |= (uint32_t)(v8[i] * rec >= 4.0f) << i;
+#pragma unroll
+  for (int g = 0; g < 16; ++g) e16 |= (uint32_t)(v16[g] * rec >= (((e8 >> (g >> 1)) & 1u) ? 4.0f : 2.0f)) << g;
+  uint32_t q[8];
+#pragma unroll
+  for (int w = 0; w < 8; ++w) {
+    uint32_t d = 0u;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int k = 8 * w + i;
+      const int sh = (int)(((e8 >> (k >> 3)) & 1u) + ((e16 >> (k >> 2)) & 1u));
+      d |= s1p2_code((v[k] * rec) * exp2_int(-sh)) << (4 * i);
+    }
+    q[w] = d;
+  }
+  const int b = 2 * u, p = b >> 2, j = b & 3, wp = min(128, K - 128 * p);
+  const int64_t pn = (int64_t)p * N;
+  uint4* c = reinterpret_cast<uint4*>(codes + pn * 64 + n * (wp / 2) + 16 * j);
+  c[0] = make_uint4(q[0], q[1], q[2], q[3]);
+  c[1] = make_uint4(q[4], q[5], q[6], q[7]);
+  *reinterpret_cast<uint32_t*>(scale + (pn * 4 + n * (wp / 32) + j) * 2) =
+      code | (e8 << 8) | (e16 << 16);
+}
+
+hipError_t launch_wquant_hif4(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
+                              hipStream_t st) {
+  const int64_t total = (int64_t)N * (K / 64);
+  dim3 grid((unsigned)((total + 255) / 256)), block(256);
+  if (wdt == 2)
+    k_wquant_hif4<float><<<grid, block, 0, st>>>(reinterpret_cast<const float*>(W), N, K, ldw, codes, scale);
+  else
+    k_wquant_hif4<uint16_t><<<grid, block, 0, st>>>(reinterpret_cast<const uint16_t*>(W), N, K, ldw, codes, scale);
+  return hipGetLastError();
 }
 
 hipError_t launch_wquant_mx(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,

@@ -18,10 +18,10 @@ import torch
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsharq.so")
 
 OK, EINVAL, EUNSUPPORTED, EALIGN, EHIP = 0, 1, 2, 3, 4
-MXFP4, NVFP4 = 0, 1
+MXFP4, NVFP4, HIF4 = 0, 1, 2
 BF16, F16, F32 = 0, 1, 2
 
-_FMT = {"mx": MXFP4, "mxfp4": MXFP4, "nv": NVFP4, "nvfp4": NVFP4}
+_FMT = {"mx": MXFP4, "mxfp4": MXFP4, "nv": NVFP4, "nvfp4": NVFP4, "hif4": HIF4}
 #: path combinations (sharq_mode): the method, and the ablation modes
 MODES = {"sharq": 0, "sparse": 1, "dense": 2, "dense_dense": 3, "sparse_sparse": 4}
 _DT = {torch.bfloat16: BF16, torch.float16: F16, torch.float32: F32}
@@ -169,8 +169,8 @@ def alloc_weight(N: int, K: int, fmt="mx", experts: int = 1, device="cuda") -> Q
     """Device buffers of a quantized weight, one flat panel-major row per expert."""
     f = _FMT[fmt] if isinstance(fmt, str) else fmt
     codes = torch.empty((experts, N * K // 2), dtype=torch.uint8, device=device)
-    scale = torch.empty((experts, N * K // 32), dtype=torch.uint8, device=device)
-    scale_dn = scale if f == MXFP4 else torch.empty((experts, N * K // 16), dtype=torch.uint8, device=device)
+    scale = torch.empty((experts, N * K // (16 if f == HIF4 else 32)), dtype=torch.uint8, device=device)
+    scale_dn = scale if f != NVFP4 else torch.empty((experts, N * K // 16), dtype=torch.uint8, device=device)
     ts = torch.empty(experts, dtype=torch.float32, device=device) if f == NVFP4 else None
     return QuantWeight(N, K, experts, f, codes, scale, scale_dn, ts)
 
@@ -258,7 +258,7 @@ def stack_weights(ws: Sequence[QuantWeight]) -> QuantWeight:
     w0 = ws[0]
     ts = None if w0.tensor_scale is None else torch.cat([w.tensor_scale for w in ws])
     scale = torch.cat([w.scale for w in ws])
-    scale_dn = scale if w0.fmt == MXFP4 else torch.cat([w.scale_dn for w in ws])
+    scale_dn = scale if w0.fmt != NVFP4 else torch.cat([w.scale_dn for w in ws])
     return QuantWeight(w0.N, w0.K, len(ws), w0.fmt, torch.cat([w.codes for w in ws]), scale, scale_dn, ts)
 
 

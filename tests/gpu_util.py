@@ -21,7 +21,8 @@ def host(t: torch.Tensor) -> np.ndarray:
     return t.detach().cpu().numpy()
 
 
-FMT_NAME = {S.MXFP4: "mx", S.NVFP4: "nv"}
+FMT_NAME = {S.MXFP4: "mx", S.NVFP4: "nv", S.HIF4: "hif4"}
+FMT_ID = {"mx": S.MXFP4, "nv": S.NVFP4, "hif4": S.HIF4}
 MODE_NAME = {v: k for k, v in S.MODES.items()}
 
 
@@ -37,7 +38,7 @@ def act_to_oracle(a: S.PreparedAct) -> dict:
 
 def oracle_to_act(o: dict) -> S.PreparedAct:
     """Oracle prepared activation -> device buffers in the library's layout."""
-    fmt = S.MXFP4 if o["fmt"] == "mx" else S.NVFP4
+    fmt = FMT_ID[o["fmt"]]
     dev = O.act_to_device_layout(o)
     ts = None
     if fmt == S.NVFP4:
@@ -51,12 +52,12 @@ def oracle_to_act(o: dict) -> S.PreparedAct:
 
 
 def oracle_to_weight(o: dict) -> S.QuantWeight:
-    fmt = S.MXFP4 if o["fmt"] == "mx" else S.NVFP4
+    fmt = FMT_ID[o["fmt"]]
     dev = O.weight_to_device_layout(o)
     codes = dev_u8(dev["codes"])[None]
     scale = dev_u8(dev["scale"])[None]
-    scale_dn = scale if fmt == S.MXFP4 else dev_u8(dev["scale_dn"])[None]
-    ts = None if fmt == S.MXFP4 else torch.tensor([float(o["tensor_scale"])], dtype=torch.float32, device="cuda")
+    scale_dn = scale if fmt != S.NVFP4 else dev_u8(dev["scale_dn"])[None]
+    ts = None if fmt != S.NVFP4 else torch.tensor([float(o["tensor_scale"])], dtype=torch.float32, device="cuda")
     return S.QuantWeight(o["N"], o["K"], 1, fmt, codes, scale, scale_dn, ts)
 
 

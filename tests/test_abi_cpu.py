@@ -285,3 +285,37 @@ def test_mode_empty_calls_launch_nothing(L):
         assert L.sharq_prepare(None, 0, 0, 128, 128, None, 1e-6, Pattern(2, 4), 0, None, ctypes.byref(a), None) == OK
         w = Weight(64, 128, 1, 0, FAKE, FAKE, FAKE, None)
         assert L.sharq_linear(ctypes.byref(a), ctypes.byref(w), None, 0, 64, None) == OK
+
+
+# ----------------------------------------------------------------------------- HiF4
+
+HIF4 = 2
+
+
+def test_hif4_buffer_sizes(L):
+    rows, K = 3, 256
+    got = [L.sharq_act_buffer_bytes(rows, K, HIF4, Pattern(2, 4), w) for w in range(5)]
+    assert got == [rows * K // 4, rows * K // 8, rows * K // 16, rows * K // 2, rows * K // 16]
+    assert L.sharq_act_buffer_bytes(rows, 96, HIF4, Pattern(2, 4), 3) == 0          # K % 64
+    assert [L.sharq_weight_buffer_bytes(40, K, HIF4, w) for w in range(3)] == [40 * K // 2, 40 * K // 16, 40 * K // 16]
+
+
+def test_hif4_rejections(L):
+    def prep(a, nm=(2, 4), K=None):
+        K = K or a.K
+        return L.sharq_prepare(FAKE, 0, a.rows, K, K, None, 1e-6, Pattern(*nm), HIF4, None, ctypes.byref(a), None)
+    assert prep(act(K=96, fmt=HIF4)) == EINVAL                             # K not a multiple of 64
+    assert prep(act(n=4, m=8, fmt=HIF4), (4, 8)) == EUNSUPPORTED           # built with 2:4 only
+    assert prep(act(fmt=HIF4, mode=SPARSE)) == EUNSUPPORTED                # the method's combination only
+    a = act(fmt=HIF4)
+    st = L.sharq_prepare_residual(FAKE, FAKE, FAKE, 0, 8, 128, 128, 128, 128, None, 1e-6, Pattern(2, 4), HIF4, None,
+                                  ctypes.byref(a), None)
+    assert st == EUNSUPPORTED
+    w = Weight(64, 128, 1, HIF4, FAKE, FAKE, FAKE, None)
+    st = L.sharq_linear_grouped(ctypes.byref(act(fmt=HIF4)), None, FAKE, 8, ctypes.byref(w), FAKE, 0, 64, None)
+    assert st == EUNSUPPORTED
+    wq = Weight(64, 96, 1, HIF4, FAKE, FAKE, FAKE, None)
+    assert L.sharq_quantize_weight(FAKE, 0, 64, 96, 96, ctypes.byref(wq), None) == EINVAL
+    # formats must agree between activation and weight
+    wmx = Weight(64, 128, 1, 0, FAKE, FAKE, FAKE, None)
+    assert L.sharq_linear(ctypes.byref(act(fmt=HIF4)), ctypes.byref(wmx), FAKE, 0, 64, None) == EINVAL
