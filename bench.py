@@ -22,8 +22,8 @@ Other workloads (--workload), one JSON line each:
                 4:8 backbone, grouped GEMMs
   ablation      the path combinations (Sparse, plain FP4 RTN, Dense+Dense,
                 Sparse+Sparse, SharQ) on the Llama prefill linears, MXFP4 2:4
-                and NVFP4 4:8 in pairs: time per step and the output error
-                against the unquantized product, per mode
+                and NVFP4 4:8 in pairs, and SharQ with HiF4 2:4: time per step
+                and the output error against the unquantized product, per mode
 --calibrate-copy MiB runs a plain device copy of that size (the reference
 kernel for scaling the profiler's HBM byte counters) and nothing else.
 
@@ -397,7 +397,7 @@ def ablation(args, torch, S, synth, dev, stream):
     T = T_TOKENS
     eps = synth.LLAMA_EPS
     outs = []
-    for fmt, n, m, pairs in (("mx", 2, 4, False), ("nv", 4, 8, True)):
+    for fmt, n, m, pairs in (("mx", 2, 4, False), ("nv", 4, 8, True), ("hif4", 2, 4, False)):
         layers = []
         for name, (K, N, norm) in synth.LLAMA_LINEARS.items():
             x = to_dev(synth.activations(T, K, seed=0))
@@ -416,7 +416,8 @@ def ablation(args, torch, S, synth, dev, stream):
             del xf, yf
         torch.cuda.synchronize()
         res = {}
-        for mode in ABLATION_MODES:
+        # HiF4 is built for the method's own combination only
+        for mode in (ABLATION_MODES if fmt != "hif4" else ["sharq"]):
             acts = [S.alloc_act(T, L["K"], n, m, fmt, dev, pairs, mode) for L in layers]
 
             def step(i, mark, acts=acts):
@@ -443,12 +444,12 @@ def ablation(args, torch, S, synth, dev, stream):
             log(f"[bench] ablation {fmt} {mode:14s} {ms_step:7.4f} ms/step  rel err "
                 + "  ".join(f"{k} {v:.4f}" for k, v in errs.items()))
             del acts
-        setting = "MXFP4 2:4" if fmt == "mx" else "NVFP4 4:8 in pairs"
+        setting = {"mx": "MXFP4 2:4", "nv": "NVFP4 4:8 in pairs", "hif4": "HiF4 2:4"}[fmt]
         out = base_record(args, "SharQ path-combination ablation: time per step and output error, Llama-8B M=2048",
                           res["sharq"]["executed_TFLOPs"], "TFLOP/s", res["sharq"]["ms_per_step"],
-                          "mxfp4" if fmt == "mx" else "nvfp4",
+                          {"mx": "mxfp4", "nv": "nvfp4", "hif4": "hif4"}[fmt],
                           {"workload": f"Llama-3.1-8B prefill linears qkv, gate_up (RMSNorm), down; M=2048; "
-                                       f"{setting}; fp32 out; modes " + ", ".join(ABLATION_MODES), "tokens": T})
+                                       f"{setting}; fp32 out; modes " + ", ".join(res), "tokens": T})
         out["modes"] = res
         out["error_definition"] = ("mean over token rows of |Y_t - y_t W^T| / |y_t W^T| (fp32 reference with the "
                                    "unquantized weight), per linear")
