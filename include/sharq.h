@@ -267,6 +267,27 @@ SHARQ_API sharq_status sharq_prepare_residual(const void *X, const void *residua
                                     const float *tensor_scale_in, sharq_act *out, void *stream);
 
 /*
+ * Preparation of a down projection's input with the SiLU.mul that produces it
+ * fused in on the producer side (Sec. 4.3: the preparation absorbs the
+ * preprocessing steps of the data flow).  Per element,
+ * h = bf16(SiLU(g) * u), SiLU(g) = g / (1 + exp(-g)), evaluated in fp32 with
+ * the hardware exponential and reciprocal (~1 ulp each; for g < 0 with e^g
+ * kept normal by a power-of-two scale) and rounded to bf16 to nearest even
+ * once; for finite inputs with |g u| < 1e19, h is within one bf16 step of the
+ * exactly rounded value.  h is prepared without RMSNorm exactly as sharq_prepare prepares X,
+ * and written to h_out (bf16 [M][K], row stride ldh) when h_out is not NULL.
+ * gate, up: bf16 [M][K], row strides ldg, ldu (e.g. the two halves of a
+ * gate/up projection's output, ldg = ldu = 2K); 16-byte aligned with 16-byte
+ * row strides.  With NVFP4 and no tensor_scale_in the amax pre-pass forms h
+ * as well.  Modes other than SHARQ_MODE_SHARQ and HiF4: SHARQ_EUNSUPPORTED.
+ * Other arguments, errors and outputs as for sharq_prepare.
+ */
+SHARQ_API sharq_status sharq_prepare_silu_mul(const void *gate, const void *up, void *h_out, sharq_dtype xdt,
+                                    int64_t M, int64_t K, int64_t ldg, int64_t ldu, int64_t ldh,
+                                    sharq_pattern nm, sharq_format fmt, const float *tensor_scale_in,
+                                    sharq_act *out, void *stream);
+
+/*
  * Two-path output (eq. "sharq-output"; Sec. 3.4 "Residual path compensation
  * by accumulation"): Y [rows][N] (row stride ldy, dtype ydt) =
  *   dequant(backbone) * dequant_sp(W)^T + dequant(residual) * dequant_dn(W)^T,

@@ -73,6 +73,10 @@ Readings where the paper is silent (each also listed in the design notes):
       spans 64 logical positions (dropped positions are zero).  No per-tensor
       scale.  Metadata bytes per unit: E6M2 code, E1_8 bits, E1_16 bits
       (low byte, high byte), bit j = group j.
+  R12 SiLU.mul fused into the preparation of the down projection's input:
+      h = bf16(SiLU(g) * u) with SiLU(g) = g / (1 + exp(-g)), the product
+      evaluated in fp64 and rounded to bf16 once (nearest even); the
+      preparation then works on h.
 """
 
 from __future__ import annotations
@@ -813,6 +817,35 @@ def prepare_residual(x_bf16: np.ndarray, res_bf16: np.ndarray, gamma_bf16: np.nd
     (R9), then prepare(h).  The dict also carries h (bf16 bits)."""
     h = residual_add_bf16(x_bf16, res_bf16)
     out = prepare(h, gamma_bf16, eps, n, m, fmt, tensor_scale, pairs)
+    out["h"] = h
+    return out
+
+
+def silu_mul_bf16(gate_bf16: np.ndarray, up_bf16: np.ndarray) -> np.ndarray:
+    """h = bf16(SiLU(g) * u) (reading R12): SiLU(g) = g / (1 + exp(-g)) and the
+    product in fp64, rounded once to bf16 (nearest even).  Returns bf16 bits."""
+    g = bf16_bits_to_f32(gate_bf16).astype(np.float64)
+    u = bf16_bits_to_f32(up_bf16).astype(np.float64)
+    with np.errstate(over="ignore"):
+        h = g / (1.0 + np.exp(-g)) * u
+    # fp64 -> bf16, nearest even: through the exact fp64 bits
+    b = h.view(np.uint64)
+    sign = (b >> np.uint64(63)).astype(np.uint16) << np.uint16(15)
+    a = np.abs(h)
+    e = np.frexp(np.where(a > 0, a, 1.0))[1] - 1                  # floor(log2 |h|)
+    q = np.ldexp(1.0, np.maximum(e, -126) - 7)                      # bf16 spacing at |h| (subnormals: 2^-133)
+    r = np.rint(a / q) * q                                          # a / q is exact: a power-of-two scaling
+    r32 = r.astype(np.float32)                                      # exact: r is a bf16 value (or overflows to inf)
+    out = (r32.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+    return (out | sign).astype(np.uint16)
+
+
+def prepare_silu_mul(gate_bf16: np.ndarray, up_bf16: np.ndarray, n: int, m: int, fmt: str = "mx",
+                     tensor_scale: float | None = None, pairs: bool = False) -> dict:
+    """Preparation with SiLU.mul in front (R12), for the down projection (no
+    RMSNorm): h = bf16(SiLU(g) * u), then prepare(h).  The dict also carries h."""
+    h = silu_mul_bf16(gate_bf16, up_bf16)
+    out = prepare(h, None, 0.0, n, m, fmt, tensor_scale, pairs)
     out["h"] = h
     return out
 

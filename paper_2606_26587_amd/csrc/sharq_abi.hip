@@ -36,6 +36,9 @@ hipError_t launch_wquant_hif4(const void* W, int wdt, int N, int K, int64_t ldw,
 hipError_t launch_linear_hif4(int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
                               const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
                               void* Y, int64_t ldy, hipStream_t st);
+hipError_t launch_prep_silu(const uint16_t* gate, const uint16_t* up, uint16_t* h, int M, int K, int64_t ldg,
+                            int64_t ldu, int64_t ldh, int pat, bool nv, const float* ts_in, float* ts_out,
+                            uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, hipStream_t st);
 hipError_t launch_linear_mx_grouped(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                                     const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx, int64_t act_rows,
                                     const int32_t* offs, int E, int64_t total, const uint8_t* wc, const uint8_t* ws,
@@ -207,15 +210,20 @@ sharq_status sharq_quantize_weight(const void* W, sharq_dtype wdt, int64_t N, in
 
 namespace {
 
-// Shared by sharq_prepare and sharq_prepare_residual (res == NULL: no
-// residual input).
-sharq_status prepare_impl(const void* X, const void* res, void* h_out, sharq_dtype xdt, int64_t M, int64_t K,
-                          int64_t ldx, int64_t ldr, int64_t ldh, const void* gamma, float eps, sharq_pattern nm,
-                          sharq_format fmt, const float* tensor_scale_in, sharq_act* out, void* stream) {
+// Shared by sharq_prepare, sharq_prepare_residual and sharq_prepare_silu_mul.
+// Source kinds: 0, X itself; 1, the residual add (res = the residual, h_out
+// required); 2, SiLU.mul (X = gate, res = up, h_out optional, no gamma).
+constexpr int kSrcPlain = 0, kSrcResidual = 1, kSrcSilu = 2;
+
+sharq_status prepare_impl(int src, const void* X, const void* res, void* h_out, sharq_dtype xdt, int64_t M,
+                          int64_t K, int64_t ldx, int64_t ldr, int64_t ldh, const void* gamma, float eps,
+                          sharq_pattern nm, sharq_format fmt, const float* tensor_scale_in, sharq_act* out,
+                          void* stream) {
   if (!out) return SHARQ_EINVAL;
   if (M < 0 || M > INT_MAX || K <= 0 || K % 32 != 0 || K > kMaxK || ldx < K) return SHARQ_EINVAL;
   if (!X && M > 0) return SHARQ_EINVAL;
-  if (res && (ldr < K || ldh < K || (!h_out && M > 0))) return SHARQ_EINVAL;
+  if (src == kSrcResidual && (ldr < K || ldh < K || (!h_out && M > 0))) return SHARQ_EINVAL;
+  if (src == kSrcSilu && (ldr < K || (h_out && ldh < K) || gamma)) return SHARQ_EINVAL;
   const int pid = pattern_id(nm);
   if (pid < 0 || K % nm.m != 0) return SHARQ_EINVAL;
   if (out->rows != M || out->K != K || out->fmt != fmt || out->nm.n != nm.n || out->nm.m != nm.m ||
@@ -230,11 +238,17 @@ sharq_status prepare_impl(const void* X, const void* res, void* h_out, sharq_dty
   if (nv && M > 0 && !out->tensor_scale) return SHARQ_EINVAL;
   if (!aligned(X, 16) || (ldx * 2) % 16 != 0 || (gamma && !aligned(gamma, 16)) || !aligned(tensor_scale_in, 4))
     return SHARQ_EALIGN;
-  if (res && (!aligned(res, 16) || !aligned(h_out, 16) || (ldr * 2) % 16 != 0 || (ldh * 2) % 16 != 0))
+  if (res && (!aligned(res, 16) || !aligned(h_out, 16) || (ldr * 2) % 16 != 0 || (h_out && (ldh * 2) % 16 != 0)))
     return SHARQ_EALIGN;
   if (res && out->mode != SHARQ_MODE_SHARQ) return SHARQ_EUNSUPPORTED;
   if (res && fmt == SHARQ_HIF4) return SHARQ_EUNSUPPORTED;
   if (M == 0) return SHARQ_OK;
+  if (src == kSrcSilu)
+    return hip_status(sharq::launch_prep_silu(static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(res),
+                                              static_cast<uint16_t*>(h_out), (int)M, (int)K, ldx, ldr, ldh, pid, nv,
+                                              nv ? tensor_scale_in : nullptr, nv ? out->tensor_scale : nullptr,
+                                              out->sp_codes, out->sp_meta, out->sp_scale, out->dn_codes,
+                                              out->dn_scale, reinterpret_cast<hipStream_t>(stream)));
   if (fmt == SHARQ_HIF4)
     return hip_status(sharq::launch_prep_hif4(static_cast<const uint16_t*>(X), (int)M, (int)K, ldx,
                                               static_cast<const uint16_t*>(gamma), eps, out->sp_codes, out->sp_meta,
@@ -263,7 +277,8 @@ extern "C" {
 sharq_status sharq_prepare(const void* X, sharq_dtype xdt, int64_t M, int64_t K, int64_t ldx, const void* gamma,
                            float eps, sharq_pattern nm, sharq_format fmt, const float* tensor_scale_in,
                            sharq_act* out, void* stream) {
-  return prepare_impl(X, nullptr, nullptr, xdt, M, K, ldx, K, K, gamma, eps, nm, fmt, tensor_scale_in, out, stream);
+  return prepare_impl(kSrcPlain, X, nullptr, nullptr, xdt, M, K, ldx, K, K, gamma, eps, nm, fmt, tensor_scale_in, out,
+                      stream);
 }
 
 sharq_status sharq_prepare_residual(const void* X, const void* residual, void* h_out, sharq_dtype xdt, int64_t M,
@@ -272,8 +287,17 @@ sharq_status sharq_prepare_residual(const void* X, const void* residual, void* h
                                     sharq_act* out, void* stream) {
   if (!residual && M > 0) return SHARQ_EINVAL;
   if (M == 0) residual = nullptr;
-  return prepare_impl(X, residual, h_out, xdt, M, K, ldx, ldr, ldh, gamma, eps, nm, fmt, tensor_scale_in, out,
-                      stream);
+  return prepare_impl(kSrcResidual, X, residual, h_out, xdt, M, K, ldx, ldr, ldh, gamma, eps, nm, fmt,
+                      tensor_scale_in, out, stream);
+}
+
+sharq_status sharq_prepare_silu_mul(const void* gate, const void* up, void* h_out, sharq_dtype xdt, int64_t M,
+                                    int64_t K, int64_t ldg, int64_t ldu, int64_t ldh, sharq_pattern nm,
+                                    sharq_format fmt, const float* tensor_scale_in, sharq_act* out, void* stream) {
+  if (!up && M > 0) return SHARQ_EINVAL;
+  if (M == 0) up = nullptr;
+  return prepare_impl(kSrcSilu, gate, up, h_out, xdt, M, K, ldg, ldu, ldh, nullptr, 0.0f, nm, fmt, tensor_scale_in,
+                      out, stream);
 }
 
 sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sharq_dtype ydt, int64_t ldy,

@@ -416,24 +416,57 @@ __device__ __forceinline__ uint32_t add_bf16x2(uint32_t a, uint32_t b) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
-// Block b (32 values, four 16-byte pieces) of `row`; with a residual input,
-// h is formed and, when write_h, stored.  Every (row, block) is stored by
-// exactly one lane, which read its residual before: in place is safe.
-template <bool RES>
+// SiLU(g) * u in fp32 for the down projection's input (the SiLU.mul that
+// follows the gate/up projection, fused into the preparation on the producer
+// side), with the hardware exponential (2^x) and reciprocal, ~1 ulp each.
+// For g < 0 the factor e^g is formed scaled by 2^64 and the scale removed
+// after the product, so that e^g * g * u keeps its precision where e^g alone
+// would be an fp32 subnormal (g < -87 next to a large u).  h = bf16(SiLU(g) *
+// u) then lies within one bf16 step of the exactly rounded value, and equals
+// it unless the exact value is within ~1e-5 (relative) of a rounding boundary.
+__device__ __forceinline__ float silu_mul(float g, float u) {
+  const float t = g * 1.44269504088896341f;   // g log2(e)
+  if (g >= 0.0f) return (g * u) * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-t));
+  const float es = __builtin_amdgcn_exp2f(t + 64.0f);   // e^g 2^64: a normal value for g > -131
+  return (((g * u) * es) * __builtin_amdgcn_rcpf(1.0f + es * 0x1p-64f)) * 0x1p-64f;
+}
+
+__device__ __forceinline__ uint32_t silu_mul_bf16x2(uint32_t g, uint32_t u) {
+  typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+  bf2 v;
+  v[0] = (__bf16)silu_mul(bf16_lo(g), bf16_lo(u));   // nearest even
+  v[1] = (__bf16)silu_mul(bf16_hi(g), bf16_hi(u));
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// Sources of the rows a preparation reads (SRC): 0, X itself; 1, the residual
+// add h = bf16(x + res) (Rs = res); 2, SiLU.mul h = bf16(SiLU(g) * u) (X = g,
+// Rs = u).  Block b (32 values, four 16-byte pieces) of `row` is loaded and h
+// formed; when write_h (and, for SiLU.mul, H given) it is stored.  Every
+// (row, block) is stored by exactly one lane, which read its inputs before:
+// in place is safe.
+template <int SRC>
 __device__ __forceinline__ void load_block(const XSrc& s, int64_t row, int b, uint4 (&q)[4], bool write_h) {
   const uint4* xr = reinterpret_cast<const uint4*>(s.X + row * s.ldx);
 #pragma unroll
   for (int j = 0; j < 4; ++j) q[j] = xr[4 * b + j];
-  if (RES) {
+  if (SRC != 0) {
     const uint4* rr = reinterpret_cast<const uint4*>(s.Rs + row * s.ldr);
     uint4 rq[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) rq[j] = rr[4 * b + j];
+    if (SRC == 1) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      q[j] = make_uint4(add_bf16x2(q[j].x, rq[j].x), add_bf16x2(q[j].y, rq[j].y), add_bf16x2(q[j].z, rq[j].z),
-                        add_bf16x2(q[j].w, rq[j].w));
-    if (write_h) {
+      for (int j = 0; j < 4; ++j)
+        q[j] = make_uint4(add_bf16x2(q[j].x, rq[j].x), add_bf16x2(q[j].y, rq[j].y), add_bf16x2(q[j].z, rq[j].z),
+                          add_bf16x2(q[j].w, rq[j].w));
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        q[j] = make_uint4(silu_mul_bf16x2(q[j].x, rq[j].x), silu_mul_bf16x2(q[j].y, rq[j].y),
+                          silu_mul_bf16x2(q[j].z, rq[j].z), silu_mul_bf16x2(q[j].w, rq[j].w));
+    }
+    if (write_h && (SRC == 1 || s.H != nullptr)) {
       uint4* hr = reinterpret_cast<uint4*>(s.H + row * s.ldh);
 #pragma unroll
       for (int j = 0; j < 4; ++j) hr[4 * b + j] = q[j];
@@ -581,7 +614,7 @@ __global__ __launch_bounds__(256) void k_prep_norm_split(XSrc src, int M, int K,
 // consecutive threads write consecutive bytes of every output buffer (and
 // read 256-byte row pieces of X).  The last panel may hold q < 4 blocks per
 // row.
-template <int PAT, bool NV, bool RES>
+template <int PAT, bool NV, int SRC>
 __global__ __launch_bounds__(256) void k_prep_blocks(XSrc src, int M, int K, ActOut o, const float* S_ptr) {
   const int nblk = K / 32, p = blockIdx.y;
   const int q = min(4, nblk - 4 * p);      // blocks per row in this panel
@@ -598,7 +631,7 @@ __global__ __launch_bounds__(256) void k_prep_blocks(XSrc src, int M, int K, Act
   const int b = 4 * p + (int)j;
   const float S = NV ? *S_ptr : 1.0f, six_s = 6.0f * S;
   uint4 xq[4];
-  load_block<RES>(src, (int64_t)row, b, xq, true);
+  load_block<SRC>(src, (int64_t)row, b, xq, true);
   float y[32];
   unpack_bf16x32(xq, y);
   const BlockOut d = block_at<NV>(o, (int64_t)p * M * 4 + t);
@@ -651,7 +684,7 @@ __global__ __launch_bounds__(256) void k_amax_norm(XSrc src, int M, int K, const
   if (lane == 0) atomicMax(slot, __float_as_uint(m));
 }
 
-template <bool RES>
+template <int SRC>
 __global__ __launch_bounds__(256) void k_amax_plain(XSrc src, int M, int K, uint32_t* slot) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -659,7 +692,7 @@ __global__ __launch_bounds__(256) void k_amax_plain(XSrc src, int M, int K, uint
   float m = 0.0f;
   for (int b = lane; b < K / 32; b += 64) {
     uint4 q[4];
-    load_block<RES>(src, row, b, q, false);
+    load_block<SRC>(src, row, b, q, false);
     float y[32];
     unpack_bf16x32(q, y);
     m = fmaxf(m, absmax32(y));
@@ -987,7 +1020,7 @@ static void go_prep(const XSrc& src, int M, int K, const uint16_t* gamma, float 
   const int nblk = K / 32;
   if (gamma == nullptr) {
     const dim3 g2((unsigned)((4 * (int64_t)M + 255) / 256), (unsigned)((nblk + 3) / 4));
-    k_prep_blocks<PAT, NV, RES><<<g2, block, 0, st>>>(src, M, K, o, S_ptr);
+    k_prep_blocks<PAT, NV, RES ? 1 : 0><<<g2, block, 0, st>>>(src, M, K, o, S_ptr);
     return;
   }
   if (nblk <= 256) {
@@ -1015,7 +1048,7 @@ template <bool RES>
 static void go_amax(const XSrc& src, int M, int K, const uint16_t* gamma, float eps, uint32_t* slot, dim3 grid,
                     hipStream_t st) {
   if (gamma == nullptr) {
-    k_amax_plain<RES><<<grid, 256, 0, st>>>(src, M, K, slot);
+    k_amax_plain<RES ? 1 : 0><<<grid, 256, 0, st>>>(src, M, K, slot);
     return;
   }
   const int chunks = (K / 32 + 63) / 64;
@@ -1131,6 +1164,41 @@ hipError_t launch_prep_hif4(const uint16_t* X, int M, int K, int64_t ldx, const 
     k_prep_hif4<true><<<grid, 256, 0, st>>>(src, M, K, gamma, eps, o);
   else
     k_prep_hif4<false><<<grid, 256, 0, st>>>(src, M, K, gamma, eps, o);
+  return hipGetLastError();
+}
+
+// Preparation of the down projection's input with SiLU.mul fused in front:
+// h = bf16(SiLU(gate) * up), written to h (when not NULL) and prepared
+// without RMSNorm.  nv: NVFP4 with the per-tensor scale from ts_in or from
+// an amax pre-pass over h.
+hipError_t launch_prep_silu(const uint16_t* gate, const uint16_t* up, uint16_t* h, int M, int K, int64_t ldg,
+                            int64_t ldu, int64_t ldh, int pat, bool nv, const float* ts_in, float* ts_out,
+                            uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, hipStream_t st) {
+  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K};
+  const XSrc src{gate, ldg, up, ldu, h, ldh};
+  const dim3 grid((unsigned)((M + 3) / 4));
+  if (nv) {
+    if (ts_in) {
+      k_copy_f32<<<1, 1, 0, st>>>(ts_in, ts_out);
+    } else {
+      uint32_t* slot = reinterpret_cast<uint32_t*>(ts_out);
+      k_store_u32<<<1, 1, 0, st>>>(slot, 0u);
+      k_amax_plain<2><<<grid, 256, 0, st>>>(src, M, K, slot);
+      k_pts_finalize<<<1, 1, 0, st>>>(slot);
+    }
+  }
+  const int nblk = K / 32;
+  const dim3 g2((unsigned)((4 * (int64_t)M + 255) / 256), (unsigned)((nblk + 3) / 4));
+  const float* S = nv ? ts_out : nullptr;
+  if (nv) {
+    if (pat == 24) k_prep_blocks<24, true, 2><<<g2, 256, 0, st>>>(src, M, K, o, S);
+    else if (pat == 49) k_prep_blocks<49, true, 2><<<g2, 256, 0, st>>>(src, M, K, o, S);
+    else k_prep_blocks<48, true, 2><<<g2, 256, 0, st>>>(src, M, K, o, S);
+  } else {
+    if (pat == 24) k_prep_blocks<24, false, 2><<<g2, 256, 0, st>>>(src, M, K, o, S);
+    else if (pat == 49) k_prep_blocks<49, false, 2><<<g2, 256, 0, st>>>(src, M, K, o, S);
+    else k_prep_blocks<48, false, 2><<<g2, 256, 0, st>>>(src, M, K, o, S);
+  }
   return hipGetLastError();
 }
 

@@ -73,6 +73,9 @@ def _load():
     L.sharq_prepare_residual.restype = ctypes.c_int
     L.sharq_prepare_residual.argtypes = [c_vp, c_vp, c_vp, ctypes.c_int, c_i64, c_i64, c_i64, c_i64, c_i64, c_vp, c_f,
                                          Pattern, ctypes.c_int, c_vp, ctypes.POINTER(ActStruct), c_vp]
+    L.sharq_prepare_silu_mul.restype = ctypes.c_int
+    L.sharq_prepare_silu_mul.argtypes = [c_vp, c_vp, c_vp, ctypes.c_int, c_i64, c_i64, c_i64, c_i64, c_i64, Pattern,
+                                         ctypes.c_int, c_vp, ctypes.POINTER(ActStruct), c_vp]
     L.sharq_linear.restype = ctypes.c_int
     L.sharq_linear.argtypes = [ctypes.POINTER(ActStruct), ctypes.POINTER(WeightStruct), c_vp, ctypes.c_int, c_i64,
                                c_vp]
@@ -226,6 +229,23 @@ def sharq_prepare_residual(x: torch.Tensor, residual: torch.Tensor, gamma: Optio
                                       Pattern(n, m, int(pairs)), f, _ptr(tensor_scale_in), ctypes.byref(st),
                                       _stream(stream)), "sharq_prepare_residual")
     return out, h_out
+
+
+def sharq_prepare_silu_mul(gate: torch.Tensor, up: torch.Tensor, n: int = 2, m: int = 4, fmt="mx",
+                           h_out: Optional[torch.Tensor] = None, tensor_scale_in: Optional[torch.Tensor] = None,
+                           out: Optional[PreparedAct] = None, stream=None, pairs: bool = False) -> PreparedAct:
+    """SiLU.mul fused into the preparation of a down projection's input:
+    h = bf16(SiLU(gate) * up) is prepared (and written to h_out when given)."""
+    M, K = gate.shape
+    if out is None:
+        out = alloc_act(M, K, n, m, fmt, gate.device, pairs)
+    f = _FMT[fmt] if isinstance(fmt, str) else fmt
+    st = out.struct()
+    _check(lib.sharq_prepare_silu_mul(_ptr(gate), _ptr(up), _ptr(h_out), _DT.get(gate.dtype, -1), M, K,
+                                      gate.stride(0), up.stride(0), h_out.stride(0) if h_out is not None else K,
+                                      Pattern(n, m, int(pairs)), f, _ptr(tensor_scale_in), ctypes.byref(st),
+                                      _stream(stream)), "sharq_prepare_silu_mul")
+    return out
 
 
 def sharq_linear(a: PreparedAct, w: QuantWeight, out: Optional[torch.Tensor] = None, dtype=torch.bfloat16,

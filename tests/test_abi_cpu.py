@@ -319,3 +319,21 @@ def test_hif4_rejections(L):
     # formats must agree between activation and weight
     wmx = Weight(64, 128, 1, 0, FAKE, FAKE, FAKE, None)
     assert L.sharq_linear(ctypes.byref(act(fmt=HIF4)), ctypes.byref(wmx), FAKE, 0, 64, None) == EINVAL
+
+
+def test_silu_mul_rejections(L):
+    L.sharq_prepare_silu_mul.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                         ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                         ctypes.c_int64, Pattern, ctypes.c_int, ctypes.c_void_p, ctypes.POINTER(Act),
+                                         ctypes.c_void_p]
+
+    def call(a, up=FAKE, h=None, ldu=128, ldh=128, fmt=0):
+        return L.sharq_prepare_silu_mul(FAKE, up, h, 0, a.rows, a.K, a.K, ldu, ldh, Pattern(a.nm.n, a.nm.m),
+                                        fmt, None, ctypes.byref(a), None)
+    assert call(act(), up=None) == EINVAL
+    assert call(act(), ldu=64) == EINVAL
+    assert call(act(), h=FAKE, ldh=64) == EINVAL
+    assert call(act(), h=FAKE + 8) == EALIGN
+    assert call(act(mode=DENSE)) == EUNSUPPORTED
+    assert call(act(fmt=HIF4), fmt=HIF4) == EUNSUPPORTED
+    assert call(act(rows=0), up=None) == OK

@@ -1,0 +1,115 @@
+"""SiLU.mul fused into the preparation of the down projection's input
+(producer-side fusion, Sec. 4.3), through the C ABI, against the CPU oracle.
+
+h = bf16(SiLU(g) * u) is computed in fp32 with the hardware exponential and
+reciprocal (~1 ulp each), so it must lie within one bf16 step of the oracle's
+exactly rounded value and equal it for almost every element; everything after
+h (mask, codes, metadata, scales, the NVFP4 per-tensor scale) must then match
+the oracle run on the device's h byte for byte."""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import sharq_oracle as O
+from paper_2606_26587_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def S():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_26587_amd import sharq
+    return sharq
+
+
+@pytest.fixture(scope="module")
+def G(S):
+    import gpu_util
+    return gpu_util
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def bf16_steps_apart(a_bits: np.ndarray, b_bits: np.ndarray) -> np.ndarray:
+    """Distance in bf16 steps between two bf16 bit patterns (sign-magnitude order)."""
+    def ordinal(b):
+        b = b.astype(np.int64)
+        return np.where(b & 0x8000, -(b & 0x7FFF), b & 0x7FFF)
+    return np.abs(ordinal(a_bits) - ordinal(b_bits))
+
+
+def check_silu(S, G, T, K, n, m, fmt, pairs, tag, strided=False, seed=0):
+    say(f"[silu] {tag} T={T} K={K} {n}:{m}{'p' if pairs else ''} {fmt} strided={strided}")
+    gate = synth.activations(T, K, seed=seed + 1)
+    up = synth.activations(T, K, seed=seed + 2)
+    if strided:   # the two halves of one [T, 2K] gate/up output
+        gu = G.dev_bf16(np.concatenate([gate, up], axis=1))
+        gd, ud = gu[:, :K], gu[:, K:]
+    else:
+        gd, ud = G.dev_bf16(gate), G.dev_bf16(up)
+    h = torch.empty((T, K), dtype=torch.bfloat16, device="cuda")
+    a = S.sharq_prepare_silu_mul(gd, ud, n, m, fmt, h_out=h, pairs=pairs)
+    b = S.sharq_prepare_silu_mul(gd, ud, n, m, fmt, pairs=pairs)     # without writing h
+    torch.cuda.synchronize()
+    h_gpu = G.host(h.view(torch.int16)).view(np.uint16)
+    h_ref = O.silu_mul_bf16(gate, up)
+    d = bf16_steps_apart(h_gpu, h_ref)
+    say(f"[silu] {tag}: {int((d > 0).sum())} of {d.size} h values one step from the exact rounding")
+    assert d.max() <= 1, (tag, int(d.max()))
+    assert (d > 0).mean() <= 0.01, (tag, float((d > 0).mean()))
+    o = O.prepare(h_gpu, None, 0.0, n, m, fmt, pairs=pairs)
+    if fmt == "nv":
+        for act in (a, b):
+            got = np.asarray(G.host(act.tensor_scale)[0], np.float32).view(np.uint32)
+            assert got == np.asarray(o["tensor_scale"], np.float32).view(np.uint32), tag
+    dev = O.act_to_device_layout(o)
+    for act in (a, b):
+        for name in O.ACT_BUFFERS:
+            G.assert_bytes_equal(f"{tag}:{name}", G.host(getattr(act, name)), dev[name])
+
+
+@pytest.mark.parametrize("T,K,n,m,pairs,fmt,strided", [
+    (8, 128, 2, 4, False, "mx", False),
+    (37, 416, 2, 4, False, "mx", True),
+    (19, 640, 4, 8, False, "mx", False),
+    (23, 1024, 4, 8, True, "nv", True),
+    (33, 3584, 2, 4, False, "nv", False),
+    (1, 14336, 2, 4, False, "mx", False),
+])
+def test_silu_mul_prep(S, G, T, K, n, m, pairs, fmt, strided):
+    check_silu(S, G, T, K, n, m, fmt, pairs, f"T{T}K{K}", strided=strided, seed=T)
+
+
+def test_silu_mul_llama_down_full_shape(S, G):
+    """The Llama-3.1-8B down projection's input at M = 2048 (K = 14336), from a
+    [2048, 28672] gate/up output, compared in full."""
+    check_silu(S, G, 2048, 14336, 2, 4, "mx", False, "llama-down", strided=True, seed=5)
+
+
+def test_silu_mul_then_linear(S, G):
+    """The fused preparation feeds the GEMM like any prepared activation."""
+    T, K, N = 64, 1024, 256
+    gate, up = synth.activations(T, K, seed=7), synth.activations(T, K, seed=8)
+    h = torch.empty((T, K), dtype=torch.bfloat16, device="cuda")
+    a = S.sharq_prepare_silu_mul(G.dev_bf16(gate), G.dev_bf16(up), 2, 4, "mx", h_out=h)
+    wq = S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=7)))
+    y = S.sharq_linear(a, wq, dtype=torch.float32)
+    torch.cuda.synchronize()
+    o = O.prepare(G.host(h.view(torch.int16)).view(np.uint16), None, 0.0, 2, 4, "mx")
+    wo = G.weight_to_oracle(wq)
+    ref, absd = O.linear(o, wo), O.linear_abs(o, wo)
+    assert O.gemm_gate_error(G.host(y), ref, absd) <= 1e-3
+
+
+def test_silu_mul_empty(S, G):
+    e = torch.empty((0, 256), dtype=torch.bfloat16, device="cuda")
+    a = S.sharq_prepare_silu_mul(e, e, 2, 4, "mx")
+    torch.cuda.synchronize()
+    assert a.rows == 0

@@ -517,3 +517,45 @@ def test_panel_layout_roundtrip_and_order(K):
     if K > 128:
         assert np.array_equal(flat[R * 64: R * 64 + 64 if K - 128 >= 128 else R * 64 + (K - 128) // 2],
                               a[0, 64: 128 if K - 128 >= 128 else 64 + (K - 128) // 2])
+
+
+# ----------------------------------------------------------------------------- SiLU.mul fused in front (R12)
+
+def _nearest_bf16_bits(x: float) -> int:
+    """The bf16 bit pattern nearest to a finite double (ties to the even
+    pattern), by search over the neighbours of its truncation."""
+    sign = 0x8000 if math.copysign(1.0, x) < 0 else 0
+    fx = Fraction(abs(x))
+    t = (int(np.array([abs(x)], np.float32).view(np.uint32)[0]) >> 16) & 0x7FFF
+    best = None
+    for c in range(max(t - 2, 0), t + 3):
+        v = Fraction(float(O.bf16_bits_to_f32(np.array([c], np.uint16))[0]))
+        key = (abs(v - fx), c & 1)
+        if best is None or key < best[0]:
+            best = (key, c)
+    return best[1] | sign
+
+
+def test_silu_mul_is_the_rounded_product():
+    rng = np.random.default_rng(12)
+    g = rng.standard_normal(300).astype(np.float32) * 4
+    u = rng.standard_normal(300).astype(np.float32) * 3
+    g[:8] = [0.0, -0.0, 100.0, -100.0, -88.7, 88.7, 1e-30, -1e-30]
+    u[:8] = [1.5, 2.0, -1.0, 3.0, 1.0, -2.0, 5.0, -5.0]
+    gb, ub = synth.f32_to_bf16_bits(g), synth.f32_to_bf16_bits(u)
+    h = O.silu_mul_bf16(gb[None], ub[None])[0]
+    gf, uf = O.bf16_bits_to_f32(gb), O.bf16_bits_to_f32(ub)
+    for i in range(300):
+        gi, ui = float(gf[i]), float(uf[i])
+        sig = 1.0 / (1.0 + math.exp(-gi)) if gi > -700 else 0.0
+        want = _nearest_bf16_bits(math.copysign(abs(gi * sig * ui), gi * ui) if gi * ui != 0 else
+                                  (gi * 0.5) * ui)
+        assert int(h[i]) == want, (i, gi, ui, hex(int(h[i])), hex(want))
+
+
+def test_prepare_silu_mul_is_prepare_of_h():
+    gate, up = synth.activations(6, 256, seed=1), synth.activations(6, 256, seed=2)
+    a = O.prepare_silu_mul(gate, up, 2, 4, "mx")
+    b = O.prepare(a["h"], None, 0.0, 2, 4, "mx")
+    for k in O.ACT_BUFFERS:
+        assert np.array_equal(a[k], b[k])
