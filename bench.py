@@ -20,6 +20,10 @@ Other workloads (--workload), one JSON line each:
                 NVFP4 with the 4:8 in-pairs backbone
   moe           Qwen3-30B-A3B expert layers, 4096 tokens, top-8 of 128 experts,
                 4:8 backbone, grouped GEMMs
+  llama-fused   the default step with the producer-side fusions of the data
+                flow: the residual add fused into the qkv and gate/up
+                preparations and SiLU.mul into the down projection's, whose
+                input is the gate/up GEMM's own output
   ablation      the path combinations (Sparse, plain FP4 RTN, Dense+Dense,
                 Sparse+Sparse, SharQ) on the Llama prefill linears, MXFP4 2:4
                 and NVFP4 4:8 in pairs, and SharQ with HiF4 2:4: time per step
@@ -380,6 +384,76 @@ def moe(args, torch, S, synth, dev, stream):
     return out
 
 
+def llama_fused(args, torch, S, synth, dev, stream):
+    """The Llama-3.1-8B prefill linears at M = 2048 with the producer-side
+    fusions of a transformer block's data flow: h = bf16(x + res) fused into
+    the RMSNorm preparation of qkv and of gate/up (h written back to the
+    residual stream in place), and h = bf16(SiLU(gate) * up) fused into the
+    down projection's preparation, read from the gate/up GEMM's output."""
+    def to_dev(u16):
+        return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    T, eps = T_TOKENS, synth.LLAMA_EPS
+    L = {}
+    for name, (K, N, norm) in synth.LLAMA_LINEARS.items():
+        L[name] = dict(K=K, N=N, norm=norm, w=S.sharq_quantize_weight(to_dev(synth.weight(N, K, seed=0))),
+                       g=to_dev(synth.gamma(K, seed=0)) if norm else None,
+                       act=S.alloc_act(T, K, 2, 4, "mx", dev),
+                       y=torch.empty((T, N), dtype=torch.bfloat16, device=dev))
+    H = synth.LLAMA_LINEARS["qkv"][0]
+    I = synth.LLAMA_LINEARS["down"][0]
+    x_in = [to_dev(synth.activations(T, H, seed=s)) for s in range(N_INPUT_SETS)]
+    attn = [to_dev(synth.activations(T, H, seed=10 + s)) for s in range(N_INPUT_SETS)]
+    res0 = to_dev(synth.activations(T, H, seed=20))
+    res = res0.clone()
+    torch.cuda.synchronize()
+
+    def step(i, mark):
+        j = i % N_INPUT_SETS
+        q, gu, dn = L["qkv"], L["gate_up"], L["down"]
+        if mark:
+            mark(0)
+        S.sharq_prepare_residual(x_in[j], res, q["g"], eps, 2, 4, "mx", h_out=res, out=q["act"], stream=stream)
+        if mark:
+            mark(1)
+        S.sharq_linear(q["act"], q["w"], out=q["y"], stream=stream)
+        if mark:
+            mark(2)
+        S.sharq_prepare_residual(attn[j], res, gu["g"], eps, 2, 4, "mx", h_out=res, out=gu["act"], stream=stream)
+        if mark:
+            mark(3)
+        S.sharq_linear(gu["act"], gu["w"], out=gu["y"], stream=stream)
+        if mark:
+            mark(4)
+        S.sharq_prepare_silu_mul(gu["y"][:, :I], gu["y"][:, I:], 2, 4, "mx", out=dn["act"], stream=stream)
+        if mark:
+            mark(5)
+        S.sharq_linear(dn["act"], dn["w"], out=dn["y"], stream=stream)
+        if mark:
+            mark(6)
+
+    ms_step, wall_ms, tm = run_steps(torch, stream, step, 6, args.steps, args.warmup)
+    flops = sum(gemm_flops(T, v["N"], v["K"]) for v in L.values())
+    # algorithmic bytes of the fused preparations: x and res read, h written
+    # (and gamma read) for the residual adds; gate and up read for SiLU.mul;
+    # the prepared activation written (0.9375 B per element at MXFP4 2:4)
+    b_res = 3 * 2.0 * T * H + 2.0 * H + 0.9375 * T * H
+    b_silu = 2 * 2.0 * T * I + 0.9375 * T * I
+    ops = {"prep_residual_qkv_us": tm.op_ms(0) * 1e3, "gemm_qkv_us": tm.op_ms(1) * 1e3,
+           "prep_residual_gate_up_us": tm.op_ms(2) * 1e3, "gemm_gate_up_us": tm.op_ms(3) * 1e3,
+           "prep_silu_mul_down_us": tm.op_ms(4) * 1e3, "gemm_down_us": tm.op_ms(5) * 1e3}
+    ops["prep_residual_GBps"] = b_res / (tm.op_ms(0) * 1e-3) / 1e9
+    ops["prep_silu_mul_GBps"] = b_silu / (tm.op_ms(4) * 1e-3) / 1e9
+    log(f"[bench] fused data flow {ms_step:.4f} ms/step: " + ", ".join(f"{k} {v:.1f}" for k, v in ops.items()))
+    out = base_record(args, "SharQ linear TFLOPS (fused prep+2 FP4 GEMMs), Llama-8B M=2048, fused data flow",
+                      flops / (ms_step * 1e-3) / 1e12, "TFLOP/s", ms_step, "mxfp4",
+                      {"workload": "Llama-3.1-8B prefill linears with the residual add fused into the qkv and "
+                                   "gate_up preparations and SiLU.mul fused into the down preparation (input = the "
+                                   "gate_up output); M=2048; 2:4; MXFP4; bf16 out", "tokens": T})
+    out["ops"] = ops
+    return out
+
+
 ABLATION_MODES = ["sharq", "sparse", "dense", "dense_dense", "sparse_sparse"]
 MODE_PATHS = {"sharq": 2, "sparse": 1, "dense": 1, "dense_dense": 2, "sparse_sparse": 2}
 
@@ -476,7 +550,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama-prefill",
                     choices=["llama-prefill", "llama-decode", "qwen-nvfp4", "llama-nvfp4-pairs", "moe",
-                             "ablation"])
+                             "ablation", "llama-fused"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=T_TOKENS)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
@@ -512,6 +586,8 @@ def main():
         print(json.dumps(qwen_nvfp4(args, torch, S, synth, dev, stream)), flush=True)
     elif args.workload == "llama-nvfp4-pairs":
         print(json.dumps(llama_nvfp4_pairs(args, torch, S, synth, dev, stream)), flush=True)
+    elif args.workload == "llama-fused":
+        print(json.dumps(llama_fused(args, torch, S, synth, dev, stream)), flush=True)
     elif args.workload == "ablation":
         for o in ablation(args, torch, S, synth, dev, stream):
             print(json.dumps(o), flush=True)
