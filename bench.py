@@ -72,11 +72,14 @@ def gemm_flops(T, N, K):
     return 4.0 * T * N * K
 
 
-def prep_bytes(T, K, norm, n=2, m=4, fmt="mx"):
+def prep_bytes(T, K, norm, n=2, m=4, fmt="mx", dense_backbone=False):
     """Algorithmic HBM bytes of one preparation call: bf16 X (and gamma) in;
     backbone codes K n/m/2, metadata K/8, backbone scales K/32, residual codes
-    K/2 and residual scales K/32 (MXFP4) or K/16 (NVFP4) out."""
+    K/2 and residual scales K/32 (MXFP4) or K/16 (NVFP4) out, and K/2 for the
+    dense backbone copy when it is written."""
     out = K * n / m / 2 + K / 8 + K / 32 + K / 2 + (K / 32 if fmt == "mx" else K / 16)
+    if dense_backbone:
+        out += K / 2
     return 2.0 * T * K + (2.0 * K if norm else 0.0) + T * out
 
 
@@ -174,7 +177,7 @@ def base_record(args, metric, value, unit, ms_step, dtype, config):
 # workloads
 # ---------------------------------------------------------------------------
 
-def dense_layers(torch, S, synth, dev, shapes, T, fmt, n, m, n_sets, pairs=False):
+def dense_layers(torch, S, synth, dev, shapes, T, fmt, n, m, n_sets, pairs=False, dense_backbone=False):
     def to_dev(u16):
         return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).to(dev)
     layers = []
@@ -182,7 +185,7 @@ def dense_layers(torch, S, synth, dev, shapes, T, fmt, n, m, n_sets, pairs=False
         xs = [to_dev(synth.activations(T, K, seed=s)) for s in range(n_sets)]
         g = to_dev(synth.gamma(K, seed=0)) if norm else None
         w = S.sharq_quantize_weight(to_dev(synth.weight(N, K, seed=0)), fmt)
-        acts = [S.alloc_act(T, K, n, m, fmt, dev, pairs) for _ in range(n_sets)]
+        acts = [S.alloc_act(T, K, n, m, fmt, dev, pairs, dense_backbone=dense_backbone) for _ in range(n_sets)]
         ys = [torch.empty((T, N), dtype=torch.bfloat16, device=dev) for _ in range(n_sets)]
         layers.append(dict(name=name, K=K, N=N, norm=norm, xs=xs, g=g, w=w, acts=acts, ys=ys))
     torch.cuda.synchronize()
@@ -204,12 +207,12 @@ def dense_step(S, layers, stream, eps, n, m, fmt, n_sets, pairs=False):
     return step
 
 
-def per_linear(layers, tm, T, fmt, n, m):
+def per_linear(layers, tm, T, fmt, n, m, dense_backbone=False):
     per = []
     for li, L in enumerate(layers):
         prep_ms, gemm_ms = tm.op_ms(2 * li), tm.op_ms(2 * li + 1)
         f = gemm_flops(T, L["N"], L["K"])
-        b = prep_bytes(T, L["K"], L["norm"], n, m, fmt)
+        b = prep_bytes(T, L["K"], L["norm"], n, m, fmt, dense_backbone)
         wb = weight_bytes(L["N"], L["K"], fmt)
         per.append({"linear": L["name"], "K": L["K"], "N": L["N"], "rmsnorm": L["norm"],
                     "prep_us": prep_ms * 1e3, "prep_bytes": b, "prep_GBps": b / (prep_ms * 1e-3) / 1e9,
@@ -222,12 +225,14 @@ def per_linear(layers, tm, T, fmt, n, m):
 
 
 def llama_prefill(args, torch, S, synth, dev, stream):
-    layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T_TOKENS, "mx", 2, 4, N_INPUT_SETS)
+    dense_bb = not args.compressed_backbone
+    layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T_TOKENS, "mx", 2, 4, N_INPUT_SETS,
+                          dense_backbone=dense_bb)
     log(f"[bench] set up {len(layers)} linears, M={T_TOKENS}")
     step = dense_step(S, layers, stream, synth.LLAMA_EPS, 2, 4, "mx", N_INPUT_SETS)
     ms_step, wall_ms, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
     log(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step (wall {wall_ms:.4f} ms/step)")
-    per = per_linear(layers, tm, T_TOKENS, "mx", 2, 4)
+    per = per_linear(layers, tm, T_TOKENS, "mx", 2, 4, dense_bb)
     flops_step = sum(p["gemm_flops"] for p in per)
     t_gemm = sum(p["gemm_us"] for p in per) * 1e-6
     t_prep = sum(p["prep_us"] for p in per) * 1e-6
@@ -242,8 +247,11 @@ def llama_prefill(args, torch, S, synth, dev, stream):
         {"workload": "Llama-3.1-8B prefill linears qkv (K4096,N6144,RMSNorm), gate_up (K4096,N28672,"
                      "RMSNorm), down (K14336,N4096); M=2048 tokens; 2:4 backbone; MXFP4; bf16 out",
          "tokens": T_TOKENS, "pattern": "2:4", "format": "MXFP4", "flops_per_step": flops_step,
+         "backbone_for_gemm": "dense copy written by the preparation" if dense_bb else "compressed, expanded in the GEMM",
          "flops_counting": "4*M*N*K per linear (two dense-executed FP4 GEMMs)"})
-    out["roofline"] = {"bound": "mfma", "kernel": "k_linear_mx_persist (two-path FP4 GEMM)", "achieved": gemm_tf,
+    kern = "k_linear_mx_persist<0> (two-path FP4 GEMM, dense backbone copy)" if dense_bb else \
+        "k_linear_mx_persist<24> (two-path FP4 GEMM, backbone expanded in registers)"
+    out["roofline"] = {"bound": "mfma", "kernel": kern, "achieved": gemm_tf,
                        "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s", "frac": gemm_tf / PEAK_FP4_TFLOPS,
                        "traffic": traffic, "flops_per_launch": flops_step / len(per),
                        "us_per_launch": t_gemm * 1e6 / len(per)}
@@ -398,7 +406,7 @@ def llama_fused(args, torch, S, synth, dev, stream):
     for name, (K, N, norm) in synth.LLAMA_LINEARS.items():
         L[name] = dict(K=K, N=N, norm=norm, w=S.sharq_quantize_weight(to_dev(synth.weight(N, K, seed=0))),
                        g=to_dev(synth.gamma(K, seed=0)) if norm else None,
-                       act=S.alloc_act(T, K, 2, 4, "mx", dev),
+                       act=S.alloc_act(T, K, 2, 4, "mx", dev, dense_backbone=True),
                        y=torch.empty((T, N), dtype=torch.bfloat16, device=dev))
     H = synth.LLAMA_LINEARS["qkv"][0]
     I = synth.LLAMA_LINEARS["down"][0]
@@ -552,6 +560,8 @@ def main():
                     choices=["llama-prefill", "llama-decode", "qwen-nvfp4", "llama-nvfp4-pairs", "moe",
                              "ablation", "llama-fused"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--compressed-backbone", action="store_true",
+                    help="prefill: let the GEMM expand the compressed backbone instead of reading the dense copy")
     ap.add_argument("--cpu-rows", type=int, default=T_TOKENS)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
     args = ap.parse_args()

@@ -147,6 +147,16 @@ typedef enum {
  *                             MXFP4: unused (may be NULL).
  *   mode                      SHARQ_MODE_SHARQ (0).
  *   dn_meta                   unused (may be NULL).
+ *   sp_dense [rows][K/2]      optional (NULL = none), MXFP4 only: the backbone's
+ *                             codes at all K positions (dropped positions
+ *                             code 0), laid out like dn_codes; 16-byte
+ *                             aligned.  When given, the preparation writes it
+ *                             beside the compressed form, and sharq_linear's
+ *                             main kernel reads it instead of expanding
+ *                             sp_codes / sp_meta: gfx950 has no sparse FP4
+ *                             matrix instruction, so the backbone runs dense
+ *                             anyway, and the copy (K/2 more bytes per row)
+ *                             takes the expansion out of every column tile.
  *
  * Other modes: path 1 lives in sp_codes / sp_meta / sp_scale and path 2 in
  * dn_codes / dn_meta / dn_scale.  A sparse path has the backbone layout above
@@ -168,6 +178,7 @@ typedef struct {
   float *tensor_scale;
   sharq_mode mode;
   uint8_t *dn_meta;
+  uint8_t *sp_dense;
 } sharq_act;
 
 /*

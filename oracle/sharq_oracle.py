@@ -711,6 +711,9 @@ def prepare(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: in
         out["sp_meta"] = np.zeros((T, 0), np.uint8)
     out.update(sp_scale=sp_s, dn_codes=pack_nibbles(dn_c), dn_scale=dn_s,
                d_sp=d_sp, R=R, d_dn=d_dn)
+    # the backbone's codes at every position (dropped positions code 0): the
+    # library's optional dense copy, in the residual codes' layout
+    out["sp_dense"] = pack_nibbles(sp_c)
     return out
 
 

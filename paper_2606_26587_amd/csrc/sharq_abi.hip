@@ -10,7 +10,7 @@ namespace sharq {
 hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* res, int64_t ldr, uint16_t* h,
                        int64_t ldh, const uint16_t* gamma, float eps, int pat, bool nv, const float* ts_in,
                        float* ts_out, uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns,
-                       hipStream_t st);
+                       uint8_t* spd, hipStream_t st);
 hipError_t launch_wquant_mx(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
                             hipStream_t st);
 hipError_t launch_wquant_nv(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
@@ -21,7 +21,7 @@ hipError_t launch_linear_nv(int pat, int ydt, const uint8_t* spc, const uint8_t*
                             hipStream_t st);
 hipError_t launch_linear_mx(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                             const uint8_t* dnc, const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws,
-                            int N, int K, void* Y, int64_t ldy, hipStream_t st);
+                            int N, int K, void* Y, int64_t ldy, const uint8_t* spd, hipStream_t st);
 hipError_t launch_prep_mode(int mode, const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps,
                             int pat, bool nv, const float* ts_in, float* ts_out, uint8_t* c1, uint8_t* m1,
                             uint8_t* s1, uint8_t* c2, uint8_t* m2, uint8_t* s2, hipStream_t st);
@@ -38,7 +38,8 @@ hipError_t launch_linear_hif4(int ydt, const uint8_t* spc, const uint8_t* spm, c
                               void* Y, int64_t ldy, hipStream_t st);
 hipError_t launch_prep_silu(const uint16_t* gate, const uint16_t* up, uint16_t* h, int M, int K, int64_t ldg,
                             int64_t ldu, int64_t ldh, int pat, bool nv, const float* ts_in, float* ts_out,
-                            uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, hipStream_t st);
+                            uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, uint8_t* spd,
+                            hipStream_t st);
 hipError_t launch_linear_mx_grouped(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                                     const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx, int64_t act_rows,
                                     const int32_t* offs, int E, int64_t total, const uint8_t* wc, const uint8_t* ws,
@@ -106,6 +107,8 @@ sharq_status check_act(const sharq_act* a) {
   if (k2 != kNone && (!a->dn_codes || !a->dn_scale)) return SHARQ_EINVAL;
   if (k2 == kSparse && !a->dn_meta) return SHARQ_EINVAL;
   if (a->fmt == SHARQ_NVFP4 && !a->tensor_scale) return SHARQ_EINVAL;
+  if (a->sp_dense && (a->fmt != SHARQ_MXFP4 || mode != SHARQ_MODE_SHARQ)) return SHARQ_EUNSUPPORTED;
+  if (!aligned(a->sp_dense, 16)) return SHARQ_EALIGN;
   if (!aligned(a->sp_codes, 16) || !aligned(a->dn_codes, 16) || !aligned(a->sp_meta, 4) ||
       !aligned(a->sp_scale, 4) || !aligned(a->dn_scale, 4) || !aligned(a->tensor_scale, 4) ||
       !aligned(a->dn_meta, 4))
@@ -248,7 +251,7 @@ sharq_status prepare_impl(int src, const void* X, const void* res, void* h_out, 
                                               static_cast<uint16_t*>(h_out), (int)M, (int)K, ldx, ldr, ldh, pid, nv,
                                               nv ? tensor_scale_in : nullptr, nv ? out->tensor_scale : nullptr,
                                               out->sp_codes, out->sp_meta, out->sp_scale, out->dn_codes,
-                                              out->dn_scale, reinterpret_cast<hipStream_t>(stream)));
+                                              out->dn_scale, out->sp_dense, reinterpret_cast<hipStream_t>(stream)));
   if (fmt == SHARQ_HIF4)
     return hip_status(sharq::launch_prep_hif4(static_cast<const uint16_t*>(X), (int)M, (int)K, ldx,
                                               static_cast<const uint16_t*>(gamma), eps, out->sp_codes, out->sp_meta,
@@ -267,7 +270,8 @@ sharq_status prepare_impl(int src, const void* X, const void* res, void* h_out, 
                                        static_cast<const uint16_t*>(res), ldr, static_cast<uint16_t*>(h_out), ldh,
                                        static_cast<const uint16_t*>(gamma), eps, pid, nv, nv ? tensor_scale_in : nullptr,
                                        nv ? out->tensor_scale : nullptr, out->sp_codes, out->sp_meta, out->sp_scale,
-                                       out->dn_codes, out->dn_scale, reinterpret_cast<hipStream_t>(stream)));
+                                       out->dn_codes, out->dn_scale, out->sp_dense,
+                                       reinterpret_cast<hipStream_t>(stream)));
 }
 
 }  // namespace
@@ -331,7 +335,7 @@ sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sh
                                               w->scale, w->tensor_scale, (int)w->N, (int)w->K, Y, ldy, st));
   return hip_status(sharq::launch_linear_mx(gemm_pattern(pattern_id(a->nm)), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale,
                                             a->dn_codes, a->dn_scale, a->rows, w->codes, w->scale, (int)w->N,
-                                            (int)w->K, Y, ldy, st));
+                                            (int)w->K, Y, ldy, a->sp_dense, st));
 }
 
 sharq_status sharq_linear_grouped(const sharq_act* a, const int32_t* row_index, const int32_t* expert_offsets,

@@ -167,6 +167,49 @@ __device__ __forceinline__ uint32_t enc8(const float* v, const Q& qz) {
 }
 
 // ---------------------------------------------------------------------------
+// Backbone expansion: compressed 32-position block -> 32 dense E2M1 nibbles
+// ---------------------------------------------------------------------------
+
+// One output dword (8 K positions) of an expanded block.
+// 2:4: byte g of `c` holds group g's two kept codes (lower K first); nibble g
+// of `meta` holds their positions i0 | i1 << 2.  Dword D covers groups 2D, 2D+1.
+// 4:8: bytes 2g, 2g+1 of `c` hold group g's four kept codes (ascending K);
+// byte g of `meta` is its keep mask.  Dword D is group D.
+template <int PAT, int D>
+__device__ __forceinline__ uint32_t expand_dw(uint2 c, uint32_t meta) {
+  const uint32_t cw = D < 2 ? c.x : c.y;
+  uint32_t r = 0u;
+  if (PAT == 24) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int g = 2 * D + h;
+      const uint32_t byte = (cw >> (8 * (g & 3))) & 0xFFu;
+      const uint32_t nib = (meta >> (4 * g)) & 0xFu;
+      r |= (byte & 0xFu) << (4 * (nib & 3u) + 16 * h);
+      r |= (byte >> 4) << (4 * (nib >> 2) + 16 * h);
+    }
+  } else {
+    uint32_t c16 = (cw >> (16 * (D & 1))) & 0xFFFFu;
+    const uint32_t mask = (meta >> (8 * D)) & 0xFFu;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      if ((mask >> p) & 1u) {
+        r |= (c16 & 0xFu) << (4 * p);
+        c16 >>= 4;
+      }
+    }
+  }
+  return r;
+}
+
+// A compressed 32-position block -> 32 dense E2M1 nibbles.
+template <int PAT>
+__device__ __forceinline__ uint4 expand_block(uint2 c, uint32_t meta) {
+  return make_uint4(expand_dw<PAT, 0>(c, meta), expand_dw<PAT, 1>(c, meta), expand_dw<PAT, 2>(c, meta),
+                    expand_dw<PAT, 3>(c, meta));
+}
+
+// ---------------------------------------------------------------------------
 // HiF4 (a three-level scaled 4-bit format; App. "HiFloat4 (HiF4) Data
 // Format"): units of 64 values along K; an E6M2 level-1 scale (6 exponent
 // bits, bias 48, 2 mantissa bits, normal values only, all-ones = NaN), one

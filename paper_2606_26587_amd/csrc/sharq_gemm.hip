@@ -34,49 +34,6 @@ constexpr int kLdsStride = 80;    // bytes per staged weight row (64 + 16 to spr
 constexpr int kSkinnyMaxM = 64;   // activation rows up to which the small-M kernel runs
 constexpr int kSkinnyMaxRowTiled = 256;   // ... and, when the main kernel has few tiles, up to this many
 
-// ---------------------------------------------------------------------------
-// Backbone expansion: compressed 32-position block -> 32 dense E2M1 nibbles
-// ---------------------------------------------------------------------------
-
-// One output dword (8 K positions) of an expanded block.
-// 2:4: byte g of `c` holds group g's two kept codes (lower K first); nibble g
-// of `meta` holds their positions i0 | i1 << 2.  Dword D covers groups 2D, 2D+1.
-// 4:8: bytes 2g, 2g+1 of `c` hold group g's four kept codes (ascending K);
-// byte g of `meta` is its keep mask.  Dword D is group D.
-template <int PAT, int D>
-__device__ __forceinline__ uint32_t expand_dw(uint2 c, uint32_t meta) {
-  const uint32_t cw = D < 2 ? c.x : c.y;
-  uint32_t r = 0u;
-  if (PAT == 24) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int g = 2 * D + h;
-      const uint32_t byte = (cw >> (8 * (g & 3))) & 0xFFu;
-      const uint32_t nib = (meta >> (4 * g)) & 0xFu;
-      r |= (byte & 0xFu) << (4 * (nib & 3u) + 16 * h);
-      r |= (byte >> 4) << (4 * (nib >> 2) + 16 * h);
-    }
-  } else {
-    uint32_t c16 = (cw >> (16 * (D & 1))) & 0xFFFFu;
-    const uint32_t mask = (meta >> (8 * D)) & 0xFFu;
-#pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      if ((mask >> p) & 1u) {
-        r |= (c16 & 0xFu) << (4 * p);
-        c16 >>= 4;
-      }
-    }
-  }
-  return r;
-}
-
-// A compressed 32-position block -> 32 dense E2M1 nibbles.
-template <int PAT>
-__device__ __forceinline__ uint4 expand_block(uint2 c, uint32_t meta) {
-  return make_uint4(expand_dw<PAT, 0>(c, meta), expand_dw<PAT, 1>(c, meta), expand_dw<PAT, 2>(c, meta),
-                    expand_dw<PAT, 3>(c, meta));
-}
-
 __device__ __forceinline__ v8i as_operand(uint4 q) {
   v8i v;
   v[0] = (int)q.x; v[1] = (int)q.y; v[2] = (int)q.z; v[3] = (int)q.w;
@@ -93,6 +50,7 @@ struct AStep {
   uint2 spc[2];      // compressed backbone codes
   uint32_t spm[2];   // backbone metadata
   uint32_t sdn, ssp; // E8M0 scales of the step's 4 blocks (byte j = block 4 ks + j)
+  uint4 spd[2];      // the dense backbone codes instead (pattern 0: a dense copy was prepared)
 };
 
 // Activation rows live in panel-major buffers: K is cut into panels of 128
@@ -452,6 +410,7 @@ __device__ __forceinline__ uint32_t exp_piece(const AStep& r) {
 
 template <int PAT, int Q>
 __device__ __forceinline__ void put_piece(AOps& o, const AStep& r, const uint2 (&sel)[8]) {
+  if (PAT == 0) return;   // the backbone arrives dense
   constexpr int B = Q / 8, D = (Q % 8) / 2, H = Q % 2;
   uint32_t& d = D == 0 ? o.sp[B].x : D == 1 ? o.sp[B].y : D == 2 ? o.sp[B].z : o.sp[B].w;
   if (PAT == 48) {
@@ -602,6 +561,10 @@ __device__ __forceinline__ void step5(v16f (&acc)[8], const AOps& ops, uint4 (&b
   mma_dn<1, 7>(acc, ops, b1, bw);
   opsn.ssp = raw.ssp >> (16 * half);
   opsn.sdn = raw.sdn >> (16 * half);
+  if (PAT == 0) {
+    opsn.sp[0] = raw.spd[0];
+    opsn.sp[1] = raw.spd[1];
+  }
   SHARQ_FENCE();
 }
 
@@ -617,14 +580,22 @@ __device__ __forceinline__ void load_a_dn(AOps& o, const ARow& a, int ks, int ha
   o.dn[1] = *reinterpret_cast<const uint4*>(dn + 16);
 }
 
+// PAT 0: a.spc is the dense backbone copy, laid out like the residual codes.
+template <int PAT>
 __device__ __forceinline__ void load_a_meta(AStep& s, const ARow& a, int ks, int half) {
   const int64_t pr = (int64_t)ks * a.R;
-  const uint4 c = *reinterpret_cast<const uint4*>(a.spc + pr * 32 + a.r * 32 + 16 * half);
-  const uint2 m = *reinterpret_cast<const uint2*>(a.spm + pr * 16 + a.r * 16 + 8 * half);
-  s.spc[0] = make_uint2(c.x, c.y);
-  s.spc[1] = make_uint2(c.z, c.w);
-  s.spm[0] = m.x;
-  s.spm[1] = m.y;
+  if (PAT == 0) {
+    const uint8_t* sp = a.spc + pr * 64 + a.r * 64 + 32 * half;
+    s.spd[0] = *reinterpret_cast<const uint4*>(sp);
+    s.spd[1] = *reinterpret_cast<const uint4*>(sp + 16);
+  } else {
+    const uint4 c = *reinterpret_cast<const uint4*>(a.spc + pr * 32 + a.r * 32 + 16 * half);
+    const uint2 m = *reinterpret_cast<const uint2*>(a.spm + pr * 16 + a.r * 16 + 8 * half);
+    s.spc[0] = make_uint2(c.x, c.y);
+    s.spc[1] = make_uint2(c.z, c.w);
+    s.spm[0] = m.x;
+    s.spm[1] = m.y;
+  }
   s.sdn = *reinterpret_cast<const uint32_t*>(a.dns + pr * 4 + a.r * 4);
   s.ssp = *reinterpret_cast<const uint32_t*>(a.sps + pr * 4 + a.r * 4);
 }
@@ -723,18 +694,23 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
   uint8_t* const st2 = lds + 2 * kStageBytes;
   const auto cl = [&](int k) { return k < last ? k : last; };
   load_w<NF, true>(w0, wc, ws, n0, N, K, 0, nblk);
-  load_a_meta(r0, a, 0, half);
+  load_a_meta<PAT>(r0, a, 0, half);
   load_a_dn(o0, a, 0, half);
   load_w<NF, true>(w1, wc, ws, n0, N, K, cl(1), nblk);
   store_w_stage(w0, st0);
   store_w_stage(w1, st1);
-  o0.sp[0] = expand_block<PAT>(r0.spc[0], r0.spm[0]);
-  o0.sp[1] = expand_block<PAT>(r0.spc[1], r0.spm[1]);
+  if (PAT == 0) {
+    o0.sp[0] = r0.spd[0];
+    o0.sp[1] = r0.spd[1];
+  } else {
+    o0.sp[0] = expand_block<PAT>(r0.spc[0], r0.spm[0]);
+    o0.sp[1] = expand_block<PAT>(r0.spc[1], r0.spm[1]);
+  }
   o0.ssp = r0.ssp >> (16 * half);
   o0.sdn = r0.sdn >> (16 * half);
   load_a_dn(o1, a, cl(1), half);
-  load_a_meta(r1, a, cl(1), half);
-  load_a_meta(r2, a, cl(2), half);
+  load_a_meta<PAT>(r1, a, cl(1), half);
+  load_a_meta<PAT>(r2, a, cl(2), half);
   load_w<NF, true>(w2, wc, ws, n0, N, K, cl(2), nblk);
   load_w<NF, true>(w0, wc, ws, n0, N, K, cl(3), nblk);
   __syncthreads();
@@ -745,19 +721,19 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
   for (; ks + 2 < nks; ks += 3) {
     step5<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [&] {
       load_a_dn(o2, a, cl(ks + 2), half);
-      load_a_meta(r0, a, cl(ks + 3), half);
+      load_a_meta<PAT>(r0, a, cl(ks + 3), half);
       load_w<NF, true>(w1, wc, ws, n0, N, K, cl(ks + 4), nblk);
     }, lut);
     __syncthreads();
     step5<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [&] {
       load_a_dn(o0, a, cl(ks + 3), half);
-      load_a_meta(r1, a, cl(ks + 4), half);
+      load_a_meta<PAT>(r1, a, cl(ks + 4), half);
       load_w<NF, true>(w2, wc, ws, n0, N, K, cl(ks + 5), nblk);
     }, lut);
     __syncthreads();
     step5<PAT>(acc, o2, b0, bwa, bwb, st2, st0, st1, o0, r0, w1, lane, [&] {
       load_a_dn(o1, a, cl(ks + 4), half);
-      load_a_meta(r2, a, cl(ks + 5), half);
+      load_a_meta<PAT>(r2, a, cl(ks + 5), half);
       load_w<NF, true>(w0, wc, ws, n0, N, K, cl(ks + 6), nblk);
     }, lut);
     __syncthreads();
@@ -2167,11 +2143,31 @@ static hipError_t go_linear_dt(int ydt, const uint8_t* spc, const uint8_t* spm, 
   return go_linear<NF, PAT, SDW, uint16_t>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
 }
 
+// The persistent interleaved kernel on a dense backbone copy (pattern 0).
+template <typename OutT>
+static hipError_t go_dense_backbone(const uint8_t* spd, const uint8_t* sps, const uint8_t* dnc, const uint8_t* dns,
+                                    int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K, void* Y,
+                                    int64_t ldy, hipStream_t st) {
+  const int gx = (N + 255) / 256, gy = (int)((M + kBM - 1) / kBM);
+  const int tiles = gx * gy, cus = device_cus();
+  k_linear_mx_persist<0, OutT><<<dim3((unsigned)(tiles < cus ? tiles : cus)), dim3(256), 0, st>>>(
+      spd, nullptr, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
+  return hipGetLastError();
+}
+
+// spd (optional): the backbone's dense copy; used by the main kernel (K a
+// multiple of 128, M beyond the small-M kernel's range), which then skips the
+// expansion.
 hipError_t launch_linear_mx(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                             const uint8_t* dnc, const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws,
-                            int N, int K, void* Y, int64_t ldy, hipStream_t st) {
+                            int N, int K, void* Y, int64_t ldy, const uint8_t* spd, hipStream_t st) {
   const bool sdw = (K % kBK) == 0;
   constexpr int NF = 8;
+  if (spd && sdw && !use_skinny(M, N, K)) {
+    if (ydt == 2) return go_dense_backbone<float>(spd, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+    if (ydt == 1) return go_dense_backbone<_Float16>(spd, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+    return go_dense_backbone<uint16_t>(spd, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  }
   if (use_skinny(M, N, K)) {
     return pat == 24 ? go_skinny_dt<24>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st)
                      : go_skinny_dt<48>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);

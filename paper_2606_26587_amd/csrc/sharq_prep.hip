@@ -254,10 +254,12 @@ __device__ __forceinline__ float absmax16(const float* v) {
 
 // Quantize and store one MXFP4 block: backbone + residual.  The group maximum
 // is always kept, so the backbone block max equals the block max of y.
+// spd (optional): the backbone's dense codes (16 bytes, dropped positions 0),
+// the GEMM-ready copy that spares the GEMM the expansion.
 template <int PAT>
 __device__ __forceinline__ void block_mx(const float (&y)[32], uint8_t* __restrict__ spc, uint8_t* __restrict__ spm,
                                          uint8_t* __restrict__ sps, uint8_t* __restrict__ dnc,
-                                         uint8_t* __restrict__ dns) {
+                                         uint8_t* __restrict__ dns, uint8_t* __restrict__ spd = nullptr) {
   const int e = mx_exponent(__float_as_uint(absmax32(y)));
   const MxQ qb = MxQ::make(e);
   uint32_t codes[2], meta;
@@ -278,6 +280,7 @@ __device__ __forceinline__ void block_mx(const float (&y)[32], uint8_t* __restri
   *sps = (uint8_t)(e + 127);
   *reinterpret_cast<uint4*>(dnc) = make_uint4(dn[0], dn[1], dn[2], dn[3]);
   *dns = (uint8_t)(er + 127);
+  if (spd) *reinterpret_cast<uint4*>(spd) = expand_block<PAT == 24 ? 24 : 48>(make_uint2(codes[0], codes[1]), meta);
 }
 
 // Quantize and store one NVFP4 block: E4M3 backbone scale per 32 positions,
@@ -345,10 +348,11 @@ struct ActOut {
   uint8_t *spc, *spm, *sps, *dnc, *dns;
   int64_t M;
   int K;
+  uint8_t* spd;   // MXFP4: the dense backbone copy, or NULL
 };
 
 struct BlockOut {
-  uint8_t *spc, *spm, *sps, *dnc, *dns;
+  uint8_t *spc, *spm, *sps, *dnc, *dns, *spd;
 };
 
 // Panel-major order is block-major order: block b of a row is block number
@@ -368,6 +372,7 @@ __device__ __forceinline__ BlockOut block_at(const ActOut& o, int64_t V) {
   r.spm = o.spm + V * 4;
   r.sps = o.sps + V;
   r.dns = o.dns + (NV ? V * 2 : V);
+  r.spd = o.spd ? o.spd + V * 16 : nullptr;
   return r;
 }
 
@@ -383,7 +388,7 @@ __device__ __forceinline__ void block_out_write(const float (&y)[32], const ActO
   if (NV)
     block_nv<PAT>(y, S, six_s, d.spc, d.spm, d.sps, d.dnc, d.dns);
   else
-    block_mx<PAT>(y, d.spc, d.spm, d.sps, d.dnc, d.dns);
+    block_mx<PAT>(y, d.spc, d.spm, d.sps, d.dnc, d.dns, d.spd);
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -638,7 +643,7 @@ __global__ __launch_bounds__(256) void k_prep_blocks(XSrc src, int M, int K, Act
   if (NV)
     block_nv<PAT>(y, S, six_s, d.spc, d.spm, d.sps, d.dnc, d.dns);
   else
-    block_mx<PAT>(y, d.spc, d.spm, d.sps, d.dnc, d.dns);
+    block_mx<PAT>(y, d.spc, d.spm, d.sps, d.dnc, d.dns, d.spd);
 }
 
 // ---------------------------------------------------------------------------
@@ -1078,8 +1083,8 @@ static void go_prep_pat(int pat, bool nv, const XSrc& src, int M, int K, const u
 hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* res, int64_t ldr, uint16_t* h,
                        int64_t ldh, const uint16_t* gamma, float eps, int pat, bool nv, const float* ts_in,
                        float* ts_out, uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns,
-                       hipStream_t st) {
-  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K};
+                       uint8_t* spd, hipStream_t st) {
+  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K, spd};
   const XSrc src{X, ldx, res, ldr, h, ldh};
   const dim3 grid((unsigned)((M + 3) / 4));
   if (nv) {
@@ -1173,8 +1178,9 @@ hipError_t launch_prep_hif4(const uint16_t* X, int M, int K, int64_t ldx, const 
 // an amax pre-pass over h.
 hipError_t launch_prep_silu(const uint16_t* gate, const uint16_t* up, uint16_t* h, int M, int K, int64_t ldg,
                             int64_t ldu, int64_t ldh, int pat, bool nv, const float* ts_in, float* ts_out,
-                            uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, hipStream_t st) {
-  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K};
+                            uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, uint8_t* spd,
+                            hipStream_t st) {
+  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K, spd};
   const XSrc src{gate, ldg, up, ldu, h, ldh};
   const dim3 grid((unsigned)((M + 3) / 4));
   if (nv) {

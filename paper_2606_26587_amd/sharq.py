@@ -41,7 +41,7 @@ class ActStruct(ctypes.Structure):
     _fields_ = [("rows", ctypes.c_int64), ("K", ctypes.c_int64), ("fmt", ctypes.c_int), ("nm", Pattern),
                 ("sp_codes", ctypes.c_void_p), ("sp_meta", ctypes.c_void_p), ("sp_scale", ctypes.c_void_p),
                 ("dn_codes", ctypes.c_void_p), ("dn_scale", ctypes.c_void_p), ("tensor_scale", ctypes.c_void_p),
-                ("mode", ctypes.c_int), ("dn_meta", ctypes.c_void_p)]
+                ("mode", ctypes.c_int), ("dn_meta", ctypes.c_void_p), ("sp_dense", ctypes.c_void_p)]
 
 
 class WeightStruct(ctypes.Structure):
@@ -125,13 +125,15 @@ class PreparedAct:
     pairs: bool = False
     mode: int = 0
     dn_meta: Optional[torch.Tensor] = None
+    sp_dense: Optional[torch.Tensor] = None   # MXFP4: the backbone's dense copy for the main GEMM
 
     def struct(self) -> ActStruct:
         return ActStruct(self.rows, self.K, self.fmt, Pattern(self.n, self.m, int(self.pairs)), self.sp_codes.data_ptr(),
                          self.sp_meta.data_ptr(), self.sp_scale.data_ptr(), self.dn_codes.data_ptr(),
                          self.dn_scale.data_ptr(),
                          None if self.tensor_scale is None else self.tensor_scale.data_ptr(), self.mode,
-                         None if self.dn_meta is None else self.dn_meta.data_ptr())
+                         None if self.dn_meta is None else self.dn_meta.data_ptr(),
+                         None if self.sp_dense is None else self.sp_dense.data_ptr())
 
 
 @dataclass
@@ -153,10 +155,12 @@ class QuantWeight:
 
 
 def alloc_act(rows: int, K: int, n: int = 2, m: int = 4, fmt="mx", device="cuda", pairs: bool = False,
-              mode="sharq") -> PreparedAct:
+              mode="sharq", dense_backbone: bool = False) -> PreparedAct:
     """Device buffers of a prepared activation (flat, panel-major; see include/sharq.h).
     pairs=True: n:m selection in pairs (4:8 in pairs).  mode: a key of MODES
-    (or its id); buffers a mode does not use are empty."""
+    (or its id); buffers a mode does not use are empty.  dense_backbone=True
+    (MXFP4): also the backbone's dense copy that the main GEMM reads without
+    expanding it."""
     f = _FMT[fmt] if isinstance(fmt, str) else fmt
     md = MODES[mode] if isinstance(mode, str) else int(mode)
     sizes = [lib.sharq_act_buffer_bytes_mode(rows, K, f, Pattern(n, m, int(pairs)), md, w) for w in range(6)]
@@ -165,7 +169,9 @@ def alloc_act(rows: int, K: int, n: int = 2, m: int = 4, fmt="mx", device="cuda"
         raise SharqError(EINVAL, "alloc_act")
     bufs = [torch.empty(sz, dtype=torch.uint8, device=device) for sz in sizes]
     ts = torch.empty(1, dtype=torch.float32, device=device) if f == NVFP4 else None
-    return PreparedAct(rows, K, f, n, m, *bufs[:5], tensor_scale=ts, pairs=pairs, mode=md, dn_meta=bufs[5])
+    spd = torch.empty(rows * K // 2, dtype=torch.uint8, device=device) if dense_backbone else None
+    return PreparedAct(rows, K, f, n, m, *bufs[:5], tensor_scale=ts, pairs=pairs, mode=md, dn_meta=bufs[5],
+                       sp_dense=spd)
 
 
 def alloc_weight(N: int, K: int, fmt="mx", experts: int = 1, device="cuda") -> QuantWeight:

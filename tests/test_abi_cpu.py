@@ -24,7 +24,7 @@ class Act(ctypes.Structure):
     _fields_ = [("rows", ctypes.c_int64), ("K", ctypes.c_int64), ("fmt", ctypes.c_int), ("nm", Pattern),
                 ("sp_codes", ctypes.c_void_p), ("sp_meta", ctypes.c_void_p), ("sp_scale", ctypes.c_void_p),
                 ("dn_codes", ctypes.c_void_p), ("dn_scale", ctypes.c_void_p), ("tensor_scale", ctypes.c_void_p),
-                ("mode", ctypes.c_int), ("dn_meta", ctypes.c_void_p)]
+                ("mode", ctypes.c_int), ("dn_meta", ctypes.c_void_p), ("sp_dense", ctypes.c_void_p)]
 
 
 class Weight(ctypes.Structure):
@@ -93,8 +93,8 @@ def test_buffer_sizes(L):
 FAKE = 1 << 20   # never dereferenced: every case below is rejected (or empty) before any launch
 
 
-def act(rows=8, K=128, n=2, m=4, fmt=0, off=0, pairs=0, mode=0, dn_meta=None):
-    return Act(rows, K, fmt, Pattern(n, m, pairs), FAKE + off, FAKE, FAKE, FAKE, FAKE, None, mode, dn_meta)
+def act(rows=8, K=128, n=2, m=4, fmt=0, off=0, pairs=0, mode=0, dn_meta=None, sp_dense=None):
+    return Act(rows, K, fmt, Pattern(n, m, pairs), FAKE + off, FAKE, FAKE, FAKE, FAKE, None, mode, dn_meta, sp_dense)
 
 
 @pytest.mark.parametrize("kw,M,K,ldx,nm,expect", [
@@ -337,3 +337,14 @@ def test_silu_mul_rejections(L):
     assert call(act(mode=DENSE)) == EUNSUPPORTED
     assert call(act(fmt=HIF4), fmt=HIF4) == EUNSUPPORTED
     assert call(act(rows=0), up=None) == OK
+
+
+def test_dense_backbone_copy_rejections(L):
+    def prep(a, fmt=0):
+        return L.sharq_prepare(FAKE, 0, a.rows, a.K, a.K, None, 1e-6, Pattern(a.nm.n, a.nm.m), fmt, None,
+                               ctypes.byref(a), None)
+    assert prep(act(sp_dense=FAKE + 8)) == EALIGN
+    nv = act(fmt=1, sp_dense=FAKE)
+    nv.tensor_scale = FAKE
+    assert prep(nv, fmt=1) == EUNSUPPORTED                             # NVFP4: the copy is MXFP4 only
+    assert prep(act(mode=SPARSE, sp_dense=FAKE)) == EUNSUPPORTED        # the method's combination only

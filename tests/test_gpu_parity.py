@@ -354,3 +354,36 @@ def test_moe_full_config(S, G):
         rows = ridx[lo:hi]
         assert hi - lo > 0 and np.abs(yh[lo:hi]).max() > 0, (e, lo, hi)
         gemm_check(yh[lo:hi], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), f"moe expert {e}")
+
+
+# --------------------------------------------------------------------------- dense backbone copy
+
+@pytest.mark.parametrize("T,K,N,use_gamma,n,m,pairs", [(256, 1024, 512, True, 2, 4, False),
+                                                       (300, 640, 300, True, 4, 8, False),
+                                                       (160, 2048, 256, False, 4, 8, True),
+                                                       (130, 416, 96, False, 2, 4, False),
+                                                       (40, 1024, 128, True, 2, 4, False)])
+def test_dense_backbone_copy(S, G, T, K, N, use_gamma, n, m, pairs):
+    """The optional dense backbone copy: byte-exact against the oracle's
+    backbone codes, and the main GEMM on it gives bit-identically the result
+    of expanding the compressed backbone (the MFMA operands are the same)."""
+    say(f"[dense-backbone] T={T} K={K} N={N} {n}:{m}{'p' if pairs else ''}")
+    x = synth.activations(T, K, seed=K + T)
+    g = synth.gamma(K, seed=3) if use_gamma else None
+    xd, gd = G.dev_bf16(x), (None if g is None else G.dev_bf16(g))
+    a = S.sharq_prepare(xd, gd, 1e-6, n, m, "mx", pairs=pairs, out=S.alloc_act(T, K, n, m, "mx", "cuda", pairs,
+                                                                                dense_backbone=True))
+    c = S.sharq_prepare(xd, gd, 1e-6, n, m, "mx", pairs=pairs)
+    wq = S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=N)))
+    yd = S.sharq_linear(a, wq, dtype=torch.float32)
+    yc = S.sharq_linear(c, wq, dtype=torch.float32)
+    yd16 = S.sharq_linear(a, wq, dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    o = O.prepare(x, g, 1e-6, n, m, "mx", pairs=pairs)
+    G.assert_bytes_equal("sp_dense", G.host(a.sp_dense), O.to_panels(o["sp_dense"], K))
+    for name in O.ACT_BUFFERS:
+        G.assert_bytes_equal(name, G.host(getattr(a, name)), G.host(getattr(c, name)))
+    assert torch.equal(yd, yc)
+    assert torch.equal(yd16, yd.to(torch.bfloat16))
+    wo = G.weight_to_oracle(wq)
+    gemm_check(G.host(yd), O.linear(o, wo), O.linear_abs(o, wo), f"dense-backbone T{T}")
