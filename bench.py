@@ -353,8 +353,8 @@ def moe(args, torch, S, synth, dev, stream):
                             for e in range(E)])
     ri = torch.from_numpy(ridx).to(dev)
     of = torch.from_numpy(offs).to(dev)
-    a1 = S.alloc_act(T, H, 4, 8, "mx", dev)
-    a2 = S.alloc_act(total, I, 4, 8, "mx", dev)
+    a1 = S.alloc_act(T, H, 4, 8, "mx", dev, dense_backbone=True)
+    a2 = S.alloc_act(total, I, 4, 8, "mx", dev, dense_backbone=True)
     y1 = torch.empty((total, 2 * I), dtype=torch.bfloat16, device=dev)
     y2 = torch.empty((total, H), dtype=torch.bfloat16, device=dev)
     torch.cuda.synchronize()

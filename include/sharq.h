@@ -151,9 +151,10 @@ typedef enum {
  *                             codes at all K positions (dropped positions
  *                             code 0), laid out like dn_codes; 16-byte
  *                             aligned.  When given, the preparation writes it
- *                             beside the compressed form, and sharq_linear's
- *                             main kernel reads it instead of expanding
- *                             sp_codes / sp_meta: gfx950 has no sparse FP4
+ *                             beside the compressed form, and the main
+ *                             kernels of sharq_linear and sharq_linear_grouped
+ *                             (K a multiple of 128) read it instead of
+ *                             expanding sp_codes / sp_meta: gfx950 has no sparse FP4
  *                             matrix instruction, so the backbone runs dense
  *                             anyway, and the copy (K/2 more bytes per row)
  *                             takes the expansion out of every column tile.

@@ -43,7 +43,7 @@ hipError_t launch_prep_silu(const uint16_t* gate, const uint16_t* up, uint16_t* 
 hipError_t launch_linear_mx_grouped(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                                     const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx, int64_t act_rows,
                                     const int32_t* offs, int E, int64_t total, const uint8_t* wc, const uint8_t* ws,
-                                    int N, int K, void* Y, int64_t ldy, hipStream_t st);
+                                    int N, int K, void* Y, int64_t ldy, const uint8_t* spd, hipStream_t st);
 }  // namespace sharq
 
 namespace {
@@ -359,7 +359,7 @@ sharq_status sharq_linear_grouped(const sharq_act* a, const int32_t* row_index, 
   return hip_status(sharq::launch_linear_mx_grouped(
       gemm_pattern(pattern_id(a->nm)), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale, a->dn_codes, a->dn_scale, row_index,
       a->rows, expert_offsets, (int)w->experts, total, w->codes, w->scale, (int)w->N, (int)w->K, Y, ldy,
-      reinterpret_cast<hipStream_t>(stream)));
+      a->sp_dense, reinterpret_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -2209,12 +2209,17 @@ static hipError_t go_grouped_dt(int ydt, const uint8_t* spc, const uint8_t* spm,
                                             st);
 }
 
+// spd (optional): the backbone's dense copy, read instead of expanding the
+// compressed backbone when K is a multiple of 128.
 hipError_t launch_linear_mx_grouped(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                                     const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx, int64_t act_rows,
                                     const int32_t* offs, int E, int64_t total, const uint8_t* wc, const uint8_t* ws,
-                                    int N, int K, void* Y, int64_t ldy, hipStream_t st) {
+                                    int N, int K, void* Y, int64_t ldy, const uint8_t* spd, hipStream_t st) {
   const bool sdw = (K % kBK) == 0;
   constexpr int NF = 8;
+  if (spd && sdw)
+    return go_grouped_dt<NF, 0, true>(ydt, spd, nullptr, sps, dnc, dns, ridx, act_rows, offs, E, total, wc, ws, N, K,
+                                      Y, ldy, st);
   if (pat == 24) {
     return sdw ? go_grouped_dt<NF, 24, true>(ydt, spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, total, wc, ws, N, K, Y,
                                              ldy, st)

@@ -387,3 +387,31 @@ def test_dense_backbone_copy(S, G, T, K, N, use_gamma, n, m, pairs):
     assert torch.equal(yd16, yd.to(torch.bfloat16))
     wo = G.weight_to_oracle(wq)
     gemm_check(G.host(yd), O.linear(o, wo), O.linear_abs(o, wo), f"dense-backbone T{T}")
+
+
+@pytest.mark.parametrize("T,E,topk,K,N", [(300, 5, 3, 512, 200), (700, 16, 4, 768, 256)])
+def test_grouped_dense_backbone(S, G, T, E, topk, K, N):
+    """The grouped GEMM on the dense backbone copy: bit-identical to expanding
+    the compressed backbone, and within the gate of the oracle."""
+    say(f"[grouped-dense] T={T} E={E} top{topk} K={K} N={N}")
+    x = synth.activations(T, K, seed=E + 1)
+    xd, gd = G.dev_bf16(x), G.dev_bf16(synth.gamma(K, seed=E))
+    a = S.sharq_prepare(xd, gd, 1e-6, 4, 8, "mx", out=S.alloc_act(T, K, 4, 8, "mx", "cuda", dense_backbone=True))
+    c = S.sharq_prepare(xd, gd, 1e-6, 4, 8, "mx")
+    w = S.stack_weights([S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=200 + e))) for e in range(E)])
+    row_index, offs = synth.router_topk(T, E, topk, seed=E)
+    total = int(offs[-1])
+    ri, of = torch.from_numpy(row_index).cuda(), torch.from_numpy(offs).cuda()
+    yd = S.sharq_linear_grouped(a, ri, of, total, w, dtype=torch.float32)
+    yc = S.sharq_linear_grouped(c, ri, of, total, w, dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(yd, yc)
+    o = G.act_to_oracle(c)
+    wos = [G.weight_to_oracle(w, e) for e in range(E)]
+    ref = O.linear_grouped(o, row_index, offs, wos)
+    yabs = np.zeros_like(ref)
+    for e in range(E):
+        lo, hi = offs[e], offs[e + 1]
+        if hi > lo:
+            yabs[lo:hi] = O.linear_abs(o, wos[e], rows=row_index[lo:hi])
+    gemm_check(G.host(yd), ref, yabs, f"grouped-dense T{T}E{E}")
