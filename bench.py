@@ -55,12 +55,12 @@ PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
 T_TOKENS = 2048
 N_INPUT_SETS = 2              # activations rotate between steps (defeats the 256 MB last-level cache)
 
-# HBM traffic of the dominant kernel (k_linear_mx_persist at the default workload,
+# HBM traffic of the dominant kernel (k_linear_mx_persist<0>, the default workload with the dense backbone copy,
 # mean over its three launch shapes), from two rocprofv3 --pmc runs
 # (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors a plain 1 GiB device copy
 # gives).  Valid only for the GEMM source it was measured on (sha256 prefix);
 # reported as null once that source has changed.
-TRAFFIC = {"gemm_source": "5c00082e57db1425", "bytes_per_launch": 261.54e6}
+TRAFFIC = {"gemm_source": "f44c82980a8bf86f", "bytes_per_launch": 270.24e6}
 
 
 def log(*a):
