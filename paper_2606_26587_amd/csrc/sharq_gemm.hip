@@ -9,14 +9,18 @@
 // ONE fp32 accumulator; Y is written once.
 //
 // gfx950 has no sparse MFMA for FP4 operands (the sparse smfmac forms take
-// 8/16-bit inputs only), so the compressed 2:4 or 4:8 backbone is expanded to
-// dense E2M1 nibbles before it enters the MFMA.  The expansion is done in the
-// registers of the wavefront that owns the rows: each wavefront owns 32
-// distinct rows of the 128-row tile, so every compressed row is expanded
-// exactly once per tile and never goes through LDS.  The shared weight tile
-// (E2M1 payload + E8M0 scales) is staged through double-buffered LDS once per
-// K step and read by both MFMAs of every fragment.
-//
+// 8/16-bit inputs only), so the 2:4 or 4:8 backbone enters the MFMA as dense
+// E2M1 nibbles with zeros at the dropped positions: either expanded from its
+// compressed form in the registers of the wavefront that owns the rows (each
+// wavefront owns 32 distinct rows of the 128-row tile, so a row is expanded
+// once per tile and never goes through LDS), or read from the dense copy the
+// preparation wrote (pattern 0), which spares every column tile the
+// expansion.  The shared weight tile (E2M1 payload + E8M0 scales) is staged
+// through LDS once per K step and read by both MFMAs of every fragment.
+// Also here: the small-M kernel for decode, the grouped (MoE) form, the
+// NVFP4 and HiF4 kernels on bf16 MFMA over exactly dequantized operands, and
+// the generic kernels of the ablation path combinations.
+
 // MFMA 32x32x64 FP4 operand layout (lane l, 64-wide wavefront): lane l holds
 // row (l % 32) and the 32 K values of block (l / 32) of the 64-wide K slice as
 // 32 nibbles in its first four dwords (lower K in the lower nibble); its

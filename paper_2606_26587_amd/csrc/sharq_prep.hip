@@ -1,12 +1,14 @@
 // Fused SharQ activation preparation for gfx950 (SharQ Sec. 3.4, "Fused
 // sparse-residual preparation"; Fig. 2).
 //
-// One wavefront per activation row.  Lane l owns whole 32-element blocks
-// b = l, l + 64, l + 128, ... of its row, so every block-local step (N:M
-// selection inside groups of 4 or 8, the block max behind each scale, the
-// residual) runs inside one lane without cross-lane traffic; only the RMSNorm
-// sum of squares crosses lanes.  Every row is read from HBM once and every
-// output byte is written once.
+// Every 32-element block is handled by one lane, so every block-local step
+// (N:M selection inside groups of 4 or 8, the block max behind each scale, the
+// residual) runs inside that lane without cross-lane traffic; only the RMSNorm
+// sum of squares crosses lanes (and, for HiF4, a unit's maximum crosses a lane
+// pair).  With RMSNorm a row is spread over 1, 2 or 4 wavefronts (or held as
+// several blocks per lane for long rows); without it, one thread takes one
+// block.  Every row is read from HBM once and every output byte is written
+// once.
 //
 // Per block of 32 normalized values y (eq. numbers of Sec. 3.3):
 //   mask     keep the n largest |y| of each group of m, ties to the lower index
