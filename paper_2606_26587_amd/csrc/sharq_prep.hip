@@ -138,6 +138,46 @@ __device__ __forceinline__ void backbone_24(const float (&y)[32], const Q& qz, u
   }
 }
 
+// The 2:4 backbone together with its dense copy (codes at all 32 positions,
+// dropped positions code 0).  Converting the kept values in place, with +0 at
+// the dropped positions, gives the dense codes directly; decoding them gives
+// the residual at every position at once: y minus the dequantized code where
+// kept, y - 0 = y (signed zeros included) where dropped -- the same values as
+// backbone_24.  The compressed codes and metadata are those of backbone_24.
+template <class Q>
+__device__ __forceinline__ void backbone_24_dense(const float (&y)[32], const Q& qz, uint32_t (&codes)[2],
+                                                  uint32_t& meta, uint32_t (&dense)[4], float (&R)[32]) {
+  codes[0] = codes[1] = 0u;
+  meta = 0u;
+#pragma unroll
+  for (int g = 7; g >= 0; --g) {
+    const float y0 = y[4 * g], y1 = y[4 * g + 1], y2 = y[4 * g + 2], y3 = y[4 * g + 3];
+    lmask k0, k1, k2, k3;
+    top2of4(y0, y1, y2, y3, k0, k1, k2, k3);
+    const float v0 = lsel(k0, y0, lsel(k1, y1, y2));   // first kept (ascending K)
+    const float v1 = lsel(k3, y3, lsel(k2, y2, y1));   // second kept
+    meta = push_bit(meta, k3 | k2);
+    meta = push_bit(meta, k3 | ~k2);
+    meta = push_bit(meta, ~(k0 | k1));
+    meta = push_bit(meta, k1 & ~k0);
+    if ((g & 3) == 3) codes[g >> 2] = __float_as_uint(v0);
+    put_pair_dyn(qz, codes[g >> 2], g, v0, v1);
+    // group g is bytes 2 (g & 1) and 2 (g & 1) + 1 of dense dword g / 2; the
+    // odd group comes first in this loop and may start from any register
+    const float b0 = lsel(k0, y0, 0.0f), b1 = lsel(k1, y1, 0.0f);
+    const float b2 = lsel(k2, y2, 0.0f), b3 = lsel(k3, y3, 0.0f);
+    if (g & 1) dense[g >> 1] = __float_as_uint(b0);
+    put_pair_dyn(qz, dense[g >> 1], 2 * (g & 1), b0, b1);
+    put_pair_dyn(qz, dense[g >> 1], 2 * (g & 1) + 1, b2, b3);
+    const v2f d01 = get_pair_dyn(qz, dense[g >> 1], 2 * (g & 1));
+    const v2f d23 = get_pair_dyn(qz, dense[g >> 1], 2 * (g & 1) + 1);
+    R[4 * g + 0] = y0 - d01.x;
+    R[4 * g + 1] = y1 - d01.y;
+    R[4 * g + 2] = y2 - d23.x;
+    R[4 * g + 3] = y3 - d23.y;
+  }
+}
+
 // Backbone of one block for the 4:8 pattern (keep mask metadata).
 template <class Q>
 __device__ __forceinline__ void backbone_48(const float (&y)[32], const Q& qz, uint32_t (&codes)[2], uint32_t& meta,
@@ -266,12 +306,17 @@ __device__ __forceinline__ void block_mx(const float (&y)[32], uint8_t* __restri
   const MxQ qb = MxQ::make(e);
   uint32_t codes[2], meta;
   float R[32];
-  if (PAT == 24)
+  if (PAT == 24 && spd != nullptr) {
+    uint32_t dense[4];
+    backbone_24_dense(y, qb, codes, meta, dense, R);
+    *reinterpret_cast<uint4*>(spd) = make_uint4(dense[0], dense[1], dense[2], dense[3]);
+  } else if (PAT == 24) {
     backbone_24(y, qb, codes, meta, R);
-  else if (PAT == 49)
+  } else if (PAT == 49) {
     backbone_48p(y, qb, codes, meta, R);
-  else
+  } else {
     backbone_48(y, qb, codes, meta, R);
+  }
   const int er = mx_exponent(__float_as_uint(absmax32(R)));
   const MxQ qr = MxQ::make(er);
   uint32_t dn[4];
@@ -282,7 +327,7 @@ __device__ __forceinline__ void block_mx(const float (&y)[32], uint8_t* __restri
   *sps = (uint8_t)(e + 127);
   *reinterpret_cast<uint4*>(dnc) = make_uint4(dn[0], dn[1], dn[2], dn[3]);
   *dns = (uint8_t)(er + 127);
-  if (spd) *reinterpret_cast<uint4*>(spd) = expand_block<PAT == 24 ? 24 : 48>(make_uint2(codes[0], codes[1]), meta);
+  if (PAT != 24 && spd) *reinterpret_cast<uint4*>(spd) = expand_block<48>(make_uint2(codes[0], codes[1]), meta);
 }
 
 // Quantize and store one NVFP4 block: E4M3 backbone scale per 32 positions,
@@ -335,10 +380,37 @@ __device__ __forceinline__ float block_sum_sq(const float (&x)[32]) {
   return s[0];
 }
 
-__device__ __forceinline__ float wave_tree_sum(float v) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) v = v + __shfl_xor(v, m, 64);
+// Cross-lane exchanges on the VALU, no LDS.  Each stage adds the partner
+// group of lanes that an xor butterfly over lane masks 1, 2, 4, 8, 16, 32
+// would add: DPP quad permutes for 1 and 2; once the lanes of a quad (then of
+// a half row) agree, the row half-mirror and row mirror read a lane of the
+// partner quad (half row); gfx950's permlane16 / permlane32 swaps exchange
+// the rows of 16 and the halves of 32.  fp32 addition is commutative, so
+// every lane ends with the same balanced-tree sum as the butterfly.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+template <class Op>
+__device__ __forceinline__ float wave_reduce(float v, Op op) {
+  v = op(v, dpp_f32<0xB1>(v));    // quad_perm [1, 0, 3, 2]: lane ^ 1
+  v = op(v, dpp_f32<0x4E>(v));    // quad_perm [2, 3, 0, 1]: lane ^ 2
+  v = op(v, dpp_f32<0x141>(v));   // row_half_mirror: the other quad of 8
+  v = op(v, dpp_f32<0x140>(v));   // row_mirror: the other half of 16
+  {
+    const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = op(__uint_as_float(p[0]), __uint_as_float(p[1]));   // rows 2i and 2i + 1
+  }
+  {
+    const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = op(__uint_as_float(p[0]), __uint_as_float(p[1]));   // lanes 0-31 and 32-63
+  }
   return v;
+}
+
+__device__ __forceinline__ float wave_tree_sum(float v) {
+  return wave_reduce(v, [](float a, float b) { return a + b; });
 }
 
 // Output addressing.  Every buffer is panel-major: K is cut into panels of
@@ -394,9 +466,7 @@ __device__ __forceinline__ void block_out_write(const float (&y)[32], const ActO
 }
 
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
-  return v;
+  return wave_reduce(v, [](float a, float b) { return fmaxf(a, b); });
 }
 
 // The activation rows a preparation reads.  Without a residual input they
@@ -552,66 +622,48 @@ __global__ __launch_bounds__(256) void k_prep_norm(XSrc src, int M, int K, const
 // wavefront c owns blocks 64 c + lane, so each lane holds one block.  Each
 // wavefront reduces its 2048-position chunk with the in-lane tree and the
 // lane butterfly; the C chunk sums meet in LDS and are added pairwise -- the
-// same balanced tree as the one-wavefront-per-row kernel.  Workgroup w
-// handles row groups w, w + G, ... (G = grid size), loading the next group's
-// rows before quantizing the current one.
+// same balanced tree as the one-wavefront-per-row kernel.  One group of 4 / C
+// rows per workgroup: load, reduce, quantize, store, with no loop-carried
+// state (a persistent form that prefetched the next group measured slower).
 template <int C, int PAT, bool NV, bool RES>
 __global__ __launch_bounds__(256) void k_prep_norm_split(XSrc src, int M, int K, const uint16_t* __restrict__ gamma,
                                                          float eps, ActOut o, const float* S_ptr) {
-  __shared__ float part[2][4];
-  constexpr int RPG = 4 / C;   // rows per group (one group per workgroup pass)
+  __shared__ float part[4];
+  constexpr int RPG = 4 / C;   // rows per workgroup
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int nblk = K / 32, b = (wave % C) * 64 + lane;
-  const int groups = (M + RPG - 1) / RPG;
   const float S = NV ? *S_ptr : 1.0f, six_s = 6.0f * S;
+  int64_t row = (int64_t)blockIdx.x * RPG + wave / C;
+  const bool real = row < M;
+  if (!real) row = M - 1;   // loads stay in bounds; only real rows store
+  // lanes past the row's last block (K < 64 C blocks) read that block again
+  // and add 0 to the sum; they store nothing
+  const bool live = b < nblk;
+  const int bl = live ? b : nblk - 1;
+  uint4 gq[4], xq[4];
+  // the gamma block is loaded with the row, before the reduction, so that its
+  // latency is not on the path after it
   const uint4* gr = reinterpret_cast<const uint4*>(gamma);
-
-  auto load = [&](int grp, uint4 (&q)[4]) {
-    int64_t row = (int64_t)grp * RPG + wave / C;
-    const bool real = row < M;
-    if (!real) row = M - 1;   // loads stay in bounds; only real rows store h
-    if (b < nblk) {
-      load_block<RES>(src, row, b, q, real);
-    } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) q[j] = make_uint4(0u, 0u, 0u, 0u);
-    }
-  };
-
-  // this lane's gamma block, loaded once with the first rows so that its
-  // latency is not on the path after the reduction
-  uint4 gq[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) gq[j] = b < nblk ? gr[4 * b + j] : make_uint4(0u, 0u, 0u, 0u);
-  uint4 xq[4], xn[4];
-  int grp = blockIdx.x;
-  if (grp < groups) load(grp, xq);
-  for (int it = 0; grp < groups; grp += gridDim.x, ++it) {
-    const int nxt = grp + gridDim.x;
-    if (nxt < groups) load(nxt, xn);
-    float x[32];
-    unpack_bf16x32(xq, x);
-    const float cs = wave_tree_sum(block_sum_sq(x));
-    float total = cs;
-    if (C > 1) {
-      // two alternating slots: a wavefront may write the next pass's sums
-      // while a slower one still reads this pass's
-      if (lane == 0) part[it & 1][wave] = cs;
-      __syncthreads();
-      const int base = (wave / C) * C;
-      const float* pp = part[it & 1];
-      if (C == 2) total = pp[base] + pp[base + 1];
-      else total = (pp[base] + pp[base + 1]) + (pp[base + 2] + pp[base + 3]);
-    }
-    const float r = (float)(1.0 / __builtin_sqrt((double)total / (double)K + (double)eps));
-    const int64_t row = (int64_t)grp * RPG + wave / C;
-    if (row < M && b < nblk) {
-      float y[32];
-      norm_block(xq, gq, r, y);
-      block_out_write<PAT, NV>(y, o, row, b, S, six_s);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) xq[j] = xn[j];
+  for (int j = 0; j < 4; ++j) gq[j] = gr[4 * bl + j];
+  load_block<RES>(src, row, bl, xq, real && live);
+  float x[32];
+  unpack_bf16x32(xq, x);
+  const float bs = block_sum_sq(x);
+  const float cs = wave_tree_sum(live ? bs : 0.0f);
+  float total = cs;
+  if (C > 1) {
+    if (lane == 0) part[wave] = cs;
+    __syncthreads();
+    const int base = (wave / C) * C;
+    if (C == 2) total = part[base] + part[base + 1];
+    else total = (part[base] + part[base + 1]) + (part[base + 2] + part[base + 3]);
+  }
+  const float r = (float)(1.0 / __builtin_sqrt((double)total / (double)K + (double)eps));
+  if (real && live) {
+    float y[32];
+    norm_block(xq, gq, r, y);
+    block_out_write<PAT, NV>(y, o, row, b, S, six_s);
   }
 }
 
@@ -1015,11 +1067,6 @@ __global__ __launch_bounds__(256) void k_prep_hif4(XSrc src, int M, int K, const
 // Host-side launchers (called from the C ABI after validation)
 // ---------------------------------------------------------------------------
 
-// Workgroups of the RMSNorm kernel.  Measured at M = 2048: one row group per
-// workgroup is fastest (walking 2 or 4 groups per workgroup with a prefetch
-// was slower), so workgroups only iterate beyond 16 per CU.
-constexpr int kPersistWG = 4096;
-
 template <int PAT, bool NV, bool RES>
 static void go_prep(const XSrc& src, int M, int K, const uint16_t* gamma, float eps, const ActOut& o,
                     const float* S_ptr, dim3 grid, hipStream_t st) {
@@ -1031,10 +1078,8 @@ static void go_prep(const XSrc& src, int M, int K, const uint16_t* gamma, float 
     return;
   }
   if (nblk <= 256) {
-    // persistent: at most kPersistWG workgroups, each walking row groups
     const int C = nblk <= 64 ? 1 : (nblk <= 128 ? 2 : 4);
-    const int groups = (M + 4 / C - 1) / (4 / C);
-    const dim3 g1((unsigned)(groups < kPersistWG ? groups : kPersistWG));
+    const dim3 g1((unsigned)((M + 4 / C - 1) / (4 / C)));
     if (C == 1) k_prep_norm_split<1, PAT, NV, RES><<<g1, block, 0, st>>>(src, M, K, gamma, eps, o, S_ptr);
     else if (C == 2) k_prep_norm_split<2, PAT, NV, RES><<<g1, block, 0, st>>>(src, M, K, gamma, eps, o, S_ptr);
     else k_prep_norm_split<4, PAT, NV, RES><<<g1, block, 0, st>>>(src, M, K, gamma, eps, o, S_ptr);
