@@ -433,14 +433,16 @@ __device__ __forceinline__ void put_piece(AOps& o, const AStep& r, const uint2 (
 // the accumulator is the transposed tile: lane l holds activation row
 // l % 32 and, in element r, output column 8 (r / 4) + 4 (l / 32) + r % 4 of
 // the fragment -- four consecutive columns per group of four elements.
-template <int SUB, int F>
-__device__ __forceinline__ void mma_sp(v16f (&acc)[8], const AOps& a, const uint4 (&b)[8], const uint32_t (&bw)[4]) {
+template <int SUB, int F, int NF>
+__device__ __forceinline__ void mma_sp(v16f (&acc)[NF], const AOps& a, const uint4 (&b)[NF],
+                                       const uint32_t (&bw)[NF / 2]) {
   acc[F] = mfma_fp4<(F & 1) ? 2 + SUB : SUB, SUB>(as_operand(b[F]), as_operand(a.sp[SUB]), acc[F], bw[F >> 1],
                                                  a.ssp);
 }
 
-template <int SUB, int F>
-__device__ __forceinline__ void mma_dn(v16f (&acc)[8], const AOps& a, const uint4 (&b)[8], const uint32_t (&bw)[4]) {
+template <int SUB, int F, int NF>
+__device__ __forceinline__ void mma_dn(v16f (&acc)[NF], const AOps& a, const uint4 (&b)[NF],
+                                       const uint32_t (&bw)[NF / 2]) {
   acc[F] = mfma_fp4<(F & 1) ? 2 + SUB : SUB, SUB>(as_operand(b[F]), as_operand(a.dn[SUB]), acc[F], bw[F >> 1],
                                                  a.sdn);
 }
@@ -476,8 +478,8 @@ struct Vec4Out<_Float16> {
   static constexpr int kAlign = 8;
 };
 
-template <int SUB, int F0, int F1>
-__device__ __forceinline__ void read_b(uint4 (&b)[8], const uint8_t* lw, int lane) {
+template <int SUB, int F0, int F1, int NB>
+__device__ __forceinline__ void read_b(uint4 (&b)[NB], const uint8_t* lw, int lane) {
   const int half = lane >> 5, col = lane & 31;
 #pragma unroll
   for (int f = F0; f < F1; ++f)
@@ -488,6 +490,13 @@ __device__ __forceinline__ void read_bw(uint32_t (&bw)[4], const uint8_t* stage,
   const int half = lane >> 5, col = lane & 31;
   const uint4 q = *reinterpret_cast<const uint4*>(stage + kStageW + (2 * col + half) * 16);
   bw[0] = q.x; bw[1] = q.y; bw[2] = q.z; bw[3] = q.w;
+}
+
+// half tiles (fragments 0-3): the first 8 bytes of the record
+__device__ __forceinline__ void read_bw(uint32_t (&bw)[2], const uint8_t* stage, int lane) {
+  const int half = lane >> 5, col = lane & 31;
+  const uint2 q = *reinterpret_cast<const uint2*>(stage + kStageW + (2 * col + half) * 16);
+  bw[0] = q.x; bw[1] = q.y;
 }
 
 // One K step k.  In: b0 / bw = sub-step 0 weight operands and scale records
@@ -572,6 +581,62 @@ __device__ __forceinline__ void step5(v16f (&acc)[8], const AOps& ops, uint4 (&b
   SHARQ_FENCE();
 }
 
+// The same K step for a half tile (128 output columns, fragments 0-3): 16
+// MFMA slots.  The weight stage keeps the full tile's layout with rows 0-127
+// (and bytes 0-7 of each scale record) filled, so the operand reads are the
+// full tile's; the extra work per slot is about twice as dense.
+template <int PAT, class Issue>
+__device__ __forceinline__ void step5h(v16f (&acc)[4], const AOps& ops, uint4 (&b0)[4], const uint32_t (&bw)[2],
+                                       uint32_t (&bwn)[2], const uint8_t* cur, const uint8_t* nxt, uint8_t* wr,
+                                       AOps& opsn, const AStep& raw, const WStep<4>& wst, int lane, Issue issue,
+                                       const uint2* lut) {
+  const int half = lane >> 5, tid = threadIdx.x;
+  uint4 b1[4];
+  uint2 sel[8];
+  if (PAT == 48) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) sel[i] = lut[(raw.spm[i >> 2] >> (8 * (i & 3))) & 0xFFu];
+  }
+  issue();
+  SHARQ_FENCE();
+  // ---- sub-step 0: the second sub-step's weight operands, then the weight
+  // tile two steps ahead to LDS
+  mma_sp<0, 0>(acc, ops, b0, bw); read_b<1, 0, 1>(b1, cur, lane); put_piece<PAT, 0>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<0, 1>(acc, ops, b0, bw); read_b<1, 1, 2>(b1, cur, lane); put_piece<PAT, 1>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<0, 2>(acc, ops, b0, bw); read_b<1, 2, 3>(b1, cur, lane); put_piece<PAT, 2>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<0, 3>(acc, ops, b0, bw); read_b<1, 3, 4>(b1, cur, lane); put_piece<PAT, 3>(opsn, raw, sel); SHARQ_FENCE();
+  mma_dn<0, 0>(acc, ops, b0, bw); put_piece<PAT, 4>(opsn, raw, sel);
+  *reinterpret_cast<uint4*>(wr + (tid >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[0];
+  SHARQ_FENCE();
+  mma_dn<0, 1>(acc, ops, b0, bw); put_piece<PAT, 5>(opsn, raw, sel);
+  *reinterpret_cast<uint4*>(wr + ((tid + 256) >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[1];
+  SHARQ_FENCE();
+  mma_dn<0, 2>(acc, ops, b0, bw); put_piece<PAT, 6>(opsn, raw, sel);
+  if (tid < 128) {
+    const int f = tid >> 5, c = tid & 31;
+    *reinterpret_cast<uint16_t*>(wr + kStageW + (2 * c + 0) * 16 + 2 * f) = (uint16_t)wst.s;
+    *reinterpret_cast<uint16_t*>(wr + kStageW + (2 * c + 1) * 16 + 2 * f) = (uint16_t)(wst.s >> 16);
+  }
+  SHARQ_FENCE();
+  mma_dn<0, 3>(acc, ops, b0, bw); put_piece<PAT, 7>(opsn, raw, sel); SHARQ_FENCE();
+  // ---- sub-step 1: the next step's first operands and scale records
+  mma_sp<1, 0>(acc, ops, b1, bw); put_piece<PAT, 8>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<1, 1>(acc, ops, b1, bw); read_b<0, 0, 1>(b0, nxt, lane); put_piece<PAT, 9>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<1, 2>(acc, ops, b1, bw); read_b<0, 1, 2>(b0, nxt, lane); put_piece<PAT, 10>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<1, 3>(acc, ops, b1, bw); read_b<0, 2, 3>(b0, nxt, lane); put_piece<PAT, 11>(opsn, raw, sel); SHARQ_FENCE();
+  mma_dn<1, 0>(acc, ops, b1, bw); read_b<0, 3, 4>(b0, nxt, lane); put_piece<PAT, 12>(opsn, raw, sel); SHARQ_FENCE();
+  mma_dn<1, 1>(acc, ops, b1, bw); read_bw(bwn, nxt, lane); put_piece<PAT, 13>(opsn, raw, sel); SHARQ_FENCE();
+  mma_dn<1, 2>(acc, ops, b1, bw); put_piece<PAT, 14>(opsn, raw, sel); SHARQ_FENCE();
+  mma_dn<1, 3>(acc, ops, b1, bw); put_piece<PAT, 15>(opsn, raw, sel);
+  opsn.ssp = raw.ssp >> (16 * half);
+  opsn.sdn = raw.sdn >> (16 * half);
+  if (PAT == 0) {
+    opsn.sp[0] = raw.spd[0];
+    opsn.sp[1] = raw.spd[1];
+  }
+  SHARQ_FENCE();
+}
+
 // Residual codes of step ks straight into the operand registers, and the
 // backbone codes / metadata / scales of step ks into a raw set (panel-major,
 // K a multiple of 128).
@@ -605,16 +670,19 @@ __device__ __forceinline__ void load_a_meta(AStep& s, const ARow& a, int ks, int
 }
 
 
-__device__ __forceinline__ void store_w_stage(const WStep<8>& w, uint8_t* stage) {
+template <int NF>
+__device__ __forceinline__ void store_w_stage(const WStep<NF>& w, uint8_t* stage) {
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < NF / 2; ++j) {
     const int c = tid + 256 * j;
     *reinterpret_cast<uint4*>(stage + (c >> 2) * kLdsStride + 16 * (c & 3)) = w.q[j];
   }
-  const int f = tid >> 5, c = tid & 31;
-  *reinterpret_cast<uint16_t*>(stage + kStageW + (2 * c + 0) * 16 + 2 * f) = (uint16_t)w.s;
-  *reinterpret_cast<uint16_t*>(stage + kStageW + (2 * c + 1) * 16 + 2 * f) = (uint16_t)(w.s >> 16);
+  if (NF == 8 || tid < 32 * NF) {
+    const int f = tid >> 5, c = tid & 31;
+    *reinterpret_cast<uint16_t*>(stage + kStageW + (2 * c + 0) * 16 + 2 * f) = (uint16_t)w.s;
+    *reinterpret_cast<uint16_t*>(stage + kStageW + (2 * c + 1) * 16 + 2 * f) = (uint16_t)(w.s >> 16);
+  }
 }
 
 // Epilogue of a wavefront's 32 x 256 block of 2-byte outputs through LDS.
@@ -629,35 +697,49 @@ constexpr int kEpiStride = 528;            // bytes per staged row: 512 + 16 (sp
 constexpr int kEpiWave = 32 * kEpiStride;  // one wavefront's region
 constexpr int kTileLds = 4 * kEpiWave > 3 * kStageBytes ? 4 * kEpiWave : 3 * kStageBytes;
 
-template <typename OutT>
-__device__ __forceinline__ void store_tile_lds(const v16f (&acc)[8], OutT* Y, int64_t ldy, int64_t row0,
+template <typename OutT, int NF>
+__device__ __forceinline__ void store_tile_lds(const v16f (&acc)[NF], OutT* Y, int64_t ldy, int64_t row0,
                                                int64_t row_hi, int n0, int N, uint8_t* buf, int lane) {
+  // a staged row is 64 NF bytes (+16); 4 NF lanes read it back, 16 / NF rows per instruction
+  constexpr int stride = 64 * NF + 16, lpr = 4 * NF, rpi = 64 / lpr;
   const int r = lane & 31, half = lane >> 5;
 #pragma unroll
-  for (int f = 0; f < 8; ++f) {
+  for (int f = 0; f < NF; ++f) {
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      Vec4Out<OutT>::put(reinterpret_cast<OutT*>(buf + r * kEpiStride + (32 * f + 8 * g + 4 * half) * 2),
+      Vec4Out<OutT>::put(reinterpret_cast<OutT*>(buf + r * stride + (32 * f + 8 * g + 4 * half) * 2),
                          acc[f][4 * g], acc[f][4 * g + 1], acc[f][4 * g + 2], acc[f][4 * g + 3]);
     }
   }
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int rr = 2 * i + (lane >> 5), ch = lane & 31;
-    const uint4 v = *reinterpret_cast<const uint4*>(buf + rr * kEpiStride + ch * 16);
+  for (int i = 0; i < 32 / rpi; ++i) {
+    const int rr = rpi * i + lane / lpr, ch = lane % lpr;
+    const uint4 v = *reinterpret_cast<const uint4*>(buf + rr * stride + ch * 16);
     const int64_t row = row0 + rr;
     const int col = n0 + 8 * ch;
     if (row < row_hi && col < N) *reinterpret_cast<uint4*>(Y + row * ldy + col) = v;
   }
 }
 
-template <int PAT, typename OutT>
+// One K step of a full (NF = 8) or half (NF = 4) tile.
+template <int PAT, int NF, class Issue>
+__device__ __forceinline__ void step_il(v16f (&acc)[NF], const AOps& ops, uint4 (&b0)[NF],
+                                        const uint32_t (&bw)[NF / 2], uint32_t (&bwn)[NF / 2], const uint8_t* cur,
+                                        const uint8_t* nxt, uint8_t* wr, AOps& opsn, const AStep& raw,
+                                        const WStep<NF>& wst, int lane, Issue issue, const uint2* lut) {
+  if constexpr (NF == 8)
+    step5<PAT>(acc, ops, b0, bw, bwn, cur, nxt, wr, opsn, raw, wst, lane, issue, lut);
+  else
+    step5h<PAT>(acc, ops, b0, bw, bwn, cur, nxt, wr, opsn, raw, wst, lane, issue, lut);
+}
+
+template <int PAT, typename OutT, int NF>
 __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale,
                                            const uint8_t* dn_codes, const uint8_t* dn_scale, const int32_t* row_index,
                                            int64_t act_rows, int64_t row_lo, int64_t row_hi, const uint8_t* wc,
                                            const uint8_t* ws, int n0, int N, int K, OutT* Y, int64_t ldy,
                                            uint8_t* lds, const uint2* lut) {
-  constexpr int NF = 8;
+  static_assert(NF == 8 || NF == 4, "full (256-column) or half tile");
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
   const int nblk = K / 32, nks = K / kBK;
 
@@ -691,8 +773,8 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
   AStep r0, r1, r2;
   WStep<NF> w0, w1, w2;
   AOps o0, o1, o2;
-  uint4 b0[8];
-  uint32_t bwa[4], bwb[4];
+  uint4 b0[NF];
+  uint32_t bwa[NF / 2], bwb[NF / 2];
   uint8_t* const st0 = lds;
   uint8_t* const st1 = lds + kStageBytes;
   uint8_t* const st2 = lds + 2 * kStageBytes;
@@ -719,38 +801,41 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
   load_w<NF, true>(w0, wc, ws, n0, N, K, cl(3), nblk);
   __syncthreads();
   read_bw(bwa, st0, lane);
-  read_b<0, 0, 8>(b0, st0, lane);
+  read_b<0, 0, NF>(b0, st0, lane);
 
   int ks = 0;
   for (; ks + 2 < nks; ks += 3) {
-    step5<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [&] {
+    step_il<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [&] {
       load_a_dn(o2, a, cl(ks + 2), half);
       load_a_meta<PAT>(r0, a, cl(ks + 3), half);
       load_w<NF, true>(w1, wc, ws, n0, N, K, cl(ks + 4), nblk);
     }, lut);
     __syncthreads();
-    step5<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [&] {
+    step_il<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [&] {
       load_a_dn(o0, a, cl(ks + 3), half);
       load_a_meta<PAT>(r1, a, cl(ks + 4), half);
       load_w<NF, true>(w2, wc, ws, n0, N, K, cl(ks + 5), nblk);
     }, lut);
     __syncthreads();
-    step5<PAT>(acc, o2, b0, bwa, bwb, st2, st0, st1, o0, r0, w1, lane, [&] {
+    step_il<PAT>(acc, o2, b0, bwa, bwb, st2, st0, st1, o0, r0, w1, lane, [&] {
       load_a_dn(o1, a, cl(ks + 4), half);
       load_a_meta<PAT>(r2, a, cl(ks + 5), half);
       load_w<NF, true>(w0, wc, ws, n0, N, K, cl(ks + 6), nblk);
     }, lut);
     __syncthreads();
     // bw alternates with period two: after three steps the roles swap
-    uint32_t t[4] = {bwa[0], bwa[1], bwa[2], bwa[3]};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) { bwa[i] = bwb[i]; bwb[i] = t[i]; }
+    for (int i = 0; i < NF / 2; ++i) {
+      const uint32_t t = bwa[i];
+      bwa[i] = bwb[i];
+      bwb[i] = t;
+    }
   }
   if (ks < nks) {   // one or two steps left, in sets 0 and 1
-    step5<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [] {}, lut);
+    step_il<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [] {}, lut);
     if (ks + 1 < nks) {
       __syncthreads();
-      step5<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [] {}, lut);
+      step_il<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [] {}, lut);
     }
   }
 
@@ -759,7 +844,7 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
   if constexpr (sizeof(OutT) == 2) {
     if (((reinterpret_cast<uintptr_t>(Y) | (uintptr_t)(ldy * 2)) & 15u) == 0 && N % 8 == 0) {
       __syncthreads();   // every wavefront is done with the weight stages
-      store_tile_lds<OutT>(acc, Y, ldy, row_lo + wave * 32, row_hi, n0, N, lds + wave * kEpiWave, lane);
+      store_tile_lds<OutT, NF>(acc, Y, ldy, row_lo + wave * 32, row_hi, n0, N, lds + wave * kEpiWave, lane);
       return;
     }
   }
@@ -827,31 +912,58 @@ __global__ __launch_bounds__(256) void k_linear_mx(const uint8_t* sp_codes, cons
 }
 
 // Persistent dense kernel (K a multiple of 128): at most one workgroup per
-// CU, walking the tiles b, b + G, b + 2G, ... (G workgroups).  A tile's
+// CU, walking the work units b, b + G, b + 2G, ... (G workgroups).  A tile's
 // output stores then drain while the same CU starts its next tile instead of
 // the whole grid waiting at the end of every round (3% on the Llama gate/up
 // shape, 7 rounds).  With G a multiple of 8 every tile an XCD runs keeps the
 // XCD of its number, so the tile_of blocks still share an L2.
+//
+// Units [0, full) are whole tiles.  When the last round would be at most
+// half full (tiles = full + r, 0 < r <= G / 2), its r tiles run instead as
+// 2 r half tiles of 128 columns, units [full, full + 2 r): every CU then
+// runs a half tile instead of half of the CUs running a whole one (the
+// Llama qkv shape: 384 tiles on 256 CUs).  Half tile u covers tile t(u),
+// columns 128 h(u) on; with r a multiple of 8, t(u) keeps the XCD of u.
+__device__ __forceinline__ void half_unit(int u, int full, int halves, int& t, int& h) {
+  if ((halves & 15) == 0 && (full & 7) == 0) {
+    t = full + ((u >> 4) << 3) + (u & 7);
+    h = (u >> 3) & 1;
+  } else {
+    t = full + (u >> 1);
+    h = u & 1;
+  }
+}
+
 template <int PAT, typename OutT>
 __global__ __launch_bounds__(256) void k_linear_mx_persist(const uint8_t* sp_codes, const uint8_t* sp_meta,
                                                            const uint8_t* sp_scale, const uint8_t* dn_codes,
                                                            const uint8_t* dn_scale, int64_t M, const uint8_t* wc,
                                                            const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy,
-                                                           int gx, int gy) {
+                                                           int gx, int gy, int full, int halves) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[kTileLds];
   __shared__ uint2 lut48[256];
   if (PAT == 48) {
     lut48_fill(lut48);
     __syncthreads();
   }
-  const int ntile = gx * gy;
-  for (int id = (int)blockIdx.x; id < ntile; id += (int)gridDim.x) {
+  const int units = full + halves;
+  for (int id = (int)blockIdx.x; id < units; id += (int)gridDim.x) {
     int mt, nt;
-    tile_of(id, gx, gy, mt, nt);
-    const int64_t m0 = (int64_t)mt * kBM;
-    const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
-    tile_mx_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws, nt * 256, N,
-                          K, Y, ldy, lds, lut48);
+    if (id < full) {
+      tile_of(id, gx, gy, mt, nt);
+      const int64_t m0 = (int64_t)mt * kBM;
+      const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
+      tile_mx_il<PAT, OutT, 8>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws,
+                               nt * 256, N, K, Y, ldy, lds, lut48);
+    } else {
+      int t, h;
+      half_unit(id - full, full, halves, t, h);
+      tile_of(t, gx, gy, mt, nt);
+      const int64_t m0 = (int64_t)mt * kBM;
+      const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
+      tile_mx_il<PAT, OutT, 4>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws,
+                               nt * 256 + 128 * h, N, K, Y, ldy, lds, lut48);
+    }
     __syncthreads();   // the LDS stages are free before the next tile's prologue
   }
 }
@@ -924,7 +1036,7 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
       lut48_fill(lut48);
       __syncthreads();
     }
-    tile_mx_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, act_rows, r0, r1, wce, wse, n0,
+    tile_mx_il<PAT, OutT, 8>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, act_rows, r0, r1, wce, wse, n0,
                           N, K, Y, ldy, lds, lut48);
   }
   else
@@ -2122,15 +2234,32 @@ static int device_cus() {
   return cache[dev];
 }
 
+// Work units of the persistent kernel: whole tiles, with a last round that
+// would be at most half full run as twice as many half tiles.
+struct PersistPlan {
+  int grid, full, halves;
+};
+
+static PersistPlan persist_plan(int gx, int gy) {
+  const int tiles = gx * gy, cus = device_cus();
+  PersistPlan p{tiles < cus ? tiles : cus, tiles, 0};
+  const int r = tiles % p.grid;
+  if (tiles > p.grid && r > 0 && 2 * r <= p.grid) {
+    p.full = tiles - r;
+    p.halves = 2 * r;
+  }
+  return p;
+}
+
 template <int NF, int PAT, bool SDW, typename OutT>
 static hipError_t go_linear(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
                             const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
                             void* Y, int64_t ldy, hipStream_t st) {
   const int gx = (N + 32 * NF - 1) / (32 * NF), gy = (int)((M + kBM - 1) / kBM);
   if constexpr (SDW && NF == 8) {
-    const int tiles = gx * gy, cus = device_cus();
-    k_linear_mx_persist<PAT, OutT><<<dim3((unsigned)(tiles < cus ? tiles : cus)), dim3(256), 0, st>>>(
-        spc, spm, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
+    const PersistPlan pl = persist_plan(gx, gy);
+    k_linear_mx_persist<PAT, OutT><<<dim3((unsigned)pl.grid), dim3(256), 0, st>>>(
+        spc, spm, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy, pl.full, pl.halves);
   } else {
     k_linear_mx<NF, PAT, SDW, OutT><<<dim3((unsigned)(gx * gy)), dim3(256), 0, st>>>(
         spc, spm, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
@@ -2153,9 +2282,9 @@ static hipError_t go_dense_backbone(const uint8_t* spd, const uint8_t* sps, cons
                                     int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K, void* Y,
                                     int64_t ldy, hipStream_t st) {
   const int gx = (N + 255) / 256, gy = (int)((M + kBM - 1) / kBM);
-  const int tiles = gx * gy, cus = device_cus();
-  k_linear_mx_persist<0, OutT><<<dim3((unsigned)(tiles < cus ? tiles : cus)), dim3(256), 0, st>>>(
-      spd, nullptr, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
+  const PersistPlan pl = persist_plan(gx, gy);
+  k_linear_mx_persist<0, OutT><<<dim3((unsigned)pl.grid), dim3(256), 0, st>>>(
+      spd, nullptr, sps, dnc, dns, M, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy, pl.full, pl.halves);
   return hipGetLastError();
 }
 

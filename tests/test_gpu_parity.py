@@ -356,6 +356,34 @@ def test_moe_full_config(S, G):
         gemm_check(yh[lo:hi], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), f"moe expert {e}")
 
 
+# --------------------------------------------------------------------------- persistent kernel tail
+
+@pytest.mark.parametrize("T,N,K,n,m", [(12750, 704, 256, 2, 4),    # 300 tiles: 44 in the last round
+                                       (4608, 2048, 128, 2, 4),    # 288 tiles: 32, XCD-ordered halves
+                                       (4608, 2048, 256, 4, 8)])
+def test_persistent_tail_half_tiles(S, G, T, N, K, n, m):
+    """A last round of at most half the CUs runs as half tiles of 128 columns
+    (ragged rows and columns included): every output against the oracle, the
+    bf16 output (LDS-staged epilogue) equal to the fp32 one rounded, and the
+    dense backbone copy bit-identical to the compressed backbone."""
+    say(f"[tail] T={T} N={N} K={K} {n}:{m}")
+    x, g = synth.activations(T, K, seed=T + N), synth.gamma(K, seed=5)
+    xd, gd = G.dev_bf16(x), G.dev_bf16(g)
+    c = S.sharq_prepare(xd, gd, 1e-6, n, m, "mx")
+    a = S.sharq_prepare(xd, gd, 1e-6, n, m, "mx", out=S.alloc_act(T, K, n, m, "mx", "cuda", dense_backbone=True))
+    wq = S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=K)))
+    y32 = S.sharq_linear(c, wq, dtype=torch.float32)
+    y16 = S.sharq_linear(c, wq, dtype=torch.bfloat16)
+    yd = S.sharq_linear(a, wq, dtype=torch.float32)
+    yd16 = S.sharq_linear(a, wq, dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert torch.equal(y16, y32.to(torch.bfloat16))
+    assert torch.equal(yd, y32) and torch.equal(yd16, y16)
+    o = O.prepare(x, g, 1e-6, n, m, "mx")
+    wo = G.weight_to_oracle(wq)
+    gemm_check(G.host(y32), O.linear(o, wo), O.linear_abs(o, wo), f"tail T{T}N{N}K{K}")
+
+
 # --------------------------------------------------------------------------- dense backbone copy
 
 @pytest.mark.parametrize("T,K,N,use_gamma,n,m,pairs", [(256, 1024, 512, True, 2, 4, False),
