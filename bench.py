@@ -60,7 +60,7 @@ N_INPUT_SETS = 2              # activations rotate between steps (defeats the 25
 # (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors a plain 1 GiB device copy
 # gives).  Valid only for the GEMM source it was measured on (sha256 prefix);
 # reported as null once that source has changed.
-TRAFFIC = {"gemm_source": "46a5317cef77e93e", "bytes_per_launch": 270.24e6}
+TRAFFIC = {"gemm_source": "93cf47f154438ecb", "bytes_per_launch": 270.30e6}
 
 
 def log(*a):
@@ -224,6 +224,31 @@ def per_linear(layers, tm, T, fmt, n, m, dense_backbone=False):
     return per
 
 
+def copy_same_bytes(torch, dev, stream, nbytes, reps=20):
+    """Mean time of a plain streaming device kernel moving `nbytes` (half
+    read, half written), with sources rotated past the 256 MB last-level
+    cache: the rate a copy reaches at this transfer size."""
+    n = int(nbytes // 2) // 16 * 4   # int32 elements, 16-byte multiple
+    nsrc = max(2, int((512 << 20) // max(4 * n, 1)) + 1)
+    srcs = [torch.full((n,), i, dtype=torch.int32, device=dev) for i in range(nsrc)]
+    dst = torch.empty(n, dtype=torch.int32, device=dev)
+    with torch.cuda.stream(stream):
+        # a streaming elementwise kernel (one read, one write per element);
+        # torch's copy_ would go to the runtime's blit kernel instead
+        for i in range(3):
+            torch.bitwise_not(srcs[i % nsrc], out=dst)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev[0].record(stream)
+        for i in range(reps):
+            torch.bitwise_not(srcs[i % nsrc], out=dst)
+            ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    us = float(np.mean([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)])) * 1e3
+    del srcs, dst
+    torch.cuda.empty_cache()
+    return us
+
+
 def llama_prefill(args, torch, S, synth, dev, stream):
     dense_bb = not args.compressed_backbone
     layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T_TOKENS, "mx", 2, 4, N_INPUT_SETS,
@@ -257,6 +282,14 @@ def llama_prefill(args, torch, S, synth, dev, stream):
                        "us_per_launch": t_gemm * 1e6 / len(per)}
     out["prep"] = {"bound": "hbm", "kernel": "k_prep_norm_split / k_prep_blocks (fused preparation)",
                    "achieved": prep_gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": prep_gbps / PEAK_HBM_GBPS}
+    # the same bytes moved by a plain device copy, one launch per linear
+    copy_us = [copy_same_bytes(torch, dev, stream, p["prep_bytes"]) for p in per]
+    for p, cu in zip(per, copy_us):
+        p["copy_same_bytes_us"] = cu
+    copy_gbps = bytes_prep / (sum(copy_us) * 1e-6) / 1e9
+    out["prep"]["copy_same_bytes"] = {"achieved": copy_gbps, "unit": "GB/s", "frac": copy_gbps / PEAK_HBM_GBPS,
+                                      "prep_vs_copy": prep_gbps / copy_gbps}
+    log(f"[bench] prep {prep_gbps:.0f} GB/s; a device copy of the same bytes {copy_gbps:.0f} GB/s")
     out["per_linear"] = per
     out["wall_ms_per_step"] = wall_ms
     return out
