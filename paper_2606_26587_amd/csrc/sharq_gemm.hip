@@ -29,6 +29,7 @@
 // 8 (r / 4) + 4 (l / 32) + (r % 4), column l % 32.
 
 #include "sharq_device.hpp"
+#include <type_traits>
 
 namespace sharq {
 
@@ -135,17 +136,20 @@ __device__ __forceinline__ void load_w(WStep<NF>& w, const uint8_t* wc, const ui
                  ? *reinterpret_cast<const uint4*>(wc + pn * 64 + (int64_t)n * (wp / 2) + 16 * part)
                  : make_uint4(0u, 0u, 0u, 0u);
   }
-  w.s = 0u;
-  if (BN >= 256 || tid < BN) {
-    const int n = min(n0 + tid, N - 1);
-    const uint8_t* sr = ws + pn * 4 + (int64_t)n * (wp / 32);
-    if (SCALE_DW) {
-      w.s = *reinterpret_cast<const uint32_t*>(sr);
-    } else {
+  // one scale dword per weight row (threads 0 .. BN-1).  Threads past BN
+  // reread row BN-1 and keep 0: no branch, which keeps the interleaved
+  // K step one basic block (the compiler would otherwise move its MFMAs
+  // out of their slots)
+  const int n = min(n0 + (BN >= 256 ? tid : min(tid, BN - 1)), N - 1);
+  const uint8_t* sr = ws + pn * 4 + (int64_t)n * (wp / 32);
+  uint32_t sv = 0u;
+  if (SCALE_DW) {
+    sv = *reinterpret_cast<const uint32_t*>(sr);
+  } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) w.s |= (uint32_t)(4 * ks + j < nblk ? sr[j] : 127u) << (8 * j);
-    }
+    for (int j = 0; j < 4; ++j) sv |= (uint32_t)(4 * ks + j < nblk ? sr[j] : 127u) << (8 * j);
   }
+  w.s = (BN >= 256 || tid < BN) ? sv : 0u;
 }
 
 // Weight scales in LDS are laid out per (column, lane half): lane (col, h)
@@ -337,8 +341,12 @@ __device__ __forceinline__ void tile_mx(const uint8_t* sp_codes, const uint8_t* 
 // two steps ahead and the reads of the next step's first weight operands.
 // The weight tile goes through three LDS stages, so the tile of step k+1 is
 // published one barrier before step k ends and its first operands are already
-// in registers when step k+1 begins.  Global loads are issued before the
-// first slot: the weights three steps ahead, the activations two steps ahead.
+// in registers when step k+1 begins.  The global loads of later steps (the
+// weights three steps ahead, the activations two steps ahead) go out in six
+// parts behind the first six MFMAs rather than as one block before the first:
+// measured on the Llama prefill shapes, a block of ~10 loads and their
+// address arithmetic ahead of every step left the matrix core idle, and
+// spreading them took the three GEMMs from ~450 to ~420-430 us.
 // Scheduling fences keep every slot in place.
 
 struct AOps {        // MFMA-ready activation operands of one K step
@@ -503,7 +511,8 @@ __device__ __forceinline__ void read_bw(uint32_t (&bw)[2], const uint8_t* stage,
 // of step k (read from stage `cur`); ops = expanded activations of step k.
 // Out: b0 / bwn = those of step k+1 (from stage `nxt`); opsn.sp and scales =
 // expansion of raw (step k+1; its residual codes are loaded into opsn.dn by
-// `issue`); wst (step k+2) stored to stage `wr`.
+// `issue`); wst (step k+2) stored to stage `wr`.  issue(part) issues part
+// 0-5 of the step's global loads (a std::integral_constant argument).
 template <int PAT, class Issue>
 __device__ __forceinline__ void step5(v16f (&acc)[8], const AOps& ops, uint4 (&b0)[8], const uint32_t (&bw)[4],
                                       uint32_t (&bwn)[4], const uint8_t* cur, const uint8_t* nxt, uint8_t* wr,
@@ -519,15 +528,20 @@ __device__ __forceinline__ void step5(v16f (&acc)[8], const AOps& ops, uint4 (&b
   // LDS traffic is spread at about one instruction per slot (a 1 KB
   // wavefront access keeps the LDS busy for several MFMA-lengths when four
   // wavefronts burst together); VALU work stays under ~8 instructions per slot.
-  issue();
+  // ---- sub-step 0, backbone: second sub-step's weight operands; the
+  // global loads of later steps go out in six parts behind the first MFMAs
+  mma_sp<0, 0>(acc, ops, b0, bw); issue(std::integral_constant<int, 0>()); read_b<1, 0, 1>(b1, cur, lane);
+  put_piece<PAT, 0>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<0, 1>(acc, ops, b0, bw); issue(std::integral_constant<int, 1>()); read_b<1, 1, 2>(b1, cur, lane);
   SHARQ_FENCE();
-  // ---- sub-step 0, backbone: second sub-step's weight operands
-  mma_sp<0, 0>(acc, ops, b0, bw); read_b<1, 0, 1>(b1, cur, lane); put_piece<PAT, 0>(opsn, raw, sel); SHARQ_FENCE();
-  mma_sp<0, 1>(acc, ops, b0, bw); read_b<1, 1, 2>(b1, cur, lane); SHARQ_FENCE();
-  mma_sp<0, 2>(acc, ops, b0, bw); read_b<1, 2, 3>(b1, cur, lane); put_piece<PAT, 1>(opsn, raw, sel); SHARQ_FENCE();
-  mma_sp<0, 3>(acc, ops, b0, bw); read_b<1, 3, 4>(b1, cur, lane); SHARQ_FENCE();
-  mma_sp<0, 4>(acc, ops, b0, bw); read_b<1, 4, 5>(b1, cur, lane); put_piece<PAT, 2>(opsn, raw, sel); SHARQ_FENCE();
-  mma_sp<0, 5>(acc, ops, b0, bw); read_b<1, 5, 6>(b1, cur, lane); SHARQ_FENCE();
+  mma_sp<0, 2>(acc, ops, b0, bw); issue(std::integral_constant<int, 2>()); read_b<1, 2, 3>(b1, cur, lane);
+  put_piece<PAT, 1>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<0, 3>(acc, ops, b0, bw); issue(std::integral_constant<int, 3>()); read_b<1, 3, 4>(b1, cur, lane);
+  SHARQ_FENCE();
+  mma_sp<0, 4>(acc, ops, b0, bw); issue(std::integral_constant<int, 4>()); read_b<1, 4, 5>(b1, cur, lane);
+  put_piece<PAT, 2>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<0, 5>(acc, ops, b0, bw); issue(std::integral_constant<int, 5>()); read_b<1, 5, 6>(b1, cur, lane);
+  SHARQ_FENCE();
   mma_sp<0, 6>(acc, ops, b0, bw); read_b<1, 6, 7>(b1, cur, lane); put_piece<PAT, 3>(opsn, raw, sel); SHARQ_FENCE();
   mma_sp<0, 7>(acc, ops, b0, bw); read_b<1, 7, 8>(b1, cur, lane); SHARQ_FENCE();
   // ---- sub-step 0, residual: the weight tile two steps ahead to LDS
@@ -597,22 +611,27 @@ __device__ __forceinline__ void step5h(v16f (&acc)[4], const AOps& ops, uint4 (&
 #pragma unroll
     for (int i = 0; i < 8; ++i) sel[i] = lut[(raw.spm[i >> 2] >> (8 * (i & 3))) & 0xFFu];
   }
-  issue();
-  SHARQ_FENCE();
-  // ---- sub-step 0: the second sub-step's weight operands, then the weight
-  // tile two steps ahead to LDS
-  mma_sp<0, 0>(acc, ops, b0, bw); read_b<1, 0, 1>(b1, cur, lane); put_piece<PAT, 0>(opsn, raw, sel); SHARQ_FENCE();
-  mma_sp<0, 1>(acc, ops, b0, bw); read_b<1, 1, 2>(b1, cur, lane); put_piece<PAT, 1>(opsn, raw, sel); SHARQ_FENCE();
-  mma_sp<0, 2>(acc, ops, b0, bw); read_b<1, 2, 3>(b1, cur, lane); put_piece<PAT, 2>(opsn, raw, sel); SHARQ_FENCE();
-  mma_sp<0, 3>(acc, ops, b0, bw); read_b<1, 3, 4>(b1, cur, lane); put_piece<PAT, 3>(opsn, raw, sel); SHARQ_FENCE();
-  mma_dn<0, 0>(acc, ops, b0, bw); put_piece<PAT, 4>(opsn, raw, sel);
+  // ---- sub-step 0: the second sub-step's weight operands and the global
+  // loads of later steps, then the weight tile two steps ahead to LDS
+  mma_sp<0, 0>(acc, ops, b0, bw); issue(std::integral_constant<int, 0>()); read_b<1, 0, 1>(b1, cur, lane);
+  put_piece<PAT, 0>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<0, 1>(acc, ops, b0, bw); issue(std::integral_constant<int, 1>()); read_b<1, 1, 2>(b1, cur, lane);
+  put_piece<PAT, 1>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<0, 2>(acc, ops, b0, bw); issue(std::integral_constant<int, 2>()); read_b<1, 2, 3>(b1, cur, lane);
+  put_piece<PAT, 2>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<0, 3>(acc, ops, b0, bw); issue(std::integral_constant<int, 3>()); read_b<1, 3, 4>(b1, cur, lane);
+  put_piece<PAT, 3>(opsn, raw, sel); SHARQ_FENCE();
+  mma_dn<0, 0>(acc, ops, b0, bw); issue(std::integral_constant<int, 4>()); put_piece<PAT, 4>(opsn, raw, sel);
   *reinterpret_cast<uint4*>(wr + (tid >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[0];
   SHARQ_FENCE();
-  mma_dn<0, 1>(acc, ops, b0, bw); put_piece<PAT, 5>(opsn, raw, sel);
+  mma_dn<0, 1>(acc, ops, b0, bw); issue(std::integral_constant<int, 5>()); put_piece<PAT, 5>(opsn, raw, sel);
   *reinterpret_cast<uint4*>(wr + ((tid + 256) >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[1];
   SHARQ_FENCE();
   mma_dn<0, 2>(acc, ops, b0, bw); put_piece<PAT, 6>(opsn, raw, sel);
-  if (tid < 128) {
+  {
+    // threads 128-255 hold no scales (wst.s = 0) and write bytes 8-15 of the
+    // records, which a half tile never reads: no branch, so the step stays
+    // one basic block and the compiler keeps every MFMA in its slot
     const int f = tid >> 5, c = tid & 31;
     *reinterpret_cast<uint16_t*>(wr + kStageW + (2 * c + 0) * 16 + 2 * f) = (uint16_t)wst.s;
     *reinterpret_cast<uint16_t*>(wr + kStageW + (2 * c + 1) * 16 + 2 * f) = (uint16_t)(wst.s >> 16);
@@ -669,6 +688,53 @@ __device__ __forceinline__ void load_a_meta(AStep& s, const ARow& a, int ks, int
   s.ssp = *reinterpret_cast<const uint32_t*>(a.sps + pr * 4 + a.r * 4);
 }
 
+
+// Parts of one K step's global loads (K a multiple of 128), so that the
+// interleaved loop can spread them over its MFMA slots: the backbone codes
+// (or the dense copy) and the two scale dwords of the activations; two halves
+// of the weight codes and the weight scales (load_w's bytes, in parts).
+template <int PAT, int P>
+__device__ __forceinline__ void load_a_meta_part(AStep& s, const ARow& a, int ks, int half) {
+  const int64_t pr = (int64_t)ks * a.R;
+  if constexpr (P == 0) {
+    if (PAT == 0) {
+      const uint8_t* sp = a.spc + pr * 64 + a.r * 64 + 32 * half;
+      s.spd[0] = *reinterpret_cast<const uint4*>(sp);
+      s.spd[1] = *reinterpret_cast<const uint4*>(sp + 16);
+    } else {
+      const uint4 c = *reinterpret_cast<const uint4*>(a.spc + pr * 32 + a.r * 32 + 16 * half);
+      const uint2 m = *reinterpret_cast<const uint2*>(a.spm + pr * 16 + a.r * 16 + 8 * half);
+      s.spc[0] = make_uint2(c.x, c.y);
+      s.spc[1] = make_uint2(c.z, c.w);
+      s.spm[0] = m.x;
+      s.spm[1] = m.y;
+    }
+  } else {
+    s.sdn = *reinterpret_cast<const uint32_t*>(a.dns + pr * 4 + a.r * 4);
+    s.ssp = *reinterpret_cast<const uint32_t*>(a.sps + pr * 4 + a.r * 4);
+  }
+}
+
+template <int NF, int P>
+__device__ __forceinline__ void load_w_part(WStep<NF>& w, const uint8_t* wc, const uint8_t* ws, int n0, int N,
+                                            int ks) {
+  constexpr int BN = 32 * NF;
+  const int tid = threadIdx.x;
+  const int64_t pn = (int64_t)ks * N;
+  if constexpr (P < 2) {
+#pragma unroll
+    for (int j = P * NF / 4; j < (P + 1) * NF / 4; ++j) {
+      const int c = tid + 256 * j;
+      const int row = c >> 2, part = c & 3;
+      const int n = min(n0 + row, N - 1);
+      w.q[j] = *reinterpret_cast<const uint4*>(wc + pn * 64 + (int64_t)n * 64 + 16 * part);
+    }
+  } else {
+    const int n = min(n0 + (BN >= 256 ? tid : min(tid, BN - 1)), N - 1);
+    const uint32_t sv = *reinterpret_cast<const uint32_t*>(ws + pn * 4 + (int64_t)n * 4);
+    w.s = (BN >= 256 || tid < BN) ? sv : 0u;
+  }
+}
 
 template <int NF>
 __device__ __forceinline__ void store_w_stage(const WStep<NF>& w, uint8_t* stage) {
@@ -805,22 +871,28 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
 
   int ks = 0;
   for (; ks + 2 < nks; ks += 3) {
-    step_il<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [&] {
-      load_a_dn(o2, a, cl(ks + 2), half);
-      load_a_meta<PAT>(r0, a, cl(ks + 3), half);
-      load_w<NF, true>(w1, wc, ws, n0, N, K, cl(ks + 4), nblk);
+    step_il<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [&](auto part) {
+      constexpr int P = decltype(part)::value;
+      if constexpr (P == 0) load_a_dn(o2, a, cl(ks + 2), half);
+      else if constexpr (P == 1) load_a_meta_part<PAT, 0>(r0, a, cl(ks + 3), half);
+      else if constexpr (P == 2) load_a_meta_part<PAT, 1>(r0, a, cl(ks + 3), half);
+      else load_w_part<NF, P - 3>(w1, wc, ws, n0, N, cl(ks + 4));
     }, lut);
     __syncthreads();
-    step_il<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [&] {
-      load_a_dn(o0, a, cl(ks + 3), half);
-      load_a_meta<PAT>(r1, a, cl(ks + 4), half);
-      load_w<NF, true>(w2, wc, ws, n0, N, K, cl(ks + 5), nblk);
+    step_il<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [&](auto part) {
+      constexpr int P = decltype(part)::value;
+      if constexpr (P == 0) load_a_dn(o0, a, cl(ks + 3), half);
+      else if constexpr (P == 1) load_a_meta_part<PAT, 0>(r1, a, cl(ks + 4), half);
+      else if constexpr (P == 2) load_a_meta_part<PAT, 1>(r1, a, cl(ks + 4), half);
+      else load_w_part<NF, P - 3>(w2, wc, ws, n0, N, cl(ks + 5));
     }, lut);
     __syncthreads();
-    step_il<PAT>(acc, o2, b0, bwa, bwb, st2, st0, st1, o0, r0, w1, lane, [&] {
-      load_a_dn(o1, a, cl(ks + 4), half);
-      load_a_meta<PAT>(r2, a, cl(ks + 5), half);
-      load_w<NF, true>(w0, wc, ws, n0, N, K, cl(ks + 6), nblk);
+    step_il<PAT>(acc, o2, b0, bwa, bwb, st2, st0, st1, o0, r0, w1, lane, [&](auto part) {
+      constexpr int P = decltype(part)::value;
+      if constexpr (P == 0) load_a_dn(o1, a, cl(ks + 4), half);
+      else if constexpr (P == 1) load_a_meta_part<PAT, 0>(r2, a, cl(ks + 5), half);
+      else if constexpr (P == 2) load_a_meta_part<PAT, 1>(r2, a, cl(ks + 5), half);
+      else load_w_part<NF, P - 3>(w0, wc, ws, n0, N, cl(ks + 6));
     }, lut);
     __syncthreads();
     // bw alternates with period two: after three steps the roles swap
@@ -832,10 +904,10 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
     }
   }
   if (ks < nks) {   // one or two steps left, in sets 0 and 1
-    step_il<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [] {}, lut);
+    step_il<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [](auto) {}, lut);
     if (ks + 1 < nks) {
       __syncthreads();
-      step_il<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [] {}, lut);
+      step_il<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [](auto) {}, lut);
     }
   }
 
