@@ -1621,12 +1621,14 @@ __device__ __forceinline__ void nv_step(v16f (&acc)[8], const NvOps& ops, uint4 
   issue();
   SHARQ_FENCE();
   // next step's activations: backbone expanded to 16 codes, then dequantized
-  const float dsp = e4m3_value(raw.ssc), ddn = e4m3_value(raw.dsc);
+  // (their scales decoded behind the first two MFMAs)
+  float dsp, ddn;
   uint32_t e0 = 0u, e1 = 0u;
   const uint2 cw = make_uint2(raw.spc, 0u);
   // ---- sub-step 0, backbone
-  nv_mma<0, 0>(acc, ops.sp[0], b0); nv_read_b<1, 0, 1>(b1, cur, lane); SHARQ_FENCE();
-  nv_mma<0, 1>(acc, ops.sp[0], b0); nv_read_b<1, 1, 2>(b1, cur, lane); e0 = expand_dw<PAT, 0>(cw, raw.spm); SHARQ_FENCE();
+  nv_mma<0, 0>(acc, ops.sp[0], b0); nv_read_b<1, 0, 1>(b1, cur, lane); dsp = e4m3_value(raw.ssc); SHARQ_FENCE();
+  nv_mma<0, 1>(acc, ops.sp[0], b0); nv_read_b<1, 1, 2>(b1, cur, lane); ddn = e4m3_value(raw.dsc);
+  e0 = expand_dw<PAT, 0>(cw, raw.spm); SHARQ_FENCE();
   nv_mma<0, 2>(acc, ops.sp[0], b0); nv_read_b<1, 2, 3>(b1, cur, lane); SHARQ_FENCE();
   nv_mma<0, 3>(acc, ops.sp[0], b0); nv_read_b<1, 3, 4>(b1, cur, lane); e1 = expand_dw<PAT, 1>(cw, raw.spm); SHARQ_FENCE();
   nv_mma<0, 4>(acc, ops.sp[0], b0); nv_read_b<1, 4, 5>(b1, cur, lane);
@@ -1646,34 +1648,36 @@ __device__ __forceinline__ void nv_step(v16f (&acc)[8], const NvOps& ops, uint4 
   opsn.dn[1].x = bf16_pair<0>(raw.dn.y, ddn); opsn.dn[1].y = bf16_pair<1>(raw.dn.y, ddn); SHARQ_FENCE();
   nv_mma<0, 3>(acc, ops.dn[0], b0);
   opsn.dn[1].z = bf16_pair<2>(raw.dn.y, ddn); opsn.dn[1].w = bf16_pair<3>(raw.dn.y, ddn); SHARQ_FENCE();
-  // the weight row two steps ahead: dequantized into the other stage
+  // the weight row two steps ahead: dequantized into the other stage, each
+  // 16-byte part over two slots (4 values per slot)
   const float dw = e4m3_value(wst.sc);
   const int wrow = tid;
+  uint32_t wx, wy;
   nv_mma<0, 4>(acc, ops.dn[0], b0);
+  wx = bf16_pair<0>(wst.codes.x, dw); wy = bf16_pair<1>(wst.codes.x, dw); SHARQ_FENCE();
+  nv_mma<0, 5>(acc, ops.dn[0], b0);
   *reinterpret_cast<uint4*>(wr + wrow * 64 + 16 * (0 ^ swz_nv(wrow))) =
-      make_uint4(bf16_pair<0>(wst.codes.x, dw), bf16_pair<1>(wst.codes.x, dw), bf16_pair<2>(wst.codes.x, dw),
-                 bf16_pair<3>(wst.codes.x, dw));
+      make_uint4(wx, wy, bf16_pair<2>(wst.codes.x, dw), bf16_pair<3>(wst.codes.x, dw));
   SHARQ_FENCE();
-  nv_mma<0, 5>(acc, ops.dn[0], b0); SHARQ_FENCE();
   nv_mma<0, 6>(acc, ops.dn[0], b0);
+  wx = bf16_pair<0>(wst.codes.y, dw); wy = bf16_pair<1>(wst.codes.y, dw); SHARQ_FENCE();
+  nv_mma<0, 7>(acc, ops.dn[0], b0);
   *reinterpret_cast<uint4*>(wr + wrow * 64 + 16 * (1 ^ swz_nv(wrow))) =
-      make_uint4(bf16_pair<0>(wst.codes.y, dw), bf16_pair<1>(wst.codes.y, dw), bf16_pair<2>(wst.codes.y, dw),
-                 bf16_pair<3>(wst.codes.y, dw));
+      make_uint4(wx, wy, bf16_pair<2>(wst.codes.y, dw), bf16_pair<3>(wst.codes.y, dw));
   SHARQ_FENCE();
-  nv_mma<0, 7>(acc, ops.dn[0], b0); SHARQ_FENCE();
   // ---- sub-step 1, backbone
   nv_mma<1, 0>(acc, ops.sp[1], b1);
+  wx = bf16_pair<0>(wst.codes.z, dw); wy = bf16_pair<1>(wst.codes.z, dw); SHARQ_FENCE();
+  nv_mma<1, 1>(acc, ops.sp[1], b1);
   *reinterpret_cast<uint4*>(wr + wrow * 64 + 16 * (2 ^ swz_nv(wrow))) =
-      make_uint4(bf16_pair<0>(wst.codes.z, dw), bf16_pair<1>(wst.codes.z, dw), bf16_pair<2>(wst.codes.z, dw),
-                 bf16_pair<3>(wst.codes.z, dw));
+      make_uint4(wx, wy, bf16_pair<2>(wst.codes.z, dw), bf16_pair<3>(wst.codes.z, dw));
   SHARQ_FENCE();
-  nv_mma<1, 1>(acc, ops.sp[1], b1); SHARQ_FENCE();
   nv_mma<1, 2>(acc, ops.sp[1], b1);
+  wx = bf16_pair<0>(wst.codes.w, dw); wy = bf16_pair<1>(wst.codes.w, dw); SHARQ_FENCE();
+  nv_mma<1, 3>(acc, ops.sp[1], b1);
   *reinterpret_cast<uint4*>(wr + wrow * 64 + 16 * (3 ^ swz_nv(wrow))) =
-      make_uint4(bf16_pair<0>(wst.codes.w, dw), bf16_pair<1>(wst.codes.w, dw), bf16_pair<2>(wst.codes.w, dw),
-                 bf16_pair<3>(wst.codes.w, dw));
+      make_uint4(wx, wy, bf16_pair<2>(wst.codes.w, dw), bf16_pair<3>(wst.codes.w, dw));
   SHARQ_FENCE();
-  nv_mma<1, 3>(acc, ops.sp[1], b1); SHARQ_FENCE();
   nv_mma<1, 4>(acc, ops.sp[1], b1); SHARQ_FENCE();
   nv_mma<1, 5>(acc, ops.sp[1], b1); SHARQ_FENCE();
   nv_mma<1, 6>(acc, ops.sp[1], b1); SHARQ_FENCE();
