@@ -717,47 +717,61 @@ __global__ void k_pts_finalize(uint32_t* slot) {
   *reinterpret_cast<float*>(slot) = S;
 }
 
+// The pre-pass walks row groups grid-stride (one row per wavefront at a
+// time) and issues one atomicMax per workgroup: atomics on one address
+// serialize (~12 ns each measured), so one per row cost ~25 us at M = 2048.
+// The grid is capped at kAmaxWG workgroups.
+constexpr int kAmaxWG = 256;
+
+__device__ __forceinline__ void amax_publish(float m, uint32_t* slot, float* wmax) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  m = wave_max(m);
+  if (lane == 0) wmax[wave] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) atomicMax(slot, __float_as_uint(fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]))));
+}
+
 template <int NB, bool RES>
 __global__ __launch_bounds__(256) void k_amax_norm(XSrc src, int M, int K, const uint16_t* __restrict__ gamma,
                                                    float eps, uint32_t* slot) {
+  __shared__ float wmax[4];
   const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= M) return;
   const int nblk = K / 32;
-  uint4 xs[NB][4];
-  const float r = load_row_rms<NB, RES>(src, row, false, lane, nblk, K, eps, xs);
   const uint4* gr = reinterpret_cast<const uint4*>(gamma);
   float m = 0.0f;
+  for (int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); row < M; row += (int64_t)gridDim.x * 4) {
+    uint4 xs[NB][4];
+    const float r = load_row_rms<NB, RES>(src, row, false, lane, nblk, K, eps, xs);
 #pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    const int b = lane + 64 * i;
-    if (b >= nblk) break;
-    uint4 gq[4];
+    for (int i = 0; i < NB; ++i) {
+      const int b = lane + 64 * i;
+      if (b >= nblk) break;
+      uint4 gq[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) gq[j] = gr[4 * b + j];
-    float y[32];
-    norm_block(xs[i], gq, r, y);
-    m = fmaxf(m, absmax32(y));
+      for (int j = 0; j < 4; ++j) gq[j] = gr[4 * b + j];
+      float y[32];
+      norm_block(xs[i], gq, r, y);
+      m = fmaxf(m, absmax32(y));
+    }
   }
-  m = wave_max(m);
-  if (lane == 0) atomicMax(slot, __float_as_uint(m));
+  amax_publish(m, slot, wmax);   // every wavefront reaches the barrier inside
 }
 
 template <int SRC>
 __global__ __launch_bounds__(256) void k_amax_plain(XSrc src, int M, int K, uint32_t* slot) {
+  __shared__ float wmax[4];
   const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= M) return;
   float m = 0.0f;
-  for (int b = lane; b < K / 32; b += 64) {
-    uint4 q[4];
-    load_block<SRC>(src, row, b, q, false);
-    float y[32];
-    unpack_bf16x32(q, y);
-    m = fmaxf(m, absmax32(y));
+  for (int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); row < M; row += (int64_t)gridDim.x * 4) {
+    for (int b = lane; b < K / 32; b += 64) {
+      uint4 q[4];
+      load_block<SRC>(src, row, b, q, false);
+      float y[32];
+      unpack_bf16x32(q, y);
+      m = fmaxf(m, absmax32(y));
+    }
   }
-  m = wave_max(m);
-  if (lane == 0) atomicMax(slot, __float_as_uint(m));
+  amax_publish(m, slot, wmax);
 }
 
 // ---------------------------------------------------------------------------
@@ -1097,8 +1111,9 @@ static void go_prep(const XSrc& src, int M, int K, const uint16_t* gamma, float 
 }
 
 template <bool RES>
-static void go_amax(const XSrc& src, int M, int K, const uint16_t* gamma, float eps, uint32_t* slot, dim3 grid,
+static void go_amax(const XSrc& src, int M, int K, const uint16_t* gamma, float eps, uint32_t* slot, dim3 rows_grid,
                     hipStream_t st) {
+  const dim3 grid(rows_grid.x < (unsigned)kAmaxWG ? rows_grid.x : (unsigned)kAmaxWG);
   if (gamma == nullptr) {
     k_amax_plain<RES ? 1 : 0><<<grid, 256, 0, st>>>(src, M, K, slot);
     return;
