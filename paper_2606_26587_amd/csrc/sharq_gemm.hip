@@ -1116,6 +1116,63 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
                                      wce, wse, n0, N, K, Y, ldy, lds_w, lds_s);
 }
 
+// Persistent grouped form (K a multiple of 128): at most one workgroup per
+// CU walks the real (column tile, item) pairs -- their count comes from the
+// same on-device scan -- in the same XCD-contiguous, column-major order, so a
+// CU starts its next tile without a new workgroup launch and the padding
+// items of the launch-per-tile form cost nothing.
+template <int PAT, typename OutT>
+__global__ __launch_bounds__(256) void k_linear_mx_grouped_persist(
+    const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale, const uint8_t* dn_codes,
+    const uint8_t* dn_scale, const int32_t* row_index, int64_t act_rows, const int32_t* offs, int E,
+    const uint8_t* wc, const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy, int gx) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kTileLds];
+  __shared__ int s_first[1025];
+  __shared__ uint2 lut48[256];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < E; e += 256) {
+    const int rows = offs[e + 1] - offs[e];
+    s_first[e + 1] = rows > 0 ? (rows + kBM - 1) / kBM : 0;
+  }
+  if (tid == 0) s_first[0] = 0;
+  if (PAT == 48) lut48_fill(lut48);
+  __syncthreads();
+  for (int step = 1; step < E; step <<= 1) {
+    int v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = tid + 256 * j + 1;
+      v[j] = (e <= E && e - step >= 1) ? s_first[e - step] : 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = tid + 256 * j + 1;
+      if (e <= E) s_first[e] += v[j];
+    }
+    __syncthreads();
+  }
+  const int items = s_first[E];
+  const int total = gx * items;
+  for (int id = (int)blockIdx.x; id < total; id += (int)gridDim.x) {
+    const int idp = (total & 7) == 0 ? (id & 7) * (total >> 3) + (id >> 3) : id;
+    const int xt = idp / items, item = idp - xt * items;
+    int lo = 0, hi = E;   // e with s_first[e] <= item < s_first[e+1]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (s_first[mid] <= item) lo = mid; else hi = mid;
+    }
+    const int e = lo;
+    const int64_t r0 = (int64_t)offs[e] + (int64_t)(item - s_first[e]) * kBM;
+    const int64_t r_end = offs[e + 1];
+    const int64_t r1 = r0 + kBM < r_end ? r0 + kBM : r_end;
+    tile_mx_il<PAT, OutT, 8>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, act_rows, r0, r1,
+                             wc + (int64_t)e * N * (K / 2), ws + (int64_t)e * N * (K / 32), xt * 256, N, K, Y, ldy,
+                             lds, lut48);
+    __syncthreads();   // the LDS stages are free before the next tile's prologue
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Small-M (decode) MXFP4 GEMM
 // ---------------------------------------------------------------------------
@@ -2398,6 +2455,13 @@ static hipError_t go_grouped(const uint8_t* spc, const uint8_t* spm, const uint8
   const int64_t items = (total + kBM - 1) / kBM + E;
   const int gx = (N + 32 * NF - 1) / (32 * NF);
   if ((int64_t)gx * items > (int64_t)INT32_MAX) return hipErrorInvalidValue;
+  if constexpr (SDW && NF == 8) {
+    const int64_t bound = (int64_t)gx * items, cus = device_cus();
+    const unsigned g = (unsigned)(bound < cus ? bound : cus);
+    k_linear_mx_grouped_persist<PAT, OutT><<<dim3(g), dim3(256), 0, st>>>(
+        spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx);
+    return hipGetLastError();
+  }
   dim3 grid((unsigned)(gx * items)), block(256);
   k_linear_mx_grouped<NF, PAT, SDW, OutT><<<grid, block, 0, st>>>(spc, spm, sps, dnc, dns, ridx, act_rows, offs, E,
                                                                   wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx);
