@@ -1774,15 +1774,12 @@ __device__ __forceinline__ void nv_store_w(const NvWRaw& w, uint8_t* stage) {
 }
 
 template <int PAT, typename OutT>
-__global__ __launch_bounds__(256) void k_linear_nv_il(const uint8_t* sp_codes, const uint8_t* sp_meta,
-                                                      const uint8_t* sp_scale, const uint8_t* dn_codes,
-                                                      const uint8_t* dn_scale, const float* ts_x, int64_t M,
-                                                      const uint8_t* wc, const uint8_t* ws, const float* ts_w, int N,
-                                                      int K, OutT* Y, int64_t ldy, int gx, int gy) {
+__device__ __forceinline__ void tile_nv_il(const uint8_t* sp_codes, const uint8_t* sp_meta,
+                                           const uint8_t* sp_scale, const uint8_t* dn_codes,
+                                           const uint8_t* dn_scale, const float* ts_x, int64_t M,
+                                           const uint8_t* wc, const uint8_t* ws, const float* ts_w, int N, int K,
+                                           OutT* Y, int64_t ldy, int mt, int nt, uint8_t* lds) {
   constexpr int NF = 8;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[3 * kNvStage];
-  int mt, nt;
-  tile_of(blockIdx.x, gx, gy, mt, nt);
   const int n0 = nt * 256;
   const int64_t row_lo = (int64_t)mt * kBM;
   const int64_t row_hi = row_lo + kBM < M ? row_lo + kBM : M;
@@ -1873,6 +1870,27 @@ __global__ __launch_bounds__(256) void k_linear_nv_il(const uint8_t* sp_codes, c
   }
 }
 
+static int device_cus();   // compute units of the current device (host launchers below)
+
+// Persistent: at most one workgroup per CU walks the tiles b, b + G, ... in
+// the XCD-aware order of tile_of, as the MXFP4 kernel does.
+template <int PAT, typename OutT>
+__global__ __launch_bounds__(256) void k_linear_nv_il(const uint8_t* sp_codes, const uint8_t* sp_meta,
+                                                      const uint8_t* sp_scale, const uint8_t* dn_codes,
+                                                      const uint8_t* dn_scale, const float* ts_x, int64_t M,
+                                                      const uint8_t* wc, const uint8_t* ws, const float* ts_w, int N,
+                                                      int K, OutT* Y, int64_t ldy, int gx, int gy) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[3 * kNvStage];
+  const int ntile = gx * gy;
+  for (int id = (int)blockIdx.x; id < ntile; id += (int)gridDim.x) {
+    int mt, nt;
+    tile_of(id, gx, gy, mt, nt);
+    tile_nv_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, ts_x, M, wc, ws, ts_w, N, K, Y, ldy, mt, nt,
+                          lds);
+    __syncthreads();   // the LDS stages are free before the next tile's prologue
+  }
+}
+
 template <int PAT, typename OutT>
 static hipError_t go_nv(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
                         const uint8_t* dns, const float* tsx, int64_t M, const uint8_t* wc, const uint8_t* ws,
@@ -1880,7 +1898,8 @@ static hipError_t go_nv(const uint8_t* spc, const uint8_t* spm, const uint8_t* s
   constexpr int NF = 8;
   const int gx = (N + 32 * NF - 1) / (32 * NF), gy = (int)((M + kBM - 1) / kBM);
   if (K % kBK == 0) {
-    k_linear_nv_il<PAT, OutT><<<dim3((unsigned)(gx * gy)), dim3(256), 0, st>>>(
+    const int tiles = gx * gy, cus = device_cus();
+    k_linear_nv_il<PAT, OutT><<<dim3((unsigned)(tiles < cus ? tiles : cus)), dim3(256), 0, st>>>(
         spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
     return hipGetLastError();
   }
