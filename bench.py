@@ -54,6 +54,7 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
 T_TOKENS = 2048
 N_INPUT_SETS = 2              # activations rotate between steps (defeats the 256 MB last-level cache)
+DECODE_W_SETS = 5             # decode: weight copies rotate between steps (5 x 107 MB, past that cache)
 
 # HBM traffic of the dominant kernel (k_linear_mx_persist<0>, the default workload with the dense backbone copy,
 # mean over its three launch shapes), from two rocprofv3 --pmc runs
@@ -177,14 +178,16 @@ def base_record(args, metric, value, unit, ms_step, dtype, config):
 # workloads
 # ---------------------------------------------------------------------------
 
-def dense_layers(torch, S, synth, dev, shapes, T, fmt, n, m, n_sets, pairs=False, dense_backbone=False):
+def dense_layers(torch, S, synth, dev, shapes, T, fmt, n, m, n_sets, pairs=False, dense_backbone=False, w_sets=1):
     def to_dev(u16):
         return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).to(dev)
     layers = []
     for name, (K, N, norm) in shapes.items():
         xs = [to_dev(synth.activations(T, K, seed=s)) for s in range(n_sets)]
         g = to_dev(synth.gamma(K, seed=0)) if norm else None
-        w = S.sharq_quantize_weight(to_dev(synth.weight(N, K, seed=0)), fmt)
+        wsrc = to_dev(synth.weight(N, K, seed=0))
+        w = [S.sharq_quantize_weight(wsrc, fmt) for _ in range(w_sets)]   # copies at distinct addresses
+        del wsrc
         acts = [S.alloc_act(T, K, n, m, fmt, dev, pairs, dense_backbone=dense_backbone) for _ in range(n_sets)]
         ys = [torch.empty((T, N), dtype=torch.bfloat16, device=dev) for _ in range(n_sets)]
         layers.append(dict(name=name, K=K, N=N, norm=norm, xs=xs, g=g, w=w, acts=acts, ys=ys))
@@ -201,7 +204,7 @@ def dense_step(S, layers, stream, eps, n, m, fmt, n_sets, pairs=False):
             S.sharq_prepare(L["xs"][j], L["g"], eps, n, m, fmt, out=L["acts"][j], stream=stream, pairs=pairs)
             if mark:
                 mark(2 * li + 1)
-            S.sharq_linear(L["acts"][j], L["w"], out=L["ys"][j], stream=stream)
+            S.sharq_linear(L["acts"][j], L["w"][i % len(L["w"])], out=L["ys"][j], stream=stream)
         if mark:
             mark(2 * len(layers))
     return step
@@ -298,7 +301,7 @@ def llama_prefill(args, torch, S, synth, dev, stream):
 def llama_decode(args, torch, S, synth, dev, stream):
     outs = []
     for T in (1, 16, 64, 256):
-        layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T, "mx", 2, 4, 1)
+        layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T, "mx", 2, 4, 1, w_sets=DECODE_W_SETS)
         step = dense_step(S, layers, stream, synth.LLAMA_EPS, 2, 4, "mx", 1)
         ms_step, wall_ms, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
         per = per_linear(layers, tm, T, "mx", 2, 4)

@@ -1344,9 +1344,9 @@ static hipError_t go_skinny(const uint8_t* spc, const uint8_t* spm, const uint8_
   return hipGetLastError();
 }
 
-// K split for the small-M kernel: about 8192 wavefronts in flight (8 per
-// SIMD) to keep the weight stream busy, at least 4 panels per wavefront, at
-// most `cap` wavefronts per workgroup.
+// K split: about 8192 weight streams in flight (wavefronts x column
+// fragments per wavefront, for M > 16 wavefronts alone) to keep HBM busy,
+// at least 4 panels per wavefront, at most `cap` wavefronts per workgroup.
 static int skinny_split(int wgs, int K, int cap) {
   const int nks = K / kBK;
   int ks = 4;
@@ -1362,10 +1362,22 @@ static hipError_t go_skinny_m(const uint8_t* spc, const uint8_t* spm, const uint
                               const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
                               void* Y, int64_t ldy, hipStream_t st) {
   if (M <= 16) {
-    const int ks = skinny_split((N + 15) / 16, K, 16);
-    if (ks == 16) return go_skinny<1, 1, 16, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
-    if (ks == 8) return go_skinny<1, 1, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
-    return go_skinny<1, 1, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+    // Column fragments: as many as leave at least 192 workgroups (one
+    // workgroup runs on one CU), since each activation block loaded and
+    // expanded then feeds more weight columns.
+    // Measured on the Llama decode shapes with the weight streamed from HBM
+    // (µs, M = 1 / 16): qkv 6.3 / 7.6 -> 5.7 / 6.3 with 2 fragments, gate_up
+    // 19.3 / 24.2 -> 16.3 / 17.3 with 4.  Sixteen wavefronts of 4 fragments
+    // spill registers, hence the cap of 8.
+    const int nb = (N + 63) / 64 >= 192 ? 4 : (N + 31) / 32 >= 192 ? 2 : 1;
+    const int ks = skinny_split((N + 15) / 16, K, nb == 4 ? 8 : 16);
+#define SHARQ_SKINNY1(NB_, KS_) \
+  if (nb == NB_ && ks == KS_) return go_skinny<1, NB_, KS_, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+    SHARQ_SKINNY1(4, 4) SHARQ_SKINNY1(4, 8)
+    SHARQ_SKINNY1(2, 4) SHARQ_SKINNY1(2, 8) SHARQ_SKINNY1(2, 16)
+    SHARQ_SKINNY1(1, 4) SHARQ_SKINNY1(1, 8) SHARQ_SKINNY1(1, 16)
+#undef SHARQ_SKINNY1
+    return hipErrorInvalidValue;   // unreachable: (nb, ks) is one of the above
   }
   if (M <= 32) {
     if (skinny_split((N + 31) / 32, K, 8) == 8)
