@@ -36,7 +36,7 @@ namespace sharq {
 constexpr int kBM = 128;          // tile rows: 4 wavefronts x 32
 constexpr int kBK = 128;          // K per step: 4 scale blocks, 64 bytes of codes per row
 constexpr int kLdsStride = 80;    // bytes per staged weight row (64 + 16 to spread LDS banks)
-constexpr int kSkinnyMaxM = 64;   // activation rows up to which the small-M kernel runs
+constexpr int kSkinnyMaxM = 32;   // activation rows up to which the small-M kernel runs
 constexpr int kSkinnyMaxRowTiled = 256;   // ... and, when the main kernel has few tiles, up to this many
 
 __device__ __forceinline__ v8i as_operand(uint4 q) {
@@ -1380,30 +1380,47 @@ static hipError_t go_skinny_m(const uint8_t* spc, const uint8_t* spm, const uint
     return hipErrorInvalidValue;   // unreachable: (nb, ks) is one of the above
   }
   if (M <= 32) {
-    if (skinny_split((N + 31) / 32, K, 8) == 8)
-      return go_skinny<2, 2, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
-    return go_skinny<2, 2, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+    // As at M <= 16, 4 column fragments when N leaves 192 workgroups of 64
+    // columns (M = 32 gate_up from HBM: 32.1 -> 26.0 µs), else 2.
+    const int ks = skinny_split((N + 15) / 16, K, 8);
+    if ((N + 63) / 64 >= 192)
+      return ks == 8 ? go_skinny<2, 4, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st)
+                     : go_skinny<2, 4, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+    return ks == 8 ? go_skinny<2, 2, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st)
+                   : go_skinny<2, 2, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
   }
-  // Of (row fragments, column fragments, K splits) = (4, 4, 4), (2, 4, 8)
-  // and (2, 2, 8), the one whose wavefront count is nearest to 2048 (in
-  // ratio; ties to the first): measured on the Llama decode shapes at
-  // M = 64-256, fewer wavefronts leave the weight stream short of loads in
-  // flight and more re-read the weight for too many row tiles.
-  const int64_t rt64 = (M + 63) / 64, rt32 = (M + 31) / 32;
-  const int64_t w444 = ((N + 63) / 64) * rt64 * 4, w248 = ((N + 63) / 64) * rt32 * 8,
-                w228 = ((N + 31) / 32) * rt32 * 8;
-  const auto dist = [](int64_t w) { return w >= 2048 ? (double)w / 2048.0 : 2048.0 / (double)w; };
-  if (dist(w444) <= dist(w248) && dist(w444) <= dist(w228))
-    return go_skinny<4, 4, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
-  if (dist(w248) <= dist(w228))
-    return go_skinny<2, 4, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
-  return go_skinny<2, 2, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  // Above 32 rows the workgroups tile M by 32 or 64.  Of the configurations
+  // (row fragments, column fragments, K splits) below, those that leave at
+  // least 192 workgroups (one workgroup runs on one CU; fewer leave CUs
+  // idle), and of them the one whose wavefront count is nearest to 1024 in
+  // ratio (ties to the first).  Measured on the Llama decode shapes with the
+  // weight streamed from HBM (µs): M = 64 qkv 12.5 -> 11.8; M = 128 qkv
+  // 23.6 -> 19.4, down 30.1 -> 28.5.
+  struct Cfg { int mf, nb, ks; };
+  constexpr Cfg cfgs[4] = {{4, 4, 4}, {2, 4, 4}, {2, 2, 4}, {2, 2, 8}};
+  const auto wgs = [&](const Cfg& c) {
+    return (int64_t)((N + 16 * c.nb - 1) / (16 * c.nb)) * ((M + 16 * c.mf - 1) / (16 * c.mf));
+  };
+  const auto dist = [](int64_t w) { return w >= 1024 ? (double)w / 1024.0 : 1024.0 / (double)w; };
+  int best = -1;
+  for (int pass = 0; pass < 2 && best < 0; ++pass)   // pass 1 only when no configuration has 192 workgroups
+    for (int i = 0; i < 4; ++i)
+      if ((pass == 1 || wgs(cfgs[i]) >= 192) &&
+          (best < 0 || dist(wgs(cfgs[i]) * cfgs[i].ks) < dist(wgs(cfgs[best]) * cfgs[best].ks)))
+        best = i;
+  switch (best) {
+    case 0: return go_skinny<4, 4, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+    case 1: return go_skinny<2, 4, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+    case 2: return go_skinny<2, 2, 4, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+    default: return go_skinny<2, 2, 8, PAT, OutT>(spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
+  }
 }
 
-// The small-M kernel serves M <= 64, and M <= 256 while the main kernel
+// The small-M kernel serves M <= 32, and M <= 256 while the main kernel
 // would have fewer than 48 tiles of 128 x 256 (measured on the Llama decode
-// shapes: at 48 tiles the two are even, at 112 the main kernel is twice as
-// fast).
+// shapes: at 48 tiles the two are even; at 112 the main kernel is faster,
+// 32.5 against 41.1 µs for gate_up at M = 64 with the weight streamed from
+// HBM, and twice as fast at M = 128).
 static bool use_skinny(int64_t M, int N, int K) {
   if (K % kBK != 0) return false;
   if (M <= kSkinnyMaxM) return true;

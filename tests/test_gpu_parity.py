@@ -249,9 +249,9 @@ def test_llama_full_shape(S, G, name):
 
 # --------------------------------------------------------------------------- decode shapes
 
-@pytest.mark.parametrize("name,T", [("qkv", 1), ("qkv", 16), ("gate_up", 1), ("gate_up", 16), ("down", 64),
-                                    ("gate_up", 33), ("down", 5), ("qkv", 48), ("down", 100), ("qkv", 128),
-                                    ("down", 256)])
+@pytest.mark.parametrize("name,T", [("qkv", 1), ("qkv", 16), ("gate_up", 1), ("gate_up", 16), ("gate_up", 32),
+                                    ("down", 64), ("gate_up", 33), ("gate_up", 64), ("down", 5), ("qkv", 48),
+                                    ("down", 100), ("qkv", 128), ("down", 256)])
 def test_llama_decode_shape(S, G, name, T):
     """Small-M (decode) Llama-3.1-8B shapes, as the decode benchmark runs them:
     preparation in full, GEMM on every row."""
@@ -272,14 +272,15 @@ def test_llama_decode_shape(S, G, name, T):
 @pytest.mark.parametrize("T,N,K,n,m", [(7, 40, 256, 4, 8), (64, 96, 1280, 2, 4), (17, 16, 128, 2, 4),
                                        (70, 40, 256, 2, 4), (200, 96, 1280, 4, 8), (129, 4104, 512, 2, 4),
                                        (3, 12300, 256, 4, 8), (5, 12300, 4096, 2, 4), (11, 6152, 640, 2, 4),
-                                       (2, 6200, 16384, 2, 4)])
+                                       (2, 6200, 16384, 2, 4), (20, 12300, 4096, 4, 8)])
 def test_small_m_ragged(S, G, T, N, K, n, m):
     """Small-M kernel: column tails (N % 16), K ranges shorter than four panels,
     4:8, and row tiles with a ragged last tile (M > 64 with few main-kernel tiles).
     At M <= 16 a wide N takes 4 or 2 column fragments per wavefront: N = 12300
     (4 fragments, a 12-column tail; K = 256 leaves two of the four wavefronts
     without a panel, K = 4096 splits K eight ways), N = 6152 (2 fragments, an
-    8-column tail) and N = 6200 with K = 16384 (2 fragments, sixteen-way split)."""
+    8-column tail) and N = 6200 with K = 16384 (2 fragments, sixteen-way split);
+    at M = 20 the same N = 12300 takes 2 row and 4 column fragments."""
     x = synth.activations(T, K, seed=K)
     o = O.prepare(x, synth.gamma(K, seed=2), 1e-6, n, m, "mx")
     wo = O.quantize_weight(synth.weight(N, K, seed=N), "mx")
