@@ -1356,7 +1356,7 @@ static int skinny_split(int wgs, int K, int cap) {
 
 // (row fragments, column fragments, K splits) by M: every activation block
 // expansion feeds NB column fragments; the K split keeps enough wavefronts
-// streaming the weight.  Above 32 rows the workgroups tile M by 64.
+// streaming the weight.  Above 16 rows the workgroups tile M by 32 or 64.
 template <int PAT, typename OutT>
 static hipError_t go_skinny_m(const uint8_t* spc, const uint8_t* spm, const uint8_t* sps, const uint8_t* dnc,
                               const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws, int N, int K,
