@@ -7,10 +7,17 @@ fused preparation kernel followed by the two-path FP4 GEMM (2:4 backbone +
 dense residual, MXFP4, bf16 output).  Weights are quantized once before
 timing, as in inference.
 
-Printed: one JSON line with the step throughput (TFLOP/s over the two FP4
-GEMMs' executed work, prep time included), the roofline of the dominant kernel
-(the two-path GEMM, against the dense MXFP4 MFMA peak), the preparation
-kernel's HBM rate, and the CPU oracle timed on a bounded sample.
+Printed: one JSON line with the step throughput (TFLOP/s of the method's
+algorithmic work F_alg = 2 M N K (1 + n/m) -- the dense residual GEMM plus the
+n/m-sparse backbone GEMM -- prep time included; the executed work F_exec =
+4 M N K, which counts the backbone's pruned zeros that gfx950 multiplies
+anyway, and the plain linear's F_lin = 2 M N K beside it), the roofline of the
+dominant kernel (the two-path GEMM, against the dense MXFP4 MFMA peak), the
+preparation kernel's HBM rate on its algorithmic bytes, and the CPU oracle
+timed on a bounded sample.  Per-kernel times come from HIP events on the
+launch stream around every launch of the timed steps (the warmup steps carry
+the same events, so a profiler's per-kernel mean over the run covers the
+same regime).
 
 Other workloads (--workload), one JSON line each:
   llama-decode  the same three linears at M = 1, 16, 64, 256 (weight-stream bound)
@@ -69,19 +76,41 @@ def log(*a):
 
 
 def gemm_flops(T, N, K):
-    """Executed FP4 work of the two-path GEMM: backbone (expanded to dense) + residual."""
+    """Executed FP4 work of the two-path GEMM (F_exec): backbone (run dense,
+    pruned zeros included) + residual."""
     return 4.0 * T * N * K
 
 
-def prep_bytes(T, K, norm, n=2, m=4, fmt="mx", dense_backbone=False):
+def alg_flops(T, N, K, n=2, m=4):
+    """The method's algorithmic work (F_alg): the dense residual GEMM and the
+    backbone GEMM over its n of every m positions."""
+    return 2.0 * T * N * K * (1.0 + n / m)
+
+
+def lin_flops(T, N, K):
+    """The work of the plain linear layer Y = X W^T (F_lin)."""
+    return 2.0 * T * N * K
+
+
+def prep_bytes(T, K, norm, n=2, m=4, fmt="mx"):
     """Algorithmic HBM bytes of one preparation call: bf16 X (and gamma) in;
     backbone codes K n/m/2, metadata K/8, backbone scales K/32, residual codes
-    K/2 and residual scales K/32 (MXFP4) or K/16 (NVFP4) out, and K/2 for the
-    dense backbone copy when it is written."""
+    K/2 and residual scales K/32 (MXFP4) or K/16 (NVFP4) out."""
     out = K * n / m / 2 + K / 8 + K / 32 + K / 2 + (K / 32 if fmt == "mx" else K / 16)
-    if dense_backbone:
-        out += K / 2
     return 2.0 * T * K + (2.0 * K if norm else 0.0) + T * out
+
+
+def prep_bytes_written(T, K, norm, n=2, m=4, fmt="mx", backbone="compressed"):
+    """Bytes a preparation call actually moves: as prep_bytes with the
+    backbone stored compressed ("compressed"), as the dense copy beside it
+    ("both", K/2 more per row) or as the dense copy alone ("dense-only": K/2
+    instead of K n/m/2 + K/8)."""
+    b = prep_bytes(T, K, norm, n, m, fmt)
+    if backbone == "both":
+        b += T * K / 2
+    elif backbone == "dense-only":
+        b += T * (K / 2 - K * n / m / 2 - K / 8)
+    return b
 
 
 def weight_bytes(N, K, fmt="mx"):
@@ -102,10 +131,24 @@ def cpu_threads():
         return 1
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or None
+
+
 def cpu_baseline(rows=T_TOKENS, min_seconds=10.0, max_passes=3):
     """The CPU oracle on a bounded sample of the same step: `rows` of the 2048
     token rows of each linear (preparation + two-path fp64 GEMM), repeated
-    until about `min_seconds` of CPU work (at most `max_passes` passes)."""
+    until about `min_seconds` of CPU work (at most `max_passes` passes).  The
+    oracle's preparation is NumPy element-wise work on one thread; its GEMM is
+    a float64 matrix product on the BLAS threads (`cores`).  value counts the
+    same algorithmic work as the GPU line (F_alg)."""
     from oracle import sharq_oracle as O
     from paper_2606_26587_amd import synth
     cases = []
@@ -114,20 +157,25 @@ def cpu_baseline(rows=T_TOKENS, min_seconds=10.0, max_passes=3):
         g = synth.gamma(K, seed=0) if norm else None
         cases.append((K, N, x, g, O.quantize_weight(synth.weight(N, K, seed=0))))
     flops = 0.0
-    elapsed = 0.0
+    t_prep = t_gemm = 0.0
     passes = 0
-    while passes < max_passes and (passes == 0 or elapsed < min_seconds):
+    while passes < max_passes and (passes == 0 or t_prep + t_gemm < min_seconds):
         for K, N, x, g, wq in cases:
             t0 = time.perf_counter()
             a = O.prepare(x, g, synth.LLAMA_EPS, 2, 4, "mx")
+            t1 = time.perf_counter()
             O.linear(a, wq)
-            elapsed += time.perf_counter() - t0
-            flops += gemm_flops(rows, N, K)
+            t2 = time.perf_counter()
+            t_prep += t1 - t0
+            t_gemm += t2 - t1
+            flops += alg_flops(rows, N, K)
         passes += 1
+    elapsed = t_prep + t_gemm
     return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": cpu_threads(), "kind": "oracle",
             "sample": f"{passes} pass(es) over {rows} of the {T_TOKENS} token rows of each Llama linear "
                       f"(qkv, gate_up, down): NumPy preparation + fp64 two-path GEMM; weight quantization untimed",
-            "seconds": elapsed, "host_cpus": len(os.sched_getaffinity(0)), "cpu": platform.processor() or None}
+            "seconds": elapsed, "prep_seconds_1_thread": t_prep, "gemm_seconds_blas_threads": t_gemm,
+            "host_cpus": len(os.sched_getaffinity(0)), "cpu": cpu_model()}
 
 
 class Timer:
@@ -145,26 +193,25 @@ class Timer:
 
 
 def run_steps(torch, stream, step, n_ops, steps, warmup):
-    """Warm up, then time exactly `steps` steps synchronized on both sides
-    (nothing but the steps' own launches in the timed region).  The same
-    steps then run once more with every op bracketed by HIP events on the
-    launch stream, for the per-kernel breakdown."""
+    """Warm up, then time exactly `steps` steps synchronized on both sides.
+    Every op of every step -- warmup and timed alike -- is bracketed by HIP
+    events on the launch stream, so the per-kernel times are those of the
+    timed steps themselves and a profiler's per-kernel mean over the whole run
+    sees the same launch pattern."""
+    tw = Timer(torch, stream, n_ops, max(warmup, 1))
     for i in range(warmup):
-        step(i, None)
+        step(i, lambda k, i=i: tw.mark(i, k))
     torch.cuda.synchronize()
+    tm = Timer(torch, stream, n_ops, steps)
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t0.record(stream)
     for i in range(steps):
-        step(i, None)
+        step(i, lambda k, i=i: tm.mark(i, k))
     t1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    tm = Timer(torch, stream, n_ops, steps)
-    for i in range(steps):
-        step(i, lambda k, i=i: tm.mark(i, k))
-    torch.cuda.synchronize()
     return t0.elapsed_time(t1) / steps, wall * 1e3 / steps, tm
 
 
@@ -178,7 +225,7 @@ def base_record(args, metric, value, unit, ms_step, dtype, config):
 # workloads
 # ---------------------------------------------------------------------------
 
-def dense_layers(torch, S, synth, dev, shapes, T, fmt, n, m, n_sets, pairs=False, dense_backbone=False, w_sets=1):
+def dense_layers(torch, S, synth, dev, shapes, T, fmt, n, m, n_sets, pairs=False, backbone="compressed", w_sets=1):
     def to_dev(u16):
         return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).to(dev)
     layers = []
@@ -188,7 +235,8 @@ def dense_layers(torch, S, synth, dev, shapes, T, fmt, n, m, n_sets, pairs=False
         wsrc = to_dev(synth.weight(N, K, seed=0))
         w = [S.sharq_quantize_weight(wsrc, fmt) for _ in range(w_sets)]   # copies at distinct addresses
         del wsrc
-        acts = [S.alloc_act(T, K, n, m, fmt, dev, pairs, dense_backbone=dense_backbone) for _ in range(n_sets)]
+        acts = [S.alloc_act(T, K, n, m, fmt, dev, pairs, dense_backbone=backbone == "both",
+                            dense_only=backbone == "dense-only") for _ in range(n_sets)]
         ys = [torch.empty((T, N), dtype=torch.bfloat16, device=dev) for _ in range(n_sets)]
         layers.append(dict(name=name, K=K, N=N, norm=norm, xs=xs, g=g, w=w, acts=acts, ys=ys))
     torch.cuda.synchronize()
@@ -210,20 +258,24 @@ def dense_step(S, layers, stream, eps, n, m, fmt, n_sets, pairs=False):
     return step
 
 
-def per_linear(layers, tm, T, fmt, n, m, dense_backbone=False):
+def per_linear(layers, tm, T, fmt, n, m, backbone="compressed"):
     per = []
     for li, L in enumerate(layers):
         prep_ms, gemm_ms = tm.op_ms(2 * li), tm.op_ms(2 * li + 1)
-        f = gemm_flops(T, L["N"], L["K"])
-        b = prep_bytes(T, L["K"], L["norm"], n, m, fmt, dense_backbone)
+        f = alg_flops(T, L["N"], L["K"], n, m)
+        fx = gemm_flops(T, L["N"], L["K"])
+        b = prep_bytes(T, L["K"], L["norm"], n, m, fmt)
+        bw = prep_bytes_written(T, L["K"], L["norm"], n, m, fmt, backbone)
         wb = weight_bytes(L["N"], L["K"], fmt)
         per.append({"linear": L["name"], "K": L["K"], "N": L["N"], "rmsnorm": L["norm"],
                     "prep_us": prep_ms * 1e3, "prep_bytes": b, "prep_GBps": b / (prep_ms * 1e-3) / 1e9,
-                    "gemm_us": gemm_ms * 1e3, "gemm_flops": f, "gemm_TFLOPs": f / (gemm_ms * 1e-3) / 1e12,
+                    "prep_bytes_moved": bw, "gemm_us": gemm_ms * 1e3, "gemm_flops_alg": f,
+                    "gemm_TFLOPs": f / (gemm_ms * 1e-3) / 1e12, "gemm_flops_exec": fx,
+                    "gemm_TFLOPs_exec": fx / (gemm_ms * 1e-3) / 1e12,
                     "weight_bytes": wb, "weight_GBps": wb / (gemm_ms * 1e-3) / 1e9})
         log(f"[bench] {L['name']:8s} T={T:5d} prep {prep_ms * 1e3:8.2f} us {per[-1]['prep_GBps']:8.1f} GB/s | "
-            f"gemm {gemm_ms * 1e3:8.2f} us {per[-1]['gemm_TFLOPs']:8.1f} TFLOP/s "
-            f"{per[-1]['weight_GBps']:8.1f} GB/s of weight")
+            f"gemm {gemm_ms * 1e3:8.2f} us {per[-1]['gemm_TFLOPs']:8.1f} TFLOP/s alg "
+            f"({per[-1]['gemm_TFLOPs_exec']:.1f} exec) {per[-1]['weight_GBps']:8.1f} GB/s of weight")
     return per
 
 
@@ -253,38 +305,53 @@ def copy_same_bytes(torch, dev, stream, nbytes, reps=20):
 
 
 def llama_prefill(args, torch, S, synth, dev, stream):
-    dense_bb = not args.compressed_backbone
+    backbone = args.backbone
     layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T_TOKENS, "mx", 2, 4, N_INPUT_SETS,
-                          dense_backbone=dense_bb)
-    log(f"[bench] set up {len(layers)} linears, M={T_TOKENS}")
+                          backbone=backbone)
+    log(f"[bench] set up {len(layers)} linears, M={T_TOKENS}, backbone stored {backbone}")
     step = dense_step(S, layers, stream, synth.LLAMA_EPS, 2, 4, "mx", N_INPUT_SETS)
     ms_step, wall_ms, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
     log(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step (wall {wall_ms:.4f} ms/step)")
-    per = per_linear(layers, tm, T_TOKENS, "mx", 2, 4, dense_bb)
-    flops_step = sum(p["gemm_flops"] for p in per)
+    per = per_linear(layers, tm, T_TOKENS, "mx", 2, 4, backbone)
+    f_alg = sum(p["gemm_flops_alg"] for p in per)
+    f_exec = sum(p["gemm_flops_exec"] for p in per)
+    f_lin = sum(lin_flops(T_TOKENS, p["N"], p["K"]) for p in per)
     t_gemm = sum(p["gemm_us"] for p in per) * 1e-6
     t_prep = sum(p["prep_us"] for p in per) * 1e-6
     bytes_prep = sum(p["prep_bytes"] for p in per)
-    gemm_tf = flops_step / t_gemm / 1e12
+    bytes_moved = sum(p["prep_bytes_moved"] for p in per)
+    gemm_tf = f_alg / t_gemm / 1e12
     prep_gbps = bytes_prep / t_prep / 1e9
     traffic = None
     if TRAFFIC is not None and TRAFFIC["gemm_source"] == gemm_source_digest():
         traffic = TRAFFIC["bytes_per_launch"]
+    step_s = ms_step * 1e-3
     out = base_record(
-        args, METRIC, flops_step / (ms_step * 1e-3) / 1e12, "TFLOP/s", ms_step, "mxfp4",
+        args, METRIC, f_alg / step_s / 1e12, "TFLOP/s", ms_step, "mxfp4",
         {"workload": "Llama-3.1-8B prefill linears qkv (K4096,N6144,RMSNorm), gate_up (K4096,N28672,"
                      "RMSNorm), down (K14336,N4096); M=2048 tokens; 2:4 backbone; MXFP4; bf16 out",
-         "tokens": T_TOKENS, "pattern": "2:4", "format": "MXFP4", "flops_per_step": flops_step,
-         "backbone_for_gemm": "dense copy written by the preparation" if dense_bb else "compressed, expanded in the GEMM",
-         "flops_counting": "4*M*N*K per linear (two dense-executed FP4 GEMMs)"})
-    kern = "k_linear_mx_persist<0> (two-path FP4 GEMM, dense backbone copy)" if dense_bb else \
-        "k_linear_mx_persist<24> (two-path FP4 GEMM, backbone expanded in registers)"
+         "tokens": T_TOKENS, "pattern": "2:4", "format": "MXFP4", "flops_per_step": f_alg,
+         "backbone_for_gemm": {"dense-only": "dense copy alone, written by the preparation",
+                               "both": "dense copy written beside the compressed backbone",
+                               "compressed": "compressed, expanded in the GEMM"}[backbone],
+         "flops_counting": "F_alg = 2*M*N*K*(1+n/m) per linear (dense residual GEMM + 2:4 backbone GEMM)",
+         "flops_exec_per_step": f_exec, "flops_lin_per_step": f_lin,
+         "exec_TFLOPs": f_exec / step_s / 1e12, "lin_TFLOPs": f_lin / step_s / 1e12})
+    kern = {"dense-only": "k_linear_mx_persist<0> (two-path FP4 GEMM reading the dense backbone copy)",
+            "both": "k_linear_mx_persist<0> (two-path FP4 GEMM reading the dense backbone copy)",
+            "compressed": "k_linear_mx_persist<24> (two-path FP4 GEMM, backbone expanded in registers)"}[backbone]
     out["roofline"] = {"bound": "mfma", "kernel": kern, "achieved": gemm_tf,
                        "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s", "frac": gemm_tf / PEAK_FP4_TFLOPS,
-                       "traffic": traffic, "flops_per_launch": flops_step / len(per),
-                       "us_per_launch": t_gemm * 1e6 / len(per)}
-    out["prep"] = {"bound": "hbm", "kernel": "k_prep_norm_split / k_prep_blocks (fused preparation)",
-                   "achieved": prep_gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": prep_gbps / PEAK_HBM_GBPS}
+                       "traffic": traffic, "flops_per_launch": f_alg / len(per),
+                       "us_per_launch": t_gemm * 1e6 / len(per), "flops": "F_alg",
+                       "achieved_exec": f_exec / t_gemm / 1e12, "frac_exec": f_exec / t_gemm / 1e12 / PEAK_FP4_TFLOPS,
+                       "achieved_lin": f_lin / t_gemm / 1e12}
+    out["prep"] = {"bound": "hbm", "kernel": "k_prep_norm_split (qkv, gate_up) / k_prep_blocks (down)",
+                   "achieved": prep_gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": prep_gbps / PEAK_HBM_GBPS,
+                   "bytes_per_step": bytes_prep,
+                   "bytes": "2 M K (X) + 2 K (gamma) + M K (n/m/2 + 1/8 + 1/32 + 1/2 + 1/32) (prepared outputs)",
+                   "bytes_moved_per_step": bytes_moved,
+                   "moved_GBps": bytes_moved / t_prep / 1e9}
     # the same bytes moved by a plain device copy, one launch per linear
     copy_us = [copy_same_bytes(torch, dev, stream, p["prep_bytes"]) for p in per]
     for p, cu in zip(per, copy_us):
@@ -292,7 +359,9 @@ def llama_prefill(args, torch, S, synth, dev, stream):
     copy_gbps = bytes_prep / (sum(copy_us) * 1e-6) / 1e9
     out["prep"]["copy_same_bytes"] = {"achieved": copy_gbps, "unit": "GB/s", "frac": copy_gbps / PEAK_HBM_GBPS,
                                       "prep_vs_copy": prep_gbps / copy_gbps}
-    log(f"[bench] prep {prep_gbps:.0f} GB/s; a device copy of the same bytes {copy_gbps:.0f} GB/s")
+    log(f"[bench] prep {prep_gbps:.0f} GB/s algorithmic ({bytes_moved / t_prep / 1e9:.0f} GB/s moved); "
+        f"a device copy of the same bytes {copy_gbps:.0f} GB/s; GEMM {gemm_tf:.0f} TFLOP/s alg, "
+        f"{f_exec / t_gemm / 1e12:.0f} exec")
     out["per_linear"] = per
     out["wall_ms_per_step"] = wall_ms
     return out
@@ -327,7 +396,7 @@ def qwen_nvfp4(args, torch, S, synth, dev, stream):
     step = dense_step(S, layers, stream, 1e-6, 2, 4, "nv", N_INPUT_SETS)
     ms_step, wall_ms, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
     per = per_linear(layers, tm, T, "nv", 2, 4)
-    flops = sum(p["gemm_flops"] for p in per)
+    flops = sum(p["gemm_flops_alg"] for p in per)
     t_gemm = sum(p["gemm_us"] for p in per) * 1e-6
     t_prep = sum(p["prep_us"] for p in per) * 1e-6
     pb = sum(p["prep_bytes"] for p in per)
@@ -352,7 +421,7 @@ def llama_nvfp4_pairs(args, torch, S, synth, dev, stream):
     step = dense_step(S, layers, stream, synth.LLAMA_EPS, 4, 8, "nv", N_INPUT_SETS, True)
     ms_step, wall_ms, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
     per = per_linear(layers, tm, T_TOKENS, "nv", 4, 8)
-    flops = sum(p["gemm_flops"] for p in per)
+    flops = sum(p["gemm_flops_alg"] for p in per)
     t_gemm = sum(p["gemm_us"] for p in per) * 1e-6
     t_prep = sum(p["prep_us"] for p in per) * 1e-6
     pb = sum(p["prep_bytes"] for p in per)
@@ -389,8 +458,8 @@ def moe(args, torch, S, synth, dev, stream):
                             for e in range(E)])
     ri = torch.from_numpy(ridx).to(dev)
     of = torch.from_numpy(offs).to(dev)
-    a1 = S.alloc_act(T, H, 4, 8, "mx", dev, dense_backbone=True)
-    a2 = S.alloc_act(total, I, 4, 8, "mx", dev, dense_backbone=True)
+    a1 = S.alloc_act(T, H, 4, 8, "mx", dev, dense_only=True)
+    a2 = S.alloc_act(total, I, 4, 8, "mx", dev, dense_only=True)
     y1 = torch.empty((total, 2 * I), dtype=torch.bfloat16, device=dev)
     y2 = torch.empty((total, H), dtype=torch.bfloat16, device=dev)
     torch.cuda.synchronize()
@@ -412,7 +481,7 @@ def moe(args, torch, S, synth, dev, stream):
             mark(4)
 
     ms_step, wall_ms, tm = run_steps(torch, stream, step, 4, args.steps, args.warmup)
-    f1, f2 = gemm_flops(total, 2 * I, H), gemm_flops(total, H, I)
+    f1, f2 = alg_flops(total, 2 * I, H, 4, 8), alg_flops(total, H, I, 4, 8)
     ops = {"prep_gate_up_us": tm.op_ms(0) * 1e3, "grouped_gate_up_us": tm.op_ms(1) * 1e3,
            "prep_down_us": tm.op_ms(2) * 1e3, "grouped_down_us": tm.op_ms(3) * 1e3}
     t_g = (tm.op_ms(1) + tm.op_ms(3)) * 1e-3
@@ -442,7 +511,7 @@ def llama_fused(args, torch, S, synth, dev, stream):
     for name, (K, N, norm) in synth.LLAMA_LINEARS.items():
         L[name] = dict(K=K, N=N, norm=norm, w=S.sharq_quantize_weight(to_dev(synth.weight(N, K, seed=0))),
                        g=to_dev(synth.gamma(K, seed=0)) if norm else None,
-                       act=S.alloc_act(T, K, 2, 4, "mx", dev, dense_backbone=True),
+                       act=S.alloc_act(T, K, 2, 4, "mx", dev, dense_only=True),
                        y=torch.empty((T, N), dtype=torch.bfloat16, device=dev))
     H = synth.LLAMA_LINEARS["qkv"][0]
     I = synth.LLAMA_LINEARS["down"][0]
@@ -477,7 +546,7 @@ def llama_fused(args, torch, S, synth, dev, stream):
             mark(6)
 
     ms_step, wall_ms, tm = run_steps(torch, stream, step, 6, args.steps, args.warmup)
-    flops = sum(gemm_flops(T, v["N"], v["K"]) for v in L.values())
+    flops = sum(alg_flops(T, v["N"], v["K"]) for v in L.values())
     # algorithmic bytes of the fused preparations: x and res read, h written
     # (and gamma read) for the residual adds; gate and up read for SiLU.mul;
     # the prepared activation written (0.9375 B per element at MXFP4 2:4)
@@ -596,8 +665,10 @@ def main():
                     choices=["llama-prefill", "llama-decode", "qwen-nvfp4", "llama-nvfp4-pairs", "moe",
                              "ablation", "llama-fused"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--compressed-backbone", action="store_true",
-                    help="prefill: let the GEMM expand the compressed backbone instead of reading the dense copy")
+    ap.add_argument("--backbone", default="dense-only", choices=["dense-only", "both", "compressed"],
+                    help="prefill: how the preparation stores the backbone for the GEMM -- the dense copy alone "
+                         "(default), the dense copy beside the compressed form, or the compressed form only "
+                         "(the GEMM then expands it)")
     ap.add_argument("--cpu-rows", type=int, default=T_TOKENS)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
     args = ap.parse_args()

@@ -92,6 +92,17 @@ typedef struct {
 } sharq_pattern;
 
 /*
+ * E8M0 scale rule of MXFP4 (ablation flag).  SHARQ_SCALE_FLOOR, the default,
+ * is the OCP Microscaling rule e = floor(log2 amax) - 2: a block peak above
+ * 6 * 2^e saturates at 6.  SHARQ_SCALE_CEIL takes e = ceil(log2(amax / 6)),
+ * the group scale amax / 6 of Sec. 3.1 eq. "group-quant" rounded up to a
+ * power of two so that nothing clips (App. A.1.1: a power-of-two scale cannot
+ * bring every block peak to the E2M1 maximum).  Both clamp at -127 and give
+ * -127 to an all-zero block.  Built for MXFP4 in SHARQ_MODE_SHARQ.
+ */
+typedef enum { SHARQ_SCALE_FLOOR = 0, SHARQ_SCALE_CEIL = 1 } sharq_scale_rule;
+
+/*
  * Path combination of a prepared activation (Sec. 4.4, table
  * "ablation-combination"; Sec. 3.1 eq. "direct-sparse-quant"; the
  * round-to-nearest FP4 rows of table "ablation-format").  Every mode has two
@@ -158,6 +169,23 @@ typedef enum {
  *                             matrix instruction, so the backbone runs dense
  *                             anyway, and the copy (K/2 more bytes per row)
  *                             takes the expansion out of every column tile.
+ *                             Dense-only form: with sp_dense given, sp_codes
+ *                             and sp_meta may both be NULL (K a multiple of
+ *                             128, SHARQ_MODE_SHARQ); the preparation then
+ *                             writes the backbone as the dense copy alone
+ *                             (0.5 B per element instead of 0.375 + 0.5), and
+ *                             every GEMM reads that copy.
+ *   scale_rule                sharq_scale_rule of both paths' E8M0 scales
+ *                             (MXFP4; SHARQ_SCALE_FLOOR = 0 by default).
+ *   dbg_mask [rows][K/8]      optional (NULL = none) debug output of
+ *                             sharq_prepare: the N:M keep mask, bit p of every
+ *                             group of 8 positions set when position p was
+ *                             kept, laid out like the 4:8 metadata (4 bytes
+ *                             per 32 positions, panel-major); 4-byte aligned.
+ *   dbg_r    [rows] fp32      optional debug output: the RMSNorm reciprocal r
+ *                             of every row (written only when gamma is given).
+ *                             Both are for parity triage; MXFP4 and NVFP4,
+ *                             SHARQ_MODE_SHARQ.
  *
  * Other modes: path 1 lives in sp_codes / sp_meta / sp_scale and path 2 in
  * dn_codes / dn_meta / dn_scale.  A sparse path has the backbone layout above
@@ -180,6 +208,9 @@ typedef struct {
   sharq_mode mode;
   uint8_t *dn_meta;
   uint8_t *sp_dense;
+  sharq_scale_rule scale_rule;
+  uint8_t *dbg_mask;
+  float *dbg_r;
 } sharq_act;
 
 /*
@@ -200,6 +231,8 @@ typedef struct {
  *   both paths (scale_dn unused, may equal `scale`).
  *   tensor_scale [experts]       NVFP4 per-tensor scale(s) S_w (device);
  *                                MXFP4: unused.
+ *   scale_rule                   MXFP4: the sharq_scale_rule sharq_quantize_weight
+ *                                applies (the GEMMs ignore it).
  */
 typedef struct {
   int64_t N, K, experts;
@@ -208,6 +241,7 @@ typedef struct {
   uint8_t *scale;
   uint8_t *scale_dn;
   float *tensor_scale;
+  sharq_scale_rule scale_rule;
 } sharq_weight;
 
 /* Bytes of each buffer of a prepared activation / quantized weight (host-side
@@ -226,10 +260,13 @@ SHARQ_API size_t sharq_act_buffer_bytes_mode(int64_t rows, int64_t K, sharq_form
  * F32) once into the shared FP4 payload and its scale views (Fig. 2 "weight
  * preparation").  MXFP4: per row, per 32 K values, E8M0 = floor(log2 amax) - 2
  * (OCP rule, clamped at -127), codes = E2M1(w / 2^e), ties to even, saturating.
+ * (out->scale_rule = SHARQ_SCALE_CEIL: ceil(log2(amax / 6)) instead).
  * NVFP4: S_w = amax(W)/2688 computed on the device, E4M3 per 32, dense view
  * duplicated per 16.  HiF4: units of 64 along K, the conversion of the HiF4
  * appendix (its algorithm "bf16-to-hif4") on the fp32 values.  `out` fields
- * N, K, fmt and the buffers must be set by the caller; experts must be 1.
+ * N, K, fmt, scale_rule and the buffers must be set by the caller; experts
+ * must be 1.  The format and the rule travel in `out` rather than as
+ * arguments, so that the weight descriptor records what its bytes mean.
  */
 SHARQ_API sharq_status sharq_quantize_weight(const void *W, sharq_dtype wdt, int64_t N, int64_t K, int64_t ldw,
                                    sharq_weight *out, void *stream);
@@ -316,9 +353,14 @@ SHARQ_API sharq_status sharq_linear(const sharq_act *a, const sharq_weight *w, v
                           int64_t ldy, void *stream);
 
 /*
- * Grouped form for mixture-of-experts layers: for every expert e and every
- * i in [expert_offsets[e], expert_offsets[e+1]),
+ * Grouped form for mixture-of-experts layers (the MoE configuration of the
+ * paper's evaluation, Sec. 4.1-4.2, Qwen3-30B-A3B): the two-path output of
+ * Sec. 3.3 eq. "sharq-output" applied per expert to the rows routed to it.
+ * For every expert e and every i in [expert_offsets[e], expert_offsets[e+1]),
  *   Y[i] = SharQ(A[row_index ? row_index[i] : i], W_e).
+ * The experts' weights are stacked in one sharq_weight (w->experts of them,
+ * one shape) rather than passed as an array of descriptors, so that the
+ * kernel reads every expert's payload from one base pointer.
  * expert_offsets: device int32 [w->experts + 1], non-decreasing, first 0,
  * last == total.  row_index: device int32 [total], each in [0, a->rows), or
  * NULL.  Y [total][N] (row stride ldy).  Offsets are read on the device; the

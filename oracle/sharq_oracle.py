@@ -77,6 +77,13 @@ Readings where the paper is silent (each also listed in the design notes):
       h = bf16(SiLU(g) * u) with SiLU(g) = g / (1 + exp(-g)), the product
       evaluated in fp64 and rounded to bf16 once (nearest even); the
       preparation then works on h.
+  R13 E8M0 scale rule as an ablation flag (MXFP4).  Besides the OCP floor
+      rule of R4, the "ceil" rule e = ceil(log2(amax / 6)): eq.
+      "group-quant" sets s = amax / 6, which E8M0 cannot hold, and App. A.1.1
+      notes that a power-of-two scale cannot bring every block peak to the
+      E2M1 maximum; rounding s up to a power of two keeps every value within
+      range (no clipping) at the price of the top binade.  It applies to both
+      paths of the preparation and to the weight.
 """
 
 from __future__ import annotations
@@ -146,14 +153,28 @@ def _floor_log2_f32(a: np.ndarray) -> np.ndarray:
     return np.where(expf > 0, expf - 127, sub)
 
 
-def e8m0_exponent(amax: np.ndarray) -> np.ndarray:
+def e8m0_exponent(amax: np.ndarray, rule: str = "floor") -> np.ndarray:
     """Shared MXFP4 exponent of a block with max magnitude amax (reading R4).
 
-    OCP Microscaling rule: e = floor(log2 amax) - emax(E2M1), emax = 2, clamped
-    to the E8M0 minimum -127; an all-zero block takes -127 (code 0).
+    rule "floor" (the default, OCP Microscaling): e = floor(log2 amax) -
+    emax(E2M1), emax = 2; the block peak may exceed 6 * 2^e and then
+    saturates.  rule "ceil" (R13): e = ceil(log2(amax / 6)), the smallest
+    power-of-two scale under which the peak does not exceed the E2M1 maximum
+    -- eq. "group-quant"'s s = amax / 6 rounded up to a power of two, so
+    nothing clips.  With E = floor(log2 amax), 6 * 2^(E-2) = 1.5 * 2^E, so
+    the ceil rule is E - 2 when amax / 2^E <= 1.5 and E - 1 above.  Both are
+    clamped to the E8M0 minimum -127; an all-zero block takes -127 (code 0).
     """
     amax = np.asarray(amax, dtype=np.float32)
-    e = np.maximum(_floor_log2_f32(np.where(amax > 0, amax, np.float32(1.0))) - 2, -127)
+    pos = np.where(amax > 0, amax, np.float32(1.0))
+    E = _floor_log2_f32(pos)
+    e = E - 2
+    if rule == "ceil":
+        frac = np.ldexp(pos.astype(np.float64), -E)   # amax / 2^E in [1, 2), exact
+        e = e + (frac > 1.5)
+    elif rule != "floor":
+        raise ValueError(rule)
+    e = np.maximum(e, -127)
     return np.where(amax > 0, e, -127).astype(np.int64)
 
 
@@ -312,13 +333,14 @@ def nm_pair_mask(y: np.ndarray, n: int, m: int) -> np.ndarray:
 # MXFP4 block quantization (eq. group-quant with an E8M0 block scale)
 # ---------------------------------------------------------------------------
 
-def mx_quantize(vals: np.ndarray, present: np.ndarray | None = None):
+def mx_quantize(vals: np.ndarray, present: np.ndarray | None = None, rule: str = "floor"):
     """Quantize rows of fp32 values to MXFP4 in blocks of 32 along K.
 
     `present` marks the positions that belong to the tensor (the backbone's kept
     positions); the block amax is taken over those only and the others get
-    code 0.  Returns (codes uint8 [T,K], exponent int [T,K/32], scale code
-    uint8 [T,K/32], dequantized values fp32 [T,K]).
+    code 0.  `rule` is the E8M0 rule of e8m0_exponent.  Returns (codes uint8
+    [T,K], exponent int [T,K/32], scale code uint8 [T,K/32], dequantized
+    values fp32 [T,K]).
     """
     v = np.asarray(vals, dtype=np.float32)
     T, K = v.shape
@@ -326,7 +348,7 @@ def mx_quantize(vals: np.ndarray, present: np.ndarray | None = None):
         present = np.ones(v.shape, dtype=bool)
     mag = np.where(present, np.abs(v), np.float32(0.0)).reshape(T, K // MX_BLOCK, MX_BLOCK)
     amax = mag.max(axis=2)
-    e = e8m0_exponent(amax)
+    e = e8m0_exponent(amax, rule)
     e_full = np.repeat(e, MX_BLOCK, axis=1)
     # v / 2^e: exact division by a power of two (fp32, correctly rounded);
     # positions outside `present` may overflow here and are discarded below
@@ -499,7 +521,7 @@ def hif4_decode(codes: np.ndarray, meta: np.ndarray) -> np.ndarray:
 
 
 # ---------------------------------------------------------------------------
-# Packing into the library's buffer layout
+# Packing: the compressed backbone and two codes per byte
 # ---------------------------------------------------------------------------
 
 def pack_nibbles(codes: np.ndarray) -> np.ndarray:
@@ -563,43 +585,8 @@ def unpack_backbone(sp_codes: np.ndarray, sp_meta: np.ndarray, K: int, n: int, m
 
 
 # ---------------------------------------------------------------------------
-# Panel-major buffer layout of the library (data movement only)
+# Names and row widths of the packed buffers
 # ---------------------------------------------------------------------------
-
-PANEL_K = 128
-
-
-def to_panels(rowmajor: np.ndarray, K: int) -> np.ndarray:
-    """Row-major [R, bytes(K)] -> flat panel-major bytes.
-
-    Every buffer holds a fixed number of bytes per 32 K positions, so K splits
-    into panels of 128 positions (the last one may be narrower); panel p stores
-    the bytes of all R rows for its K range, row after row, and panels follow
-    each other.
-    """
-    a = np.asarray(rowmajor, dtype=np.uint8)
-    R, B = a.shape
-    per32 = B // (K // 32)
-    parts = []
-    for lo in range(0, K, PANEL_K):
-        hi = min(lo + PANEL_K, K)
-        parts.append(a[:, lo // 32 * per32: hi // 32 * per32].reshape(-1))
-    return np.concatenate(parts) if parts else np.zeros(0, np.uint8)
-
-
-def from_panels(flat: np.ndarray, R: int, K: int, bytes_per_row: int) -> np.ndarray:
-    """Inverse of to_panels: flat panel-major bytes -> row-major [R, bytes_per_row]."""
-    flat = np.asarray(flat, dtype=np.uint8).reshape(-1)
-    per32 = bytes_per_row // (K // 32)
-    out = np.zeros((R, bytes_per_row), dtype=np.uint8)
-    off = 0
-    for lo in range(0, K, PANEL_K):
-        hi = min(lo + PANEL_K, K)
-        w = (hi - lo) // 32 * per32
-        out[:, lo // 32 * per32: hi // 32 * per32] = flat[off: off + R * w].reshape(R, w)
-        off += R * w
-    return out
-
 
 ACT_BUFFERS = ("sp_codes", "sp_meta", "sp_scale", "dn_codes", "dn_scale")
 #: every buffer a prepared activation may use (dn_meta: a sparse second path)
@@ -625,44 +612,13 @@ def act_widths(K: int, n: int, m: int, fmt: str, mode: str = "sharq") -> dict:
     return {"sp_codes": c1, "sp_meta": m1, "sp_scale": s1, "dn_codes": c2, "dn_meta": m2, "dn_scale": s2}
 
 
-def act_to_device_layout(act: dict) -> dict:
-    """The prepared-activation buffers in the library's panel-major layout."""
-    return {k: to_panels(act[k], act["K"]) for k in ACT_BUFFERS_ALL if k in act}
-
-
-def act_from_device_layout(bufs: dict, rows: int, K: int, n: int, m: int, fmt: str, tensor_scale=None,
-                           mode: str = "sharq", pairs: bool = False) -> dict:
-    """Panel-major device buffers -> the row-major dict the oracle's GEMM reads."""
-    widths = act_widths(K, n, m, fmt, mode)
-    d = {"rows": rows, "K": K, "n": n, "m": m, "fmt": fmt, "tensor_scale": tensor_scale, "mode": mode,
-         "pairs": pairs}
-    for k in ACT_BUFFERS_ALL:
-        if widths[k] == 0:
-            d[k] = np.zeros((rows, 0), np.uint8)
-        else:
-            d[k] = from_panels(bufs[k], rows, K, widths[k])
-    return d
-
-
-def weight_to_device_layout(wq: dict) -> dict:
-    return {k: to_panels(wq[k], wq["K"]) for k in WEIGHT_BUFFERS}
-
-
-def weight_from_device_layout(bufs: dict, N: int, K: int, fmt: str, tensor_scale=None) -> dict:
-    widths = {"codes": K // 2, "scale": K // 16 if fmt == "hif4" else K // 32,
-              "scale_dn": K // 32 if fmt == "mx" else K // 16}
-    d = {"N": N, "K": K, "fmt": fmt, "tensor_scale": tensor_scale}
-    for k in WEIGHT_BUFFERS:
-        d[k] = from_panels(bufs[k], N, K, widths[k])
-    return d
-
-
 # ---------------------------------------------------------------------------
 # Preparation (Sec. 3.3 eqs. sharq-sparse-backbone / quantized-backbone / residual)
 # ---------------------------------------------------------------------------
 
 def prepare(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: int, m: int,
-            fmt: str = "mx", tensor_scale: float | None = None, pairs: bool = False) -> dict:
+            fmt: str = "mx", tensor_scale: float | None = None, pairs: bool = False,
+            scale_rule: str = "floor") -> dict:
     """Activation preparation for one linear call.
 
     1. y = RMSNorm(x) * gamma (or y = x);
@@ -670,8 +626,11 @@ def prepare(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: in
     3. backbone: quantize y on the kept positions (X_sp = M(X) o X, then Q_sp);
     4. residual R = y - D_sp(Q_sp(X_sp)), taken against the dequantized backbone;
     5. quantize R densely (Q_dn).
+    scale_rule (MXFP4): the E8M0 rule of both paths, "floor" or "ceil" (R13).
     Returns the packed buffers plus debug arrays.
     """
+    if scale_rule != "floor" and fmt != "mx":
+        raise ValueError("the E8M0 scale rule applies to MXFP4 only")
     x = bf16_bits_to_f32(x_bf16)
     T, K = x.shape
     g = None if gamma_bf16 is None else bf16_bits_to_f32(gamma_bf16)
@@ -684,10 +643,11 @@ def prepare(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: in
         keep = nm_mask(y, n, m)
     out = {"rows": T, "K": K, "n": n, "m": m, "pairs": pairs, "fmt": fmt, "y": y, "r": r, "keep": keep}
     if fmt == "mx":
-        sp_c, _, sp_s, d_sp = mx_quantize(y, keep)
+        sp_c, _, sp_s, d_sp = mx_quantize(y, keep, scale_rule)
         R = (y - d_sp).astype(np.float32)
-        dn_c, _, dn_s, d_dn = mx_quantize(R)
+        dn_c, _, dn_s, d_dn = mx_quantize(R, None, scale_rule)
         out["tensor_scale"] = None
+        out["scale_rule"] = scale_rule
     elif fmt == "nv":
         if tensor_scale is None:
             S = pts_scale(np.abs(y).max() if y.size else 0.0)
@@ -711,9 +671,6 @@ def prepare(x_bf16: np.ndarray, gamma_bf16: np.ndarray | None, eps: float, n: in
         out["sp_meta"] = np.zeros((T, 0), np.uint8)
     out.update(sp_scale=sp_s, dn_codes=pack_nibbles(dn_c), dn_scale=dn_s,
                d_sp=d_sp, R=R, d_dn=d_dn)
-    # the backbone's codes at every position (dropped positions code 0): the
-    # library's optional dense copy, in the residual codes' layout
-    out["sp_dense"] = pack_nibbles(sp_c)
     return out
 
 
@@ -853,18 +810,21 @@ def prepare_silu_mul(gate_bf16: np.ndarray, up_bf16: np.ndarray, n: int, m: int,
     return out
 
 
-def quantize_weight(w_bf16: np.ndarray, fmt: str = "mx") -> dict:
+def quantize_weight(w_bf16: np.ndarray, fmt: str = "mx", scale_rule: str = "floor") -> dict:
     """Quantize W [N,K] once into one shared FP4 payload (Sec. 3.4, "Shared FP4 weights").
 
-    MXFP4: E8M0 per 32 along K, used by both paths.  NVFP4: per-tensor scale
-    S_w = amax(W)/2688, E4M3 per 32 (the sparse view), and a dense view that
-    repeats every scale for its two 16-element halves.  HiF4: units of 64
-    along K with their three-level metadata, one view for both paths.
+    MXFP4: E8M0 per 32 along K (rule "floor" or "ceil", R13), used by both
+    paths.  NVFP4: per-tensor scale S_w = amax(W)/2688, E4M3 per 32 (the
+    sparse view), and a dense view that repeats every scale for its two
+    16-element halves.  HiF4: units of 64 along K with their three-level
+    metadata, one view for both paths.
     """
     w = bf16_bits_to_f32(w_bf16)
     N, K = w.shape
+    if scale_rule != "floor" and fmt != "mx":
+        raise ValueError("the E8M0 scale rule applies to MXFP4 only")
     if fmt == "mx":
-        c, _, s, deq = mx_quantize(w)
+        c, _, s, deq = mx_quantize(w, None, scale_rule)
         return {"N": N, "K": K, "fmt": "mx", "codes": pack_nibbles(c), "scale": s,
                 "scale_dn": s, "tensor_scale": None, "deq": deq}
     if fmt == "hif4":

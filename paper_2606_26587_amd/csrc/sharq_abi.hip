@@ -10,9 +10,9 @@ namespace sharq {
 hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* res, int64_t ldr, uint16_t* h,
                        int64_t ldh, const uint16_t* gamma, float eps, int pat, bool nv, const float* ts_in,
                        float* ts_out, uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns,
-                       uint8_t* spd, hipStream_t st);
+                       uint8_t* spd, PrepExtras ex, hipStream_t st);
 hipError_t launch_wquant_mx(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
-                            hipStream_t st);
+                            uint32_t rule_bias, hipStream_t st);
 hipError_t launch_wquant_nv(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
                             uint8_t* scale_dn, float* ts, hipStream_t st);
 hipError_t launch_linear_nv(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
@@ -39,7 +39,7 @@ hipError_t launch_linear_hif4(int ydt, const uint8_t* spc, const uint8_t* spm, c
 hipError_t launch_prep_silu(const uint16_t* gate, const uint16_t* up, uint16_t* h, int M, int K, int64_t ldg,
                             int64_t ldu, int64_t ldh, int pat, bool nv, const float* ts_in, float* ts_out,
                             uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, uint8_t* spd,
-                            hipStream_t st);
+                            PrepExtras ex, hipStream_t st);
 hipError_t launch_linear_mx_grouped(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                                     const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx, int64_t act_rows,
                                     const int32_t* offs, int E, int64_t total, const uint8_t* wc, const uint8_t* ws,
@@ -101,9 +101,18 @@ sharq_status check_act(const sharq_act* a) {
     if (a->K % 64 != 0) return SHARQ_EINVAL;
     if (pid != 24 || mode != SHARQ_MODE_SHARQ) return SHARQ_EUNSUPPORTED;
   }
+  if (a->scale_rule != SHARQ_SCALE_FLOOR && a->scale_rule != SHARQ_SCALE_CEIL) return SHARQ_EINVAL;
+  if (a->scale_rule == SHARQ_SCALE_CEIL && (a->fmt != SHARQ_MXFP4 || mode != SHARQ_MODE_SHARQ))
+    return SHARQ_EUNSUPPORTED;
+  if ((a->dbg_mask || a->dbg_r) && (a->fmt == SHARQ_HIF4 || mode != SHARQ_MODE_SHARQ)) return SHARQ_EUNSUPPORTED;
   if (a->rows == 0) return SHARQ_OK;   // an empty activation is never dereferenced
   const int k1 = kind1(mode), k2 = kind2(mode);
-  if (k1 != kNone && (!a->sp_codes || !a->sp_scale || (k1 == kSparse && !a->sp_meta))) return SHARQ_EINVAL;
+  // the dense-only backbone: sp_dense without the compressed codes and metadata
+  const bool dense_only = a->sp_dense && !a->sp_codes && !a->sp_meta && mode == SHARQ_MODE_SHARQ;
+  if (dense_only && (a->fmt != SHARQ_MXFP4 || a->K % 128 != 0)) return SHARQ_EUNSUPPORTED;
+  if (k1 != kNone && !dense_only && (!a->sp_codes || !a->sp_scale || (k1 == kSparse && !a->sp_meta)))
+    return SHARQ_EINVAL;
+  if (dense_only && !a->sp_scale) return SHARQ_EINVAL;
   if (k2 != kNone && (!a->dn_codes || !a->dn_scale)) return SHARQ_EINVAL;
   if (k2 == kSparse && !a->dn_meta) return SHARQ_EINVAL;
   if (a->fmt == SHARQ_NVFP4 && !a->tensor_scale) return SHARQ_EINVAL;
@@ -111,10 +120,12 @@ sharq_status check_act(const sharq_act* a) {
   if (!aligned(a->sp_dense, 16)) return SHARQ_EALIGN;
   if (!aligned(a->sp_codes, 16) || !aligned(a->dn_codes, 16) || !aligned(a->sp_meta, 4) ||
       !aligned(a->sp_scale, 4) || !aligned(a->dn_scale, 4) || !aligned(a->tensor_scale, 4) ||
-      !aligned(a->dn_meta, 4))
+      !aligned(a->dn_meta, 4) || !aligned(a->dbg_mask, 4) || !aligned(a->dbg_r, 4))
     return SHARQ_EALIGN;
   return SHARQ_OK;
 }
+
+uint32_t rule_bias(sharq_scale_rule r) { return r == SHARQ_SCALE_CEIL ? sharq::kE8Ceil : sharq::kE8Floor; }
 
 sharq_status check_weight(const sharq_weight* w) {
   if (!w) return SHARQ_EINVAL;
@@ -193,6 +204,8 @@ sharq_status sharq_quantize_weight(const void* W, sharq_dtype wdt, int64_t N, in
   if (wdt != SHARQ_BF16 && wdt != SHARQ_F32) return SHARQ_EUNSUPPORTED;
   if (!fmt_ok(out->fmt)) return SHARQ_EINVAL;
   if (out->fmt == SHARQ_HIF4 && K % 64 != 0) return SHARQ_EINVAL;
+  if (out->scale_rule != SHARQ_SCALE_FLOOR && out->scale_rule != SHARQ_SCALE_CEIL) return SHARQ_EINVAL;
+  if (out->scale_rule == SHARQ_SCALE_CEIL && out->fmt != SHARQ_MXFP4) return SHARQ_EUNSUPPORTED;
   const bool nv = out->fmt == SHARQ_NVFP4;
   if (!out->codes || !out->scale) return SHARQ_EINVAL;
   if (nv && (!out->scale_dn || !out->tensor_scale)) return SHARQ_EINVAL;
@@ -206,7 +219,8 @@ sharq_status sharq_quantize_weight(const void* W, sharq_dtype wdt, int64_t N, in
   if (nv)
     return hip_status(sharq::launch_wquant_nv(W, (int)wdt, (int)N, (int)K, ldw, out->codes, out->scale,
                                               out->scale_dn, out->tensor_scale, st));
-  return hip_status(sharq::launch_wquant_mx(W, (int)wdt, (int)N, (int)K, ldw, out->codes, out->scale, st));
+  return hip_status(sharq::launch_wquant_mx(W, (int)wdt, (int)N, (int)K, ldw, out->codes, out->scale,
+                                            rule_bias(out->scale_rule), st));
 }
 
 }  // extern "C"
@@ -246,12 +260,13 @@ sharq_status prepare_impl(int src, const void* X, const void* res, void* h_out, 
   if (res && out->mode != SHARQ_MODE_SHARQ) return SHARQ_EUNSUPPORTED;
   if (res && fmt == SHARQ_HIF4) return SHARQ_EUNSUPPORTED;
   if (M == 0) return SHARQ_OK;
+  const sharq::PrepExtras ex{rule_bias(out->scale_rule), reinterpret_cast<uint32_t*>(out->dbg_mask), out->dbg_r};
   if (src == kSrcSilu)
     return hip_status(sharq::launch_prep_silu(static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(res),
                                               static_cast<uint16_t*>(h_out), (int)M, (int)K, ldx, ldr, ldh, pid, nv,
                                               nv ? tensor_scale_in : nullptr, nv ? out->tensor_scale : nullptr,
                                               out->sp_codes, out->sp_meta, out->sp_scale, out->dn_codes,
-                                              out->dn_scale, out->sp_dense, reinterpret_cast<hipStream_t>(stream)));
+                                              out->dn_scale, out->sp_dense, ex, reinterpret_cast<hipStream_t>(stream)));
   if (fmt == SHARQ_HIF4)
     return hip_status(sharq::launch_prep_hif4(static_cast<const uint16_t*>(X), (int)M, (int)K, ldx,
                                               static_cast<const uint16_t*>(gamma), eps, out->sp_codes, out->sp_meta,
@@ -270,7 +285,7 @@ sharq_status prepare_impl(int src, const void* X, const void* res, void* h_out, 
                                        static_cast<const uint16_t*>(res), ldr, static_cast<uint16_t*>(h_out), ldh,
                                        static_cast<const uint16_t*>(gamma), eps, pid, nv, nv ? tensor_scale_in : nullptr,
                                        nv ? out->tensor_scale : nullptr, out->sp_codes, out->sp_meta, out->sp_scale,
-                                       out->dn_codes, out->dn_scale, out->sp_dense,
+                                       out->dn_codes, out->dn_scale, out->sp_dense, ex,
                                        reinterpret_cast<hipStream_t>(stream)));
 }
 

@@ -30,13 +30,28 @@ __device__ __forceinline__ int floor_log2_abs_bits(uint32_t abits) {
   return ex ? (int)ex - 127 : (31 - (int)__builtin_clz(abits)) - 149;
 }
 
-// OCP MX shared exponent of a block whose largest magnitude has bits
-// `amax_bits`: floor(log2 amax) - 2, clamped at -127; -127 for an all-zero block.
-__device__ __forceinline__ int mx_exponent(uint32_t amax_bits) {
-  if (amax_bits == 0) return -127;
-  int e = floor_log2_abs_bits(amax_bits) - 2;
+// E8M0 rules of the shared exponent of a block whose largest magnitude has
+// bits `amax_bits` (non-negative, finite), as the bias added to those bits:
+//   kE8Floor  floor(log2 amax) - 2 (OCP MX): the exponent field minus 129;
+//   kE8Ceil   ceil(log2(amax / 6)), the smallest power of two under which the
+//             peak does not exceed 6: one more than the floor rule exactly
+//             when the mantissa is above 1.5 (6 * 2^(E-2) = 1.5 * 2^E), i.e.
+//             when adding 0x3FFFFF carries into the exponent field.
+// Both clamped at -127; subnormal and zero maxima give -127.
+constexpr uint32_t kE8Floor = 0u, kE8Ceil = 0x3FFFFFu;
+
+__device__ __forceinline__ int mx_exponent(uint32_t amax_bits, uint32_t rule_bias = kE8Floor) {
+  const int e = (int)((amax_bits + rule_bias) >> 23) - 129;
   return e < -127 ? -127 : e;
 }
+
+// Options of a preparation beyond its buffers: the E8M0 rule (MXFP4) and
+// the optional debug outputs (keep bits per block, RMSNorm r per row).
+struct PrepExtras {
+  uint32_t rule_bias;
+  uint32_t* dbg_mask;
+  float* dbg_r;
+};
 
 // 2^e as fp32 for e in [-149, 127] (2^-127 is subnormal).
 __device__ __forceinline__ float exp2_int(int e) {

@@ -1198,10 +1198,13 @@ struct SkinnyStage {
   uint4 dn[MF];            // residual codes of row 16 m + l % 16, block l / 16
   uint2 spc[MF];           // backbone codes and metadata of the same block
   uint32_t spm[MF];
+  uint4 spd[MF];           // or (pattern 0) its dense backbone codes
   uint32_t sdn[MF], ssp[MF];
 };
 
-template <int MF, int NB>
+// PAT 0: spc is the dense backbone copy (16 bytes per block, the residual
+// codes' layout) and spm is unused.
+template <int MF, int NB, int PAT>
 __device__ __forceinline__ void skinny_load(SkinnyStage<MF, NB>& st, const uint8_t* spc, const uint8_t* spm,
                                             const uint8_t* sps, const uint8_t* dnc, const uint8_t* dns, int64_t M,
                                             int64_t r0, const uint8_t* wc, const uint8_t* ws, int N, int n0, int ks,
@@ -1220,8 +1223,12 @@ __device__ __forceinline__ void skinny_load(SkinnyStage<MF, NB>& st, const uint8
     if (row >= M) row = M - 1;
     const int64_t V = (pm + row) * 4 + j;   // block-major index of (row, block)
     st.dn[m] = *reinterpret_cast<const uint4*>(dnc + V * 16);
-    st.spc[m] = *reinterpret_cast<const uint2*>(spc + V * 8);
-    st.spm[m] = *reinterpret_cast<const uint32_t*>(spm + V * 4);
+    if (PAT == 0) {
+      st.spd[m] = *reinterpret_cast<const uint4*>(spc + V * 16);
+    } else {
+      st.spc[m] = *reinterpret_cast<const uint2*>(spc + V * 8);
+      st.spm[m] = *reinterpret_cast<const uint32_t*>(spm + V * 4);
+    }
     st.sdn[m] = dns[V];
     st.ssp[m] = sps[V];
   }
@@ -1233,7 +1240,7 @@ template <int MF, int NB, int PAT>
 __device__ __forceinline__ void skinny_step(v4f_t (&acc)[MF][NB], const SkinnyStage<MF, NB>& st) {
 #pragma unroll
   for (int m = 0; m < MF; ++m) {
-    const v8i asp = as_operand(expand_block<PAT>(st.spc[m], st.spm[m]));
+    const v8i asp = as_operand(PAT == 0 ? st.spd[m] : expand_block<PAT>(st.spc[m], st.spm[m]));
     const v8i adn = as_operand(st.dn[m]);
 #pragma unroll
     for (int n = 0; n < NB; ++n) {
@@ -1287,17 +1294,17 @@ __global__ __launch_bounds__(64 * KS) void k_linear_mx_skinny(const uint8_t* sp_
 
   SkinnyStage<MF, NB> s0, s1;
   if (k0 < k1)
-    skinny_load<MF, NB>(s0, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, r0, wc, ws, N, n0, k0, lane);
+    skinny_load<MF, NB, PAT>(s0, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, r0, wc, ws, N, n0, k0, lane);
   if (k0 + 1 < k1)
-    skinny_load<MF, NB>(s1, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, r0, wc, ws, N, n0, k0 + 1, lane);
+    skinny_load<MF, NB, PAT>(s1, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, r0, wc, ws, N, n0, k0 + 1, lane);
   int ks = k0;
   for (; ks + 1 < k1; ks += 2) {
     skinny_step<MF, NB, PAT>(acc, s0);
     if (ks + 2 < k1)
-      skinny_load<MF, NB>(s0, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, r0, wc, ws, N, n0, ks + 2, lane);
+      skinny_load<MF, NB, PAT>(s0, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, r0, wc, ws, N, n0, ks + 2, lane);
     skinny_step<MF, NB, PAT>(acc, s1);
     if (ks + 3 < k1)
-      skinny_load<MF, NB>(s1, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, r0, wc, ws, N, n0, ks + 3, lane);
+      skinny_load<MF, NB, PAT>(s1, sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, r0, wc, ws, N, n0, ks + 3, lane);
   }
   if (ks < k1) skinny_step<MF, NB, PAT>(acc, s0);
 
@@ -2483,9 +2490,12 @@ hipError_t launch_linear_mx(int pat, int ydt, const uint8_t* spc, const uint8_t*
     return go_dense_backbone<uint16_t>(spd, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
   }
   if (use_skinny(M, N, K)) {
+    if (spc == nullptr)   // the backbone exists as its dense copy only
+      return go_skinny_dt<0>(ydt, spd, nullptr, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
     return pat == 24 ? go_skinny_dt<24>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st)
                      : go_skinny_dt<48>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);
   }
+  if (spc == nullptr) return hipErrorInvalidValue;   // rejected by the C ABI (K not a multiple of 128)
   if (pat == 24) {
     return sdw ? go_linear_dt<NF, 24, true>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st)
                : go_linear_dt<NF, 24, false>(ydt, spc, spm, sps, dnc, dns, M, wc, ws, N, K, Y, ldy, st);

@@ -178,6 +178,45 @@ __device__ __forceinline__ void backbone_24_dense(const float (&y)[32], const Q&
   }
 }
 
+// The 2:4 backbone as its dense codes only (no compressed codes, no
+// metadata): the kept values converted in place with +0 at the dropped
+// positions, and the residual decoded from them as in backbone_24_dense.
+template <class Q>
+__device__ __forceinline__ void backbone_24_dense_only(const float (&y)[32], const Q& qz, uint32_t (&dense)[4],
+                                                       float (&R)[32]) {
+#pragma unroll
+  for (int g = 7; g >= 0; --g) {
+    const float y0 = y[4 * g], y1 = y[4 * g + 1], y2 = y[4 * g + 2], y3 = y[4 * g + 3];
+    lmask k0, k1, k2, k3;
+    top2of4(y0, y1, y2, y3, k0, k1, k2, k3);
+    const float b0 = lsel(k0, y0, 0.0f), b1 = lsel(k1, y1, 0.0f);
+    const float b2 = lsel(k2, y2, 0.0f), b3 = lsel(k3, y3, 0.0f);
+    if (g & 1) dense[g >> 1] = __float_as_uint(b0);
+    put_pair_dyn(qz, dense[g >> 1], 2 * (g & 1), b0, b1);
+    put_pair_dyn(qz, dense[g >> 1], 2 * (g & 1) + 1, b2, b3);
+    const v2f d01 = get_pair_dyn(qz, dense[g >> 1], 2 * (g & 1));
+    const v2f d23 = get_pair_dyn(qz, dense[g >> 1], 2 * (g & 1) + 1);
+    R[4 * g + 0] = y0 - d01.x;
+    R[4 * g + 1] = y1 - d01.y;
+    R[4 * g + 2] = y2 - d23.x;
+    R[4 * g + 3] = y3 - d23.y;
+  }
+}
+
+// Keep bits of one block (bit p = position p kept) from its metadata: 2:4
+// nibbles i0 | i1 << 2 per group, or the 4:8 keep masks themselves.
+template <int PAT>
+__device__ __forceinline__ uint32_t keep_bits(uint32_t meta) {
+  if (PAT != 24) return meta;
+  uint32_t k = 0u;
+#pragma unroll
+  for (int g = 0; g < 8; ++g) {
+    const uint32_t nib = (meta >> (4 * g)) & 0xFu;
+    k |= ((1u << (nib & 3u)) | (1u << (nib >> 2))) << (4 * g);
+  }
+  return k;
+}
+
 // Backbone of one block for the 4:8 pattern (keep mask metadata).
 template <class Q>
 __device__ __forceinline__ void backbone_48(const float (&y)[32], const Q& qz, uint32_t (&codes)[2], uint32_t& meta,
@@ -294,22 +333,33 @@ __device__ __forceinline__ float absmax16(const float* v) {
   return m;
 }
 
+// Where one block's outputs go.  spc / spm may be NULL when the dense
+// backbone copy spd is given (the compressed backbone is then not written);
+// dbg_mask (optional): the block's 32 keep bits.
+struct BlockOut {
+  uint8_t *spc, *spm, *sps, *dnc, *dns, *spd;
+  uint32_t* dbg_mask;
+};
+
 // Quantize and store one MXFP4 block: backbone + residual.  The group maximum
 // is always kept, so the backbone block max equals the block max of y.
-// spd (optional): the backbone's dense codes (16 bytes, dropped positions 0),
-// the GEMM-ready copy that spares the GEMM the expansion.
+// d.spd (optional): the backbone's dense codes (16 bytes, dropped positions
+// 0), the GEMM-ready copy that spares the GEMM the expansion; without d.spc
+// only that copy is written.  rule_bias: the E8M0 rule (kE8Floor, kE8Ceil).
 template <int PAT>
-__device__ __forceinline__ void block_mx(const float (&y)[32], uint8_t* __restrict__ spc, uint8_t* __restrict__ spm,
-                                         uint8_t* __restrict__ sps, uint8_t* __restrict__ dnc,
-                                         uint8_t* __restrict__ dns, uint8_t* __restrict__ spd = nullptr) {
-  const int e = mx_exponent(__float_as_uint(absmax32(y)));
+__device__ __forceinline__ void block_mx(const float (&y)[32], const BlockOut& d, uint32_t rule_bias) {
+  const int e = mx_exponent(__float_as_uint(absmax32(y)), rule_bias);
   const MxQ qb = MxQ::make(e);
-  uint32_t codes[2], meta;
+  uint32_t codes[2] = {0u, 0u}, meta = 0u;
   float R[32];
-  if (PAT == 24 && spd != nullptr) {
+  if (PAT == 24 && d.spd != nullptr && d.spc == nullptr && d.dbg_mask == nullptr) {
+    uint32_t dense[4];
+    backbone_24_dense_only(y, qb, dense, R);
+    *reinterpret_cast<uint4*>(d.spd) = make_uint4(dense[0], dense[1], dense[2], dense[3]);
+  } else if (PAT == 24 && d.spd != nullptr) {
     uint32_t dense[4];
     backbone_24_dense(y, qb, codes, meta, dense, R);
-    *reinterpret_cast<uint4*>(spd) = make_uint4(dense[0], dense[1], dense[2], dense[3]);
+    *reinterpret_cast<uint4*>(d.spd) = make_uint4(dense[0], dense[1], dense[2], dense[3]);
   } else if (PAT == 24) {
     backbone_24(y, qb, codes, meta, R);
   } else if (PAT == 49) {
@@ -317,17 +367,20 @@ __device__ __forceinline__ void block_mx(const float (&y)[32], uint8_t* __restri
   } else {
     backbone_48(y, qb, codes, meta, R);
   }
-  const int er = mx_exponent(__float_as_uint(absmax32(R)));
+  const int er = mx_exponent(__float_as_uint(absmax32(R)), rule_bias);
   const MxQ qr = MxQ::make(er);
   uint32_t dn[4];
 #pragma unroll
   for (int w = 0; w < 4; ++w) dn[w] = enc8(R + 8 * w, qr);
-  *reinterpret_cast<uint2*>(spc) = make_uint2(codes[0], codes[1]);
-  *reinterpret_cast<uint32_t*>(spm) = meta;
-  *sps = (uint8_t)(e + 127);
-  *reinterpret_cast<uint4*>(dnc) = make_uint4(dn[0], dn[1], dn[2], dn[3]);
-  *dns = (uint8_t)(er + 127);
-  if (PAT != 24 && spd) *reinterpret_cast<uint4*>(spd) = expand_block<48>(make_uint2(codes[0], codes[1]), meta);
+  if (d.spc != nullptr) {
+    *reinterpret_cast<uint2*>(d.spc) = make_uint2(codes[0], codes[1]);
+    *reinterpret_cast<uint32_t*>(d.spm) = meta;
+  }
+  *d.sps = (uint8_t)(e + 127);
+  *reinterpret_cast<uint4*>(d.dnc) = make_uint4(dn[0], dn[1], dn[2], dn[3]);
+  *d.dns = (uint8_t)(er + 127);
+  if (PAT != 24 && d.spd) *reinterpret_cast<uint4*>(d.spd) = expand_block<48>(make_uint2(codes[0], codes[1]), meta);
+  if (d.dbg_mask) *d.dbg_mask = keep_bits<PAT>(meta);
 }
 
 // Quantize and store one NVFP4 block: E4M3 backbone scale per 32 positions,
@@ -422,11 +475,10 @@ struct ActOut {
   uint8_t *spc, *spm, *sps, *dnc, *dns;
   int64_t M;
   int K;
-  uint8_t* spd;   // MXFP4: the dense backbone copy, or NULL
-};
-
-struct BlockOut {
-  uint8_t *spc, *spm, *sps, *dnc, *dns, *spd;
+  uint8_t* spd;          // MXFP4: the dense backbone copy, or NULL (spc / spm may then be NULL)
+  uint32_t rule_bias;    // MXFP4: E8M0 rule (kE8Floor or kE8Ceil)
+  uint32_t* dbg_mask;    // optional: 32 keep bits per block, laid out like the 4:8 metadata
+  float* dbg_r;          // optional: the RMSNorm reciprocal r of every row
 };
 
 // Panel-major order is block-major order: block b of a row is block number
@@ -442,11 +494,12 @@ template <bool NV>
 __device__ __forceinline__ BlockOut block_at(const ActOut& o, int64_t V) {
   BlockOut r;
   r.dnc = o.dnc + V * 16;
-  r.spc = o.spc + V * 8;
-  r.spm = o.spm + V * 4;
+  r.spc = o.spc ? o.spc + V * 8 : nullptr;
+  r.spm = o.spm ? o.spm + V * 4 : nullptr;
   r.sps = o.sps + V;
   r.dns = o.dns + (NV ? V * 2 : V);
   r.spd = o.spd ? o.spd + V * 16 : nullptr;
+  r.dbg_mask = o.dbg_mask ? o.dbg_mask + V : nullptr;
   return r;
 }
 
@@ -459,10 +512,12 @@ template <int PAT, bool NV>
 __device__ __forceinline__ void block_out_write(const float (&y)[32], const ActOut& o, int64_t row, int b, float S,
                                                 float six_s) {
   const BlockOut d = block_out<NV>(o, row, b);
-  if (NV)
+  if (NV) {
     block_nv<PAT>(y, S, six_s, d.spc, d.spm, d.sps, d.dnc, d.dns);
-  else
-    block_mx<PAT>(y, d.spc, d.spm, d.sps, d.dnc, d.dns, d.spd);
+    if (d.dbg_mask) *d.dbg_mask = keep_bits<PAT == 49 ? 48 : PAT>(*reinterpret_cast<const uint32_t*>(d.spm));
+  } else {
+    block_mx<PAT>(y, d, o.rule_bias);
+  }
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -604,6 +659,7 @@ __global__ __launch_bounds__(256) void k_prep_norm(XSrc src, int M, int K, const
   const float S = NV ? *S_ptr : 1.0f, six_s = 6.0f * S;
   uint4 xs[NB][4];
   const float r = load_row_rms<NB, RES>(src, row, true, lane, nblk, K, eps, xs);
+  if (o.dbg_r && lane == 0) o.dbg_r[row] = r;
   const uint4* gr = reinterpret_cast<const uint4*>(gamma);
 #pragma unroll
   for (int i = 0; i < NB; ++i) {
@@ -660,6 +716,7 @@ __global__ __launch_bounds__(256) void k_prep_norm_split(XSrc src, int M, int K,
     else total = (part[base] + part[base + 1]) + (part[base + 2] + part[base + 3]);
   }
   const float r = (float)(1.0 / __builtin_sqrt((double)total / (double)K + (double)eps));
+  if (o.dbg_r && real && lane == 0 && wave % C == 0) o.dbg_r[row] = r;
   if (real && live) {
     float y[32];
     norm_block(xq, gq, r, y);
@@ -694,10 +751,12 @@ __global__ __launch_bounds__(256) void k_prep_blocks(XSrc src, int M, int K, Act
   float y[32];
   unpack_bf16x32(xq, y);
   const BlockOut d = block_at<NV>(o, (int64_t)p * M * 4 + t);
-  if (NV)
+  if (NV) {
     block_nv<PAT>(y, S, six_s, d.spc, d.spm, d.sps, d.dnc, d.dns);
-  else
-    block_mx<PAT>(y, d.spc, d.spm, d.sps, d.dnc, d.dns, d.spd);
+    if (d.dbg_mask) *d.dbg_mask = keep_bits<PAT == 49 ? 48 : PAT>(*reinterpret_cast<const uint32_t*>(d.spm));
+  } else {
+    block_mx<PAT>(y, d, o.rule_bias);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1145,8 +1204,8 @@ static void go_prep_pat(int pat, bool nv, const XSrc& src, int M, int K, const u
 hipError_t launch_prep(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* res, int64_t ldr, uint16_t* h,
                        int64_t ldh, const uint16_t* gamma, float eps, int pat, bool nv, const float* ts_in,
                        float* ts_out, uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns,
-                       uint8_t* spd, hipStream_t st) {
-  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K, spd};
+                       uint8_t* spd, PrepExtras ex, hipStream_t st) {
+  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K, spd, ex.rule_bias, ex.dbg_mask, ex.dbg_r};
   const XSrc src{X, ldx, res, ldr, h, ldh};
   const dim3 grid((unsigned)((M + 3) / 4));
   if (nv) {
@@ -1224,7 +1283,7 @@ hipError_t launch_prep_mode(int mode, const uint16_t* X, int M, int K, int64_t l
 // with RMSNorm).
 hipError_t launch_prep_hif4(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps,
                             uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, hipStream_t st) {
-  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K};
+  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K, nullptr, kE8Floor, nullptr, nullptr};
   const XSrc src{X, ldx, nullptr, 0, nullptr, 0};
   const dim3 grid((unsigned)((M + 3) / 4));
   if (gamma)
@@ -1241,8 +1300,8 @@ hipError_t launch_prep_hif4(const uint16_t* X, int M, int K, int64_t ldx, const 
 hipError_t launch_prep_silu(const uint16_t* gate, const uint16_t* up, uint16_t* h, int M, int K, int64_t ldg,
                             int64_t ldu, int64_t ldh, int pat, bool nv, const float* ts_in, float* ts_out,
                             uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, uint8_t* spd,
-                            hipStream_t st) {
-  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K, spd};
+                            PrepExtras ex, hipStream_t st) {
+  const ActOut o{spc, spm, sps, dnc, dns, (int64_t)M, K, spd, ex.rule_bias, ex.dbg_mask, nullptr};
   const XSrc src{gate, ldg, up, ldu, h, ldh};
   const dim3 grid((unsigned)((M + 3) / 4));
   if (nv) {

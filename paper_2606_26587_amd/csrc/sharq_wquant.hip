@@ -44,7 +44,8 @@ __device__ __forceinline__ void load32<float>(const float* p, float (&v)[32]) {
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_wquant_mx(const T* __restrict__ W, int N, int K, int64_t ldw,
-                                                   uint8_t* __restrict__ codes, uint8_t* __restrict__ scale) {
+                                                   uint8_t* __restrict__ codes, uint8_t* __restrict__ scale,
+                                                   uint32_t rule_bias) {
   const int nblk = K / 32;
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (gid >= (int64_t)N * nblk) return;
@@ -55,7 +56,7 @@ __global__ __launch_bounds__(256) void k_wquant_mx(const T* __restrict__ W, int 
   float amax = 0.0f;
 #pragma unroll
   for (int k = 0; k < 32; ++k) amax = fmaxf(amax, fabsf(v[k]));
-  const int e = mx_exponent(__float_as_uint(amax));
+  const int e = mx_exponent(__float_as_uint(amax), rule_bias);
   const MxQ qz = MxQ::make(e);
   uint32_t q[4];
 #pragma unroll
@@ -199,13 +200,15 @@ hipError_t launch_wquant_hif4(const void* W, int wdt, int N, int K, int64_t ldw,
 }
 
 hipError_t launch_wquant_mx(const void* W, int wdt, int N, int K, int64_t ldw, uint8_t* codes, uint8_t* scale,
-                            hipStream_t st) {
+                            uint32_t rule_bias, hipStream_t st) {
   const int64_t total = (int64_t)N * (K / 32);
   dim3 grid((unsigned)((total + 255) / 256)), block(256);
   if (wdt == 2)
-    k_wquant_mx<float><<<grid, block, 0, st>>>(reinterpret_cast<const float*>(W), N, K, ldw, codes, scale);
+    k_wquant_mx<float><<<grid, block, 0, st>>>(reinterpret_cast<const float*>(W), N, K, ldw, codes, scale,
+                                                rule_bias);
   else
-    k_wquant_mx<uint16_t><<<grid, block, 0, st>>>(reinterpret_cast<const uint16_t*>(W), N, K, ldw, codes, scale);
+    k_wquant_mx<uint16_t><<<grid, block, 0, st>>>(reinterpret_cast<const uint16_t*>(W), N, K, ldw, codes, scale,
+                                                   rule_bias);
   return hipGetLastError();
 }
 

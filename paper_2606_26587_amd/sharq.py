@@ -25,6 +25,8 @@ _FMT = {"mx": MXFP4, "mxfp4": MXFP4, "nv": NVFP4, "nvfp4": NVFP4, "hif4": HIF4}
 #: path combinations (sharq_mode): the method, and the ablation modes
 MODES = {"sharq": 0, "sparse": 1, "dense": 2, "dense_dense": 3, "sparse_sparse": 4}
 _DT = {torch.bfloat16: BF16, torch.float16: F16, torch.float32: F32}
+#: E8M0 scale rules of MXFP4 (sharq_scale_rule)
+SCALE_RULES = {"floor": 0, "ceil": 1}
 
 
 class SharqError(RuntimeError):
@@ -41,13 +43,14 @@ class ActStruct(ctypes.Structure):
     _fields_ = [("rows", ctypes.c_int64), ("K", ctypes.c_int64), ("fmt", ctypes.c_int), ("nm", Pattern),
                 ("sp_codes", ctypes.c_void_p), ("sp_meta", ctypes.c_void_p), ("sp_scale", ctypes.c_void_p),
                 ("dn_codes", ctypes.c_void_p), ("dn_scale", ctypes.c_void_p), ("tensor_scale", ctypes.c_void_p),
-                ("mode", ctypes.c_int), ("dn_meta", ctypes.c_void_p), ("sp_dense", ctypes.c_void_p)]
+                ("mode", ctypes.c_int), ("dn_meta", ctypes.c_void_p), ("sp_dense", ctypes.c_void_p),
+                ("scale_rule", ctypes.c_int), ("dbg_mask", ctypes.c_void_p), ("dbg_r", ctypes.c_void_p)]
 
 
 class WeightStruct(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int64), ("K", ctypes.c_int64), ("experts", ctypes.c_int64), ("fmt", ctypes.c_int),
                 ("codes", ctypes.c_void_p), ("scale", ctypes.c_void_p), ("scale_dn", ctypes.c_void_p),
-                ("tensor_scale", ctypes.c_void_p)]
+                ("tensor_scale", ctypes.c_void_p), ("scale_rule", ctypes.c_int)]
 
 
 def _load():
@@ -126,14 +129,17 @@ class PreparedAct:
     mode: int = 0
     dn_meta: Optional[torch.Tensor] = None
     sp_dense: Optional[torch.Tensor] = None   # MXFP4: the backbone's dense copy for the main GEMM
+    scale_rule: int = 0                       # MXFP4: E8M0 rule (SCALE_RULES)
+    dbg_mask: Optional[torch.Tensor] = None   # debug: keep bits, 4 bytes per 32 positions
+    dbg_r: Optional[torch.Tensor] = None      # debug: RMSNorm r per row (fp32)
 
     def struct(self) -> ActStruct:
-        return ActStruct(self.rows, self.K, self.fmt, Pattern(self.n, self.m, int(self.pairs)), self.sp_codes.data_ptr(),
-                         self.sp_meta.data_ptr(), self.sp_scale.data_ptr(), self.dn_codes.data_ptr(),
-                         self.dn_scale.data_ptr(),
-                         None if self.tensor_scale is None else self.tensor_scale.data_ptr(), self.mode,
-                         None if self.dn_meta is None else self.dn_meta.data_ptr(),
-                         None if self.sp_dense is None else self.sp_dense.data_ptr())
+        def p(t):
+            return None if t is None else t.data_ptr()
+        return ActStruct(self.rows, self.K, self.fmt, Pattern(self.n, self.m, int(self.pairs)), p(self.sp_codes),
+                         p(self.sp_meta), p(self.sp_scale), p(self.dn_codes), p(self.dn_scale), p(self.tensor_scale),
+                         self.mode, p(self.dn_meta), p(self.sp_dense), self.scale_rule, p(self.dbg_mask),
+                         p(self.dbg_r))
 
 
 @dataclass
@@ -147,20 +153,24 @@ class QuantWeight:
     scale: torch.Tensor
     scale_dn: torch.Tensor
     tensor_scale: Optional[torch.Tensor] = None
+    scale_rule: int = 0                       # MXFP4: E8M0 rule used by sharq_quantize_weight
 
     def struct(self) -> WeightStruct:
         return WeightStruct(self.N, self.K, self.experts, self.fmt, self.codes.data_ptr(), self.scale.data_ptr(),
                             self.scale_dn.data_ptr(),
-                            None if self.tensor_scale is None else self.tensor_scale.data_ptr())
+                            None if self.tensor_scale is None else self.tensor_scale.data_ptr(), self.scale_rule)
 
 
 def alloc_act(rows: int, K: int, n: int = 2, m: int = 4, fmt="mx", device="cuda", pairs: bool = False,
-              mode="sharq", dense_backbone: bool = False) -> PreparedAct:
+              mode="sharq", dense_backbone: bool = False, dense_only: bool = False, scale_rule="floor",
+              debug: bool = False) -> PreparedAct:
     """Device buffers of a prepared activation (flat, panel-major; see include/sharq.h).
     pairs=True: n:m selection in pairs (4:8 in pairs).  mode: a key of MODES
     (or its id); buffers a mode does not use are empty.  dense_backbone=True
     (MXFP4): also the backbone's dense copy that the main GEMM reads without
-    expanding it."""
+    expanding it; dense_only=True: that copy instead of the compressed
+    backbone.  scale_rule: "floor" or "ceil" (MXFP4 E8M0 rule).  debug=True:
+    also the keep-mask and per-row r debug outputs."""
     f = _FMT[fmt] if isinstance(fmt, str) else fmt
     md = MODES[mode] if isinstance(mode, str) else int(mode)
     sizes = [lib.sharq_act_buffer_bytes_mode(rows, K, f, Pattern(n, m, int(pairs)), md, w) for w in range(6)]
@@ -169,30 +179,38 @@ def alloc_act(rows: int, K: int, n: int = 2, m: int = 4, fmt="mx", device="cuda"
         raise SharqError(EINVAL, "alloc_act")
     bufs = [torch.empty(sz, dtype=torch.uint8, device=device) for sz in sizes]
     ts = torch.empty(1, dtype=torch.float32, device=device) if f == NVFP4 else None
-    spd = torch.empty(rows * K // 2, dtype=torch.uint8, device=device) if dense_backbone else None
+    spd = torch.empty(rows * K // 2, dtype=torch.uint8, device=device) if (dense_backbone or dense_only) else None
+    if dense_only:
+        bufs[0] = bufs[1] = None
+    rule = SCALE_RULES[scale_rule] if isinstance(scale_rule, str) else int(scale_rule)
+    dbg_mask = torch.empty(rows * K // 8, dtype=torch.uint8, device=device) if debug else None
+    dbg_r = torch.empty(rows, dtype=torch.float32, device=device) if debug else None
     return PreparedAct(rows, K, f, n, m, *bufs[:5], tensor_scale=ts, pairs=pairs, mode=md, dn_meta=bufs[5],
-                       sp_dense=spd)
+                       sp_dense=spd, scale_rule=rule, dbg_mask=dbg_mask, dbg_r=dbg_r)
 
 
-def alloc_weight(N: int, K: int, fmt="mx", experts: int = 1, device="cuda") -> QuantWeight:
+def alloc_weight(N: int, K: int, fmt="mx", experts: int = 1, device="cuda", scale_rule="floor") -> QuantWeight:
     """Device buffers of a quantized weight, one flat panel-major row per expert."""
     f = _FMT[fmt] if isinstance(fmt, str) else fmt
     codes = torch.empty((experts, N * K // 2), dtype=torch.uint8, device=device)
     scale = torch.empty((experts, N * K // (16 if f == HIF4 else 32)), dtype=torch.uint8, device=device)
     scale_dn = scale if f != NVFP4 else torch.empty((experts, N * K // 16), dtype=torch.uint8, device=device)
     ts = torch.empty(experts, dtype=torch.float32, device=device) if f == NVFP4 else None
-    return QuantWeight(N, K, experts, f, codes, scale, scale_dn, ts)
+    rule = SCALE_RULES[scale_rule] if isinstance(scale_rule, str) else int(scale_rule)
+    return QuantWeight(N, K, experts, f, codes, scale, scale_dn, ts, rule)
 
 
 # ---------------------------------------------------------------------------
 # Entry points (same names as the C ABI)
 # ---------------------------------------------------------------------------
 
-def sharq_quantize_weight(w: torch.Tensor, fmt="mx", out: Optional[QuantWeight] = None, stream=None) -> QuantWeight:
-    """Quantize W [N, K] (bf16 or fp32, on the GPU) into the shared FP4 payload."""
+def sharq_quantize_weight(w: torch.Tensor, fmt="mx", out: Optional[QuantWeight] = None, stream=None,
+                          scale_rule="floor") -> QuantWeight:
+    """Quantize W [N, K] (bf16 or fp32, on the GPU) into the shared FP4 payload
+    (scale_rule: the MXFP4 E8M0 rule, ignored when `out` is given)."""
     N, K = w.shape
     if out is None:
-        out = alloc_weight(N, K, fmt, 1, w.device)
+        out = alloc_weight(N, K, fmt, 1, w.device, scale_rule)
     ws = out.struct()
     _check(lib.sharq_quantize_weight(_ptr(w), _DT.get(w.dtype, -1), N, K, w.stride(0), ctypes.byref(ws),
                                      _stream(stream)), "sharq_quantize_weight")
@@ -201,13 +219,14 @@ def sharq_quantize_weight(w: torch.Tensor, fmt="mx", out: Optional[QuantWeight] 
 
 def sharq_prepare(x: torch.Tensor, gamma: Optional[torch.Tensor], eps: float = 1e-6, n: int = 2, m: int = 4,
                   fmt="mx", tensor_scale_in: Optional[torch.Tensor] = None, out: Optional[PreparedAct] = None,
-                  stream=None, pairs: bool = False, mode="sharq") -> PreparedAct:
+                  stream=None, pairs: bool = False, mode="sharq", scale_rule="floor") -> PreparedAct:
     """Fused preparation of activation rows X [M, K] (bf16, on the GPU).
-    pairs=True: n:m selection in pairs (NVFP4's 4:8 in pairs).  mode: the
-    path combination (MODES; ignored when `out` is given, which carries it)."""
+    pairs=True: n:m selection in pairs (NVFP4's 4:8 in pairs).  mode, scale_rule:
+    the path combination (MODES) and the MXFP4 E8M0 rule (SCALE_RULES), both
+    ignored when `out` is given, which carries them."""
     M, K = x.shape
     if out is None:
-        out = alloc_act(M, K, n, m, fmt, x.device, pairs, mode)
+        out = alloc_act(M, K, n, m, fmt, x.device, pairs, mode, scale_rule=scale_rule)
     f = _FMT[fmt] if isinstance(fmt, str) else fmt
     st = out.struct()
     _check(lib.sharq_prepare(_ptr(x), _DT.get(x.dtype, -1), M, K, x.stride(0), _ptr(gamma), ctypes.c_float(eps),
@@ -285,7 +304,8 @@ def stack_weights(ws: Sequence[QuantWeight]) -> QuantWeight:
     ts = None if w0.tensor_scale is None else torch.cat([w.tensor_scale for w in ws])
     scale = torch.cat([w.scale for w in ws])
     scale_dn = scale if w0.fmt != NVFP4 else torch.cat([w.scale_dn for w in ws])
-    return QuantWeight(w0.N, w0.K, len(ws), w0.fmt, torch.cat([w.codes for w in ws]), scale, scale_dn, ts)
+    return QuantWeight(w0.N, w0.K, len(ws), w0.fmt, torch.cat([w.codes for w in ws]), scale, scale_dn, ts,
+                       w0.scale_rule)
 
 
 def version() -> str:

@@ -6,6 +6,7 @@ import numpy as np
 import torch
 
 from oracle import sharq_oracle as O
+import panel_layout as L
 from paper_2606_26587_amd import sharq as S
 
 
@@ -32,14 +33,16 @@ def act_to_oracle(a: S.PreparedAct) -> dict:
     if a.dn_meta is not None:
         bufs["dn_meta"] = host(a.dn_meta)
     ts = None if a.tensor_scale is None else np.float32(host(a.tensor_scale)[0])
-    return O.act_from_device_layout(bufs, a.rows, a.K, a.n, a.m, FMT_NAME[a.fmt], ts, mode=MODE_NAME[a.mode],
+    return L.act_from_device_layout(bufs, a.rows, a.K, a.n, a.m, FMT_NAME[a.fmt], ts, mode=MODE_NAME[a.mode],
                                     pairs=a.pairs)
 
 
-def oracle_to_act(o: dict) -> S.PreparedAct:
-    """Oracle prepared activation -> device buffers in the library's layout."""
+def oracle_to_act(o: dict, dense_backbone: bool = False) -> S.PreparedAct:
+    """Oracle prepared activation -> device buffers in the library's layout
+    (dense_backbone: with the MXFP4 dense backbone copy as well)."""
     fmt = FMT_ID[o["fmt"]]
-    dev = O.act_to_device_layout(o)
+    dev = L.act_to_device_layout(o)
+    spd = dev_u8(L.dense_backbone_to_device_layout(o)) if dense_backbone else None
     ts = None
     if fmt == S.NVFP4:
         ts = torch.tensor([float(o["tensor_scale"])], dtype=torch.float32, device="cuda")
@@ -48,12 +51,12 @@ def oracle_to_act(o: dict) -> S.PreparedAct:
     return S.PreparedAct(o["rows"], o["K"], fmt, o["n"], o["m"], dev_u8(dev["sp_codes"]),
                          dev_u8(dev["sp_meta"]), dev_u8(dev["sp_scale"]), dev_u8(dev["dn_codes"]),
                          dev_u8(dev["dn_scale"]), tensor_scale=ts, pairs=bool(o.get("pairs", False)), mode=mode,
-                         dn_meta=dn_meta)
+                         dn_meta=dn_meta, sp_dense=spd)
 
 
 def oracle_to_weight(o: dict) -> S.QuantWeight:
     fmt = FMT_ID[o["fmt"]]
-    dev = O.weight_to_device_layout(o)
+    dev = L.weight_to_device_layout(o)
     codes = dev_u8(dev["codes"])[None]
     scale = dev_u8(dev["scale"])[None]
     scale_dn = scale if fmt != S.NVFP4 else dev_u8(dev["scale_dn"])[None]
@@ -64,7 +67,7 @@ def oracle_to_weight(o: dict) -> S.QuantWeight:
 def weight_to_oracle(w: S.QuantWeight, e: int = 0) -> dict:
     bufs = {"codes": host(w.codes[e]), "scale": host(w.scale[e]), "scale_dn": host(w.scale_dn[e])}
     ts = None if w.tensor_scale is None else np.float32(host(w.tensor_scale)[e])
-    return O.weight_from_device_layout(bufs, w.N, w.K, FMT_NAME[w.fmt], ts)
+    return L.weight_from_device_layout(bufs, w.N, w.K, FMT_NAME[w.fmt], ts)
 
 
 def assert_bytes_equal(name, got: np.ndarray, want: np.ndarray):

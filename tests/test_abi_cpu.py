@@ -24,13 +24,14 @@ class Act(ctypes.Structure):
     _fields_ = [("rows", ctypes.c_int64), ("K", ctypes.c_int64), ("fmt", ctypes.c_int), ("nm", Pattern),
                 ("sp_codes", ctypes.c_void_p), ("sp_meta", ctypes.c_void_p), ("sp_scale", ctypes.c_void_p),
                 ("dn_codes", ctypes.c_void_p), ("dn_scale", ctypes.c_void_p), ("tensor_scale", ctypes.c_void_p),
-                ("mode", ctypes.c_int), ("dn_meta", ctypes.c_void_p), ("sp_dense", ctypes.c_void_p)]
+                ("mode", ctypes.c_int), ("dn_meta", ctypes.c_void_p), ("sp_dense", ctypes.c_void_p),
+                ("scale_rule", ctypes.c_int), ("dbg_mask", ctypes.c_void_p), ("dbg_r", ctypes.c_void_p)]
 
 
 class Weight(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int64), ("K", ctypes.c_int64), ("experts", ctypes.c_int64), ("fmt", ctypes.c_int),
                 ("codes", ctypes.c_void_p), ("scale", ctypes.c_void_p), ("scale_dn", ctypes.c_void_p),
-                ("tensor_scale", ctypes.c_void_p)]
+                ("tensor_scale", ctypes.c_void_p), ("scale_rule", ctypes.c_int)]
 
 
 @pytest.fixture(scope="module")
@@ -348,3 +349,36 @@ def test_dense_backbone_copy_rejections(L):
     nv.tensor_scale = FAKE
     assert prep(nv, fmt=1) == EUNSUPPORTED                             # NVFP4: the copy is MXFP4 only
     assert prep(act(mode=SPARSE, sp_dense=FAKE)) == EUNSUPPORTED        # the method's combination only
+
+
+def test_scale_rule_debug_and_dense_only_rejections(L):
+    """The E8M0 rule, the debug outputs and the dense-only backbone are
+    validated before any launch."""
+    def prep(a, K=128, fmt=0, nm=(2, 4, 0)):
+        return L.sharq_prepare(FAKE, 0, a.rows, K, K, None, ctypes.c_float(1e-6), Pattern(*nm), fmt, None,
+                               ctypes.byref(a), None)
+    a = act()
+    a.scale_rule = 2
+    assert prep(a) == EINVAL
+    nv = act(fmt=1)
+    nv.tensor_scale = FAKE
+    nv.scale_rule = 1
+    assert prep(nv, fmt=1) == EUNSUPPORTED            # the ceil rule is an MXFP4 option
+    m = act(mode=1)
+    m.scale_rule = 1
+    assert prep(m) == EUNSUPPORTED                    # ... of the method's own combination
+    h = act(fmt=2)
+    h.dbg_mask = FAKE
+    assert prep(h, fmt=2) == EUNSUPPORTED             # no debug outputs for HiF4
+    d = act()
+    d.dbg_r = FAKE + 2
+    assert prep(d) == EALIGN
+    # dense-only backbone: sp_codes and sp_meta NULL beside sp_dense
+    do = Act(8, 160, 0, Pattern(2, 4, 0), None, None, FAKE, FAKE, FAKE, None, 0, None, FAKE)
+    assert prep(do, K=160) == EUNSUPPORTED            # K must be a multiple of 128
+    half = Act(8, 128, 0, Pattern(2, 4, 0), FAKE, None, FAKE, FAKE, FAKE, None, 0, None, FAKE)
+    assert prep(half) == EINVAL                       # codes without metadata
+    w = Weight(64, 128, 1, 1, FAKE, FAKE, FAKE, FAKE, 1)
+    assert L.sharq_quantize_weight(FAKE, 0, 64, 128, 128, ctypes.byref(w), None) == EUNSUPPORTED
+    w = Weight(64, 128, 1, 0, FAKE, FAKE, FAKE, None, 7)
+    assert L.sharq_quantize_weight(FAKE, 0, 64, 128, 128, ctypes.byref(w), None) == EINVAL

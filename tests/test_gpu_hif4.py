@@ -10,6 +10,7 @@ import pytest
 import torch
 
 from oracle import sharq_oracle as O
+import panel_layout as L
 from paper_2606_26587_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -40,7 +41,7 @@ def check_prep(S, G, x, g, eps, tag):
     a = S.sharq_prepare(G.dev_bf16(x), None if g is None else G.dev_bf16(g), eps, 2, 4, "hif4")
     torch.cuda.synchronize()
     o = O.prepare(x, g, eps, 2, 4, "hif4")
-    dev = O.act_to_device_layout(o)
+    dev = L.act_to_device_layout(o)
     for name in O.ACT_BUFFERS:
         G.assert_bytes_equal(f"{tag}:{name}", G.host(getattr(a, name)), dev[name])
     return a, o
@@ -83,7 +84,7 @@ def test_hif4_weight_quant_bit_exact(S, G, N, K, dt):
     wd = G.dev_bf16(w) if dt == "bf16" else torch.from_numpy(O.bf16_bits_to_f32(w)).cuda()
     q = S.sharq_quantize_weight(wd, "hif4")
     torch.cuda.synchronize()
-    o = O.weight_to_device_layout(O.quantize_weight(w, "hif4"))
+    o = L.weight_to_device_layout(O.quantize_weight(w, "hif4"))
     G.assert_bytes_equal("codes", G.host(q.codes[0]), o["codes"])
     G.assert_bytes_equal("scale", G.host(q.scale[0]), o["scale"])
 

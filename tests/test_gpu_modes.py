@@ -13,6 +13,7 @@ import pytest
 import torch
 
 from oracle import sharq_oracle as O
+import panel_layout as L
 from paper_2606_26587_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -49,7 +50,7 @@ def check_prep(S, G, x, g, eps, n, m, fmt, mode, pairs, tag):
     if fmt == "nv":
         got = np.asarray(G.host(a.tensor_scale)[0], np.float32).view(np.uint32)
         assert got == np.asarray(o["tensor_scale"], np.float32).view(np.uint32), tag
-    dev = O.act_to_device_layout(o)
+    dev = L.act_to_device_layout(o)
     for name in O.ACT_BUFFERS_ALL:
         t = a.dn_meta if name == "dn_meta" else getattr(a, name)
         G.assert_bytes_equal(f"{tag}:{mode}:{name}", G.host(t), dev[name])

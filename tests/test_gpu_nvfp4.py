@@ -12,6 +12,7 @@ import pytest
 import torch
 
 from oracle import sharq_oracle as O
+import panel_layout as L
 from paper_2606_26587_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -51,7 +52,7 @@ def check_prep_nv(S, G, x, g, eps, n, m, tag, ts_in=None):
     o = O.prepare(x, g, eps, n, m, "nv", tensor_scale=ts_in)
     assert f32_bits(G.host(a.tensor_scale)[0]) == f32_bits(o["tensor_scale"]), \
         (tag, float(G.host(a.tensor_scale)[0]), float(o["tensor_scale"]))
-    dev = O.act_to_device_layout(o)
+    dev = L.act_to_device_layout(o)
     for name in O.ACT_BUFFERS:
         G.assert_bytes_equal(f"{tag}:{name}", G.host(getattr(a, name)), dev[name])
     return a, o
@@ -125,7 +126,7 @@ def test_nv_weight_quant_bit_exact(S, G, N, K, dt):
     q = S.sharq_quantize_weight(wd, "nv")
     torch.cuda.synchronize()
     wo = O.quantize_weight(w, "nv")
-    o = O.weight_to_device_layout(wo)
+    o = L.weight_to_device_layout(wo)
     assert f32_bits(G.host(q.tensor_scale)[0]) == f32_bits(wo["tensor_scale"])
     for name in O.WEIGHT_BUFFERS:
         G.assert_bytes_equal(name, G.host(getattr(q, name)[0]), o[name])

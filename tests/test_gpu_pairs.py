@@ -14,6 +14,7 @@ import pytest
 import torch
 
 from oracle import sharq_oracle as O
+import panel_layout as L
 from paper_2606_26587_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -50,7 +51,7 @@ def check_prep_pairs(S, G, x, g, eps, fmt, tag):
     o = O.prepare(x, g, eps, 4, 8, fmt, pairs=True)
     if fmt == "nv":
         assert f32_bits(G.host(a.tensor_scale)[0]) == f32_bits(o["tensor_scale"]), tag
-    dev = O.act_to_device_layout(o)
+    dev = L.act_to_device_layout(o)
     for name in O.ACT_BUFFERS:
         G.assert_bytes_equal(f"{tag}:{name}", G.host(getattr(a, name)), dev[name])
     return a, o

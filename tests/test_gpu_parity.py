@@ -13,6 +13,7 @@ import pytest
 import torch
 
 from oracle import sharq_oracle as O
+import panel_layout as L
 from paper_2606_26587_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -68,7 +69,7 @@ def check_prep(S, G, x_u16, gamma_u16, eps, n, m, tag):
     say(f"[prep] {tag} shape={x_u16.shape} n:m={n}:{m} gamma={gamma_u16 is not None}")
     a = run_prep(S, G, x_u16, gamma_u16, eps, n, m)
     o = O.prepare(x_u16, gamma_u16, eps, n, m, "mx")
-    dev = O.act_to_device_layout(o)
+    dev = L.act_to_device_layout(o)
     for name in O.ACT_BUFFERS:
         G.assert_bytes_equal(f"{tag}:{name}", G.host(getattr(a, name)), dev[name])
     return a, o
@@ -131,7 +132,7 @@ def test_prep_strided_rows(S, G):
     a = S.sharq_prepare(xd, None, 1e-6, 2, 4, "mx")
     torch.cuda.synchronize()
     o = O.prepare(np.ascontiguousarray(full[:, :K]), None, 1e-6, 2, 4, "mx")
-    dev = O.act_to_device_layout(o)
+    dev = L.act_to_device_layout(o)
     for name in O.ACT_BUFFERS:
         G.assert_bytes_equal(name, G.host(getattr(a, name)), dev[name])
 
@@ -142,7 +143,7 @@ def test_weight_quant_bit_exact(S, G, N, K):
     w = synth.weight(N, K, seed=N)
     q = S.sharq_quantize_weight(G.dev_bf16(w), "mx")
     torch.cuda.synchronize()
-    o = O.weight_to_device_layout(O.quantize_weight(w, "mx"))
+    o = L.weight_to_device_layout(O.quantize_weight(w, "mx"))
     G.assert_bytes_equal("codes", G.host(q.codes[0]), o["codes"])
     G.assert_bytes_equal("scale", G.host(q.scale[0]), o["scale"])
 
@@ -152,7 +153,7 @@ def test_weight_quant_fp32_input(S, G):
     wf = torch.from_numpy(O.bf16_bits_to_f32(w)).cuda()
     q = S.sharq_quantize_weight(wf, "mx")
     torch.cuda.synchronize()
-    o = O.weight_to_device_layout(O.quantize_weight(w, "mx"))
+    o = L.weight_to_device_layout(O.quantize_weight(w, "mx"))
     G.assert_bytes_equal("codes", G.host(q.codes[0]), o["codes"])
 
 
@@ -227,24 +228,118 @@ def test_end_to_end_deterministic(S, G):
 LLAMA_T = 2048
 
 
+# rows of the full-shape GEMM comparison: every row of qkv and down, 512 of
+# gate_up's 2048 (token 0, the massive-activation row, among them)
+FULL_ROWS = {"qkv": None, "gate_up": 512, "down": None}
+
+
+def full_rows(name):
+    if FULL_ROWS[name] is None:
+        return np.arange(LLAMA_T)
+    rows = np.random.default_rng(1).choice(LLAMA_T, FULL_ROWS[name], replace=False)
+    rows[0] = 0
+    return np.sort(rows)
+
+
 @pytest.mark.parametrize("name", ["qkv", "gate_up", "down"])
 def test_llama_full_shape(S, G, name):
-    """Full M=2048 Llama-3.1-8B shapes in the benchmark's launch configuration:
-    preparation compared in full, GEMM on 64 sampled rows x all columns."""
+    """Full M=2048 Llama-3.1-8B shapes in the benchmark's launch configuration
+    (the preparation writes the dense backbone copy, the GEMM reads it):
+    preparation compared in full, dense copy included; the GEMM on every row
+    (qkv, down) or 512 rows (gate_up) x all columns against the oracle, and
+    bit-identical to the GEMM that expands the compressed backbone."""
     K, N, norm = synth.LLAMA_LINEARS[name]
-    say(f"[llama] {name} T={LLAMA_T} K={K} N={N}")
+    say(f"[llama] {name} T={LLAMA_T} K={K} N={N} (dense backbone copy)")
     x = synth.activations(LLAMA_T, K, seed=0)
     g = synth.gamma(K, seed=0) if norm else None
     w = synth.weight(N, K, seed=0)
-    a, o = check_prep(S, G, x, g, synth.LLAMA_EPS, 2, 4, name)
+    xd, gd = G.dev_bf16(x), (None if g is None else G.dev_bf16(g))
+    a = S.sharq_prepare(xd, gd, synth.LLAMA_EPS, 2, 4, "mx",
+                        out=S.alloc_act(LLAMA_T, K, 2, 4, "mx", "cuda", dense_backbone=True))
     wq = S.sharq_quantize_weight(G.dev_bf16(w))
     y = S.sharq_linear(a, wq, dtype=torch.float32)
+    y16 = S.sharq_linear(a, wq, dtype=torch.bfloat16)
+    c = S.sharq_prepare(xd, gd, synth.LLAMA_EPS, 2, 4, "mx")
+    yc = S.sharq_linear(c, wq, dtype=torch.float32)
     torch.cuda.synchronize()
+    o = O.prepare(x, g, synth.LLAMA_EPS, 2, 4, "mx")
+    dev = L.act_to_device_layout(o)
+    for buf in O.ACT_BUFFERS:
+        G.assert_bytes_equal(f"{name}:{buf}", G.host(getattr(a, buf)), dev[buf])
+    G.assert_bytes_equal(f"{name}:sp_dense", G.host(a.sp_dense), L.dense_backbone_to_device_layout(o))
+    assert torch.equal(y, yc)
+    assert torch.equal(y16, y.to(torch.bfloat16))
     wo = G.weight_to_oracle(wq)
-    rows = np.random.default_rng(1).choice(LLAMA_T, 64, replace=False)
-    rows[0] = 0   # the massive-activation token
+    rows = full_rows(name)
+    gemm_check(G.host(y)[rows], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), name)
+
+
+# --------------------------------------------------------------------------- exact sums at full K
+
+def exact_operands(T, N, K, variant, seed):
+    """A prepared activation (2:4) and a weight built directly from random
+    codes and scales such that every fp32 partial sum of the two-path GEMM is
+    exact, whatever the order of accumulation:
+      'unit'    every E8M0 scale 127 (2^0), all 16 codes: products are
+                multiples of 1/4 below 36, and 2 K 36 < 2^22 for K <= 14336;
+      'act'     activation scales in {126, 127, 128} with activation codes of
+                magnitude <= 2, weight scales 127: multiples of 1/8 below 24;
+      'weight'  the same with the roles exchanged.
+    The fp32 result must then equal the exact (fp64) sum bit for bit, so a
+    single dropped, repeated or misplaced product shows."""
+    rng = np.random.default_rng(seed)
+    pairs = np.array([(0, 1), (0, 2), (0, 3), (1, 2), (1, 3), (2, 3)])
+    sel = pairs[rng.integers(0, 6, size=(T, K // 4))]
+    keep = np.zeros((T, K // 4, 4), bool)
+    t, gi = np.meshgrid(np.arange(T), np.arange(K // 4), indexing="ij")
+    keep[t, gi, sel[..., 0]] = True
+    keep[t, gi, sel[..., 1]] = True
+    keep = keep.reshape(T, K)
+
+    def codes(shape, small):
+        mag = rng.integers(0, 5 if small else 8, size=shape)
+        return (mag | (rng.integers(0, 2, size=shape) << 3)).astype(np.uint8)
+
+    def scales(shape, vary):
+        return (rng.integers(126, 129, size=shape) if vary else np.full(shape, 127)).astype(np.uint8)
+
+    small_a, small_w = variant == "act", variant == "weight"
+    sp = np.where(keep, codes((T, K), small_a), 0).astype(np.uint8)
+    sp_codes, sp_meta = O.pack_backbone(sp, keep, 2, 4)
+    act = {"rows": T, "K": K, "n": 2, "m": 4, "pairs": False, "fmt": "mx", "tensor_scale": None, "mode": "sharq",
+           "sp_codes": sp_codes, "sp_meta": sp_meta, "sp_scale": scales((T, K // 32), small_a),
+           "dn_codes": O.pack_nibbles(codes((T, K), small_a)), "dn_scale": scales((T, K // 32), small_a),
+           "dn_meta": np.zeros((T, 0), np.uint8)}
+    wq = {"N": N, "K": K, "fmt": "mx", "tensor_scale": None, "codes": O.pack_nibbles(codes((N, K), small_w)),
+          "scale": scales((N, K // 32), small_w)}
+    wq["scale_dn"] = wq["scale"]
+    return act, wq
+
+
+@pytest.mark.parametrize("variant", ["unit", "act", "weight"])
+@pytest.mark.parametrize("name", ["qkv", "gate_up", "down"])
+def test_exact_sums_full_shape(S, G, name, variant):
+    """The benchmarked GEMM (dense backbone copy) and the compressed-backbone
+    GEMM at the full Llama shapes, on operands whose sums are exact in fp32:
+    the output must equal the oracle's exact result bit for bit (every row of
+    qkv and down, 512 rows of gate_up)."""
+    K, N, _ = synth.LLAMA_LINEARS[name]
+    say(f"[exact] {name} T={LLAMA_T} K={K} N={N} variant={variant}")
+    o, wo = exact_operands(LLAMA_T, N, K, variant, seed=K + N + len(variant))
+    a = G.oracle_to_act(o, dense_backbone=True)
+    w = G.oracle_to_weight(wo)
+    yd = S.sharq_linear(a, w, dtype=torch.float32)
+    a.sp_dense = None
+    yc = S.sharq_linear(a, w, dtype=torch.float32)
+    torch.cuda.synchronize()
+    rows = full_rows(name)
     ref = O.linear(o, wo, rows=rows)
-    gemm_check(G.host(y)[rows], ref, O.linear_abs(o, wo, rows=rows), name)
+    for tag, y in (("dense copy", yd), ("compressed", yc)):
+        got = G.host(y)[rows].astype(np.float64)
+        bad = np.nonzero(got != ref)
+        assert bad[0].size == 0, (f"{name} {variant} {tag}: {bad[0].size} outputs differ from the exact sum; "
+                                  f"first at {bad[0][0]},{bad[1][0]}: {got[bad[0][0], bad[1][0]]} "
+                                  f"vs {ref[bad[0][0], bad[1][0]]}")
 
 
 # --------------------------------------------------------------------------- decode shapes
@@ -394,15 +489,20 @@ def test_persistent_tail_half_tiles(S, G, T, N, K, n, m):
 
 # --------------------------------------------------------------------------- dense backbone copy
 
-@pytest.mark.parametrize("T,K,N,use_gamma,n,m,pairs", [(256, 1024, 512, True, 2, 4, False),
+@pytest.mark.parametrize("T,K,N,use_gamma,n,m,pairs", [(300, 1024, 512, True, 2, 4, False),
                                                        (300, 640, 300, True, 4, 8, False),
-                                                       (160, 2048, 256, False, 4, 8, True),
-                                                       (130, 416, 96, False, 2, 4, False),
-                                                       (40, 1024, 128, True, 2, 4, False)])
+                                                       (288, 2048, 256, False, 4, 8, True),
+                                                       (40, 1024, 12544, True, 2, 4, False),
+                                                       (200, 512, 12800, False, 2, 4, False),
+                                                       (130, 416, 96, False, 2, 4, False)])
 def test_dense_backbone_copy(S, G, T, K, N, use_gamma, n, m, pairs):
     """The optional dense backbone copy: byte-exact against the oracle's
     backbone codes, and the main GEMM on it gives bit-identically the result
-    of expanding the compressed backbone (the MFMA operands are the same)."""
+    of expanding the compressed backbone (the MFMA operands are the same).
+    Every case but the last reaches the persistent kernel that reads the copy
+    (K a multiple of 128, and M > 256 or at least 48 tiles of 128 x 256: the
+    small-M kernel takes the rest); the last (K = 416) runs the ragged-K
+    kernel, which ignores the copy."""
     say(f"[dense-backbone] T={T} K={K} N={N} {n}:{m}{'p' if pairs else ''}")
     x = synth.activations(T, K, seed=K + T)
     g = synth.gamma(K, seed=3) if use_gamma else None
@@ -416,7 +516,7 @@ def test_dense_backbone_copy(S, G, T, K, N, use_gamma, n, m, pairs):
     yd16 = S.sharq_linear(a, wq, dtype=torch.bfloat16)
     torch.cuda.synchronize()
     o = O.prepare(x, g, 1e-6, n, m, "mx", pairs=pairs)
-    G.assert_bytes_equal("sp_dense", G.host(a.sp_dense), O.to_panels(o["sp_dense"], K))
+    G.assert_bytes_equal("sp_dense", G.host(a.sp_dense), L.dense_backbone_to_device_layout(o))
     for name in O.ACT_BUFFERS:
         G.assert_bytes_equal(name, G.host(getattr(a, name)), G.host(getattr(c, name)))
     assert torch.equal(yd, yc)

@@ -9,6 +9,7 @@ import pytest
 import torch
 
 from oracle import sharq_oracle as O
+import panel_layout as L
 from paper_2606_26587_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -51,7 +52,7 @@ def check(S, G, x, res, g, eps, n, m, fmt, pairs, tag, in_place=False):
         G.assert_bytes_equal(f"{tag}:residual untouched", G.host(rd.view(torch.int16)).view(np.uint16), res)
     if fmt == "nv":
         assert f32_bits(G.host(a.tensor_scale)[0]) == f32_bits(o["tensor_scale"]), tag
-    dev = O.act_to_device_layout(o)
+    dev = L.act_to_device_layout(o)
     for name in O.ACT_BUFFERS:
         G.assert_bytes_equal(f"{tag}:{name}", G.host(getattr(a, name)), dev[name])
 

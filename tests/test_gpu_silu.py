@@ -14,6 +14,7 @@ import pytest
 import torch
 
 from oracle import sharq_oracle as O
+import panel_layout as L
 from paper_2606_26587_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -69,7 +70,7 @@ def check_silu(S, G, T, K, n, m, fmt, pairs, tag, strided=False, seed=0):
         for act in (a, b):
             got = np.asarray(G.host(act.tensor_scale)[0], np.float32).view(np.uint32)
             assert got == np.asarray(o["tensor_scale"], np.float32).view(np.uint32), tag
-    dev = O.act_to_device_layout(o)
+    dev = L.act_to_device_layout(o)
     for act in (a, b):
         for name in O.ACT_BUFFERS:
             G.assert_bytes_equal(f"{tag}:{name}", G.host(getattr(act, name)), dev[name])

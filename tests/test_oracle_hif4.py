@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 
 from oracle import sharq_oracle as O
+import panel_layout as L
 from paper_2606_26587_amd import synth
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -224,10 +225,29 @@ def test_hif4_backbone_residual_and_gemm():
 def test_hif4_device_layout_roundtrip():
     x = synth.activations(9, 384, seed=2)
     o = O.prepare(x, None, 1e-6, 2, 4, "hif4")
-    back = O.act_from_device_layout(O.act_to_device_layout(o), 9, 384, 2, 4, "hif4")
+    back = L.act_from_device_layout(L.act_to_device_layout(o), 9, 384, 2, 4, "hif4")
     for k in O.ACT_BUFFERS:
         assert np.array_equal(back[k], o[k]), k
     wq = O.quantize_weight(synth.weight(40, 384, seed=2), "hif4")
-    wb = O.weight_from_device_layout(O.weight_to_device_layout(wq), 40, 384, "hif4")
+    wb = L.weight_from_device_layout(L.weight_to_device_layout(wq), 40, 384, "hif4")
     for k in O.WEIGHT_BUFFERS:
         assert np.array_equal(wb[k], wq[k]), k
+
+
+def test_hif4_scale_factor_reading_differs_from_a_bf16_intermediate():
+    """Reading R11 rounds SF = fl32(Vmax * bf16(1/7)) straight to E6M2.  The
+    algorithm's name for SF suggests a bf16 intermediate; with Vmax = 7.9 the
+    two readings give different E6M2 codes (SF = 1.1264: bf16 takes it to the
+    E6M2 midpoint 1.125, which then rounds to the even 1.0, while direct
+    rounding gives 1.25), so the choice is observable and the oracle's is the
+    direct one."""
+    v = np.zeros((1, 64), np.float32)
+    v[0, 5] = 7.9
+    v[0, 40] = -3.0
+    _, meta, _ = O.hif4_quantize(v)
+    sf = np.float32(np.float32(7.9) * O.ONE_SEVENTH_BF16)
+    direct = int(O.e6m2_round(sf))
+    via_bf16 = int(O.e6m2_round(O.bf16_round_f32(sf)))
+    assert direct != via_bf16
+    assert direct == (48 << 2) | 1 and via_bf16 == 48 << 2
+    assert int(meta[0, 0]) == direct

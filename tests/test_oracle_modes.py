@@ -16,6 +16,7 @@ import numpy as np
 import pytest
 
 from oracle import sharq_oracle as O
+import panel_layout as L
 from paper_2606_26587_amd import synth
 
 GRID = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]
@@ -192,8 +193,8 @@ def test_buffer_widths_per_mode():
 def test_mode_device_layout_roundtrip(mode, K):
     x, g = case("nv", T=9, K=K, seed=K)
     o = O.prepare_mode(x, g, 1e-6, 4, 8, "nv", mode)
-    dev = O.act_to_device_layout(o)
-    back = O.act_from_device_layout(dev, 9, K, 4, 8, "nv", o["tensor_scale"], mode=mode)
+    dev = L.act_to_device_layout(o)
+    back = L.act_from_device_layout(dev, 9, K, 4, 8, "nv", o["tensor_scale"], mode=mode)
     for k in O.ACT_BUFFERS_ALL:
         assert np.array_equal(back[k], o[k]), k
 

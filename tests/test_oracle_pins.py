@@ -15,6 +15,7 @@ import numpy as np
 import pytest
 
 from oracle import sharq_oracle as O
+import panel_layout as L
 from paper_2606_26587_amd import synth
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -94,6 +95,55 @@ def test_e8m0_exponent_matches_frexp_and_normalizes_peak():
     un = e > -127
     assert np.all((r[un] >= 4) & (r[un] < 8))
     assert O.e8m0_exponent(f32([0.0]))[0] == -127
+
+
+def _ceil_rule_brute_force(a: float) -> int:
+    """Smallest e in [-127, 127] with a <= 6 * 2^e, by search in exact
+    arithmetic (-127 for a = 0)."""
+    fa = Fraction(a)
+    for e in range(-127, 128):
+        if fa <= 6 * Fraction(2) ** e:
+            return e
+    raise AssertionError(a)
+
+
+def test_e8m0_ceil_rule_is_brute_force_smallest_unclipped_scale():
+    """R13: e = ceil(log2(amax / 6)) against a search over every E8M0
+    exponent, on values at and around the 1.5 * 2^E switch points, powers of
+    two, subnormals, random magnitudes over the whole fp32 range, and the
+    largest float."""
+    rng = np.random.default_rng(13)
+    E = rng.integers(-140, 127, size=200)
+    edges = np.concatenate([np.ldexp(1.5, E), np.ldexp(1.0, E), np.ldexp(1.75, E)])
+    rand = np.ldexp(rng.uniform(1.0, 2.0, 400), rng.integers(-149, 128, 400))
+    a = np.concatenate([ulps_around(f32(edges[np.isfinite(edges)]), 2),
+                        f32(rand[np.isfinite(f32(rand))]), f32([1e-45, 3e-39, 6.0, 12.0, 3.4028235e38])])
+    a = a[(a > 0) & np.isfinite(a)]
+    got = O.e8m0_exponent(a, "ceil")
+    for v, e in zip(a, got):
+        assert int(e) == _ceil_rule_brute_force(float(v)), (float(v), int(e))
+    assert int(O.e8m0_exponent(f32([0.0]), "ceil")[0]) == -127
+    # the floor rule is the ceil rule or one below it
+    d = got - O.e8m0_exponent(a, "floor")
+    assert set(np.unique(d)) <= {0, 1}
+
+
+def test_e8m0_ceil_rule_never_clips_and_normalizes_the_peak():
+    """Under the ceil rule no value of a block exceeds 6 * 2^e, so no code
+    saturates, and a block peak of normal magnitude lands in (3, 6] * 2^e;
+    the residual against the quantized backbone stays exact."""
+    x = synth.activations(16, 1024, seed=13)
+    y = O.bf16_bits_to_f32(x)
+    codes, e, _, deq = O.mx_quantize(y, None, "ceil")
+    peak = np.abs(y).reshape(16, 32, 32).max(axis=2)
+    scaled = peak / np.ldexp(1.0, e)
+    assert np.all(scaled <= 6.0) and np.all(scaled > 3.0)
+    # a value rounds to the nearest E2M1 magnitude without saturating: the
+    # error is at most half the grid step at its magnitude (1 between 4 and 6)
+    err = np.abs(deq.astype(np.float64) - y) / np.ldexp(1.0, np.repeat(e, 32, axis=1))
+    assert err.max() <= 1.0
+    o = O.prepare(x, None, 1e-6, 2, 4, "mx", scale_rule="ceil")
+    assert np.array_equal((o["d_sp"] + o["R"]).astype(np.float32), y)
 
 
 def test_pow2_f32_exact():
@@ -508,9 +558,9 @@ def test_panel_layout_roundtrip_and_order(K):
     rng = np.random.default_rng(K)
     R = 7
     a = rng.integers(0, 256, size=(R, K // 2), dtype=np.uint8)
-    flat = O.to_panels(a, K)
+    flat = L.to_panels(a, K)
     assert flat.size == a.size
-    assert np.array_equal(O.from_panels(flat, R, K, K // 2), a)
+    assert np.array_equal(L.from_panels(flat, R, K, K // 2), a)
     # panel 0 holds row 0's first 64 bytes, then row 1's first 64 bytes, ...
     w0 = min(128, K) // 2
     assert np.array_equal(flat[:w0], a[0, :w0]) and np.array_equal(flat[w0:2 * w0], a[1, :w0])
