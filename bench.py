@@ -44,6 +44,7 @@ kernel for scaling the profiler's HBM byte counters) and nothing else.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -142,40 +143,119 @@ def cpu_model():
     return platform.processor() or None
 
 
-def cpu_baseline(rows=T_TOKENS, min_seconds=10.0, max_passes=3):
-    """The CPU oracle on a bounded sample of the same step: `rows` of the 2048
-    token rows of each linear (preparation + two-path fp64 GEMM), repeated
-    until about `min_seconds` of CPU work (at most `max_passes` passes).  The
-    oracle's preparation is NumPy element-wise work on one thread; its GEMM is
-    a float64 matrix product on the BLAS threads (`cores`).  value counts the
-    same algorithmic work as the GPU line (F_alg)."""
+def cpu_baseline(rows=256):
+    """The CPU oracles on a bounded sample of the same step: `rows` of the 2048
+    token rows of each Llama linear (preparation + two-path fp64 GEMM; the
+    weights are quantized beforehand, untimed, as on the GPU).  The plain C
+    oracle (oracle/sharq_ref.c, OpenMP over rows) is timed with one thread and
+    with every host core for the preparation, and with every core for the
+    GEMM; value is F_alg of the sample over its all-core time.  The NumPy
+    oracle (element-wise preparation on one thread, BLAS float64 GEMM) is
+    timed on the same sample beside it."""
+    import ctypes as ct
+    from oracle import build_ref
     from oracle import sharq_oracle as O
     from paper_2606_26587_amd import synth
-    cases = []
+    C = build_ref.load()
+    cores = len(os.sched_getaffinity(0))
+
+    def p(a):
+        return ct.c_void_p(a.ctypes.data)
+
+    flops = t_prep1 = t_prep = t_gemm = t_np_prep = t_np_gemm = 0.0
     for name, (K, N, norm) in synth.LLAMA_LINEARS.items():
-        x = synth.activations(T_TOKENS, K, seed=0)[:rows]
+        x = np.ascontiguousarray(synth.activations(T_TOKENS, K, seed=0)[:rows])
         g = synth.gamma(K, seed=0) if norm else None
-        cases.append((K, N, x, g, O.quantize_weight(synth.weight(N, K, seed=0))))
-    flops = 0.0
-    t_prep = t_gemm = 0.0
-    passes = 0
-    while passes < max_passes and (passes == 0 or t_prep + t_gemm < min_seconds):
-        for K, N, x, g, wq in cases:
+        w = np.ascontiguousarray(synth.weight(N, K, seed=0))
+        wc, ws = np.zeros((N, K // 2), np.uint8), np.zeros((N, K // 32), np.uint8)
+        C.sharq_ref_set_threads(0)
+        C.sharq_ref_quantize_weight(p(w), N, K, K, 0, p(wc), p(ws))
+        bufs = [np.zeros((rows, K // 4), np.uint8), np.zeros((rows, K // 8), np.uint8),
+                np.zeros((rows, K // 32), np.uint8), np.zeros((rows, K // 2), np.uint8),
+                np.zeros((rows, K // 32), np.uint8)]
+        args = [p(x), rows, K, K, None if g is None else p(g), ct.c_float(synth.LLAMA_EPS), 2, 4, 0,
+                *(p(b) for b in bufs), None, None]
+        for threads in (1, cores):
+            C.sharq_ref_set_threads(threads)
             t0 = time.perf_counter()
-            a = O.prepare(x, g, synth.LLAMA_EPS, 2, 4, "mx")
-            t1 = time.perf_counter()
-            O.linear(a, wq)
-            t2 = time.perf_counter()
-            t_prep += t1 - t0
-            t_gemm += t2 - t1
-            flops += alg_flops(rows, N, K)
-        passes += 1
-    elapsed = t_prep + t_gemm
-    return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": cpu_threads(), "kind": "oracle",
-            "sample": f"{passes} pass(es) over {rows} of the {T_TOKENS} token rows of each Llama linear "
-                      f"(qkv, gate_up, down): NumPy preparation + fp64 two-path GEMM; weight quantization untimed",
-            "seconds": elapsed, "prep_seconds_1_thread": t_prep, "gemm_seconds_blas_threads": t_gemm,
-            "host_cpus": len(os.sched_getaffinity(0)), "cpu": cpu_model()}
+            if C.sharq_ref_prepare(*args) != 0:
+                raise RuntimeError("C oracle preparation failed")
+            dt = time.perf_counter() - t0
+            if threads == 1:
+                t_prep1 += dt
+            else:
+                t_prep += dt
+        Y = np.zeros((rows, N), np.float64)
+        t0 = time.perf_counter()
+        if C.sharq_ref_linear(rows, K, 2, 4, *(p(b) for b in bufs), N, p(wc), p(ws), p(Y), N) != 0:
+            raise RuntimeError("C oracle GEMM failed")
+        t_gemm += time.perf_counter() - t0
+        # the NumPy oracle's GEMM reads the same weight bytes (the two oracles
+        # quantize identically; their tests compare them byte for byte)
+        wq = {"N": N, "K": K, "fmt": "mx", "codes": wc, "scale": ws, "scale_dn": ws, "tensor_scale": None}
+        t0 = time.perf_counter()
+        a = O.prepare(x, g, synth.LLAMA_EPS, 2, 4, "mx")
+        t1 = time.perf_counter()
+        O.linear(a, wq)
+        t_np_prep += t1 - t0
+        t_np_gemm += time.perf_counter() - t1
+        flops += alg_flops(rows, N, K)
+    C.sharq_ref_set_threads(0)
+    return {"value": flops / (t_prep + t_gemm) / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"{rows} of the {T_TOKENS} token rows of each Llama linear (qkv, gate_up, down): the C "
+                      f"oracle's preparation and fp64 two-path GEMM on all {cores} host cores; weight quantization "
+                      f"untimed",
+            "seconds": t_prep + t_gemm, "prep_seconds_1_thread": t_prep1, "prep_seconds_all_cores": t_prep,
+            "gemm_seconds_all_cores": t_gemm, "prep_speedup_all_cores": t_prep1 / max(t_prep, 1e-12),
+            "numpy_oracle": {"value": flops / (t_np_prep + t_np_gemm) / 1e12, "unit": "TFLOP/s",
+                             "prep_seconds_1_thread": t_np_prep, "gemm_seconds_blas": t_np_gemm,
+                             "blas_threads": cpu_threads()},
+            "host_cpus": cores, "cpu": cpu_model()}
+
+
+class HipEvent:
+    """A timing-only HIP event created with hipEventDisableSystemFence: its
+    record carries no system-scope release, so it does not write back and
+    invalidate the caches between the kernels it brackets (with the default
+    flags every record left a gap of ~6 us between kernels on MI355X).  The
+    calls go to the HIP runtime torch has loaded (one libamdhip64.so.7 per
+    process)."""
+
+    DISABLE_SYSTEM_FENCE = 0x20000000
+    _lib = None
+
+    @classmethod
+    def lib(cls):
+        if cls._lib is None:
+            L = ctypes.CDLL("libamdhip64.so.7")
+            L.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            L.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            L.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+            L.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            L.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            cls._lib = L
+        return cls._lib
+
+    def __init__(self):
+        self.h = ctypes.c_void_p()
+        if self.lib().hipEventCreateWithFlags(ctypes.byref(self.h), self.DISABLE_SYSTEM_FENCE) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
+
+    def record(self, stream):
+        if self.lib().hipEventRecord(self.h, ctypes.c_void_p(stream.cuda_stream)) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_time(self, end) -> float:
+        """Milliseconds from this event to `end` (both recorded)."""
+        self.lib().hipEventSynchronize(end.h)
+        ms = ctypes.c_float()
+        if self.lib().hipEventElapsedTime(ctypes.byref(ms), self.h, end.h) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def __del__(self):
+        if self._lib is not None and self.h:
+            self._lib.hipEventDestroy(self.h)
 
 
 class Timer:
@@ -183,7 +263,7 @@ class Timer:
 
     def __init__(self, torch, stream, n_ops, steps):
         self.stream = stream
-        self.ev = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ops + 1)] for _ in range(steps)]
+        self.ev = [[HipEvent() for _ in range(n_ops + 1)] for _ in range(steps)]
 
     def mark(self, step, i):
         self.ev[step][i].record(self.stream)
@@ -203,7 +283,7 @@ def run_steps(torch, stream, step, n_ops, steps, warmup):
         step(i, lambda k, i=i: tw.mark(i, k))
     torch.cuda.synchronize()
     tm = Timer(torch, stream, n_ops, steps)
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0, t1 = HipEvent(), HipEvent()
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t0.record(stream)
@@ -292,7 +372,7 @@ def copy_same_bytes(torch, dev, stream, nbytes, reps=20):
         # torch's copy_ would go to the runtime's blit kernel instead
         for i in range(3):
             torch.bitwise_not(srcs[i % nsrc], out=dst)
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev = [HipEvent() for _ in range(reps + 1)]
         ev[0].record(stream)
         for i in range(reps):
             torch.bitwise_not(srcs[i % nsrc], out=dst)
@@ -669,7 +749,7 @@ def main():
                     help="prefill: how the preparation stores the backbone for the GEMM -- the dense copy alone "
                          "(default), the dense copy beside the compressed form, or the compressed form only "
                          "(the GEMM then expands it)")
-    ap.add_argument("--cpu-rows", type=int, default=T_TOKENS)
+    ap.add_argument("--cpu-rows", type=int, default=256)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
     args = ap.parse_args()
     if args.gpus != 1:

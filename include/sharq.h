@@ -319,12 +319,13 @@ SHARQ_API sharq_status sharq_prepare_residual(const void *X, const void *residua
  * Preparation of a down projection's input with the SiLU.mul that produces it
  * fused in on the producer side (Sec. 4.3: the preparation absorbs the
  * preprocessing steps of the data flow).  Per element,
- * h = bf16(SiLU(g) * u), SiLU(g) = g / (1 + exp(-g)), evaluated in fp32 with
- * the hardware exponential and reciprocal (~1 ulp each; for g < 0 with e^g
- * kept normal by a power-of-two scale) and rounded to bf16 to nearest even
- * once; for finite inputs with |g u| < 1e19, h is within one bf16 step of the
- * exactly rounded value.  h is prepared without RMSNorm exactly as sharq_prepare prepares X,
- * and written to h_out (bf16 [M][K], row stride ldh) when h_out is not NULL.
+ * h = bf16(SiLU(g) * u), SiLU(g) = g / (1 + exp(-g)), by one fixed fp32
+ * recipe: t = e^-|g| (Cody-Waite argument reduction and the degree-7 Taylor
+ * polynomial, within 2 ulp), s = g / (1 + t) for g >= 0 and g t / (1 + t)
+ * below (correctly rounded division), h = bf16(s u) to nearest even.  h is
+ * thus a fixed function of (g, u), within one bf16 step of the exactly
+ * rounded value; inputs must keep s u finite.  h is prepared without RMSNorm
+ * exactly as sharq_prepare prepares X, and written to h_out (bf16 [M][K], row stride ldh) when h_out is not NULL.
  * gate, up: bf16 [M][K], row strides ldg, ldu (e.g. the two halves of a
  * gate/up projection's output, ldg = ldu = 2K); 16-byte aligned with 16-byte
  * row strides.  With NVFP4 and no tensor_scale_in the amax pre-pass forms h

@@ -74,8 +74,13 @@ Readings where the paper is silent (each also listed in the design notes):
       scale.  Metadata bytes per unit: E6M2 code, E1_8 bits, E1_16 bits
       (low byte, high byte), bit j = group j.
   R12 SiLU.mul fused into the preparation of the down projection's input:
-      h = bf16(SiLU(g) * u) with SiLU(g) = g / (1 + exp(-g)), the product
-      evaluated in fp64 and rounded to bf16 once (nearest even); the
+      h = bf16(SiLU(g) * u), SiLU(g) = g / (1 + exp(-g)).  The paper does not
+      fix its arithmetic; it is taken as one fp32 recipe that the kernel
+      evaluates identically: t = e^-|g| by Cody-Waite reduction (Cody and
+      Waite, "Software Manual for the Elementary Functions", 1980) and the
+      degree-7 Taylor polynomial, q = 1 + t, s = g / q (g >= 0) or
+      (g t) / q (g < 0) with correctly rounded division, h = bf16(s u) to
+      nearest even; every step IEEE fp32, no fused multiply-add.  The
       preparation then works on h.
   R13 E8M0 scale rule as an ablation flag (MXFP4).  Besides the OCP floor
       rule of R4, the "ceil" rule e = ceil(log2(amax / 6)): eq.
@@ -781,23 +786,57 @@ def prepare_residual(x_bf16: np.ndarray, res_bf16: np.ndarray, gamma_bf16: np.nd
     return out
 
 
+#: Cody-Waite split of ln 2 (R12): C1 carries the leading 16 bits of ln 2, so
+#: k * C1 is exact for |k| < 2^8, and C2 = fl32(ln 2 - C1)
+EXP_LN2_HI = np.float32(0.693145751953125)
+EXP_LN2_LO = np.float32(1.428606765330187e-06)
+EXP_LOG2E = np.float32(1.4426950408889634)
+#: Taylor coefficients 1/j! (j = 7 .. 0) of e^r, rounded to fp32
+EXP_TAYLOR = tuple(np.float32(1.0 / math.factorial(j)) for j in range(7, -1, -1))
+
+
+def exp_nonpositive_f32(x: np.ndarray) -> np.ndarray:
+    """e^x for fp32 x <= 0 by the recipe of reading R12, every step an IEEE
+    fp32 operation rounded to nearest even (no fused multiply-add):
+    Cody-Waite argument reduction x = k ln2 + r with k = rint(fl(x log2 e))
+    and r = fl(fl(x - fl(k C1)) - fl(k C2)), the degree-7 Taylor polynomial of
+    e^r in Horner form, then the exact power of two 2^k applied by one fp32
+    multiply (which rounds into the subnormal range for k < -126).  Results
+    below 2^-149 (k < -149) are 0."""
+    x = np.asarray(x, dtype=np.float32)
+    k = np.rint((x * EXP_LOG2E).astype(np.float32)).astype(np.float32)
+    r = ((x - (k * EXP_LN2_HI).astype(np.float32)).astype(np.float32) - (k * EXP_LN2_LO).astype(np.float32))
+    r = r.astype(np.float32)
+    p = np.full(x.shape, EXP_TAYLOR[0], dtype=np.float32)
+    for c in EXP_TAYLOR[1:]:
+        p = ((p * r).astype(np.float32) + c).astype(np.float32)
+    ki = k.astype(np.int64)
+    two_k = pow2_f32(np.clip(ki, -149, 127))
+    return np.where(ki < -149, np.float32(0.0), (p * two_k).astype(np.float32)).astype(np.float32)
+
+
 def silu_mul_bf16(gate_bf16: np.ndarray, up_bf16: np.ndarray) -> np.ndarray:
-    """h = bf16(SiLU(g) * u) (reading R12): SiLU(g) = g / (1 + exp(-g)) and the
-    product in fp64, rounded once to bf16 (nearest even).  Returns bf16 bits."""
-    g = bf16_bits_to_f32(gate_bf16).astype(np.float64)
-    u = bf16_bits_to_f32(up_bf16).astype(np.float64)
+    """h = bf16(SiLU(g) * u) by the fp32 recipe of reading R12: t = e^-|g|
+    (exp_nonpositive_f32), q = fl(1 + t); s = fl(g / q) for g >= 0 and
+    s = fl(fl(g t) / q) for g < 0 (SiLU(g) = g / (1 + e^-g) = g e^g / (1 + e^g)),
+    with correctly rounded division; h = bf16(fl(s u)), nearest even.
+    Returns bf16 bits."""
+    g = bf16_bits_to_f32(gate_bf16)
+    u = bf16_bits_to_f32(up_bf16)
+    t = exp_nonpositive_f32(-np.abs(g))
+    q = (np.float32(1.0) + t).astype(np.float32)
+    num = np.where(g >= 0, g, (g * t).astype(np.float32)).astype(np.float32)
+    sv = (num / q).astype(np.float32)
     with np.errstate(over="ignore"):
-        h = g / (1.0 + np.exp(-g)) * u
-    # fp64 -> bf16, nearest even: through the exact fp64 bits
-    b = h.view(np.uint64)
-    sign = (b >> np.uint64(63)).astype(np.uint16) << np.uint16(15)
-    a = np.abs(h)
-    e = np.frexp(np.where(a > 0, a, 1.0))[1] - 1                  # floor(log2 |h|)
-    q = np.ldexp(1.0, np.maximum(e, -126) - 7)                      # bf16 spacing at |h| (subnormals: 2^-133)
-    r = np.rint(a / q) * q                                          # a / q is exact: a power-of-two scaling
-    r32 = r.astype(np.float32)                                      # exact: r is a bf16 value (or overflows to inf)
-    out = (r32.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
-    return (out | sign).astype(np.uint16)
+        h = (sv * u).astype(np.float32)
+    return bf16_round_bits(h)
+
+
+def bf16_round_bits(v: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bits, nearest with ties to even (finite inputs; overflow
+    rounds to infinity as the fp32 -> bf16 conversion does)."""
+    u = np.asarray(v, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
 
 
 def prepare_silu_mul(gate_bf16: np.ndarray, up_bf16: np.ndarray, n: int, m: int, fmt: str = "mx",

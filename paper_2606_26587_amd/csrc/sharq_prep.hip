@@ -548,19 +548,41 @@ __device__ __forceinline__ uint32_t add_bf16x2(uint32_t a, uint32_t b) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+// e^x for x <= 0 in fp32, every step an IEEE fp32 operation rounded to
+// nearest even (the file is compiled without contraction): Cody-Waite
+// argument reduction (Cody and Waite, "Software Manual for the Elementary
+// Functions", 1980) x = k ln2 + r, k = rint(x log2 e), with ln2 split into a
+// 16-bit head (k * head exact for |k| < 2^8) and an fp32 tail; the degree-7
+// Taylor polynomial of e^r in Horner form; then one multiply by the exact
+// power of two 2^k, which rounds into the subnormal range below 2^-126.
+// Results below 2^-149 are 0.  Within 2 ulp of e^x.
+__device__ __forceinline__ float exp_nonpositive(float x) {
+  const float k = __builtin_rintf(x * 0x1.715476p+0f);
+  const float r = (x - k * 0x1.62e4p-1f) - k * 0x1.7f7d1cp-20f;
+  float p = 0x1.a01a02p-13f;        // 1/7!
+  p = p * r + 0x1.6c16c2p-10f;      // 1/6!
+  p = p * r + 0x1.111112p-7f;       // 1/5!
+  p = p * r + 0x1.555556p-5f;       // 1/4!
+  p = p * r + 0x1.555556p-3f;       // 1/3!
+  p = p * r + 0.5f;
+  p = p * r + 1.0f;
+  p = p * r + 1.0f;
+  const int ki = (int)k;
+  return ki < -149 ? 0.0f : p * exp2_int(ki);
+}
+
 // SiLU(g) * u in fp32 for the down projection's input (the SiLU.mul that
 // follows the gate/up projection, fused into the preparation on the producer
-// side), with the hardware exponential (2^x) and reciprocal, ~1 ulp each.
-// For g < 0 the factor e^g is formed scaled by 2^64 and the scale removed
-// after the product, so that e^g * g * u keeps its precision where e^g alone
-// would be an fp32 subnormal (g < -87 next to a large u).  h = bf16(SiLU(g) *
-// u) then lies within one bf16 step of the exactly rounded value, and equals
-// it unless the exact value is within ~1e-5 (relative) of a rounding boundary.
+// side): t = e^-|g|, q = 1 + t, s = g / q (g >= 0) or (g t) / q (g < 0) --
+// SiLU(g) = g / (1 + e^-g) = g e^g / (1 + e^g) -- with correctly rounded
+// division, then s u.  One fixed fp32 recipe, so h = bf16(s u) is a
+// deterministic function of (g, u), within one bf16 step of the exactly
+// rounded SiLU(g) u.
 __device__ __forceinline__ float silu_mul(float g, float u) {
-  const float t = g * 1.44269504088896341f;   // g log2(e)
-  if (g >= 0.0f) return (g * u) * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-t));
-  const float es = __builtin_amdgcn_exp2f(t + 64.0f);   // e^g 2^64: a normal value for g > -131
-  return (((g * u) * es) * __builtin_amdgcn_rcpf(1.0f + es * 0x1p-64f)) * 0x1p-64f;
+  const float t = exp_nonpositive(-fabsf(g));
+  const float q = 1.0f + t;
+  const float num = g >= 0.0f ? g : g * t;
+  return (num / q) * u;
 }
 
 __device__ __forceinline__ uint32_t silu_mul_bf16x2(uint32_t g, uint32_t u) {

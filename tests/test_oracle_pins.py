@@ -586,21 +586,62 @@ def _nearest_bf16_bits(x: float) -> int:
     return best[1] | sign
 
 
-def test_silu_mul_is_the_rounded_product():
+def test_exp_recipe_within_two_ulp_of_exp():
+    """The recipe's e^x (R12: Cody-Waite reduction, degree-7 Taylor
+    polynomial, fp32 steps) against the library exponential in fp64: within
+    2 ulp of fp32 for normal results, within one subnormal step 2^-149 below
+    2^-126, exact at 0, and 0 below the subnormal range."""
+    rng = np.random.default_rng(21)
+    x = np.concatenate([-np.abs(rng.standard_normal(50000) * 30), -rng.uniform(0, 1e-3, 2000),
+                        np.linspace(-104.0, 0.0, 20001), [-0.0, -87.33654, -87.33655, -103.2789, -103.97208,
+                                                          -104.5, -150.0, -1e-30]]).astype(np.float32)
+    e = O.exp_nonpositive_f32(x).astype(np.float64)
+    ref = np.array([math.exp(float(v)) for v in x])
+    normal = ref >= 2.0 ** -126
+    ulp = np.spacing(ref[normal].astype(np.float32)).astype(np.float64)
+    assert np.all(np.abs(e[normal] - ref[normal]) <= 2 * ulp)
+    assert np.all(np.abs(e[~normal] - ref[~normal]) <= 2.0 ** -149)
+    assert float(O.exp_nonpositive_f32(np.float32(0.0))) == 1.0
+    assert float(O.exp_nonpositive_f32(np.float32(-150.0))) == 0.0
+
+
+def test_bf16_rounding_is_nearest_even():
+    rng = np.random.default_rng(22)
+    v = np.concatenate([rng.standard_normal(3000) * 10.0 ** rng.integers(-38, 38, 3000),
+                        [1e-40, -3e-39, 1.00390625, 1.01171875, -2.0 ** -133]]).astype(np.float32)
+    got = O.bf16_round_bits(v)
+    for x, b in zip(v, got):
+        assert int(b) == _nearest_bf16_bits(float(x)), (float(x), hex(int(b)))
+
+
+def test_silu_mul_within_one_step_of_the_exact_product():
+    """h of the fp32 recipe against bf16 of the exact SiLU(g) u: at most one
+    bf16 step apart everywhere (the recipe's relative error is a few fp32 ulp,
+    far below bf16's half step), and equal for almost every element; the signs
+    and zeros of the special values follow the exact product."""
     rng = np.random.default_rng(12)
-    g = rng.standard_normal(300).astype(np.float32) * 4
-    u = rng.standard_normal(300).astype(np.float32) * 3
+    g = rng.standard_normal(3000).astype(np.float32) * 4
+    u = rng.standard_normal(3000).astype(np.float32) * 3
     g[:8] = [0.0, -0.0, 100.0, -100.0, -88.7, 88.7, 1e-30, -1e-30]
     u[:8] = [1.5, 2.0, -1.0, 3.0, 1.0, -2.0, 5.0, -5.0]
     gb, ub = synth.f32_to_bf16_bits(g), synth.f32_to_bf16_bits(u)
     h = O.silu_mul_bf16(gb[None], ub[None])[0]
     gf, uf = O.bf16_bits_to_f32(gb), O.bf16_bits_to_f32(ub)
-    for i in range(300):
+
+    def ordinal(b):
+        return -(b & 0x7FFF) if b & 0x8000 else b & 0x7FFF
+
+    off = 0
+    for i in range(3000):
         gi, ui = float(gf[i]), float(uf[i])
         sig = 1.0 / (1.0 + math.exp(-gi)) if gi > -700 else 0.0
         want = _nearest_bf16_bits(math.copysign(abs(gi * sig * ui), gi * ui) if gi * ui != 0 else
                                   (gi * 0.5) * ui)
-        assert int(h[i]) == want, (i, gi, ui, hex(int(h[i])), hex(want))
+        d = abs(ordinal(int(h[i])) - ordinal(want))
+        assert d <= 1, (i, gi, ui, hex(int(h[i])), hex(want))
+        off += d
+    assert off <= 15, off   # a few elements within ~1e-6 of a rounding boundary
+    assert [hex(int(v)) for v in h[:2]] == ["0x0", "0x8000"]
 
 
 def test_prepare_silu_mul_is_prepare_of_h():
