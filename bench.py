@@ -143,7 +143,7 @@ def cpu_model():
     return platform.processor() or None
 
 
-def cpu_baseline(rows=256):
+def cpu_baseline(rows=768):
     """The CPU oracles on a bounded sample of the same step: `rows` of the 2048
     token rows of each Llama linear (preparation + two-path fp64 GEMM; the
     weights are quantized beforehand, untimed, as on the GPU).  The plain C
@@ -448,21 +448,42 @@ def llama_prefill(args, torch, S, synth, dev, stream):
 
 
 def llama_decode(args, torch, S, synth, dev, stream):
+    """Decode: the three Llama linears at M = 1 ... 256 tokens, weight copies
+    rotated past the last-level cache.  Each M is timed twice: the
+    preparation and the GEMM as two launches, and through
+    sharq_prepare_linear, which runs both in one kernel for a few rows."""
     outs = []
-    for T in (1, 16, 64, 256):
+    for T in (1, 2, 4, 16, 64, 256):
         layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T, "mx", 2, 4, 1, w_sets=DECODE_W_SETS)
         step = dense_step(S, layers, stream, synth.LLAMA_EPS, 2, 4, "mx", 1)
         ms_step, wall_ms, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
         per = per_linear(layers, tm, T, "mx", 2, 4)
+
+        def fused_step(i, mark):
+            for li, L in enumerate(layers):
+                if mark:
+                    mark(li)
+                S.sharq_prepare_linear(L["xs"][0], L["g"], L["w"][i % len(L["w"])], synth.LLAMA_EPS, 2, 4, "mx",
+                                       act=L["acts"][0], out=L["ys"][0], stream=stream)
+            if mark:
+                mark(len(layers))
+
+        ms_fused, _, tf = run_steps(torch, stream, fused_step, len(layers), args.steps, args.warmup)
+        for li, p in enumerate(per):
+            p["prepare_linear_us"] = tf.op_ms(li) * 1e3
+            p["separate_us"] = p["prep_us"] + p["gemm_us"]
         wb = sum(p["weight_bytes"] for p in per)
         t_gemm = sum(p["gemm_us"] for p in per) * 1e-6
+        log(f"[bench] decode M={T}: separate {ms_step * 1e3:.1f} us/step, one call {ms_fused * 1e3:.1f} us/step; "
+            + ", ".join(f"{p['linear']} {p['separate_us']:.1f} -> {p['prepare_linear_us']:.1f}" for p in per))
         out = base_record(args, "SharQ decode linears weight-stream GB/s (prep+GEMM), Llama-8B",
                           wb / (ms_step * 1e-3) / 1e9, "GB/s", ms_step, "mxfp4",
                           {"workload": f"Llama-3.1-8B decode linears qkv, gate_up, down; M={T}; 2:4; MXFP4",
                            "tokens": T})
-        out["roofline"] = {"bound": "hbm", "kernel": "k_linear_mx", "achieved": wb / t_gemm / 1e9,
-                           "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": wb / t_gemm / 1e9 / PEAK_HBM_GBPS,
-                           "traffic": None}
+        out["roofline"] = {"bound": "hbm", "kernel": "k_linear_mx_skinny / k_linear_mx_persist",
+                           "achieved": wb / t_gemm / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                           "frac": wb / t_gemm / 1e9 / PEAK_HBM_GBPS, "traffic": None}
+        out["prepare_linear_ms_per_step"] = ms_fused
         out["per_linear"] = per
         outs.append(out)
         del layers
@@ -749,7 +770,7 @@ def main():
                     help="prefill: how the preparation stores the backbone for the GEMM -- the dense copy alone "
                          "(default), the dense copy beside the compressed form, or the compressed form only "
                          "(the GEMM then expands it)")
-    ap.add_argument("--cpu-rows", type=int, default=256)
+    ap.add_argument("--cpu-rows", type=int, default=768)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
     args = ap.parse_args()
     if args.gpus != 1:

@@ -354,6 +354,23 @@ SHARQ_API sharq_status sharq_linear(const sharq_act *a, const sharq_weight *w, v
                           int64_t ldy, void *stream);
 
 /*
+ * Preparation and two-path output in one call (Sec. 4.3: the fused
+ * preparation, the shared weight and the accumulating residual path keep the
+ * data flow close to a single linear kernel; Sec. 3.4; Sec. 3.3 eq.
+ * "sharq-output"): exactly sharq_prepare(X ..., act) followed by
+ * sharq_linear(act, w, Y ...), with every argument of both validated before
+ * anything is launched.  For a few rows (decode: MXFP4, the method's path
+ * combination, K a multiple of 128 up to 16384, M <= 4 when the prepared rows
+ * fit in LDS) it runs as ONE kernel: each workgroup of the small-M GEMM
+ * prepares the rows in its prologue and workgroup 0 writes them to `act`;
+ * the outputs (act's buffers and Y) are bit-identical to the two calls.
+ */
+SHARQ_API sharq_status sharq_prepare_linear(const void *X, sharq_dtype xdt, int64_t M, int64_t K, int64_t ldx,
+                                            const void *gamma, float eps, sharq_pattern nm, sharq_format fmt,
+                                            const float *tensor_scale_in, sharq_act *act, const sharq_weight *w,
+                                            void *Y, sharq_dtype ydt, int64_t ldy, void *stream);
+
+/*
  * Grouped form for mixture-of-experts layers (the MoE configuration of the
  * paper's evaluation, Sec. 4.1-4.2, Qwen3-30B-A3B): the two-path output of
  * Sec. 3.3 eq. "sharq-output" applied per expert to the rows routed to it.

@@ -40,6 +40,11 @@ hipError_t launch_prep_silu(const uint16_t* gate, const uint16_t* up, uint16_t* 
                             int64_t ldu, int64_t ldh, int pat, bool nv, const float* ts_in, float* ts_out,
                             uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns, uint8_t* spd,
                             PrepExtras ex, hipStream_t st);
+bool fused_prep_linear_applies(int64_t M, int K, int N);
+hipError_t launch_prep_linear_fused(const uint16_t* X, int M, int K, int64_t ldx, const uint16_t* gamma, float eps,
+                                    int pat, uint8_t* spc, uint8_t* spm, uint8_t* sps, uint8_t* dnc, uint8_t* dns,
+                                    uint8_t* spd, PrepExtras ex, const uint8_t* wc, const uint8_t* ws, int N, int ydt,
+                                    void* Y, int64_t ldy, hipStream_t st);
 hipError_t launch_linear_mx_grouped(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                                     const uint8_t* dnc, const uint8_t* dns, const int32_t* ridx, int64_t act_rows,
                                     const int32_t* offs, int E, int64_t total, const uint8_t* wc, const uint8_t* ws,
@@ -232,10 +237,11 @@ namespace {
 // required); 2, SiLU.mul (X = gate, res = up, h_out optional, no gamma).
 constexpr int kSrcPlain = 0, kSrcResidual = 1, kSrcSilu = 2;
 
+// check_only: validate the arguments and return before any launch.
 sharq_status prepare_impl(int src, const void* X, const void* res, void* h_out, sharq_dtype xdt, int64_t M,
                           int64_t K, int64_t ldx, int64_t ldr, int64_t ldh, const void* gamma, float eps,
                           sharq_pattern nm, sharq_format fmt, const float* tensor_scale_in, sharq_act* out,
-                          void* stream) {
+                          void* stream, bool check_only = false) {
   if (!out) return SHARQ_EINVAL;
   if (M < 0 || M > INT_MAX || K <= 0 || K % 32 != 0 || K > kMaxK || ldx < K) return SHARQ_EINVAL;
   if (!X && M > 0) return SHARQ_EINVAL;
@@ -259,7 +265,7 @@ sharq_status prepare_impl(int src, const void* X, const void* res, void* h_out, 
     return SHARQ_EALIGN;
   if (res && out->mode != SHARQ_MODE_SHARQ) return SHARQ_EUNSUPPORTED;
   if (res && fmt == SHARQ_HIF4) return SHARQ_EUNSUPPORTED;
-  if (M == 0) return SHARQ_OK;
+  if (M == 0 || check_only) return SHARQ_OK;
   const sharq::PrepExtras ex{rule_bias(out->scale_rule), reinterpret_cast<uint32_t*>(out->dbg_mask), out->dbg_r};
   if (src == kSrcSilu)
     return hip_status(sharq::launch_prep_silu(static_cast<const uint16_t*>(X), static_cast<const uint16_t*>(res),
@@ -319,8 +325,11 @@ sharq_status sharq_prepare_silu_mul(const void* gate, const void* up, void* h_ou
                       out, stream);
 }
 
-sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sharq_dtype ydt, int64_t ldy,
-                          void* stream) {
+}  // extern "C"
+
+namespace {
+
+sharq_status check_linear(const sharq_act* a, const sharq_weight* w, const void* Y, sharq_dtype ydt, int64_t ldy) {
   sharq_status s = check_act(a);
   if (s != SHARQ_OK) return s;
   if (!Y && a->rows > 0) return SHARQ_EINVAL;
@@ -330,6 +339,17 @@ sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sh
   if (!ydt_ok(ydt)) return SHARQ_EUNSUPPORTED;
   if (ldy < w->N) return SHARQ_EINVAL;
   if (!aligned(Y, ysize(ydt))) return SHARQ_EALIGN;
+  return SHARQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sharq_dtype ydt, int64_t ldy,
+                          void* stream) {
+  const sharq_status s = check_linear(a, w, Y, ydt, ldy);
+  if (s != SHARQ_OK) return s;
   if (a->rows == 0 || w->N == 0) return SHARQ_OK;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   if (a->fmt == SHARQ_HIF4)
@@ -351,6 +371,36 @@ sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sh
   return hip_status(sharq::launch_linear_mx(gemm_pattern(pattern_id(a->nm)), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale,
                                             a->dn_codes, a->dn_scale, a->rows, w->codes, w->scale, (int)w->N,
                                             (int)w->K, Y, ldy, a->sp_dense, st));
+}
+
+sharq_status sharq_prepare_linear(const void* X, sharq_dtype xdt, int64_t M, int64_t K, int64_t ldx, const void* gamma,
+                                  float eps, sharq_pattern nm, sharq_format fmt, const float* tensor_scale_in,
+                                  sharq_act* act, const sharq_weight* w, void* Y, sharq_dtype ydt, int64_t ldy,
+                                  void* stream) {
+  // every argument of both steps is validated before anything is launched
+  sharq_status s = prepare_impl(kSrcPlain, X, nullptr, nullptr, xdt, M, K, ldx, K, K, gamma, eps, nm, fmt,
+                                tensor_scale_in, act, stream, true);
+  if (s != SHARQ_OK) return s;
+  s = check_linear(act, w, Y, ydt, ldy);
+  if (s != SHARQ_OK) return s;
+  if (M == 0 || w->N == 0) {
+    if (M == 0) return SHARQ_OK;
+    return prepare_impl(kSrcPlain, X, nullptr, nullptr, xdt, M, K, ldx, K, K, gamma, eps, nm, fmt, tensor_scale_in,
+                        act, stream);
+  }
+  const int pid = pattern_id(nm);
+  if (fmt == SHARQ_MXFP4 && act->mode == SHARQ_MODE_SHARQ && pid > 0 &&
+      sharq::fused_prep_linear_applies(M, (int)K, (int)w->N)) {
+    const sharq::PrepExtras ex{rule_bias(act->scale_rule), reinterpret_cast<uint32_t*>(act->dbg_mask), act->dbg_r};
+    return hip_status(sharq::launch_prep_linear_fused(
+        static_cast<const uint16_t*>(X), (int)M, (int)K, ldx, static_cast<const uint16_t*>(gamma), eps, pid,
+        act->sp_codes, act->sp_meta, act->sp_scale, act->dn_codes, act->dn_scale, act->sp_dense, ex, w->codes,
+        w->scale, (int)w->N, (int)ydt, Y, ldy, reinterpret_cast<hipStream_t>(stream)));
+  }
+  s = prepare_impl(kSrcPlain, X, nullptr, nullptr, xdt, M, K, ldx, K, K, gamma, eps, nm, fmt, tensor_scale_in, act,
+                   stream);
+  if (s != SHARQ_OK) return s;
+  return sharq_linear(act, w, Y, ydt, ldy, stream);
 }
 
 sharq_status sharq_linear_grouped(const sharq_act* a, const int32_t* row_index, const int32_t* expert_offsets,

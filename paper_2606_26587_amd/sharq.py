@@ -82,6 +82,10 @@ def _load():
     L.sharq_linear.restype = ctypes.c_int
     L.sharq_linear.argtypes = [ctypes.POINTER(ActStruct), ctypes.POINTER(WeightStruct), c_vp, ctypes.c_int, c_i64,
                                c_vp]
+    L.sharq_prepare_linear.restype = ctypes.c_int
+    L.sharq_prepare_linear.argtypes = [c_vp, ctypes.c_int, c_i64, c_i64, c_i64, c_vp, c_f, Pattern, ctypes.c_int, c_vp,
+                                       ctypes.POINTER(ActStruct), ctypes.POINTER(WeightStruct), c_vp, ctypes.c_int,
+                                       c_i64, c_vp]
     L.sharq_linear_grouped.restype = ctypes.c_int
     L.sharq_linear_grouped.argtypes = [ctypes.POINTER(ActStruct), c_vp, c_vp, c_i64, ctypes.POINTER(WeightStruct),
                                        c_vp, ctypes.c_int, c_i64, c_vp]
@@ -282,6 +286,26 @@ def sharq_linear(a: PreparedAct, w: QuantWeight, out: Optional[torch.Tensor] = N
     _check(lib.sharq_linear(ctypes.byref(ast), ctypes.byref(wst), _ptr(out), _DT.get(out.dtype, -1),
                             out.stride(0) if out.dim() == 2 else w.N, _stream(stream)), "sharq_linear")
     return out
+
+
+def sharq_prepare_linear(x: torch.Tensor, gamma: Optional[torch.Tensor], w: QuantWeight, eps: float = 1e-6, n: int = 2,
+                         m: int = 4, fmt="mx", act: Optional[PreparedAct] = None, out: Optional[torch.Tensor] = None,
+                         dtype=torch.bfloat16, tensor_scale_in: Optional[torch.Tensor] = None, stream=None,
+                         pairs: bool = False, scale_rule="floor"):
+    """Preparation of X [M, K] into `act` and Y = SharQ(act, w) in one call
+    (one kernel for a few rows).  Returns (prepared activation, Y)."""
+    M, K = x.shape
+    if act is None:
+        act = alloc_act(M, K, n, m, fmt, x.device, pairs, scale_rule=scale_rule)
+    if out is None:
+        out = torch.empty((M, w.N), dtype=dtype, device=x.device)
+    f = _FMT[fmt] if isinstance(fmt, str) else fmt
+    ast, wst = act.struct(), w.struct()
+    _check(lib.sharq_prepare_linear(_ptr(x), _DT.get(x.dtype, -1), M, K, x.stride(0), _ptr(gamma), ctypes.c_float(eps),
+                                    Pattern(n, m, int(pairs)), f, _ptr(tensor_scale_in), ctypes.byref(ast),
+                                    ctypes.byref(wst), _ptr(out), _DT.get(out.dtype, -1),
+                                    out.stride(0) if out.dim() == 2 else w.N, _stream(stream)), "sharq_prepare_linear")
+    return act, out
 
 
 def sharq_linear_grouped(a: PreparedAct, row_index: Optional[torch.Tensor], expert_offsets: torch.Tensor, total: int,
