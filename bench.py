@@ -14,7 +14,11 @@ n/m-sparse backbone GEMM -- prep time included; the executed work F_exec =
 anyway, and the plain linear's F_lin = 2 M N K beside it), the roofline of the
 dominant kernel (the two-path GEMM, against the dense MXFP4 MFMA peak), the
 preparation kernel's HBM rate on its algorithmic bytes, and the CPU oracle
-timed on a bounded sample.  Per-kernel times come from HIP events on the
+timed on a bounded sample.  Beside the published MFMA peak the roofline also
+reports the sustained FP4 MFMA rate this device reaches right after the timed
+steps (libsharq_probe.so: back-to-back MFMAs on every SIMD, with the shader
+clock it ran at): under such load the part runs well below its rated clock.
+Per-kernel times come from HIP events on the
 launch stream around every launch of the timed steps (the warmup steps carry
 the same events, so a profiler's per-kernel mean over the run covers the
 same regime).
@@ -384,6 +388,43 @@ def copy_same_bytes(torch, dev, stream, nbytes, reps=20):
     return us
 
 
+PROBE_ITERS = 2500               # ~1.7 ms of back-to-back MFMAs per probe launch
+
+
+def mfma_probe(torch, dev, stream, iters=PROBE_ITERS, reps=3):
+    """The sustained scaled-FP4 MFMA rate of this device (libsharq_probe.so:
+    four wavefronts per CU issuing independent 32x32x64 FP4 MFMAs), and the
+    shader clock the probe ran at (shader-clock cycles over 100 MHz real-time
+    ticks, averaged over the workgroups of the last launch).  This is the
+    executed-work ceiling of the two-path GEMM on the part as it runs under
+    that load, beside the published peak at the rated clock."""
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2606_26587_amd", "libsharq_probe.so"))
+    lib.sharq_probe_mfma_fp4.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_void_p]
+    lib.sharq_probe_mfma_fp4.restype = ctypes.c_int
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    sink = torch.empty(cus * 256, dtype=torch.float32, device=dev)
+    clk = torch.zeros(cus * 2, dtype=torch.int64, device=dev)
+    ev = [HipEvent() for _ in range(reps + 2)]
+    for i in range(reps + 1):   # launch 0 warms up
+        ev[i].record(stream)
+        rc = lib.sharq_probe_mfma_fp4(iters, cus, sink.data_ptr(), clk.data_ptr(), stream.cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"sharq_probe_mfma_fp4 failed: {rc}")
+    ev[reps + 1].record(stream)
+    torch.cuda.synchronize()
+    us = sorted(ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(1, reps + 1))
+    c = clk.view(cus, 2).cpu().numpy().astype(np.float64)
+    flops = cus * 4 * iters * 32 * 2.0 * 32 * 32 * 64
+    med = us[len(us) // 2]
+    return {"kernel": "sharq_probe_mfma_fp4: back-to-back v_mfma_scale_f32_32x32x64_f8f6f4 (E2M1), "
+                      "4 wavefronts x 8 accumulators per CU",
+            "achieved": flops / (med * 1e-6) / 1e12, "unit": "TFLOP/s",
+            "frac_of_peak": flops / (med * 1e-6) / 1e12 / PEAK_FP4_TFLOPS,
+            "clock_GHz": float(c[:, 0].sum() / c[:, 1].sum() * 0.1), "launch_us": us,
+            "flops_per_launch": flops}
+
+
 def llama_prefill(args, torch, S, synth, dev, stream):
     backbone = args.backbone
     layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T_TOKENS, "mx", 2, 4, N_INPUT_SETS,
@@ -439,6 +480,13 @@ def llama_prefill(args, torch, S, synth, dev, stream):
     copy_gbps = bytes_prep / (sum(copy_us) * 1e-6) / 1e9
     out["prep"]["copy_same_bytes"] = {"achieved": copy_gbps, "unit": "GB/s", "frac": copy_gbps / PEAK_HBM_GBPS,
                                       "prep_vs_copy": prep_gbps / copy_gbps}
+    # the sustained FP4 MFMA rate of this device, measured after the timed steps
+    sus = mfma_probe(torch, dev, stream)
+    out["roofline"]["sustained_mfma"] = sus
+    out["roofline"]["frac_exec_of_sustained"] = f_exec / t_gemm / 1e12 / sus["achieved"]
+    out["roofline"]["frac_alg_of_sustained"] = gemm_tf / sus["achieved"]
+    log(f"[bench] FP4 MFMA probe: {sus['achieved']:.0f} TFLOP/s sustained at {sus['clock_GHz']:.2f} GHz; "
+        f"GEMM executed work at {f_exec / t_gemm / 1e12 / sus['achieved']:.2f} of it")
     log(f"[bench] prep {prep_gbps:.0f} GB/s algorithmic ({bytes_moved / t_prep / 1e9:.0f} GB/s moved); "
         f"a device copy of the same bytes {copy_gbps:.0f} GB/s; GEMM {gemm_tf:.0f} TFLOP/s alg, "
         f"{f_exec / t_gemm / 1e12:.0f} exec")

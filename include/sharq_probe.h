@@ -1,0 +1,42 @@
+/*
+ * sharq_probe.h -- a measurement aid, not part of the SharQ method.
+ *
+ * libsharq_probe.so runs back-to-back scaled FP4 MFMAs
+ * (v_mfma_scale_f32_32x32x64_f8f6f4, E2M1 operands, unit E8M0 scales) on
+ * every SIMD of the device and records the shader clock.  The rate it reaches
+ * is the sustained matrix-core ceiling that bounds the two-path FP4 GEMM
+ * (whose backbone and residual products both run on this instruction): under
+ * such load the part runs below its rated clock, so this ceiling sits below
+ * the published dense FP4 peak.  The benchmark reports the GEMM's rate against
+ * both.  Callers: the benchmark and its tests.
+ */
+#ifndef SHARQ_PROBE_H
+#define SHARQ_PROBE_H
+
+#include <hip/hip_runtime.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * Launch one workgroup of four wavefronts (one per SIMD) on each of
+ * `workgroups` compute units (pass the device's CU count); every wavefront
+ * issues iters x 32 independent FP4 MFMAs (8 accumulators, operand registers
+ * cycled through four sets of pseudo-random E2M1 codes), then writes one float
+ * per lane to `sink` (device, workgroups x 256 floats, contents meaningless)
+ * and, from lane 0 of wavefront 0, two counters to `clk` (device,
+ * workgroups x 2 uint64): shader-clock cycles and 100 MHz real-time ticks
+ * between the first and the last MFMA.  Total work: workgroups x 4 x iters x 32
+ * MFMAs of 2 x 32 x 32 x 64 flops.  Asynchronous on `stream`; time it with
+ * events on that stream.
+ * Returns hipSuccess, hipErrorInvalidValue (iters < 1, workgroups < 1, a NULL
+ * pointer) or the launch error.
+ */
+int sharq_probe_mfma_fp4(int iters, int workgroups, float* sink, unsigned long long* clk, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

@@ -382,3 +382,23 @@ def test_scale_rule_debug_and_dense_only_rejections(L):
     assert L.sharq_quantize_weight(FAKE, 0, 64, 128, 128, ctypes.byref(w), None) == EUNSUPPORTED
     w = Weight(64, 128, 1, 0, FAKE, FAKE, FAKE, None, 7)
     assert L.sharq_quantize_weight(FAKE, 0, 64, 128, 128, ctypes.byref(w), None) == EINVAL
+
+
+PROBE_LIB = os.path.join(ROOT, "paper_2606_26587_amd", "libsharq_probe.so")
+PROBE_HEADER = os.path.join(ROOT, "include", "sharq_probe.h")
+
+
+@pytest.mark.skipif(not os.path.exists(PROBE_LIB), reason="libsharq_probe.so not built")
+def test_probe_library_exports_and_rejects():
+    """The benchmark's MFMA-rate probe library exports what its header
+    declares and rejects bad arguments before any launch."""
+    names = re.findall(r"\bint\s+(sharq_probe_\w+)\s*\(", open(PROBE_HEADER).read())
+    assert names == ["sharq_probe_mfma_fp4"]
+    P = ctypes.CDLL(PROBE_LIB)
+    for n in names:
+        assert hasattr(P, n), n
+    P.sharq_probe_mfma_fp4.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    fake = 1 << 20   # never dereferenced
+    hip_invalid_value = 1
+    for iters, wgs, sink, clk in [(0, 1, fake, fake), (1, 0, fake, fake), (1, 1, None, fake), (1, 1, fake, None)]:
+        assert P.sharq_probe_mfma_fp4(iters, wgs, sink, clk, None) == hip_invalid_value
