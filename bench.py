@@ -43,6 +43,10 @@ Other workloads (--workload), one JSON line each:
 kernel for scaling the profiler's HBM byte counters) and nothing else.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--workload NAME] [--no-cpu-baseline]
+
+The default warmup is 200 steps (about 0.1 s of the default workload): over
+the first ~50 steps after start-up the step time falls by ~12% as the part
+ramps its clocks, and the timed steps measure the steady state after it.
 """
 
 from __future__ import annotations
@@ -286,6 +290,9 @@ def run_steps(torch, stream, step, n_ops, steps, warmup):
     for i in range(warmup):
         step(i, lambda k, i=i: tw.mark(i, k))
     torch.cuda.synchronize()
+    # step times over the warmup, in tenths: the part reaches its steady
+    # clocks only after tens of milliseconds of load
+    ramp = [tw.ev[i][0].elapsed_time(tw.ev[i][n_ops]) for i in range(warmup)]
     tm = Timer(torch, stream, n_ops, steps)
     t0, t1 = HipEvent(), HipEvent()
     torch.cuda.synchronize()
@@ -296,6 +303,7 @@ def run_steps(torch, stream, step, n_ops, steps, warmup):
     t1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
+    tm.warmup_ramp_ms = [float(np.mean(c)) for c in np.array_split(np.array(ramp), min(10, len(ramp))) if len(c)]
     return t0.elapsed_time(t1) / steps, wall * 1e3 / steps, tm
 
 
@@ -492,6 +500,8 @@ def llama_prefill(args, torch, S, synth, dev, stream):
         f"{f_exec / t_gemm / 1e12:.0f} exec")
     out["per_linear"] = per
     out["wall_ms_per_step"] = wall_ms
+    out["warmup_ramp_ms"] = tm.warmup_ramp_ms
+    log("[bench] step time over the warmup, by tenths (ms): " + " ".join(f"{v:.3f}" for v in tm.warmup_ramp_ms))
     return out
 
 
@@ -809,7 +819,9 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=200,
+                    help="untimed steps first: the part needs tens of milliseconds of load to reach its steady "
+                         "clocks (the step time over the warmup is reported by tenths)")
     ap.add_argument("--workload", default="llama-prefill",
                     choices=["llama-prefill", "llama-decode", "qwen-nvfp4", "llama-nvfp4-pairs", "moe",
                              "ablation", "llama-fused"])
