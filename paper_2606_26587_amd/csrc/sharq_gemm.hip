@@ -137,9 +137,10 @@ __device__ __forceinline__ void load_w(WStep<NF>& w, const uint8_t* wc, const ui
                  : make_uint4(0u, 0u, 0u, 0u);
   }
   // one scale dword per weight row (threads 0 .. BN-1).  Threads past BN
-  // reread row BN-1 and keep 0: no branch, which keeps the interleaved
-  // K step one basic block (the compiler would otherwise move its MFMAs
-  // out of their slots)
+  // reread row BN-1 and never store it: no branch, which keeps the
+  // interleaved K step one basic block (the compiler would otherwise move its
+  // MFMAs out of their slots), and no select on the loaded value, which
+  // would make the thread wait for the load where it is issued
   const int n = min(n0 + (BN >= 256 ? tid : min(tid, BN - 1)), N - 1);
   const uint8_t* sr = ws + pn * 4 + (int64_t)n * (wp / 32);
   uint32_t sv = 0u;
@@ -149,7 +150,7 @@ __device__ __forceinline__ void load_w(WStep<NF>& w, const uint8_t* wc, const ui
 #pragma unroll
     for (int j = 0; j < 4; ++j) sv |= (uint32_t)(4 * ks + j < nblk ? sr[j] : 127u) << (8 * j);
   }
-  w.s = (BN >= 256 || tid < BN) ? sv : 0u;
+  w.s = sv;
 }
 
 // Weight scales in LDS are laid out per (column, lane half): lane (col, h)
@@ -629,9 +630,9 @@ __device__ __forceinline__ void step5h(v16f (&acc)[4], const AOps& ops, uint4 (&
   SHARQ_FENCE();
   mma_dn<0, 2>(acc, ops, b0, bw); put_piece<PAT, 6>(opsn, raw, sel);
   {
-    // threads 128-255 hold no scales (wst.s = 0) and write bytes 8-15 of the
-    // records, which a half tile never reads: no branch, so the step stays
-    // one basic block and the compiler keeps every MFMA in its slot
+    // threads 128-255 hold a copy of column 127's scales and write bytes 8-15
+    // of the records, which a half tile never reads: no branch, so the step
+    // stays one basic block and the compiler keeps every MFMA in its slot
     const int f = tid >> 5, c = tid & 31;
     *reinterpret_cast<uint16_t*>(wr + kStageW + (2 * c + 0) * 16 + 2 * f) = (uint16_t)wst.s;
     *reinterpret_cast<uint16_t*>(wr + kStageW + (2 * c + 1) * 16 + 2 * f) = (uint16_t)(wst.s >> 16);
@@ -730,9 +731,14 @@ __device__ __forceinline__ void load_w_part(WStep<NF>& w, const uint8_t* wc, con
       w.q[j] = *reinterpret_cast<const uint4*>(wc + pn * 64 + (int64_t)n * 64 + 16 * part);
     }
   } else {
+    // In a half tile threads BN..255 load column BN - 1's scales again: their
+    // copy lands in record bytes that a half tile never reads.  Selecting 0
+    // for them instead would make the value depend on the load at issue time,
+    // and the wait for it (the newest load) drained every load in flight once
+    // per step: 57.5 -> 53.5 us on the Llama qkv shape, whose last round runs
+    // as half tiles.
     const int n = min(n0 + (BN >= 256 ? tid : min(tid, BN - 1)), N - 1);
-    const uint32_t sv = *reinterpret_cast<const uint32_t*>(ws + pn * 4 + (int64_t)n * 4);
-    w.s = (BN >= 256 || tid < BN) ? sv : 0u;
+    w.s = *reinterpret_cast<const uint32_t*>(ws + pn * 4 + (int64_t)n * 4);
   }
 }
 
