@@ -459,6 +459,77 @@ def test_moe_full_config(S, G):
         gemm_check(yh[lo:hi], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), f"moe expert {e}")
 
 
+def test_moe_bench_layout(S, G):
+    """Both Qwen3-30B-A3B expert GEMMs as the benchmark launches them: each
+    input prepared with the dense backbone copy alone (4:8), the grouped GEMM
+    reading it.  gate/up: 4096 tokens x 2048 with RMSNorm, rows gathered by the
+    router; down: the 32768 expert-sorted rows x 768, no norm, identity row
+    map.  Prepared bytes against the oracle (all rows for gate/up; the rows of
+    the checked experts for down -- the preparation is row-wise), the bf16
+    output equal to the fp32 one rounded, and the slices of four experts (all
+    their rows, all columns) against the oracle."""
+    cfg = synth.MOE
+    T, H, E, I, k = cfg["tokens"], cfg["hidden"], cfg["experts"], cfg["inter"], cfg["topk"]
+    ridx, offs = synth.router_topk(T, E, k, seed=0)
+    total = int(offs[-1])
+    ri, of = torch.from_numpy(ridx).cuda(), torch.from_numpy(offs).cuda()
+    experts = (0, 1, 63, 127)
+
+    def quantized_experts(N, K, seed0):
+        return S.stack_weights([S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=seed0 + e)))
+                                for e in range(E)])
+
+    # gate/up input: RMSNorm, dense backbone copy alone
+    say(f"[moe-bench] gate_up T={T} K={H} N={2 * I}")
+    x, g = synth.activations(T, H, seed=0), synth.gamma(H, seed=0)
+    a1 = S.sharq_prepare(G.dev_bf16(x), G.dev_bf16(g), 1e-6, 4, 8, "mx",
+                         out=S.alloc_act(T, H, 4, 8, "mx", "cuda", dense_only=True))
+    w1 = quantized_experts(2 * I, H, 100)
+    y1 = S.sharq_linear_grouped(a1, ri, of, total, w1, dtype=torch.float32)
+    y1b = S.sharq_linear_grouped(a1, ri, of, total, w1, dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert a1.sp_codes is None and a1.sp_meta is None
+    o1 = O.prepare(x, g, 1e-6, 4, 8, "mx")
+    dev1 = L.act_to_device_layout(o1)
+    G.assert_bytes_equal("moe gate_up sp_dense", G.host(a1.sp_dense), L.dense_backbone_to_device_layout(o1))
+    for name in ("sp_scale", "dn_codes", "dn_scale"):
+        G.assert_bytes_equal(f"moe gate_up {name}", G.host(getattr(a1, name)), dev1[name])
+    assert torch.equal(y1b, y1.to(torch.bfloat16))
+    yh = G.host(y1)
+    for e in experts:
+        lo, hi = int(offs[e]), int(offs[e + 1])
+        wo = O.quantize_weight(synth.weight(2 * I, H, seed=100 + e), "mx")
+        rows = ridx[lo:hi]
+        gemm_check(yh[lo:hi], O.linear(o1, wo, rows=rows), O.linear_abs(o1, wo, rows=rows), f"moe gate_up e{e}")
+    del w1, y1, y1b
+
+    # down input: expert-sorted rows, no norm, identity row map
+    say(f"[moe-bench] down T={total} K={I} N={H}")
+    h = synth.activations(total, I, seed=1)
+    a2 = S.sharq_prepare(G.dev_bf16(h), None, 1e-6, 4, 8, "mx",
+                         out=S.alloc_act(total, I, 4, 8, "mx", "cuda", dense_only=True))
+    w2 = quantized_experts(H, I, 1000)
+    y2 = S.sharq_linear_grouped(a2, None, of, total, w2, dtype=torch.float32)
+    y2b = S.sharq_linear_grouped(a2, None, of, total, w2, dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert torch.equal(y2b, y2.to(torch.bfloat16))
+    chk = np.concatenate([np.arange(offs[e], offs[e + 1]) for e in experts])
+    o2 = O.prepare(h[chk], None, 1e-6, 4, 8, "mx")
+    G.assert_bytes_equal("moe down sp_dense", L.from_panels(G.host(a2.sp_dense), total, I, I // 2)[chk],
+                         L.dense_backbone_rowmajor(o2))
+    for name, width in (("sp_scale", I // 32), ("dn_codes", I // 2), ("dn_scale", I // 32)):
+        G.assert_bytes_equal(f"moe down {name}", L.from_panels(G.host(getattr(a2, name)), total, I, width)[chk],
+                             o2[name])
+    yh = G.host(y2)
+    start = 0
+    for e in experts:
+        lo, hi = int(offs[e]), int(offs[e + 1])
+        wo = O.quantize_weight(synth.weight(H, I, seed=1000 + e), "mx")
+        rows = np.arange(start, start + hi - lo)
+        start += hi - lo
+        gemm_check(yh[lo:hi], O.linear(o2, wo, rows=rows), O.linear_abs(o2, wo, rows=rows), f"moe down e{e}")
+
+
 # --------------------------------------------------------------------------- persistent kernel tail
 
 @pytest.mark.parametrize("T,N,K,n,m", [(12750, 704, 256, 2, 4),    # 300 tiles: 44 in the last round
