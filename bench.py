@@ -280,6 +280,13 @@ class Timer:
         return float(np.mean([e[i].elapsed_time(e[i + 1]) for e in self.ev]))
 
 
+def tenths(values):
+    """Means of `values` over (up to) ten consecutive, nearly equal parts."""
+    if not values:
+        return []
+    return [float(np.mean(c)) for c in np.array_split(np.asarray(values, dtype=np.float64), min(10, len(values)))]
+
+
 def run_steps(torch, stream, step, n_ops, steps, warmup):
     """Warm up, then time exactly `steps` steps synchronized on both sides.
     Every op of every step -- warmup and timed alike -- is bracketed by HIP
@@ -303,7 +310,7 @@ def run_steps(torch, stream, step, n_ops, steps, warmup):
     t1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    tm.warmup_ramp_ms = [float(np.mean(c)) for c in np.array_split(np.array(ramp), min(10, len(ramp))) if len(c)]
+    tm.warmup_ramp_ms = tenths(ramp)
     return t0.elapsed_time(t1) / steps, wall * 1e3 / steps, tm
 
 

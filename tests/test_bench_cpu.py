@@ -47,3 +47,11 @@ def test_more_than_one_gpu_is_refused():
                        text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_warmup_tenths():
+    assert bench.tenths([]) == []
+    assert bench.tenths([2.0]) == [2.0]
+    assert bench.tenths([1.0, 3.0, 5.0]) == [1.0, 3.0, 5.0]
+    t = bench.tenths(list(range(200)))
+    assert len(t) == 10 and t[0] == 9.5 and t[-1] == 189.5
