@@ -207,20 +207,27 @@ __device__ __forceinline__ void backbone_48(const float (&y)[32], const Q& qz, u
   meta = 0u;
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
+    // of p < q, p beats q iff |y_p| >= |y_q|; p survives iff it beats at least
+    // 4 of the other 7.  One comparison per pair counts on both sides
+    // (beats[p] starts at p, the lower positions it beats unless they beat it).
     float a[8];
-#pragma unroll
-    for (int p = 0; p < 8; ++p) a[p] = fabsf(y[8 * g + p]);
-    bool keep[8];
+    int beats[8];
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
-      int rank = 0;
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        if (q < p) rank += a[q] >= a[p];
-        if (q > p) rank += a[q] > a[p];
-      }
-      keep[p] = rank < 4;
+      a[p] = fabsf(y[8 * g + p]);
+      beats[p] = p;
     }
+#pragma unroll
+    for (int p = 0; p < 8; ++p)
+#pragma unroll
+      for (int q = p + 1; q < 8; ++q) {
+        const int c = a[p] >= a[q];
+        beats[p] += c;
+        beats[q] -= c;
+      }
+    bool keep[8];
+#pragma unroll
+    for (int p = 0; p < 8; ++p) keep[p] = beats[p] >= 4;
     // kept values in ascending position order
     float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     int pre[8];
@@ -250,6 +257,83 @@ __device__ __forceinline__ void backbone_48(const float (&y)[32], const Q& qz, u
         if (keep[p] && pre[p] == s) dp = d[s];
       R[8 * g + p] = y[8 * g + p] - dp;
     }
+  }
+}
+
+// Dense codes of one group of 8 (b: kept values, +0 where dropped) into one
+// dword, low nibble first in ascending K, and the group's residual
+// y - dequant(code): y itself where dropped (y - (+0) = y, signed zeros
+// included).
+template <class Q>
+__device__ __forceinline__ void dense_group8(const Q& qz, const float (&b)[8], const float* y, uint32_t& word,
+                                             float* R) {
+  word = __float_as_uint(b[0]);   // every byte is overwritten below
+  put_pair<0>(qz, word, b[0], b[1]);
+  put_pair<1>(qz, word, b[2], b[3]);
+  put_pair<2>(qz, word, b[4], b[5]);
+  put_pair<3>(qz, word, b[6], b[7]);
+  const v2f d0 = qz.template dec2<0>(word), d1 = qz.template dec2<1>(word);
+  const v2f d2 = qz.template dec2<2>(word), d3 = qz.template dec2<3>(word);
+  R[0] = y[0] - d0.x;
+  R[1] = y[1] - d0.y;
+  R[2] = y[2] - d1.x;
+  R[3] = y[3] - d1.y;
+  R[4] = y[4] - d2.x;
+  R[5] = y[5] - d2.y;
+  R[6] = y[6] - d3.x;
+  R[7] = y[7] - d3.y;
+}
+
+// The backbone of one 4:8 block as its dense codes alone (dropped positions
+// +0, so code 0), and the residual: no compressed codes or metadata are
+// formed.  Each group of 8 is converted in place into one dword.  The
+// selection is backbone_48's: of p < q, p beats q iff |y_p| >= |y_q|, and a
+// position survives iff it beats at least 4 of the other 7.  One comparison
+// per pair updates a per-lane count on both sides (beats[p] starts at p, the
+// number of lower positions, which it beats unless they beat it).
+template <class Q>
+__device__ __forceinline__ void backbone_48_dense_only(const float (&y)[32], const Q& qz, uint32_t (&dense)[4],
+                                                       float (&R)[32]) {
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const float* e = y + 8 * g;
+    float a[8];
+    int beats[8];
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      a[p] = fabsf(e[p]);
+      beats[p] = p;
+    }
+#pragma unroll
+    for (int p = 0; p < 8; ++p)
+#pragma unroll
+      for (int q = p + 1; q < 8; ++q) {
+        const int c = a[p] >= a[q];
+        beats[p] += c;
+        beats[q] -= c;
+      }
+    float b[8];
+#pragma unroll
+    for (int p = 0; p < 8; ++p) b[p] = beats[p] >= 4 ? e[p] : 0.0f;
+    dense_group8(qz, b, e, dense[g], R + 8 * g);
+  }
+}
+
+// The same for 4:8 in pairs: the 2:4 selection on the pair scores
+// max(|y_2i|, |y_2i+1|), whole pairs kept (backbone_48p's selection).
+template <class Q>
+__device__ __forceinline__ void backbone_48p_dense_only(const float (&y)[32], const Q& qz, uint32_t (&dense)[4],
+                                                        float (&R)[32]) {
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const float* e = y + 8 * g;
+    const float s0 = fmaxf(fabsf(e[0]), fabsf(e[1])), s1 = fmaxf(fabsf(e[2]), fabsf(e[3]));
+    const float s2 = fmaxf(fabsf(e[4]), fabsf(e[5])), s3 = fmaxf(fabsf(e[6]), fabsf(e[7]));
+    lmask p0, p1, p2, p3;
+    top2of4(s0, s1, s2, s3, p0, p1, p2, p3);
+    const float b[8] = {lsel(p0, e[0], 0.0f), lsel(p0, e[1], 0.0f), lsel(p1, e[2], 0.0f), lsel(p1, e[3], 0.0f),
+                        lsel(p2, e[4], 0.0f), lsel(p2, e[5], 0.0f), lsel(p3, e[6], 0.0f), lsel(p3, e[7], 0.0f)};
+    dense_group8(qz, b, e, dense[g], R + 8 * g);
   }
 }
 
@@ -344,6 +428,11 @@ __device__ __forceinline__ void block_mx(const float (&y)[32], const BlockOut& d
     *reinterpret_cast<uint4*>(d.spd) = make_uint4(dense[0], dense[1], dense[2], dense[3]);
   } else if (PAT == 24) {
     backbone_24(y, qb, codes, meta, R);
+  } else if (d.spd != nullptr && d.spc == nullptr && d.dbg_mask == nullptr) {   // 4:8, dense copy alone
+    uint32_t dense[4];
+    if (PAT == 49) backbone_48p_dense_only(y, qb, dense, R);
+    else backbone_48_dense_only(y, qb, dense, R);
+    *reinterpret_cast<uint4*>(d.spd) = make_uint4(dense[0], dense[1], dense[2], dense[3]);
   } else if (PAT == 49) {
     backbone_48p(y, qb, codes, meta, R);
   } else {
@@ -361,7 +450,8 @@ __device__ __forceinline__ void block_mx(const float (&y)[32], const BlockOut& d
   *d.sps = (uint8_t)(e + 127);
   *reinterpret_cast<uint4*>(d.dnc) = make_uint4(dn[0], dn[1], dn[2], dn[3]);
   *d.dns = (uint8_t)(er + 127);
-  if (PAT != 24 && d.spd) *reinterpret_cast<uint4*>(d.spd) = expand_block<48>(make_uint2(codes[0], codes[1]), meta);
+  if (PAT != 24 && d.spd != nullptr && (d.spc != nullptr || d.dbg_mask != nullptr))
+    *reinterpret_cast<uint4*>(d.spd) = expand_block<48>(make_uint2(codes[0], codes[1]), meta);
   if (d.dbg_mask) *d.dbg_mask = keep_bits<PAT>(meta);
 }
 
