@@ -17,9 +17,6 @@ namespace sharq {
 // N:M selection inside one block
 // ---------------------------------------------------------------------------
 
-// Smallest float above a non-negative finite a (FLT_MAX -> +inf).
-__device__ __forceinline__ float next_up(float a) { return __uint_as_float(__float_as_uint(a) + 1u); }
-
 // Lane masks.  A comparison over the wavefront is one vector instruction that
 // leaves a 64-bit mask in scalar registers; logic on masks runs on the
 // scalar unit, beside the vector work of the other wavefronts, and the masks
