@@ -196,7 +196,66 @@ __device__ __forceinline__ uint32_t keep_bits(uint32_t meta) {
   return k;
 }
 
-// Backbone of one block for the 4:8 pattern (keep mask metadata).
+// 4:8 selection on one group of 8: of p < q, p beats q iff |y_p| >= |y_q|
+// (a tie goes to the lower index), and a position survives iff it beats at
+// least 4 of the other 7.  One comparison per pair counts on both sides in
+// per-lane integers (beats[p] starts at p: the lower positions, which it
+// beats unless they beat them).  Returns the 8-bit keep mask and b = y where
+// kept, +0 where dropped.
+__device__ __forceinline__ uint32_t select48(const float* e, float (&b)[8]) {
+  float a[8];
+  int beats[8];
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    a[p] = fabsf(e[p]);
+    beats[p] = p;
+  }
+#pragma unroll
+  for (int p = 0; p < 8; ++p)
+#pragma unroll
+    for (int q = p + 1; q < 8; ++q) {
+      const int c = a[p] >= a[q];
+      beats[p] += c;
+      beats[q] -= c;
+    }
+  uint32_t mask = 0u;
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    const uint32_t kb = (uint32_t)beats[p] >> 2;   // 1 iff beats[p] >= 4 (beats[p] <= 7)
+    mask |= kb << p;
+    b[p] = __uint_as_float(__float_as_uint(e[p]) & (0u - kb));
+  }
+  return mask;
+}
+
+// The four kept codes of a group (exactly four bits of mask set) out of its
+// dense dword (code of position p in nibble p), packed in ascending position,
+// low nibble first: the nibbles are spread to one byte per position, the
+// kept bytes gathered by one byte permute, and the bytes packed back.
+__device__ __forceinline__ uint32_t compact48(uint32_t dense, uint32_t mask) {
+  const uint32_t lo = dense & 0x0F0F0F0Fu;          // positions 0, 2, 4, 6
+  const uint32_t hi = (dense >> 4) & 0x0F0F0F0Fu;   // positions 1, 3, 5, 7
+  // perm(s0, s1, sel): selector 0-3 takes byte k of s1, 4-7 byte k - 4 of s0
+  const uint32_t q0 = __builtin_amdgcn_perm(hi, lo, 0x05010400u);   // positions 0..3, one per byte
+  const uint32_t q1 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);   // positions 4..7
+  uint32_t m = mask, sel = 0u;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    sel |= (uint32_t)__builtin_ctz(m) << (8 * s);
+    m &= m - 1u;
+  }
+  const uint32_t c = __builtin_amdgcn_perm(q1, q0, sel);   // kept codes k0..k3, one per byte
+  const uint32_t t = c | (c >> 4);                          // k0 | k1 << 4 in byte 0, k2 | k3 << 4 in byte 2
+  return (t & 0xFFu) | ((t >> 8) & 0xFF00u);
+}
+
+template <class Q>
+__device__ __forceinline__ void dense_group8(const Q& qz, const float (&b)[8], const float* y, uint32_t& word,
+                                             float* R);
+
+// Backbone of one block for the 4:8 pattern (keep mask metadata): each group
+// is converted in place (kept values, +0 where dropped), its residual taken
+// against that, and the kept codes gathered from the dense dword.
 template <class Q>
 __device__ __forceinline__ void backbone_48(const float (&y)[32], const Q& qz, uint32_t (&codes)[2], uint32_t& meta,
                                             float (&R)[32]) {
@@ -204,56 +263,12 @@ __device__ __forceinline__ void backbone_48(const float (&y)[32], const Q& qz, u
   meta = 0u;
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    // of p < q, p beats q iff |y_p| >= |y_q|; p survives iff it beats at least
-    // 4 of the other 7.  One comparison per pair counts on both sides
-    // (beats[p] starts at p, the lower positions it beats unless they beat it).
-    float a[8];
-    int beats[8];
-#pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      a[p] = fabsf(y[8 * g + p]);
-      beats[p] = p;
-    }
-#pragma unroll
-    for (int p = 0; p < 8; ++p)
-#pragma unroll
-      for (int q = p + 1; q < 8; ++q) {
-        const int c = a[p] >= a[q];
-        beats[p] += c;
-        beats[q] -= c;
-      }
-    bool keep[8];
-#pragma unroll
-    for (int p = 0; p < 8; ++p) keep[p] = beats[p] >= 4;
-    // kept values in ascending position order
-    float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    int pre[8];
-    int cnt = 0;
-    uint32_t mask = 0u;
-#pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      pre[p] = cnt;
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-        if (keep[p] && cnt == s) v[s] = y[8 * g + p];
-      cnt += keep[p];
-      mask |= (uint32_t)keep[p] << p;
-    }
+    float b[8];
+    const uint32_t mask = select48(y + 8 * g, b);
     meta |= mask << (8 * g);
-    int byte0 = 2 * g;   // group g's four codes occupy bytes 2g, 2g+1 of the 8
-    put_pair_dyn(qz, codes[byte0 >> 2], byte0, v[0], v[1]);
-    put_pair_dyn(qz, codes[(byte0 + 1) >> 2], byte0 + 1, v[2], v[3]);
-    const v2f d01 = get_pair_dyn(qz, codes[byte0 >> 2], byte0);
-    const v2f d23 = get_pair_dyn(qz, codes[(byte0 + 1) >> 2], byte0 + 1);
-    float d[4] = {d01.x, d01.y, d23.x, d23.y};
-#pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      float dp = 0.0f;
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-        if (keep[p] && pre[p] == s) dp = d[s];
-      R[8 * g + p] = y[8 * g + p] - dp;
-    }
+    uint32_t dense;
+    dense_group8(qz, b, y + 8 * g, dense, R + 8 * g);
+    codes[g >> 1] |= compact48(dense, mask) << (16 * (g & 1));
   }
 }
 
@@ -282,37 +297,16 @@ __device__ __forceinline__ void dense_group8(const Q& qz, const float (&b)[8], c
 }
 
 // The backbone of one 4:8 block as its dense codes alone (dropped positions
-// +0, so code 0), and the residual: no compressed codes or metadata are
-// formed.  Each group of 8 is converted in place into one dword.  The
-// selection is backbone_48's: of p < q, p beats q iff |y_p| >= |y_q|, and a
-// position survives iff it beats at least 4 of the other 7.  One comparison
-// per pair updates a per-lane count on both sides (beats[p] starts at p, the
-// number of lower positions, which it beats unless they beat it).
+// +0, so code 0), and the residual: backbone_48 without the compressed codes
+// and the metadata.
 template <class Q>
 __device__ __forceinline__ void backbone_48_dense_only(const float (&y)[32], const Q& qz, uint32_t (&dense)[4],
                                                        float (&R)[32]) {
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    const float* e = y + 8 * g;
-    float a[8];
-    int beats[8];
-#pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      a[p] = fabsf(e[p]);
-      beats[p] = p;
-    }
-#pragma unroll
-    for (int p = 0; p < 8; ++p)
-#pragma unroll
-      for (int q = p + 1; q < 8; ++q) {
-        const int c = a[p] >= a[q];
-        beats[p] += c;
-        beats[q] -= c;
-      }
     float b[8];
-#pragma unroll
-    for (int p = 0; p < 8; ++p) b[p] = beats[p] >= 4 ? e[p] : 0.0f;
-    dense_group8(qz, b, e, dense[g], R + 8 * g);
+    select48(y + 8 * g, b);
+    dense_group8(qz, b, y + 8 * g, dense[g], R + 8 * g);
   }
 }
 
