@@ -765,9 +765,22 @@ __device__ __forceinline__ void store_w_stage(const WStep<NF>& w, uint8_t* stage
 // along rows: each store instruction then writes two whole 512-byte row
 // segments.  The wavefront owns its LDS region, and its LDS accesses execute
 // in order, so no barrier is needed inside.
+// A value that is the same in every lane, read from the first active one.
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Fourth dword of a raw buffer resource (no stride, no swizzle, 32-bit
+// data format: the range check is on the byte offset).
+constexpr int kBufferWord3 = 0x00020000;
+typedef uint32_t v4u32_t __attribute__((ext_vector_type(4)));
+
 constexpr int kEpiStride = 528;            // bytes per staged row: 512 + 16 (spreads rows over banks)
 constexpr int kEpiWave = 32 * kEpiStride;  // one wavefront's region
 constexpr int kTileLds = 4 * kEpiWave > 3 * kStageBytes ? 4 * kEpiWave : 3 * kStageBytes;
+constexpr int kPersistLds = 3 * kStageBytes + 4 * kEpiWave;   // stages and epilogue apart: 129 KB
 
 template <typename OutT, int NF>
 __device__ __forceinline__ void store_tile_lds(const v16f (&acc)[NF], OutT* Y, int64_t ldy, int64_t row0,
@@ -783,13 +796,43 @@ __device__ __forceinline__ void store_tile_lds(const v16f (&acc)[NF], OutT* Y, i
                          acc[f][4 * g], acc[f][4 * g + 1], acc[f][4 * g + 2], acc[f][4 * g + 3]);
     }
   }
+  // every read back first: a store under a per-row condition would take its
+  // read into its own branch and wait for it there, one LDS round trip per
+  // store
+  constexpr int kReads = 32 / rpi;
+  uint4 v[kReads];
 #pragma unroll
-  for (int i = 0; i < 32 / rpi; ++i) {
-    const int rr = rpi * i + lane / lpr, ch = lane % lpr;
-    const uint4 v = *reinterpret_cast<const uint4*>(buf + rr * stride + ch * 16);
-    const int64_t row = row0 + rr;
-    const int col = n0 + 8 * ch;
-    if (row < row_hi && col < N) *reinterpret_cast<uint4*>(Y + row * ldy + col) = v;
+  for (int i = 0; i < kReads; ++i)
+    v[i] = *reinterpret_cast<const uint4*>(buf + (rpi * i + lane / lpr) * stride + (lane % lpr) * 16);
+  // row0 and row_hi are the same in every lane; the compiler cannot see it,
+  // and a buffer resource held in vector registers would cost a loop over
+  // lanes around every store
+  row0 = uniform64(row0);
+  row_hi = uniform64(row_hi);
+  const int64_t rows = row_hi - row0 < 32 ? row_hi - row0 : 32;   // the wavefront's rows in the tile
+  if (rows <= 0) return;
+  const int64_t span = rows * ldy * (int64_t)sizeof(OutT);
+  const int ch = lane % lpr, col = n0 + 8 * ch;
+  if (span <= (int64_t)1 << 30) {
+    // Unconditional buffer stores over a range of exactly the wavefront's
+    // rows: the range check drops a store to a row past the tile, and a
+    // column past N gets an offset (2^31 - 16) past any such range.
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(Y + row0 * ldy, (short)0, (int)span,
+                                                                        kBufferWord3);
+#pragma unroll
+    for (int i = 0; i < kReads; ++i) {
+      const int rr = rpi * i + lane / lpr;
+      const int off = col < N ? (int)(((int64_t)rr * ldy + col) * (int64_t)sizeof(OutT)) : 0x7FFFFFF0;
+      v4u32_t q;
+      q[0] = v[i].x; q[1] = v[i].y; q[2] = v[i].z; q[3] = v[i].w;
+      __builtin_amdgcn_raw_buffer_store_b128(q, rs, off, 0, 0);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kReads; ++i) {
+      const int rr = rpi * i + lane / lpr;
+      if (rr < rows && col < N) *reinterpret_cast<uint4*>(Y + (row0 + rr) * ldy + col) = v[i];
+    }
   }
 }
 
@@ -805,100 +848,101 @@ __device__ __forceinline__ void step_il(v16f (&acc)[NF], const AOps& ops, uint4 
     step5h<PAT>(acc, ops, b0, bw, bwn, cur, nxt, wr, opsn, raw, wst, lane, issue, lut);
 }
 
-template <int PAT, typename OutT, int NF>
-__device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale,
-                                           const uint8_t* dn_codes, const uint8_t* dn_scale, const int32_t* row_index,
-                                           int64_t act_rows, int64_t row_lo, int64_t row_hi, const uint8_t* wc,
-                                           const uint8_t* ws, int n0, int N, int K, OutT* Y, int64_t ldy,
-                                           uint8_t* lds, const uint2* lut) {
-  static_assert(NF == 8 || NF == 4, "full (256-column) or half tile");
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
-  const int nblk = K / 32, nks = K / kBK;
-
-  int64_t orow = row_lo + wave * 32 + (lane & 31);
-  if (orow >= row_hi) orow = row_hi - 1;   // clamp: loads stay in bounds, stores are masked
-  ARow a;
-  a.r = row_index ? (int64_t)row_index[orow] : orow;
-  a.R = act_rows;
-  a.dn = dn_codes;
-  a.spc = sp_codes;
-  a.spm = sp_meta;
-  a.dns = dn_scale;
-  a.sps = sp_scale;
-
-  v16f acc[NF];
-#pragma unroll
-  for (int f = 0; f < NF; ++f)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[f][r] = 0.0f;
-
-  // Register sets rotate with period three, so the loop is unrolled by
-  // three and the LDS stages are fixed per unrolled step.  Invariant at the
-  // start of step k (sets indexed by k mod 3): stages k, k+1 hold W(k),
-  // W(k+1); b0 / bw hold step k's first weight operands; o[k] is complete;
-  // o[k+1].dn = residual codes of step k+1 (in flight); r[k+1], r[k+2] = raw
-  // backbone data of steps k+1, k+2; w[k+2], w[k] = raw W(k+2), W(k+3).
-  // Step k loads the residual codes of step k+2, the raw backbone of step k+3
-  // and W(k+4): every load has two full steps to arrive.  Loads past the last
-  // step re-read it (clamped) and their results are never used.
-  const int last = nks - 1;
+// The register sets of the interleaved pipeline.  They rotate with period
+// three, so the main loop is unrolled by three and the LDS stages are fixed
+// per unrolled step.  Invariant at the start of step k (sets indexed by
+// k mod 3): stages k, k+1 hold W(k), W(k+1); b0 / bw hold step k's first
+// weight operands; o[k] is complete; o[k+1].dn = residual codes of step k+1
+// (in flight); r[k+1], r[k+2] = raw backbone data of steps k+1, k+2; w[k+2],
+// w[k] = raw W(k+2), W(k+3).  Step k loads the residual codes of step k+2, the
+// raw backbone of step k+3 and W(k+4): every load has two full steps to
+// arrive.  Loads past the last step re-read it (clamped) and their results
+// are never used.
+template <int NF>
+struct IlSets {
   AStep r0, r1, r2;
   WStep<NF> w0, w1, w2;
   AOps o0, o1, o2;
-  uint4 b0[NF];
-  uint32_t bwa[NF / 2], bwb[NF / 2];
+};
+
+// A tile's first global loads: W(0..2), the residual codes of steps 0 and 1,
+// the raw backbone of steps 0..2.  They touch no LDS, so a persistent loop can
+// issue them for its next tile before the current tile's output stores.
+template <int PAT, int NF>
+__device__ __forceinline__ void il_issue(IlSets<NF>& p, const ARow& a, const uint8_t* wc, const uint8_t* ws,
+                                         int n0, int N, int K, int half) {
+  const int nblk = K / 32, last = K / kBK - 1;
+  const auto cl = [&](int k) { return k < last ? k : last; };
+  load_w<NF, true>(p.w0, wc, ws, n0, N, K, 0, nblk);
+  load_a_meta<PAT>(p.r0, a, 0, half);
+  load_a_dn(p.o0, a, 0, half);
+  load_w<NF, true>(p.w1, wc, ws, n0, N, K, cl(1), nblk);
+  load_a_dn(p.o1, a, cl(1), half);
+  load_a_meta<PAT>(p.r1, a, cl(1), half);
+  load_a_meta<PAT>(p.r2, a, cl(2), half);
+  load_w<NF, true>(p.w2, wc, ws, n0, N, K, cl(2), nblk);
+}
+
+// The rest of a tile's prologue: W(0), W(1) into stages 0 and 1, step 0's
+// backbone operands, the load of W(3), and step 0's first weight operands.
+// The stages must be free (a barrier after the previous tile's last step).
+template <int PAT, int NF>
+__device__ __forceinline__ void il_start(IlSets<NF>& p, const uint8_t* wc, const uint8_t* ws, int n0, int N,
+                                         int K, uint8_t* lds, uint4 (&b0)[NF], uint32_t (&bwa)[NF / 2], int lane,
+                                         int half) {
+  const int nblk = K / 32, last = K / kBK - 1;
+  store_w_stage(p.w0, lds);
+  store_w_stage(p.w1, lds + kStageBytes);
+  if (PAT == 0) {
+    p.o0.sp[0] = p.r0.spd[0];
+    p.o0.sp[1] = p.r0.spd[1];
+  } else {
+    p.o0.sp[0] = expand_block<PAT>(p.r0.spc[0], p.r0.spm[0]);
+    p.o0.sp[1] = expand_block<PAT>(p.r0.spc[1], p.r0.spm[1]);
+  }
+  p.o0.ssp = p.r0.ssp >> (16 * half);
+  p.o0.sdn = p.r0.sdn >> (16 * half);
+  load_w<NF, true>(p.w0, wc, ws, n0, N, K, 3 < last ? 3 : last, nblk);
+  __syncthreads();
+  read_bw(bwa, lds, lane);
+  read_b<0, 0, NF>(b0, lds, lane);
+}
+
+// Every K step of a started tile into acc.
+template <int PAT, int NF>
+__device__ __forceinline__ void il_main(v16f (&acc)[NF], IlSets<NF>& p, uint4 (&b0)[NF], uint32_t (&bwa)[NF / 2],
+                                        const ARow& a, const uint8_t* wc, const uint8_t* ws, int n0, int N, int K,
+                                        uint8_t* lds, int lane, int half, const uint2* lut) {
+  const int nks = K / kBK, last = nks - 1;
+  const auto cl = [&](int k) { return k < last ? k : last; };
   uint8_t* const st0 = lds;
   uint8_t* const st1 = lds + kStageBytes;
   uint8_t* const st2 = lds + 2 * kStageBytes;
-  const auto cl = [&](int k) { return k < last ? k : last; };
-  load_w<NF, true>(w0, wc, ws, n0, N, K, 0, nblk);
-  load_a_meta<PAT>(r0, a, 0, half);
-  load_a_dn(o0, a, 0, half);
-  load_w<NF, true>(w1, wc, ws, n0, N, K, cl(1), nblk);
-  store_w_stage(w0, st0);
-  store_w_stage(w1, st1);
-  if (PAT == 0) {
-    o0.sp[0] = r0.spd[0];
-    o0.sp[1] = r0.spd[1];
-  } else {
-    o0.sp[0] = expand_block<PAT>(r0.spc[0], r0.spm[0]);
-    o0.sp[1] = expand_block<PAT>(r0.spc[1], r0.spm[1]);
-  }
-  o0.ssp = r0.ssp >> (16 * half);
-  o0.sdn = r0.sdn >> (16 * half);
-  load_a_dn(o1, a, cl(1), half);
-  load_a_meta<PAT>(r1, a, cl(1), half);
-  load_a_meta<PAT>(r2, a, cl(2), half);
-  load_w<NF, true>(w2, wc, ws, n0, N, K, cl(2), nblk);
-  load_w<NF, true>(w0, wc, ws, n0, N, K, cl(3), nblk);
-  __syncthreads();
-  read_bw(bwa, st0, lane);
-  read_b<0, 0, NF>(b0, st0, lane);
-
+  uint32_t bwb[NF / 2];
   int ks = 0;
   for (; ks + 2 < nks; ks += 3) {
-    step_il<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [&](auto part) {
+    step_il<PAT>(acc, p.o0, b0, bwa, bwb, st0, st1, st2, p.o1, p.r1, p.w2, lane, [&](auto part) {
       constexpr int P = decltype(part)::value;
-      if constexpr (P == 0) load_a_dn(o2, a, cl(ks + 2), half);
-      else if constexpr (P == 1) load_a_meta_part<PAT, 0>(r0, a, cl(ks + 3), half);
-      else if constexpr (P == 2) load_a_meta_part<PAT, 1>(r0, a, cl(ks + 3), half);
-      else load_w_part<NF, P - 3>(w1, wc, ws, n0, N, cl(ks + 4));
+      if constexpr (P == 0) load_a_dn(p.o2, a, cl(ks + 2), half);
+      else if constexpr (P == 1) load_a_meta_part<PAT, 0>(p.r0, a, cl(ks + 3), half);
+      else if constexpr (P == 2) load_a_meta_part<PAT, 1>(p.r0, a, cl(ks + 3), half);
+      else load_w_part<NF, P - 3>(p.w1, wc, ws, n0, N, cl(ks + 4));
     }, lut);
     __syncthreads();
-    step_il<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [&](auto part) {
+    step_il<PAT>(acc, p.o1, b0, bwb, bwa, st1, st2, st0, p.o2, p.r2, p.w0, lane, [&](auto part) {
       constexpr int P = decltype(part)::value;
-      if constexpr (P == 0) load_a_dn(o0, a, cl(ks + 3), half);
-      else if constexpr (P == 1) load_a_meta_part<PAT, 0>(r1, a, cl(ks + 4), half);
-      else if constexpr (P == 2) load_a_meta_part<PAT, 1>(r1, a, cl(ks + 4), half);
-      else load_w_part<NF, P - 3>(w2, wc, ws, n0, N, cl(ks + 5));
+      if constexpr (P == 0) load_a_dn(p.o0, a, cl(ks + 3), half);
+      else if constexpr (P == 1) load_a_meta_part<PAT, 0>(p.r1, a, cl(ks + 4), half);
+      else if constexpr (P == 2) load_a_meta_part<PAT, 1>(p.r1, a, cl(ks + 4), half);
+      else load_w_part<NF, P - 3>(p.w2, wc, ws, n0, N, cl(ks + 5));
     }, lut);
     __syncthreads();
-    step_il<PAT>(acc, o2, b0, bwa, bwb, st2, st0, st1, o0, r0, w1, lane, [&](auto part) {
+    step_il<PAT>(acc, p.o2, b0, bwa, bwb, st2, st0, st1, p.o0, p.r0, p.w1, lane, [&](auto part) {
       constexpr int P = decltype(part)::value;
-      if constexpr (P == 0) load_a_dn(o1, a, cl(ks + 4), half);
-      else if constexpr (P == 1) load_a_meta_part<PAT, 0>(r2, a, cl(ks + 5), half);
-      else if constexpr (P == 2) load_a_meta_part<PAT, 1>(r2, a, cl(ks + 5), half);
-      else load_w_part<NF, P - 3>(w0, wc, ws, n0, N, cl(ks + 6));
+      if constexpr (P == 0) load_a_dn(p.o1, a, cl(ks + 4), half);
+      else if constexpr (P == 1) load_a_meta_part<PAT, 0>(p.r2, a, cl(ks + 5), half);
+      else if constexpr (P == 2) load_a_meta_part<PAT, 1>(p.r2, a, cl(ks + 5), half);
+      else load_w_part<NF, P - 3>(p.w0, wc, ws, n0, N, cl(ks + 6));
     }, lut);
     __syncthreads();
     // bw alternates with period two: after three steps the roles swap
@@ -910,23 +954,28 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
     }
   }
   if (ks < nks) {   // one or two steps left, in sets 0 and 1
-    step_il<PAT>(acc, o0, b0, bwa, bwb, st0, st1, st2, o1, r1, w2, lane, [](auto) {}, lut);
+    step_il<PAT>(acc, p.o0, b0, bwa, bwb, st0, st1, st2, p.o1, p.r1, p.w2, lane, [](auto) {}, lut);
     if (ks + 1 < nks) {
       __syncthreads();
-      step_il<PAT>(acc, o1, b0, bwb, bwa, st1, st2, st0, o2, r2, w0, lane, [](auto) {}, lut);
+      step_il<PAT>(acc, p.o1, b0, bwb, bwa, st1, st2, st0, p.o2, p.r2, p.w0, lane, [](auto) {}, lut);
     }
   }
+}
 
-  // Epilogue.  2-byte outputs go through LDS as whole row segments when the
-  // output allows 16-byte stores (every workgroup-uniform condition).
+// Epilogue.  2-byte outputs go through the wavefront's LDS region `epi` as
+// whole row segments when the output allows 16-byte stores (every
+// workgroup-uniform condition); otherwise each lane stores its own row, four
+// consecutive columns per store.  The caller makes `epi` free.
+template <typename OutT, int NF>
+__device__ __forceinline__ void il_epilogue(const v16f (&acc)[NF], OutT* Y, int64_t ldy, int64_t row_lo,
+                                            int64_t row_hi, int n0, int N, uint8_t* epi, int wave, int lane) {
+  const int half = lane >> 5;
   if constexpr (sizeof(OutT) == 2) {
     if (((reinterpret_cast<uintptr_t>(Y) | (uintptr_t)(ldy * 2)) & 15u) == 0 && N % 8 == 0) {
-      __syncthreads();   // every wavefront is done with the weight stages
-      store_tile_lds<OutT, NF>(acc, Y, ldy, row_lo + wave * 32, row_hi, n0, N, lds + wave * kEpiWave, lane);
+      store_tile_lds<OutT, NF>(acc, Y, ldy, row_lo + wave * 32, row_hi, n0, N, epi, lane);
       return;
     }
   }
-  // Otherwise this lane's output row, four consecutive columns per store.
   const int64_t row = row_lo + wave * 32 + (lane & 31);
   if (row >= row_hi) return;
   OutT* yr = Y + row * ldy;
@@ -945,6 +994,102 @@ __device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_
           if (col + e < N) store_out<OutT>(yr + col + e, acc[f][4 * g + e]);
       }
     }
+  }
+}
+
+// This lane's activation row in a tile of rows [row_lo, row_hi): rows past
+// the end are clamped (loads stay in bounds, stores are masked).
+__device__ __forceinline__ int64_t il_row(const int32_t* row_index, int64_t row_lo, int64_t row_hi) {
+  int64_t orow = row_lo + (threadIdx.x >> 6) * 32 + (threadIdx.x & 31);
+  if (orow >= row_hi) orow = row_hi - 1;
+  return row_index ? (int64_t)row_index[orow] : orow;
+}
+
+// One tile of the interleaved pipeline, alone: its LDS stages at lds, its
+// epilogue staged over them once every wavefront is done with them.
+template <int PAT, typename OutT, int NF>
+__device__ __forceinline__ void tile_mx_il(const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale,
+                                           const uint8_t* dn_codes, const uint8_t* dn_scale, const int32_t* row_index,
+                                           int64_t act_rows, int64_t row_lo, int64_t row_hi, const uint8_t* wc,
+                                           const uint8_t* ws, int n0, int N, int K, OutT* Y, int64_t ldy,
+                                           uint8_t* lds, const uint2* lut) {
+  static_assert(NF == 8 || NF == 4, "full (256-column) or half tile");
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
+  ARow a;
+  a.r = il_row(row_index, row_lo, row_hi);
+  a.R = act_rows;
+  a.dn = dn_codes;
+  a.spc = sp_codes;
+  a.spm = sp_meta;
+  a.dns = dn_scale;
+  a.sps = sp_scale;
+  v16f acc[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[f][r] = 0.0f;
+  IlSets<NF> p;
+  uint4 b0[NF];
+  uint32_t bwa[NF / 2];
+  il_issue<PAT, NF>(p, a, wc, ws, n0, N, K, half);
+  il_start<PAT, NF>(p, wc, ws, n0, N, K, lds, b0, bwa, lane, half);
+  il_main<PAT, NF>(acc, p, b0, bwa, a, wc, ws, n0, N, K, lds, lane, half, lut);
+  __syncthreads();   // every wavefront is done with the weight stages
+  il_epilogue<OutT, NF>(acc, Y, ldy, row_lo, row_hi, n0, N, lds + wave * kEpiWave, wave, lane);
+}
+
+// A tile of the persistent loops: output rows [row_lo, row_hi), this lane's
+// activation row r, weight columns n0.. of the payload at wc / ws.
+struct IlTile {
+  int64_t row_lo, row_hi, r;
+  const uint8_t *wc, *ws;
+  int n0;
+};
+
+// Full tiles back to back, as handed out by next(IlTile&) until it returns
+// false.  The next tile's first loads go out after the current tile's last
+// step and before its output stores: the vector-memory counter completes in
+// issue order, so loads issued behind the stores would first wait for the
+// stores (64 KB per tile) to drain.  The epilogue therefore has its own LDS
+// region `epi` (4 kEpiWave bytes) beside the three stages at `lds`.
+template <int PAT, typename OutT, class Next>
+__device__ __forceinline__ void tiles_mx_il(const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale,
+                                            const uint8_t* dn_codes, const uint8_t* dn_scale, int64_t act_rows, int N,
+                                            int K, OutT* Y, int64_t ldy, uint8_t* lds, uint8_t* epi,
+                                            const uint2* lut, Next next) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, half = lane >> 5;
+  IlTile t;
+  if (!next(t)) return;
+  ARow a;
+  a.r = t.r;
+  a.R = act_rows;
+  a.dn = dn_codes;
+  a.spc = sp_codes;
+  a.spm = sp_meta;
+  a.dns = dn_scale;
+  a.sps = sp_scale;
+  IlSets<8> p;
+  il_issue<PAT, 8>(p, a, t.wc, t.ws, t.n0, N, K, half);
+  for (;;) {
+    uint4 b0[8];
+    uint32_t bwa[4];
+    il_start<PAT, 8>(p, t.wc, t.ws, t.n0, N, K, lds, b0, bwa, lane, half);
+    IlTile tn;
+    const bool more = next(tn);   // the row-index load has the whole tile to arrive
+    v16f acc[8];
+#pragma unroll
+    for (int f = 0; f < 8; ++f)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[f][r] = 0.0f;
+    il_main<PAT, 8>(acc, p, b0, bwa, a, t.wc, t.ws, t.n0, N, K, lds, lane, half, lut);
+    if (more) {
+      a.r = tn.r;
+      il_issue<PAT, 8>(p, a, tn.wc, tn.ws, tn.n0, N, K, half);
+    }
+    il_epilogue<OutT, 8>(acc, Y, ldy, t.row_lo, t.row_hi, t.n0, N, epi + wave * kEpiWave, wave, lane);
+    if (!more) return;
+    t = tn;
+    __syncthreads();   // every wavefront is done with the stages before they are refilled
   }
 }
 
@@ -1018,31 +1163,36 @@ __global__ __launch_bounds__(256) void k_linear_mx_persist(const uint8_t* sp_cod
                                                            const uint8_t* dn_scale, int64_t M, const uint8_t* wc,
                                                            const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy,
                                                            int gx, int gy, int full, int halves) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kTileLds];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kPersistLds];
   __shared__ uint2 lut48[256];
   if (PAT == 48) {
     lut48_fill(lut48);
     __syncthreads();
   }
-  const int units = full + halves;
-  for (int id = (int)blockIdx.x; id < units; id += (int)gridDim.x) {
-    int mt, nt;
-    if (id < full) {
-      tile_of(id, gx, gy, mt, nt);
-      const int64_t m0 = (int64_t)mt * kBM;
-      const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
-      tile_mx_il<PAT, OutT, 8>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws,
-                               nt * 256, N, K, Y, ldy, lds, lut48);
-    } else {
-      int t, h;
-      half_unit(id - full, full, halves, t, h);
-      tile_of(t, gx, gy, mt, nt);
-      const int64_t m0 = (int64_t)mt * kBM;
-      const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
-      tile_mx_il<PAT, OutT, 4>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws,
-                               nt * 256 + 128 * h, N, K, Y, ldy, lds, lut48);
-    }
-    __syncthreads();   // the LDS stages are free before the next tile's prologue
+  int id = (int)blockIdx.x;
+  tiles_mx_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, M, N, K, Y, ldy, lds,
+                         lds + 3 * kStageBytes, lut48, [&](IlTile& t) {
+                           if (id >= full) return false;
+                           int mt, nt;
+                           tile_of(id, gx, gy, mt, nt);
+                           t.row_lo = (int64_t)mt * kBM;
+                           t.row_hi = t.row_lo + kBM < M ? t.row_lo + kBM : M;
+                           t.r = il_row(nullptr, t.row_lo, t.row_hi);
+                           t.wc = wc;
+                           t.ws = ws;
+                           t.n0 = nt * 256;
+                           id += (int)gridDim.x;
+                           return true;
+                         });
+  for (; id < full + halves; id += (int)gridDim.x) {
+    int t, h, mt, nt;
+    half_unit(id - full, full, halves, t, h);
+    tile_of(t, gx, gy, mt, nt);
+    const int64_t m0 = (int64_t)mt * kBM;
+    const int64_t m1 = m0 + kBM < M ? m0 + kBM : M;
+    __syncthreads();   // the LDS stages are free before this tile's prologue
+    tile_mx_il<PAT, OutT, 4>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, nullptr, M, m0, m1, wc, ws,
+                             nt * 256 + 128 * h, N, K, Y, ldy, lds, lut48);
   }
 }
 
@@ -1132,7 +1282,7 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped_persist(
     const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale, const uint8_t* dn_codes,
     const uint8_t* dn_scale, const int32_t* row_index, int64_t act_rows, const int32_t* offs, int E,
     const uint8_t* wc, const uint8_t* ws, int N, int K, OutT* Y, int64_t ldy, int gx) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kTileLds];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kPersistLds];
   __shared__ int s_first[1025];
   __shared__ uint2 lut48[256];
   const int tid = threadIdx.x;
@@ -1160,23 +1310,28 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped_persist(
   }
   const int items = s_first[E];
   const int total = gx * items;
-  for (int id = (int)blockIdx.x; id < total; id += (int)gridDim.x) {
-    const int idp = (total & 7) == 0 ? (id & 7) * (total >> 3) + (id >> 3) : id;
-    const int xt = idp / items, item = idp - xt * items;
-    int lo = 0, hi = E;   // e with s_first[e] <= item < s_first[e+1]
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (s_first[mid] <= item) lo = mid; else hi = mid;
-    }
-    const int e = lo;
-    const int64_t r0 = (int64_t)offs[e] + (int64_t)(item - s_first[e]) * kBM;
-    const int64_t r_end = offs[e + 1];
-    const int64_t r1 = r0 + kBM < r_end ? r0 + kBM : r_end;
-    tile_mx_il<PAT, OutT, 8>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, act_rows, r0, r1,
-                             wc + (int64_t)e * N * (K / 2), ws + (int64_t)e * N * (K / 32), xt * 256, N, K, Y, ldy,
-                             lds, lut48);
-    __syncthreads();   // the LDS stages are free before the next tile's prologue
-  }
+  int id = (int)blockIdx.x;
+  tiles_mx_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, act_rows, N, K, Y, ldy, lds,
+                         lds + 3 * kStageBytes, lut48, [&](IlTile& t) {
+                           if (id >= total) return false;
+                           const int idp = (total & 7) == 0 ? (id & 7) * (total >> 3) + (id >> 3) : id;
+                           const int xt = idp / items, item = idp - xt * items;
+                           int lo = 0, hi = E;   // e with s_first[e] <= item < s_first[e+1]
+                           while (hi - lo > 1) {
+                             const int mid = (lo + hi) >> 1;
+                             if (s_first[mid] <= item) lo = mid; else hi = mid;
+                           }
+                           const int e = lo;
+                           t.row_lo = (int64_t)offs[e] + (int64_t)(item - s_first[e]) * kBM;
+                           const int64_t r_end = offs[e + 1];
+                           t.row_hi = t.row_lo + kBM < r_end ? t.row_lo + kBM : r_end;
+                           t.r = il_row(row_index, t.row_lo, t.row_hi);
+                           t.wc = wc + (int64_t)e * N * (K / 2);
+                           t.ws = ws + (int64_t)e * N * (K / 32);
+                           t.n0 = xt * 256;
+                           id += (int)gridDim.x;
+                           return true;
+                         });
 }
 
 // ---------------------------------------------------------------------------
