@@ -186,16 +186,20 @@ QWEN_T = 4096
 @pytest.mark.parametrize("name", ["gate_up", "down"])
 def test_qwen_full_shape_nv(S, G, name):
     """Full M=4096 Qwen2.5-7B shapes: preparation compared in full, the GEMM on
-    64 sampled rows x all columns."""
+    256 sampled rows x all columns, and every output written (the output is
+    filled with NaN first: the persistent kernel's tile order skips ids past
+    the last of its 148 x 32 or 14 x 32 tiles)."""
     K, N, norm = synth.QWEN_LINEARS[name]
     say(f"[qwen-nv] {name} T={QWEN_T} K={K} N={N}")
     x = synth.activations(QWEN_T, K, seed=1)
     g = synth.gamma(K, seed=1) if norm else None
     a, o = check_prep_nv(S, G, x, g, 1e-6, 2, 4, name)
     wq = S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=1)), "nv")
-    y = S.sharq_linear(a, wq, dtype=torch.float32)
+    y = torch.full((QWEN_T, N), float("nan"), dtype=torch.float32, device="cuda")
+    S.sharq_linear(a, wq, out=y)
     torch.cuda.synchronize()
+    assert bool(torch.isfinite(y).all()), f"{name}: outputs left unwritten"
     wo = G.weight_to_oracle(wq)
-    rows = np.random.default_rng(2).choice(QWEN_T, 64, replace=False)
-    rows[0] = 0
+    rows = np.random.default_rng(2).choice(QWEN_T, 256, replace=False)
+    rows[0], rows[1] = 0, QWEN_T - 1
     gemm_check(G.host(y)[rows], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), name)

@@ -466,8 +466,11 @@ def test_moe_bench_layout(S, G):
     router; down: the 32768 expert-sorted rows x 768, no norm, identity row
     map.  Prepared bytes against the oracle (all rows for gate/up; the rows of
     the checked experts for down -- the preparation is row-wise), the bf16
-    output equal to the fp32 one rounded, and the slices of four experts (all
-    their rows, all columns) against the oracle."""
+    output equal to the fp32 one rounded, every routed output written (the
+    fp32 output is filled with NaN first; gate/up's 1902 (column tile, row
+    tile) units are not a multiple of the 8 XCDs, so the tile order skips
+    ids), and the slices of four experts (all their rows, all columns)
+    against the oracle."""
     cfg = synth.MOE
     T, H, E, I, k = cfg["tokens"], cfg["hidden"], cfg["experts"], cfg["inter"], cfg["topk"]
     ridx, offs = synth.router_topk(T, E, k, seed=0)
@@ -485,9 +488,11 @@ def test_moe_bench_layout(S, G):
     a1 = S.sharq_prepare(G.dev_bf16(x), G.dev_bf16(g), 1e-6, 4, 8, "mx",
                          out=S.alloc_act(T, H, 4, 8, "mx", "cuda", dense_only=True))
     w1 = quantized_experts(2 * I, H, 100)
-    y1 = S.sharq_linear_grouped(a1, ri, of, total, w1, dtype=torch.float32)
+    y1 = torch.full((total, 2 * I), float("nan"), dtype=torch.float32, device="cuda")
+    S.sharq_linear_grouped(a1, ri, of, total, w1, out=y1)
     y1b = S.sharq_linear_grouped(a1, ri, of, total, w1, dtype=torch.bfloat16)
     torch.cuda.synchronize()
+    assert bool(torch.isfinite(y1).all()), "gate_up: routed outputs left unwritten"
     assert a1.sp_codes is None and a1.sp_meta is None
     o1 = O.prepare(x, g, 1e-6, 4, 8, "mx")
     dev1 = L.act_to_device_layout(o1)
@@ -509,9 +514,11 @@ def test_moe_bench_layout(S, G):
     a2 = S.sharq_prepare(G.dev_bf16(h), None, 1e-6, 4, 8, "mx",
                          out=S.alloc_act(total, I, 4, 8, "mx", "cuda", dense_only=True))
     w2 = quantized_experts(H, I, 1000)
-    y2 = S.sharq_linear_grouped(a2, None, of, total, w2, dtype=torch.float32)
+    y2 = torch.full((total, H), float("nan"), dtype=torch.float32, device="cuda")
+    S.sharq_linear_grouped(a2, None, of, total, w2, out=y2)
     y2b = S.sharq_linear_grouped(a2, None, of, total, w2, dtype=torch.bfloat16)
     torch.cuda.synchronize()
+    assert bool(torch.isfinite(y2).all()), "down: routed outputs left unwritten"
     assert torch.equal(y2b, y2.to(torch.bfloat16))
     chk = np.concatenate([np.arange(offs[e], offs[e + 1]) for e in experts])
     o2 = O.prepare(h[chk], None, 1e-6, 4, 8, "mx")
