@@ -134,14 +134,16 @@ def test_hif4_empty(S, G):
 @pytest.mark.parametrize("name", ["qkv", "down"])
 def test_hif4_llama_full_shape(S, G, name):
     """Full M = 2048 Llama-3.1-8B shapes: preparation compared in full, the
-    GEMM on 16 sampled rows x all columns."""
+    GEMM on 256 sampled rows x all columns, and every output written."""
     K, N, norm = synth.LLAMA_LINEARS[name]
     x = synth.activations(2048, K, seed=1)
     a, o = check_prep(S, G, x, synth.gamma(K, seed=1) if norm else None, synth.LLAMA_EPS, name)
     wq = S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=1)), "hif4")
-    y = S.sharq_linear(a, wq, dtype=torch.float32)
+    y = torch.full((2048, N), float("nan"), dtype=torch.float32, device="cuda")
+    S.sharq_linear(a, wq, out=y)
     torch.cuda.synchronize()
+    assert bool(torch.isfinite(y).all()), "outputs left unwritten"
     wo = G.weight_to_oracle(wq)
-    rows = np.random.default_rng(2).choice(2048, 16, replace=False)
-    rows[0] = 0
+    rows = np.random.default_rng(2).choice(2048, 256, replace=False)
+    rows[0], rows[1] = 0, 2048 - 1
     gemm_check(G.host(y)[rows], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), name)

@@ -172,14 +172,16 @@ LLAMA_T = 2048
 @pytest.mark.parametrize("mode", MODES)
 def test_mode_llama_qkv_full_shape(S, G, mode):
     """Full M = 2048 Llama-3.1-8B qkv shape (K 4096, N 6144, MXFP4 2:4):
-    preparation compared in full, the GEMM on 16 sampled rows x all columns."""
+    preparation compared in full, the GEMM on 256 sampled rows x all columns, and every output written."""
     K, N, _ = synth.LLAMA_LINEARS["qkv"]
     x, g = synth.activations(LLAMA_T, K, seed=1), synth.gamma(K, seed=1)
     a, o = check_prep(S, G, x, g, synth.LLAMA_EPS, 2, 4, "mx", mode, False, "qkv")
     wq = S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=1)))
-    y = S.sharq_linear(a, wq, dtype=torch.float32)
+    y = torch.full((LLAMA_T, N), float("nan"), dtype=torch.float32, device="cuda")
+    S.sharq_linear(a, wq, out=y)
     torch.cuda.synchronize()
+    assert bool(torch.isfinite(y).all()), "outputs left unwritten"
     wo = G.weight_to_oracle(wq)
-    rows = np.random.default_rng(2).choice(LLAMA_T, 16, replace=False)
-    rows[0] = 0
+    rows = np.random.default_rng(2).choice(LLAMA_T, 256, replace=False)
+    rows[0], rows[1] = 0, LLAMA_T - 1
     gemm_check(G.host(y)[rows], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), f"qkv-{mode}")
