@@ -1299,7 +1299,9 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
 // expert's weight tiles).  Measured on the Qwen3-30B-A3B experts (4096
 // tokens, top-8): gate_up 190.7 -> 173.7 us, bit-identical; its 1902 units
 // had fallen outside the earlier numbering, which required a multiple of 8,
-// and were spread round-robin over the XCDs.
+// and were spread round-robin over the XCDs.  A last round at most half
+// full runs as half tiles, as in the dense kernel (gate_up's 110 leftover
+// units as 220 halves: 164.4 -> 162.8 us).
 template <int PAT, typename OutT>
 __global__ __launch_bounds__(256) void k_linear_mx_grouped_persist(
     const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale, const uint8_t* dn_codes,
@@ -1333,35 +1335,55 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped_persist(
   }
   const int items = s_first[E];
   const int total = gx * items;
-  // XCD-contiguous numbering for any unit count: ids [0, 8 per) map one to
-  // one onto units, XCD x (id mod 8) taking units [x per, (x + 1) per); ids
-  // whose unit is past the last are skipped.
-  const int per = (total + 7) >> 3;
+  // When the last round would be at most half full, its units run as twice
+  // as many half tiles of 128 columns (as in k_linear_mx_persist).
+  const int G = (int)gridDim.x, rem = total % G;
+  const int halves = rem > 0 && 2 * rem <= G ? 2 * rem : 0;
+  const int full = total - halves / 2;
+  // unit u (item-major: item u / gx, column tile u mod gx) -> expert, rows
+  const auto locate = [&](int u, int& e, int64_t& row_lo, int64_t& row_hi) {
+    const int item = u / gx;
+    int lo = 0, hi = E;   // e with s_first[e] <= item < s_first[e+1]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (s_first[mid] <= item) lo = mid; else hi = mid;
+    }
+    e = lo;
+    row_lo = (int64_t)offs[e] + (int64_t)(item - s_first[e]) * kBM;
+    const int64_t r_end = offs[e + 1];
+    row_hi = row_lo + kBM < r_end ? row_lo + kBM : r_end;
+  };
+  // XCD-contiguous numbering of the whole-tile units for any count: ids
+  // [0, 8 per) map one to one onto units, XCD x (id mod 8) taking units
+  // [x per, (x + 1) per); ids whose unit is past the last are skipped.
+  const int per = (full + 7) >> 3;
   int id = (int)blockIdx.x;
   tiles_mx_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, act_rows, N, K, Y, ldy, lds,
                          lds + 3 * kStageBytes, lut48, [&](IlTile& t) {
-                           int idp = total;
-                           while (idp >= total) {
+                           int u = full;
+                           while (u >= full) {
                              if (id >= 8 * per) return false;
-                             idp = (id & 7) * per + (id >> 3);
-                             id += (int)gridDim.x;
+                             u = (id & 7) * per + (id >> 3);
+                             id += G;
                            }
-                           const int item = idp / gx, xt = idp - item * gx;
-                           int lo = 0, hi = E;   // e with s_first[e] <= item < s_first[e+1]
-                           while (hi - lo > 1) {
-                             const int mid = (lo + hi) >> 1;
-                             if (s_first[mid] <= item) lo = mid; else hi = mid;
-                           }
-                           const int e = lo;
-                           t.row_lo = (int64_t)offs[e] + (int64_t)(item - s_first[e]) * kBM;
-                           const int64_t r_end = offs[e + 1];
-                           t.row_hi = t.row_lo + kBM < r_end ? t.row_lo + kBM : r_end;
+                           int e;
+                           locate(u, e, t.row_lo, t.row_hi);
                            t.r = il_row(row_index, t.row_lo, t.row_hi);
                            t.wc = wc + (int64_t)e * N * (K / 2);
                            t.ws = ws + (int64_t)e * N * (K / 32);
-                           t.n0 = xt * 256;
+                           t.n0 = (u % gx) * 256;
                            return true;
                          });
+  if ((int)blockIdx.x < halves) {
+    int u, h, e;
+    half_unit((int)blockIdx.x, full, halves, u, h);
+    int64_t row_lo, row_hi;
+    locate(u, e, row_lo, row_hi);
+    __syncthreads();   // the LDS stages are free before this tile's prologue
+    tile_mx_il<PAT, OutT, 4>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, row_index, act_rows, row_lo, row_hi,
+                             wc + (int64_t)e * N * (K / 2), ws + (int64_t)e * N * (K / 32), (u % gx) * 256 + 128 * h,
+                             N, K, Y, ldy, lds, lut48);
+  }
 }
 
 // ---------------------------------------------------------------------------
