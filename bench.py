@@ -406,38 +406,66 @@ def copy_same_bytes(torch, dev, stream, nbytes, reps=20):
 PROBE_ITERS = 2500               # ~1.7 ms of back-to-back MFMAs per probe launch
 
 
-def mfma_probe(torch, dev, stream, iters=PROBE_ITERS, reps=3):
-    """The sustained scaled-FP4 MFMA rate of this device (libsharq_probe.so:
-    four wavefronts per CU issuing independent 32x32x64 FP4 MFMAs), and the
-    shader clock the probe ran at (shader-clock cycles over 100 MHz real-time
-    ticks, averaged over the workgroups of the last launch).  This is the
-    executed-work ceiling of the two-path GEMM on the part as it runs under
-    that load, beside the published peak at the rated clock."""
+PROBES = {  # instruction: (entry point, flops per MFMA, description)
+    "fp4": ("sharq_probe_mfma_fp4", 2.0 * 32 * 32 * 64,
+            "back-to-back v_mfma_scale_f32_32x32x64_f8f6f4 (E2M1), 4 wavefronts x 8 accumulators per CU"),
+    "bf16": ("sharq_probe_mfma_bf16", 2.0 * 32 * 32 * 16,
+             "back-to-back v_mfma_f32_32x32x16_bf16, 4 wavefronts x 8 accumulators per CU"),
+}
+
+
+def mfma_probe(torch, dev, stream, iters=PROBE_ITERS, reps=3, kind="fp4"):
+    """The sustained MFMA rate of this device for one instruction
+    (libsharq_probe.so: four wavefronts per CU issuing independent 32x32 MFMAs
+    -- the scaled FP4 one the MXFP4 GEMM runs on, or the bf16 one of the NVFP4
+    and HiF4 GEMMs), and the shader clock the probe ran at (shader-clock
+    cycles over 100 MHz real-time ticks, averaged over the workgroups of the
+    last launch).  This is the executed-work ceiling of a GEMM on that
+    instruction on the part as it runs under that load, beside the published
+    peak at the rated clock."""
+    name, flops_per_mfma, desc = PROBES[kind]
+    peak = PEAK_FP4_TFLOPS if kind == "fp4" else PEAK_BF16_TFLOPS
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2606_26587_amd", "libsharq_probe.so"))
-    lib.sharq_probe_mfma_fp4.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
-                                         ctypes.c_void_p]
-    lib.sharq_probe_mfma_fp4.restype = ctypes.c_int
+    fn = getattr(lib, name)
+    fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
     cus = torch.cuda.get_device_properties(dev).multi_processor_count
     sink = torch.empty(cus * 256, dtype=torch.float32, device=dev)
     clk = torch.zeros(cus * 2, dtype=torch.int64, device=dev)
     ev = [HipEvent() for _ in range(reps + 2)]
     for i in range(reps + 1):   # launch 0 warms up
         ev[i].record(stream)
-        rc = lib.sharq_probe_mfma_fp4(iters, cus, sink.data_ptr(), clk.data_ptr(), stream.cuda_stream)
+        rc = fn(iters, cus, sink.data_ptr(), clk.data_ptr(), stream.cuda_stream)
         if rc != 0:
-            raise RuntimeError(f"sharq_probe_mfma_fp4 failed: {rc}")
+            raise RuntimeError(f"{name} failed: {rc}")
     ev[reps + 1].record(stream)
     torch.cuda.synchronize()
     us = sorted(ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(1, reps + 1))
     c = clk.view(cus, 2).cpu().numpy().astype(np.float64)
-    flops = cus * 4 * iters * 32 * 2.0 * 32 * 32 * 64
+    flops = cus * 4 * iters * 32 * flops_per_mfma
     med = us[len(us) // 2]
-    return {"kernel": "sharq_probe_mfma_fp4: back-to-back v_mfma_scale_f32_32x32x64_f8f6f4 (E2M1), "
-                      "4 wavefronts x 8 accumulators per CU",
+    return {"kernel": f"{name}: {desc}",
             "achieved": flops / (med * 1e-6) / 1e12, "unit": "TFLOP/s",
-            "frac_of_peak": flops / (med * 1e-6) / 1e12 / PEAK_FP4_TFLOPS,
+            "frac_of_peak": flops / (med * 1e-6) / 1e12 / peak,
             "clock_GHz": float(c[:, 0].sum() / c[:, 1].sum() * 0.1), "launch_us": us,
             "flops_per_launch": flops}
+
+
+def nv_roofline(torch, dev, stream, per, t_gemm):
+    """The NVFP4 GEMMs' roofline record: algorithmic and executed work against
+    the published bf16 peak and against the sustained bf16 MFMA rate measured
+    right after the timed steps."""
+    flops = sum(p["gemm_flops_alg"] for p in per)
+    f_exec = sum(p["gemm_flops_exec"] for p in per)
+    sus = mfma_probe(torch, dev, stream, kind="bf16")
+    log(f"[bench] bf16 MFMA probe: {sus['achieved']:.0f} TFLOP/s sustained at {sus['clock_GHz']:.2f} GHz; "
+        f"GEMM executed work at {f_exec / t_gemm / 1e12 / sus['achieved']:.2f} of it")
+    return {"bound": "mfma", "kernel": "k_linear_nv (bf16 MFMA over dequantized FP4)",
+            "achieved": flops / t_gemm / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": flops / t_gemm / 1e12 / PEAK_BF16_TFLOPS, "traffic": None, "flops": "F_alg",
+            "achieved_exec": f_exec / t_gemm / 1e12, "frac_exec": f_exec / t_gemm / 1e12 / PEAK_BF16_TFLOPS,
+            "sustained_mfma": sus, "frac_exec_of_sustained": f_exec / t_gemm / 1e12 / sus["achieved"],
+            "frac_alg_of_sustained": flops / t_gemm / 1e12 / sus["achieved"]}
 
 
 def llama_prefill(args, torch, S, synth, dev, stream):
@@ -570,9 +598,7 @@ def qwen_nvfp4(args, torch, S, synth, dev, stream):
                       flops / (ms_step * 1e-3) / 1e12, "TFLOP/s", ms_step, "nvfp4",
                       {"workload": "Qwen2.5-7B prefill linears gate_up (K3584,N37888,RMSNorm), down (K18944,N3584); "
                                    "M=4096; 2:4; NVFP4 with dynamic per-tensor scale", "tokens": T})
-    out["roofline"] = {"bound": "mfma", "kernel": "k_linear_nv (bf16 MFMA over dequantized FP4)",
-                       "achieved": flops / t_gemm / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                       "frac": flops / t_gemm / 1e12 / PEAK_BF16_TFLOPS, "traffic": None}
+    out["roofline"] = nv_roofline(torch, dev, stream, per, t_gemm)
     out["prep"] = {"bound": "hbm", "achieved": pb / t_prep / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                    "frac": pb / t_prep / 1e9 / PEAK_HBM_GBPS,
                    "note": "time includes the per-tensor amax pre-pass (a second read of X)"}
@@ -595,9 +621,7 @@ def llama_nvfp4_pairs(args, torch, S, synth, dev, stream):
                       flops / (ms_step * 1e-3) / 1e12, "TFLOP/s", ms_step, "nvfp4",
                       {"workload": "Llama-3.1-8B prefill linears qkv, gate_up (RMSNorm), down; M=2048; "
                                    "4:8 in pairs; NVFP4 with dynamic per-tensor scale", "tokens": T_TOKENS})
-    out["roofline"] = {"bound": "mfma", "kernel": "k_linear_nv (bf16 MFMA over dequantized FP4)",
-                       "achieved": flops / t_gemm / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                       "frac": flops / t_gemm / 1e12 / PEAK_BF16_TFLOPS, "traffic": None}
+    out["roofline"] = nv_roofline(torch, dev, stream, per, t_gemm)
     out["prep"] = {"bound": "hbm", "achieved": pb / t_prep / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                    "frac": pb / t_prep / 1e9 / PEAK_HBM_GBPS,
                    "note": "time includes the per-tensor amax pre-pass (a second read of X)"}

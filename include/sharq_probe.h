@@ -2,13 +2,14 @@
  * sharq_probe.h -- a measurement aid, not part of the SharQ method.
  *
  * libsharq_probe.so runs back-to-back scaled FP4 MFMAs
- * (v_mfma_scale_f32_32x32x64_f8f6f4, E2M1 operands, unit E8M0 scales) on
- * every SIMD of the device and records the shader clock.  The rate it reaches
- * is the sustained matrix-core ceiling that bounds the two-path FP4 GEMM
- * (whose backbone and residual products both run on this instruction): under
- * such load the part runs below its rated clock, so this ceiling sits below
- * the published dense FP4 peak.  The benchmark reports the GEMM's rate against
- * both.  Callers: the benchmark and its tests.
+ * (v_mfma_scale_f32_32x32x64_f8f6f4, E2M1 operands, unit E8M0 scales), or
+ * bf16 MFMAs, on every SIMD of the device and records the shader clock.  The
+ * rate it reaches is the sustained matrix-core ceiling that bounds a GEMM
+ * built on that instruction (the two-path MXFP4 GEMM on the FP4 one, the
+ * NVFP4 and HiF4 GEMMs on the bf16 one): under such load the part runs below
+ * its rated clock, so this ceiling sits below the published dense peak.  The
+ * benchmark reports each GEMM's rate against both.  Callers: the benchmark
+ * and its tests.
  */
 #ifndef SHARQ_PROBE_H
 #define SHARQ_PROBE_H
@@ -34,6 +35,14 @@ extern "C" {
  * pointer) or the launch error.
  */
 int sharq_probe_mfma_fp4(int iters, int workgroups, float* sink, unsigned long long* clk, hipStream_t stream);
+
+/*
+ * The same for the bf16 MFMA (v_mfma_f32_32x32x16_bf16, pseudo-random finite
+ * bf16 operands), the instruction the NVFP4 and HiF4 GEMMs run on: every
+ * wavefront issues iters x 32 independent MFMAs of 2 x 32 x 32 x 16 flops.
+ * Same arguments, outputs and errors as sharq_probe_mfma_fp4.
+ */
+int sharq_probe_mfma_bf16(int iters, int workgroups, float* sink, unsigned long long* clk, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -59,7 +59,64 @@ __global__ __launch_bounds__(256, 1) void k_mfma_fp4_rate(float* sink, unsigned 
   }
 }
 
+// The same for the bf16 MFMA (v_mfma_f32_32x32x16_bf16), which the NVFP4
+// and HiF4 GEMMs run on: pseudo-random finite bf16 operands (sign, exponent
+// 120..135, random mantissa), four sets cycled, 8 accumulators.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ bf16x8 bf16_operand(uint32_t seed) {
+  bf16x8 v;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t h = hash32(seed * 8u + (uint32_t)i);
+    const uint16_t bits = (uint16_t)((h & 0x807Fu) | ((120u + ((h >> 8) & 15u)) << 7));
+    v[i] = __builtin_bit_cast(__bf16, bits);
+  }
+  return v;
+}
+
+__global__ __launch_bounds__(256, 1) void k_mfma_bf16_rate(float* sink, unsigned long long* clk, int iters) {
+  const uint32_t g = blockIdx.x * 256u + threadIdx.x;
+  bf16x8 a[4], b[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    a[j] = bf16_operand(g * 8u + (uint32_t)j);
+    b[j] = bf16_operand(0x9E3779B9u ^ (g * 8u + (uint32_t)j));
+  }
+  v16f acc[8];
+#pragma unroll
+  for (int f = 0; f < 8; ++f)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[f][r] = 0.0f;
+  const uint64_t t0 = __builtin_amdgcn_s_memtime(), r0 = __builtin_amdgcn_s_memrealtime();
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int f = 0; f < 8; ++f) acc[f] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[j], b[(j + f) & 3], acc[f], 0, 0, 0);
+  }
+  const uint64_t t1 = __builtin_amdgcn_s_memtime(), r1 = __builtin_amdgcn_s_memrealtime();
+  float s = 0.0f;
+#pragma unroll
+  for (int f = 0; f < 8; ++f)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s += acc[f][r];
+  sink[g] = s;
+  if (threadIdx.x == 0) {
+    clk[2 * blockIdx.x] = t1 - t0;
+    clk[2 * blockIdx.x + 1] = r1 - r0;
+  }
+}
+
 }  // namespace
+
+extern "C" __attribute__((visibility("default"))) int sharq_probe_mfma_bf16(int iters, int workgroups, float* sink,
+                                                                            unsigned long long* clk,
+                                                                            hipStream_t stream) {
+  if (iters < 1 || workgroups < 1 || sink == nullptr || clk == nullptr) return (int)hipErrorInvalidValue;
+  k_mfma_bf16_rate<<<dim3((unsigned)workgroups), dim3(256), 0, stream>>>(sink, clk, iters);
+  return (int)hipGetLastError();
+}
 
 extern "C" __attribute__((visibility("default"))) int sharq_probe_mfma_fp4(int iters, int workgroups, float* sink,
                                                                            unsigned long long* clk,

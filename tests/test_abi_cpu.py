@@ -393,12 +393,13 @@ def test_probe_library_exports_and_rejects():
     """The benchmark's MFMA-rate probe library exports what its header
     declares and rejects bad arguments before any launch."""
     names = re.findall(r"\bint\s+(sharq_probe_\w+)\s*\(", open(PROBE_HEADER).read())
-    assert names == ["sharq_probe_mfma_fp4"]
+    assert names == ["sharq_probe_mfma_fp4", "sharq_probe_mfma_bf16"]
     P = ctypes.CDLL(PROBE_LIB)
-    for n in names:
-        assert hasattr(P, n), n
-    P.sharq_probe_mfma_fp4.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     fake = 1 << 20   # never dereferenced
     hip_invalid_value = 1
-    for iters, wgs, sink, clk in [(0, 1, fake, fake), (1, 0, fake, fake), (1, 1, None, fake), (1, 1, fake, None)]:
-        assert P.sharq_probe_mfma_fp4(iters, wgs, sink, clk, None) == hip_invalid_value
+    for n in names:
+        assert hasattr(P, n), n
+        fn = getattr(P, n)
+        fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        for iters, wgs, sink, clk in [(0, 1, fake, fake), (1, 0, fake, fake), (1, 1, None, fake), (1, 1, fake, None)]:
+            assert fn(iters, wgs, sink, clk, None) == hip_invalid_value, n
