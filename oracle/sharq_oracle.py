@@ -89,6 +89,15 @@ Readings where the paper is silent (each also listed in the design notes):
       E2M1 maximum; rounding s up to a power of two keeps every value within
       range (no clipping) at the price of the top binade.  It applies to both
       paths of the preparation and to the weight.
+
+Parity unpinned.  The paper prints no worked numeric example, and for these
+readings nothing it states decides between the choices, so their tests check
+invariants, range facts and exhibited differences, not values the paper
+fixes: the NVFP4 formula choices of R7 (pts_scale, nv_quantize: where S is
+applied and the fp32 division by d S); the pair score of R8 (the larger
+magnitude rather than the sum); the fp32 SF of R11 (hif4_quantize, rather
+than a bf16 intermediate); the SiLU.mul recipe of R12 (silu_mul_bf16, pinned
+to the exact product within one bf16 step, the recipe itself a choice).
 """
 
 from __future__ import annotations
@@ -314,7 +323,8 @@ def nm_pair_mask(y: np.ndarray, n: int, m: int) -> np.ndarray:
 
     score_i = max(|y_2i|, |y_2i+1|); pair i is kept iff
     #{j : score_j > score_i, or score_j == score_i and j < i} < n/2,
-    and a kept pair keeps both of its positions.
+    and a kept pair keeps both of its positions.  Parity unpinned in the
+    score (the larger magnitude rather than the sum).
     """
     y = np.asarray(y, dtype=np.float32)
     T, K = y.shape
@@ -370,7 +380,8 @@ def mx_quantize(vals: np.ndarray, present: np.ndarray | None = None, rule: str =
 # ---------------------------------------------------------------------------
 
 def pts_scale(amax: float) -> np.float32:
-    """Per-tensor scale S = fl32(amax / 2688), or 1 for an all-zero tensor."""
+    """Per-tensor scale S = fl32(amax / 2688), or 1 for an all-zero tensor.
+    Parity unpinned (reading R7)."""
     amax = np.float32(amax)
     if amax == 0:
         return np.float32(1.0)
@@ -379,6 +390,7 @@ def pts_scale(amax: float) -> np.float32:
 
 def nv_quantize(vals: np.ndarray, S: np.float32, block: int, present: np.ndarray | None = None):
     """NVFP4 quantization of rows in blocks of `block` along K under per-tensor scale S.
+    Parity unpinned (reading R7: where S is applied, the fp32 division).
 
     d_b = E4M3(fl32(amax_b / fl32(6 S))); code = E2M1(fl32(v / fl32(d_b S)));
     dequantized value fl32(fl32(q d_b) S).  A zero d_b gives signed-zero codes.
@@ -474,7 +486,7 @@ def s1p2_decode(codes) -> np.ndarray:
 
 def hif4_quantize(vals: np.ndarray, present: np.ndarray | None = None):
     """HiF4 quantization of rows in units of 64 along K (Algorithm
-    "bf16-to-hif4", reading R11).  `present` marks the positions of the tensor
+    "bf16-to-hif4", reading R11; parity unpinned in its fp32 SF).  `present` marks the positions of the tensor
     (the backbone's kept ones); the others count as zero and get code 0.
     Returns (codes uint8 [T,K], meta uint8 [T,K/64*4], deq fp32 [T,K])."""
     v = np.asarray(vals, dtype=np.float32)
@@ -816,7 +828,8 @@ def exp_nonpositive_f32(x: np.ndarray) -> np.ndarray:
 
 
 def silu_mul_bf16(gate_bf16: np.ndarray, up_bf16: np.ndarray) -> np.ndarray:
-    """h = bf16(SiLU(g) * u) by the fp32 recipe of reading R12: t = e^-|g|
+    """Parity unpinned (reading R12: the recipe is a choice).
+    h = bf16(SiLU(g) * u) by the fp32 recipe of reading R12: t = e^-|g|
     (exp_nonpositive_f32), q = fl(1 + t); s = fl(g / q) for g >= 0 and
     s = fl(fl(g t) / q) for g < 0 (SiLU(g) = g / (1 + e^-g) = g e^g / (1 + e^g)),
     with correctly rounded division; h = bf16(fl(s u)), nearest even.
