@@ -565,6 +565,60 @@ def test_persistent_tail_half_tiles(S, G, T, N, K, n, m):
     gemm_check(G.host(y32), O.linear(o, wo), O.linear_abs(o, wo), f"tail T{T}N{N}K{K}")
 
 
+@pytest.mark.parametrize("T,N,K", [(2176, 4000, 512),    # 272 tiles: 16 as half tiles; ragged last columns
+                                   (300, 520, 256)])      # ragged rows and columns, one round
+def test_persistent_bf16_row_pitch(S, G, T, N, K):
+    """The persistent kernel's LDS-staged bf16 epilogue writing into rows
+    longer than N (an output column slice): the range-checked stores land in
+    the slice only (the columns past N keep their sentinel), equal to the
+    contiguous fp32 output rounded, which matches the oracle."""
+    say(f"[pitch] T={T} N={N} K={K}")
+    x, g = synth.activations(T, K, seed=T + 7), synth.gamma(K, seed=7)
+    a = S.sharq_prepare(G.dev_bf16(x), G.dev_bf16(g), 1e-6, 2, 4, "mx",
+                        out=S.alloc_act(T, K, 2, 4, "mx", "cuda", dense_only=True))
+    wq = S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=N)))
+    pitch = N + 96
+    big = torch.full((T + 1, pitch), 3.0, dtype=torch.bfloat16, device="cuda")
+    y32 = S.sharq_linear(a, wq, dtype=torch.float32)
+    S.sharq_linear(a, wq, out=big[:T, :N])
+    torch.cuda.synchronize()
+    assert torch.equal(big[:T, :N], y32.to(torch.bfloat16))
+    assert torch.all(big[:T, N:] == 3.0) and torch.all(big[T] == 3.0), "stores outside the slice"
+    o = O.prepare(x, g, 1e-6, 2, 4, "mx")
+    wo = G.weight_to_oracle(wq)
+    rows = np.unique(np.concatenate([np.arange(0, T, max(1, T // 256)), [T - 1]]))
+    gemm_check(G.host(y32)[rows], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), f"pitch T{T}N{N}")
+
+
+def test_grouped_bf16_row_pitch(S, G):
+    """The grouped kernel's bf16 epilogue into rows longer than N, whole and
+    half tiles (few units: every unit runs as two halves), ragged expert
+    slices: the slice equals the contiguous fp32 output rounded, and nothing
+    outside it is written."""
+    T, E, topk, K, N = 300, 5, 3, 512, 200
+    x = synth.activations(T, K, seed=11)
+    o = O.prepare(x, synth.gamma(K, seed=11), 1e-6, 4, 8, "mx")
+    wos = [O.quantize_weight(synth.weight(N, K, seed=300 + e), "mx") for e in range(E)]
+    row_index, offs = synth.router_topk(T, E, topk, seed=11)
+    total = int(offs[-1])
+    a = G.oracle_to_act(o, dense_backbone=True)
+    w = S.stack_weights([G.oracle_to_weight(wo) for wo in wos])
+    ri, of = torch.from_numpy(row_index).cuda(), torch.from_numpy(offs).cuda()
+    y32 = S.sharq_linear_grouped(a, ri, of, total, w, dtype=torch.float32)
+    big = torch.full((total + 1, N + 40), 3.0, dtype=torch.bfloat16, device="cuda")
+    S.sharq_linear_grouped(a, ri, of, total, w, out=big[:total, :N])
+    torch.cuda.synchronize()
+    assert torch.equal(big[:total, :N], y32.to(torch.bfloat16))
+    assert torch.all(big[:total, N:] == 3.0) and torch.all(big[total] == 3.0), "stores outside the slice"
+    ref = O.linear_grouped(o, row_index, offs, wos)
+    yabs = np.zeros_like(ref)
+    for e in range(E):
+        lo, hi = offs[e], offs[e + 1]
+        if hi > lo:
+            yabs[lo:hi] = O.linear_abs(o, wos[e], rows=row_index[lo:hi])
+    gemm_check(G.host(y32), ref, yabs, "grouped pitch")
+
+
 # --------------------------------------------------------------------------- dense backbone copy
 
 @pytest.mark.parametrize("T,K,N,use_gamma,n,m,pairs", [(300, 1024, 512, True, 2, 4, False),
