@@ -198,33 +198,39 @@ __device__ __forceinline__ uint32_t keep_bits(uint32_t meta) {
 
 // 4:8 selection on one group of 8: of p < q, p beats q iff |y_p| >= |y_q|
 // (a tie goes to the lower index), and a position survives iff it beats at
-// least 4 of the other 7.  One comparison per pair counts on both sides in
-// per-lane integers (beats[p] starts at p: the lower positions, which it
-// beats unless they beat them).  Returns the 8-bit keep mask and b = y where
-// kept, +0 where dropped.
+// least 4 of the other 7.  One comparison per pair counts on both sides
+// (beats[p] starts at p: the lower positions, which it beats unless they
+// beat it), the eight counts held as the nibbles of one word.  Returns the
+// 8-bit keep mask and b = y where kept, +0 where dropped.
 __device__ __forceinline__ uint32_t select48(const float* e, float (&b)[8]) {
   float a[8];
-  int beats[8];
 #pragma unroll
-  for (int p = 0; p < 8; ++p) {
-    a[p] = fabsf(e[p]);
-    beats[p] = p;
-  }
+  for (int p = 0; p < 8; ++p) a[p] = fabsf(e[p]);
+  // the eight counts as the nibbles of one word (nibble p = beats[p], 0..7 at
+  // every point, so no nibble borrows or carries); a decided pair adds +1 to
+  // nibble p and -1 to nibble q in one constant, two pairs per add
+  uint32_t W = 0x76543210u, pend = 0u;
+  int n = 0;
 #pragma unroll
   for (int p = 0; p < 8; ++p)
 #pragma unroll
     for (int q = p + 1; q < 8; ++q) {
-      const int c = a[p] >= a[q];
-      beats[p] += c;
-      beats[q] -= c;
+      const uint32_t d = a[p] >= a[q] ? (1u << (4 * p)) - (1u << (4 * q)) : 0u;
+      if (++n & 1) {
+        pend = d;
+      } else {
+        W += pend + d;
+      }
     }
-  uint32_t mask = 0u;
+  // 28 pairs: every increment added.  Position p survives iff bit 2 of its
+  // nibble is set (beats[p] >= 4).
+  uint32_t m = (W >> 2) & 0x11111111u;
+  m = (m | (m >> 3)) & 0x03030303u;
+  m = (m | (m >> 6)) & 0x000F000Fu;
+  const uint32_t mask = (m | (m >> 12)) & 0xFFu;
 #pragma unroll
-  for (int p = 0; p < 8; ++p) {
-    const uint32_t kb = (uint32_t)beats[p] >> 2;   // 1 iff beats[p] >= 4 (beats[p] <= 7)
-    mask |= kb << p;
-    b[p] = __uint_as_float(__float_as_uint(e[p]) & (0u - kb));
-  }
+  for (int p = 0; p < 8; ++p)
+    b[p] = __uint_as_float(__float_as_uint(e[p]) & (uint32_t)((int32_t)(W << (29 - 4 * p)) >> 31));
   return mask;
 }
 
