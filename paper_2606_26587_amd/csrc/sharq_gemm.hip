@@ -1851,13 +1851,13 @@ __global__ __launch_bounds__(256) void k_linear_nv(const uint8_t* sp_codes, cons
 // Interleaved NVFP4 main loop (K a multiple of 128)
 // ---------------------------------------------------------------------------
 //
-// The same slot schedule as the MXFP4 loop, on v_mfma_f32_32x32x16_bf16 with
+// The same slot schedule as the MXFP4 loop, on v_mfma_f32_32x32x16_f16 with
 // the weight as first operand (each lane then owns an output row).  One K
 // step is one 32-position block: two 16-position MFMA sub-steps t, where lane
 // half h supplies positions 16 h + 8 t + 0..7 -- so a lane needs only its
 // half of each block (one residual scale, 8 bytes of residual codes, half the
 // backbone).  Between the step's 32 MFMAs run the weight reads of sub-step 1,
-// the bf16 dequantization of the next step's activations, the dequantization
+// the fp16 dequantization of the next step's activations, the dequantization
 // and LDS store of the weight two steps ahead (three LDS stages) and the
 // reads of the next step's first weight operands.
 
@@ -1868,7 +1868,7 @@ struct NvRaw {          // this lane's raw activation data of one step
   uint32_t ssc, dsc;    // backbone and residual E4M3 scales (bytes)
 };
 
-struct NvOps {          // MFMA-ready bf16 operands of one step
+struct NvOps {          // MFMA-ready fp16 operands of one step
   uint4 sp[2], dn[2];
 };
 
@@ -1877,14 +1877,35 @@ struct NvWRaw {         // one weight row of one step
   uint32_t sc;
 };
 
-constexpr int kNvStage = 256 * 64;   // bf16 weight tile of one step: 256 rows x 32 positions
+constexpr int kNvStage = 256 * 64;   // fp16 weight tile of one step: 256 rows x 32 positions
 
-// Pieces of the exact bf16 dequantization q * d: codes byte SEL (two E2M1
-// values, lower position in the low nibble) -> one packed bf16 pair.
+// Pieces of the exact dequantization q * d in fp16: codes byte SEL (two
+// E2M1 values, lower position in the low nibble) -> one packed fp16 pair.
+// Every such product is exact in fp16: q has at most 2 significant bits and
+// |q| <= 6, an E4M3 scale d has at most 4 and lies in [2^-9, 448], so q d has
+// at most 6 significant bits and lies in [2^-10, 2688], inside fp16's normal
+// range.  The FP4 pair is decoded to fp16 and scaled by one packed fp16
+// multiply (two values per instruction), half the work of decoding to fp32,
+// scaling and packing to bf16.
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ f16x8 as_f16x8(uint4 q) {
+  f16x8 v;
+  __builtin_memcpy(&v, &q, 16);
+  return v;
+}
+
+// an E4M3 scale as an fp16 pair (exact)
+__device__ __forceinline__ f16x2 nv_scale2(uint32_t code) {
+  const _Float16 h = (_Float16)e4m3_value(code);
+  return f16x2{h, h};
+}
+
 template <int SEL>
-__device__ __forceinline__ uint32_t bf16_pair(uint32_t codes, float d) {
-  const v2f v = fp4x2_decode<SEL>(codes);
-  return __builtin_amdgcn_perm(__float_as_uint(v.y * d), __float_as_uint(v.x * d), 0x07060302u);
+__device__ __forceinline__ uint32_t f16_pair(uint32_t codes, f16x2 d) {
+  const f16x2 v = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, 1.0f, SEL);
+  return __builtin_bit_cast(uint32_t, v * d);
 }
 
 __device__ __forceinline__ void nv_load_a(NvRaw& s, const ARow& a, int ks, int half) {
@@ -1915,7 +1936,7 @@ __device__ __forceinline__ void nv_read_b(uint4 (&b)[8], const uint8_t* lw, int 
 
 template <int SUB, int F>
 __device__ __forceinline__ void nv_mma(v16f (&acc)[8], const uint4& a, const uint4 (&b)[8]) {
-  acc[F] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(b[F]), as_bf16x8(a), acc[F], 0, 0, 0);
+  acc[F] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_f16x8(b[F]), as_f16x8(a), acc[F], 0, 0, 0);
 }
 
 template <int PAT, class Issue>
@@ -1928,61 +1949,61 @@ __device__ __forceinline__ void nv_step(v16f (&acc)[8], const NvOps& ops, uint4 
   SHARQ_FENCE();
   // next step's activations: backbone expanded to 16 codes, then dequantized
   // (their scales decoded behind the first two MFMAs)
-  float dsp, ddn;
+  f16x2 dsp, ddn;
   uint32_t e0 = 0u, e1 = 0u;
   const uint2 cw = make_uint2(raw.spc, 0u);
   // ---- sub-step 0, backbone
-  nv_mma<0, 0>(acc, ops.sp[0], b0); nv_read_b<1, 0, 1>(b1, cur, lane); dsp = e4m3_value(raw.ssc); SHARQ_FENCE();
-  nv_mma<0, 1>(acc, ops.sp[0], b0); nv_read_b<1, 1, 2>(b1, cur, lane); ddn = e4m3_value(raw.dsc);
+  nv_mma<0, 0>(acc, ops.sp[0], b0); nv_read_b<1, 0, 1>(b1, cur, lane); dsp = nv_scale2(raw.ssc); SHARQ_FENCE();
+  nv_mma<0, 1>(acc, ops.sp[0], b0); nv_read_b<1, 1, 2>(b1, cur, lane); ddn = nv_scale2(raw.dsc);
   e0 = expand_dw<PAT, 0>(cw, raw.spm); SHARQ_FENCE();
   nv_mma<0, 2>(acc, ops.sp[0], b0); nv_read_b<1, 2, 3>(b1, cur, lane); SHARQ_FENCE();
   nv_mma<0, 3>(acc, ops.sp[0], b0); nv_read_b<1, 3, 4>(b1, cur, lane); e1 = expand_dw<PAT, 1>(cw, raw.spm); SHARQ_FENCE();
   nv_mma<0, 4>(acc, ops.sp[0], b0); nv_read_b<1, 4, 5>(b1, cur, lane);
-  opsn.sp[0].x = bf16_pair<0>(e0, dsp); opsn.sp[0].y = bf16_pair<1>(e0, dsp); SHARQ_FENCE();
+  opsn.sp[0].x = f16_pair<0>(e0, dsp); opsn.sp[0].y = f16_pair<1>(e0, dsp); SHARQ_FENCE();
   nv_mma<0, 5>(acc, ops.sp[0], b0); nv_read_b<1, 5, 6>(b1, cur, lane);
-  opsn.sp[0].z = bf16_pair<2>(e0, dsp); opsn.sp[0].w = bf16_pair<3>(e0, dsp); SHARQ_FENCE();
+  opsn.sp[0].z = f16_pair<2>(e0, dsp); opsn.sp[0].w = f16_pair<3>(e0, dsp); SHARQ_FENCE();
   nv_mma<0, 6>(acc, ops.sp[0], b0); nv_read_b<1, 6, 7>(b1, cur, lane);
-  opsn.sp[1].x = bf16_pair<0>(e1, dsp); opsn.sp[1].y = bf16_pair<1>(e1, dsp); SHARQ_FENCE();
+  opsn.sp[1].x = f16_pair<0>(e1, dsp); opsn.sp[1].y = f16_pair<1>(e1, dsp); SHARQ_FENCE();
   nv_mma<0, 7>(acc, ops.sp[0], b0); nv_read_b<1, 7, 8>(b1, cur, lane);
-  opsn.sp[1].z = bf16_pair<2>(e1, dsp); opsn.sp[1].w = bf16_pair<3>(e1, dsp); SHARQ_FENCE();
+  opsn.sp[1].z = f16_pair<2>(e1, dsp); opsn.sp[1].w = f16_pair<3>(e1, dsp); SHARQ_FENCE();
   // ---- sub-step 0, residual
   nv_mma<0, 0>(acc, ops.dn[0], b0);
-  opsn.dn[0].x = bf16_pair<0>(raw.dn.x, ddn); opsn.dn[0].y = bf16_pair<1>(raw.dn.x, ddn); SHARQ_FENCE();
+  opsn.dn[0].x = f16_pair<0>(raw.dn.x, ddn); opsn.dn[0].y = f16_pair<1>(raw.dn.x, ddn); SHARQ_FENCE();
   nv_mma<0, 1>(acc, ops.dn[0], b0);
-  opsn.dn[0].z = bf16_pair<2>(raw.dn.x, ddn); opsn.dn[0].w = bf16_pair<3>(raw.dn.x, ddn); SHARQ_FENCE();
+  opsn.dn[0].z = f16_pair<2>(raw.dn.x, ddn); opsn.dn[0].w = f16_pair<3>(raw.dn.x, ddn); SHARQ_FENCE();
   nv_mma<0, 2>(acc, ops.dn[0], b0);
-  opsn.dn[1].x = bf16_pair<0>(raw.dn.y, ddn); opsn.dn[1].y = bf16_pair<1>(raw.dn.y, ddn); SHARQ_FENCE();
+  opsn.dn[1].x = f16_pair<0>(raw.dn.y, ddn); opsn.dn[1].y = f16_pair<1>(raw.dn.y, ddn); SHARQ_FENCE();
   nv_mma<0, 3>(acc, ops.dn[0], b0);
-  opsn.dn[1].z = bf16_pair<2>(raw.dn.y, ddn); opsn.dn[1].w = bf16_pair<3>(raw.dn.y, ddn); SHARQ_FENCE();
+  opsn.dn[1].z = f16_pair<2>(raw.dn.y, ddn); opsn.dn[1].w = f16_pair<3>(raw.dn.y, ddn); SHARQ_FENCE();
   // the weight row two steps ahead: dequantized into the other stage, each
   // 16-byte part over two slots (4 values per slot)
-  const float dw = e4m3_value(wst.sc);
+  const f16x2 dw = nv_scale2(wst.sc);
   const int wrow = tid;
   uint32_t wx, wy;
   nv_mma<0, 4>(acc, ops.dn[0], b0);
-  wx = bf16_pair<0>(wst.codes.x, dw); wy = bf16_pair<1>(wst.codes.x, dw); SHARQ_FENCE();
+  wx = f16_pair<0>(wst.codes.x, dw); wy = f16_pair<1>(wst.codes.x, dw); SHARQ_FENCE();
   nv_mma<0, 5>(acc, ops.dn[0], b0);
   *reinterpret_cast<uint4*>(wr + wrow * 64 + 16 * (0 ^ swz_nv(wrow))) =
-      make_uint4(wx, wy, bf16_pair<2>(wst.codes.x, dw), bf16_pair<3>(wst.codes.x, dw));
+      make_uint4(wx, wy, f16_pair<2>(wst.codes.x, dw), f16_pair<3>(wst.codes.x, dw));
   SHARQ_FENCE();
   nv_mma<0, 6>(acc, ops.dn[0], b0);
-  wx = bf16_pair<0>(wst.codes.y, dw); wy = bf16_pair<1>(wst.codes.y, dw); SHARQ_FENCE();
+  wx = f16_pair<0>(wst.codes.y, dw); wy = f16_pair<1>(wst.codes.y, dw); SHARQ_FENCE();
   nv_mma<0, 7>(acc, ops.dn[0], b0);
   *reinterpret_cast<uint4*>(wr + wrow * 64 + 16 * (1 ^ swz_nv(wrow))) =
-      make_uint4(wx, wy, bf16_pair<2>(wst.codes.y, dw), bf16_pair<3>(wst.codes.y, dw));
+      make_uint4(wx, wy, f16_pair<2>(wst.codes.y, dw), f16_pair<3>(wst.codes.y, dw));
   SHARQ_FENCE();
   // ---- sub-step 1, backbone
   nv_mma<1, 0>(acc, ops.sp[1], b1);
-  wx = bf16_pair<0>(wst.codes.z, dw); wy = bf16_pair<1>(wst.codes.z, dw); SHARQ_FENCE();
+  wx = f16_pair<0>(wst.codes.z, dw); wy = f16_pair<1>(wst.codes.z, dw); SHARQ_FENCE();
   nv_mma<1, 1>(acc, ops.sp[1], b1);
   *reinterpret_cast<uint4*>(wr + wrow * 64 + 16 * (2 ^ swz_nv(wrow))) =
-      make_uint4(wx, wy, bf16_pair<2>(wst.codes.z, dw), bf16_pair<3>(wst.codes.z, dw));
+      make_uint4(wx, wy, f16_pair<2>(wst.codes.z, dw), f16_pair<3>(wst.codes.z, dw));
   SHARQ_FENCE();
   nv_mma<1, 2>(acc, ops.sp[1], b1);
-  wx = bf16_pair<0>(wst.codes.w, dw); wy = bf16_pair<1>(wst.codes.w, dw); SHARQ_FENCE();
+  wx = f16_pair<0>(wst.codes.w, dw); wy = f16_pair<1>(wst.codes.w, dw); SHARQ_FENCE();
   nv_mma<1, 3>(acc, ops.sp[1], b1);
   *reinterpret_cast<uint4*>(wr + wrow * 64 + 16 * (3 ^ swz_nv(wrow))) =
-      make_uint4(wx, wy, bf16_pair<2>(wst.codes.w, dw), bf16_pair<3>(wst.codes.w, dw));
+      make_uint4(wx, wy, f16_pair<2>(wst.codes.w, dw), f16_pair<3>(wst.codes.w, dw));
   SHARQ_FENCE();
   nv_mma<1, 4>(acc, ops.sp[1], b1); SHARQ_FENCE();
   nv_mma<1, 5>(acc, ops.sp[1], b1); SHARQ_FENCE();
@@ -2001,25 +2022,25 @@ __device__ __forceinline__ void nv_step(v16f (&acc)[8], const NvOps& ops, uint4 
 
 template <int PAT>
 __device__ __forceinline__ void nv_ops_from_raw(NvOps& o, const NvRaw& r) {
-  const float dsp = e4m3_value(r.ssc), ddn = e4m3_value(r.dsc);
+  const f16x2 dsp = nv_scale2(r.ssc), ddn = nv_scale2(r.dsc);
   const uint2 cw = make_uint2(r.spc, 0u);
   const uint32_t e0 = expand_dw<PAT, 0>(cw, r.spm), e1 = expand_dw<PAT, 1>(cw, r.spm);
-  o.sp[0] = make_uint4(bf16_pair<0>(e0, dsp), bf16_pair<1>(e0, dsp), bf16_pair<2>(e0, dsp), bf16_pair<3>(e0, dsp));
-  o.sp[1] = make_uint4(bf16_pair<0>(e1, dsp), bf16_pair<1>(e1, dsp), bf16_pair<2>(e1, dsp), bf16_pair<3>(e1, dsp));
-  o.dn[0] = make_uint4(bf16_pair<0>(r.dn.x, ddn), bf16_pair<1>(r.dn.x, ddn), bf16_pair<2>(r.dn.x, ddn),
-                       bf16_pair<3>(r.dn.x, ddn));
-  o.dn[1] = make_uint4(bf16_pair<0>(r.dn.y, ddn), bf16_pair<1>(r.dn.y, ddn), bf16_pair<2>(r.dn.y, ddn),
-                       bf16_pair<3>(r.dn.y, ddn));
+  o.sp[0] = make_uint4(f16_pair<0>(e0, dsp), f16_pair<1>(e0, dsp), f16_pair<2>(e0, dsp), f16_pair<3>(e0, dsp));
+  o.sp[1] = make_uint4(f16_pair<0>(e1, dsp), f16_pair<1>(e1, dsp), f16_pair<2>(e1, dsp), f16_pair<3>(e1, dsp));
+  o.dn[0] = make_uint4(f16_pair<0>(r.dn.x, ddn), f16_pair<1>(r.dn.x, ddn), f16_pair<2>(r.dn.x, ddn),
+                       f16_pair<3>(r.dn.x, ddn));
+  o.dn[1] = make_uint4(f16_pair<0>(r.dn.y, ddn), f16_pair<1>(r.dn.y, ddn), f16_pair<2>(r.dn.y, ddn),
+                       f16_pair<3>(r.dn.y, ddn));
 }
 
 __device__ __forceinline__ void nv_store_w(const NvWRaw& w, uint8_t* stage) {
   const int row = threadIdx.x;
-  const float d = e4m3_value(w.sc);
+  const f16x2 d = nv_scale2(w.sc);
   const uint32_t c[4] = {w.codes.x, w.codes.y, w.codes.z, w.codes.w};
 #pragma unroll
   for (int q = 0; q < 4; ++q)
     *reinterpret_cast<uint4*>(stage + row * 64 + 16 * (q ^ swz_nv(row))) =
-        make_uint4(bf16_pair<0>(c[q], d), bf16_pair<1>(c[q], d), bf16_pair<2>(c[q], d), bf16_pair<3>(c[q], d));
+        make_uint4(f16_pair<0>(c[q], d), f16_pair<1>(c[q], d), f16_pair<2>(c[q], d), f16_pair<3>(c[q], d));
 }
 
 template <int PAT, typename OutT>
