@@ -66,7 +66,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 
 METRIC = "SharQ linear TFLOPS (prep+2 FP4 GEMMs) & prep HBM GB/s, Llama-8B M=2048"
 PEAK_FP4_TFLOPS = 10100.0     # MI355X dense MXFP4 MFMA
-PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 (and fp16) MFMA
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
 T_TOKENS = 2048
 N_INPUT_SETS = 2              # activations rotate between steps (defeats the 256 MB last-level cache)
@@ -411,14 +411,16 @@ PROBES = {  # instruction: (entry point, flops per MFMA, description)
             "back-to-back v_mfma_scale_f32_32x32x64_f8f6f4 (E2M1), 4 wavefronts x 8 accumulators per CU"),
     "bf16": ("sharq_probe_mfma_bf16", 2.0 * 32 * 32 * 16,
              "back-to-back v_mfma_f32_32x32x16_bf16, 4 wavefronts x 8 accumulators per CU"),
+    "f16": ("sharq_probe_mfma_f16", 2.0 * 32 * 32 * 16,
+            "back-to-back v_mfma_f32_32x32x16_f16, 4 wavefronts x 8 accumulators per CU"),
 }
 
 
 def mfma_probe(torch, dev, stream, iters=PROBE_ITERS, reps=3, kind="fp4"):
     """The sustained MFMA rate of this device for one instruction
     (libsharq_probe.so: four wavefronts per CU issuing independent 32x32 MFMAs
-    -- the scaled FP4 one the MXFP4 GEMM runs on, or the bf16 one of the NVFP4
-    and HiF4 GEMMs), and the shader clock the probe ran at (shader-clock
+    -- the scaled FP4 one the MXFP4 GEMM runs on, the fp16 one of the NVFP4
+    GEMM, or the bf16 one of the HiF4 GEMM), and the shader clock the probe ran at (shader-clock
     cycles over 100 MHz real-time ticks, averaged over the workgroups of the
     last launch).  This is the executed-work ceiling of a GEMM on that
     instruction on the part as it runs under that load, beside the published
@@ -453,14 +455,15 @@ def mfma_probe(torch, dev, stream, iters=PROBE_ITERS, reps=3, kind="fp4"):
 
 def nv_roofline(torch, dev, stream, per, t_gemm):
     """The NVFP4 GEMMs' roofline record: algorithmic and executed work against
-    the published bf16 peak and against the sustained bf16 MFMA rate measured
-    right after the timed steps."""
+    the published 16-bit peak and against the sustained fp16 MFMA rate (the
+    instruction the NVFP4 GEMM runs on for these K) measured right after the
+    timed steps."""
     flops = sum(p["gemm_flops_alg"] for p in per)
     f_exec = sum(p["gemm_flops_exec"] for p in per)
-    sus = mfma_probe(torch, dev, stream, kind="bf16")
-    log(f"[bench] bf16 MFMA probe: {sus['achieved']:.0f} TFLOP/s sustained at {sus['clock_GHz']:.2f} GHz; "
+    sus = mfma_probe(torch, dev, stream, kind="f16")
+    log(f"[bench] fp16 MFMA probe: {sus['achieved']:.0f} TFLOP/s sustained at {sus['clock_GHz']:.2f} GHz; "
         f"GEMM executed work at {f_exec / t_gemm / 1e12 / sus['achieved']:.2f} of it")
-    return {"bound": "mfma", "kernel": "k_linear_nv (bf16 MFMA over dequantized FP4)",
+    return {"bound": "mfma", "kernel": "k_linear_nv_il (fp16 MFMA over dequantized FP4)",
             "achieved": flops / t_gemm / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": flops / t_gemm / 1e12 / PEAK_BF16_TFLOPS, "traffic": None, "flops": "F_alg",
             "achieved_exec": f_exec / t_gemm / 1e12, "frac_exec": f_exec / t_gemm / 1e12 / PEAK_BF16_TFLOPS,

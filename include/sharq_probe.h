@@ -3,10 +3,11 @@
  *
  * libsharq_probe.so runs back-to-back scaled FP4 MFMAs
  * (v_mfma_scale_f32_32x32x64_f8f6f4, E2M1 operands, unit E8M0 scales), or
- * bf16 MFMAs, on every SIMD of the device and records the shader clock.  The
- * rate it reaches is the sustained matrix-core ceiling that bounds a GEMM
- * built on that instruction (the two-path MXFP4 GEMM on the FP4 one, the
- * NVFP4 and HiF4 GEMMs on the bf16 one): under such load the part runs below
+ * bf16 or fp16 MFMAs, on every SIMD of the device and records the shader
+ * clock.  The rate it reaches is the sustained matrix-core ceiling that bounds
+ * a GEMM built on that instruction (the two-path MXFP4 GEMM on the FP4 one,
+ * the NVFP4 GEMM on the fp16 one, the HiF4 GEMM and the NVFP4 GEMM for K not a
+ * multiple of 64 on the bf16 one): under such load the part runs below
  * its rated clock, so this ceiling sits below the published dense peak.  The
  * benchmark reports each GEMM's rate against both.  Callers: the benchmark
  * and its tests.
@@ -38,11 +39,19 @@ int sharq_probe_mfma_fp4(int iters, int workgroups, float* sink, unsigned long l
 
 /*
  * The same for the bf16 MFMA (v_mfma_f32_32x32x16_bf16, pseudo-random finite
- * bf16 operands), the instruction the NVFP4 and HiF4 GEMMs run on: every
- * wavefront issues iters x 32 independent MFMAs of 2 x 32 x 32 x 16 flops.
- * Same arguments, outputs and errors as sharq_probe_mfma_fp4.
+ * bf16 operands), the instruction the HiF4 GEMM and the NVFP4 GEMM for K not
+ * a multiple of 64 run on: every wavefront issues iters x 32 independent
+ * MFMAs of 2 x 32 x 32 x 16 flops.  Same arguments, outputs and errors as
+ * sharq_probe_mfma_fp4.
  */
 int sharq_probe_mfma_bf16(int iters, int workgroups, float* sink, unsigned long long* clk, hipStream_t stream);
+
+/*
+ * The same for the fp16 MFMA (v_mfma_f32_32x32x16_f16, pseudo-random finite
+ * fp16 operands), the instruction of the NVFP4 GEMM for K a multiple of 64.
+ * Same arguments, outputs and errors as sharq_probe_mfma_fp4.
+ */
+int sharq_probe_mfma_f16(int iters, int workgroups, float* sink, unsigned long long* clk, hipStream_t stream);
 
 #ifdef __cplusplus
 }

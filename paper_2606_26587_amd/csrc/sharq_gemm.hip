@@ -18,7 +18,8 @@
 // expansion.  The shared weight tile (E2M1 payload + E8M0 scales) is staged
 // through LDS once per K step and read by both MFMAs of every fragment.
 // Also here: the small-M kernel for decode, the grouped (MoE) form, the
-// NVFP4 and HiF4 kernels on bf16 MFMA over exactly dequantized operands, and
+// NVFP4 and HiF4 kernels on 16-bit MFMA over exactly dequantized operands
+// (fp16 in the NVFP4 kernel for K a multiple of 64, bf16 elsewhere), and
 // the generic kernels of the ablation path combinations.
 
 // MFMA 32x32x64 FP4 operand layout (lane l, 64-wide wavefront): lane l holds
@@ -2144,8 +2145,8 @@ static int device_cus();   // compute units of the current device (host launcher
 
 // Persistent: at most one workgroup per CU walks the tiles b, b + G, ... in
 // the XCD-aware order of tile_at (any grid: the Qwen2.5-7B shapes have 148
-// and 14 column tiles; measured neutral there, where the bf16 MFMA work
-// bounds the kernel).
+// and 14 column tiles; measured neutral there, where the dequantization and
+// MFMA work bound the kernel).
 template <int PAT, typename OutT>
 __global__ __launch_bounds__(256) void k_linear_nv_il(const uint8_t* sp_codes, const uint8_t* sp_meta,
                                                       const uint8_t* sp_scale, const uint8_t* dn_codes,

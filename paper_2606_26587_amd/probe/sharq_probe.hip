@@ -59,29 +59,39 @@ __global__ __launch_bounds__(256, 1) void k_mfma_fp4_rate(float* sink, unsigned 
   }
 }
 
-// The same for the bf16 MFMA (v_mfma_f32_32x32x16_bf16), which the NVFP4
-// and HiF4 GEMMs run on: pseudo-random finite bf16 operands (sign, exponent
-// 120..135, random mantissa), four sets cycled, 8 accumulators.
+// The same for the 16-bit MFMAs (v_mfma_f32_32x32x16_bf16 / _f16), which the
+// NVFP4 and HiF4 GEMMs run on: pseudo-random finite operands (sign, exponent
+// 2^-7..2^8, random mantissa), four sets cycled, 8 accumulators.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
-__device__ __forceinline__ bf16x8 bf16_operand(uint32_t seed) {
-  bf16x8 v;
+template <typename V, typename E>
+__device__ __forceinline__ V operand16(uint32_t seed) {
+  V v;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const uint32_t h = hash32(seed * 8u + (uint32_t)i);
-    const uint16_t bits = (uint16_t)((h & 0x807Fu) | ((120u + ((h >> 8) & 15u)) << 7));
-    v[i] = __builtin_bit_cast(__bf16, bits);
+    const float x = __uint_as_float((h & 0x807FFFFFu) | ((120u + ((h >> 23) & 15u)) << 23));
+    v[i] = (E)x;
   }
   return v;
 }
 
-__global__ __launch_bounds__(256, 1) void k_mfma_bf16_rate(float* sink, unsigned long long* clk, int iters) {
+__device__ __forceinline__ v16f mfma16(bf16x8 a, bf16x8 b, v16f c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ v16f mfma16(f16x8 a, f16x8 b, v16f c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+template <typename V, typename E>
+__global__ __launch_bounds__(256, 1) void k_mfma16_rate(float* sink, unsigned long long* clk, int iters) {
   const uint32_t g = blockIdx.x * 256u + threadIdx.x;
-  bf16x8 a[4], b[4];
+  V a[4], b[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    a[j] = bf16_operand(g * 8u + (uint32_t)j);
-    b[j] = bf16_operand(0x9E3779B9u ^ (g * 8u + (uint32_t)j));
+    a[j] = operand16<V, E>(g * 8u + (uint32_t)j);
+    b[j] = operand16<V, E>(0x9E3779B9u ^ (g * 8u + (uint32_t)j));
   }
   v16f acc[8];
 #pragma unroll
@@ -93,7 +103,7 @@ __global__ __launch_bounds__(256, 1) void k_mfma_bf16_rate(float* sink, unsigned
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int f = 0; f < 8; ++f) acc[f] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[j], b[(j + f) & 3], acc[f], 0, 0, 0);
+      for (int f = 0; f < 8; ++f) acc[f] = mfma16(a[j], b[(j + f) & 3], acc[f]);
   }
   const uint64_t t1 = __builtin_amdgcn_s_memtime(), r1 = __builtin_amdgcn_s_memrealtime();
   float s = 0.0f;
@@ -114,7 +124,15 @@ extern "C" __attribute__((visibility("default"))) int sharq_probe_mfma_bf16(int 
                                                                             unsigned long long* clk,
                                                                             hipStream_t stream) {
   if (iters < 1 || workgroups < 1 || sink == nullptr || clk == nullptr) return (int)hipErrorInvalidValue;
-  k_mfma_bf16_rate<<<dim3((unsigned)workgroups), dim3(256), 0, stream>>>(sink, clk, iters);
+  k_mfma16_rate<bf16x8, __bf16><<<dim3((unsigned)workgroups), dim3(256), 0, stream>>>(sink, clk, iters);
+  return (int)hipGetLastError();
+}
+
+extern "C" __attribute__((visibility("default"))) int sharq_probe_mfma_f16(int iters, int workgroups, float* sink,
+                                                                           unsigned long long* clk,
+                                                                           hipStream_t stream) {
+  if (iters < 1 || workgroups < 1 || sink == nullptr || clk == nullptr) return (int)hipErrorInvalidValue;
+  k_mfma16_rate<f16x8, _Float16><<<dim3((unsigned)workgroups), dim3(256), 0, stream>>>(sink, clk, iters);
   return (int)hipGetLastError();
 }
 

@@ -393,7 +393,7 @@ def test_probe_library_exports_and_rejects():
     """The benchmark's MFMA-rate probe library exports what its header
     declares and rejects bad arguments before any launch."""
     names = re.findall(r"\bint\s+(sharq_probe_\w+)\s*\(", open(PROBE_HEADER).read())
-    assert names == ["sharq_probe_mfma_fp4", "sharq_probe_mfma_bf16"]
+    assert names == ["sharq_probe_mfma_fp4", "sharq_probe_mfma_bf16", "sharq_probe_mfma_f16"]
     P = ctypes.CDLL(PROBE_LIB)
     fake = 1 << 20   # never dereferenced
     hip_invalid_value = 1
