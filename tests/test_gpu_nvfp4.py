@@ -5,6 +5,7 @@ oracle byte for byte (the per-tensor scale as fp32 bits); the two-path GEMM
 must meet the same 1e-3 accumulation gate as the MXFP4 path.
 """
 
+import math
 import sys
 
 import numpy as np
@@ -203,3 +204,111 @@ def test_qwen_full_shape_nv(S, G, name):
     rows = np.random.default_rng(2).choice(QWEN_T, 256, replace=False)
     rows[0], rows[1] = 0, QWEN_T - 1
     gemm_check(G.host(y)[rows], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), name)
+
+
+E2M1_MAGS = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+
+
+def e4m3_positive_value(code: int) -> float:
+    """The E4M3 value of a positive code, from the format's definition
+    (exponent bias 7, three mantissa bits, subnormals at exponent field 0)."""
+    e, m = (code >> 3) & 15, code & 7
+    return m * 2.0 ** -9 if e == 0 else 2.0 ** (e - 7) * (1 + m / 8)
+
+
+def dyadic_gcd(values) -> float:
+    """Largest power of two dividing every value (all are dyadic rationals)."""
+    def low_bit(v):
+        mant, ex = math.frexp(v)
+        i = int(mant * 2.0 ** 53)
+        return ex - 53 + (i & -i).bit_length() - 1
+    return 2.0 ** min(low_bit(v) for v in values)
+
+
+NV_EXACT_SCALES = {
+    # variant: (activation scale codes, weight scale codes); the other side at 1.0
+    "act_lo": (range(0x01, 0x09), [0x38]),    # subnormals 2^-9..7*2^-9, and 2^-6
+    "act_hi": (range(0x70, 0x7F), [0x38]),    # 128 .. 448 (the largest finite code)
+    "w_lo": ([0x38], range(0x01, 0x09)),
+    "w_hi": ([0x38], range(0x70, 0x7F)),
+}
+
+
+def nv_exact_operands(T, N, K, n, m, variant, seed):
+    """An NVFP4 prepared activation and weight built from codes and E4M3
+    scales at one end of the scale range, with the code magnitudes of the
+    other operand limited so that every fp32 partial sum of the two-path GEMM
+    is exact whatever the order: each product q_a d_a q_w d_w is a multiple
+    of Q = (1/2 gcd(d_a)) (1/2 gcd(d_w)), and at most 2K of them, each below
+    max|q_a d_a| max|q_w d_w|, must stay below 2^24 Q.  The dequantized
+    operands q d range over [2^-10, 2688]: exact and normal in fp16 and bf16.
+    Tensor scales 2^-2 and 2^3 make the epilogue's multiply exact too."""
+    rng = np.random.default_rng(seed)
+    a_codes, w_codes = (list(c) for c in NV_EXACT_SCALES[variant])
+    da = [e4m3_positive_value(c) for c in a_codes]
+    dw = [e4m3_positive_value(c) for c in w_codes]
+    q = 0.25 * dyadic_gcd(da) * dyadic_gcd(dw)
+    amax, wmax = 7, 7        # largest magnitude code index of each side
+    extreme_act = variant.startswith("act")
+    while 2 * K * E2M1_MAGS[amax] * max(da) * E2M1_MAGS[wmax] * max(dw) >= 2.0 ** 24 * q:
+        if extreme_act:
+            wmax -= 1
+        else:
+            amax -= 1
+        assert min(amax, wmax) >= 1
+    keep = np.zeros((T, K // m, m), bool)
+    order = rng.random((T, K // m, m)).argsort(axis=2)[..., :n]
+    np.put_along_axis(keep, order, True, axis=2)
+    keep = keep.reshape(T, K)
+
+    def codes(shape, mag_max):
+        return (rng.integers(0, mag_max + 1, size=shape) | (rng.integers(0, 2, size=shape) << 3)).astype(np.uint8)
+
+    def scales(shape, pool):
+        return np.asarray(pool, np.uint8)[rng.integers(0, len(pool), size=shape)]
+
+    sp = np.where(keep, codes((T, K), amax), 0).astype(np.uint8)
+    sp_codes, sp_meta = O.pack_backbone(sp, keep, n, m)
+    act = {"rows": T, "K": K, "n": n, "m": m, "pairs": False, "fmt": "nv", "tensor_scale": np.float32(0.25),
+           "mode": "sharq", "sp_codes": sp_codes, "sp_meta": sp_meta, "sp_scale": scales((T, K // 32), a_codes),
+           "dn_codes": O.pack_nibbles(codes((T, K), amax)), "dn_scale": scales((T, K // 16), a_codes),
+           "dn_meta": np.zeros((T, 0), np.uint8)}
+    ws = scales((N, K // 32), w_codes)
+    wq = {"N": N, "K": K, "fmt": "nv", "codes": O.pack_nibbles(codes((N, K), wmax)), "scale": ws,
+          "scale_dn": np.repeat(ws, 2, axis=1), "tensor_scale": np.float32(8.0)}
+    return act, wq, (amax, wmax)
+
+
+NV_EXACT_CASES = ([("gate_up", 2, 4, "act_hi"), ("gate_up", 2, 4, "w_lo"), ("down", 2, 4, "act_lo"),
+                   ("down", 2, 4, "w_hi")]
+                  + [("ragged", n, m, v) for n, m in ((2, 4), (4, 8)) for v in sorted(NV_EXACT_SCALES)]
+                  + [("mid", 4, 8, v) for v in sorted(NV_EXACT_SCALES)])
+
+
+@pytest.mark.parametrize("name,n,m,variant", NV_EXACT_CASES)
+def test_nv_exact_sums(S, G, name, n, m, variant):
+    """The NVFP4 GEMMs on operands whose sums are exact in fp32, with the
+    activation or weight block scales at either end of the E4M3 range: the
+    output must equal the oracle's exact result bit for bit.  The Qwen2.5-7B
+    shapes at M = 4096 run the persistent fp16 kernel (256 sampled rows, all
+    columns; each shape takes two of the four scale ranges), and so does the
+    4:8 case with ragged rows and columns; the ragged case (K not a multiple
+    of 128) the bf16 one (all outputs, every range)."""
+    if name in ("ragged", "mid"):
+        T, K, N = (300, 416, 520) if name == "ragged" else (300, 1024, 520)
+        rows = np.arange(T)
+    else:
+        K, N, _ = synth.QWEN_LINEARS[name]
+        T = QWEN_T
+        rows = np.random.default_rng(5).choice(T, 256, replace=False)
+        rows[0], rows[1] = 0, T - 1
+    o, wo, mags = nv_exact_operands(T, N, K, n, m, variant, seed=K + N + len(variant))
+    say(f"[nv-exact] {name} T={T} K={K} N={N} {n}:{m} {variant} code magnitude limits {mags}")
+    a, w = G.oracle_to_act(o), G.oracle_to_weight(wo)
+    y = S.sharq_linear(a, w, dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = O.linear(o, wo, rows=rows)
+    got = G.host(y)[rows].astype(np.float64)
+    bad = np.nonzero(got != ref)
+    assert bad[0].size == 0, (f"{name} {variant}: {bad[0].size} outputs differ from the exact sum; first at "
+                              f"{bad[0][0]},{bad[1][0]}: {got[bad[0][0], bad[1][0]]} vs {ref[bad[0][0], bad[1][0]]}")
