@@ -158,17 +158,19 @@ typedef enum {
  *                             MXFP4: unused (may be NULL).
  *   mode                      SHARQ_MODE_SHARQ (0).
  *   dn_meta                   unused (may be NULL).
- *   sp_dense [rows][K/2]      optional (NULL = none), MXFP4 only: the backbone's
- *                             codes at all K positions (dropped positions
- *                             code 0), laid out like dn_codes; 16-byte
- *                             aligned.  When given, the preparation writes it
- *                             beside the compressed form, and the main
- *                             kernels of sharq_linear and sharq_linear_grouped
- *                             (K a multiple of 128) read it instead of
- *                             expanding sp_codes / sp_meta: gfx950 has no sparse FP4
- *                             matrix instruction, so the backbone runs dense
- *                             anyway, and the copy (K/2 more bytes per row)
- *                             takes the expansion out of every column tile.
+ *   sp_dense [rows][K/2]      optional (NULL = none), MXFP4 and NVFP4 (not
+ *                             HiF4): the backbone's codes at all K positions
+ *                             (dropped positions code 0), laid out like
+ *                             dn_codes, with the backbone's scales sp_scale;
+ *                             16-byte aligned.  When given, the preparation
+ *                             writes it beside the compressed form, and the
+ *                             main kernels of sharq_linear and (MXFP4)
+ *                             sharq_linear_grouped (K a multiple of 128) read
+ *                             it instead of expanding sp_codes / sp_meta:
+ *                             gfx950 has no sparse FP4 matrix instruction, so
+ *                             the backbone runs dense anyway, and the copy
+ *                             (K/2 more bytes per row) takes the expansion
+ *                             out of every column tile.
  *                             Dense-only form: with sp_dense given, sp_codes
  *                             and sp_meta may both be NULL (K a multiple of
  *                             128, SHARQ_MODE_SHARQ); the preparation then

@@ -18,7 +18,7 @@ hipError_t launch_wquant_nv(const void* W, int wdt, int N, int K, int64_t ldw, u
 hipError_t launch_linear_nv(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                             const uint8_t* dnc, const uint8_t* dns, const float* tsx, int64_t M, const uint8_t* wc,
                             const uint8_t* ws, const float* tsw, int N, int K, void* Y, int64_t ldy,
-                            hipStream_t st);
+                            const uint8_t* spd, hipStream_t st);
 hipError_t launch_linear_mx(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                             const uint8_t* dnc, const uint8_t* dns, int64_t M, const uint8_t* wc, const uint8_t* ws,
                             int N, int K, void* Y, int64_t ldy, const uint8_t* spd, hipStream_t st);
@@ -114,14 +114,14 @@ sharq_status check_act(const sharq_act* a) {
   const int k1 = kind1(mode), k2 = kind2(mode);
   // the dense-only backbone: sp_dense without the compressed codes and metadata
   const bool dense_only = a->sp_dense && !a->sp_codes && !a->sp_meta && mode == SHARQ_MODE_SHARQ;
-  if (dense_only && (a->fmt != SHARQ_MXFP4 || a->K % 128 != 0)) return SHARQ_EUNSUPPORTED;
+  if (dense_only && (a->fmt == SHARQ_HIF4 || a->K % 128 != 0)) return SHARQ_EUNSUPPORTED;
   if (k1 != kNone && !dense_only && (!a->sp_codes || !a->sp_scale || (k1 == kSparse && !a->sp_meta)))
     return SHARQ_EINVAL;
   if (dense_only && !a->sp_scale) return SHARQ_EINVAL;
   if (k2 != kNone && (!a->dn_codes || !a->dn_scale)) return SHARQ_EINVAL;
   if (k2 == kSparse && !a->dn_meta) return SHARQ_EINVAL;
   if (a->fmt == SHARQ_NVFP4 && !a->tensor_scale) return SHARQ_EINVAL;
-  if (a->sp_dense && (a->fmt != SHARQ_MXFP4 || mode != SHARQ_MODE_SHARQ)) return SHARQ_EUNSUPPORTED;
+  if (a->sp_dense && (a->fmt == SHARQ_HIF4 || mode != SHARQ_MODE_SHARQ)) return SHARQ_EUNSUPPORTED;
   if (!aligned(a->sp_dense, 16)) return SHARQ_EALIGN;
   if (!aligned(a->sp_codes, 16) || !aligned(a->dn_codes, 16) || !aligned(a->sp_meta, 4) ||
       !aligned(a->sp_scale, 4) || !aligned(a->dn_scale, 4) || !aligned(a->tensor_scale, 4) ||
@@ -367,7 +367,8 @@ sharq_status sharq_linear(const sharq_act* a, const sharq_weight* w, void* Y, sh
   if (a->fmt == SHARQ_NVFP4)
     return hip_status(sharq::launch_linear_nv(gemm_pattern(pattern_id(a->nm)), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale,
                                               a->dn_codes, a->dn_scale, a->tensor_scale, a->rows, w->codes,
-                                              w->scale, w->tensor_scale, (int)w->N, (int)w->K, Y, ldy, st));
+                                              w->scale, w->tensor_scale, (int)w->N, (int)w->K, Y, ldy,
+                                              a->sp_dense, st));
   return hip_status(sharq::launch_linear_mx(gemm_pattern(pattern_id(a->nm)), (int)ydt, a->sp_codes, a->sp_meta, a->sp_scale,
                                             a->dn_codes, a->dn_scale, a->rows, w->codes, w->scale, (int)w->N,
                                             (int)w->K, Y, ldy, a->sp_dense, st));

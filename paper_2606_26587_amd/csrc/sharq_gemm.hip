@@ -1864,8 +1864,9 @@ __global__ __launch_bounds__(256) void k_linear_nv(const uint8_t* sp_codes, cons
 
 struct NvRaw {          // this lane's raw activation data of one step
   uint2 dn;             // residual codes of positions 16 h + 0..15
-  uint32_t spc;         // compressed backbone codes of the same 16 positions
-  uint32_t spm;         // their metadata (low 16 bits)
+  uint32_t spc;         // compressed backbone codes of the same 16 positions;
+                        // from the dense backbone copy (PAT 0): their first 8 codes
+  uint32_t spm;         // their metadata (low 16 bits); PAT 0: the last 8 codes
   uint32_t ssc, dsc;    // backbone and residual E4M3 scales (bytes)
 };
 
@@ -1909,13 +1910,29 @@ __device__ __forceinline__ uint32_t f16_pair(uint32_t codes, f16x2 d) {
   return __builtin_bit_cast(uint32_t, v * d);
 }
 
+// PAT 0: a.spc is the dense backbone copy (16 bytes per block, block-major).
+template <int PAT>
 __device__ __forceinline__ void nv_load_a(NvRaw& s, const ARow& a, int ks, int half) {
   const int64_t V = ((int64_t)(ks >> 2) * a.R + a.r) * 4 + (ks & 3);   // block-major index
   s.dn = *reinterpret_cast<const uint2*>(a.dn + V * 16 + 8 * half);
-  s.spc = *reinterpret_cast<const uint32_t*>(a.spc + V * 8 + 4 * half);
-  s.spm = (uint32_t)*reinterpret_cast<const uint16_t*>(a.spm + V * 4 + 2 * half);
+  if (PAT == 0) {
+    const uint2 c = *reinterpret_cast<const uint2*>(a.spc + V * 16 + 8 * half);
+    s.spc = c.x;
+    s.spm = c.y;
+  } else {
+    s.spc = *reinterpret_cast<const uint32_t*>(a.spc + V * 8 + 4 * half);
+    s.spm = (uint32_t)*reinterpret_cast<const uint16_t*>(a.spm + V * 4 + 2 * half);
+  }
   s.ssc = a.sps[V];
   s.dsc = a.dns[V * 2 + half];
+}
+
+// Dense backbone codes D (0: positions 16 h + 0..7, 1: + 8..15) of a step:
+// read as they are from the dense copy, or expanded from the compressed form.
+template <int PAT, int D>
+__device__ __forceinline__ uint32_t nv_backbone_dw(const NvRaw& r) {
+  if (PAT == 0) return D == 0 ? r.spc : r.spm;
+  return expand_dw<PAT, D>(make_uint2(r.spc, 0u), r.spm);
 }
 
 __device__ __forceinline__ void nv_load_w(NvWRaw& w, const uint8_t* wc, const uint8_t* ws, int n0, int N, int ks) {
@@ -1952,13 +1969,12 @@ __device__ __forceinline__ void nv_step(v16f (&acc)[8], const NvOps& ops, uint4 
   // (their scales decoded behind the first two MFMAs)
   f16x2 dsp, ddn;
   uint32_t e0 = 0u, e1 = 0u;
-  const uint2 cw = make_uint2(raw.spc, 0u);
   // ---- sub-step 0, backbone
   nv_mma<0, 0>(acc, ops.sp[0], b0); nv_read_b<1, 0, 1>(b1, cur, lane); dsp = nv_scale2(raw.ssc); SHARQ_FENCE();
   nv_mma<0, 1>(acc, ops.sp[0], b0); nv_read_b<1, 1, 2>(b1, cur, lane); ddn = nv_scale2(raw.dsc);
-  e0 = expand_dw<PAT, 0>(cw, raw.spm); SHARQ_FENCE();
+  e0 = nv_backbone_dw<PAT, 0>(raw); SHARQ_FENCE();
   nv_mma<0, 2>(acc, ops.sp[0], b0); nv_read_b<1, 2, 3>(b1, cur, lane); SHARQ_FENCE();
-  nv_mma<0, 3>(acc, ops.sp[0], b0); nv_read_b<1, 3, 4>(b1, cur, lane); e1 = expand_dw<PAT, 1>(cw, raw.spm); SHARQ_FENCE();
+  nv_mma<0, 3>(acc, ops.sp[0], b0); nv_read_b<1, 3, 4>(b1, cur, lane); e1 = nv_backbone_dw<PAT, 1>(raw); SHARQ_FENCE();
   nv_mma<0, 4>(acc, ops.sp[0], b0); nv_read_b<1, 4, 5>(b1, cur, lane);
   opsn.sp[0].x = f16_pair<0>(e0, dsp); opsn.sp[0].y = f16_pair<1>(e0, dsp); SHARQ_FENCE();
   nv_mma<0, 5>(acc, ops.sp[0], b0); nv_read_b<1, 5, 6>(b1, cur, lane);
@@ -2024,8 +2040,7 @@ __device__ __forceinline__ void nv_step(v16f (&acc)[8], const NvOps& ops, uint4 
 template <int PAT>
 __device__ __forceinline__ void nv_ops_from_raw(NvOps& o, const NvRaw& r) {
   const f16x2 dsp = nv_scale2(r.ssc), ddn = nv_scale2(r.dsc);
-  const uint2 cw = make_uint2(r.spc, 0u);
-  const uint32_t e0 = expand_dw<PAT, 0>(cw, r.spm), e1 = expand_dw<PAT, 1>(cw, r.spm);
+  const uint32_t e0 = nv_backbone_dw<PAT, 0>(r), e1 = nv_backbone_dw<PAT, 1>(r);
   o.sp[0] = make_uint4(f16_pair<0>(e0, dsp), f16_pair<1>(e0, dsp), f16_pair<2>(e0, dsp), f16_pair<3>(e0, dsp));
   o.sp[1] = make_uint4(f16_pair<0>(e1, dsp), f16_pair<1>(e1, dsp), f16_pair<2>(e1, dsp), f16_pair<3>(e1, dsp));
   o.dn[0] = make_uint4(f16_pair<0>(r.dn.x, ddn), f16_pair<1>(r.dn.x, ddn), f16_pair<2>(r.dn.x, ddn),
@@ -2088,8 +2103,8 @@ __device__ __forceinline__ void tile_nv_il(const uint8_t* sp_codes, const uint8_
   uint8_t* st2 = lds + 2 * kNvStage;
   nv_load_w(w0, wc, ws, n0, N, 0);
   nv_load_w(w1, wc, ws, n0, N, cl(1));
-  nv_load_a(r0, a, 0, half);
-  nv_load_a(r1, a, cl(1), half);
+  nv_load_a<PAT>(r0, a, 0, half);
+  nv_load_a<PAT>(r1, a, cl(1), half);
   nv_store_w(w0, st0);
   nv_store_w(w1, st1);
   nv_ops_from_raw<PAT>(o0, r0);
@@ -2101,12 +2116,12 @@ __device__ __forceinline__ void tile_nv_il(const uint8_t* sp_codes, const uint8_
   for (; ks + 1 < nks; ks += 2) {
     nv_step<PAT>(acc, o0, b0, st0, st1, st2, o1, r1, w0, lane, [&] {
       nv_load_w(w1, wc, ws, n0, N, cl(ks + 3));
-      nv_load_a(r0, a, cl(ks + 2), half);
+      nv_load_a<PAT>(r0, a, cl(ks + 2), half);
     });
     __syncthreads();
     nv_step<PAT>(acc, o1, b0, st1, st2, st0, o0, r0, w1, lane, [&] {
       nv_load_w(w0, wc, ws, n0, N, cl(ks + 4));
-      nv_load_a(r1, a, cl(ks + 3), half);
+      nv_load_a<PAT>(r1, a, cl(ks + 3), half);
     });
     __syncthreads();
     uint8_t* t = st0;   // rotate the stages by two
@@ -2176,9 +2191,13 @@ static hipError_t go_nv(const uint8_t* spc, const uint8_t* spm, const uint8_t* s
         spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
     return hipGetLastError();
   }
-  k_linear_nv<NF, PAT, OutT><<<dim3((unsigned)(gx * gy)), dim3(256), 0, st>>>(
-      spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
-  return hipGetLastError();
+  if constexpr (PAT == 0) {
+    return hipErrorInvalidValue;   // the dense backbone copy needs K a multiple of 128
+  } else {
+    k_linear_nv<NF, PAT, OutT><<<dim3((unsigned)(gx * gy)), dim3(256), 0, st>>>(
+        spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, reinterpret_cast<OutT*>(Y), ldy, gx, gy);
+    return hipGetLastError();
+  }
 }
 
 template <int PAT>
@@ -2193,7 +2212,9 @@ static hipError_t go_nv_dt(int ydt, const uint8_t* spc, const uint8_t* spm, cons
 hipError_t launch_linear_nv(int pat, int ydt, const uint8_t* spc, const uint8_t* spm, const uint8_t* sps,
                             const uint8_t* dnc, const uint8_t* dns, const float* tsx, int64_t M, const uint8_t* wc,
                             const uint8_t* ws, const float* tsw, int N, int K, void* Y, int64_t ldy,
-                            hipStream_t st) {
+                            const uint8_t* spd, hipStream_t st) {
+  if (spd && K % kBK == 0) return go_nv_dt<0>(ydt, spd, nullptr, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
+  if (spc == nullptr) return hipErrorInvalidValue;   // rejected by the C ABI (K not a multiple of 128)
   return pat == 24 ? go_nv_dt<24>(ydt, spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, Y, ldy, st)
                    : go_nv_dt<48>(ydt, spc, spm, sps, dnc, dns, tsx, M, wc, ws, tsw, N, K, Y, ldy, st);
 }

@@ -138,8 +138,7 @@ __global__ __launch_bounds__(256) void k_prep_blocks(XSrc src, int M, int K, Act
   unpack_bf16x32(xq, y);
   const BlockOut d = block_at<NV>(o, (int64_t)p * M * 4 + t);
   if (NV) {
-    block_nv<PAT>(y, S, six_s, d.spc, d.spm, d.sps, d.dnc, d.dns);
-    if (d.dbg_mask) *d.dbg_mask = keep_bits<PAT == 49 ? 48 : PAT>(*reinterpret_cast<const uint32_t*>(d.spm));
+    block_nv<PAT>(y, S, six_s, d);
   } else {
     block_mx<PAT>(y, d, o.rule_bias);
   }

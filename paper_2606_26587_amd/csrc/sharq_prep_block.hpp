@@ -454,28 +454,44 @@ __device__ __forceinline__ void block_mx(const float (&y)[32], const BlockOut& d
 
 // Quantize and store one NVFP4 block: E4M3 backbone scale per 32 positions,
 // E4M3 residual scales per 16 positions (two bytes), per-tensor scale S.
+// d.spd (optional): the backbone's dense codes, as in block_mx; without d.spc
+// only that copy is written.
 template <int PAT>
-__device__ __forceinline__ void block_nv(const float (&y)[32], float S, float six_s, uint8_t* __restrict__ spc,
-                                         uint8_t* __restrict__ spm, uint8_t* __restrict__ sps,
-                                         uint8_t* __restrict__ dnc, uint8_t* __restrict__ dns) {
+__device__ __forceinline__ void block_nv(const float (&y)[32], float S, float six_s, const BlockOut& d) {
   const NvQ qb = NvQ::make(absmax32(y), six_s, S);
-  uint32_t codes[2], meta;
+  uint32_t codes[2] = {0u, 0u}, meta = 0u;
   float R[32];
-  if (PAT == 24)
+  if (d.spd != nullptr && d.spc == nullptr && d.dbg_mask == nullptr) {   // dense copy alone
+    uint32_t dense[4];
+    if (PAT == 24) backbone_24_dense_only(y, qb, dense, R);
+    else if (PAT == 49) backbone_48p_dense_only(y, qb, dense, R);
+    else backbone_48_dense_only(y, qb, dense, R);
+    *reinterpret_cast<uint4*>(d.spd) = make_uint4(dense[0], dense[1], dense[2], dense[3]);
+  } else if (PAT == 24 && d.spd != nullptr) {
+    uint32_t dense[4];
+    backbone_24_dense(y, qb, codes, meta, dense, R);
+    *reinterpret_cast<uint4*>(d.spd) = make_uint4(dense[0], dense[1], dense[2], dense[3]);
+  } else if (PAT == 24) {
     backbone_24(y, qb, codes, meta, R);
-  else if (PAT == 49)
+  } else if (PAT == 49) {
     backbone_48p(y, qb, codes, meta, R);
-  else
+  } else {
     backbone_48(y, qb, codes, meta, R);
+  }
   const NvQ q0 = NvQ::make(absmax16(R), six_s, S);
   const NvQ q1 = NvQ::make(absmax16(R + 16), six_s, S);
   const uint32_t dn0 = enc8(R, q0), dn1 = enc8(R + 8, q0), dn2 = enc8(R + 16, q1), dn3 = enc8(R + 24, q1);
-  *reinterpret_cast<uint2*>(spc) = make_uint2(codes[0], codes[1]);
-  *reinterpret_cast<uint32_t*>(spm) = meta;
-  *sps = (uint8_t)e4m3_bits(qb.d);
-  *reinterpret_cast<uint4*>(dnc) = make_uint4(dn0, dn1, dn2, dn3);
-  dns[0] = (uint8_t)e4m3_bits(q0.d);
-  dns[1] = (uint8_t)e4m3_bits(q1.d);
+  if (d.spc != nullptr) {
+    *reinterpret_cast<uint2*>(d.spc) = make_uint2(codes[0], codes[1]);
+    *reinterpret_cast<uint32_t*>(d.spm) = meta;
+  }
+  *d.sps = (uint8_t)e4m3_bits(qb.d);
+  *reinterpret_cast<uint4*>(d.dnc) = make_uint4(dn0, dn1, dn2, dn3);
+  d.dns[0] = (uint8_t)e4m3_bits(q0.d);
+  d.dns[1] = (uint8_t)e4m3_bits(q1.d);
+  if (PAT != 24 && d.spd != nullptr && (d.spc != nullptr || d.dbg_mask != nullptr))
+    *reinterpret_cast<uint4*>(d.spd) = expand_block<48>(make_uint2(codes[0], codes[1]), meta);
+  if (d.dbg_mask) *d.dbg_mask = keep_bits<PAT == 49 ? 48 : PAT>(meta);
 }
 
 __device__ __forceinline__ void unpack_bf16x32(const uint4 (&q)[4], float (&x)[32]) {
@@ -582,8 +598,7 @@ __device__ __forceinline__ void block_out_write(const float (&y)[32], const ActO
                                                 float six_s) {
   const BlockOut d = block_out<NV>(o, row, b);
   if (NV) {
-    block_nv<PAT>(y, S, six_s, d.spc, d.spm, d.sps, d.dnc, d.dns);
-    if (d.dbg_mask) *d.dbg_mask = keep_bits<PAT == 49 ? 48 : PAT>(*reinterpret_cast<const uint32_t*>(d.spm));
+    block_nv<PAT>(y, S, six_s, d);
   } else {
     block_mx<PAT>(y, d, o.rule_bias);
   }

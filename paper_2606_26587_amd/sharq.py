@@ -132,7 +132,7 @@ class PreparedAct:
     pairs: bool = False
     mode: int = 0
     dn_meta: Optional[torch.Tensor] = None
-    sp_dense: Optional[torch.Tensor] = None   # MXFP4: the backbone's dense copy for the main GEMM
+    sp_dense: Optional[torch.Tensor] = None   # MXFP4/NVFP4: the backbone's dense copy for the main GEMM
     scale_rule: int = 0                       # MXFP4: E8M0 rule (SCALE_RULES)
     dbg_mask: Optional[torch.Tensor] = None   # debug: keep bits, 4 bytes per 32 positions
     dbg_r: Optional[torch.Tensor] = None      # debug: RMSNorm r per row (fp32)
@@ -171,7 +171,7 @@ def alloc_act(rows: int, K: int, n: int = 2, m: int = 4, fmt="mx", device="cuda"
     """Device buffers of a prepared activation (flat, panel-major; see include/sharq.h).
     pairs=True: n:m selection in pairs (4:8 in pairs).  mode: a key of MODES
     (or its id); buffers a mode does not use are empty.  dense_backbone=True
-    (MXFP4): also the backbone's dense copy that the main GEMM reads without
+    (MXFP4, NVFP4): also the backbone's dense copy that the main GEMM reads without
     expanding it; dense_only=True: that copy instead of the compressed
     backbone.  scale_rule: "floor" or "ceil" (MXFP4 E8M0 rule).  debug=True:
     also the keep-mask and per-row r debug outputs."""

@@ -345,9 +345,13 @@ def test_dense_backbone_copy_rejections(L):
         return L.sharq_prepare(FAKE, 0, a.rows, a.K, a.K, None, 1e-6, Pattern(a.nm.n, a.nm.m), fmt, None,
                                ctypes.byref(a), None)
     assert prep(act(sp_dense=FAKE + 8)) == EALIGN
-    nv = act(fmt=1, sp_dense=FAKE)
+    assert prep(act(fmt=2, sp_dense=FAKE), fmt=2) == EUNSUPPORTED       # MXFP4 and NVFP4, not HiF4
+    nv = Act(8, 160, 1, Pattern(2, 4, 0), None, None, FAKE, FAKE, FAKE, FAKE, 0, None, FAKE)
+    assert L.sharq_prepare(FAKE, 0, 8, 160, 160, None, 1e-6, Pattern(2, 4), 1, None, ctypes.byref(nv),
+                           None) == EUNSUPPORTED                        # NVFP4 dense-only: K a multiple of 128
+    nv = act(fmt=1, sp_dense=FAKE + 8)
     nv.tensor_scale = FAKE
-    assert prep(nv, fmt=1) == EUNSUPPORTED                             # NVFP4: the copy is MXFP4 only
+    assert prep(nv, fmt=1) == EALIGN
     assert prep(act(mode=SPARSE, sp_dense=FAKE)) == EUNSUPPORTED        # the method's combination only
 
 

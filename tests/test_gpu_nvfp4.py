@@ -189,7 +189,8 @@ def test_qwen_full_shape_nv(S, G, name):
     """Full M=4096 Qwen2.5-7B shapes: preparation compared in full, the GEMM on
     256 sampled rows x all columns, and every output written (the output is
     filled with NaN first: the persistent kernel's tile order skips ids past
-    the last of its 148 x 32 or 14 x 32 tiles)."""
+    the last of its 148 x 32 or 14 x 32 tiles), then the same with the
+    dense-only backbone: its copy byte-exact and the output bit-identical."""
     K, N, norm = synth.QWEN_LINEARS[name]
     say(f"[qwen-nv] {name} T={QWEN_T} K={K} N={N}")
     x = synth.activations(QWEN_T, K, seed=1)
@@ -198,8 +199,17 @@ def test_qwen_full_shape_nv(S, G, name):
     wq = S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=1)), "nv")
     y = torch.full((QWEN_T, N), float("nan"), dtype=torch.float32, device="cuda")
     S.sharq_linear(a, wq, out=y)
+    # the dense-only backbone (the benchmark's form): same buffers, same output
+    d = S.sharq_prepare(G.dev_bf16(x), None if g is None else G.dev_bf16(g), 1e-6, 2, 4, "nv",
+                        out=S.alloc_act(QWEN_T, K, 2, 4, "nv", "cuda", dense_only=True))
+    yd = torch.full((QWEN_T, N), float("nan"), dtype=torch.float32, device="cuda")
+    S.sharq_linear(d, wq, out=yd)
     torch.cuda.synchronize()
     assert bool(torch.isfinite(y).all()), f"{name}: outputs left unwritten"
+    G.assert_bytes_equal("sp_dense", G.host(d.sp_dense), L.dense_backbone_to_device_layout(o))
+    for buf in ("sp_scale", "dn_codes", "dn_scale", "tensor_scale"):
+        G.assert_bytes_equal(buf, G.host(getattr(d, buf)).view(np.uint8), G.host(getattr(a, buf)).view(np.uint8))
+    assert torch.equal(yd, y), f"{name}: the dense-only backbone changes the output"
     wo = G.weight_to_oracle(wq)
     rows = np.random.default_rng(2).choice(QWEN_T, 256, replace=False)
     rows[0], rows[1] = 0, QWEN_T - 1
@@ -293,7 +303,9 @@ def test_nv_exact_sums(S, G, name, n, m, variant):
     shapes at M = 4096 run the persistent fp16 kernel (256 sampled rows, all
     columns; each shape takes two of the four scale ranges), and so does the
     4:8 case with ragged rows and columns; the ragged case (K not a multiple
-    of 128) the bf16 one (all outputs, every range)."""
+    of 128) the bf16 one (all outputs, every range).  Each runs on the
+    compressed backbone and on its dense copy (read where K is a multiple of
+    128)."""
     if name in ("ragged", "mid"):
         T, K, N = (300, 416, 520) if name == "ragged" else (300, 1024, 520)
         rows = np.arange(T)
@@ -304,11 +316,55 @@ def test_nv_exact_sums(S, G, name, n, m, variant):
         rows[0], rows[1] = 0, T - 1
     o, wo, mags = nv_exact_operands(T, N, K, n, m, variant, seed=K + N + len(variant))
     say(f"[nv-exact] {name} T={T} K={K} N={N} {n}:{m} {variant} code magnitude limits {mags}")
-    a, w = G.oracle_to_act(o), G.oracle_to_weight(wo)
-    y = S.sharq_linear(a, w, dtype=torch.float32)
+    w = G.oracle_to_weight(wo)
+    y = S.sharq_linear(G.oracle_to_act(o), w, dtype=torch.float32)
+    yd = S.sharq_linear(G.oracle_to_act(o, dense_backbone=True), w, dtype=torch.float32)
     torch.cuda.synchronize()
     ref = O.linear(o, wo, rows=rows)
-    got = G.host(y)[rows].astype(np.float64)
-    bad = np.nonzero(got != ref)
-    assert bad[0].size == 0, (f"{name} {variant}: {bad[0].size} outputs differ from the exact sum; first at "
-                              f"{bad[0][0]},{bad[1][0]}: {got[bad[0][0], bad[1][0]]} vs {ref[bad[0][0], bad[1][0]]}")
+    for tag, out in (("compressed", y), ("dense copy", yd)):
+        got = G.host(out)[rows].astype(np.float64)
+        bad = np.nonzero(got != ref)
+        assert bad[0].size == 0, (f"{name} {variant} {tag}: {bad[0].size} outputs differ from the exact sum; "
+                                  f"first at {bad[0][0]},{bad[1][0]}: {got[bad[0][0], bad[1][0]]} vs "
+                                  f"{ref[bad[0][0], bad[1][0]]}")
+
+
+@pytest.mark.parametrize("T,K,N,use_gamma,n,m,pairs,form", [(300, 1024, 520, True, 2, 4, False, "both"),
+                                                            (300, 640, 300, True, 4, 8, False, "only"),
+                                                            (288, 2048, 256, False, 4, 8, True, "only"),
+                                                            (2048, 4096, 6144, True, 4, 8, True, "only"),
+                                                            (37, 3584, 300, True, 2, 4, False, "only"),
+                                                            (130, 416, 96, False, 2, 4, False, "both")])
+def test_nv_dense_backbone(S, G, T, K, N, use_gamma, n, m, pairs, form):
+    """The NVFP4 backbone's dense copy, written beside the compressed form
+    ("both") or alone ("only"): byte-exact against the oracle's backbone
+    expanded to all positions, the other buffers and the per-tensor scale
+    unchanged, and the GEMM on it bit-identical to the GEMM on the compressed
+    backbone (same fp16 operands) and within the gate of the oracle.  K = 416
+    runs the ragged-K kernel, which ignores the copy."""
+    say(f"[nv-dense] T={T} K={K} N={N} {n}:{m}{'p' if pairs else ''} {form}")
+    x = synth.activations(T, K, seed=K + T)
+    g = synth.gamma(K, seed=3) if use_gamma else None
+    xd, gd = G.dev_bf16(x), (None if g is None else G.dev_bf16(g))
+    a = S.sharq_prepare(xd, gd, 1e-6, n, m, "nv", pairs=pairs,
+                        out=S.alloc_act(T, K, n, m, "nv", "cuda", pairs, dense_backbone=form == "both",
+                                        dense_only=form == "only"))
+    c = S.sharq_prepare(xd, gd, 1e-6, n, m, "nv", pairs=pairs)
+    wq = S.sharq_quantize_weight(G.dev_bf16(synth.weight(N, K, seed=N)), "nv")
+    yd = S.sharq_linear(a, wq, dtype=torch.float32)
+    yc = S.sharq_linear(c, wq, dtype=torch.float32)
+    yd16 = S.sharq_linear(a, wq, dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    o = O.prepare(x, g, 1e-6, n, m, "nv", pairs=pairs)
+    G.assert_bytes_equal("sp_dense", G.host(a.sp_dense), L.dense_backbone_to_device_layout(o))
+    names = O.ACT_BUFFERS if form == "both" else ("sp_scale", "dn_codes", "dn_scale")
+    if form == "only":
+        assert a.sp_codes is None and a.sp_meta is None
+    for name in names:
+        G.assert_bytes_equal(name, G.host(getattr(a, name)), G.host(getattr(c, name)))
+    assert f32_bits(G.host(a.tensor_scale)[0]) == f32_bits(o["tensor_scale"])
+    assert torch.equal(yd, yc)
+    assert torch.equal(yd16, yd.to(torch.bfloat16))
+    rows = np.arange(T) if T <= 512 else np.random.default_rng(3).choice(T, 256, replace=False)
+    wo = G.weight_to_oracle(wq)
+    gemm_check(G.host(yd)[rows], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), f"nv-dense T{T}")
