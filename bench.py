@@ -77,7 +77,7 @@ DECODE_W_SETS = 5             # decode: weight copies rotate between steps (5 x 
 # (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors a plain 1 GiB device copy
 # gives).  Valid only for the GEMM source it was measured on (sha256 prefix);
 # reported as null once that source has changed.
-TRAFFIC = {"gemm_source": "00df2e3863b18332", "bytes_per_launch": 270.30e6}
+TRAFFIC = {"gemm_source": "b82cebda0a75bf94", "bytes_per_launch": 270.33e6}
 
 
 def log(*a):
@@ -589,10 +589,11 @@ def llama_decode(args, torch, S, synth, dev, stream):
 
 def qwen_nvfp4(args, torch, S, synth, dev, stream):
     T = 4096
-    layers = dense_layers(torch, S, synth, dev, synth.QWEN_LINEARS, T, "nv", 2, 4, N_INPUT_SETS)
+    layers = dense_layers(torch, S, synth, dev, synth.QWEN_LINEARS, T, "nv", 2, 4, N_INPUT_SETS,
+                          backbone=args.backbone)
     step = dense_step(S, layers, stream, 1e-6, 2, 4, "nv", N_INPUT_SETS)
     ms_step, wall_ms, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
-    per = per_linear(layers, tm, T, "nv", 2, 4)
+    per = per_linear(layers, tm, T, "nv", 2, 4, args.backbone)
     flops = sum(p["gemm_flops_alg"] for p in per)
     t_gemm = sum(p["gemm_us"] for p in per) * 1e-6
     t_prep = sum(p["prep_us"] for p in per) * 1e-6
@@ -600,7 +601,8 @@ def qwen_nvfp4(args, torch, S, synth, dev, stream):
     out = base_record(args, "SharQ linear TFLOPS (prep+2 FP4 GEMMs), Qwen2.5-7B M=4096 NVFP4",
                       flops / (ms_step * 1e-3) / 1e12, "TFLOP/s", ms_step, "nvfp4",
                       {"workload": "Qwen2.5-7B prefill linears gate_up (K3584,N37888,RMSNorm), down (K18944,N3584); "
-                                   "M=4096; 2:4; NVFP4 with dynamic per-tensor scale", "tokens": T})
+                                   "M=4096; 2:4; NVFP4 with dynamic per-tensor scale", "tokens": T,
+                       "backbone_for_gemm": args.backbone})
     out["roofline"] = nv_roofline(torch, dev, stream, per, t_gemm)
     out["prep"] = {"bound": "hbm", "achieved": pb / t_prep / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                    "frac": pb / t_prep / 1e9 / PEAK_HBM_GBPS,
@@ -612,10 +614,11 @@ def qwen_nvfp4(args, torch, S, synth, dev, stream):
 def llama_nvfp4_pairs(args, torch, S, synth, dev, stream):
     """The paper's own instantiation on the headline shapes: NVFP4 with the
     4:8 in-pairs backbone, Llama-3.1-8B prefill linears at M = 2048."""
-    layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T_TOKENS, "nv", 4, 8, N_INPUT_SETS, True)
+    layers = dense_layers(torch, S, synth, dev, synth.LLAMA_LINEARS, T_TOKENS, "nv", 4, 8, N_INPUT_SETS, True,
+                          backbone=args.backbone)
     step = dense_step(S, layers, stream, synth.LLAMA_EPS, 4, 8, "nv", N_INPUT_SETS, True)
     ms_step, wall_ms, tm = run_steps(torch, stream, step, 2 * len(layers), args.steps, args.warmup)
-    per = per_linear(layers, tm, T_TOKENS, "nv", 4, 8)
+    per = per_linear(layers, tm, T_TOKENS, "nv", 4, 8, args.backbone)
     flops = sum(p["gemm_flops_alg"] for p in per)
     t_gemm = sum(p["gemm_us"] for p in per) * 1e-6
     t_prep = sum(p["prep_us"] for p in per) * 1e-6
@@ -623,7 +626,8 @@ def llama_nvfp4_pairs(args, torch, S, synth, dev, stream):
     out = base_record(args, "SharQ linear TFLOPS (prep+2 FP4 GEMMs), Llama-8B M=2048, NVFP4 4:8 in pairs",
                       flops / (ms_step * 1e-3) / 1e12, "TFLOP/s", ms_step, "nvfp4",
                       {"workload": "Llama-3.1-8B prefill linears qkv, gate_up (RMSNorm), down; M=2048; "
-                                   "4:8 in pairs; NVFP4 with dynamic per-tensor scale", "tokens": T_TOKENS})
+                                   "4:8 in pairs; NVFP4 with dynamic per-tensor scale", "tokens": T_TOKENS,
+                       "backbone_for_gemm": args.backbone})
     out["roofline"] = nv_roofline(torch, dev, stream, per, t_gemm)
     out["prep"] = {"bound": "hbm", "achieved": pb / t_prep / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                    "frac": pb / t_prep / 1e9 / PEAK_HBM_GBPS,
@@ -798,7 +802,10 @@ def ablation(args, torch, S, synth, dev, stream):
         res = {}
         # HiF4 is built for the method's own combination only
         for mode in (ABLATION_MODES if fmt != "hif4" else ["sharq"]):
-            acts = [S.alloc_act(T, L["K"], n, m, fmt, dev, pairs, mode) for L in layers]
+            # SharQ stores its backbone as the benchmark's --backbone says (HiF4: compressed)
+            bb = args.backbone if mode == "sharq" and fmt != "hif4" else "compressed"
+            acts = [S.alloc_act(T, L["K"], n, m, fmt, dev, pairs, mode, dense_backbone=bb == "both",
+                                dense_only=bb == "dense-only") for L in layers]
 
             def step(i, mark, acts=acts):
                 for li, L in enumerate(layers):
@@ -829,7 +836,8 @@ def ablation(args, torch, S, synth, dev, stream):
                           res["sharq"]["executed_TFLOPs"], "TFLOP/s", res["sharq"]["ms_per_step"],
                           {"mx": "mxfp4", "nv": "nvfp4", "hif4": "hif4"}[fmt],
                           {"workload": f"Llama-3.1-8B prefill linears qkv, gate_up (RMSNorm), down; M=2048; "
-                                       f"{setting}; fp32 out; modes " + ", ".join(res), "tokens": T})
+                                       f"{setting}; fp32 out; modes " + ", ".join(res), "tokens": T,
+                           "sharq_backbone": args.backbone if fmt != "hif4" else "compressed"})
         out["modes"] = res
         out["error_definition"] = ("mean over token rows of |Y_t - y_t W^T| / |y_t W^T| (fp32 reference with the "
                                    "unquantized weight), per linear")
@@ -861,9 +869,9 @@ def main():
                              "ablation", "llama-fused"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--backbone", default="dense-only", choices=["dense-only", "both", "compressed"],
-                    help="prefill: how the preparation stores the backbone for the GEMM -- the dense copy alone "
-                         "(default), the dense copy beside the compressed form, or the compressed form only "
-                         "(the GEMM then expands it)")
+                    help="prefill and the NVFP4 workloads: how the preparation stores the backbone for the "
+                         "GEMM -- the dense copy alone (default), the dense copy beside the compressed form, or "
+                         "the compressed form only (the GEMM then expands it)")
     ap.add_argument("--cpu-rows", type=int, default=768)
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB")
     args = ap.parse_args()
