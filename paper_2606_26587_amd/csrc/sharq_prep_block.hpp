@@ -455,29 +455,21 @@ __device__ __forceinline__ void block_mx(const float (&y)[32], const BlockOut& d
 // Quantize and store one NVFP4 block: E4M3 backbone scale per 32 positions,
 // E4M3 residual scales per 16 positions (two bytes), per-tensor scale S.
 // d.spd (optional): the backbone's dense codes, as in block_mx; without d.spc
-// only that copy is written.
+// only that copy is written.  Unlike block_mx, the dense copy is always
+// expanded from the compressed codes: an NVFP4 code costs a correctly rounded
+// division, so converting only the kept values and moving nibbles is cheaper
+// than converting every position with zeros at the dropped ones.
 template <int PAT>
 __device__ __forceinline__ void block_nv(const float (&y)[32], float S, float six_s, const BlockOut& d) {
   const NvQ qb = NvQ::make(absmax32(y), six_s, S);
-  uint32_t codes[2] = {0u, 0u}, meta = 0u;
+  uint32_t codes[2], meta;
   float R[32];
-  if (d.spd != nullptr && d.spc == nullptr && d.dbg_mask == nullptr) {   // dense copy alone
-    uint32_t dense[4];
-    if (PAT == 24) backbone_24_dense_only(y, qb, dense, R);
-    else if (PAT == 49) backbone_48p_dense_only(y, qb, dense, R);
-    else backbone_48_dense_only(y, qb, dense, R);
-    *reinterpret_cast<uint4*>(d.spd) = make_uint4(dense[0], dense[1], dense[2], dense[3]);
-  } else if (PAT == 24 && d.spd != nullptr) {
-    uint32_t dense[4];
-    backbone_24_dense(y, qb, codes, meta, dense, R);
-    *reinterpret_cast<uint4*>(d.spd) = make_uint4(dense[0], dense[1], dense[2], dense[3]);
-  } else if (PAT == 24) {
+  if (PAT == 24)
     backbone_24(y, qb, codes, meta, R);
-  } else if (PAT == 49) {
+  else if (PAT == 49)
     backbone_48p(y, qb, codes, meta, R);
-  } else {
+  else
     backbone_48(y, qb, codes, meta, R);
-  }
   const NvQ q0 = NvQ::make(absmax16(R), six_s, S);
   const NvQ q1 = NvQ::make(absmax16(R + 16), six_s, S);
   const uint32_t dn0 = enc8(R, q0), dn1 = enc8(R + 8, q0), dn2 = enc8(R + 16, q1), dn3 = enc8(R + 24, q1);
@@ -489,8 +481,8 @@ __device__ __forceinline__ void block_nv(const float (&y)[32], float S, float si
   *reinterpret_cast<uint4*>(d.dnc) = make_uint4(dn0, dn1, dn2, dn3);
   d.dns[0] = (uint8_t)e4m3_bits(q0.d);
   d.dns[1] = (uint8_t)e4m3_bits(q1.d);
-  if (PAT != 24 && d.spd != nullptr && (d.spc != nullptr || d.dbg_mask != nullptr))
-    *reinterpret_cast<uint4*>(d.spd) = expand_block<48>(make_uint2(codes[0], codes[1]), meta);
+  if (d.spd != nullptr)
+    *reinterpret_cast<uint4*>(d.spd) = expand_block<PAT == 24 ? 24 : 48>(make_uint2(codes[0], codes[1]), meta);
   if (d.dbg_mask) *d.dbg_mask = keep_bits<PAT == 49 ? 48 : PAT>(meta);
 }
 
