@@ -49,6 +49,15 @@ def load():
     L.sharq_ref_quantize_weight.restype = ctypes.c_int
     L.sharq_ref_linear.argtypes = [i64, i64, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, vp, i64, vp, vp, vp, i64]
     L.sharq_ref_linear.restype = ctypes.c_int
+    f32, i32 = ctypes.c_float, ctypes.c_int
+    L.sharq_ref_prepare_nv.argtypes = [vp, i64, i64, i64, vp, f32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+    L.sharq_ref_prepare_nv.restype = ctypes.c_int
+    L.sharq_ref_quantize_weight_nv.argtypes = [vp, i64, i64, i64, vp, vp, vp]
+    L.sharq_ref_quantize_weight_nv.restype = ctypes.c_int
+    L.sharq_ref_linear_nv.argtypes = [i64, i64, i32, i32, vp, vp, vp, vp, vp, f32, i64, vp, vp, f32, vp, i64]
+    L.sharq_ref_linear_nv.restype = ctypes.c_int
+    L.sharq_ref_e4m3_code.argtypes = [f32]
+    L.sharq_ref_e4m3_code.restype = ctypes.c_uint8
     L.sharq_ref_set_threads.argtypes = [ctypes.c_int]
     L.sharq_ref_max_threads.restype = ctypes.c_int
     return L

@@ -98,6 +98,8 @@ applied and the fp32 division by d S); the pair score of R8 (the larger
 magnitude rather than the sum); the fp32 SF of R11 (hif4_quantize, rather
 than a bf16 intermediate); the SiLU.mul recipe of R12 (silu_mul_bf16, pinned
 to the exact product within one bf16 step, the recipe itself a choice).
+An independent C implementation of R7 and R8 (sharq_ref.c) agrees with this
+one byte for byte, which guards the code, not the reading.
 """
 
 from __future__ import annotations

@@ -2,6 +2,8 @@
 independent implementations of the same definitions and readings must agree
 byte for byte on every prepared buffer, the keep mask and r, and on the weight
 bytes; their fp64 GEMMs agree to rounding (exactly on exact-sum operands).
+MXFP4 and NVFP4 (with the per-tensor scale's bits, and E4M3 rounding against
+an exhaustive search).
 Also: the C oracle's argument checks return the library's status codes for
 the arguments both validate, and its OpenMP rows do not change results."""
 
@@ -150,6 +152,147 @@ def test_c_threads_do_not_change_results(C):
     C.sharq_ref_set_threads(0)
     for k in O.ACT_BUFFERS:
         assert np.array_equal(outs[0][k], outs[1][k]) and np.array_equal(outs[0][k], outs[2][k])
+
+
+# --------------------------------------------------------------------------- NVFP4
+
+NV_BUFS = ("sp_codes", "sp_meta", "sp_scale", "dn_codes", "dn_scale")
+
+
+def c_prepare_nv(C, x, g, eps, n, m, pairs=False, ts=None):
+    T, K = x.shape
+    out = {"sp_codes": np.zeros((T, K * n // m // 2), np.uint8), "sp_meta": np.zeros((T, K // 8), np.uint8),
+           "sp_scale": np.zeros((T, K // 32), np.uint8), "dn_codes": np.zeros((T, K // 2), np.uint8),
+           "dn_scale": np.zeros((T, K // 16), np.uint8)}
+    tso = np.zeros(1, np.float32)
+    tsi = None if ts is None else np.array([ts], np.float32)
+    x = np.ascontiguousarray(x)
+    st = C.sharq_ref_prepare_nv(ptr(x), T, K, K, ptr(g), eps, n, m, int(pairs), ptr(tsi), ptr(tso),
+                                *(ptr(out[k]) for k in NV_BUFS))
+    assert st == 0, st
+    out["tensor_scale"] = tso[0]
+    return out
+
+
+def assert_nv_prep_equal(c, o, tag):
+    for k in NV_BUFS:
+        assert np.array_equal(c[k], o[k]), (tag, k)
+    assert np.float32(c["tensor_scale"]).view(np.uint32) == np.float32(o["tensor_scale"]).view(np.uint32), tag
+
+
+NV_CASES = [(8, 128, True, 2, 4, False, None), (37, 416, True, 2, 4, False, None),
+            (37, 416, False, 4, 8, False, None), (20, 1024, True, 4, 8, True, None),
+            (9, 3584, True, 2, 4, False, None), (5, 18944, False, 2, 4, False, None),
+            (12, 768, True, 4, 8, True, 0.02), (3, 96, True, 2, 4, False, 3e-4)]
+
+
+@pytest.mark.parametrize("T,K,use_gamma,n,m,pairs,ts", NV_CASES)
+def test_c_prepare_nv_equals_numpy(C, T, K, use_gamma, n, m, pairs, ts):
+    """NVFP4 preparation (per-tensor scale computed or given, 2:4, 4:8, 4:8
+    in pairs): every buffer and the per-tensor scale's bits."""
+    x = synth.activations(T, K, seed=T + K)
+    g = synth.gamma(K, seed=K + 2) if use_gamma else None
+    c = c_prepare_nv(C, x, g, 1e-6, n, m, pairs, ts)
+    o = O.prepare(x, g, 1e-6, n, m, "nv", tensor_scale=ts, pairs=pairs)
+    assert_nv_prep_equal(c, o, f"T{T}K{K}")
+
+
+@pytest.mark.parametrize("kind", ["zeros", "ties", "subnormal", "huge", "mixed"])
+@pytest.mark.parametrize("n,m,pairs", [(2, 4, False), (4, 8, False), (4, 8, True)])
+@pytest.mark.parametrize("use_gamma", [True, False])
+def test_c_prepare_nv_edge_values(C, kind, n, m, pairs, use_gamma):
+    """All-zero input (S = 1, every block scale 0, signed-zero codes), ties,
+    subnormals, huge values and mixed rows whose block scales underflow."""
+    x = special(kind, 12, 256, seed=len(kind) + 7)
+    g = synth.gamma(256, seed=5) if use_gamma else None
+    c = c_prepare_nv(C, x, g, 1e-6, n, m, pairs)
+    with np.errstate(over="ignore", under="ignore"):
+        o = O.prepare(x, g, 1e-6, n, m, "nv", pairs=pairs)
+    assert_nv_prep_equal(c, o, kind)
+
+
+@pytest.mark.parametrize("N,K", [(70, 640), (33, 18944), (5, 96)])
+def test_c_weight_nv_equals_numpy(C, N, K):
+    w = np.ascontiguousarray(synth.weight(N, K, seed=N + K))
+    codes, scale = np.zeros((N, K // 2), np.uint8), np.zeros((N, K // 32), np.uint8)
+    ts = np.zeros(1, np.float32)
+    assert C.sharq_ref_quantize_weight_nv(ptr(w), N, K, K, ptr(codes), ptr(scale), ptr(ts)) == 0
+    o = O.quantize_weight(w, "nv")
+    assert np.array_equal(codes, o["codes"]) and np.array_equal(scale, o["scale"])
+    assert ts.view(np.uint32)[0] == np.float32(o["tensor_scale"]).view(np.uint32)
+
+
+def c_linear_nv(C, o, wq, n, m):
+    T, K, N = o["rows"], o["K"], wq["N"]
+    Y = np.zeros((T, N), np.float64)
+    args = [np.ascontiguousarray(o[k]) for k in NV_BUFS]
+    assert C.sharq_ref_linear_nv(T, K, n, m, *(ptr(a) for a in args), float(o["tensor_scale"]), N,
+                                 ptr(np.ascontiguousarray(wq["codes"])), ptr(np.ascontiguousarray(wq["scale"])),
+                                 float(wq["tensor_scale"]), ptr(Y), N) == 0
+    return Y
+
+
+@pytest.mark.parametrize("T,N,K,n,m,pairs", [(8, 64, 128, 2, 4, False), (33, 100, 1024, 4, 8, True),
+                                             (5, 40, 3584, 2, 4, False)])
+def test_c_linear_nv_agrees_with_numpy(C, T, N, K, n, m, pairs):
+    x = synth.activations(T, K, seed=N + 1)
+    o = O.prepare(x, synth.gamma(K, seed=4), 1e-6, n, m, "nv", pairs=pairs)
+    wq = O.quantize_weight(synth.weight(N, K, seed=T + 1), "nv")
+    y_c, y_o = c_linear_nv(C, o, wq, n, m), O.linear(o, wq)
+    den = O.linear_abs(o, wq)
+    assert np.max(np.abs(y_c - y_o) / np.where(den > 0, den, 1.0)) <= 1e-13
+
+
+def test_c_linear_nv_exact_on_exact_sums(C):
+    """Unit block and tensor scales: every sum is exact in fp64, so the two
+    implementations give identical results; then the same operands with the
+    tensor scales 2^-3 and 2^5, which scale every output exactly."""
+    rng = np.random.default_rng(11)
+    T, N, K = 6, 30, 512
+    keep = np.zeros((T, K), bool)
+    for t in range(T):
+        for g in range(K // 8):
+            keep[t, 8 * g + rng.choice(8, 4, replace=False)] = True
+    sp = np.where(keep, rng.integers(0, 16, (T, K)), 0).astype(np.uint8)
+    spc, spm = O.pack_backbone(sp, keep, 4, 8)
+    one = 0x38   # E4M3 1.0
+    o = {"rows": T, "K": K, "n": 4, "m": 8, "fmt": "nv", "tensor_scale": np.float32(1.0), "mode": "sharq",
+         "sp_codes": spc, "sp_meta": spm, "sp_scale": np.full((T, K // 32), one, np.uint8),
+         "dn_codes": O.pack_nibbles(rng.integers(0, 16, (T, K)).astype(np.uint8)),
+         "dn_scale": np.full((T, K // 16), one, np.uint8)}
+    ws = np.full((N, K // 32), one, np.uint8)
+    wq = {"N": N, "K": K, "fmt": "nv", "tensor_scale": np.float32(1.0),
+          "codes": O.pack_nibbles(rng.integers(0, 16, (N, K)).astype(np.uint8)), "scale": ws,
+          "scale_dn": np.repeat(ws, 2, axis=1)}
+    y1 = c_linear_nv(C, o, wq, 4, 8)
+    assert np.array_equal(y1, O.linear(o, wq))
+    o["tensor_scale"], wq["tensor_scale"] = np.float32(2.0 ** -3), np.float32(2.0 ** 5)
+    assert np.array_equal(c_linear_nv(C, o, wq, 4, 8), y1 * 4.0)
+    assert np.array_equal(O.linear(o, wq), y1 * 4.0)
+
+
+def test_e4m3_rounding_numpy_equals_exhaustive_search(C):
+    """The NumPy oracle's E4M3 rounding (binade arithmetic) against the format's
+    definition, nearest of the 126 finite non-negative values with ties to the
+    even code and saturation at 448, found by exhaustive search in C: every
+    value, every midpoint between neighbours and the floats next to each
+    midpoint, the subnormal range, zero, and values past 448."""
+    vals = O.e4m3_values()
+    mids = (vals[:-1] + vals[1:]) / 2.0
+    probe = [np.float32(0.0), np.float32(2.0 ** -11), np.float32(2.0 ** -10), np.float32(500.0),
+             np.float32(464.0), np.float32(3.0e38)]
+    for v in np.concatenate([vals, mids]).astype(np.float32):
+        probe += [v, np.nextafter(v, np.float32(0.0)), np.nextafter(v, np.float32(np.inf))]
+    rng = np.random.default_rng(3)
+    probe += list((2.0 ** rng.uniform(-12, 10, 4000)).astype(np.float32))
+    a = np.array(probe, np.float32)
+    want = O.e4m3_encode_bits(O.e4m3_round(a))
+    got = np.array([C.sharq_ref_e4m3_code(float(v)) for v in a], np.uint8)
+    bad = np.nonzero(got != want)[0]
+    assert bad.size == 0, [(float(a[i]), int(got[i]), int(want[i])) for i in bad[:5]]
+    # the exhaustive search is the definition: spot values
+    assert C.sharq_ref_e4m3_code(448.0) == 0x7E and C.sharq_ref_e4m3_code(1.0) == 0x38
+    assert C.sharq_ref_e4m3_code(2.0 ** -9) == 0x01 and C.sharq_ref_e4m3_code(2.0 ** -10) == 0x00
 
 
 LIB = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2606_26587_amd",
