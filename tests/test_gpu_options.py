@@ -134,7 +134,8 @@ def test_dense_only_backbone(S, G, T, K, N, use_gamma, n, m, pairs):
     (37, 416, True, 2, 4, False, "mx", False), (64, 4096, True, 2, 4, False, "mx", True),
     (9, 14336, False, 2, 4, False, "mx", True), (20, 1024, True, 4, 8, False, "mx", False),
     (20, 1024, True, 4, 8, True, "nv", False), (17, 3584, True, 2, 4, False, "nv", False),
-    (2048, 4096, True, 2, 4, False, "mx", True)])
+    (2048, 4096, True, 2, 4, False, "mx", True), (20, 1024, True, 4, 8, True, "nv", True),
+    (9, 18944, False, 2, 4, False, "nv", True), (33, 640, True, 4, 8, False, "nv", True)])
 def test_debug_outputs(S, G, T, K, use_gamma, n, m, pairs, fmt, dense):
     """The keep bits of every block and the per-row RMSNorm reciprocal r equal
     the oracle's mask and r; the prepared buffers are unchanged by the debug
@@ -153,3 +154,5 @@ def test_debug_outputs(S, G, T, K, use_gamma, n, m, pairs, fmt, dense):
     dev = L.act_to_device_layout(o)
     for name in O.ACT_BUFFERS:
         G.assert_bytes_equal(f"debug:{name}", G.host(getattr(a, name)), dev[name])
+    if dense:
+        G.assert_bytes_equal("debug:sp_dense", G.host(a.sp_dense), L.dense_backbone_to_device_layout(o))
