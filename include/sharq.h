@@ -346,8 +346,9 @@ SHARQ_API sharq_status sharq_prepare_silu_mul(const void *gate, const void *up, 
  * both products accumulated in one fp32 accumulator and written once.
  * The activation and weight formats must match.  MXFP4 runs on the
  * block-scaled FP4 matrix cores; NVFP4 (whose E4M3 block scales those cannot
- * apply) multiplies the exactly dequantized bf16 values q * d and applies
- * S_x * S_w once to the fp32 sums.  NVFP4 needs a->tensor_scale and
+ * apply) multiplies the exactly dequantized values q * d on 16-bit matrix
+ * cores (fp16 for K a multiple of 128, where every q * d is an exact normal
+ * fp16 value; bf16 otherwise) and applies S_x * S_w once to the fp32 sums.  NVFP4 needs a->tensor_scale and
  * w->tensor_scale.  For the other modes of a->mode, Y is the sum over the
  * mode's paths, each against the weight's view of its kind (sparse view for a
  * sparse path, dense view for a dense one).

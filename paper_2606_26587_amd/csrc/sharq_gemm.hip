@@ -19,7 +19,7 @@
 // through LDS once per K step and read by both MFMAs of every fragment.
 // Also here: the small-M kernel for decode, the grouped (MoE) form, the
 // NVFP4 and HiF4 kernels on 16-bit MFMA over exactly dequantized operands
-// (fp16 in the NVFP4 kernel for K a multiple of 64, bf16 elsewhere), and
+// (fp16 in the NVFP4 kernel for K a multiple of 128, bf16 elsewhere), and
 // the generic kernels of the ablation path combinations.
 
 // MFMA 32x32x64 FP4 operand layout (lane l, 64-wide wavefront): lane l holds
