@@ -100,3 +100,25 @@ def test_prepare_residual_cancellation_and_ties(S, G):
     res[3:] = np.uint16(0x3B80)                    # 2^-8: ties against the integers
     check(S, G, x, res, synth.gamma(K, seed=5), 1e-6, 2, 4, "mx", False, "ties")
     check(S, G, x, res, None, 1e-6, 2, 4, "mx", False, "ties-plain")
+
+
+@pytest.mark.parametrize("T,K,use_gamma,n,m,pairs", [(17, 3584, True, 2, 4, False), (40, 4096, True, 4, 8, True),
+                                                     (6, 18944, False, 2, 4, False)])
+def test_prepare_residual_nv_dense_only(S, G, T, K, use_gamma, n, m, pairs):
+    """NVFP4 with the backbone as its dense copy alone: h, the per-tensor
+    scale, the copy and the other buffers byte-exact against the oracle."""
+    say(f"[residual] nv dense-only T={T} K={K} {n}:{m}{'p' if pairs else ''}")
+    x = synth.activations(T, K, seed=T + K + 5)
+    res = synth.activations(T, K, seed=T + 2 * K + 6)
+    g = synth.gamma(K, seed=K + 1) if use_gamma else None
+    a, h = S.sharq_prepare_residual(G.dev_bf16(x), G.dev_bf16(res), None if g is None else G.dev_bf16(g), 1e-5,
+                                    n, m, "nv", pairs=pairs,
+                                    out=S.alloc_act(T, K, n, m, "nv", "cuda", pairs, dense_only=True))
+    torch.cuda.synchronize()
+    o = O.prepare_residual(x, res, g, 1e-5, n, m, "nv", pairs=pairs)
+    G.assert_bytes_equal("h", G.host(h.view(torch.int16)).view(np.uint16), o["h"])
+    assert f32_bits(G.host(a.tensor_scale)[0]) == f32_bits(o["tensor_scale"])
+    G.assert_bytes_equal("sp_dense", G.host(a.sp_dense), L.dense_backbone_to_device_layout(o))
+    dev = L.act_to_device_layout(o)
+    for name in ("sp_scale", "dn_codes", "dn_scale"):
+        G.assert_bytes_equal(name, G.host(getattr(a, name)), dev[name])

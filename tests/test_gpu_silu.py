@@ -123,3 +123,22 @@ def test_silu_mul_empty(S, G):
     a = S.sharq_prepare_silu_mul(e, e, 2, 4, "mx")
     torch.cuda.synchronize()
     assert a.rows == 0
+
+
+@pytest.mark.parametrize("T,K,n,m,pairs", [(33, 3584, 2, 4, False), (23, 1024, 4, 8, True)])
+def test_silu_mul_prep_nv_dense_only(S, G, T, K, n, m, pairs):
+    """NVFP4 SiLU.mul preparation with the backbone as its dense copy alone:
+    the copy and the other buffers byte-exact against the oracle."""
+    say(f"[silu] nv dense-only T={T} K={K} {n}:{m}{'p' if pairs else ''}")
+    gate = synth.activations(T, K, seed=T + 11)
+    up = synth.activations(T, K, seed=T + 12)
+    a = S.sharq_prepare_silu_mul(G.dev_bf16(gate), G.dev_bf16(up), n, m, "nv", pairs=pairs,
+                                 out=S.alloc_act(T, K, n, m, "nv", "cuda", pairs, dense_only=True))
+    torch.cuda.synchronize()
+    o = O.prepare_silu_mul(gate, up, n, m, "nv", pairs=pairs)
+    got = np.asarray(G.host(a.tensor_scale)[0], np.float32).view(np.uint32)
+    assert got == np.asarray(o["tensor_scale"], np.float32).view(np.uint32)
+    G.assert_bytes_equal("sp_dense", G.host(a.sp_dense), L.dense_backbone_to_device_layout(o))
+    dev = L.act_to_device_layout(o)
+    for name in ("sp_scale", "dn_codes", "dn_scale"):
+        G.assert_bytes_equal(name, G.host(getattr(a, name)), dev[name])
