@@ -78,6 +78,8 @@ DECODE_W_SETS = 5             # decode: weight copies rotate between steps (5 x 
 # gives).  Valid only for the GEMM source it was measured on (sha256 prefix);
 # reported as null once that source has changed.
 TRAFFIC = {"gemm_source": "9a3f8104bbfaf0cf", "bytes_per_launch": 270.33e6}
+# the same for the MoE workload's k_linear_mx_grouped_persist<0> (mean of its gate_up and down launches)
+MOE_TRAFFIC = {"gemm_source": "9a3f8104bbfaf0cf", "bytes_per_launch": 464.7e6}
 
 
 def log(*a):
@@ -687,9 +689,16 @@ def moe(args, torch, S, synth, dev, stream):
                       (f1 + f2) / (ms_step * 1e-3) / 1e12, "TFLOP/s", ms_step, "mxfp4",
                       {"workload": f"Qwen3-30B-A3B experts: {T} tokens, top-{k} of {E}, gate_up {2 * I}x{H} "
                                    f"(RMSNorm), down {H}x{I}; 4:8; MXFP4", "tokens": T, "routed_rows": total})
-    out["roofline"] = {"bound": "mfma", "kernel": "k_linear_mx_grouped", "achieved": (f1 + f2) / t_g / 1e12,
-                       "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s", "frac": (f1 + f2) / t_g / 1e12 / PEAK_FP4_TFLOPS,
-                       "traffic": None}
+    traffic = None
+    if MOE_TRAFFIC is not None and MOE_TRAFFIC["gemm_source"] == gemm_source_digest():
+        traffic = MOE_TRAFFIC["bytes_per_launch"]
+    out["roofline"] = {"bound": "mfma",
+                       "kernel": "k_linear_mx_grouped_persist<0> (grouped two-path FP4 GEMM reading the dense "
+                                 "backbone copy)",
+                       "achieved": (f1 + f2) / t_g / 1e12, "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s",
+                       "frac": (f1 + f2) / t_g / 1e12 / PEAK_FP4_TFLOPS, "traffic": traffic, "flops": "F_alg",
+                       "traffic_note": "HBM-side bytes per launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain "
+                                       "copy's counters), mean of the gate_up and down launches"}
     out["ops"] = ops
     return out
 
