@@ -515,7 +515,11 @@ __device__ __forceinline__ void read_bw(uint32_t (&bw)[2], const uint8_t* stage,
 // expansion of raw (step k+1; its residual codes are loaded into opsn.dn by
 // `issue`); wst (step k+2) stored to stage `wr`.  issue(part) issues part
 // 0-5 of the step's global loads (a std::integral_constant argument).
-template <int PAT, class Issue>
+// SPR = 0: the six parts go out behind the first six MFMAs; SPR = 1: spread
+// over the whole step, two slots of each group of eight apart (the schedule of
+// the row-gathering grouped GEMM, whose scattered activation rows make each
+// load slower to issue; for contiguous rows the burst is faster).
+template <int PAT, int SPR = 0, class Issue>
 __device__ __forceinline__ void step5(v16f (&acc)[8], const AOps& ops, uint4 (&b0)[8], const uint32_t (&bw)[4],
                                       uint32_t (&bwn)[4], const uint8_t* cur, const uint8_t* nxt, uint8_t* wr,
                                       AOps& opsn, const AStep& raw, const WStep<8>& wst, int lane, Issue issue,
@@ -534,15 +538,26 @@ __device__ __forceinline__ void step5(v16f (&acc)[8], const AOps& ops, uint4 (&b
   // global loads of later steps go out in six parts behind the first MFMAs
   mma_sp<0, 0>(acc, ops, b0, bw); issue(std::integral_constant<int, 0>()); read_b<1, 0, 1>(b1, cur, lane);
   put_piece<PAT, 0>(opsn, raw, sel); SHARQ_FENCE();
-  mma_sp<0, 1>(acc, ops, b0, bw); issue(std::integral_constant<int, 1>()); read_b<1, 1, 2>(b1, cur, lane);
+  mma_sp<0, 1>(acc, ops, b0, bw);
+  if constexpr (SPR == 0) issue(std::integral_constant<int, 1>());
+  read_b<1, 1, 2>(b1, cur, lane);
   SHARQ_FENCE();
-  mma_sp<0, 2>(acc, ops, b0, bw); issue(std::integral_constant<int, 2>()); read_b<1, 2, 3>(b1, cur, lane);
+  mma_sp<0, 2>(acc, ops, b0, bw);
+  if constexpr (SPR == 0) issue(std::integral_constant<int, 2>());
+  read_b<1, 2, 3>(b1, cur, lane);
   put_piece<PAT, 1>(opsn, raw, sel); SHARQ_FENCE();
-  mma_sp<0, 3>(acc, ops, b0, bw); issue(std::integral_constant<int, 3>()); read_b<1, 3, 4>(b1, cur, lane);
+  mma_sp<0, 3>(acc, ops, b0, bw);
+  if constexpr (SPR == 0) issue(std::integral_constant<int, 3>());
+  read_b<1, 3, 4>(b1, cur, lane);
   SHARQ_FENCE();
-  mma_sp<0, 4>(acc, ops, b0, bw); issue(std::integral_constant<int, 4>()); read_b<1, 4, 5>(b1, cur, lane);
+  mma_sp<0, 4>(acc, ops, b0, bw);
+  if constexpr (SPR == 0) issue(std::integral_constant<int, 4>());
+  read_b<1, 4, 5>(b1, cur, lane);
   put_piece<PAT, 2>(opsn, raw, sel); SHARQ_FENCE();
-  mma_sp<0, 5>(acc, ops, b0, bw); issue(std::integral_constant<int, 5>()); read_b<1, 5, 6>(b1, cur, lane);
+  mma_sp<0, 5>(acc, ops, b0, bw);
+  if constexpr (SPR == 0) issue(std::integral_constant<int, 5>());
+  else issue(std::integral_constant<int, 1>());
+  read_b<1, 5, 6>(b1, cur, lane);
   SHARQ_FENCE();
   mma_sp<0, 6>(acc, ops, b0, bw); read_b<1, 6, 7>(b1, cur, lane); put_piece<PAT, 3>(opsn, raw, sel); SHARQ_FENCE();
   mma_sp<0, 7>(acc, ops, b0, bw); read_b<1, 7, 8>(b1, cur, lane); SHARQ_FENCE();
@@ -551,7 +566,9 @@ __device__ __forceinline__ void step5(v16f (&acc)[8], const AOps& ops, uint4 (&b
   mma_dn<0, 1>(acc, ops, b0, bw);
   *reinterpret_cast<uint4*>(wr + (tid >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[0];
   SHARQ_FENCE();
-  mma_dn<0, 2>(acc, ops, b0, bw); put_piece<PAT, 5>(opsn, raw, sel); SHARQ_FENCE();
+  mma_dn<0, 2>(acc, ops, b0, bw); put_piece<PAT, 5>(opsn, raw, sel);
+  if constexpr (SPR == 1) issue(std::integral_constant<int, 2>());
+  SHARQ_FENCE();
   mma_dn<0, 3>(acc, ops, b0, bw);
   *reinterpret_cast<uint4*>(wr + ((tid + 256) >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[1];
   SHARQ_FENCE();
@@ -559,7 +576,9 @@ __device__ __forceinline__ void step5(v16f (&acc)[8], const AOps& ops, uint4 (&b
   mma_dn<0, 5>(acc, ops, b0, bw);
   *reinterpret_cast<uint4*>(wr + ((tid + 512) >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[2];
   SHARQ_FENCE();
-  mma_dn<0, 6>(acc, ops, b0, bw); put_piece<PAT, 7>(opsn, raw, sel); SHARQ_FENCE();
+  mma_dn<0, 6>(acc, ops, b0, bw); put_piece<PAT, 7>(opsn, raw, sel);
+  if constexpr (SPR == 1) issue(std::integral_constant<int, 3>());
+  SHARQ_FENCE();
   mma_dn<0, 7>(acc, ops, b0, bw);
   *reinterpret_cast<uint4*>(wr + ((tid + 768) >> 2) * kLdsStride + 16 * (tid & 3)) = wst.q[3];
   SHARQ_FENCE();
@@ -573,11 +592,15 @@ __device__ __forceinline__ void step5(v16f (&acc)[8], const AOps& ops, uint4 (&b
     *reinterpret_cast<uint16_t*>(wr + kStageW + (2 * c + 1) * 16 + 2 * f) = (uint16_t)(wst.s >> 16);
   }
   SHARQ_FENCE();
-  mma_sp<1, 2>(acc, ops, b1, bw); put_piece<PAT, 9>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<1, 2>(acc, ops, b1, bw); put_piece<PAT, 9>(opsn, raw, sel);
+  if constexpr (SPR == 1) issue(std::integral_constant<int, 4>());
+  SHARQ_FENCE();
   mma_sp<1, 3>(acc, ops, b1, bw); read_b<0, 0, 1>(b0, nxt, lane); SHARQ_FENCE();
   mma_sp<1, 4>(acc, ops, b1, bw); put_piece<PAT, 10>(opsn, raw, sel); SHARQ_FENCE();
   mma_sp<1, 5>(acc, ops, b1, bw); read_b<0, 1, 2>(b0, nxt, lane); SHARQ_FENCE();
-  mma_sp<1, 6>(acc, ops, b1, bw); put_piece<PAT, 11>(opsn, raw, sel); SHARQ_FENCE();
+  mma_sp<1, 6>(acc, ops, b1, bw); put_piece<PAT, 11>(opsn, raw, sel);
+  if constexpr (SPR == 1) issue(std::integral_constant<int, 5>());
+  SHARQ_FENCE();
   mma_sp<1, 7>(acc, ops, b1, bw); read_b<0, 2, 3>(b0, nxt, lane); SHARQ_FENCE();
   // ---- sub-step 1, residual
   mma_dn<1, 0>(acc, ops, b1, bw); put_piece<PAT, 12>(opsn, raw, sel); read_b<0, 3, 4>(b0, nxt, lane); SHARQ_FENCE();
@@ -837,14 +860,15 @@ __device__ __forceinline__ void store_tile_lds(const v16f (&acc)[NF], OutT* Y, i
   }
 }
 
-// One K step of a full (NF = 8) or half (NF = 4) tile.
-template <int PAT, int NF, class Issue>
+// One K step of a full (NF = 8) or half (NF = 4) tile; SPR: the load
+// schedule of step5.
+template <int PAT, int SPR = 0, int NF, class Issue>
 __device__ __forceinline__ void step_il(v16f (&acc)[NF], const AOps& ops, uint4 (&b0)[NF],
                                         const uint32_t (&bw)[NF / 2], uint32_t (&bwn)[NF / 2], const uint8_t* cur,
                                         const uint8_t* nxt, uint8_t* wr, AOps& opsn, const AStep& raw,
                                         const WStep<NF>& wst, int lane, Issue issue, const uint2* lut) {
   if constexpr (NF == 8)
-    step5<PAT>(acc, ops, b0, bw, bwn, cur, nxt, wr, opsn, raw, wst, lane, issue, lut);
+    step5<PAT, SPR>(acc, ops, b0, bw, bwn, cur, nxt, wr, opsn, raw, wst, lane, issue, lut);
   else
     step5h<PAT>(acc, ops, b0, bw, bwn, cur, nxt, wr, opsn, raw, wst, lane, issue, lut);
 }
@@ -910,7 +934,7 @@ __device__ __forceinline__ void il_start(IlSets<NF>& p, const uint8_t* wc, const
 }
 
 // Every K step of a started tile into acc.
-template <int PAT, int NF>
+template <int PAT, int NF, int SPR = 0>
 __device__ __forceinline__ void il_main(v16f (&acc)[NF], IlSets<NF>& p, uint4 (&b0)[NF], uint32_t (&bwa)[NF / 2],
                                         const ARow& a, const uint8_t* wc, const uint8_t* ws, int n0, int N, int K,
                                         uint8_t* lds, int lane, int half, const uint2* lut) {
@@ -922,7 +946,7 @@ __device__ __forceinline__ void il_main(v16f (&acc)[NF], IlSets<NF>& p, uint4 (&
   uint32_t bwb[NF / 2];
   int ks = 0;
   for (; ks + 2 < nks; ks += 3) {
-    step_il<PAT>(acc, p.o0, b0, bwa, bwb, st0, st1, st2, p.o1, p.r1, p.w2, lane, [&](auto part) {
+    step_il<PAT, SPR>(acc, p.o0, b0, bwa, bwb, st0, st1, st2, p.o1, p.r1, p.w2, lane, [&](auto part) {
       constexpr int P = decltype(part)::value;
       if constexpr (P == 0) load_a_dn(p.o2, a, cl(ks + 2), half);
       else if constexpr (P == 1) load_a_meta_part<PAT, 0>(p.r0, a, cl(ks + 3), half);
@@ -930,7 +954,7 @@ __device__ __forceinline__ void il_main(v16f (&acc)[NF], IlSets<NF>& p, uint4 (&
       else load_w_part<NF, P - 3>(p.w1, wc, ws, n0, N, cl(ks + 4));
     }, lut);
     __syncthreads();
-    step_il<PAT>(acc, p.o1, b0, bwb, bwa, st1, st2, st0, p.o2, p.r2, p.w0, lane, [&](auto part) {
+    step_il<PAT, SPR>(acc, p.o1, b0, bwb, bwa, st1, st2, st0, p.o2, p.r2, p.w0, lane, [&](auto part) {
       constexpr int P = decltype(part)::value;
       if constexpr (P == 0) load_a_dn(p.o0, a, cl(ks + 3), half);
       else if constexpr (P == 1) load_a_meta_part<PAT, 0>(p.r1, a, cl(ks + 4), half);
@@ -938,7 +962,7 @@ __device__ __forceinline__ void il_main(v16f (&acc)[NF], IlSets<NF>& p, uint4 (&
       else load_w_part<NF, P - 3>(p.w2, wc, ws, n0, N, cl(ks + 5));
     }, lut);
     __syncthreads();
-    step_il<PAT>(acc, p.o2, b0, bwa, bwb, st2, st0, st1, p.o0, p.r0, p.w1, lane, [&](auto part) {
+    step_il<PAT, SPR>(acc, p.o2, b0, bwa, bwb, st2, st0, st1, p.o0, p.r0, p.w1, lane, [&](auto part) {
       constexpr int P = decltype(part)::value;
       if constexpr (P == 0) load_a_dn(p.o1, a, cl(ks + 4), half);
       else if constexpr (P == 1) load_a_meta_part<PAT, 0>(p.r2, a, cl(ks + 5), half);
@@ -955,10 +979,10 @@ __device__ __forceinline__ void il_main(v16f (&acc)[NF], IlSets<NF>& p, uint4 (&
     }
   }
   if (ks < nks) {   // one or two steps left, in sets 0 and 1
-    step_il<PAT>(acc, p.o0, b0, bwa, bwb, st0, st1, st2, p.o1, p.r1, p.w2, lane, [](auto) {}, lut);
+    step_il<PAT, SPR>(acc, p.o0, b0, bwa, bwb, st0, st1, st2, p.o1, p.r1, p.w2, lane, [](auto) {}, lut);
     if (ks + 1 < nks) {
       __syncthreads();
-      step_il<PAT>(acc, p.o1, b0, bwb, bwa, st1, st2, st0, p.o2, p.r2, p.w0, lane, [](auto) {}, lut);
+      step_il<PAT, SPR>(acc, p.o1, b0, bwb, bwa, st1, st2, st0, p.o2, p.r2, p.w0, lane, [](auto) {}, lut);
     }
   }
 }
@@ -1053,7 +1077,7 @@ struct IlTile {
 // issue order, so loads issued behind the stores would first wait for the
 // stores (64 KB per tile) to drain.  The epilogue therefore has its own LDS
 // region `epi` (4 kEpiWave bytes) beside the three stages at `lds`.
-template <int PAT, typename OutT, class Next>
+template <int PAT, typename OutT, int SPR = 0, class Next>
 __device__ __forceinline__ void tiles_mx_il(const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale,
                                             const uint8_t* dn_codes, const uint8_t* dn_scale, int64_t act_rows, int N,
                                             int K, OutT* Y, int64_t ldy, uint8_t* lds, uint8_t* epi,
@@ -1082,7 +1106,7 @@ __device__ __forceinline__ void tiles_mx_il(const uint8_t* sp_codes, const uint8
     for (int f = 0; f < 8; ++f)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[f][r] = 0.0f;
-    il_main<PAT, 8>(acc, p, b0, bwa, a, t.wc, t.ws, t.n0, N, K, lds, lane, half, lut);
+    il_main<PAT, 8, SPR>(acc, p, b0, bwa, a, t.wc, t.ws, t.n0, N, K, lds, lane, half, lut);
     if (more) {
       a.r = tn.r;
       il_issue<PAT, 8>(p, a, tn.wc, tn.ws, tn.n0, N, K, half);
@@ -1302,8 +1326,10 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped(
 // had fallen outside the earlier numbering, which required a multiple of 8,
 // and were spread round-robin over the XCDs.  A last round at most half
 // full runs as half tiles, as in the dense kernel (gate_up's 110 leftover
-// units as 220 halves: 164.4 -> 162.8 us).
-template <int PAT, typename OutT>
+// units as 220 halves: 164.4 -> 162.8 us).  GATHER (a row map is given):
+// full tiles take the spread load schedule of step5 (gate_up 165 -> 154 us,
+// bit-identical; contiguous rows keep the burst, which is faster for them).
+template <int PAT, typename OutT, bool GATHER = false>
 __global__ __launch_bounds__(256) void k_linear_mx_grouped_persist(
     const uint8_t* sp_codes, const uint8_t* sp_meta, const uint8_t* sp_scale, const uint8_t* dn_codes,
     const uint8_t* dn_scale, const int32_t* row_index, int64_t act_rows, const int32_t* offs, int E,
@@ -1359,7 +1385,7 @@ __global__ __launch_bounds__(256) void k_linear_mx_grouped_persist(
   // [x per, (x + 1) per); ids whose unit is past the last are skipped.
   const int per = (full + 7) >> 3;
   int id = (int)blockIdx.x;
-  tiles_mx_il<PAT, OutT>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, act_rows, N, K, Y, ldy, lds,
+  tiles_mx_il<PAT, OutT, GATHER ? 1 : 0>(sp_codes, sp_meta, sp_scale, dn_codes, dn_scale, act_rows, N, K, Y, ldy, lds,
                          lds + 3 * kStageBytes, lut48, [&](IlTile& t) {
                            int u = full;
                            while (u >= full) {
@@ -2774,8 +2800,12 @@ static hipError_t go_grouped(const uint8_t* spc, const uint8_t* spm, const uint8
   if constexpr (SDW && NF == 8) {
     const int64_t bound = (int64_t)gx * items, cus = device_cus();
     const unsigned g = (unsigned)(bound < cus ? bound : cus);
-    k_linear_mx_grouped_persist<PAT, OutT><<<dim3(g), dim3(256), 0, st>>>(
-        spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx);
+    if (ridx)
+      k_linear_mx_grouped_persist<PAT, OutT, true><<<dim3(g), dim3(256), 0, st>>>(
+          spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx);
+    else
+      k_linear_mx_grouped_persist<PAT, OutT, false><<<dim3(g), dim3(256), 0, st>>>(
+          spc, spm, sps, dnc, dns, ridx, act_rows, offs, E, wc, ws, N, K, reinterpret_cast<OutT*>(Y), ldy, gx);
     return hipGetLastError();
   }
   dim3 grid((unsigned)(gx * items)), block(256);
