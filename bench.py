@@ -77,9 +77,9 @@ DECODE_W_SETS = 5             # decode: weight copies rotate between steps (5 x 
 # (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors a plain 1 GiB device copy
 # gives).  Valid only for the GEMM source it was measured on (sha256 prefix);
 # reported as null once that source has changed.
-TRAFFIC = {"gemm_source": "9a3f8104bbfaf0cf", "bytes_per_launch": 270.33e6}
+TRAFFIC = {"gemm_source": "54b1cdd92ca6fd6a", "bytes_per_launch": 270.32e6}
 # the same for the MoE workload's k_linear_mx_grouped_persist<0> (mean of its gate_up and down launches)
-MOE_TRAFFIC = {"gemm_source": "9a3f8104bbfaf0cf", "bytes_per_launch": 464.7e6}
+MOE_TRAFFIC = {"gemm_source": "54b1cdd92ca6fd6a", "bytes_per_launch": 436.6e6}
 
 
 def log(*a):
