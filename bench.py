@@ -66,7 +66,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 
 METRIC = "SharQ linear TFLOPS (prep+2 FP4 GEMMs) & prep HBM GB/s, Llama-8B M=2048"
 PEAK_FP4_TFLOPS = 10100.0     # MI355X dense MXFP4 MFMA
-PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 (and fp16) MFMA
+PEAK_16BIT_TFLOPS = 2500.0    # MI355X dense fp16 and bf16 MFMA
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
 T_TOKENS = 2048
 N_INPUT_SETS = 2              # activations rotate between steps (defeats the 256 MB last-level cache)
@@ -428,7 +428,7 @@ def mfma_probe(torch, dev, stream, iters=PROBE_ITERS, reps=3, kind="fp4"):
     instruction on the part as it runs under that load, beside the published
     peak at the rated clock."""
     name, flops_per_mfma, desc = PROBES[kind]
-    peak = PEAK_FP4_TFLOPS if kind == "fp4" else PEAK_BF16_TFLOPS
+    peak = PEAK_FP4_TFLOPS if kind == "fp4" else PEAK_16BIT_TFLOPS
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2606_26587_amd", "libsharq_probe.so"))
     fn = getattr(lib, name)
     fn.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
@@ -466,9 +466,9 @@ def nv_roofline(torch, dev, stream, per, t_gemm):
     log(f"[bench] fp16 MFMA probe: {sus['achieved']:.0f} TFLOP/s sustained at {sus['clock_GHz']:.2f} GHz; "
         f"GEMM executed work at {f_exec / t_gemm / 1e12 / sus['achieved']:.2f} of it")
     return {"bound": "mfma", "kernel": "k_linear_nv_il (fp16 MFMA over dequantized FP4)",
-            "achieved": flops / t_gemm / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": flops / t_gemm / 1e12 / PEAK_BF16_TFLOPS, "traffic": None, "flops": "F_alg",
-            "achieved_exec": f_exec / t_gemm / 1e12, "frac_exec": f_exec / t_gemm / 1e12 / PEAK_BF16_TFLOPS,
+            "achieved": flops / t_gemm / 1e12, "peak": PEAK_16BIT_TFLOPS, "unit": "TFLOP/s",
+            "frac": flops / t_gemm / 1e12 / PEAK_16BIT_TFLOPS, "traffic": None, "flops": "F_alg",
+            "achieved_exec": f_exec / t_gemm / 1e12, "frac_exec": f_exec / t_gemm / 1e12 / PEAK_16BIT_TFLOPS,
             "sustained_mfma": sus, "frac_exec_of_sustained": f_exec / t_gemm / 1e12 / sus["achieved"],
             "frac_alg_of_sustained": flops / t_gemm / 1e12 / sus["achieved"]}
 
