@@ -292,7 +292,8 @@ def nv_exact_operands(T, N, K, n, m, variant, seed):
 NV_EXACT_CASES = ([("gate_up", 2, 4, "act_hi"), ("gate_up", 2, 4, "w_lo"), ("down", 2, 4, "act_lo"),
                    ("down", 2, 4, "w_hi")]
                   + [("ragged", n, m, v) for n, m in ((2, 4), (4, 8)) for v in sorted(NV_EXACT_SCALES)]
-                  + [("mid", 4, 8, v) for v in sorted(NV_EXACT_SCALES)])
+                  + [("mid", 4, 8, v) for v in sorted(NV_EXACT_SCALES)]
+                  + [("llama_qkv", 4, 8, "act_lo"), ("llama_down", 4, 8, "w_hi")])
 
 
 @pytest.mark.parametrize("name,n,m,variant", NV_EXACT_CASES)
@@ -302,13 +303,19 @@ def test_nv_exact_sums(S, G, name, n, m, variant):
     output must equal the oracle's exact result bit for bit.  The Qwen2.5-7B
     shapes at M = 4096 run the persistent fp16 kernel (256 sampled rows, all
     columns; each shape takes two of the four scale ranges), and so does the
-    4:8 case with ragged rows and columns; the ragged case (K not a multiple
+    4:8 case with ragged rows and columns, and 4:8 at two Llama-3.1-8B shapes
+    at M = 2048 (the NVFP4 4:8-in-pairs benchmark's); the ragged case (K not a multiple
     of 128) the bf16 one (all outputs, every range).  Each runs on the
     compressed backbone and on its dense copy (read where K is a multiple of
     128)."""
     if name in ("ragged", "mid"):
         T, K, N = (300, 416, 520) if name == "ragged" else (300, 1024, 520)
         rows = np.arange(T)
+    elif name.startswith("llama_"):
+        K, N, _ = synth.LLAMA_LINEARS[name[6:]]
+        T = 2048
+        rows = np.random.default_rng(6).choice(T, 256, replace=False)
+        rows[0], rows[1] = 0, T - 1
     else:
         K, N, _ = synth.QWEN_LINEARS[name]
         T = QWEN_T
