@@ -147,3 +147,65 @@ def test_hif4_llama_full_shape(S, G, name):
     rows = np.random.default_rng(2).choice(2048, 256, replace=False)
     rows[0], rows[1] = 0, 2048 - 1
     gemm_check(G.host(y)[rows], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), name)
+
+
+def hif4_exact_operands(T, N, K, seed):
+    """A HiF4 prepared activation (2:4) and weight built directly from codes
+    and unit metadata: activation units with E6M2 scales in {1/2, 1, 2},
+    weight units with every mantissa, {1, 1.25, 1.5, 1.75}, and random
+    micro-exponent bits on both sides.  Every activation value is a multiple of
+    1/8 and every weight value of 1/16, so every product is a multiple of
+    1/128; the S1P2 magnitudes are limited so that the at most 2K products of
+    an output, each below max|a| max|w|, stay below 2^24 / 128: every fp32
+    partial sum is then exact whatever the order."""
+    rng = np.random.default_rng(seed)
+    ma, mw = 7, 7
+    while 2 * K * (ma / 4 * 4 * 2) * (mw / 4 * 4 * 1.75) * 128 >= 2.0 ** 24:
+        if ma >= mw:
+            ma -= 1
+        else:
+            mw -= 1
+    keep = np.zeros((T, K // 4, 4), bool)
+    order = rng.random((T, K // 4, 4)).argsort(axis=2)[..., :2]
+    np.put_along_axis(keep, order, True, axis=2)
+    keep = keep.reshape(T, K)
+
+    def codes(shape, mmax):
+        return (rng.integers(0, mmax + 1, size=shape) | (rng.integers(0, 2, size=shape) << 3)).astype(np.uint8)
+
+    def meta(rows, bases):
+        U = K // 64
+        m = np.zeros((rows, U, 4), np.uint8)
+        m[..., 0] = np.asarray(bases, np.uint8)[rng.integers(0, len(bases), size=(rows, U))]
+        m[..., 1:] = rng.integers(0, 256, size=(rows, U, 3))
+        return m.reshape(rows, U * 4)
+
+    act_bases, w_bases = [47 * 4, 48 * 4, 49 * 4], [48 * 4, 48 * 4 + 1, 48 * 4 + 2, 48 * 4 + 3]
+    sp = np.where(keep, codes((T, K), ma), 0).astype(np.uint8)
+    sp_codes, sp_meta = O.pack_backbone(sp, keep, 2, 4)
+    act = {"rows": T, "K": K, "n": 2, "m": 4, "pairs": False, "fmt": "hif4", "tensor_scale": None, "mode": "sharq",
+           "sp_codes": sp_codes, "sp_meta": sp_meta, "sp_scale": meta(T, act_bases),
+           "dn_codes": O.pack_nibbles(codes((T, K), ma)), "dn_scale": meta(T, act_bases),
+           "dn_meta": np.zeros((T, 0), np.uint8)}
+    wm = meta(N, w_bases)
+    wq = {"N": N, "K": K, "fmt": "hif4", "codes": O.pack_nibbles(codes((N, K), mw)), "scale": wm, "scale_dn": wm,
+          "tensor_scale": None}
+    return act, wq, (ma, mw)
+
+
+@pytest.mark.parametrize("T,N,K", [(300, 520, 1024), (130, 300, 448), (2048, 4096, 4096)])
+def test_hif4_exact_sums(S, G, T, N, K):
+    """The HiF4 GEMM on operands whose sums are exact in fp32: the output
+    equals the oracle's exact result bit for bit (all rows, or 256 sampled at
+    M = 2048), so a dropped or repeated product or a misread micro-exponent,
+    E6M2 mantissa or unit shows."""
+    o, wo, mags = hif4_exact_operands(T, N, K, seed=T + N + K)
+    say(f"[hif4-exact] T={T} N={N} K={K} code magnitude limits {mags}")
+    y = S.sharq_linear(G.oracle_to_act(o), G.oracle_to_weight(wo), dtype=torch.float32)
+    torch.cuda.synchronize()
+    rows = np.arange(T) if T <= 512 else np.random.default_rng(7).choice(T, 256, replace=False)
+    ref = O.linear(o, wo, rows=rows)
+    got = G.host(y)[rows].astype(np.float64)
+    bad = np.nonzero(got != ref)
+    assert bad[0].size == 0, (f"{bad[0].size} outputs differ from the exact sum; first at {bad[0][0]},{bad[1][0]}: "
+                              f"{got[bad[0][0], bad[1][0]]} vs {ref[bad[0][0], bad[1][0]]}")
