@@ -342,6 +342,55 @@ def test_exact_sums_full_shape(S, G, name, variant):
                                   f"vs {ref[bad[0][0], bad[1][0]]}")
 
 
+@pytest.mark.parametrize("name,T,variant", [("qkv", 1, "unit"), ("gate_up", 4, "act"), ("down", 16, "weight"),
+                                            ("gate_up", 32, "unit"), ("down", 64, "act"), ("qkv", 256, "weight")])
+def test_exact_sums_decode(S, G, name, T, variant):
+    """The small-M kernels (K split over wavefronts, partial tiles added in
+    LDS) on exact-sum operands at the Llama shapes: the output equals the
+    oracle's exact result bit for bit, on the dense backbone copy and on the
+    compressed backbone, so a lost or doubled partial tile shows."""
+    K, N, _ = synth.LLAMA_LINEARS[name]
+    say(f"[exact-decode] {name} T={T} K={K} N={N} variant={variant}")
+    o, wo = exact_operands(T, N, K, variant, seed=K + N + T)
+    w = G.oracle_to_weight(wo)
+    yd = S.sharq_linear(G.oracle_to_act(o, dense_backbone=True), w, dtype=torch.float32)
+    yc = S.sharq_linear(G.oracle_to_act(o), w, dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = O.linear(o, wo)
+    for tag, y in (("dense copy", yd), ("compressed", yc)):
+        got = G.host(y).astype(np.float64)
+        bad = np.nonzero(got != ref)
+        assert bad[0].size == 0, (f"{name} T={T} {variant} {tag}: {bad[0].size} outputs differ from the exact sum; "
+                                  f"first at {bad[0][0]},{bad[1][0]}")
+
+
+@pytest.mark.parametrize("gather", [True, False])
+def test_exact_sums_grouped(S, G, gather):
+    """The grouped GEMM on exact-sum operands (unit scales, all codes): with
+    a row map (the gathering kernel and its spread load schedule) and on
+    expert-sorted rows, on the dense backbone copy and on the compressed
+    backbone, the output equals the oracle's exact result bit for bit."""
+    T, E, topk, K, N = 512, 16, 4, 2048, 520
+    row_index, offs = synth.router_topk(T, E, topk, seed=3)
+    total = int(offs[-1])
+    rows = T if gather else total
+    say(f"[exact-grouped] gather={gather} rows={rows} total={total} E={E} K={K} N={N}")
+    o, _ = exact_operands(rows, 32, K, "unit", seed=5)
+    wos = [exact_operands(1, N, K, "unit", seed=100 + e)[1] for e in range(E)]
+    w = S.stack_weights([G.oracle_to_weight(wo) for wo in wos])
+    ri = torch.from_numpy(row_index).cuda() if gather else None
+    of = torch.from_numpy(offs).cuda()
+    yd = S.sharq_linear_grouped(G.oracle_to_act(o, dense_backbone=True), ri, of, total, w, dtype=torch.float32)
+    yc = S.sharq_linear_grouped(G.oracle_to_act(o), ri, of, total, w, dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = O.linear_grouped(o, row_index if gather else None, offs, wos)
+    for tag, y in (("dense copy", yd), ("compressed", yc)):
+        got = G.host(y).astype(np.float64)
+        bad = np.nonzero(got != ref)
+        assert bad[0].size == 0, (f"gather={gather} {tag}: {bad[0].size} outputs differ from the exact sum; "
+                                  f"first at {bad[0][0]},{bad[1][0]}")
+
+
 # --------------------------------------------------------------------------- decode shapes
 
 @pytest.mark.parametrize("name,T", [("qkv", 1), ("qkv", 16), ("gate_up", 1), ("gate_up", 16), ("gate_up", 32),
