@@ -185,3 +185,57 @@ def test_mode_llama_qkv_full_shape(S, G, mode):
     rows = np.random.default_rng(2).choice(LLAMA_T, 256, replace=False)
     rows[0], rows[1] = 0, LLAMA_T - 1
     gemm_check(G.host(y)[rows], O.linear(o, wo, rows=rows), O.linear_abs(o, wo, rows=rows), f"qkv-{mode}")
+
+
+def mode_exact_operands(T, N, K, n, m, fmt, mode, seed):
+    """Operands of a path combination built directly from random codes (every
+    code) under unit block scales (E8M0 127, or E4M3 1.0 with unit per-tensor
+    scales): every product is a multiple of 1/4 below 36 and 2 K 36 < 2^22, so
+    every fp32 partial sum is exact whatever the order."""
+    rng = np.random.default_rng(seed)
+    one = 127 if fmt == "mx" else 0x38
+
+    def codes(shape):
+        return rng.integers(0, 16, size=shape).astype(np.uint8)
+
+    def path(kind):
+        if kind is None:
+            z = np.zeros((T, 0), np.uint8)
+            return z, z, z
+        if kind == "dense":
+            return O.pack_nibbles(codes((T, K))), np.zeros((T, 0), np.uint8), \
+                np.full((T, K // (32 if fmt == "mx" else 16)), one, np.uint8)
+        keep = np.zeros((T, K // m, m), bool)
+        np.put_along_axis(keep, rng.random((T, K // m, m)).argsort(axis=2)[..., :n], True, axis=2)
+        keep = keep.reshape(T, K)
+        c, meta = O.pack_backbone(np.where(keep, codes((T, K)), 0).astype(np.uint8), keep, n, m)
+        return c, meta, np.full((T, K // 32), one, np.uint8)
+
+    k1, k2 = O.MODE_PATHS[mode]
+    c1, m1, s1 = path(k1)
+    c2, m2, s2 = path(k2)
+    act = {"rows": T, "K": K, "n": n, "m": m, "pairs": False, "fmt": fmt, "mode": mode,
+           "tensor_scale": None if fmt == "mx" else np.float32(1.0),
+           "sp_codes": c1, "sp_meta": m1, "sp_scale": s1, "dn_codes": c2, "dn_meta": m2, "dn_scale": s2}
+    ws = np.full((N, K // 32), one, np.uint8)
+    wq = {"N": N, "K": K, "fmt": fmt, "codes": O.pack_nibbles(codes((N, K))), "scale": ws,
+          "scale_dn": ws if fmt == "mx" else np.repeat(ws, 2, axis=1),
+          "tensor_scale": None if fmt == "mx" else np.float32(1.0)}
+    return act, wq
+
+
+@pytest.mark.parametrize("fmt", ["mx", "nv"])
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("T,N,K,n,m", [(300, 520, 1024, 2, 4), (130, 300, 416, 4, 8)])
+def test_mode_exact_sums(S, G, fmt, mode, T, N, K, n, m):
+    """Every path combination's GEMM on exact-sum operands equals the
+    oracle's exact result bit for bit."""
+    say(f"[mode-exact] {mode} {fmt} T={T} N={N} K={K} {n}:{m}")
+    o, wo = mode_exact_operands(T, N, K, n, m, fmt, mode, seed=T + K + len(mode))
+    y = S.sharq_linear(G.oracle_to_act(o), G.oracle_to_weight(wo), dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = O.linear(o, wo)
+    got = G.host(y).astype(np.float64)
+    bad = np.nonzero(got != ref)
+    assert bad[0].size == 0, (f"{mode} {fmt}: {bad[0].size} outputs differ from the exact sum; first at "
+                              f"{bad[0][0]},{bad[1][0]}: {got[bad[0][0], bad[1][0]]} vs {ref[bad[0][0], bad[1][0]]}")
