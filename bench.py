@@ -80,6 +80,8 @@ DECODE_W_SETS = 5             # decode: weight copies rotate between steps (5 x 
 TRAFFIC = {"gemm_source": "54b1cdd92ca6fd6a", "bytes_per_launch": 270.32e6}
 # the same for the MoE workload's k_linear_mx_grouped_persist<0> (mean of its gate_up and down launches)
 MOE_TRAFFIC = {"gemm_source": "54b1cdd92ca6fd6a", "bytes_per_launch": 436.6e6}
+# and for the Qwen2.5-7B NVFP4 workload's k_linear_nv_il (mean of its gate_up and down launches)
+NV_TRAFFIC = {"gemm_source": "54b1cdd92ca6fd6a", "bytes_per_launch": 840.4e6}
 
 
 def log(*a):
@@ -455,11 +457,11 @@ def mfma_probe(torch, dev, stream, iters=PROBE_ITERS, reps=3, kind="fp4"):
             "flops_per_launch": flops}
 
 
-def nv_roofline(torch, dev, stream, per, t_gemm):
+def nv_roofline(torch, dev, stream, per, t_gemm, measured=None):
     """The NVFP4 GEMMs' roofline record: algorithmic and executed work against
     the published 16-bit peak and against the sustained fp16 MFMA rate (the
     instruction the NVFP4 GEMM runs on for these K) measured right after the
-    timed steps."""
+    timed steps.  measured: the workload's HBM traffic record (NV_TRAFFIC), or None."""
     flops = sum(p["gemm_flops_alg"] for p in per)
     f_exec = sum(p["gemm_flops_exec"] for p in per)
     sus = mfma_probe(torch, dev, stream, kind="f16")
@@ -467,7 +469,9 @@ def nv_roofline(torch, dev, stream, per, t_gemm):
         f"GEMM executed work at {f_exec / t_gemm / 1e12 / sus['achieved']:.2f} of it")
     return {"bound": "mfma", "kernel": "k_linear_nv_il (fp16 MFMA over dequantized FP4)",
             "achieved": flops / t_gemm / 1e12, "peak": PEAK_16BIT_TFLOPS, "unit": "TFLOP/s",
-            "frac": flops / t_gemm / 1e12 / PEAK_16BIT_TFLOPS, "traffic": None, "flops": "F_alg",
+            "frac": flops / t_gemm / 1e12 / PEAK_16BIT_TFLOPS, "flops": "F_alg",
+            "traffic": (measured["bytes_per_launch"] if measured is not None
+                        and measured["gemm_source"] == gemm_source_digest() else None),
             "achieved_exec": f_exec / t_gemm / 1e12, "frac_exec": f_exec / t_gemm / 1e12 / PEAK_16BIT_TFLOPS,
             "sustained_mfma": sus, "frac_exec_of_sustained": f_exec / t_gemm / 1e12 / sus["achieved"],
             "frac_alg_of_sustained": flops / t_gemm / 1e12 / sus["achieved"]}
@@ -605,7 +609,8 @@ def qwen_nvfp4(args, torch, S, synth, dev, stream):
                       {"workload": "Qwen2.5-7B prefill linears gate_up (K3584,N37888,RMSNorm), down (K18944,N3584); "
                                    "M=4096; 2:4; NVFP4 with dynamic per-tensor scale", "tokens": T,
                        "backbone_for_gemm": args.backbone})
-    out["roofline"] = nv_roofline(torch, dev, stream, per, t_gemm)
+    out["roofline"] = nv_roofline(torch, dev, stream, per, t_gemm,
+                                  NV_TRAFFIC if args.backbone == "dense-only" else None)
     out["prep"] = {"bound": "hbm", "achieved": pb / t_prep / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                    "frac": pb / t_prep / 1e9 / PEAK_HBM_GBPS,
                    "note": "time includes the per-tensor amax pre-pass (a second read of X)"}
